@@ -1,0 +1,382 @@
+// ggref: CPU oracle of the per-window feature-fetch path.
+//
+// TEST INFRASTRUCTURE ONLY: loaded by the test suite, the smoke check and
+// the benchmark's CPU-baseline leg, never by the product path.  Plain,
+// single-threaded, written for clarity: std::set, std::sort and one memcpy
+// per feature row.  It follows the paper (GreenGNN, arXiv 2606.02916) step
+// by step; where the paper is silent the reading taken is stated at the
+// function.  Nothing here is shared with the HIP library.
+
+#include "ggref.h"
+
+#include <algorithm>
+#include <cstring>
+#include <set>
+#include <vector>
+
+namespace {
+
+// ---------------------------------------------------------------------------
+// Philox4x32-10, from its definition in Salmon, Moraes, Dror and Shaw,
+// "Parallel random numbers: as easy as 1, 2, 3" (SC'11), Sec. 3.2: ten
+// rounds; each round multiplies words 0 and 2 by the two Philox-4x32
+// multipliers, and the new block is (hi(R1) ^ x1 ^ k0, lo(R1),
+// hi(R0) ^ x3 ^ k1, lo(R0)); the key is bumped by the Weyl constants
+// (golden ratio and sqrt(3)-1, as 32-bit fractions) between rounds.
+// ---------------------------------------------------------------------------
+const uint32_t kPhiloxM0 = 0xD2511F53u;
+const uint32_t kPhiloxM1 = 0xCD9E8D57u;
+const uint32_t kWeyl0 = 0x9E3779B9u;
+const uint32_t kWeyl1 = 0xBB67AE85u;
+
+void philox_block(const uint32_t in[4], const uint32_t key_in[2], uint32_t out[4]) {
+  uint32_t x0 = in[0], x1 = in[1], x2 = in[2], x3 = in[3];
+  uint32_t k0 = key_in[0], k1 = key_in[1];
+  for (int round = 0; round < 10; ++round) {
+    if (round > 0) {
+      k0 += kWeyl0;
+      k1 += kWeyl1;
+    }
+    const uint64_t p0 = (uint64_t)kPhiloxM0 * (uint64_t)x0;
+    const uint64_t p1 = (uint64_t)kPhiloxM1 * (uint64_t)x2;
+    const uint32_t hi0 = (uint32_t)(p0 >> 32), lo0 = (uint32_t)p0;
+    const uint32_t hi1 = (uint32_t)(p1 >> 32), lo1 = (uint32_t)p1;
+    const uint32_t y0 = hi1 ^ x1 ^ k0;
+    const uint32_t y1 = lo1;
+    const uint32_t y2 = hi0 ^ x3 ^ k1;
+    const uint32_t y3 = lo0;
+    x0 = y0;
+    x1 = y1;
+    x2 = y2;
+    x3 = y3;
+  }
+  out[0] = x0;
+  out[1] = x1;
+  out[2] = x2;
+  out[3] = x3;
+}
+
+int64_t row_start(const ggref_csr_t* g, int64_t u) {
+  if (g->row_ptr_bits == 32) return (int64_t)((const int32_t*)g->row_ptr)[u];
+  return ((const int64_t*)g->row_ptr)[u];
+}
+
+std::vector<int32_t> sort_unique(std::vector<int32_t> v) {
+  std::sort(v.begin(), v.end());
+  v.erase(std::unique(v.begin(), v.end()), v.end());
+  return v;
+}
+
+bool part_ok(const ggref_part_t* part) {
+  if (!part || part->num_parts < 1 || part->num_parts > GGREF_MAX_PARTS) return false;
+  if (part->local_owner < -1 || part->local_owner >= part->num_parts) return false;
+  if (part->kind == GGREF_PART_RANGE) {
+    if (part->range_start[0] != 0 || part->range_start[part->num_parts] != part->num_nodes) return false;
+    for (int m = 0; m < part->num_parts; ++m)
+      if (part->range_start[m + 1] < part->range_start[m]) return false;
+  } else if (part->kind != GGREF_PART_MOD) {
+    return false;
+  }
+  return true;
+}
+
+const char* src_row(const ggref_feat_t* feat, int32_t m, int64_t r) {
+  return (const char*)feat->shard[m] + r * feat->row_stride[m];
+}
+
+}  // namespace
+
+extern "C" {
+
+void ggref_philox4x32_10(const uint32_t ctr[4], const uint32_t key[2], uint32_t out[4]) {
+  philox_block(ctr, key, out);
+}
+
+// Lemire's multiply-shift map of a 32-bit word onto [0, bound), without the
+// rejection step: floor(r * bound / 2^32).  bound <= 2^32.
+uint64_t ggref_bounded(uint32_t r, uint64_t bound) {
+  return ((uint64_t)r * bound) >> 32;
+}
+
+// Floyd's algorithm (Bentley and Floyd, "Programming pearls: a sample of
+// brilliance", CACM 30(9), 1987).  For i = 0..k-1 with j = d-k+i, the i-th
+// draw t[i] is uniform on [0, j]; it joins the set unless it is already
+// there, in which case j joins instead.  The result has exactly k distinct
+// positions of [0, d).
+int ggref_floyd(int64_t d, int32_t k, const int64_t* t, int64_t* pos) {
+  if (k < 1 || d <= k) return GGREF_ERR_ARG;
+  std::set<int64_t> chosen;
+  for (int32_t i = 0; i < k; ++i) {
+    const int64_t j = d - k + i;
+    if (t[i] < 0 || t[i] > j) return GGREF_ERR_ARG;
+    if (chosen.count(t[i]))
+      chosen.insert(j);
+    else
+      chosen.insert(t[i]);
+  }
+  int32_t n = 0;
+  for (int64_t p : chosen) pos[n++] = p;
+  return GGREF_OK;
+}
+
+int32_t ggref_owner(const ggref_part_t* part, int64_t u) {
+  if (part->kind == GGREF_PART_MOD) return (int32_t)(u % part->num_parts);
+  for (int32_t m = 0; m < part->num_parts; ++m)
+    if (u >= part->range_start[m] && u < part->range_start[m + 1]) return m;
+  return -1;
+}
+
+int64_t ggref_row(const ggref_part_t* part, int64_t u) {
+  if (part->kind == GGREF_PART_MOD) return u / part->num_parts;
+  const int32_t m = ggref_owner(part, u);
+  return m < 0 ? -1 : u - part->range_start[m];
+}
+
+// Sampling of one window (Sec. IV-A step 2; the paper takes the sampler
+// from DGL).  Readings where the paper is silent:
+//  * fanout[l] applies at hop l+1, seed side first;
+//  * sampling is without replacement: a node of degree d <= k keeps all
+//    its neighbours in CSR order, a node with d > k keeps the k positions
+//    chosen by Floyd's algorithm, ascending;
+//  * nested frontiers: F_0 = the batch's distinct seeds, F_{l+1} = F_l
+//    together with every neighbour sampled at hop l+1, so N_b = F_L;
+//  * draw i of node u at hop l in global batch b uses word i mod 4 of the
+//    Philox block with counter (u, b, epoch, (l << 16) | (i div 4)) and
+//    key (low, high 32 bits of rng_seed); the bounded map gives the Floyd
+//    draw on [0, d-k+i].
+int ggref_sample_window(const ggref_csr_t* csr, const int32_t* seeds, const int64_t* seed_off,
+                        int32_t W, const int32_t* fanout, int32_t L, uint64_t rng_seed,
+                        int32_t epoch, int64_t batch0, int32_t* frontier_ids,
+                        int64_t frontier_cap, int64_t* frontier_off, int32_t* nbr_ids,
+                        int64_t nbr_cap, int64_t* nbr_off, int64_t* need) {
+  if (!csr || W < 1 || L < 1 || !seed_off || !fanout) return GGREF_ERR_ARG;
+  for (int32_t l = 0; l < L; ++l)
+    if (fanout[l] < 1 || fanout[l] > 4 * 65536) return GGREF_ERR_ARG;
+  const int64_t N = csr->num_nodes;
+  const uint32_t key[2] = {(uint32_t)rng_seed, (uint32_t)(rng_seed >> 32)};
+
+  // frontier[b][l] and sampled[b][l] for every batch of the window.
+  std::vector<std::vector<std::vector<int32_t>>> frontier(W), sampled(W);
+  for (int32_t b = 0; b < W; ++b) {
+    frontier[b].resize(L + 1);
+    sampled[b].resize(L);
+    std::vector<int32_t> s0;
+    for (int64_t i = seed_off[b]; i < seed_off[b + 1]; ++i) {
+      if (seeds[i] < 0 || seeds[i] >= N) return GGREF_ERR_RANGE;
+      s0.push_back(seeds[i]);
+    }
+    frontier[b][0] = sort_unique(s0);
+    const uint32_t bglob = (uint32_t)(batch0 + b);
+    for (int32_t l = 0; l < L; ++l) {
+      const int32_t k = fanout[l];
+      std::vector<int32_t> next = frontier[b][l];
+      std::vector<int32_t>& out = sampled[b][l];
+      for (int32_t u : frontier[b][l]) {
+        const int64_t beg = row_start(csr, u);
+        const int64_t d = row_start(csr, (int64_t)u + 1) - beg;
+        std::vector<int64_t> positions;
+        if (d <= k) {
+          for (int64_t p = 0; p < d; ++p) positions.push_back(p);
+        } else {
+          if (d > 0xFFFFFFFFLL) return GGREF_ERR_RANGE;
+          std::vector<int64_t> t(k), pos(k);
+          for (int32_t i = 0; i < k; ++i) {
+            const uint32_t ctr[4] = {(uint32_t)u, bglob, (uint32_t)epoch,
+                                     ((uint32_t)l << 16) | (uint32_t)(i / 4)};
+            uint32_t block[4];
+            philox_block(ctr, key, block);
+            t[i] = (int64_t)ggref_bounded(block[i % 4], (uint64_t)(d - k + i + 1));
+          }
+          if (ggref_floyd(d, k, t.data(), pos.data()) != GGREF_OK) return GGREF_ERR_ARG;
+          positions = pos;
+        }
+        for (int64_t p : positions) {
+          const int32_t v = csr->col_idx[beg + p];
+          if (v < 0 || v >= N) return GGREF_ERR_RANGE;
+          out.push_back(v);
+          next.push_back(v);
+        }
+        for (int64_t p = (int64_t)positions.size(); p < k; ++p) out.push_back(-1);
+      }
+      frontier[b][l + 1] = sort_unique(next);
+    }
+  }
+
+  // Level-major layout.
+  int64_t fpos = 0, npos = 0;
+  for (int32_t l = 0; l <= L; ++l)
+    for (int32_t b = 0; b < W; ++b) fpos += (int64_t)frontier[b][l].size();
+  for (int32_t l = 0; l < L; ++l)
+    for (int32_t b = 0; b < W; ++b) npos += (int64_t)sampled[b][l].size();
+  if (need) {
+    need[0] = fpos;
+    need[1] = npos;
+  }
+  if (fpos > frontier_cap || npos > nbr_cap) return GGREF_ERR_CAPACITY;
+  fpos = 0;
+  for (int32_t l = 0; l <= L; ++l)
+    for (int32_t b = 0; b < W; ++b) {
+      frontier_off[l * W + b] = fpos;
+      for (int32_t u : frontier[b][l]) frontier_ids[fpos++] = u;
+    }
+  frontier_off[(L + 1) * W] = fpos;
+  npos = 0;
+  for (int32_t l = 0; l < L; ++l)
+    for (int32_t b = 0; b < W; ++b) {
+      nbr_off[l * W + b] = npos;
+      for (int32_t v : sampled[b][l]) nbr_ids[npos++] = v;
+    }
+  nbr_off[L * W] = npos;
+  return GGREF_OK;
+}
+
+// Hot set H_k of one window (Sec. IV-A window simulation: the most
+// frequently accessed remote nodes of the window).  freq(u) counts the
+// batches of the window whose N_b holds u.  n_hot < 0 keeps every remote
+// node of the window (the union); otherwise the first n_hot in order of
+// decreasing freq, ties broken by smaller id.
+int ggref_build_hotset(const int32_t* frontier_ids, const int64_t* frontier_off, int32_t W,
+                       int32_t L, const ggref_part_t* part, int64_t n_hot, int32_t* hot_ids,
+                       int32_t* hot_freq, int64_t cap, int64_t* hot_count) {
+  if (!part_ok(part) || W < 1 || L < 0) return GGREF_ERR_ARG;
+  std::vector<int32_t> remote;
+  for (int32_t b = 0; b < W; ++b) {
+    const int64_t s = (int64_t)L * W + b;
+    for (int64_t i = frontier_off[s]; i < frontier_off[s + 1]; ++i) {
+      const int32_t u = frontier_ids[i];
+      if (ggref_owner(part, u) != part->local_owner) remote.push_back(u);
+    }
+  }
+  std::sort(remote.begin(), remote.end());
+  std::vector<std::pair<int32_t, int32_t>> uf;  // (id, freq), id ascending
+  for (size_t i = 0; i < remote.size();) {
+    size_t j = i;
+    while (j < remote.size() && remote[j] == remote[i]) ++j;
+    uf.push_back({remote[i], (int32_t)(j - i)});
+    i = j;
+  }
+  if (n_hot >= 0 && n_hot < (int64_t)uf.size()) {
+    std::stable_sort(uf.begin(), uf.end(),
+                     [](const std::pair<int32_t, int32_t>& a, const std::pair<int32_t, int32_t>& b) {
+                       return a.second > b.second;
+                     });
+    uf.resize((size_t)n_hot);
+    std::sort(uf.begin(), uf.end());
+  }
+  if (hot_count) *hot_count = (int64_t)uf.size();
+  if ((int64_t)uf.size() > cap) return GGREF_ERR_CAPACITY;
+  for (size_t i = 0; i < uf.size(); ++i) {
+    hot_ids[i] = uf[i].first;
+    if (hot_freq) hot_freq[i] = uf[i].second;
+  }
+  return GGREF_OK;
+}
+
+// Owner grouping (Sec. IV-A rebuild events, Sec. IV-C: one bulk request per
+// partition owner).  count[m] = members of owner m; owner_off is its
+// exclusive scan; members keep their input order inside each owner.
+int ggref_bucket_by_owner(const int32_t* hot_ids, int64_t hot_count, const ggref_part_t* part,
+                          int32_t* bucket_ids, int64_t* owner_off) {
+  if (!part_ok(part) || hot_count < 0) return GGREF_ERR_ARG;
+  const int32_t P = part->num_parts;
+  std::vector<int64_t> count(P, 0);
+  for (int64_t i = 0; i < hot_count; ++i) {
+    const int32_t m = ggref_owner(part, hot_ids[i]);
+    if (m < 0) return GGREF_ERR_RANGE;
+    ++count[m];
+  }
+  owner_off[0] = 0;
+  for (int32_t m = 0; m < P; ++m) owner_off[m + 1] = owner_off[m] + count[m];
+  std::vector<int64_t> cursor(owner_off, owner_off + P);
+  for (int64_t i = 0; i < hot_count; ++i) {
+    const int32_t m = ggref_owner(part, hot_ids[i]);
+    bucket_ids[cursor[m]++] = hot_ids[i];
+  }
+  return GGREF_OK;
+}
+
+// Bulk staging of the window cache (Sec. IV-C; Algorithm 1 WarmCache).
+// The previous window's remap entries are cleared first; then, for every
+// owner with a non-empty bucket, one request copies that owner's rows into
+// the contiguous cache slots of its bucket and points slot_of at them.
+// delta_rows[m] = |bucket_m(H_k) \ H_{k-1}|, the rebuild delta of Sec. IV-A
+// (reported; the whole hot set is restaged).
+int ggref_stage_bulk(const int32_t* bucket_ids, const int64_t* owner_off,
+                     const ggref_part_t* part, const ggref_feat_t* feat, void* cache,
+                     int64_t cache_stride, int64_t cache_rows, int32_t* slot_of,
+                     const int32_t* prev_ids, int64_t prev_count, ggref_stage_stats_t* stats) {
+  if (!part_ok(part) || !feat || feat->num_parts != part->num_parts) return GGREF_ERR_ARG;
+  const int32_t P = part->num_parts;
+  std::memset(stats, 0, sizeof(*stats));
+  for (int64_t i = 0; i < prev_count; ++i) slot_of[prev_ids[i]] = -1;
+  stats->invalidated = prev_count;
+  const int64_t total = owner_off[P];
+  if (total > cache_rows) return GGREF_ERR_CAPACITY;
+  std::set<int32_t> prev(prev_ids, prev_ids + prev_count);
+  for (int32_t m = 0; m < P; ++m) {
+    const int64_t n = owner_off[m + 1] - owner_off[m];
+    stats->rows[m] = n;
+    stats->bytes[m] = n * feat->row_bytes;
+    stats->requests[m] = n > 0 ? 1 : 0;
+    stats->rows_total += n;
+    stats->requests_total += stats->requests[m];
+    for (int64_t s = owner_off[m]; s < owner_off[m + 1]; ++s) {
+      const int32_t u = bucket_ids[s];
+      if (ggref_owner(part, u) != m) return GGREF_ERR_RANGE;
+      const int64_t r = ggref_row(part, u);
+      if (r < 0 || r >= feat->shard_rows[m]) return GGREF_ERR_RANGE;
+      std::memcpy((char*)cache + s * cache_stride, src_row(feat, m, r), (size_t)feat->row_bytes);
+      slot_of[u] = (int32_t)s;
+      if (!prev.count(u)) ++stats->delta_rows[m];
+    }
+  }
+  return GGREF_OK;
+}
+
+// Per-batch feature assembly (Algorithm 1, inner loop): a local node is
+// read from the local shard, a cached remote node from its cache slot, and
+// every other node is a residual miss.  Misses are grouped by owner, input
+// order kept, and each non-empty group is one on-demand request
+// (the indicator of Eq. (2)); its rows go straight to their output rows.
+int ggref_gather_batch(const int32_t* in_ids, int64_t n, const ggref_part_t* part,
+                       const ggref_feat_t* feat, const void* cache, int64_t cache_stride,
+                       int64_t cache_rows, const int32_t* slot_of, void* out, int64_t out_stride,
+                       ggref_gather_stats_t* stats) {
+  if (!part_ok(part) || !feat || feat->num_parts != part->num_parts || n < 0) return GGREF_ERR_ARG;
+  const int32_t P = part->num_parts;
+  std::memset(stats, 0, sizeof(*stats));
+  std::vector<std::vector<int64_t>> miss(P);
+  for (int64_t i = 0; i < n; ++i) {
+    const int32_t u = in_ids[i];
+    if (u < 0 || u >= part->num_nodes) return GGREF_ERR_RANGE;
+    const int32_t m = ggref_owner(part, u);
+    char* dst = (char*)out + i * out_stride;
+    if (m == part->local_owner) {
+      const int64_t r = ggref_row(part, u);
+      if (r >= feat->shard_rows[m]) return GGREF_ERR_RANGE;
+      std::memcpy(dst, src_row(feat, m, r), (size_t)feat->row_bytes);
+      ++stats->local;
+    } else if (slot_of[u] >= 0) {
+      if (slot_of[u] >= cache_rows) return GGREF_ERR_RANGE;
+      std::memcpy(dst, (const char*)cache + (int64_t)slot_of[u] * cache_stride,
+                  (size_t)feat->row_bytes);
+      ++stats->hits;
+    } else {
+      miss[m].push_back(i);
+    }
+  }
+  for (int32_t m = 0; m < P; ++m) {
+    stats->miss_rows[m] = (int64_t)miss[m].size();
+    stats->miss_requests[m] = miss[m].empty() ? 0 : 1;
+    stats->misses += (int64_t)miss[m].size();
+    for (int64_t i : miss[m]) {
+      const int64_t r = ggref_row(part, in_ids[i]);
+      if (r >= feat->shard_rows[m]) return GGREF_ERR_RANGE;
+      std::memcpy((char*)out + i * out_stride, src_row(feat, m, r), (size_t)feat->row_bytes);
+    }
+  }
+  stats->rows = n;
+  return GGREF_OK;
+}
+
+}  // extern "C"

@@ -1,0 +1,239 @@
+"""Seeded synthetic workloads for the per-window feature-fetch path.
+
+This package builds inputs only: R-MAT power-law graphs in CSR form, the
+partition book, feature shards and the per-batch seed lists.  It holds none
+of the method's arithmetic and is shared by the oracle side and the HIP side
+of every test and benchmark.
+
+The five workloads stand in for the paper's datasets (Reddit, OGBN-Products
+and OGBN-Papers100M, Sec. VI-A), with their node and edge counts, on R-MAT
+graphs with (a, b, c) = (0.57, 0.19, 0.19).
+"""
+from __future__ import annotations
+
+import ctypes as C
+import dataclasses
+import os
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libsynth.so")
+
+PART_MOD = 0
+PART_RANGE = 1
+MASTER_SEED = 0
+
+_lib = None
+
+
+def lib():
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise ImportError(f"synthetic-input library not built: {LIB_PATH}")
+        L = C.CDLL(LIB_PATH)
+        P = C.c_void_p
+        L.synth_permutation.argtypes = [C.c_int64, C.c_uint64, C.c_uint64, P]
+        L.synth_permutation.restype = None
+        L.synth_rmat_csr.argtypes = [C.c_int64, C.c_int64, C.c_double, C.c_double, C.c_double,
+                                     C.c_uint64, C.c_int, P, P]
+        L.synth_rmat_csr.restype = C.c_int
+        L.synth_features.argtypes = [C.c_int64, C.c_int64, C.c_int32, C.c_int32, C.c_int32,
+                                     C.c_int64, C.c_uint64, P]
+        L.synth_features.restype = None
+        _lib = L
+    return _lib
+
+
+@dataclasses.dataclass(frozen=True)
+class Workload:
+    name: str
+    num_nodes: int
+    num_edges: int
+    relabel: bool
+    row_ptr_bits: int
+    part_kind: int
+    num_parts: int
+    local_owner: int
+    feat_dim: int
+    feat_dtype: str          # "fp32" | "fp16"
+    feat_dist: str           # "normal" | "uniform"
+    fanout: tuple
+    batch_size: int
+    W: int
+    seed_rule: str           # "perm_all" | "train_split" | "owner0"
+    train_frac: float = 1.0
+    n_windows: int = 0       # owner0 / perm_all: windows of seeds generated
+    remote_on_host: bool = False
+
+    @property
+    def elem_bytes(self):
+        return 4 if self.feat_dtype == "fp32" else 2
+
+    @property
+    def row_bytes(self):
+        return self.feat_dim * self.elem_bytes
+
+    @property
+    def row_stride(self):
+        return (self.row_bytes + 15) // 16 * 16
+
+    def range_start(self):
+        P, N = self.num_parts, self.num_nodes
+        return [m * N // P for m in range(P)] + [N]
+
+
+WORKLOADS = {
+    # 10,000-node R-MAT, owners by node id mod 4, fp32 x 64, fanout [10,5],
+    # batch 256, W = 4, one window.
+    "tiny": Workload("tiny", 10_000, 100_000, False, 32, PART_MOD, 4, 0, 64, "fp32", "normal",
+                     (10, 5), 256, 4, "perm_all", n_windows=1),
+    # Reddit-shaped: 233,000 nodes, 114M edges, fp32 x 602, fanout [25,10],
+    # batch 1024, W = 8, one epoch over a 66% training split.
+    "dense_mid": Workload("dense_mid", 233_000, 114_000_000, True, 64, PART_RANGE, 4, 0, 602,
+                          "fp32", "normal", (25, 10), 1024, 8, "train_split", train_frac=0.66),
+    # OGBN-Products-shaped: 2.45M nodes, 62M edges, fp32 x 100 ~ U(-1,1),
+    # fanout [15,10,5], batch 1024, W = 16, one epoch over an 8% split.
+    "large_sparse": Workload("large_sparse", 2_450_000, 62_000_000, True, 64, PART_RANGE, 4, 0,
+                             100, "fp32", "uniform", (15, 10, 5), 1024, 16, "train_split",
+                             train_frac=0.08),
+    # The same graph at batch 4096 for the window-size sweep.
+    "wsweep": Workload("wsweep", 2_450_000, 62_000_000, True, 64, PART_RANGE, 4, 0, 100, "fp32",
+                       "uniform", (15, 10, 5), 4096, 16, "train_split", train_frac=0.08),
+    # One GPU's share of a 4-way split of a Papers100M-shaped graph:
+    # 111M nodes, 1.6B edges, fp16 x 128; local shard in HBM, the three
+    # remote shards in pinned host memory.
+    "papers_share": Workload("papers_share", 111_000_000, 1_600_000_000, True, 64, PART_RANGE, 4,
+                             0, 128, "fp16", "normal", (15, 10, 5), 1024, 16, "owner0",
+                             n_windows=5, remote_on_host=True),
+}
+
+# A small graph for tests that must finish in seconds on the CPU oracle but
+# still span several tiles and a ragged tail on the GPU.
+WORKLOADS["small"] = Workload("small", 60_001, 700_000, True, 64, PART_RANGE, 4, 0, 100, "fp32",
+                              "uniform", (15, 10, 5), 512, 4, "train_split", train_frac=0.2)
+
+
+def rmat_csr(num_nodes, num_edges, seed=MASTER_SEED, relabel=True, row_ptr_bits=64,
+             a=0.57, b=0.19, c=0.19):
+    row_ptr = np.empty(num_nodes + 1, dtype=np.int64)
+    col_idx = np.empty(num_edges, dtype=np.int32)
+    rc = lib().synth_rmat_csr(num_nodes, num_edges, a, b, c, seed, int(relabel),
+                              row_ptr.ctypes.data, col_idx.ctypes.data)
+    if rc != 0:
+        raise RuntimeError("R-MAT generation ran out of candidates")
+    if row_ptr_bits == 32:
+        assert num_edges < 2**31
+        row_ptr = row_ptr.astype(np.int32)
+    return row_ptr, col_idx
+
+
+def permutation(n, seed, stream):
+    out = np.empty(n, dtype=np.int64)
+    lib().synth_permutation(n, seed, stream, out.ctypes.data)
+    return out
+
+
+def features(u_begin, u_end, dim, dtype, dist, stride, seed=MASTER_SEED, out=None):
+    """Feature rows of nodes [u_begin, u_end) as a uint8 array (rows x stride)."""
+    n = u_end - u_begin
+    if out is None:
+        out = np.empty((n, stride), dtype=np.uint8)
+    assert out.shape == (n, stride) and out.flags.c_contiguous
+    if n:
+        lib().synth_features(u_begin, u_end, dim, 0 if dtype == "fp32" else 1,
+                             0 if dist == "normal" else 1, stride, seed, out.ctypes.data)
+    return out
+
+
+def seed_batches(wl: Workload, epoch=0, seed=MASTER_SEED):
+    """All seed batches of one epoch: (seeds int32, batch_off int64[n_batches+1])."""
+    N, B = wl.num_nodes, wl.batch_size
+    if wl.seed_rule == "perm_all":
+        n = min(N, wl.n_windows * wl.W * B)
+        seeds = permutation(N, seed, 11)[:n]
+    elif wl.seed_rule == "train_split":
+        n_train = int(wl.train_frac * N)
+        train = permutation(N, seed, 11)[:n_train]
+        order = permutation(n_train, seed, 1000 + epoch)
+        seeds = train[order]
+    elif wl.seed_rule == "owner0":
+        lo, hi = wl.range_start()[0], wl.range_start()[1]
+        n = min(hi - lo, wl.n_windows * wl.W * B)
+        seeds = lo + permutation(hi - lo, seed, 11)[:n]
+    else:
+        raise ValueError(wl.seed_rule)
+    n = seeds.shape[0]
+    nb = (n + B - 1) // B
+    off = np.minimum(np.arange(nb + 1, dtype=np.int64) * B, n)
+    return seeds.astype(np.int32), off
+
+
+def window_batches(batch_off, W, k):
+    """Global batch range [b0, b1) of window k (the last window may be short)."""
+    nb = batch_off.shape[0] - 1
+    b0 = k * W
+    return b0, min(nb, b0 + W)
+
+
+def n_windows(batch_off, W):
+    nb = batch_off.shape[0] - 1
+    return (nb + W - 1) // W
+
+
+@dataclasses.dataclass
+class Instance:
+    wl: Workload
+    row_ptr: np.ndarray
+    col_idx: np.ndarray
+    seeds: np.ndarray
+    batch_off: np.ndarray
+    shards: list          # per owner: uint8 array (rows x stride)
+    range_start: list
+
+
+def shard_rows(wl: Workload, m):
+    if wl.part_kind == PART_MOD:
+        N, P = wl.num_nodes, wl.num_parts
+        return (N - m + P - 1) // P
+    rs = wl.range_start()
+    return rs[m + 1] - rs[m]
+
+
+def shard_features(wl: Workload, m, out=None):
+    """Owner m's feature shard: rows in owner-local order."""
+    stride = wl.row_stride
+    if wl.part_kind == PART_RANGE:
+        rs = wl.range_start()
+        return features(rs[m], rs[m + 1], wl.feat_dim, wl.feat_dtype, wl.feat_dist, stride,
+                        out=out)
+    full = features(0, wl.num_nodes, wl.feat_dim, wl.feat_dtype, wl.feat_dist, stride)
+    sh = np.ascontiguousarray(full[m::wl.num_parts])
+    if out is not None:
+        out[...] = sh
+        return out
+    return sh
+
+
+def full_features(wl: Workload):
+    """The unsharded feature matrix (row u = node u); ground truth for tests."""
+    return features(0, wl.num_nodes, wl.feat_dim, wl.feat_dtype, wl.feat_dist, wl.row_stride)
+
+
+_cache = {}
+
+
+def instance(name, with_features=True):
+    key = (name, with_features)
+    if key in _cache:
+        return _cache[key]
+    wl = WORKLOADS[name]
+    row_ptr, col_idx = rmat_csr(wl.num_nodes, wl.num_edges, relabel=wl.relabel,
+                                row_ptr_bits=wl.row_ptr_bits)
+    seeds, boff = seed_batches(wl)
+    shards = [shard_features(wl, m) for m in range(wl.num_parts)] if with_features else []
+    inst = Instance(wl, row_ptr, col_idx, seeds, boff, shards,
+                    wl.range_start() if wl.part_kind == PART_RANGE else None)
+    _cache[key] = inst
+    return inst
