@@ -1,0 +1,240 @@
+#!/usr/bin/env python3
+"""Benchmark of the per-window feature-fetch path on one MI355X.
+
+One step = one window of W consecutive GraphSAGE mini-batches through the
+whole path: sampling, hot-set build, owner bucketing, bulk staging and the
+W per-batch gathers (with the miss path).  Inputs (CSR, feature shards,
+seeds) are resident in HBM before the timed region.  Steps cycle through
+the windows of one epoch.  Prints one JSON line on stdout.
+
+value   = feature rows gathered per second over the timed steps.
+roofline: the gather (gg_gather_batch) is the dominant kernel; its
+          algorithmic bytes per launch (2 * row_bytes + 4 B id per row, + 4 B
+          slot lookup per remote row) over its HIP-event duration, against
+          8 TB/s HBM.
+cpu_baseline: the single-threaded CPU oracle on one window of the same
+          workload, on this host.
+"""
+import argparse
+import json
+import os
+import platform
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0
+
+
+def log(msg):
+    print(f"[bench] {msg}", file=sys.stderr, flush=True)
+
+
+def cpu_model():
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return platform.processor()
+
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=24)
+    ap.add_argument("--warmup", type=int, default=2)
+    ap.add_argument("--config", default="large_sparse",
+                    help="tiny | dense_mid | large_sparse | wsweep | small")
+    ap.add_argument("--W", type=int, default=None, help="window size (default: the workload's)")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-seconds", type=float, default=10.0,
+                    help="minimum oracle time for the CPU baseline sample")
+    args = ap.parse_args()
+
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print("bench.py runs the per-window fetch path on one GPU only; multi-GPU runs are not "
+              "part of this build (see DESIGN.md for how the path would shard)", file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+
+    import synth
+    from paper_2606_02916_amd import FetchPipeline
+
+    dev = torch.device("cuda:0")
+    wl = synth.WORKLOADS[args.config]
+    W = args.W or wl.W
+    t = time.time()
+    inst = synth.instance(args.config)
+    log(f"generated {args.config}: N={wl.num_nodes} E={wl.num_edges} in {time.time() - t:.1f}s")
+    P, L = wl.num_parts, len(wl.fanout)
+    row_ptr_d = torch.from_numpy(inst.row_ptr).to(dev)
+    col_idx_d = torch.from_numpy(inst.col_idx).to(dev)
+    shards_d = [torch.from_numpy(s).to(dev) for s in inst.shards]
+    seeds_d = torch.from_numpy(inst.seeds).to(dev)
+    pipe = FetchPipeline(row_ptr_d, col_idx_d, P, wl.part_kind, wl.local_owner, inst.range_start,
+                         shards_d, [s.shape[0] for s in inst.shards], wl.row_bytes, wl.row_stride,
+                         W, wl.fanout, wl.batch_size, device=dev)
+    boff = inst.batch_off
+    nwin = synth.n_windows(boff, W)
+    wins = []
+    for k in range(nwin):
+        b0, b1 = synth.window_batches(boff, W, k)
+        so = boff[b0:b1 + 1] - boff[b0]
+        wins.append((seeds_d[boff[b0]:boff[b1]], so, b0))
+    torch.cuda.synchronize()
+    log(f"uploaded; {nwin} windows of W={W}; out_cap={pipe.out_cap} hot_cap={pipe.hot_cap}")
+
+    # Pass over every window once: per-window row counts for the metric and
+    # per-batch local/remote counts for the gather's algorithmic bytes.
+    rb = wl.row_bytes
+    rows_w, gbytes_w, hot_w, sbytes_w, req_w = [], [], [], [], []
+    for k, (s, so, b0) in enumerate(wins):
+        Wk = pipe.window(s, so, b0)
+        torch.cuda.synchronize()
+        st = pipe.read_status()
+        if st != 0:
+            raise RuntimeError(f"device status {st} in window {k}")
+        g = [pipe.gather_stats_dict(b) for b in range(Wk)]
+        rows_w.append(sum(x["rows"] for x in g))
+        gbytes_w.append([x["rows"] * (2 * rb + 4) + (x["hits"] + x["misses"]) * 4 for x in g])
+        ss = pipe.stage_stats_dict()
+        hot_w.append(ss["rows_total"])
+        sbytes_w.append(ss["rows_total"] * (2 * rb + 8) + ss["invalidated"] * 4)
+        req_w.append(ss["requests_total"])
+    log(f"rows per window: {rows_w[:4]}... hot set: {hot_w[:4]}...")
+
+    for i in range(args.warmup):
+        s, so, b0 = wins[i % nwin]
+        pipe.window(s, so, b0)
+    torch.cuda.synchronize()
+
+    K = args.steps
+    mk = lambda: torch.cuda.Event(enable_timing=True)  # noqa: E731
+    evs = [[mk() for _ in range(6)] for _ in range(K)]
+    gevs = [[(mk(), mk()) for _ in range(W)] for _ in range(K)]
+    order = [(args.warmup + i) % nwin for i in range(K)]
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i, k in enumerate(order):
+        s, so, b0 = wins[k]
+        pipe.window(s, so, b0, events=evs[i], gather_events=gevs[i])
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    if pipe.read_status() != 0:
+        raise RuntimeError(f"device status {pipe.read_status()} after the timed steps")
+    elapsed = t1 - t0
+    rows = sum(rows_w[k] for k in order)
+    value = rows / elapsed
+
+    g_ms, g_bytes, n_launch = 0.0, 0, 0
+    stage_ms = {"sample": [], "hotset": [], "bucket": [], "stage": [], "gathers": []}
+    st_ms, st_bytes = 0.0, 0
+    for i, k in enumerate(order):
+        e = evs[i]
+        for name, (a, b) in zip(stage_ms, [(0, 1), (1, 2), (2, 3), (3, 4), (4, 5)]):
+            stage_ms[name].append(e[a].elapsed_time(e[b]))
+        st_ms += e[3].elapsed_time(e[4])
+        st_bytes += sbytes_w[k]
+        for b in range(len(wins[k][1]) - 1):
+            g_ms += gevs[i][b][0].elapsed_time(gevs[i][b][1])
+            g_bytes += gbytes_w[k][b]
+            n_launch += 1
+    avg_ms = g_ms / n_launch
+    avg_bytes = g_bytes / n_launch
+    achieved = avg_bytes / (avg_ms * 1e-3) / 1e9
+    stage_gbs = st_bytes / (st_ms * 1e-3) / 1e9
+
+    cpu = None
+    if not args.no_cpu_baseline:
+        cpu = cpu_baseline(inst, wl, W, wins[0][1], wins[0][2], args.cpu_seconds)
+
+    line = {
+        "metric": "feature rows gathered/s (per-window fetch path: sample, hot set, owner "
+                  "buckets, bulk stage, per-batch gathers)",
+        "value": round(value, 1),
+        "unit": "rows/s",
+        "n_gpus": 1,
+        "steps": K,
+        "warmup": args.warmup,
+        "ms_per_step": round(elapsed / K * 1e3, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "u8",
+        "data": "synthetic R-MAT (a,b,c)=(0.57,0.19,0.19), seeded; features as opaque bytes",
+        "config": {"workload": args.config, "nodes": wl.num_nodes, "edges": wl.num_edges,
+                   "features": f"{wl.feat_dtype}x{wl.feat_dim}", "row_bytes": rb,
+                   "fanout": list(wl.fanout), "batch": wl.batch_size, "W": W,
+                   "partitions": P, "local_owner": wl.local_owner, "windows_per_epoch": nwin},
+        "roofline": {"bound": "hbm", "kernel": "gg_gather_batch",
+                     "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                     "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": None,
+                     "bytes_per_launch": int(avg_bytes), "avg_launch_us": round(avg_ms * 1e3, 2)},
+        "stage_roofline": {"kernel": "gg_stage_bulk", "achieved": round(stage_gbs, 1),
+                           "frac": round(stage_gbs / HBM_PEAK_GBS, 4), "unit": "GB/s"},
+        "stage_ms_median": {k: round(float(np.median(v)), 4) for k, v in stage_ms.items()},
+        "rows_per_window": int(np.mean(rows_w)),
+        "hot_set_rows_per_window": int(np.mean(hot_w)),
+        "bulk_requests_per_window": float(np.mean(req_w)),
+        "gather_rows_per_s": round(rows / (g_ms * 1e-3) if g_ms else 0.0, 1),
+        "cpu_baseline": cpu,
+    }
+    print(json.dumps(line), flush=True)
+
+
+def cpu_baseline(inst, wl, W, so, b0, min_seconds):
+    """The CPU oracle, untuned and single-threaded, on window 0 of the same
+    workload; repeated until at least min_seconds of work when one window is
+    shorter than that."""
+    import numpy as np
+
+    from oracle import ggref
+    P = wl.num_parts
+    part = ggref.make_part(P, wl.part_kind, wl.local_owner, wl.num_nodes, inst.range_start)
+    feat = ggref.make_feat(wl.row_bytes, inst.shards, [wl.row_stride] * P)
+    boff = inst.batch_off
+    seeds = inst.seeds[boff[b0]:boff[b0 + len(so) - 1]]
+    slot_of = np.full(wl.num_nodes, -1, dtype=np.int32)
+    cache = None
+    reps, rows, t_total = 0, 0, 0.0
+    while True:
+        t = time.perf_counter()
+        fids, foff, nids, noff = ggref.sample_window(inst.row_ptr, inst.col_idx, seeds, so,
+                                                     wl.fanout, 0, 0, b0)
+        Wk = len(so) - 1
+        L = len(wl.fanout)
+        hot, freq = ggref.build_hotset(fids, foff, Wk, L, part, -1)
+        bucket, owner_off = ggref.bucket_by_owner(hot, part)
+        if cache is None or cache.shape[0] < len(hot):
+            t_alloc = time.perf_counter()
+            cache = np.zeros((len(hot), wl.row_stride), dtype=np.uint8)
+            t += time.perf_counter() - t_alloc
+        slot_of.fill(-1)
+        ggref.stage_bulk(bucket, owner_off, part, feat, cache, wl.row_stride, slot_of, None)
+        for b in range(Wk):
+            s = L * Wk + b
+            ids = fids[foff[s]:foff[s + 1]]
+            out = np.empty((len(ids), wl.row_stride), dtype=np.uint8)
+            ggref.gather_batch(ids, part, feat, cache, wl.row_stride, slot_of, out, wl.row_stride)
+            rows += len(ids)
+        t_total += time.perf_counter() - t
+        reps += 1
+        if t_total >= min_seconds or reps >= 1000:
+            break
+    log(f"cpu oracle: {reps} window(s), {rows} rows in {t_total:.1f}s")
+    return {"value": round(rows / t_total, 1), "unit": "rows/s", "cores": 1, "kind": "oracle",
+            "sample": f"{reps} x window 0 of {wl.name} (W={len(so) - 1}, {rows // reps} rows per "
+                      f"window), single-threaded C++ oracle, excluding input generation",
+            "host_cpu": cpu_model(), "host_nproc": os.cpu_count()}
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,250 @@
+/*
+ * gg.h -- C ABI of libgg, the MI355X (gfx950) per-window feature-fetch path.
+ *
+ * The method is GreenGNN's window-based caching (arXiv 2606.02916): the
+ * epoch is cut into windows of W consecutive sampled mini-batches
+ * (Sec. IV-A); each window's remote receptive-field nodes form a hot set
+ * that is staged into a local cache with one bulk request per partition
+ * owner, and every mini-batch then reads its input features from the cache,
+ * with an on-demand path for the residual misses (Sec. IV-C, Algorithm 1).
+ * The five calls below are the steps of that path for one window:
+ *
+ *   gg_sample_window    neighbour sampling of the W batches (Sec. IV-A step 2)
+ *   gg_build_hotset     hot set H_k of the window (Sec. IV-A window simulation)
+ *   gg_bucket_by_owner  H_k grouped by partition owner (Sec. IV-A rebuild events)
+ *   gg_stage_bulk       one bulk copy per non-empty owner into the cache (Sec. IV-C)
+ *   gg_gather_batch     per-batch assembly: local rows, cache hits, misses
+ *                       (Algorithm 1 inner loop; Eq. (2) request indicators)
+ *
+ * Conventions shared by every call:
+ *  - Pointers ending in _d are device pointers (memory from hipMalloc, or
+ *    pinned host memory from hipHostMalloc used through its device
+ *    address); pointers ending in _h are host pointers read during the call.
+ *    The caller owns every buffer and keeps it alive until the work queued
+ *    on `stream` has finished.
+ *  - Calls only enqueue work on `stream`; they never allocate, never
+ *    synchronise and keep no state between calls.  Scratch memory is the
+ *    caller's workspace `ws` of at least the size returned by the matching
+ *    gg_ws_* function; its contents need no initialisation.
+ *  - Return value: GG_OK, or a GG_ERR_* code when a host-visible argument
+ *    is invalid (nothing is enqueued then) or a launch failed;
+ *    gg_last_error() gives a message (per thread).
+ *  - Data-dependent failures found on the device (a capacity too small, a
+ *    node id or a feature row out of range) never write outside a buffer:
+ *    the kernels OR a GG_DEV_* bit into the caller's sticky status word
+ *    *status_d (int32, zeroed by the caller) and clamp.  Read it once per
+ *    window.
+ *  - Node ids are int32 in [0, num_nodes).  Feature rows are opaque bytes;
+ *    row_bytes must be a multiple of 4 and at most 32768.  The 16-byte
+ *    vector copy path is used when every base pointer and stride involved
+ *    is a multiple of 16, a 4-byte path otherwise.
+ */
+#ifndef GG_H
+#define GG_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define GG_VERSION 1
+
+#define GG_MAX_PARTS 64   /* partition owners */
+#define GG_MAX_LAYERS 4   /* sampling hops L */
+#define GG_MAX_W 64       /* batches per window */
+#define GG_MAX_FANOUT 32  /* neighbours drawn per node and hop */
+#define GG_MAX_ROW_BYTES 32768
+
+/* Return codes. */
+#define GG_OK 0
+#define GG_ERR_ARG 1
+#define GG_ERR_CAPACITY 2
+#define GG_ERR_HIP 3
+#define GG_ERR_UNSUPPORTED 4
+
+/* Bits of the sticky device status word. */
+#define GG_DEV_CAPACITY 1   /* an output capacity was too small; results clamped */
+#define GG_DEV_BAD_ID 2     /* a seed or neighbour id outside [0, num_nodes) */
+#define GG_DEV_BAD_ROW 4    /* a feature row or cache slot outside its shard or cache */
+#define GG_DEV_BAD_DEGREE 8 /* a node degree of 2^32 or more */
+
+/* Graph in CSR form (device): row u holds the sampled-from neighbours of u
+ * at col_idx[row_ptr[u] .. row_ptr[u+1]). */
+typedef struct gg_csr {
+  int64_t num_nodes;     /* < 2^31 */
+  int64_t num_edges;
+  const void* row_ptr;   /* num_nodes + 1 entries of int32 or int64 */
+  int32_t row_ptr_bits;  /* 32 or 64 */
+  int32_t pad_;
+  const int32_t* col_idx;
+} gg_csr_t;
+
+/* Partition book (Sec. IV notation: each node belongs to exactly one owner).
+ * Passed by value to the kernels; range_start is read on the host. */
+enum { GG_PART_MOD = 0, GG_PART_RANGE = 1 };
+typedef struct gg_part {
+  int32_t num_parts;    /* P, 1..GG_MAX_PARTS */
+  int32_t kind;         /* GG_PART_MOD: owner = u mod P, row = u div P.
+                           GG_PART_RANGE: owner = m with range_start[m] <= u <
+                           range_start[m+1], row = u - range_start[m]. */
+  int32_t local_owner;  /* this worker's own partition, or -1 (all remote) */
+  int32_t pad_;
+  int64_t num_nodes;
+  int64_t range_start[GG_MAX_PARTS + 1]; /* RANGE only: 0 = start[0] <= ... <= start[P] = num_nodes */
+} gg_part_t;
+
+/* Feature shards: owner m's row r is row_bytes bytes at
+ * shard[m] + r * row_stride[m] (device memory, or pinned host memory through
+ * its device address for remote owners kept in host memory). */
+typedef struct gg_feat {
+  int32_t row_bytes;
+  int32_t num_parts;
+  const void* shard[GG_MAX_PARTS];
+  int64_t row_stride[GG_MAX_PARTS];
+  int64_t shard_rows[GG_MAX_PARTS];
+} gg_feat_t;
+
+/* Outputs of gg_sample_window (all device, caller allocated).
+ * Level-major layout: segment s = l*W + b (l = 0..L, b = 0..W-1) holds the
+ * frontier F_l of batch b, ascending, at
+ * frontier_ids[frontier_off[s] .. frontier_off[s+1]); F_0 is the batch's
+ * distinct seeds and N_b = F_L is the batch's input node set.
+ * Segment l*W + b (l < L) of nbr_ids holds fanout[l] entries per node of
+ * F_l, in frontier order: the sampled neighbour ids, then -1 padding.
+ * frontier_bits holds, for every batch b, the bit set of N_b:
+ * bit (u & 31) of word frontier_bits[b * gg_bits_words(num_nodes) + (u >> 5)].
+ * need[0], need[1] receive the frontier and neighbour entries required;
+ * offsets are clamped to the capacities. */
+typedef struct gg_wsample {
+  int32_t* frontier_ids;
+  int64_t frontier_cap;
+  int64_t* frontier_off;   /* (L+1)*W + 1 entries */
+  int32_t* nbr_ids;
+  int64_t nbr_cap;
+  int64_t* nbr_off;        /* L*W + 1 entries */
+  uint32_t* frontier_bits; /* W * gg_bits_words(num_nodes) words */
+  int64_t* need;           /* 2 entries */
+} gg_wsample_t;
+
+/* Per-window staging statistics (device). */
+typedef struct gg_stage_stats {
+  int64_t rows_total;
+  int64_t requests_total;
+  int64_t invalidated;       /* previous-window entries cleared */
+  int64_t pad_;
+  int64_t requests[GG_MAX_PARTS];   /* 1 per non-empty owner bucket */
+  int64_t rows[GG_MAX_PARTS];
+  int64_t bytes[GG_MAX_PARTS];
+  int64_t delta_rows[GG_MAX_PARTS]; /* |bucket_m(H_k) \ H_{k-1}|, Sec. IV-A rebuild delta */
+} gg_stage_stats_t;
+
+/* Per-batch gather statistics (device). */
+typedef struct gg_gather_stats {
+  int64_t rows;
+  int64_t local;
+  int64_t hits;
+  int64_t misses;
+  int64_t miss_requests[GG_MAX_PARTS]; /* indicator of M_{b,m} != empty, Eq. (2) */
+  int64_t miss_rows[GG_MAX_PARTS];
+} gg_gather_stats_t;
+
+/* Words per batch of frontier_bits (a multiple of 2048). */
+int64_t gg_bits_words(int64_t num_nodes);
+
+/* Worst-case capacities of the sampling outputs for W batches of at most
+ * max_batch seeds: sum over l of min(num_nodes, max_batch * prod_{i<l}
+ * (fanout[i] + 1)) frontier entries per batch, and that bound times fanout[l]
+ * neighbour entries. */
+int gg_sample_caps(int64_t num_nodes, int32_t W, int64_t max_batch, const int32_t* fanout_h,
+                   int32_t L, int64_t* frontier_cap, int64_t* nbr_cap);
+
+/* Workspace sizes in bytes. */
+size_t gg_ws_sample(int64_t num_nodes, int32_t W);
+size_t gg_ws_hotset(int64_t num_nodes, int32_t W);
+size_t gg_ws_bucket(int64_t cap, int32_t num_parts);
+size_t gg_ws_gather(int64_t n_cap, int32_t num_parts);
+
+/* Neighbour sampling of one window (Sec. IV-A step 2: one epoch of
+ * deterministic sampling under fixed seeds fixes every later access).
+ * seeds_d[seed_off_h[b] .. seed_off_h[b+1]) are batch b's seed nodes
+ * (b = 0..W-1; seed_off_h[0] = 0).  Hop l (0-based) draws fanout_h[l] <=
+ * GG_MAX_FANOUT distinct neighbours of every node of F_l without
+ * replacement: all neighbours in CSR order when the degree d is at most
+ * fanout_h[l], else the positions chosen by Floyd's algorithm from a
+ * Philox4x32-10 stream (key = rng_seed; counter = (u, batch0 + b, epoch,
+ * (l << 16) | i/4), word i mod 4 for draw i, mapped onto [0, d-k+i] by
+ * floor(r * (d-k+i+1) / 2^32)), ascending.  F_{l+1} is F_l together with
+ * the neighbours drawn at hop l.  batch0 is the epoch-global index of the
+ * window's first batch, so N_b does not depend on W. */
+int gg_sample_window(const gg_csr_t* csr, const int32_t* seeds_d, const int64_t* seed_off_h,
+                     int32_t W, const int32_t* fanout_h, int32_t L, uint64_t rng_seed,
+                     int32_t epoch, int64_t batch0, const gg_wsample_t* out, int32_t* status_d,
+                     void* ws, size_t ws_bytes, hipStream_t stream);
+
+/* Hot set of the window (Sec. IV-A: the most frequently accessed remote
+ * nodes of the window).  Input: the W bit sets N_b written by
+ * gg_sample_window (frontier_bits_d).  freq(u) = number of batches whose N_b
+ * holds u; a node is remote when its owner is not part->local_owner.
+ * n_hot < 0 keeps every remote node of the window (the union); n_hot >= 0
+ * keeps the n_hot most frequent (ties: smaller id first).  hot_ids_d
+ * receives the chosen ids ascending, hot_freq_d (may be NULL) their freq;
+ * hot_count_d[0] = entries written (<= cap), hot_count_d[1] = entries
+ * required. */
+int gg_build_hotset(const uint32_t* frontier_bits_d, int32_t W, const gg_part_t* part,
+                    int64_t n_hot, int32_t* hot_ids_d, int32_t* hot_freq_d, int64_t cap,
+                    int64_t* hot_count_d, int32_t* status_d, void* ws, size_t ws_bytes,
+                    hipStream_t stream);
+
+/* Groups the hot set by owner, one bucket per owner (Sec. IV-A: one bulk
+ * request per partition owner): bucket_ids_d receives the hot_count_d[0]
+ * (<= cap) ids owner-major, input order kept inside each owner;
+ * owner_off_d[m] .. owner_off_d[m+1] is owner m's bucket (P+1 entries). */
+int gg_bucket_by_owner(const int32_t* hot_ids_d, const int64_t* hot_count_d, int64_t cap,
+                       const gg_part_t* part, int32_t* bucket_ids_d, int64_t* owner_off_d,
+                       int32_t* status_d, void* ws, size_t ws_bytes, hipStream_t stream);
+
+/* Stages the window cache (Sec. IV-C; Algorithm 1 WarmCache): clears the
+ * previous window's remap entries slot_of_d[prev_ids_d[i]] = -1 for
+ * i < prev_count_d[0] (both may be NULL), then for every owner with a
+ * non-empty bucket issues one bulk copy of its rows into cache slots
+ * owner_off_d[m] .. owner_off_d[m+1] (slot s at cache_d + s * cache_stride)
+ * and sets slot_of_d[u] = s.  slot_of_d has num_nodes entries, -1 where a
+ * node is not cached; the caller sets it to -1 once before the first
+ * window.  At most cap bucket entries and cache_rows slots are used.
+ * stats_d->delta_rows counts the staged rows absent from the previous
+ * window's cache (the rebuild delta); every hot row is copied. */
+int gg_stage_bulk(const int32_t* bucket_ids_d, const int64_t* owner_off_d, int64_t cap,
+                  const gg_part_t* part, const gg_feat_t* feat, void* cache_d,
+                  int64_t cache_stride, int64_t cache_rows, int32_t* slot_of_d,
+                  const int32_t* prev_ids_d, const int64_t* prev_count_d,
+                  gg_stage_stats_t* stats_d, int32_t* status_d, hipStream_t stream);
+
+/* Assembles one batch's input features (Algorithm 1 inner loop): for
+ * i < n = bounds_d[1] - bounds_d[0] (at most n_cap), with u =
+ * in_ids_d[bounds_d[0] + i], output row i (at out_d + i * out_stride)
+ * receives u's feature row: from the local shard when u's owner is
+ * part->local_owner, from cache slot slot_of_d[u] when that is >= 0 (a
+ * hit), and otherwise through the miss path: misses are grouped by owner
+ * and each non-empty group is one on-demand request served straight from
+ * that owner's shard (M_{b,m} of Sec. IV-A, Eq. (2)).  Passing
+ * in_ids_d = frontier_ids and bounds_d = frontier_off + L*W + b gathers N_b
+ * without a host synchronisation. */
+int gg_gather_batch(const int32_t* in_ids_d, const int64_t* bounds_d, int64_t n_cap,
+                    const gg_part_t* part, const gg_feat_t* feat, const void* cache_d,
+                    int64_t cache_stride, int64_t cache_rows, const int32_t* slot_of_d,
+                    void* out_d, int64_t out_stride, gg_gather_stats_t* stats_d,
+                    int32_t* status_d, void* ws, size_t ws_bytes, hipStream_t stream);
+
+/* Helpers. */
+const char* gg_status_string(int32_t code);
+const char* gg_last_error(void);
+int gg_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* GG_H */

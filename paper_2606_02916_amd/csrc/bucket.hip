@@ -1,0 +1,158 @@
+// gg_bucket_by_owner: stable partition of the hot set by partition owner.
+//
+// Three passes over the ids: per-block owner histograms, one exclusive scan
+// over the (owner, block) counts in owner-major order, and a scatter in
+// which every wavefront ranks its 64 ids among equal owners with ballots
+// (one ballot per distinct owner present in the wave), so order is kept
+// inside each owner.
+#include "gg_host.hpp"
+
+namespace gg {
+namespace {
+
+constexpr int kIdsPerBlock = 4096;             // 16 per thread
+constexpr int kIdsPerWave = kIdsPerBlock / 4;  // 1024 = 16 groups of 64
+
+__device__ __forceinline__ int64_t bucket_n(const int64_t* hot_count, int64_t cap) {
+  const int64_t n = hot_count[0];
+  return n < cap ? n : cap;
+}
+
+__global__ void __launch_bounds__(kBlock) k_bucket_count(const int32_t* ids, const int64_t* hot_count,
+                                                         int64_t cap, KPart part, int32_t* cnt,
+                                                         int32_t nblk, int32_t* status) {
+  __shared__ int32_t hist[GG_MAX_PARTS];
+  __shared__ int64_t s_start[GG_MAX_PARTS + 1];
+  for (int t = threadIdx.x; t < GG_MAX_PARTS; t += blockDim.x) hist[t] = 0;
+  for (int t = threadIdx.x; t <= GG_MAX_PARTS; t += blockDim.x) s_start[t] = part.start[t];
+  __syncthreads();
+  const int64_t n = bucket_n(hot_count, cap);
+  const int64_t i0 = (int64_t)blockIdx.x * kIdsPerBlock;
+  int32_t st = 0;
+  for (int it = 0; it < kIdsPerBlock / kBlock; ++it) {
+    const int64_t i = i0 + it * kBlock + threadIdx.x;
+    if (i < n) {
+      const int32_t u = ids[i];
+      if (u < 0 || (int64_t)u >= part.N) {
+        st |= GG_DEV_BAD_ID;
+      } else {
+        atomicAdd(&hist[owner_of(part, s_start, u)], 1);
+      }
+    }
+  }
+  if (st) set_status(status, st);
+  __syncthreads();
+  for (int m = threadIdx.x; m < part.P; m += blockDim.x) cnt[(int64_t)m * nblk + blockIdx.x] = hist[m];
+}
+
+__global__ void __launch_bounds__(1024) k_bucket_scan(const int32_t* cnt, int64_t ncnt, int32_t nblk,
+                                                      int32_t P, int64_t* off, int64_t* owner_off) {
+  __shared__ int64_t lds[16];
+  const int64_t total = block_scan_large(cnt, off, ncnt, 0, lds);
+  __syncthreads();
+  for (int m = threadIdx.x; m < P; m += blockDim.x) owner_off[m] = off[(int64_t)m * nblk];
+  if (threadIdx.x == 0) owner_off[P] = total;
+}
+
+__global__ void __launch_bounds__(kBlock) k_bucket_scatter(const int32_t* ids, const int64_t* hot_count,
+                                                           int64_t cap, KPart part, const int64_t* off,
+                                                           int32_t nblk, int32_t* out) {
+  __shared__ int32_t wcnt[4][GG_MAX_PARTS];
+  __shared__ int64_t wbase[4][GG_MAX_PARTS];
+  __shared__ int64_t s_start[GG_MAX_PARTS + 1];
+  const int w = threadIdx.x / kWave, lane = lane_id();
+  for (int t = threadIdx.x; t < 4 * GG_MAX_PARTS; t += blockDim.x) (&wcnt[0][0])[t] = 0;
+  for (int t = threadIdx.x; t <= GG_MAX_PARTS; t += blockDim.x) s_start[t] = part.start[t];
+  __syncthreads();
+  const int64_t n = bucket_n(hot_count, cap);
+  const int64_t i0 = (int64_t)blockIdx.x * kIdsPerBlock + (int64_t)w * kIdsPerWave;
+  // Per-wave owner counts.
+  for (int g = 0; g < kIdsPerWave / kWave; ++g) {
+    const int64_t i = i0 + g * kWave + lane;
+    if (i < n) {
+      const int32_t u = ids[i];
+      if (u >= 0 && (int64_t)u < part.N) atomicAdd(&wcnt[w][owner_of(part, s_start, u)], 1);
+    }
+  }
+  __syncthreads();
+  for (int t = threadIdx.x; t < 4 * part.P; t += blockDim.x) {
+    const int ww = t / part.P, m = t - ww * part.P;
+    int64_t b = off[(int64_t)m * nblk + blockIdx.x];
+    for (int v = 0; v < ww; ++v) b += wcnt[v][m];
+    wbase[ww][m] = b;
+  }
+  __syncthreads();
+  // Ordered scatter: groups of 64 in id order, ranks by ballot per owner.
+  // Lane m keeps the running output position of owner m.
+  int64_t my_base = lane < part.P ? wbase[w][lane] : 0;
+  for (int g = 0; g < kIdsPerWave / kWave; ++g) {
+    const int64_t i = i0 + g * kWave + lane;
+    int32_t u = -1, o = -1;
+    bool valid = false;
+    if (i < n) {
+      u = ids[i];
+      valid = u >= 0 && (int64_t)u < part.N;
+      if (valid) o = owner_of(part, s_start, u);
+    }
+    uint64_t active = __ballot(valid);
+    while (active) {
+      const int leader = __ffsll((unsigned long long)active) - 1;
+      const int32_t ol = __shfl(o, leader, kWave);
+      const uint64_t mm = __ballot(valid && o == ol);
+      const int64_t b = __shfl(my_base, ol, kWave);
+      if (valid && o == ol) out[b + lanes_below(mm)] = u;
+      if (lane == ol) my_base += __popcll(mm);
+      active &= ~mm;
+    }
+  }
+}
+
+struct BucketWs {
+  int32_t* cnt;
+  int64_t* off;
+};
+
+size_t bucket_ws_layout(int64_t cap, int32_t P, char* base, BucketWs* out) {
+  const int64_t nblk = std::max<int64_t>(1, cdiv(cap, kIdsPerBlock));
+  Carve cv{base, 0, ~(size_t)0};
+  BucketWs b;
+  b.cnt = cv.take<int32_t>((size_t)(nblk * P));
+  b.off = cv.take<int64_t>((size_t)(nblk * P));
+  if (out) *out = b;
+  return align_up(cv.used, 256);
+}
+
+}  // namespace
+}  // namespace gg
+
+using namespace gg;
+
+extern "C" size_t gg_ws_bucket(int64_t cap, int32_t num_parts) {
+  return bucket_ws_layout(cap, num_parts, nullptr, nullptr);
+}
+
+extern "C" int gg_bucket_by_owner(const int32_t* hot_ids_d, const int64_t* hot_count_d, int64_t cap,
+                                  const gg_part_t* part, int32_t* bucket_ids_d,
+                                  int64_t* owner_off_d, int32_t* status_d, void* ws,
+                                  size_t ws_bytes, hipStream_t stream) {
+  GG_REQUIRE(hot_count_d && owner_off_d && status_d, "NULL argument");
+  GG_REQUIRE(cap >= 0 && cap < (1LL << 31), "capacity %lld unsupported", (long long)cap);
+  GG_REQUIRE(cap == 0 || (hot_ids_d && bucket_ids_d), "NULL id buffer");
+  KPart kp;
+  int rc = pack_part(part, &kp);
+  if (rc != GG_OK) return rc;
+  BucketWs bw;
+  const size_t need_ws = bucket_ws_layout(cap, kp.P, (char*)ws, &bw);
+  GG_REQUIRE(ws && ws_bytes >= need_ws, "workspace of %zu bytes < %zu", ws_bytes, need_ws);
+  const int32_t nblk = (int32_t)std::max<int64_t>(1, cdiv(cap, kIdsPerBlock));
+  hipLaunchKernelGGL(k_bucket_count, dim3(nblk), dim3(kBlock), 0, stream, hot_ids_d, hot_count_d, cap,
+                     kp, bw.cnt, nblk, status_d);
+  GG_LAUNCH_CHECK("k_bucket_count");
+  hipLaunchKernelGGL(k_bucket_scan, dim3(1), dim3(1024), 0, stream, bw.cnt, (int64_t)nblk * kp.P,
+                     nblk, kp.P, bw.off, owner_off_d);
+  GG_LAUNCH_CHECK("k_bucket_scan");
+  hipLaunchKernelGGL(k_bucket_scatter, dim3(nblk), dim3(kBlock), 0, stream, hot_ids_d, hot_count_d,
+                     cap, kp, bw.off, nblk, bucket_ids_d);
+  GG_LAUNCH_CHECK("k_bucket_scatter");
+  return GG_OK;
+}

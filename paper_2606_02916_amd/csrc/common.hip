@@ -1,0 +1,122 @@
+// libgg: status strings, error reporting, argument packing, sizes.
+#include <string.h>
+
+#include "gg_host.hpp"
+
+namespace gg {
+
+static thread_local char g_err[512] = "";
+
+void set_error(const char* fmt, ...) {
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(g_err, sizeof(g_err), fmt, ap);
+  va_end(ap);
+}
+
+int pack_part(const gg_part_t* part, KPart* out) {
+  GG_REQUIRE(part != nullptr, "partition book is NULL");
+  const int32_t P = part->num_parts;
+  GG_REQUIRE(P >= 1 && P <= GG_MAX_PARTS, "num_parts %d outside 1..%d", P, GG_MAX_PARTS);
+  GG_REQUIRE(part->local_owner >= -1 && part->local_owner < P, "local_owner %d outside -1..%d",
+             part->local_owner, P - 1);
+  GG_REQUIRE(part->num_nodes >= 0 && part->num_nodes < (1LL << 31), "num_nodes %lld unsupported",
+             (long long)part->num_nodes);
+  out->P = P;
+  out->kind = part->kind;
+  out->local = part->local_owner;
+  out->pad_ = 0;
+  out->N = part->num_nodes;
+  out->div_magic = ((1ULL << 40) + (uint64_t)P - 1) / (uint64_t)P;
+  if (part->kind == GG_PART_RANGE) {
+    GG_REQUIRE(part->range_start[0] == 0, "range_start[0] must be 0");
+    GG_REQUIRE(part->range_start[P] == part->num_nodes, "range_start[P] must equal num_nodes");
+    for (int m = 0; m < P; ++m)
+      GG_REQUIRE(part->range_start[m + 1] >= part->range_start[m], "range_start not ascending");
+  } else {
+    GG_REQUIRE(part->kind == GG_PART_MOD, "unknown partition kind %d", part->kind);
+  }
+  for (int m = 0; m <= GG_MAX_PARTS; ++m)
+    out->start[m] = (part->kind == GG_PART_RANGE && m <= P) ? part->range_start[m] : part->num_nodes;
+  return GG_OK;
+}
+
+int pack_feat(const gg_feat_t* feat, const gg_part_t* part, KFeat* out) {
+  GG_REQUIRE(feat != nullptr, "feature description is NULL");
+  GG_REQUIRE(feat->num_parts == part->num_parts, "feature shards (%d) != partitions (%d)",
+             feat->num_parts, part->num_parts);
+  GG_REQUIRE(feat->row_bytes > 0 && feat->row_bytes <= GG_MAX_ROW_BYTES && feat->row_bytes % 4 == 0,
+             "row_bytes %d must be a positive multiple of 4 up to %d", feat->row_bytes,
+             GG_MAX_ROW_BYTES);
+  memset(out, 0, sizeof(*out));
+  out->row_bytes = feat->row_bytes;
+  out->P = feat->num_parts;
+  for (int m = 0; m < feat->num_parts; ++m) {
+    GG_REQUIRE(feat->shard_rows[m] >= 0, "shard_rows[%d] negative", m);
+    GG_REQUIRE(feat->shard_rows[m] == 0 || feat->shard[m] != nullptr, "shard[%d] is NULL", m);
+    GG_REQUIRE(feat->shard_rows[m] == 0 ||
+                   (feat->row_stride[m] >= feat->row_bytes && feat->row_stride[m] % 4 == 0),
+               "row_stride[%d] = %lld invalid", m, (long long)feat->row_stride[m]);
+    GG_REQUIRE(((uintptr_t)feat->shard[m] & 3u) == 0, "shard[%d] not 4-byte aligned", m);
+    out->shard[m] = (const char*)feat->shard[m];
+    out->stride[m] = feat->row_stride[m];
+    out->rows[m] = feat->shard_rows[m];
+  }
+  return GG_OK;
+}
+
+CopyGeom copy_geom(int32_t row_bytes, int vb) {
+  CopyGeom g;
+  g.row_bytes = row_bytes;
+  g.cpr = (uint32_t)(row_bytes / vb);
+  g.tail = vb == 16 ? (uint32_t)((row_bytes % 16) / 4) : 0u;
+  g.magic = g.cpr ? (uint32_t)(((1ULL << 32) + g.cpr - 1) / g.cpr) : 0u;
+  g.tmagic = g.tail ? (uint32_t)(((1ULL << 32) + g.tail - 1) / g.tail) : 0u;
+  return g;
+}
+
+}  // namespace gg
+
+extern "C" {
+
+const char* gg_last_error(void) { return gg::g_err; }
+
+int gg_version(void) { return GG_VERSION; }
+
+const char* gg_status_string(int32_t code) {
+  switch (code) {
+    case GG_OK: return "ok";
+    case GG_ERR_ARG: return "invalid argument";
+    case GG_ERR_CAPACITY: return "capacity too small";
+    case GG_ERR_HIP: return "HIP runtime error";
+    case GG_ERR_UNSUPPORTED: return "unsupported";
+    default: return "unknown status";
+  }
+}
+
+int64_t gg_bits_words(int64_t num_nodes) {
+  const int64_t words = (num_nodes + 31) / 32;
+  const int64_t w = gg::cdiv(words > 0 ? words : 1, gg::kChunkWords) * gg::kChunkWords;
+  return w;
+}
+
+int gg_sample_caps(int64_t num_nodes, int32_t W, int64_t max_batch, const int32_t* fanout_h,
+                   int32_t L, int64_t* frontier_cap, int64_t* nbr_cap) {
+  GG_REQUIRE(W >= 1 && W <= GG_MAX_W && L >= 1 && L <= GG_MAX_LAYERS && fanout_h && max_batch >= 0,
+             "bad arguments to gg_sample_caps");
+  int64_t f = 0, n = 0;
+  int64_t level = max_batch < num_nodes ? max_batch : num_nodes;
+  for (int32_t l = 0; l <= L; ++l) {
+    f += level;
+    if (l < L) {
+      n += level * fanout_h[l];
+      const int64_t grow = level * (int64_t)(fanout_h[l] + 1);
+      level = grow < num_nodes ? grow : num_nodes;
+    }
+  }
+  *frontier_cap = f * W;
+  *nbr_cap = n * W;
+  return GG_OK;
+}
+
+}  // extern "C"

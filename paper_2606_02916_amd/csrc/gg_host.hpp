@@ -1,0 +1,65 @@
+// Host-side helpers of libgg: argument checks, error reporting, kernel
+// argument packing and workspace carving.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdarg.h>
+#include <stdint.h>
+#include <stdio.h>
+
+#include <algorithm>
+
+#include "gg.h"
+#include "gg_dev.hpp"
+
+namespace gg {
+
+void set_error(const char* fmt, ...);
+
+#define GG_REQUIRE(cond, ...)        \
+  do {                               \
+    if (!(cond)) {                   \
+      ::gg::set_error(__VA_ARGS__);  \
+      return GG_ERR_ARG;             \
+    }                                \
+  } while (0)
+
+#define GG_LAUNCH_CHECK(what)                                                           \
+  do {                                                                                  \
+    hipError_t e_ = hipGetLastError();                                                  \
+    if (e_ != hipSuccess) {                                                             \
+      ::gg::set_error("%s: launch failed: %s", what, hipGetErrorString(e_));           \
+      return GG_ERR_HIP;                                                                \
+    }                                                                                   \
+  } while (0)
+
+inline int64_t cdiv(int64_t a, int64_t b) { return (a + b - 1) / b; }
+inline size_t align_up(size_t a, size_t b) { return (a + b - 1) / b * b; }
+
+// Checks a partition book and packs it for the kernels.
+int pack_part(const gg_part_t* part, KPart* out);
+
+// Checks feature shards against a partition book and packs them.
+int pack_feat(const gg_feat_t* feat, const gg_part_t* part, KFeat* out);
+
+// Geometry of the row copy for row_bytes and the vector width vb (16 or 4).
+CopyGeom copy_geom(int32_t row_bytes, int vb);
+
+inline bool aligned16(const void* p) { return ((uintptr_t)p & 15u) == 0; }
+
+// Bump allocator over the caller's workspace.
+struct Carve {
+  char* base;
+  size_t used;
+  size_t cap;
+  template <typename T>
+  T* take(size_t count) {
+    used = align_up(used, 256);
+    T* p = (T*)(base + used);
+    used += count * sizeof(T);
+    return p;
+  }
+  bool ok() const { return used <= cap; }
+};
+
+}  // namespace gg

@@ -1,0 +1,366 @@
+// gg_build_hotset: the hot set of one window from the W bit sets N_b.
+//
+// For every 32-node word the W batch words are summed into bit-sliced
+// counters (plane p holds bit p of every node's freq), so freq, the union
+// and the comparisons freq > f / freq == f are a handful of bitwise ops per
+// word.  With a budget n_hot the frequency histogram fixes a threshold f*
+// and a remainder r: the hot set is every remote node with freq > f* plus
+// the r smallest ids with freq == f*, which is the n_hot most frequent with
+// ties broken by smaller id.  Ids come out ascending because words are
+// visited in id order.
+#include "gg_host.hpp"
+
+namespace gg {
+namespace {
+
+constexpr int kPlanes = 7;  // freq <= GG_MAX_W = 64 needs 7 bits
+
+struct HotArgs {
+  int64_t wpb;
+  int64_t cap;
+  int32_t W;
+  int32_t fstar;   // used when params == nullptr
+  int64_t r;       // used when params == nullptr
+};
+
+__device__ __forceinline__ void bs_add(uint32_t (&pl)[kPlanes], uint32_t x) {
+  uint32_t carry = x;
+#pragma unroll
+  for (int p = 0; p < kPlanes; ++p) {
+    const uint32_t t = pl[p] & carry;
+    pl[p] ^= carry;
+    carry = t;
+  }
+}
+
+// Masks of the nodes of a word whose freq is > f and == f.
+__device__ __forceinline__ void bs_cmp(const uint32_t (&pl)[kPlanes], uint32_t f, uint32_t* gt,
+                                       uint32_t* eq) {
+  uint32_t g = 0u, e = 0xFFFFFFFFu;
+#pragma unroll
+  for (int p = kPlanes - 1; p >= 0; --p) {
+    if ((f >> p) & 1u) {
+      e &= pl[p];
+    } else {
+      g |= e & pl[p];
+      e &= ~pl[p];
+    }
+  }
+  *gt = g;
+  *eq = e;
+}
+
+__device__ __forceinline__ uint32_t bs_freq(const uint32_t (&pl)[kPlanes], int bit) {
+  uint32_t f = 0;
+#pragma unroll
+  for (int p = 0; p < kPlanes; ++p) f |= ((pl[p] >> bit) & 1u) << p;
+  return f;
+}
+
+// Bits of word w that belong to remote nodes (owner != local).
+__device__ __forceinline__ uint32_t remote_mask(const KPart& p, int64_t w) {
+  if (p.local < 0) return 0xFFFFFFFFu;
+  const int64_t u0 = w * 32;
+  uint32_t local = 0;
+  if (p.kind == GG_PART_MOD) {
+    const int32_t r0 = (int32_t)(u0 - (int64_t)mod_div(p, (uint32_t)u0) * p.P);
+    int j = p.local - r0;
+    if (j < 0) j += p.P;
+    for (; j < 32; j += p.P) local |= 1u << j;
+  } else {
+    const int64_t lo = p.start[p.local], hi = p.start[p.local + 1];
+    const int64_t a = lo > u0 ? lo : u0;
+    const int64_t b = hi < u0 + 32 ? hi : u0 + 32;
+    if (b > a) {
+      const int n = (int)(b - a), s = (int)(a - u0);
+      local = (n == 32 ? 0xFFFFFFFFu : ((1u << n) - 1u)) << s;
+    }
+  }
+  return ~local;
+}
+
+// Loads the 8 words of this thread for every batch and sums them into planes.
+__device__ __forceinline__ void load_planes(const uint32_t* bits, const HotArgs& a, int64_t w0,
+                                            uint32_t (&pl)[8][kPlanes]) {
+#pragma unroll
+  for (int j = 0; j < 8; ++j)
+#pragma unroll
+    for (int p = 0; p < kPlanes; ++p) pl[j][p] = 0u;
+  for (int32_t b = 0; b < a.W; ++b) {
+    const u32x4* q = (const u32x4*)(bits + (int64_t)b * a.wpb + w0);
+    const u32x4 x = q[0], y = q[1];
+    bs_add(pl[0], x.x);
+    bs_add(pl[1], x.y);
+    bs_add(pl[2], x.z);
+    bs_add(pl[3], x.w);
+    bs_add(pl[4], y.x);
+    bs_add(pl[5], y.y);
+    bs_add(pl[6], y.z);
+    bs_add(pl[7], y.w);
+  }
+}
+
+__device__ __forceinline__ void mask_planes(const KPart& p, int64_t w0, uint32_t (&pl)[8][kPlanes]) {
+#pragma unroll
+  for (int j = 0; j < 8; ++j) {
+    const uint32_t m = remote_mask(p, w0 + j);
+#pragma unroll
+    for (int q = 0; q < kPlanes; ++q) pl[j][q] &= m;
+  }
+}
+
+// Per-chunk histogram of freq over the remote nodes of the window.
+__global__ void __launch_bounds__(kBlock) k_hot_hist(const uint32_t* bits, KPart part, HotArgs a,
+                                                     int32_t* chunk_hist) {
+  __shared__ int32_t hist[GG_MAX_W + 2];
+  for (int t = threadIdx.x; t < GG_MAX_W + 2; t += blockDim.x) hist[t] = 0;
+  __syncthreads();
+  const int c = blockIdx.x;
+  const int64_t w0 = (int64_t)c * kChunkWords + threadIdx.x * kWordsPerThread;
+  uint32_t pl[8][kPlanes];
+  load_planes(bits, a, w0, pl);
+  mask_planes(part, w0, pl);
+  for (int32_t f = 1; f <= a.W; ++f) {
+    int n = 0;
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+      uint32_t g, e;
+      bs_cmp(pl[j], (uint32_t)f, &g, &e);
+      n += __popc(e);
+    }
+    if (n) atomicAdd(&hist[f], n);
+  }
+  __syncthreads();
+  for (int t = threadIdx.x; t <= a.W; t += blockDim.x) chunk_hist[(int64_t)c * (a.W + 1) + t] = hist[t];
+}
+
+// One block: total histogram, then the threshold f* and remainder r.
+__global__ void __launch_bounds__(1024) k_hot_select(const int32_t* chunk_hist, int32_t nch,
+                                                     int32_t W, int64_t n_hot, int64_t* params) {
+  __shared__ int64_t hist[GG_MAX_W + 2];
+  for (int t = threadIdx.x; t < GG_MAX_W + 2; t += blockDim.x) hist[t] = 0;
+  __syncthreads();
+  for (int64_t c = threadIdx.x; c < nch; c += blockDim.x)
+    for (int32_t f = 1; f <= W; ++f) {
+      const int32_t v = chunk_hist[c * (W + 1) + f];
+      if (v) atomicAdd((unsigned long long*)&hist[f], (unsigned long long)v);
+    }
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    int64_t total = 0;
+    for (int32_t f = 1; f <= W; ++f) total += hist[f];
+    int64_t fstar = 0, r = 0;
+    if (n_hot >= total) {
+      fstar = 0;
+    } else if (n_hot == 0) {
+      fstar = W + 1;
+    } else {
+      int64_t cum = 0;
+      for (int32_t f = W; f >= 1; --f) {
+        if (cum + hist[f] >= n_hot) {
+          fstar = f;
+          r = n_hot - cum;
+          break;
+        }
+        cum += hist[f];
+      }
+    }
+    params[0] = fstar;
+    params[1] = r;
+  }
+}
+
+__device__ __forceinline__ void get_sel(const HotArgs& a, const int64_t* params, uint32_t* fstar,
+                                        int64_t* r) {
+  if (params) {
+    *fstar = (uint32_t)params[0];
+    *r = params[1];
+  } else {
+    *fstar = (uint32_t)a.fstar;
+    *r = a.r;
+  }
+}
+
+// Per-chunk counts of nodes with freq > f* and freq == f*.
+__global__ void __launch_bounds__(kBlock) k_hot_count(const uint32_t* bits, KPart part, HotArgs a,
+                                                      const int64_t* params, int32_t* cnt_gt,
+                                                      int32_t* cnt_eq) {
+  __shared__ int32_t lds[2][kBlock / kWave];
+  const int c = blockIdx.x;
+  const int64_t w0 = (int64_t)c * kChunkWords + threadIdx.x * kWordsPerThread;
+  uint32_t fstar;
+  int64_t r;
+  get_sel(a, params, &fstar, &r);
+  uint32_t pl[8][kPlanes];
+  load_planes(bits, a, w0, pl);
+  mask_planes(part, w0, pl);
+  int ng = 0, ne = 0;
+#pragma unroll
+  for (int j = 0; j < 8; ++j) {
+    uint32_t g, e;
+    bs_cmp(pl[j], fstar, &g, &e);
+    if (fstar == 0) e = 0u;  // freq == 0 is not a member
+    ng += __popc(g);
+    ne += __popc(e);
+  }
+  ng = wave_sum(ng);
+  ne = wave_sum(ne);
+  if (lane_id() == 0) {
+    lds[0][threadIdx.x / kWave] = ng;
+    lds[1][threadIdx.x / kWave] = ne;
+  }
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    cnt_gt[c] = lds[0][0] + lds[0][1] + lds[0][2] + lds[0][3];
+    cnt_eq[c] = lds[1][0] + lds[1][1] + lds[1][2] + lds[1][3];
+  }
+}
+
+__global__ void __launch_bounds__(1024) k_hot_scan(const int32_t* cnt_gt, const int32_t* cnt_eq,
+                                                   int32_t nch, HotArgs a, const int64_t* params,
+                                                   int64_t* off_gt, int64_t* off_eq,
+                                                   int64_t* hot_count, int32_t* status) {
+  __shared__ int64_t lds[16];
+  uint32_t fstar;
+  int64_t r;
+  get_sel(a, params, &fstar, &r);
+  const int64_t tg = block_scan_large(cnt_gt, off_gt, nch, 0, lds);
+  const int64_t te = block_scan_large(cnt_eq, off_eq, nch, 0, lds);
+  if (threadIdx.x == 0) {
+    const int64_t total = tg + (te < r ? te : r);
+    hot_count[0] = total < a.cap ? total : a.cap;
+    hot_count[1] = total;
+    if (total > a.cap) set_status(status, GG_DEV_CAPACITY);
+  }
+}
+
+__global__ void __launch_bounds__(kBlock) k_hot_emit(const uint32_t* bits, KPart part, HotArgs a,
+                                                     const int64_t* params, const int64_t* off_gt,
+                                                     const int64_t* off_eq, int32_t* hot_ids,
+                                                     int32_t* hot_freq) {
+  __shared__ int64_t lds[kBlock / kWave];
+  const int c = blockIdx.x;
+  const int64_t w0 = (int64_t)c * kChunkWords + threadIdx.x * kWordsPerThread;
+  uint32_t fstar;
+  int64_t r;
+  get_sel(a, params, &fstar, &r);
+  uint32_t pl[8][kPlanes];
+  load_planes(bits, a, w0, pl);
+  mask_planes(part, w0, pl);
+  uint32_t gm[8], em[8];
+  int64_t ng = 0, ne = 0;
+#pragma unroll
+  for (int j = 0; j < 8; ++j) {
+    bs_cmp(pl[j], fstar, &gm[j], &em[j]);
+    if (fstar == 0) em[j] = 0u;
+    ng += __popc(gm[j]);
+    ne += __popc(em[j]);
+  }
+  int64_t tot;
+  const int64_t eq_rank0 = off_eq[c] + block_excl_scan<kBlock>(ne, lds, &tot);
+  int64_t take_eq = r - eq_rank0;
+  take_eq = take_eq < 0 ? 0 : (take_eq > ne ? ne : take_eq);
+  const int64_t sel_before_chunk = off_gt[c] + (off_eq[c] < r ? off_eq[c] : r);
+  int64_t pos = sel_before_chunk + block_excl_scan<kBlock>(ng + take_eq, lds, &tot);
+  int64_t eq_rank = eq_rank0;
+#pragma unroll
+  for (int j = 0; j < 8; ++j) {
+    uint32_t m = gm[j] | em[j];
+    while (m) {
+      const int bit = __ffs(m) - 1;
+      m &= m - 1;
+      bool take = true;
+      if ((em[j] >> bit) & 1u) {
+        take = eq_rank < r;
+        ++eq_rank;
+      }
+      if (take) {
+        if (pos < a.cap) {
+          hot_ids[pos] = (int32_t)((w0 + j) * 32 + bit);
+          if (hot_freq) hot_freq[pos] = (int32_t)bs_freq(pl[j], bit);
+        }
+        ++pos;
+      }
+    }
+  }
+}
+
+struct HotWs {
+  int32_t* chunk_hist;
+  int32_t* cnt_gt;
+  int32_t* cnt_eq;
+  int64_t* off_gt;
+  int64_t* off_eq;
+  int64_t* params;
+};
+
+size_t hot_ws_layout(int64_t num_nodes, int32_t W, char* base, HotWs* out) {
+  const int64_t nch = gg_bits_words(num_nodes) / kChunkWords;
+  Carve cv{base, 0, ~(size_t)0};
+  HotWs h;
+  h.chunk_hist = cv.take<int32_t>((size_t)(nch * (W + 1)));
+  h.cnt_gt = cv.take<int32_t>((size_t)nch);
+  h.cnt_eq = cv.take<int32_t>((size_t)nch);
+  h.off_gt = cv.take<int64_t>((size_t)nch);
+  h.off_eq = cv.take<int64_t>((size_t)nch);
+  h.params = cv.take<int64_t>(4);
+  if (out) *out = h;
+  return align_up(cv.used, 256);
+}
+
+}  // namespace
+}  // namespace gg
+
+using namespace gg;
+
+extern "C" size_t gg_ws_hotset(int64_t num_nodes, int32_t W) {
+  return hot_ws_layout(num_nodes, W, nullptr, nullptr);
+}
+
+extern "C" int gg_build_hotset(const uint32_t* frontier_bits_d, int32_t W, const gg_part_t* part,
+                               int64_t n_hot, int32_t* hot_ids_d, int32_t* hot_freq_d,
+                               int64_t cap, int64_t* hot_count_d, int32_t* status_d, void* ws,
+                               size_t ws_bytes, hipStream_t stream) {
+  GG_REQUIRE(frontier_bits_d && hot_count_d && status_d && (cap == 0 || hot_ids_d),
+             "NULL argument");
+  GG_REQUIRE(W >= 1 && W <= GG_MAX_W, "W = %d outside 1..%d", W, GG_MAX_W);
+  GG_REQUIRE(cap >= 0, "negative capacity");
+  GG_REQUIRE(aligned16(frontier_bits_d), "frontier_bits must be 16-byte aligned");
+  KPart kp;
+  int rc = pack_part(part, &kp);
+  if (rc != GG_OK) return rc;
+  GG_REQUIRE(kp.N >= 1, "empty graph");
+  HotWs hw;
+  const size_t need_ws = hot_ws_layout(kp.N, W, (char*)ws, &hw);
+  GG_REQUIRE(ws && ws_bytes >= need_ws, "workspace of %zu bytes < %zu", ws_bytes, need_ws);
+  const int64_t wpb = gg_bits_words(kp.N);
+  const int32_t nch = (int32_t)(wpb / kChunkWords);
+  HotArgs a;
+  a.wpb = wpb;
+  a.cap = cap;
+  a.W = W;
+  a.fstar = 0;
+  a.r = 0;
+  const int64_t* params = nullptr;
+  if (n_hot == 0) {
+    a.fstar = W + 1;
+  } else if (n_hot > 0) {
+    hipLaunchKernelGGL(k_hot_hist, dim3(nch), dim3(kBlock), 0, stream, frontier_bits_d, kp, a,
+                       hw.chunk_hist);
+    GG_LAUNCH_CHECK("k_hot_hist");
+    hipLaunchKernelGGL(k_hot_select, dim3(1), dim3(1024), 0, stream, hw.chunk_hist, nch, W, n_hot,
+                       hw.params);
+    GG_LAUNCH_CHECK("k_hot_select");
+    params = hw.params;
+  }
+  hipLaunchKernelGGL(k_hot_count, dim3(nch), dim3(kBlock), 0, stream, frontier_bits_d, kp, a, params,
+                     hw.cnt_gt, hw.cnt_eq);
+  GG_LAUNCH_CHECK("k_hot_count");
+  hipLaunchKernelGGL(k_hot_scan, dim3(1), dim3(1024), 0, stream, hw.cnt_gt, hw.cnt_eq, nch, a,
+                     params, hw.off_gt, hw.off_eq, hot_count_d, status_d);
+  GG_LAUNCH_CHECK("k_hot_scan");
+  hipLaunchKernelGGL(k_hot_emit, dim3(nch), dim3(kBlock), 0, stream, frontier_bits_d, kp, a, params,
+                     hw.off_gt, hw.off_eq, hot_ids_d, hot_freq_d);
+  GG_LAUNCH_CHECK("k_hot_emit");
+  return GG_OK;
+}

@@ -1,0 +1,415 @@
+// gg_sample_window: neighbour sampling of the W batches of one window.
+//
+// Every batch keeps a bit set over all node ids (N bits, in HBM).  The set
+// starts as the batch's seeds; hop l samples the neighbours of every node of
+// the current frontier F_l and ORs them in, so the set becomes F_{l+1} =
+// F_l plus the sampled neighbours.  After each hop the sets are compacted
+// into ascending id lists: a per-chunk popcount, one device-wide exclusive
+// scan, and an emit pass.  Deduplication therefore costs one streaming pass
+// over N/8 bytes per batch and hop instead of a sort of the sampled ids.
+#include <limits.h>
+
+#include "gg_host.hpp"
+
+namespace gg {
+namespace {
+
+struct SeedOff {
+  int64_t off[GG_MAX_W + 1];  // entries past W hold INT64_MAX
+};
+
+struct LevelArgs {
+  int32_t lv, L, W, k;
+  int32_t nch;
+  int32_t pad_;
+  int64_t fcap, ncap;
+};
+
+struct SampleArgs {
+  int64_t N;
+  int64_t wpb;
+  int64_t fcap, ncap;
+  int64_t batch0;
+  int32_t W, l, k;
+  uint32_t key0, key1, epoch;
+};
+
+// Largest b in [0, 64) with off[b] <= x, for a table padded with INT64_MAX.
+__device__ __forceinline__ int find_batch(const int64_t* off, int64_t x) {
+  int idx = 0;
+#pragma unroll
+  for (int step = 32; step >= 1; step >>= 1)
+    if (off[idx + step] <= x) idx += step;
+  return idx;
+}
+
+__global__ void __launch_bounds__(kBlock) k_zero_words(uint32_t* p, int64_t n4) {
+  u32x4* q = (u32x4*)p;
+  const u32x4 z = {0u, 0u, 0u, 0u};
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n4;
+       i += (int64_t)gridDim.x * blockDim.x)
+    q[i] = z;
+}
+
+__global__ void __launch_bounds__(kBlock) k_mark_seeds(const int32_t* seeds, SeedOff so, int32_t W,
+                                                       uint32_t* bits, int64_t wpb, int64_t N,
+                                                       int32_t* status) {
+  const int64_t total = so.off[W];
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < total;
+       i += (int64_t)gridDim.x * blockDim.x) {
+    const int b = find_batch(so.off, i);
+    const int32_t u = seeds[i];
+    if (u < 0 || (int64_t)u >= N) {
+      set_status(status, GG_DEV_BAD_ID);
+      continue;
+    }
+    atomicOr(bits + (int64_t)b * wpb + (u >> 5), 1u << (u & 31));
+  }
+}
+
+// Popcount of one chunk (kChunkWords words) of one batch's bit set.
+__global__ void __launch_bounds__(kBlock) k_bits_count(const uint32_t* bits, int64_t wpb,
+                                                       int32_t* cnt) {
+  __shared__ int32_t lds[kBlock / kWave];
+  const int c = blockIdx.x, b = blockIdx.y, nch = gridDim.x;
+  const u32x4* p = (const u32x4*)(bits + (int64_t)b * wpb + (int64_t)c * kChunkWords +
+                                  threadIdx.x * kWordsPerThread);
+  const u32x4 x = p[0], y = p[1];
+  int s = __popc(x.x) + __popc(x.y) + __popc(x.z) + __popc(x.w) + __popc(y.x) + __popc(y.y) +
+          __popc(y.z) + __popc(y.w);
+  s = wave_sum(s);
+  if (lane_id() == 0) lds[threadIdx.x / kWave] = s;
+  __syncthreads();
+  if (threadIdx.x == 0) cnt[(int64_t)b * nch + c] = lds[0] + lds[1] + lds[2] + lds[3];
+}
+
+// One block of 1024 threads: scans the chunk counts of level lv and writes
+// the level's frontier and neighbour offsets (clamped to the capacities).
+// lvl[0] = raw frontier end, lvl[1] = raw neighbour end, lvl[2+l] = raw
+// neighbour base of level l.
+__global__ void __launch_bounds__(1024) k_level_scan(const int32_t* cnt, int64_t* chunk_off,
+                                                     int64_t* frontier_off, int64_t* nbr_off,
+                                                     int64_t* lvl, int64_t* need, int32_t* status,
+                                                     LevelArgs a) {
+  __shared__ int64_t lds[16];
+  __shared__ int64_t s_base[2];
+  if (threadIdx.x == 0) {
+    s_base[0] = a.lv == 0 ? 0 : lvl[0];
+    s_base[1] = a.lv == 0 ? 0 : lvl[1];
+  }
+  __syncthreads();
+  const int64_t raw_base = s_base[0];
+  const int64_t raw_nbase = s_base[1];
+  const int64_t n = (int64_t)a.W * a.nch;
+  const int64_t total = block_scan_large(cnt, chunk_off, n, raw_base, lds);
+  __syncthreads();
+  const int64_t raw_end = raw_base + total;
+  const int64_t cb = raw_base < a.fcap ? raw_base : a.fcap;
+  const int64_t ce = raw_end < a.fcap ? raw_end : a.fcap;
+  const int t = threadIdx.x;
+  if (t < a.W) {
+    int64_t v = chunk_off[(int64_t)t * a.nch];
+    v = v < a.fcap ? v : a.fcap;
+    frontier_off[(int64_t)a.lv * a.W + t] = v;
+    if (a.lv < a.L) {
+      int64_t nv = raw_nbase + (v - cb) * a.k;
+      nbr_off[(int64_t)a.lv * a.W + t] = nv < a.ncap ? nv : a.ncap;
+    }
+  }
+  if (t == 0) {
+    frontier_off[(int64_t)(a.lv + 1) * a.W] = ce;
+    lvl[0] = raw_end;
+    need[0] = raw_end;
+    int32_t st = raw_end > a.fcap ? GG_DEV_CAPACITY : 0;
+    if (a.lv < a.L) {
+      const int64_t nend = raw_nbase + (ce - cb) * a.k;
+      nbr_off[(int64_t)(a.lv + 1) * a.W] = nend < a.ncap ? nend : a.ncap;
+      lvl[2 + a.lv] = raw_nbase;
+      lvl[1] = nend;
+      need[1] = nend;
+      if (nend > a.ncap) st |= GG_DEV_CAPACITY;
+    }
+    if (st) set_status(status, st);
+  }
+}
+
+// Writes the ids of one chunk of one batch's bit set, ascending.
+__global__ void __launch_bounds__(kBlock) k_bits_emit(const uint32_t* bits, int64_t wpb,
+                                                      const int64_t* chunk_off, int32_t* ids,
+                                                      int64_t fcap) {
+  __shared__ int32_t lds[kBlock / kWave];
+  const int c = blockIdx.x, b = blockIdx.y, nch = gridDim.x;
+  const int64_t w0 = (int64_t)c * kChunkWords + threadIdx.x * kWordsPerThread;
+  const u32x4* p = (const u32x4*)(bits + (int64_t)b * wpb + w0);
+  const u32x4 x = p[0], y = p[1];
+  const uint32_t w[8] = {x.x, x.y, x.z, x.w, y.x, y.y, y.z, y.w};
+  int n = 0;
+#pragma unroll
+  for (int j = 0; j < 8; ++j) n += __popc(w[j]);
+  int32_t tot;
+  const int32_t ex = block_excl_scan<kBlock>(n, lds, &tot);
+  int64_t pos = chunk_off[(int64_t)b * nch + c] + ex;
+#pragma unroll
+  for (int j = 0; j < 8; ++j) {
+    uint32_t m = w[j];
+    while (m) {
+      const int bit = __ffs(m) - 1;
+      m &= m - 1;
+      if (pos < fcap) ids[pos] = (int32_t)((w0 + j) * 32 + bit);
+      ++pos;
+    }
+  }
+}
+
+template <int KMAX>
+__device__ __forceinline__ void floyd_positions(uint32_t u, uint32_t bglob, const SampleArgs& a,
+                                                uint32_t d, uint32_t* pos) {
+  const uint32_t k = (uint32_t)a.k;
+  uint4 blk = make_uint4(0u, 0u, 0u, 0u);
+#pragma unroll
+  for (int i = 0; i < KMAX; ++i) {
+    if ((uint32_t)i < k) {
+      if ((i & 3) == 0)
+        blk = philox4x32_10(make_uint4(u, bglob, a.epoch, ((uint32_t)a.l << 16) | (uint32_t)(i >> 2)),
+                            a.key0, a.key1);
+      const uint32_t r = (i & 3) == 0 ? blk.x : (i & 3) == 1 ? blk.y : (i & 3) == 2 ? blk.z : blk.w;
+      const uint32_t j = d - k + (uint32_t)i;
+      const uint32_t t = (uint32_t)(((uint64_t)r * ((uint64_t)j + 1u)) >> 32);
+      bool dup = false;
+#pragma unroll
+      for (int q = 0; q < i; ++q) dup |= (pos[q] == t);
+      pos[i] = dup ? j : t;
+    } else {
+      pos[i] = 0xFFFFFFFFu;
+    }
+  }
+  // Bitonic sorting network, ascending.
+#pragma unroll
+  for (int size = 2; size <= KMAX; size <<= 1) {
+#pragma unroll
+    for (int stride = size >> 1; stride > 0; stride >>= 1) {
+#pragma unroll
+      for (int i = 0; i < KMAX; ++i) {
+        const int j = i ^ stride;
+        if (j > i) {
+          const bool up = (i & size) == 0;
+          const uint32_t x = pos[i], y = pos[j];
+          const bool sw = up ? (x > y) : (x < y);
+          pos[i] = sw ? y : x;
+          pos[j] = sw ? x : y;
+        }
+      }
+    }
+  }
+}
+
+// One lane per frontier node of level l (all batches of the window).
+template <typename RowT, int KMAX>
+__global__ void __launch_bounds__(kBlock) k_sample(const RowT* row_ptr, const int32_t* col_idx,
+                                                   const int32_t* fids, const int64_t* frontier_off,
+                                                   const int64_t* lvl, int32_t* nbr, uint32_t* bits,
+                                                   int32_t* status, SampleArgs a) {
+  __shared__ int64_t so[GG_MAX_W + 1];
+  __shared__ int64_t s_nbase;
+  for (int t = threadIdx.x; t <= GG_MAX_W; t += blockDim.x)
+    so[t] = t <= a.W ? frontier_off[(int64_t)a.l * a.W + t] : INT64_MAX;
+  if (threadIdx.x == 0) s_nbase = lvl[2 + a.l];
+  __syncthreads();
+  const int64_t begin = so[0], end = so[a.W];
+  const int64_t nbase = s_nbase;
+  const int32_t k = a.k;
+  int32_t st = 0;
+  for (int64_t gi = begin + (int64_t)blockIdx.x * blockDim.x + threadIdx.x; gi < end;
+       gi += (int64_t)gridDim.x * blockDim.x) {
+    const int b = find_batch(so, gi);
+    const int32_t u = fids[gi];
+    const int64_t obase = nbase + (gi - begin) * k;
+    if (obase + k > a.ncap) {
+      st |= GG_DEV_CAPACITY;
+      continue;
+    }
+    int32_t* out = nbr + obase;
+    uint32_t* brow = bits + (int64_t)b * a.wpb;
+    const int64_t beg = (int64_t)row_ptr[u];
+    const int64_t d = (int64_t)row_ptr[u + 1] - beg;
+    if (d <= k) {
+      for (int32_t p = 0; p < k; ++p) {
+        int32_t v = -1;
+        if (p < d) {
+          v = col_idx[beg + p];
+          if (v < 0 || (int64_t)v >= a.N) {
+            st |= GG_DEV_BAD_ID;
+            v = -1;
+          } else {
+            atomicOr(brow + (v >> 5), 1u << (v & 31));
+          }
+        }
+        out[p] = v;
+      }
+    } else if (d > 0xFFFFFFFFLL) {
+      st |= GG_DEV_BAD_DEGREE;
+      for (int32_t p = 0; p < k; ++p) out[p] = -1;
+    } else {
+      uint32_t pos[KMAX];
+      floyd_positions<KMAX>((uint32_t)u, (uint32_t)(a.batch0 + b), a, (uint32_t)d, pos);
+#pragma unroll
+      for (int i = 0; i < KMAX; ++i) {
+        if (i < k) {
+          int32_t v = col_idx[beg + pos[i]];
+          if (v < 0 || (int64_t)v >= a.N) {
+            st |= GG_DEV_BAD_ID;
+            v = -1;
+          } else {
+            atomicOr(brow + (v >> 5), 1u << (v & 31));
+          }
+          out[i] = v;
+        }
+      }
+    }
+  }
+  if (st) set_status(status, st);
+}
+
+struct SampleWs {
+  int32_t* cnt;
+  int64_t* chunk_off;
+  int64_t* lvl;
+};
+
+size_t sample_ws_layout(int64_t num_nodes, int32_t W, char* base, SampleWs* out) {
+  const int64_t nch = gg_bits_words(num_nodes) / kChunkWords;
+  Carve cv{base, 0, ~(size_t)0};
+  SampleWs s;
+  s.cnt = cv.take<int32_t>((size_t)(W * nch));
+  s.chunk_off = cv.take<int64_t>((size_t)(W * nch));
+  s.lvl = cv.take<int64_t>(2 + GG_MAX_LAYERS);
+  if (out) *out = s;
+  return align_up(cv.used, 256);
+}
+
+template <typename RowT>
+int launch_sample(const gg_csr_t* csr, const gg_wsample_t* out, const SampleWs& ws, int32_t* status,
+                  const SampleArgs& a, int64_t bound, hipStream_t stream) {
+  const int grid = (int)std::min<int64_t>(std::max<int64_t>(cdiv(bound, kBlock), 1), 8192);
+  const RowT* rp = (const RowT*)csr->row_ptr;
+  if (a.k <= 8)
+    hipLaunchKernelGGL((k_sample<RowT, 8>), dim3(grid), dim3(kBlock), 0, stream, rp, csr->col_idx,
+                       out->frontier_ids, out->frontier_off, ws.lvl, out->nbr_ids,
+                       out->frontier_bits, status, a);
+  else if (a.k <= 16)
+    hipLaunchKernelGGL((k_sample<RowT, 16>), dim3(grid), dim3(kBlock), 0, stream, rp,
+                       csr->col_idx, out->frontier_ids, out->frontier_off, ws.lvl, out->nbr_ids,
+                       out->frontier_bits, status, a);
+  else
+    hipLaunchKernelGGL((k_sample<RowT, 32>), dim3(grid), dim3(kBlock), 0, stream, rp,
+                       csr->col_idx, out->frontier_ids, out->frontier_off, ws.lvl, out->nbr_ids,
+                       out->frontier_bits, status, a);
+  GG_LAUNCH_CHECK("k_sample");
+  return GG_OK;
+}
+
+}  // namespace
+}  // namespace gg
+
+using namespace gg;
+
+extern "C" size_t gg_ws_sample(int64_t num_nodes, int32_t W) {
+  return sample_ws_layout(num_nodes, W, nullptr, nullptr);
+}
+
+extern "C" int gg_sample_window(const gg_csr_t* csr, const int32_t* seeds_d,
+                                const int64_t* seed_off_h, int32_t W, const int32_t* fanout_h,
+                                int32_t L, uint64_t rng_seed, int32_t epoch, int64_t batch0,
+                                const gg_wsample_t* out, int32_t* status_d, void* ws,
+                                size_t ws_bytes, hipStream_t stream) {
+  GG_REQUIRE(csr && out && seed_off_h && fanout_h && status_d, "NULL argument");
+  GG_REQUIRE(W >= 1 && W <= GG_MAX_W, "W = %d outside 1..%d", W, GG_MAX_W);
+  GG_REQUIRE(L >= 1 && L <= GG_MAX_LAYERS, "L = %d outside 1..%d", L, GG_MAX_LAYERS);
+  GG_REQUIRE(csr->num_nodes >= 1 && csr->num_nodes < (1LL << 31), "num_nodes %lld unsupported",
+             (long long)csr->num_nodes);
+  GG_REQUIRE(csr->row_ptr_bits == 32 || csr->row_ptr_bits == 64, "row_ptr_bits must be 32 or 64");
+  GG_REQUIRE(csr->row_ptr && (csr->num_edges == 0 || csr->col_idx), "CSR arrays are NULL");
+  GG_REQUIRE(csr->row_ptr_bits == 64 || csr->num_edges < (1LL << 31),
+             "int32 row_ptr with %lld edges", (long long)csr->num_edges);
+  for (int l = 0; l < L; ++l)
+    GG_REQUIRE(fanout_h[l] >= 1 && fanout_h[l] <= GG_MAX_FANOUT, "fanout[%d] = %d outside 1..%d",
+               l, fanout_h[l], GG_MAX_FANOUT);
+  GG_REQUIRE(seed_off_h[0] == 0, "seed_off[0] must be 0");
+  for (int b = 0; b < W; ++b)
+    GG_REQUIRE(seed_off_h[b + 1] >= seed_off_h[b], "seed_off not ascending");
+  GG_REQUIRE(seed_off_h[W] == 0 || seeds_d, "seeds are NULL");
+  GG_REQUIRE(out->frontier_ids && out->frontier_off && out->nbr_ids && out->nbr_off &&
+                 out->frontier_bits && out->need,
+             "NULL output buffer");
+  GG_REQUIRE(out->frontier_cap >= 0 && out->nbr_cap >= 0, "negative capacity");
+  GG_REQUIRE(aligned16(out->frontier_bits), "frontier_bits must be 16-byte aligned");
+  const int64_t N = csr->num_nodes;
+  SampleWs sw;
+  const size_t need_ws = sample_ws_layout(N, W, (char*)ws, &sw);
+  GG_REQUIRE(ws && ws_bytes >= need_ws, "workspace of %zu bytes < %zu", ws_bytes, need_ws);
+
+  const int64_t wpb = gg_bits_words(N);
+  const int32_t nch = (int32_t)(wpb / kChunkWords);
+
+  hipLaunchKernelGGL(k_zero_words, dim3((unsigned)std::min<int64_t>(cdiv(W * wpb / 4, kBlock), 4096)),
+                     dim3(kBlock), 0, stream, out->frontier_bits, W * wpb / 4);
+  GG_LAUNCH_CHECK("k_zero_words");
+  SeedOff so;
+  for (int b = 0; b <= GG_MAX_W; ++b) so.off[b] = b <= W ? seed_off_h[b] : INT64_MAX;
+  if (seed_off_h[W] > 0) {
+    hipLaunchKernelGGL(k_mark_seeds,
+                       dim3((unsigned)std::min<int64_t>(cdiv(seed_off_h[W], kBlock), 4096)),
+                       dim3(kBlock), 0, stream, seeds_d, so, W, out->frontier_bits, wpb, N,
+                       status_d);
+    GG_LAUNCH_CHECK("k_mark_seeds");
+  }
+  // Host bound on each level's entries, for the sampler's grid.
+  int64_t bound[GG_MAX_LAYERS + 1] = {0};
+  for (int b = 0; b < W; ++b) {
+    int64_t lev = std::min<int64_t>(seed_off_h[b + 1] - seed_off_h[b], N);
+    for (int l = 0; l <= L; ++l) {
+      bound[l] += lev;
+      if (l < L) lev = std::min<int64_t>(lev * (fanout_h[l] + 1), N);
+    }
+  }
+  for (int lv = 0; lv <= L; ++lv) {
+    if (lv > 0) {
+      SampleArgs a;
+      a.N = N;
+      a.wpb = wpb;
+      a.fcap = out->frontier_cap;
+      a.ncap = out->nbr_cap;
+      a.batch0 = batch0;
+      a.W = W;
+      a.l = lv - 1;
+      a.k = fanout_h[lv - 1];
+      a.key0 = (uint32_t)rng_seed;
+      a.key1 = (uint32_t)(rng_seed >> 32);
+      a.epoch = (uint32_t)epoch;
+      const int64_t bnd = std::min<int64_t>(bound[lv - 1], out->frontier_cap);
+      int rc = csr->row_ptr_bits == 64
+                   ? launch_sample<int64_t>(csr, out, sw, status_d, a, bnd, stream)
+                   : launch_sample<int32_t>(csr, out, sw, status_d, a, bnd, stream);
+      if (rc != GG_OK) return rc;
+    }
+    hipLaunchKernelGGL(k_bits_count, dim3(nch, W), dim3(kBlock), 0, stream, out->frontier_bits, wpb,
+                       sw.cnt);
+    GG_LAUNCH_CHECK("k_bits_count");
+    LevelArgs la;
+    la.lv = lv;
+    la.L = L;
+    la.W = W;
+    la.k = lv < L ? fanout_h[lv] : 0;
+    la.nch = nch;
+    la.pad_ = 0;
+    la.fcap = out->frontier_cap;
+    la.ncap = out->nbr_cap;
+    hipLaunchKernelGGL(k_level_scan, dim3(1), dim3(1024), 0, stream, sw.cnt, sw.chunk_off,
+                       out->frontier_off, out->nbr_off, sw.lvl, out->need, status_d, la);
+    GG_LAUNCH_CHECK("k_level_scan");
+    hipLaunchKernelGGL(k_bits_emit, dim3(nch, W), dim3(kBlock), 0, stream, out->frontier_bits, wpb,
+                       sw.chunk_off, out->frontier_ids, out->frontier_cap);
+    GG_LAUNCH_CHECK("k_bits_emit");
+  }
+  return GG_OK;
+}

@@ -1,0 +1,207 @@
+// gg_stage_bulk: one bulk request per non-empty owner bucket into the
+// window cache, plus the ID-to-slot remap.
+//
+// The bucketed hot set is owner-major, so each owner's rows form one
+// contiguous run of cache slots: the bulk request of owner m is the copy of
+// slots owner_off[m] .. owner_off[m+1] from shard m.  All owners' requests
+// go out in one launch; each wavefront copies 64 consecutive slots with the
+// row copy engine and writes slot_of for them.
+#include <stdlib.h>
+#include <string.h>
+
+#include "gg_host.hpp"
+
+namespace gg {
+namespace {
+
+struct StageArgs {
+  int64_t cap;         // bucket entries usable
+  int64_t cache_rows;
+  int64_t cache_stride;
+  CopyGeom geom;
+};
+
+__device__ __forceinline__ int64_t stage_n(const int64_t* owner_off, int32_t P, const StageArgs& a) {
+  int64_t n = owner_off[P];
+  n = n < a.cap ? n : a.cap;
+  return n < a.cache_rows ? n : a.cache_rows;
+}
+
+__global__ void k_stage_prep(gg_stage_stats_t* stats) {
+  int64_t* p = (int64_t*)stats;
+  const int n = (int)(sizeof(gg_stage_stats_t) / sizeof(int64_t));
+  for (int t = threadIdx.x; t < n; t += blockDim.x) p[t] = 0;
+}
+
+// Rebuild delta: staged rows whose node is not in the previous window's
+// cache (slot_of still describes that cache here).
+__global__ void __launch_bounds__(kBlock) k_stage_delta(const int32_t* bucket, const int64_t* owner_off,
+                                                        KPart part, StageArgs a, const int32_t* slot_of,
+                                                        gg_stage_stats_t* stats) {
+  __shared__ int32_t hist[GG_MAX_PARTS];
+  __shared__ int64_t s_start[GG_MAX_PARTS + 1];
+  for (int t = threadIdx.x; t < GG_MAX_PARTS; t += blockDim.x) hist[t] = 0;
+  for (int t = threadIdx.x; t <= GG_MAX_PARTS; t += blockDim.x) s_start[t] = part.start[t];
+  __syncthreads();
+  const int64_t n = stage_n(owner_off, part.P, a);
+  for (int64_t s = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; s < n;
+       s += (int64_t)gridDim.x * blockDim.x) {
+    const int32_t u = bucket[s];
+    if (u < 0 || (int64_t)u >= part.N) continue;
+    if (slot_of[u] < 0) atomicAdd(&hist[owner_of(part, s_start, u)], 1);
+  }
+  __syncthreads();
+  for (int m = threadIdx.x; m < part.P; m += blockDim.x)
+    if (hist[m])
+      atomicAdd((unsigned long long*)&stats->delta_rows[m], (unsigned long long)hist[m]);
+}
+
+__global__ void __launch_bounds__(kBlock) k_slot_reset(const int32_t* prev, const int64_t* prev_count,
+                                                       int64_t N, int32_t* slot_of) {
+  const int64_t n = prev_count[0];
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n;
+       i += (int64_t)gridDim.x * blockDim.x) {
+    const int32_t u = prev[i];
+    if (u >= 0 && (int64_t)u < N) slot_of[u] = -1;
+  }
+}
+
+template <int VB, bool NT>
+__global__ void __launch_bounds__(kBlock) k_stage_rows(const int32_t* bucket, const int64_t* owner_off,
+                                                       KPart part, KFeat feat, StageArgs a,
+                                                       char* cache, int32_t* slot_of,
+                                                       int32_t* status) {
+  __shared__ int64_t s_start[GG_MAX_PARTS + 1];
+  for (int t = threadIdx.x; t <= GG_MAX_PARTS; t += blockDim.x) s_start[t] = part.start[t];
+  __syncthreads();
+  const int64_t n = stage_n(owner_off, part.P, a);
+  const int64_t ntiles = (n + kWave - 1) / kWave;
+  const int lane = lane_id();
+  int32_t st = 0;
+  for (int64_t tile = (int64_t)blockIdx.x * (kBlock / kWave) + threadIdx.x / kWave; tile < ntiles;
+       tile += (int64_t)gridDim.x * (kBlock / kWave)) {
+    const int64_t s0 = tile * kWave;
+    const int64_t s = s0 + lane;
+    const char* src = nullptr;
+    if (s < n) {
+      const int32_t u = bucket[s];
+      if (u < 0 || (int64_t)u >= part.N) {
+        st |= GG_DEV_BAD_ID;
+      } else {
+        const int32_t m = owner_of(part, s_start, u);
+        const int64_t r = row_of(part, s_start, u, m);
+        if (r >= feat.rows[m]) {
+          st |= GG_DEV_BAD_ROW;
+        } else {
+          src = feat.shard[m] + r * feat.stride[m];
+          slot_of[u] = (int32_t)s;
+        }
+      }
+    }
+    const int nrows = (int)((n - s0) < kWave ? (n - s0) : kWave);
+    wave_copy_rows<VB, NT>(src, cache + s0 * a.cache_stride, a.cache_stride, nrows, a.geom);
+  }
+  if (st) set_status(status, st);
+}
+
+__global__ void k_stage_finish(const int64_t* owner_off, KPart part, StageArgs a,
+                               const int64_t* prev_count, int32_t row_bytes,
+                               gg_stage_stats_t* stats, int32_t* status) {
+  const int64_t n = stage_n(owner_off, part.P, a);
+  for (int m = threadIdx.x; m < part.P; m += blockDim.x) {
+    int64_t lo = owner_off[m], hi = owner_off[m + 1];
+    lo = lo < n ? lo : n;
+    hi = hi < n ? hi : n;
+    const int64_t rows = hi > lo ? hi - lo : 0;
+    stats->rows[m] = rows;
+    stats->bytes[m] = rows * row_bytes;
+    stats->requests[m] = rows > 0 ? 1 : 0;
+  }
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    int64_t req = 0;
+    for (int m = 0; m < part.P; ++m) req += stats->requests[m];
+    stats->rows_total = n;
+    stats->requests_total = req;
+    stats->invalidated = prev_count ? prev_count[0] : 0;
+    if (owner_off[part.P] > n) set_status(status, GG_DEV_CAPACITY);
+  }
+}
+
+bool env_flag(const char* name, bool dflt) {
+  const char* v = getenv(name);
+  if (!v || !*v) return dflt;
+  return strcmp(v, "0") != 0;
+}
+
+template <int VB>
+void launch_stage_rows(bool nt, int grid, hipStream_t stream, const int32_t* bucket,
+                       const int64_t* owner_off, const KPart& kp, const KFeat& kf,
+                       const StageArgs& a, char* cache, int32_t* slot_of, int32_t* status) {
+  if (nt)
+    hipLaunchKernelGGL((k_stage_rows<VB, true>), dim3(grid), dim3(kBlock), 0, stream, bucket,
+                       owner_off, kp, kf, a, cache, slot_of, status);
+  else
+    hipLaunchKernelGGL((k_stage_rows<VB, false>), dim3(grid), dim3(kBlock), 0, stream, bucket,
+                       owner_off, kp, kf, a, cache, slot_of, status);
+}
+
+}  // namespace
+}  // namespace gg
+
+using namespace gg;
+
+extern "C" int gg_stage_bulk(const int32_t* bucket_ids_d, const int64_t* owner_off_d, int64_t cap,
+                             const gg_part_t* part, const gg_feat_t* feat, void* cache_d,
+                             int64_t cache_stride, int64_t cache_rows, int32_t* slot_of_d,
+                             const int32_t* prev_ids_d, const int64_t* prev_count_d,
+                             gg_stage_stats_t* stats_d, int32_t* status_d, hipStream_t stream) {
+  GG_REQUIRE(owner_off_d && slot_of_d && stats_d && status_d, "NULL argument");
+  GG_REQUIRE(cap >= 0 && cap < (1LL << 31) && cache_rows >= 0, "bad capacity");
+  GG_REQUIRE(cap == 0 || bucket_ids_d, "bucket ids are NULL");
+  GG_REQUIRE(cache_rows == 0 || cache_d, "cache is NULL");
+  GG_REQUIRE((prev_ids_d == nullptr) == (prev_count_d == nullptr),
+             "prev_ids and prev_count must both be given or both be NULL");
+  KPart kp;
+  int rc = pack_part(part, &kp);
+  if (rc != GG_OK) return rc;
+  KFeat kf;
+  rc = pack_feat(feat, part, &kf);
+  if (rc != GG_OK) return rc;
+  GG_REQUIRE(cache_stride >= kf.row_bytes && cache_stride % 4 == 0, "cache_stride %lld invalid",
+             (long long)cache_stride);
+  bool v16 = aligned16(cache_d) && cache_stride % 16 == 0;
+  for (int m = 0; m < kf.P; ++m)
+    if (kf.rows[m] > 0) v16 = v16 && aligned16(kf.shard[m]) && kf.stride[m] % 16 == 0;
+  StageArgs a;
+  a.cap = cap;
+  a.cache_rows = cache_rows;
+  a.cache_stride = cache_stride;
+  a.geom = copy_geom(kf.row_bytes, v16 ? 16 : 4);
+  static const bool nt = env_flag("GG_NT_STAGE", false);
+
+  hipLaunchKernelGGL(k_stage_prep, dim3(1), dim3(256), 0, stream, stats_d);
+  GG_LAUNCH_CHECK("k_stage_prep");
+  const int gridd = (int)std::min<int64_t>(std::max<int64_t>(cdiv(cap, kBlock), 1), 2048);
+  hipLaunchKernelGGL(k_stage_delta, dim3(gridd), dim3(kBlock), 0, stream, bucket_ids_d, owner_off_d,
+                     kp, a, slot_of_d, stats_d);
+  GG_LAUNCH_CHECK("k_stage_delta");
+  if (prev_ids_d) {
+    hipLaunchKernelGGL(k_slot_reset, dim3(2048), dim3(kBlock), 0, stream, prev_ids_d, prev_count_d,
+                       kp.N, slot_of_d);
+    GG_LAUNCH_CHECK("k_slot_reset");
+  }
+  const int64_t ntiles = cdiv(std::min(cap, cache_rows), kWave);
+  const int grid = (int)std::min<int64_t>(std::max<int64_t>(cdiv(ntiles, kBlock / kWave), 1), 16384);
+  if (v16)
+    launch_stage_rows<16>(nt, grid, stream, bucket_ids_d, owner_off_d, kp, kf, a, (char*)cache_d,
+                          slot_of_d, status_d);
+  else
+    launch_stage_rows<4>(nt, grid, stream, bucket_ids_d, owner_off_d, kp, kf, a, (char*)cache_d,
+                         slot_of_d, status_d);
+  GG_LAUNCH_CHECK("k_stage_rows");
+  hipLaunchKernelGGL(k_stage_finish, dim3(1), dim3(64), 0, stream, owner_off_d, kp, a, prev_count_d,
+                     kf.row_bytes, stats_d, status_d);
+  GG_LAUNCH_CHECK("k_stage_finish");
+  return GG_OK;
+}

@@ -1,0 +1,276 @@
+"""ctypes binding of libgg (include/gg.h): argument marshalling only.
+
+Every function keeps the C name and argument order.  Device buffers are
+torch tensors on a ROCm device (or pinned host tensors for shards kept in
+host memory); they are passed by data pointer, and the stream defaults to
+torch's current stream.  Every step of the path runs in libgg's kernels;
+if the library is missing this module raises on import.
+"""
+from __future__ import annotations
+
+import ctypes as C
+import os
+
+import numpy as np
+
+MAX_PARTS = 64
+MAX_LAYERS = 4
+MAX_W = 64
+MAX_FANOUT = 32
+PART_MOD = 0
+PART_RANGE = 1
+
+GG_OK = 0
+GG_ERR_ARG = 1
+GG_ERR_CAPACITY = 2
+GG_ERR_HIP = 3
+GG_ERR_UNSUPPORTED = 4
+
+DEV_CAPACITY = 1
+DEV_BAD_ID = 2
+DEV_BAD_ROW = 4
+DEV_BAD_DEGREE = 8
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libgg.so")
+
+
+class gg_csr_t(C.Structure):
+    _fields_ = [("num_nodes", C.c_int64), ("num_edges", C.c_int64), ("row_ptr", C.c_void_p),
+                ("row_ptr_bits", C.c_int32), ("pad_", C.c_int32), ("col_idx", C.c_void_p)]
+
+
+class gg_part_t(C.Structure):
+    _fields_ = [("num_parts", C.c_int32), ("kind", C.c_int32), ("local_owner", C.c_int32),
+                ("pad_", C.c_int32), ("num_nodes", C.c_int64),
+                ("range_start", C.c_int64 * (MAX_PARTS + 1))]
+
+
+class gg_feat_t(C.Structure):
+    _fields_ = [("row_bytes", C.c_int32), ("num_parts", C.c_int32),
+                ("shard", C.c_void_p * MAX_PARTS), ("row_stride", C.c_int64 * MAX_PARTS),
+                ("shard_rows", C.c_int64 * MAX_PARTS)]
+
+
+class gg_wsample_t(C.Structure):
+    _fields_ = [("frontier_ids", C.c_void_p), ("frontier_cap", C.c_int64),
+                ("frontier_off", C.c_void_p), ("nbr_ids", C.c_void_p), ("nbr_cap", C.c_int64),
+                ("nbr_off", C.c_void_p), ("frontier_bits", C.c_void_p), ("need", C.c_void_p)]
+
+
+class gg_stage_stats_t(C.Structure):
+    _fields_ = [("rows_total", C.c_int64), ("requests_total", C.c_int64),
+                ("invalidated", C.c_int64), ("pad_", C.c_int64),
+                ("requests", C.c_int64 * MAX_PARTS), ("rows", C.c_int64 * MAX_PARTS),
+                ("bytes", C.c_int64 * MAX_PARTS), ("delta_rows", C.c_int64 * MAX_PARTS)]
+
+
+class gg_gather_stats_t(C.Structure):
+    _fields_ = [("rows", C.c_int64), ("local", C.c_int64), ("hits", C.c_int64),
+                ("misses", C.c_int64), ("miss_requests", C.c_int64 * MAX_PARTS),
+                ("miss_rows", C.c_int64 * MAX_PARTS)]
+
+
+STAGE_STATS_BYTES = C.sizeof(gg_stage_stats_t)
+GATHER_STATS_BYTES = C.sizeof(gg_gather_stats_t)
+
+# Every function include/gg.h declares, with its ctypes signature.
+_P, _I32, _I64, _U64, _SZ = C.c_void_p, C.c_int32, C.c_int64, C.c_uint64, C.c_size_t
+SIGNATURES = {
+    "gg_bits_words": (_I64, [_I64]),
+    "gg_sample_caps": (C.c_int, [_I64, _I32, _I64, _P, _I32, _P, _P]),
+    "gg_ws_sample": (_SZ, [_I64, _I32]),
+    "gg_ws_hotset": (_SZ, [_I64, _I32]),
+    "gg_ws_bucket": (_SZ, [_I64, _I32]),
+    "gg_ws_gather": (_SZ, [_I64, _I32]),
+    "gg_sample_window": (C.c_int, [_P, _P, _P, _I32, _P, _I32, _U64, _I32, _I64, _P, _P, _P, _SZ,
+                                   _P]),
+    "gg_build_hotset": (C.c_int, [_P, _I32, _P, _I64, _P, _P, _I64, _P, _P, _P, _SZ, _P]),
+    "gg_bucket_by_owner": (C.c_int, [_P, _P, _I64, _P, _P, _P, _P, _P, _SZ, _P]),
+    "gg_stage_bulk": (C.c_int, [_P, _P, _I64, _P, _P, _P, _I64, _I64, _P, _P, _P, _P, _P, _P]),
+    "gg_gather_batch": (C.c_int, [_P, _P, _I64, _P, _P, _P, _I64, _I64, _P, _P, _I64, _P, _P, _P,
+                                  _SZ, _P]),
+    "gg_status_string": (C.c_char_p, [_I32]),
+    "gg_last_error": (C.c_char_p, []),
+    "gg_version": (C.c_int, []),
+}
+
+if not os.path.exists(LIB_PATH):
+    raise ImportError(f"libgg is not built ({LIB_PATH}); run __graft_entry__.build()")
+lib = C.CDLL(LIB_PATH)
+for _name, (_res, _args) in SIGNATURES.items():
+    _f = getattr(lib, _name)
+    _f.restype = _res
+    _f.argtypes = _args
+
+
+class GGError(RuntimeError):
+    pass
+
+
+def check(rc, what):
+    if rc != GG_OK:
+        msg = lib.gg_last_error().decode()
+        raise GGError(f"{what}: {lib.gg_status_string(rc).decode()} ({msg})")
+    return rc
+
+
+def _ptr(t):
+    return None if t is None else t.data_ptr()
+
+
+def _stream(stream):
+    if stream is None:
+        import torch
+        return torch.cuda.current_stream().cuda_stream
+    return stream.cuda_stream if hasattr(stream, "cuda_stream") else stream
+
+
+def make_csr(row_ptr, col_idx, num_nodes=None):
+    g = gg_csr_t()
+    g.num_nodes = row_ptr.numel() - 1 if num_nodes is None else num_nodes
+    g.num_edges = col_idx.numel()
+    g.row_ptr = row_ptr.data_ptr()
+    g.row_ptr_bits = 64 if row_ptr.element_size() == 8 else 32
+    g.col_idx = col_idx.data_ptr()
+    return g
+
+
+def make_part(num_parts, kind, local_owner, num_nodes, range_start=None):
+    p = gg_part_t()
+    p.num_parts = num_parts
+    p.kind = kind
+    p.local_owner = local_owner
+    p.num_nodes = num_nodes
+    if range_start is not None:
+        for i, v in enumerate(range_start):
+            p.range_start[i] = int(v)
+    return p
+
+
+def make_feat(row_bytes, shards, strides, rows):
+    """shards: tensors (device, or pinned host used through its device address)."""
+    f = gg_feat_t()
+    f.row_bytes = row_bytes
+    f.num_parts = len(shards)
+    for m, (s, st, r) in enumerate(zip(shards, strides, rows)):
+        f.shard[m] = s.data_ptr() if (s is not None and r > 0) else None
+        f.row_stride[m] = st
+        f.shard_rows[m] = r
+    return f
+
+
+def make_wsample(frontier_ids, frontier_off, nbr_ids, nbr_off, frontier_bits, need):
+    w = gg_wsample_t()
+    w.frontier_ids = frontier_ids.data_ptr()
+    w.frontier_cap = frontier_ids.numel()
+    w.frontier_off = frontier_off.data_ptr()
+    w.nbr_ids = nbr_ids.data_ptr()
+    w.nbr_cap = nbr_ids.numel()
+    w.nbr_off = nbr_off.data_ptr()
+    w.frontier_bits = frontier_bits.data_ptr()
+    w.need = need.data_ptr()
+    return w
+
+
+def gg_bits_words(num_nodes):
+    return int(lib.gg_bits_words(num_nodes))
+
+
+def gg_sample_caps(num_nodes, W, max_batch, fanout):
+    fan = np.ascontiguousarray(fanout, dtype=np.int32)
+    fc, nc = C.c_int64(0), C.c_int64(0)
+    check(lib.gg_sample_caps(num_nodes, W, max_batch, fan.ctypes.data, len(fan), C.byref(fc),
+                             C.byref(nc)), "gg_sample_caps")
+    return fc.value, nc.value
+
+
+def gg_ws_sample(num_nodes, W):
+    return int(lib.gg_ws_sample(num_nodes, W))
+
+
+def gg_ws_hotset(num_nodes, W):
+    return int(lib.gg_ws_hotset(num_nodes, W))
+
+
+def gg_ws_bucket(cap, num_parts):
+    return int(lib.gg_ws_bucket(cap, num_parts))
+
+
+def gg_ws_gather(n_cap, num_parts):
+    return int(lib.gg_ws_gather(n_cap, num_parts))
+
+
+def gg_sample_window(csr, seeds, seed_off, W, fanout, L, rng_seed, epoch, batch0, out, status, ws,
+                     stream=None):
+    so = np.ascontiguousarray(seed_off, dtype=np.int64)
+    fan = np.ascontiguousarray(fanout, dtype=np.int32)
+    return check(lib.gg_sample_window(C.byref(csr), _ptr(seeds), so.ctypes.data, W,
+                                      fan.ctypes.data, L, C.c_uint64(rng_seed), epoch, batch0,
+                                      C.byref(out), _ptr(status), _ptr(ws), ws.numel(),
+                                      _stream(stream)), "gg_sample_window")
+
+
+def gg_build_hotset(frontier_bits, W, part, n_hot, hot_ids, hot_freq, cap, hot_count, status, ws,
+                    stream=None):
+    return check(lib.gg_build_hotset(_ptr(frontier_bits), W, C.byref(part), n_hot, _ptr(hot_ids),
+                                     _ptr(hot_freq), cap, _ptr(hot_count), _ptr(status), _ptr(ws),
+                                     ws.numel(), _stream(stream)), "gg_build_hotset")
+
+
+def gg_bucket_by_owner(hot_ids, hot_count, cap, part, bucket_ids, owner_off, status, ws,
+                       stream=None):
+    return check(lib.gg_bucket_by_owner(_ptr(hot_ids), _ptr(hot_count), cap, C.byref(part),
+                                        _ptr(bucket_ids), _ptr(owner_off), _ptr(status), _ptr(ws),
+                                        ws.numel(), _stream(stream)), "gg_bucket_by_owner")
+
+
+def gg_stage_bulk(bucket_ids, owner_off, cap, part, feat, cache, cache_stride, cache_rows, slot_of,
+                  prev_ids, prev_count, stats, status, stream=None):
+    return check(lib.gg_stage_bulk(_ptr(bucket_ids), _ptr(owner_off), cap, C.byref(part),
+                                   C.byref(feat), _ptr(cache), cache_stride, cache_rows,
+                                   _ptr(slot_of), _ptr(prev_ids), _ptr(prev_count), _ptr(stats),
+                                   _ptr(status), _stream(stream)), "gg_stage_bulk")
+
+
+def gg_gather_batch(in_ids, bounds_ptr, n_cap, part, feat, cache, cache_stride, cache_rows,
+                    slot_of, out, out_stride, stats_ptr, status, ws, stream=None):
+    """bounds_ptr and stats_ptr are raw device addresses (e.g. an offset into
+    frontier_off or into a stats array)."""
+    return check(lib.gg_gather_batch(_ptr(in_ids), bounds_ptr, n_cap, C.byref(part),
+                                     C.byref(feat), _ptr(cache), cache_stride, cache_rows,
+                                     _ptr(slot_of), _ptr(out), out_stride, stats_ptr,
+                                     _ptr(status), _ptr(ws), ws.numel(), _stream(stream)),
+                 "gg_gather_batch")
+
+
+def gg_status_string(code):
+    return lib.gg_status_string(code).decode()
+
+
+def gg_last_error():
+    return lib.gg_last_error().decode()
+
+
+def gg_version():
+    return int(lib.gg_version())
+
+
+def stage_stats_from_bytes(buf, P):
+    st = gg_stage_stats_t.from_buffer_copy(bytes(buf))
+    return _stats_dict(st, P)
+
+
+def gather_stats_from_bytes(buf, P):
+    st = gg_gather_stats_t.from_buffer_copy(bytes(buf))
+    return _stats_dict(st, P)
+
+
+def _stats_dict(st, P):
+    d = {}
+    for name, _ in st._fields_:
+        if name == "pad_":
+            continue
+        v = getattr(st, name)
+        d[name] = [int(x) for x in v][:P] if hasattr(v, "__len__") else int(v)
+    return d

@@ -1,0 +1,123 @@
+"""Shared set-up for the GPU parity tests: the same seeded inputs go to the
+HIP path (through the C ABI) and to the CPU oracle; results are compared
+byte for byte."""
+from __future__ import annotations
+
+import numpy as np
+import torch
+
+import synth
+from oracle import ggref
+from paper_2606_02916_amd import FetchPipeline
+
+
+def log(msg):
+    print(msg, flush=True)
+
+
+class World:
+    """One workload instance on the GPU and its oracle counterpart."""
+
+    def __init__(self, inst, W=None, n_hot=-1, local_owner=None, fanout=None, batch=None,
+                 device="cuda:0", shards=None, row_bytes=None, stride=None):
+        wl = inst.wl
+        self.inst = inst
+        self.wl = wl
+        self.shards = inst.shards if shards is None else shards
+        self.row_bytes = wl.row_bytes if row_bytes is None else row_bytes
+        self.stride = wl.row_stride if stride is None else stride
+        self.W = W or wl.W
+        self.n_hot = n_hot
+        self.local = wl.local_owner if local_owner is None else local_owner
+        self.fanout = tuple(fanout or wl.fanout)
+        self.batch = batch or wl.batch_size
+        self.dev = torch.device(device)
+        self.P = wl.num_parts
+        self.rs = inst.range_start
+        self.row_ptr_d = torch.from_numpy(inst.row_ptr).to(self.dev)
+        self.col_idx_d = torch.from_numpy(inst.col_idx).to(self.dev)
+        self.shards_d = [torch.from_numpy(s).to(self.dev) for s in self.shards]
+        rows = [s.shape[0] for s in self.shards]
+        self.pipe = FetchPipeline(self.row_ptr_d, self.col_idx_d, self.P, wl.part_kind, self.local,
+                                  self.rs, self.shards_d, rows, self.row_bytes, self.stride,
+                                  self.W, self.fanout, self.batch, n_hot=n_hot, device=self.dev)
+        self.part_ref = ggref.make_part(self.P, wl.part_kind, self.local, wl.num_nodes, self.rs)
+        self.feat_ref = ggref.make_feat(self.row_bytes, self.shards, [self.stride] * self.P)
+        self.cache_ref = np.zeros((self.pipe.hot_cap, self.stride), dtype=np.uint8)
+        self.slot_ref = np.full(wl.num_nodes, -1, dtype=np.int32)
+        self.prev_ref = None
+
+    def window_inputs(self, k, W=None):
+        W = W or self.W
+        b0, b1 = synth.window_batches(self.inst.batch_off, W, k)
+        boff = self.inst.batch_off
+        so = boff[b0:b1 + 1] - boff[b0]
+        seeds = self.inst.seeds[boff[b0]:boff[b1]]
+        return seeds, so, b0
+
+    def run_and_compare(self, k, epoch=0, rng_seed=0, check_outputs=True, seeds=None, so=None,
+                        b0=None):
+        """Runs window k on both sides and asserts every intermediate equal."""
+        if seeds is None:
+            seeds, so, b0 = self.window_inputs(k)
+        pipe, rb, st = self.pipe, self.row_bytes, self.stride
+        L = len(self.fanout)
+        seeds_d = torch.from_numpy(np.ascontiguousarray(seeds, dtype=np.int32)).to(self.dev)
+        cur = pipe.k & 1
+        Wk = pipe.sample(seeds_d, so, b0, epoch, rng_seed)
+        pipe.hotset(Wk, cur)
+        pipe.bucket(cur)
+        pipe.stage(cur)
+        torch.cuda.synchronize()
+        assert pipe.read_status() == 0, pipe.read_status()
+        # sampling
+        fids, foff, nids, noff = ggref.sample_window(self.inst.row_ptr, self.inst.col_idx, seeds,
+                                                     so, self.fanout, rng_seed, epoch, b0)
+        g_fids, g_foff, g_nids, g_noff = pipe.sample_outputs(Wk)
+        assert np.array_equal(g_foff, foff)
+        assert np.array_equal(g_fids, fids)
+        assert np.array_equal(g_noff, noff)
+        assert np.array_equal(g_nids, nids)
+        # the bit sets hold exactly N_b
+        bits = pipe.frontier_bits.view(torch.int32)[:Wk * pipe.wpb].cpu().numpy().view(np.uint32)
+        for b in range(Wk):
+            ids = fids[foff[L * Wk + b]:foff[L * Wk + b + 1]]
+            row = bits[b * pipe.wpb:(b + 1) * pipe.wpb]
+            got = np.nonzero(np.unpackbits(row.view(np.uint8), bitorder="little"))[0]
+            assert np.array_equal(got, ids)
+        # hot set and buckets
+        hot, freq = ggref.build_hotset(fids, foff, Wk, L, self.part_ref, self.n_hot)
+        bucket, owner_off = ggref.bucket_by_owner(hot, self.part_ref)
+        g_hot, g_freq, g_cnt, g_bucket, g_owner_off = pipe.hot_outputs(cur)
+        assert int(g_cnt[0]) == len(hot) == int(g_cnt[1])
+        assert np.array_equal(g_hot, hot)
+        assert np.array_equal(g_freq, freq)
+        assert np.array_equal(g_bucket, bucket)
+        assert np.array_equal(g_owner_off, owner_off)
+        # stage
+        sst = ggref.stage_bulk(bucket, owner_off, self.part_ref, self.feat_ref, self.cache_ref,
+                               st, self.slot_ref, self.prev_ref)
+        self.prev_ref = bucket.copy()
+        assert pipe.stage_stats_dict() == sst
+        assert np.array_equal(pipe.slot_of.cpu().numpy(), self.slot_ref)
+        H = len(hot)
+        g_cache = pipe.cache[:H].cpu().numpy()
+        assert np.array_equal(g_cache[:, :rb], self.cache_ref[:H, :rb])
+        # gathers, one batch at a time
+        for b in range(Wk):
+            out = torch.empty((pipe.out_cap, st), dtype=torch.uint8,
+                              device=self.dev)
+            pipe.gather(Wk, b, out)
+            torch.cuda.synchronize()
+            assert pipe.read_status() == 0
+            s = L * Wk + b
+            ids = fids[foff[s]:foff[s + 1]]
+            ref = np.zeros((len(ids), st), dtype=np.uint8)
+            gs = ggref.gather_batch(ids, self.part_ref, self.feat_ref, self.cache_ref,
+                                    st, self.slot_ref, ref, st)
+            assert pipe.gather_stats_dict(b) == gs
+            if check_outputs:
+                got = out[:len(ids)].cpu().numpy()
+                assert np.array_equal(got[:, :rb], ref[:, :rb]), f"batch {b}"
+        pipe.k += 1
+        return dict(Wk=Wk, fids=fids, foff=foff, hot=hot, stage=sst)

@@ -1,0 +1,144 @@
+"""The C ABI without a GPU: libgg loads, exports every function include/gg.h
+declares, the ctypes structures match the header's layout, and host-side
+argument checks reject bad calls before anything is enqueued."""
+import ctypes as C
+import os
+import re
+import subprocess
+import tempfile
+
+import numpy as np
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "gg.h")
+
+
+@pytest.fixture(scope="module")
+def gg():
+    lib = os.path.join(ROOT, "paper_2606_02916_amd", "libgg.so")
+    if not os.path.exists(lib):
+        from paper_2606_02916_amd import build
+        build.build()
+    from paper_2606_02916_amd import gg as mod
+    return mod
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(gg_[a-z_]+)\s*\(", text)))
+
+
+def test_every_declared_function_is_exported_and_bound(gg):
+    names = declared_functions()
+    assert len(names) >= 14
+    out = subprocess.run(["nm", "-D", "--defined-only", gg.LIB_PATH], capture_output=True,
+                         text=True, check=True).stdout
+    exported = set(re.findall(r" T (gg_\w+)", out))
+    for n in names:
+        assert n in exported, n
+        assert n in gg.SIGNATURES, n
+    assert set(gg.SIGNATURES) == set(names)
+
+
+LAYOUT_PROBE = r"""
+#include <stddef.h>
+#include <stdio.h>
+#include "gg.h"
+#define F(T, f) printf(#T " " #f " %zu\n", offsetof(T, f));
+#define S(T) printf(#T " sizeof %zu\n", sizeof(T));
+int main() {
+  S(gg_csr_t) F(gg_csr_t, num_edges) F(gg_csr_t, row_ptr) F(gg_csr_t, row_ptr_bits) F(gg_csr_t, col_idx)
+  S(gg_part_t) F(gg_part_t, local_owner) F(gg_part_t, num_nodes) F(gg_part_t, range_start)
+  S(gg_feat_t) F(gg_feat_t, shard) F(gg_feat_t, row_stride) F(gg_feat_t, shard_rows)
+  S(gg_wsample_t) F(gg_wsample_t, frontier_cap) F(gg_wsample_t, nbr_ids) F(gg_wsample_t, nbr_off)
+  F(gg_wsample_t, frontier_bits) F(gg_wsample_t, need)
+  S(gg_stage_stats_t) F(gg_stage_stats_t, invalidated) F(gg_stage_stats_t, requests)
+  F(gg_stage_stats_t, rows) F(gg_stage_stats_t, bytes) F(gg_stage_stats_t, delta_rows)
+  S(gg_gather_stats_t) F(gg_gather_stats_t, misses) F(gg_gather_stats_t, miss_requests)
+  F(gg_gather_stats_t, miss_rows)
+  return 0;
+}
+"""
+
+
+def test_struct_layouts_match_the_header(gg):
+    d = tempfile.mkdtemp(prefix="ggabi_")
+    src = os.path.join(d, "probe.cpp")
+    with open(src, "w") as f:
+        f.write(LAYOUT_PROBE)
+    exe = os.path.join(d, "probe")
+    subprocess.run(["g++", "-D__HIP_PLATFORM_AMD__", "-I/opt/rocm/include",
+                    "-I" + os.path.join(ROOT, "include"), src, "-o", exe], check=True)
+    lines = subprocess.run([exe], capture_output=True, text=True, check=True).stdout.split("\n")
+    for line in filter(None, lines):
+        tname, field, val = line.split()
+        T = getattr(gg, tname)
+        if field == "sizeof":
+            assert C.sizeof(T) == int(val), line
+        else:
+            assert getattr(T, field).offset == int(val), line
+
+
+def test_host_helpers(gg):
+    assert gg.gg_version() == 1
+    assert gg.gg_status_string(gg.GG_ERR_ARG) == "invalid argument"
+    for n in (1, 31, 32, 33, 65536, 65537, 10**7):
+        w = gg.gg_bits_words(n)
+        assert w % 2048 == 0 and w * 32 >= n and (w - 2048) * 32 < max(n, 1)
+    # worst-case capacities: sum over levels of min(N, B * prod(k_i + 1))
+    fc, nc = gg.gg_sample_caps(2_450_000, 16, 1024, [15, 10, 5])
+    lev = [1024, 1024 * 16, 1024 * 16 * 11, min(2_450_000, 1024 * 16 * 11 * 6)]
+    assert fc == 16 * sum(lev)
+    assert nc == 16 * (lev[0] * 15 + lev[1] * 10 + lev[2] * 5)
+    fc, nc = gg.gg_sample_caps(1000, 2, 600, [3])
+    assert fc == 2 * (600 + 1000) and nc == 2 * 600 * 3
+    for f in (gg.gg_ws_sample, gg.gg_ws_hotset):
+        assert f(10_000, 4) > 0 and f(10_000, 4) % 256 == 0
+    assert gg.gg_ws_bucket(0, 4) > 0 and gg.gg_ws_gather(0, 4) > 0
+
+
+class _FakeTensor:
+    """Stands in for a device tensor in calls that must be rejected before
+    any device work: only its address and size are read."""
+
+    def __init__(self, addr, n=1):
+        self.addr, self.n = addr, n
+
+    def data_ptr(self):
+        return self.addr
+
+    def numel(self):
+        return self.n
+
+    def element_size(self):
+        return 8
+
+
+def test_bad_arguments_are_rejected_on_the_host(gg):
+    t = _FakeTensor(1 << 20, 1 << 20)
+    csr = gg.make_csr(_FakeTensor(4096, 101), _FakeTensor(8192, 500), num_nodes=100)
+    ws = gg.make_wsample(t, t, t, t, t, t)
+    for W, fan, off in [(0, [2], [0]), (65, [2], [0] * 66), (2, [0], [0, 1, 2]),
+                        (2, [33], [0, 1, 2]), (2, [2], [0, 3, 2]), (2, [2], [1, 2, 3])]:
+        with pytest.raises(gg.GGError) as e:
+            gg.gg_sample_window(csr, t, np.array(off), W, fan, len(fan), 0, 0, 0, ws, t, t,
+                                stream=0)
+        assert "invalid argument" in str(e.value)
+    part = gg.make_part(0, gg.PART_MOD, 0, 100)
+    with pytest.raises(gg.GGError):
+        gg.gg_build_hotset(t, 4, part, -1, t, None, 10, t, t, t, stream=0)
+    part = gg.make_part(4, gg.PART_RANGE, 0, 100, [0, 10, 20, 30, 99])  # does not end at N
+    with pytest.raises(gg.GGError):
+        gg.gg_bucket_by_owner(t, t, 10, part, t, t, t, t, stream=0)
+    part = gg.make_part(4, gg.PART_MOD, 4, 100)                          # local owner >= P
+    feat = gg.make_feat(256, [t] * 4, [256] * 4, [25] * 4)
+    with pytest.raises(gg.GGError):
+        gg.gg_stage_bulk(t, t, 10, part, feat, t, 256, 10, t, None, None, t, t, stream=0)
+    part = gg.make_part(4, gg.PART_MOD, 0, 100)
+    feat = gg.make_feat(250, [t] * 4, [256] * 4, [25] * 4)              # row_bytes % 4 != 0
+    with pytest.raises(gg.GGError):
+        gg.gg_gather_batch(t, t.data_ptr(), 10, part, feat, t, 256, 10, t, t, 256,
+                           t.data_ptr(), t, t, stream=0)
+    assert "row_bytes" in gg.gg_last_error()

@@ -1,0 +1,164 @@
+"""GPU parity: the HIP path through the C ABI against the CPU oracle, byte
+for byte (the path moves ids and opaque feature bytes only, so the
+tolerance is exact equality)."""
+import numpy as np
+import pytest
+
+import synth
+from tests import helpers
+
+torch = pytest.importorskip("torch")
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    from tests import gpu_util  # noqa: F401  (loads libgg)
+    yield
+
+
+def world(*a, **k):
+    from tests.gpu_util import World
+    return World(*a, **k)
+
+
+def log(m):
+    print(m, flush=True)
+
+
+def test_tiny_window_matches_oracle():
+    log("tiny: mod-4 owners, fanout [10,5], W=4")
+    w = world(synth.instance("tiny"))
+    w.run_and_compare(0)
+
+
+@pytest.mark.parametrize("n_hot", [0, 1, 100, 2000, 10**7])
+def test_tiny_hot_budget_and_miss_path(n_hot):
+    log(f"tiny: n_hot={n_hot}")
+    w = world(synth.instance("tiny"), n_hot=n_hot)
+    w.run_and_compare(0)
+
+
+def test_tiny_all_owners_remote():
+    log("tiny: local_owner=-1")
+    w = world(synth.instance("tiny"), local_owner=-1)
+    w.run_and_compare(0)
+
+
+def test_small_consecutive_windows_restage_and_invalidate():
+    log("small: range owners, 3 consecutive windows, W=4")
+    w = world(synth.instance("small"))
+    for k in range(3):
+        r = w.run_and_compare(k)
+        assert r["stage"]["invalidated"] == (0 if k == 0 else len(prev))
+        prev = r["hot"]
+
+
+@pytest.mark.parametrize("W", [1, 3, 7])
+def test_small_window_sizes(W):
+    log(f"small: W={W}")
+    w = world(synth.instance("small"), W=W)
+    w.run_and_compare(0)
+    w.run_and_compare(1)
+
+
+def test_small_budget_misses_across_windows():
+    log("small: n_hot=3000 over two windows")
+    w = world(synth.instance("small"), n_hot=3000)
+    w.run_and_compare(0)
+    w.run_and_compare(1)
+
+
+def test_ragged_and_empty_batches():
+    log("tiny: ragged batch sizes with an empty batch")
+    inst = synth.instance("tiny")
+    w = world(inst, W=5, batch=1000)
+    sizes = [1, 0, 65, 257, 1000]
+    seeds = inst.seeds[:sum(sizes)]
+    so = np.concatenate([[0], np.cumsum(sizes)]).astype(np.int64)
+    w.run_and_compare(0, seeds=seeds, so=so, b0=3)
+
+
+def test_fanout_above_every_degree_is_the_bfs_ball():
+    log("hand graph: fanout above max degree")
+    rng = np.random.default_rng(3)
+    row_ptr, col_idx = helpers.random_graph(3000, 20000, rng)
+    maxdeg = int(np.diff(row_ptr).max())
+    assert maxdeg < 32
+    wl = synth.Workload("hand", 3000, col_idx.shape[0], False, 64, synth.PART_MOD, 4, 1, 16, "fp32",
+                        "normal", (maxdeg + 1, maxdeg + 1), 40, 2, "perm_all", n_windows=1)
+    inst = synth.Instance(wl, row_ptr, col_idx, *synth.seed_batches(wl),
+                          [synth.shard_features(wl, m) for m in range(4)], None)
+    w = world(inst)
+    r = w.run_and_compare(0)
+    L, W = 2, 2
+    for b in range(W):
+        s = inst.batch_off
+        want = helpers.bfs_ball(row_ptr, col_idx, inst.seeds[s[b]:s[b + 1]], L)
+        got = r["fids"][r["foff"][L * W + b]:r["foff"][L * W + b + 1]].tolist()
+        assert got == want
+
+
+def test_unaligned_rows_use_the_word_path():
+    log("tiny: 44-byte rows at a 44-byte stride, 4-byte copy path")
+    inst = synth.instance("tiny")
+    rng = np.random.default_rng(5)
+    shards = [rng.integers(0, 256, size=(s.shape[0], 44), dtype=np.uint8) for s in inst.shards]
+    w = world(inst, shards=shards, row_bytes=44, stride=44)
+    w.run_and_compare(0)
+
+
+def test_row_with_tail_words():
+    log("tiny: 1 KB + 12 byte rows at a 16-byte-aligned stride (vector path with tail)")
+    inst = synth.instance("tiny")
+    rng = np.random.default_rng(6)
+    shards = [rng.integers(0, 256, size=(s.shape[0], 1040), dtype=np.uint8) for s in inst.shards]
+    w = world(inst, shards=shards, row_bytes=1036, stride=1040)
+    w.run_and_compare(0)
+
+
+def test_repeat_runs_are_identical():
+    log("small: determinism across two pipelines")
+    inst = synth.instance("small")
+    a = world(inst)
+    b = world(inst)
+    ra = a.run_and_compare(0)
+    rb = b.run_and_compare(0)
+    assert np.array_equal(ra["fids"], rb["fids"])
+
+
+def test_capacity_overflow_is_flagged_and_clamped():
+    log("tiny: frontier capacity too small -> status bit, no out-of-bounds writes")
+    import torch as T
+    from paper_2606_02916_amd import gg
+    w = world(synth.instance("tiny"))
+    p = w.pipe
+    guard = 4096
+    small = T.full((1000 + guard,), 0x7EADBEEF, dtype=T.int32, device=w.dev)
+    ws = gg.make_wsample(small[:1000], p.frontier_off, p.nbr_ids, p.nbr_off, p.frontier_bits,
+                         p.need)
+    seeds, so, b0 = w.window_inputs(0)
+    sd = T.from_numpy(seeds).to(w.dev)
+    gg.gg_sample_window(p.csr, sd, so, len(so) - 1, list(w.fanout), len(w.fanout), 0, 0, b0, ws,
+                        p.status, p.ws)
+    T.cuda.synchronize()
+    assert p.read_status() & gg.DEV_CAPACITY
+    assert int(p.need[0].item()) > 1000
+    assert bool((small[1000:] == 0x7EADBEEF).all())
+    assert int(p.frontier_off.max().item()) <= 1000
+
+
+@pytest.mark.timeout(900)
+def test_large_sparse_full_window_matches_oracle():
+    log("large_sparse: 2.45M nodes, 62M edges, fanout [15,10,5], batch 1024, W=16, window 0")
+    w = world(synth.instance("large_sparse"))
+    w.run_and_compare(0)
+
+
+@pytest.mark.timeout(900)
+def test_dense_mid_full_window_matches_oracle():
+    log("dense_mid: 233K nodes, 114M edges, fp32x602 (stride 2416), fanout [25,10], W=8, window 0")
+    w = world(synth.instance("dense_mid"))
+    w.run_and_compare(0)
