@@ -54,6 +54,8 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=10.0,
                     help="minimum oracle time for the CPU baseline sample")
+    ap.add_argument("--per-batch", action="store_true",
+                    help="one gather launch per batch instead of one per window")
     args = ap.parse_args()
 
     world = int(os.environ.get("WORLD_SIZE", "1"))
@@ -96,15 +98,17 @@ def main():
     # per-batch local/remote counts for the gather's algorithmic bytes.
     rb = wl.row_bytes
     rows_w, gbytes_w, hot_w, sbytes_w, req_w = [], [], [], [], []
+    pb = args.per_batch
     for k, (s, so, b0) in enumerate(wins):
-        Wk = pipe.window(s, so, b0)
+        Wk = pipe.window(s, so, b0, per_batch=pb)
         torch.cuda.synchronize()
         st = pipe.read_status()
         if st != 0:
             raise RuntimeError(f"device status {st} in window {k}")
         g = [pipe.gather_stats_dict(b) for b in range(Wk)]
         rows_w.append(sum(x["rows"] for x in g))
-        gbytes_w.append([x["rows"] * (2 * rb + 4) + (x["hits"] + x["misses"]) * 4 for x in g])
+        gb = [x["rows"] * (2 * rb + 4) + (x["hits"] + x["misses"]) * 4 for x in g]
+        gbytes_w.append(gb if pb else [sum(gb)])
         ss = pipe.stage_stats_dict()
         hot_w.append(ss["rows_total"])
         sbytes_w.append(ss["rows_total"] * (2 * rb + 8) + ss["invalidated"] * 4)
@@ -113,19 +117,19 @@ def main():
 
     for i in range(args.warmup):
         s, so, b0 = wins[i % nwin]
-        pipe.window(s, so, b0)
+        pipe.window(s, so, b0, per_batch=pb)
     torch.cuda.synchronize()
 
     K = args.steps
     mk = lambda: torch.cuda.Event(enable_timing=True)  # noqa: E731
     evs = [[mk() for _ in range(6)] for _ in range(K)]
-    gevs = [[(mk(), mk()) for _ in range(W)] for _ in range(K)]
+    gevs = [[(mk(), mk()) for _ in range(W if pb else 1)] for _ in range(K)]
     order = [(args.warmup + i) % nwin for i in range(K)]
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     for i, k in enumerate(order):
         s, so, b0 = wins[k]
-        pipe.window(s, so, b0, events=evs[i], gather_events=gevs[i])
+        pipe.window(s, so, b0, events=evs[i], gather_events=gevs[i], per_batch=pb)
     torch.cuda.synchronize()
     t1 = time.perf_counter()
     if pipe.read_status() != 0:
@@ -143,7 +147,7 @@ def main():
             stage_ms[name].append(e[a].elapsed_time(e[b]))
         st_ms += e[3].elapsed_time(e[4])
         st_bytes += sbytes_w[k]
-        for b in range(len(wins[k][1]) - 1):
+        for b in range(len(gbytes_w[k])):
             g_ms += gevs[i][b][0].elapsed_time(gevs[i][b][1])
             g_bytes += gbytes_w[k][b]
             n_launch += 1
@@ -173,7 +177,8 @@ def main():
         "config": {"workload": args.config, "nodes": wl.num_nodes, "edges": wl.num_edges,
                    "features": f"{wl.feat_dtype}x{wl.feat_dim}", "row_bytes": rb,
                    "fanout": list(wl.fanout), "batch": wl.batch_size, "W": W,
-                   "partitions": P, "local_owner": wl.local_owner, "windows_per_epoch": nwin},
+                   "partitions": P, "local_owner": wl.local_owner, "windows_per_epoch": nwin,
+                   "gather_launch": "per batch" if pb else "per window"},
         "roofline": {"bound": "hbm", "kernel": "gg_gather_batch",
                      "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
                      "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": None,

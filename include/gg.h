@@ -166,7 +166,7 @@ int gg_sample_caps(int64_t num_nodes, int32_t W, int64_t max_batch, const int32_
 size_t gg_ws_sample(int64_t num_nodes, int32_t W);
 size_t gg_ws_hotset(int64_t num_nodes, int32_t W);
 size_t gg_ws_bucket(int64_t cap, int32_t num_parts);
-size_t gg_ws_gather(int64_t n_cap, int32_t num_parts);
+size_t gg_ws_gather(int64_t n_cap, int32_t nseg, int32_t num_parts);
 
 /* Neighbour sampling of one window (Sec. IV-A step 2: one epoch of
  * deterministic sampling under fixed seeds fixes every later access).
@@ -223,21 +223,28 @@ int gg_stage_bulk(const int32_t* bucket_ids_d, const int64_t* owner_off_d, int64
                   const int32_t* prev_ids_d, const int64_t* prev_count_d,
                   gg_stage_stats_t* stats_d, int32_t* status_d, hipStream_t stream);
 
-/* Assembles one batch's input features (Algorithm 1 inner loop): for
- * i < n = bounds_d[1] - bounds_d[0] (at most n_cap), with u =
- * in_ids_d[bounds_d[0] + i], output row i (at out_d + i * out_stride)
- * receives u's feature row: from the local shard when u's owner is
- * part->local_owner, from cache slot slot_of_d[u] when that is >= 0 (a
- * hit), and otherwise through the miss path: misses are grouped by owner
- * and each non-empty group is one on-demand request served straight from
- * that owner's shard (M_{b,m} of Sec. IV-A, Eq. (2)).  Passing
- * in_ids_d = frontier_ids and bounds_d = frontier_off + L*W + b gathers N_b
- * without a host synchronisation. */
-int gg_gather_batch(const int32_t* in_ids_d, const int64_t* bounds_d, int64_t n_cap,
-                    const gg_part_t* part, const gg_feat_t* feat, const void* cache_d,
-                    int64_t cache_stride, int64_t cache_rows, const int32_t* slot_of_d,
-                    void* out_d, int64_t out_stride, gg_gather_stats_t* stats_d,
-                    int32_t* status_d, void* ws, size_t ws_bytes, hipStream_t stream);
+/* Assembles the input features of nseg consecutive batches (Algorithm 1
+ * inner loop) in one launch.  Segment s (s < nseg) is batch s: its ids are
+ * in_ids_d[bounds_d[s] .. bounds_d[s+1]) (bounds_d has nseg + 1 entries, on
+ * the device) and they land in order at output rows bounds_d[s] - bounds_d[0]
+ * onwards (row i at out_d + i * out_stride); out_d holds n_cap rows.  Row
+ * i receives the feature row of its node u: from the local shard when u's
+ * owner is part->local_owner, from cache slot slot_of_d[u] when that is
+ * >= 0 (a hit), and otherwise through the miss path: u is one of the
+ * residual misses M_{b,m} = (N_b in owner m) minus H_k (Sec. IV-A), served
+ * on demand straight from owner m's shard.  stats_d[s] receives batch s's
+ * counts; miss_requests[m] = 1 for every owner with a non-empty miss set,
+ * the request indicator of Eq. (2).  Passing in_ids_d = frontier_ids and
+ * bounds_d = frontier_off + L*W + b with nseg = 1 gathers N_b; with
+ * bounds_d = frontier_off + L*W and nseg = W it gathers the whole window.
+ * No host synchronisation is needed.  Rows past n_cap are dropped and set
+ * GG_DEV_CAPACITY. */
+int gg_gather_batch(const int32_t* in_ids_d, const int64_t* bounds_d, int32_t nseg,
+                    int64_t n_cap, const gg_part_t* part, const gg_feat_t* feat,
+                    const void* cache_d, int64_t cache_stride, int64_t cache_rows,
+                    const int32_t* slot_of_d, void* out_d, int64_t out_stride,
+                    gg_gather_stats_t* stats_d, int32_t* status_d, void* ws, size_t ws_bytes,
+                    hipStream_t stream);
 
 /* Helpers. */
 const char* gg_status_string(int32_t code);

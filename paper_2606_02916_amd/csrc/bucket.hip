@@ -31,14 +31,18 @@ __global__ void __launch_bounds__(kBlock) k_bucket_count(const int32_t* ids, con
   int32_t st = 0;
   for (int it = 0; it < kIdsPerBlock / kBlock; ++it) {
     const int64_t i = i0 + it * kBlock + threadIdx.x;
+    bool valid = false;
+    int32_t m = 0;
     if (i < n) {
       const int32_t u = ids[i];
       if (u < 0 || (int64_t)u >= part.N) {
         st |= GG_DEV_BAD_ID;
       } else {
-        atomicAdd(&hist[owner_of(part, s_start, u)], 1);
+        valid = true;
+        m = owner_of(part, s_start, u);
       }
     }
+    wave_hist_add(hist, valid, m);
   }
   if (st) set_status(status, st);
   __syncthreads();
@@ -69,10 +73,16 @@ __global__ void __launch_bounds__(kBlock) k_bucket_scatter(const int32_t* ids, c
   // Per-wave owner counts.
   for (int g = 0; g < kIdsPerWave / kWave; ++g) {
     const int64_t i = i0 + g * kWave + lane;
+    bool valid = false;
+    int32_t m = 0;
     if (i < n) {
       const int32_t u = ids[i];
-      if (u >= 0 && (int64_t)u < part.N) atomicAdd(&wcnt[w][owner_of(part, s_start, u)], 1);
+      if (u >= 0 && (int64_t)u < part.N) {
+        valid = true;
+        m = owner_of(part, s_start, u);
+      }
     }
+    wave_hist_add(wcnt[w], valid, m);
   }
   __syncthreads();
   for (int t = threadIdx.x; t < 4 * part.P; t += blockDim.x) {

@@ -164,6 +164,19 @@ __device__ __forceinline__ int64_t block_scan_large(const int32_t* in, int64_t* 
   return carry - base;
 }
 
+// hist[key] += number of active lanes with `valid` and that key: one LDS
+// atomic per distinct key present in the wave.  Call from every active lane.
+__device__ __forceinline__ void wave_hist_add(int32_t* hist, bool valid, int32_t key) {
+  const int lane = lane_id();
+  for (uint64_t act = __ballot(valid); act;) {
+    const int leader = __ffsll((unsigned long long)act) - 1;
+    const int32_t kl = __shfl(key, leader, kWave);
+    const uint64_t sel = __ballot(valid && key == kl);
+    if (lane == leader) atomicAdd(&hist[kl], (int32_t)__popcll(sel));
+    act &= ~sel;
+  }
+}
+
 // ---------------------------------------------------------------------------
 // Row copy engine.  A wavefront copies up to 64 rows: lane r supplies the
 // source of row r (nullptr = skip that row) and the rows land at

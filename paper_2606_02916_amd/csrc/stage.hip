@@ -44,11 +44,19 @@ __global__ void __launch_bounds__(kBlock) k_stage_delta(const int32_t* bucket, c
   for (int t = threadIdx.x; t <= GG_MAX_PARTS; t += blockDim.x) s_start[t] = part.start[t];
   __syncthreads();
   const int64_t n = stage_n(owner_off, part.P, a);
-  for (int64_t s = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; s < n;
-       s += (int64_t)gridDim.x * blockDim.x) {
-    const int32_t u = bucket[s];
-    if (u < 0 || (int64_t)u >= part.N) continue;
-    if (slot_of[u] < 0) atomicAdd(&hist[owner_of(part, s_start, u)], 1);
+  for (int64_t base = (int64_t)blockIdx.x * blockDim.x + (threadIdx.x & ~(kWave - 1)); base < n;
+       base += (int64_t)gridDim.x * blockDim.x) {
+    const int64_t s = base + lane_id();
+    bool fresh = false;
+    int32_t m = 0;
+    if (s < n) {
+      const int32_t u = bucket[s];
+      if (u >= 0 && (int64_t)u < part.N && slot_of[u] < 0) {
+        fresh = true;
+        m = owner_of(part, s_start, u);
+      }
+    }
+    wave_hist_add(hist, fresh, m);
   }
   __syncthreads();
   for (int m = threadIdx.x; m < part.P; m += blockDim.x)

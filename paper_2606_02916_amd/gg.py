@@ -82,14 +82,14 @@ SIGNATURES = {
     "gg_ws_sample": (_SZ, [_I64, _I32]),
     "gg_ws_hotset": (_SZ, [_I64, _I32]),
     "gg_ws_bucket": (_SZ, [_I64, _I32]),
-    "gg_ws_gather": (_SZ, [_I64, _I32]),
+    "gg_ws_gather": (_SZ, [_I64, _I32, _I32]),
     "gg_sample_window": (C.c_int, [_P, _P, _P, _I32, _P, _I32, _U64, _I32, _I64, _P, _P, _P, _SZ,
                                    _P]),
     "gg_build_hotset": (C.c_int, [_P, _I32, _P, _I64, _P, _P, _I64, _P, _P, _P, _SZ, _P]),
     "gg_bucket_by_owner": (C.c_int, [_P, _P, _I64, _P, _P, _P, _P, _P, _SZ, _P]),
     "gg_stage_bulk": (C.c_int, [_P, _P, _I64, _P, _P, _P, _I64, _I64, _P, _P, _P, _P, _P, _P]),
-    "gg_gather_batch": (C.c_int, [_P, _P, _I64, _P, _P, _P, _I64, _I64, _P, _P, _I64, _P, _P, _P,
-                                  _SZ, _P]),
+    "gg_gather_batch": (C.c_int, [_P, _P, _I32, _I64, _P, _P, _P, _I64, _I64, _P, _P, _I64, _P,
+                                  _P, _P, _SZ, _P]),
     "gg_status_string": (C.c_char_p, [_I32]),
     "gg_last_error": (C.c_char_p, []),
     "gg_version": (C.c_int, []),
@@ -197,14 +197,17 @@ def gg_ws_bucket(cap, num_parts):
     return int(lib.gg_ws_bucket(cap, num_parts))
 
 
-def gg_ws_gather(n_cap, num_parts):
-    return int(lib.gg_ws_gather(n_cap, num_parts))
+def gg_ws_gather(n_cap, nseg, num_parts):
+    return int(lib.gg_ws_gather(n_cap, nseg, num_parts))
 
 
 def gg_sample_window(csr, seeds, seed_off, W, fanout, L, rng_seed, epoch, batch0, out, status, ws,
                      stream=None):
     so = np.ascontiguousarray(seed_off, dtype=np.int64)
     fan = np.ascontiguousarray(fanout, dtype=np.int32)
+    if seeds is not None and hasattr(seeds, "numel") and seeds.numel() < int(so[-1]):
+        raise GGError(f"gg_sample_window: seed_off ends at {int(so[-1])} but only "
+                      f"{seeds.numel()} seeds were given")
     return check(lib.gg_sample_window(C.byref(csr), _ptr(seeds), so.ctypes.data, W,
                                       fan.ctypes.data, L, C.c_uint64(rng_seed), epoch, batch0,
                                       C.byref(out), _ptr(status), _ptr(ws), ws.numel(),
@@ -233,11 +236,11 @@ def gg_stage_bulk(bucket_ids, owner_off, cap, part, feat, cache, cache_stride, c
                                    _ptr(status), _stream(stream)), "gg_stage_bulk")
 
 
-def gg_gather_batch(in_ids, bounds_ptr, n_cap, part, feat, cache, cache_stride, cache_rows,
+def gg_gather_batch(in_ids, bounds_ptr, nseg, n_cap, part, feat, cache, cache_stride, cache_rows,
                     slot_of, out, out_stride, stats_ptr, status, ws, stream=None):
     """bounds_ptr and stats_ptr are raw device addresses (e.g. an offset into
-    frontier_off or into a stats array)."""
-    return check(lib.gg_gather_batch(_ptr(in_ids), bounds_ptr, n_cap, C.byref(part),
+    frontier_off, or into an array of nseg statistics structures)."""
+    return check(lib.gg_gather_batch(_ptr(in_ids), bounds_ptr, nseg, n_cap, C.byref(part),
                                      C.byref(feat), _ptr(cache), cache_stride, cache_rows,
                                      _ptr(slot_of), _ptr(out), out_stride, stats_ptr,
                                      _ptr(status), _ptr(ws), ws.numel(), _stream(stream)),

@@ -61,15 +61,27 @@ class FetchPipeline:
         self.owner_off = torch.zeros(self.P + 1, dtype=torch.int64, device=dev)
         self.cache = torch.empty((self.hot_cap, self.stride), dtype=torch.uint8, device=dev)
         self.slot_of = torch.full((self.N,), -1, dtype=torch.int32, device=dev)
+        self.win_cap = self.W * self.out_cap
         ws_bytes = max(gg.gg_ws_sample(self.N, self.W), gg.gg_ws_hotset(self.N, self.W),
-                       gg.gg_ws_bucket(self.hot_cap, self.P), gg.gg_ws_gather(self.out_cap, self.P))
+                       gg.gg_ws_bucket(self.hot_cap, self.P),
+                       gg.gg_ws_gather(self.out_cap, 1, self.P),
+                       gg.gg_ws_gather(self.win_cap, self.W, self.P))
         self.ws = torch.empty(ws_bytes, dtype=torch.uint8, device=dev)
         self.stage_stats = torch.zeros(gg.STAGE_STATS_BYTES, dtype=torch.uint8, device=dev)
         self.gather_stats = torch.zeros((self.W, gg.GATHER_STATS_BYTES), dtype=torch.uint8,
                                         device=dev)
         self.outs = [torch.empty((self.out_cap, self.stride), dtype=torch.uint8, device=dev)
                      for _ in range(out_buffers)]
+        self._win_out = None
         self.k = 0
+
+    @property
+    def win_out(self):
+        """Output of a whole-window gather: the W batches' rows back to back."""
+        if self._win_out is None:
+            self._win_out = torch.empty((self.win_cap, self.stride), dtype=torch.uint8,
+                                        device=self.device)
+        return self._win_out
 
     def reset_cache(self):
         self.slot_of.fill_(-1)
@@ -100,18 +112,30 @@ class FetchPipeline:
                          self.status)
 
     def gather(self, Wk, b, out):
+        """Batch b of the window into out (one launch)."""
         bounds = self.frontier_off.data_ptr() + 8 * (self.L * Wk + b)
         stats = self.gather_stats.data_ptr() + b * gg.GATHER_STATS_BYTES
-        gg.gg_gather_batch(self.frontier_ids, bounds, self.out_cap, self.part, self.feat,
+        gg.gg_gather_batch(self.frontier_ids, bounds, 1, out.shape[0], self.part, self.feat,
                            self.cache, self.stride, self.hot_cap, self.slot_of, out, self.stride,
                            stats, self.status, self.ws)
 
+    def gather_window(self, Wk, out=None):
+        """All Wk batches of the window in one launch; batch b's rows start at
+        row frontier_off[L*Wk + b] - frontier_off[L*Wk] of out."""
+        out = self.win_out if out is None else out
+        bounds = self.frontier_off.data_ptr() + 8 * (self.L * Wk)
+        gg.gg_gather_batch(self.frontier_ids, bounds, Wk, out.shape[0], self.part, self.feat,
+                           self.cache, self.stride, self.hot_cap, self.slot_of, out, self.stride,
+                           self.gather_stats.data_ptr(), self.status, self.ws)
+        return out
+
     def window(self, seeds, seed_off, batch0, epoch=0, rng_seed=0, outs=None, events=None,
-               gather_events=None):
-        """Enqueues one window.  outs: per-batch output tensors (default: the
-        driver's ping-pong buffers).  events: optional list of 6 torch events
-        recorded between the calls; gather_events: optional list of (start,
-        end) event pairs, one per batch."""
+               gather_events=None, per_batch=False):
+        """Enqueues one window.  By default the W gathers run as one launch
+        into win_out; with per_batch=True every batch is its own launch into
+        outs[b] (default: the driver's ping-pong buffers).  events: optional
+        list of 6 torch events recorded between the calls; gather_events:
+        optional list of (start, end) event pairs, one per gather launch."""
         cur = self.k & 1
         ev = events if events is not None else [None] * 6
         _rec(ev[0])
@@ -123,13 +147,20 @@ class FetchPipeline:
         _rec(ev[3])
         self.stage(cur)
         _rec(ev[4])
-        for b in range(Wk):
-            out = outs[b] if outs is not None else self.outs[b % len(self.outs)]
+        if per_batch:
+            for b in range(Wk):
+                out = outs[b] if outs is not None else self.outs[b % len(self.outs)]
+                if gather_events is not None:
+                    gather_events[b][0].record()
+                self.gather(Wk, b, out)
+                if gather_events is not None:
+                    gather_events[b][1].record()
+        else:
             if gather_events is not None:
-                gather_events[b][0].record()
-            self.gather(Wk, b, out)
+                gather_events[0][0].record()
+            self.gather_window(Wk, outs)
             if gather_events is not None:
-                gather_events[b][1].record()
+                gather_events[0][1].record()
         _rec(ev[5])
         self.k += 1
         return Wk

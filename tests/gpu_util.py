@@ -103,7 +103,8 @@ class World:
         H = len(hot)
         g_cache = pipe.cache[:H].cpu().numpy()
         assert np.array_equal(g_cache[:, :rb], self.cache_ref[:H, :rb])
-        # gathers, one batch at a time
+        # gathers, one batch at a time, then the whole window in one launch
+        refs, gstats = [], []
         for b in range(Wk):
             out = torch.empty((pipe.out_cap, st), dtype=torch.uint8,
                               device=self.dev)
@@ -116,8 +117,22 @@ class World:
             gs = ggref.gather_batch(ids, self.part_ref, self.feat_ref, self.cache_ref,
                                     st, self.slot_ref, ref, st)
             assert pipe.gather_stats_dict(b) == gs
+            gstats.append(gs)
             if check_outputs:
                 got = out[:len(ids)].cpu().numpy()
                 assert np.array_equal(got[:, :rb], ref[:, :rb]), f"batch {b}"
+                refs.append(ref)
+            del out
+        pipe.gather_stats.zero_()
+        win = pipe.gather_window(Wk)
+        torch.cuda.synchronize()
+        assert pipe.read_status() == 0
+        base = foff[L * Wk]
+        for b in range(Wk):
+            assert pipe.gather_stats_dict(b) == gstats[b]
+            if check_outputs:
+                lo, hi = foff[L * Wk + b] - base, foff[L * Wk + b + 1] - base
+                got = win[lo:hi].cpu().numpy()
+                assert np.array_equal(got[:, :rb], refs[b][:, :rb]), f"window batch {b}"
         pipe.k += 1
         return dict(Wk=Wk, fids=fids, foff=foff, hot=hot, stage=sst)

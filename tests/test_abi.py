@@ -96,7 +96,7 @@ def test_host_helpers(gg):
     assert fc == 2 * (600 + 1000) and nc == 2 * 600 * 3
     for f in (gg.gg_ws_sample, gg.gg_ws_hotset):
         assert f(10_000, 4) > 0 and f(10_000, 4) % 256 == 0
-    assert gg.gg_ws_bucket(0, 4) > 0 and gg.gg_ws_gather(0, 4) > 0
+    assert gg.gg_ws_bucket(0, 4) > 0 and gg.gg_ws_gather(0, 1, 4) > 0
 
 
 class _FakeTensor:
@@ -139,6 +139,10 @@ def test_bad_arguments_are_rejected_on_the_host(gg):
     part = gg.make_part(4, gg.PART_MOD, 0, 100)
     feat = gg.make_feat(250, [t] * 4, [256] * 4, [25] * 4)              # row_bytes % 4 != 0
     with pytest.raises(gg.GGError):
-        gg.gg_gather_batch(t, t.data_ptr(), 10, part, feat, t, 256, 10, t, t, 256,
+        gg.gg_gather_batch(t, t.data_ptr(), 1, 10, part, feat, t, 256, 10, t, t, 256,
                            t.data_ptr(), t, t, stream=0)
-    assert "row_bytes" in gg.gg_last_error()
+    feat = gg.make_feat(256, [t] * 4, [256] * 4, [25] * 4)
+    with pytest.raises(gg.GGError):                                      # nseg outside 1..64
+        gg.gg_gather_batch(t, t.data_ptr(), 0, 10, part, feat, t, 256, 10, t, t, 256,
+                           t.data_ptr(), t, t, stream=0)
+    assert "nseg" in gg.gg_last_error()
