@@ -56,6 +56,9 @@ def main():
                     help="minimum oracle time for the CPU baseline sample")
     ap.add_argument("--per-batch", action="store_true",
                     help="one gather launch per batch instead of one per window")
+    ap.add_argument("--copy-calibration-mib", type=int, default=0,
+                    help="after the timed steps, copy this many MiB device to device three "
+                         "times (a plain copy of known size for scaling HBM counters)")
     args = ap.parse_args()
 
     world = int(os.environ.get("WORLD_SIZE", "1"))
@@ -155,6 +158,16 @@ def main():
     avg_bytes = g_bytes / n_launch
     achieved = avg_bytes / (avg_ms * 1e-3) / 1e9
     stage_gbs = st_bytes / (st_ms * 1e-3) / 1e9
+
+    if args.copy_calibration_mib:
+        nb = args.copy_calibration_mib << 20
+        a = torch.empty(nb, dtype=torch.uint8, device=dev).fill_(1)
+        b = torch.empty(nb, dtype=torch.uint8, device=dev)
+        for _ in range(3):
+            b.copy_(a)
+        torch.cuda.synchronize()
+        log(f"copy calibration: 3 x {args.copy_calibration_mib} MiB device-to-device")
+        del a, b
 
     cpu = None
     if not args.no_cpu_baseline:

@@ -166,6 +166,7 @@ int gg_sample_caps(int64_t num_nodes, int32_t W, int64_t max_batch, const int32_
 size_t gg_ws_sample(int64_t num_nodes, int32_t W);
 size_t gg_ws_hotset(int64_t num_nodes, int32_t W);
 size_t gg_ws_bucket(int64_t cap, int32_t num_parts);
+size_t gg_ws_stage(int64_t cap, int32_t num_parts);
 size_t gg_ws_gather(int64_t n_cap, int32_t nseg, int32_t num_parts);
 
 /* Neighbour sampling of one window (Sec. IV-A step 2: one epoch of
@@ -221,7 +222,8 @@ int gg_stage_bulk(const int32_t* bucket_ids_d, const int64_t* owner_off_d, int64
                   const gg_part_t* part, const gg_feat_t* feat, void* cache_d,
                   int64_t cache_stride, int64_t cache_rows, int32_t* slot_of_d,
                   const int32_t* prev_ids_d, const int64_t* prev_count_d,
-                  gg_stage_stats_t* stats_d, int32_t* status_d, hipStream_t stream);
+                  gg_stage_stats_t* stats_d, int32_t* status_d, void* ws, size_t ws_bytes,
+                  hipStream_t stream);
 
 /* Assembles the input features of nseg consecutive batches (Algorithm 1
  * inner loop) in one launch.  Segment s (s < nseg) is batch s: its ids are

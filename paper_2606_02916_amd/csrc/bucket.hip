@@ -5,6 +5,12 @@
 // which every wavefront ranks its 64 ids among equal owners with ballots
 // (one ballot per distinct owner present in the wave), so order is kept
 // inside each owner.
+//
+// Range partitions first try the identity: when owners never decrease along
+// the input (the ascending hot set always satisfies this), the input is
+// already owner-major.  k_bucket_range copies it, writes owner_off from the
+// owner changes and records per block whether its ids were in owner order;
+// the general passes then run only if some block saw a decrease.
 #include "gg_host.hpp"
 
 namespace gg {
@@ -18,9 +24,66 @@ __device__ __forceinline__ int64_t bucket_n(const int64_t* hot_count, int64_t ca
   return n < cap ? n : cap;
 }
 
+// Owner-order check and identity bucketing for range partitions.  Every
+// block writes ok[blockIdx.x] (1 when its ids are valid and in owner order).
+__global__ void __launch_bounds__(kBlock) k_bucket_range(const int32_t* ids, const int64_t* hot_count,
+                                                         int64_t cap, KPart part, int32_t* out,
+                                                         int64_t* owner_off, int32_t* ok) {
+  __shared__ int64_t s_start[GG_MAX_PARTS + 1];
+  __shared__ int32_t s_bad;
+  for (int t = threadIdx.x; t <= GG_MAX_PARTS; t += blockDim.x) s_start[t] = part.start[t];
+  if (threadIdx.x == 0) s_bad = 0;
+  __syncthreads();
+  const int64_t n = bucket_n(hot_count, cap);
+  const int P = part.P;
+  if (n == 0) {
+    if (blockIdx.x == 0)
+      for (int m = threadIdx.x; m <= P; m += blockDim.x) owner_off[m] = 0;
+  }
+  int bad = 0;
+  const int64_t i0 = (int64_t)blockIdx.x * kIdsPerBlock;
+  for (int it = 0; it < kIdsPerBlock / kBlock; ++it) {
+    const int64_t i = i0 + it * kBlock + threadIdx.x;
+    if (i >= n) break;
+    const int32_t u = ids[i];
+    if (u < 0 || (int64_t)u >= part.N) {
+      bad = 1;
+      continue;
+    }
+    const int32_t o = owner_of(part, s_start, u);
+    int32_t op = -1;
+    if (i > 0) {
+      const int32_t up = ids[i - 1];
+      op = (up < 0 || (int64_t)up >= part.N) ? P : owner_of(part, s_start, up);
+    }
+    if (op > o) bad = 1;
+    for (int32_t m = op + 1; m <= o; ++m) owner_off[m] = i;
+    if (i == n - 1)
+      for (int32_t m = o + 1; m <= P; ++m) owner_off[m] = n;
+    out[i] = u;
+  }
+  if (bad) s_bad = 1;
+  __syncthreads();
+  if (threadIdx.x == 0) ok[blockIdx.x] = s_bad ? 0 : 1;
+}
+
+// True when the identity pass of every block succeeded.
+__device__ __forceinline__ bool range_done(const int32_t* ok, int32_t nok, int32_t* s_flag) {
+  if (ok == nullptr) return false;
+  if (threadIdx.x == 0) *s_flag = 1;
+  __syncthreads();
+  for (int x = threadIdx.x; x < nok; x += blockDim.x)
+    if (ok[x] == 0) *s_flag = 0;
+  __syncthreads();
+  return *s_flag != 0;
+}
+
 __global__ void __launch_bounds__(kBlock) k_bucket_count(const int32_t* ids, const int64_t* hot_count,
                                                          int64_t cap, KPart part, int32_t* cnt,
-                                                         int32_t nblk, int32_t* status) {
+                                                         int32_t nblk, const int32_t* ok,
+                                                         int32_t* status) {
+  __shared__ int32_t s_flag;
+  if (range_done(ok, nblk, &s_flag)) return;
   __shared__ int32_t hist[GG_MAX_PARTS];
   __shared__ int64_t s_start[GG_MAX_PARTS + 1];
   for (int t = threadIdx.x; t < GG_MAX_PARTS; t += blockDim.x) hist[t] = 0;
@@ -50,7 +113,10 @@ __global__ void __launch_bounds__(kBlock) k_bucket_count(const int32_t* ids, con
 }
 
 __global__ void __launch_bounds__(1024) k_bucket_scan(const int32_t* cnt, int64_t ncnt, int32_t nblk,
-                                                      int32_t P, int64_t* off, int64_t* owner_off) {
+                                                      int32_t P, int64_t* off, int64_t* owner_off,
+                                                      const int32_t* ok) {
+  __shared__ int32_t s_flag;
+  if (range_done(ok, nblk, &s_flag)) return;
   __shared__ int64_t lds[16];
   const int64_t total = block_scan_large(cnt, off, ncnt, 0, lds);
   __syncthreads();
@@ -60,7 +126,10 @@ __global__ void __launch_bounds__(1024) k_bucket_scan(const int32_t* cnt, int64_
 
 __global__ void __launch_bounds__(kBlock) k_bucket_scatter(const int32_t* ids, const int64_t* hot_count,
                                                            int64_t cap, KPart part, const int64_t* off,
-                                                           int32_t nblk, int32_t* out) {
+                                                           int32_t nblk, const int32_t* ok,
+                                                           int32_t* out) {
+  __shared__ int32_t s_flag;
+  if (range_done(ok, nblk, &s_flag)) return;
   __shared__ int32_t wcnt[4][GG_MAX_PARTS];
   __shared__ int64_t wbase[4][GG_MAX_PARTS];
   __shared__ int64_t s_start[GG_MAX_PARTS + 1];
@@ -120,6 +189,7 @@ __global__ void __launch_bounds__(kBlock) k_bucket_scatter(const int32_t* ids, c
 struct BucketWs {
   int32_t* cnt;
   int64_t* off;
+  int32_t* ok;
 };
 
 size_t bucket_ws_layout(int64_t cap, int32_t P, char* base, BucketWs* out) {
@@ -128,6 +198,7 @@ size_t bucket_ws_layout(int64_t cap, int32_t P, char* base, BucketWs* out) {
   BucketWs b;
   b.cnt = cv.take<int32_t>((size_t)(nblk * P));
   b.off = cv.take<int64_t>((size_t)(nblk * P));
+  b.ok = cv.take<int32_t>((size_t)nblk);
   if (out) *out = b;
   return align_up(cv.used, 256);
 }
@@ -155,14 +226,21 @@ extern "C" int gg_bucket_by_owner(const int32_t* hot_ids_d, const int64_t* hot_c
   const size_t need_ws = bucket_ws_layout(cap, kp.P, (char*)ws, &bw);
   GG_REQUIRE(ws && ws_bytes >= need_ws, "workspace of %zu bytes < %zu", ws_bytes, need_ws);
   const int32_t nblk = (int32_t)std::max<int64_t>(1, cdiv(cap, kIdsPerBlock));
+  const int32_t* ok = nullptr;
+  if (kp.kind == GG_PART_RANGE) {
+    hipLaunchKernelGGL(k_bucket_range, dim3(nblk), dim3(kBlock), 0, stream, hot_ids_d, hot_count_d,
+                       cap, kp, bucket_ids_d, owner_off_d, bw.ok);
+    GG_LAUNCH_CHECK("k_bucket_range");
+    ok = bw.ok;
+  }
   hipLaunchKernelGGL(k_bucket_count, dim3(nblk), dim3(kBlock), 0, stream, hot_ids_d, hot_count_d, cap,
-                     kp, bw.cnt, nblk, status_d);
+                     kp, bw.cnt, nblk, ok, status_d);
   GG_LAUNCH_CHECK("k_bucket_count");
   hipLaunchKernelGGL(k_bucket_scan, dim3(1), dim3(1024), 0, stream, bw.cnt, (int64_t)nblk * kp.P,
-                     nblk, kp.P, bw.off, owner_off_d);
+                     nblk, kp.P, bw.off, owner_off_d, ok);
   GG_LAUNCH_CHECK("k_bucket_scan");
   hipLaunchKernelGGL(k_bucket_scatter, dim3(nblk), dim3(kBlock), 0, stream, hot_ids_d, hot_count_d,
-                     cap, kp, bw.off, nblk, bucket_ids_d);
+                     cap, kp, bw.off, nblk, ok, bucket_ids_d);
   GG_LAUNCH_CHECK("k_bucket_scatter");
   return GG_OK;
 }

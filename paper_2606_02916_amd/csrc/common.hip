@@ -25,7 +25,8 @@ int pack_part(const gg_part_t* part, KPart* out) {
   out->P = P;
   out->kind = part->kind;
   out->local = part->local_owner;
-  out->pad_ = 0;
+  out->step0 = 1;
+  while (out->step0 * 2 <= P - 1) out->step0 *= 2;
   out->N = part->num_nodes;
   out->div_magic = ((1ULL << 40) + (uint64_t)P - 1) / (uint64_t)P;
   if (part->kind == GG_PART_RANGE) {

@@ -44,7 +44,7 @@ __global__ void k_gather_zero(int64_t* miss_count) {
   if (threadIdx.x == 0) miss_count[0] = 0;
 }
 
-template <int VB, bool NT>
+template <int VB, bool NT, int U>
 __global__ void __launch_bounds__(kBlock) k_gather_rows(const int32_t* in_ids, const int64_t* bounds,
                                                         KPart part, KFeat feat, GatherArgs a,
                                                         const char* cache, const int32_t* slot_of,
@@ -121,7 +121,7 @@ __global__ void __launch_bounds__(kBlock) k_gather_rows(const int32_t* in_ids, c
     }
     const int64_t left = hi - r0;
     const int nrows = left < kWave ? (int)left : kWave;
-    wave_copy_rows<VB, NT>(src, out + r0 * a.out_stride, a.out_stride, nrows, a.geom);
+    wave_copy_rows<VB, NT, U>(src, out + r0 * a.out_stride, a.out_stride, nrows, a.geom);
   }
   if (lane == 0) {
     if (c_local) atomicAdd(&s_cnt[0], c_local);
@@ -212,6 +212,11 @@ bool env_flag(const char* name, bool dflt) {
   return strcmp(v, "0") != 0;
 }
 
+int env_int(const char* name, int dflt) {
+  const char* v = getenv(name);
+  return (v && *v) ? atoi(v) : dflt;
+}
+
 struct GatherWs {
   int64_t* miss_count;
   int32_t* blk_stat;
@@ -238,14 +243,23 @@ size_t gather_ws_layout(int64_t n_cap, int32_t nseg, int32_t P, char* base, Gath
 }
 
 template <int VB, bool NT>
-void launch_gather(hipStream_t stream, int32_t bx, const int32_t* in_ids, const int64_t* bounds,
+void launch_gather(hipStream_t stream, int unroll, int32_t bx, const int32_t* in_ids, const int64_t* bounds,
                    const KPart& kp, const KFeat& kf, const GatherArgs& a, const char* cache,
                    const int32_t* slot_of, char* out, const GatherWs& w, gg_gather_stats_t* stats,
                    int32_t* status) {
   hipLaunchKernelGGL(k_gather_zero, dim3(1), dim3(64), 0, stream, w.miss_count);
-  hipLaunchKernelGGL((k_gather_rows<VB, NT>), dim3(bx, a.nseg), dim3(kBlock), 0, stream, in_ids,
-                     bounds, kp, kf, a, cache, slot_of, out, w.blk_stat, w.miss_count, w.miss_pos,
-                     w.miss_id, status);
+  if (VB == 16 && unroll == 8)
+    hipLaunchKernelGGL((k_gather_rows<VB, NT, 8>), dim3(bx, a.nseg), dim3(kBlock), 0, stream, in_ids,
+                       bounds, kp, kf, a, cache, slot_of, out, w.blk_stat, w.miss_count, w.miss_pos,
+                       w.miss_id, status);
+  else if (VB == 16 && unroll == 2)
+    hipLaunchKernelGGL((k_gather_rows<VB, NT, 2>), dim3(bx, a.nseg), dim3(kBlock), 0, stream, in_ids,
+                       bounds, kp, kf, a, cache, slot_of, out, w.blk_stat, w.miss_count, w.miss_pos,
+                       w.miss_id, status);
+  else
+    hipLaunchKernelGGL((k_gather_rows<VB, NT, VB == 16 ? 4 : 8>), dim3(bx, a.nseg), dim3(kBlock), 0,
+                       stream, in_ids, bounds, kp, kf, a, cache, slot_of, out, w.blk_stat,
+                       w.miss_count, w.miss_pos, w.miss_id, status);
   const int miss_blocks = (int)std::min<int64_t>(std::max<int64_t>(cdiv(a.n_cap, kBlock), 1), 1024);
   hipLaunchKernelGGL((k_gather_finish<VB, NT>), dim3(a.nseg + miss_blocks), dim3(kBlock), 0, stream,
                      bounds, kp, kf, a, bx, w.blk_stat, w.miss_count, w.miss_pos, w.miss_id, out,
@@ -302,21 +316,22 @@ extern "C" int gg_gather_batch(const int32_t* in_ids_d, const int64_t* bounds_d,
   a.geom = copy_geom(kf.row_bytes, v16 ? 16 : 4);
   const int32_t bx = blocks_per_seg(n_cap, nseg);
   static const bool nt = env_flag("GG_NT_GATHER", true);
+  static const int unroll = env_int("GG_GATHER_UNROLL", 8);
   const char* cache = (const char*)cache_d;
   char* out = (char*)out_d;
   if (v16) {
     if (nt)
-      launch_gather<16, true>(stream, bx, in_ids_d, bounds_d, kp, kf, a, cache, slot_of_d, out, gw,
+      launch_gather<16, true>(stream, unroll, bx, in_ids_d, bounds_d, kp, kf, a, cache, slot_of_d, out, gw,
                               stats_d, status_d);
     else
-      launch_gather<16, false>(stream, bx, in_ids_d, bounds_d, kp, kf, a, cache, slot_of_d, out, gw,
+      launch_gather<16, false>(stream, unroll, bx, in_ids_d, bounds_d, kp, kf, a, cache, slot_of_d, out, gw,
                                stats_d, status_d);
   } else {
     if (nt)
-      launch_gather<4, true>(stream, bx, in_ids_d, bounds_d, kp, kf, a, cache, slot_of_d, out, gw,
+      launch_gather<4, true>(stream, unroll, bx, in_ids_d, bounds_d, kp, kf, a, cache, slot_of_d, out, gw,
                              stats_d, status_d);
     else
-      launch_gather<4, false>(stream, bx, in_ids_d, bounds_d, kp, kf, a, cache, slot_of_d, out, gw,
+      launch_gather<4, false>(stream, unroll, bx, in_ids_d, bounds_d, kp, kf, a, cache, slot_of_d, out, gw,
                               stats_d, status_d);
   }
   GG_LAUNCH_CHECK("k_gather_zero/k_gather_rows/k_gather_finish");

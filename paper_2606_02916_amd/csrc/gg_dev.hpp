@@ -16,13 +16,13 @@ constexpr int kWordsPerThread = kChunkWords / kBlock;
 // ---------------------------------------------------------------------------
 // Partition book, passed by value.  MOD uses a multiply-shift for u div P
 // (exact for u < 2^34 and P <= 64); RANGE finds the last start <= u by a
-// fixed six-step binary search over the 64-entry padded start table.
+// binary search over the P starts (the table is padded with N up to 64).
 // ---------------------------------------------------------------------------
 struct KPart {
   int32_t P;
   int32_t kind;
   int32_t local;
-  int32_t pad_;
+  int32_t step0;  // RANGE: largest power of two <= max(P - 1, 1)
   int64_t N;
   uint64_t div_magic;
   int64_t start[GG_MAX_PARTS + 1];  // entries past P hold N
@@ -39,8 +39,7 @@ __device__ __forceinline__ int32_t owner_of(const KPart& p, const int64_t* start
     return u - q * p.P;
   }
   int32_t idx = 0;
-#pragma unroll
-  for (int step = 32; step >= 1; step >>= 1)
+  for (int step = p.step0; step >= 1; step >>= 1)
     if (start[idx + step] <= (int64_t)u) idx += step;
   return idx;
 }
@@ -213,11 +212,10 @@ __device__ __forceinline__ void st4(char* p, uint32_t v) {
     *(uint32_t*)p = v;
 }
 
-template <int VB, bool NT>
+template <int VB, bool NT, int U = (VB == 16 ? 4 : 8)>
 __device__ __forceinline__ void wave_copy_rows(const char* src, char* dst0, int64_t dst_stride,
                                                int nrows, const CopyGeom& g) {
   const int lane = lane_id();
-  constexpr int U = VB == 16 ? 4 : 8;
   const uint32_t total = (uint32_t)nrows * g.cpr;
   const long long srcl = (long long)src;
   for (uint32_t base = 0; base < total; base += kWave * U) {

@@ -203,6 +203,58 @@ __device__ __forceinline__ void floyd_positions(uint32_t u, uint32_t bglob, cons
   }
 }
 
+// Samples frontier entry gi of level l (batch b): writes its k neighbour
+// slots and sets the sampled neighbours' bits in batch b's set.  All
+// neighbour loads are issued before any store or atomic.
+template <typename RowT, int KMAX>
+__device__ __forceinline__ void sample_one(const RowT* row_ptr, const int32_t* col_idx,
+                                           const int32_t* fids, int64_t gi, int b, int64_t begin,
+                                           int64_t nbase, int32_t* nbr, uint32_t* bits,
+                                           const SampleArgs& a, int32_t& st) {
+  const int32_t k = a.k;
+  const int32_t u = fids[gi];
+  const int64_t obase = nbase + (gi - begin) * k;
+  if (obase + k > a.ncap) {
+    st |= GG_DEV_CAPACITY;
+    return;
+  }
+  int32_t* out = nbr + obase;
+  uint32_t* brow = bits + (int64_t)b * a.wpb;
+  const int64_t beg = (int64_t)row_ptr[u];
+  const int64_t d = (int64_t)row_ptr[u + 1] - beg;
+  uint32_t pos[KMAX];
+  int32_t cnt;
+  if (d <= k) {
+#pragma unroll
+    for (int i = 0; i < KMAX; ++i) pos[i] = (uint32_t)i;
+    cnt = (int32_t)d;
+  } else if (d > 0xFFFFFFFFLL) {
+    st |= GG_DEV_BAD_DEGREE;
+    cnt = 0;
+  } else {
+    floyd_positions<KMAX>((uint32_t)u, (uint32_t)(a.batch0 + b), a, (uint32_t)d, pos);
+    cnt = k;
+  }
+  int32_t v[KMAX];
+#pragma unroll
+  for (int i = 0; i < KMAX; ++i) v[i] = (i < cnt) ? col_idx[beg + pos[i]] : -1;
+#pragma unroll
+  for (int i = 0; i < KMAX; ++i) {
+    if (i < k && i < cnt && (v[i] < 0 || (int64_t)v[i] >= a.N)) {
+      st |= GG_DEV_BAD_ID;
+      v[i] = -1;
+    }
+  }
+#pragma unroll
+  for (int i = 0; i < KMAX; ++i) {
+    if (i < k) {
+      const int32_t x = v[i];
+      if (x >= 0) atomicOr(brow + (x >> 5), 1u << (x & 31));
+      out[i] = (i < cnt) ? x : -1;
+    }
+  }
+}
+
 // One lane per frontier node of level l (all batches of the window).
 template <typename RowT, int KMAX>
 __global__ void __launch_bounds__(kBlock) k_sample(const RowT* row_ptr, const int32_t* col_idx,
@@ -217,56 +269,11 @@ __global__ void __launch_bounds__(kBlock) k_sample(const RowT* row_ptr, const in
   __syncthreads();
   const int64_t begin = so[0], end = so[a.W];
   const int64_t nbase = s_nbase;
-  const int32_t k = a.k;
   int32_t st = 0;
   for (int64_t gi = begin + (int64_t)blockIdx.x * blockDim.x + threadIdx.x; gi < end;
-       gi += (int64_t)gridDim.x * blockDim.x) {
-    const int b = find_batch(so, gi);
-    const int32_t u = fids[gi];
-    const int64_t obase = nbase + (gi - begin) * k;
-    if (obase + k > a.ncap) {
-      st |= GG_DEV_CAPACITY;
-      continue;
-    }
-    int32_t* out = nbr + obase;
-    uint32_t* brow = bits + (int64_t)b * a.wpb;
-    const int64_t beg = (int64_t)row_ptr[u];
-    const int64_t d = (int64_t)row_ptr[u + 1] - beg;
-    if (d <= k) {
-      for (int32_t p = 0; p < k; ++p) {
-        int32_t v = -1;
-        if (p < d) {
-          v = col_idx[beg + p];
-          if (v < 0 || (int64_t)v >= a.N) {
-            st |= GG_DEV_BAD_ID;
-            v = -1;
-          } else {
-            atomicOr(brow + (v >> 5), 1u << (v & 31));
-          }
-        }
-        out[p] = v;
-      }
-    } else if (d > 0xFFFFFFFFLL) {
-      st |= GG_DEV_BAD_DEGREE;
-      for (int32_t p = 0; p < k; ++p) out[p] = -1;
-    } else {
-      uint32_t pos[KMAX];
-      floyd_positions<KMAX>((uint32_t)u, (uint32_t)(a.batch0 + b), a, (uint32_t)d, pos);
-#pragma unroll
-      for (int i = 0; i < KMAX; ++i) {
-        if (i < k) {
-          int32_t v = col_idx[beg + pos[i]];
-          if (v < 0 || (int64_t)v >= a.N) {
-            st |= GG_DEV_BAD_ID;
-            v = -1;
-          } else {
-            atomicOr(brow + (v >> 5), 1u << (v & 31));
-          }
-          out[i] = v;
-        }
-      }
-    }
-  }
+       gi += (int64_t)gridDim.x * blockDim.x)
+    sample_one<RowT, KMAX>(row_ptr, col_idx, fids, gi, find_batch(so, gi), begin, nbase, nbr, bits,
+                           a, st);
   if (st) set_status(status, st);
 }
 

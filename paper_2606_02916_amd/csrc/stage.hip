@@ -27,17 +27,12 @@ __device__ __forceinline__ int64_t stage_n(const int64_t* owner_off, int32_t P, 
   return n < a.cache_rows ? n : a.cache_rows;
 }
 
-__global__ void k_stage_prep(gg_stage_stats_t* stats) {
-  int64_t* p = (int64_t*)stats;
-  const int n = (int)(sizeof(gg_stage_stats_t) / sizeof(int64_t));
-  for (int t = threadIdx.x; t < n; t += blockDim.x) p[t] = 0;
-}
-
 // Rebuild delta: staged rows whose node is not in the previous window's
-// cache (slot_of still describes that cache here).
+// cache (slot_of still describes that cache here).  Every block writes its
+// per-owner counts to dcnt[block * P + m].
 __global__ void __launch_bounds__(kBlock) k_stage_delta(const int32_t* bucket, const int64_t* owner_off,
                                                         KPart part, StageArgs a, const int32_t* slot_of,
-                                                        gg_stage_stats_t* stats) {
+                                                        int32_t* dcnt) {
   __shared__ int32_t hist[GG_MAX_PARTS];
   __shared__ int64_t s_start[GG_MAX_PARTS + 1];
   for (int t = threadIdx.x; t < GG_MAX_PARTS; t += blockDim.x) hist[t] = 0;
@@ -59,9 +54,7 @@ __global__ void __launch_bounds__(kBlock) k_stage_delta(const int32_t* bucket, c
     wave_hist_add(hist, fresh, m);
   }
   __syncthreads();
-  for (int m = threadIdx.x; m < part.P; m += blockDim.x)
-    if (hist[m])
-      atomicAdd((unsigned long long*)&stats->delta_rows[m], (unsigned long long)hist[m]);
+  for (int m = threadIdx.x; m < part.P; m += blockDim.x) dcnt[(int64_t)blockIdx.x * part.P + m] = hist[m];
 }
 
 __global__ void __launch_bounds__(kBlock) k_slot_reset(const int32_t* prev, const int64_t* prev_count,
@@ -112,26 +105,46 @@ __global__ void __launch_bounds__(kBlock) k_stage_rows(const int32_t* bucket, co
   if (st) set_status(status, st);
 }
 
-__global__ void k_stage_finish(const int64_t* owner_off, KPart part, StageArgs a,
-                               const int64_t* prev_count, int32_t row_bytes,
-                               gg_stage_stats_t* stats, int32_t* status) {
+__global__ void __launch_bounds__(kBlock) k_stage_finish(const int64_t* owner_off, KPart part,
+                                                         StageArgs a, const int64_t* prev_count,
+                                                         int32_t row_bytes, const int32_t* dcnt,
+                                                         int32_t nblk_delta, gg_stage_stats_t* stats,
+                                                         int32_t* status) {
+  __shared__ int32_t s_delta[GG_MAX_PARTS];
+  for (int t = threadIdx.x; t < GG_MAX_PARTS; t += blockDim.x) s_delta[t] = 0;
+  __syncthreads();
+  for (int m = 0; m < part.P; ++m) {
+    int32_t v = 0;
+    for (int x = threadIdx.x; x < nblk_delta; x += blockDim.x) v += dcnt[(int64_t)x * part.P + m];
+    v = wave_sum(v);
+    if (lane_id() == 0 && v) atomicAdd(&s_delta[m], v);
+  }
+  __syncthreads();
   const int64_t n = stage_n(owner_off, part.P, a);
-  for (int m = threadIdx.x; m < part.P; m += blockDim.x) {
-    int64_t lo = owner_off[m], hi = owner_off[m + 1];
-    lo = lo < n ? lo : n;
-    hi = hi < n ? hi : n;
-    const int64_t rows = hi > lo ? hi - lo : 0;
+  if (threadIdx.x < GG_MAX_PARTS) {
+    const int m = threadIdx.x;
+    int64_t rows = 0;
+    if (m < part.P) {
+      int64_t lo = owner_off[m], hi = owner_off[m + 1];
+      lo = lo < n ? lo : n;
+      hi = hi < n ? hi : n;
+      rows = hi > lo ? hi - lo : 0;
+    }
     stats->rows[m] = rows;
     stats->bytes[m] = rows * row_bytes;
     stats->requests[m] = rows > 0 ? 1 : 0;
+    stats->delta_rows[m] = s_delta[m];
   }
-  __syncthreads();
   if (threadIdx.x == 0) {
     int64_t req = 0;
-    for (int m = 0; m < part.P; ++m) req += stats->requests[m];
+    for (int m = 0; m < part.P; ++m) {
+      int64_t lo = owner_off[m] < n ? owner_off[m] : n, hi = owner_off[m + 1] < n ? owner_off[m + 1] : n;
+      req += hi > lo ? 1 : 0;
+    }
     stats->rows_total = n;
     stats->requests_total = req;
     stats->invalidated = prev_count ? prev_count[0] : 0;
+    stats->pad_ = 0;
     if (owner_off[part.P] > n) set_status(status, GG_DEV_CAPACITY);
   }
 }
@@ -154,16 +167,25 @@ void launch_stage_rows(bool nt, int grid, hipStream_t stream, const int32_t* buc
                        owner_off, kp, kf, a, cache, slot_of, status);
 }
 
+int stage_delta_blocks(int64_t cap) {
+  return (int)std::min<int64_t>(std::max<int64_t>(cdiv(cap, kBlock), 1), 1024);
+}
+
 }  // namespace
 }  // namespace gg
 
 using namespace gg;
 
+extern "C" size_t gg_ws_stage(int64_t cap, int32_t num_parts) {
+  return align_up((size_t)stage_delta_blocks(cap) * (size_t)num_parts * sizeof(int32_t), 256);
+}
+
 extern "C" int gg_stage_bulk(const int32_t* bucket_ids_d, const int64_t* owner_off_d, int64_t cap,
                              const gg_part_t* part, const gg_feat_t* feat, void* cache_d,
                              int64_t cache_stride, int64_t cache_rows, int32_t* slot_of_d,
                              const int32_t* prev_ids_d, const int64_t* prev_count_d,
-                             gg_stage_stats_t* stats_d, int32_t* status_d, hipStream_t stream) {
+                             gg_stage_stats_t* stats_d, int32_t* status_d, void* ws,
+                             size_t ws_bytes, hipStream_t stream) {
   GG_REQUIRE(owner_off_d && slot_of_d && stats_d && status_d, "NULL argument");
   GG_REQUIRE(cap >= 0 && cap < (1LL << 31) && cache_rows >= 0, "bad capacity");
   GG_REQUIRE(cap == 0 || bucket_ids_d, "bucket ids are NULL");
@@ -188,11 +210,12 @@ extern "C" int gg_stage_bulk(const int32_t* bucket_ids_d, const int64_t* owner_o
   a.geom = copy_geom(kf.row_bytes, v16 ? 16 : 4);
   static const bool nt = env_flag("GG_NT_STAGE", false);
 
-  hipLaunchKernelGGL(k_stage_prep, dim3(1), dim3(256), 0, stream, stats_d);
-  GG_LAUNCH_CHECK("k_stage_prep");
-  const int gridd = (int)std::min<int64_t>(std::max<int64_t>(cdiv(cap, kBlock), 1), 2048);
+  const int gridd = stage_delta_blocks(cap);
+  GG_REQUIRE(ws && ws_bytes >= gg_ws_stage(cap, kp.P), "workspace of %zu bytes < %zu", ws_bytes,
+             gg_ws_stage(cap, kp.P));
+  int32_t* dcnt = (int32_t*)ws;
   hipLaunchKernelGGL(k_stage_delta, dim3(gridd), dim3(kBlock), 0, stream, bucket_ids_d, owner_off_d,
-                     kp, a, slot_of_d, stats_d);
+                     kp, a, slot_of_d, dcnt);
   GG_LAUNCH_CHECK("k_stage_delta");
   if (prev_ids_d) {
     hipLaunchKernelGGL(k_slot_reset, dim3(2048), dim3(kBlock), 0, stream, prev_ids_d, prev_count_d,
@@ -208,8 +231,8 @@ extern "C" int gg_stage_bulk(const int32_t* bucket_ids_d, const int64_t* owner_o
     launch_stage_rows<4>(nt, grid, stream, bucket_ids_d, owner_off_d, kp, kf, a, (char*)cache_d,
                          slot_of_d, status_d);
   GG_LAUNCH_CHECK("k_stage_rows");
-  hipLaunchKernelGGL(k_stage_finish, dim3(1), dim3(64), 0, stream, owner_off_d, kp, a, prev_count_d,
-                     kf.row_bytes, stats_d, status_d);
+  hipLaunchKernelGGL(k_stage_finish, dim3(1), dim3(kBlock), 0, stream, owner_off_d, kp, a,
+                     prev_count_d, kf.row_bytes, dcnt, gridd, stats_d, status_d);
   GG_LAUNCH_CHECK("k_stage_finish");
   return GG_OK;
 }

@@ -82,12 +82,14 @@ SIGNATURES = {
     "gg_ws_sample": (_SZ, [_I64, _I32]),
     "gg_ws_hotset": (_SZ, [_I64, _I32]),
     "gg_ws_bucket": (_SZ, [_I64, _I32]),
+    "gg_ws_stage": (_SZ, [_I64, _I32]),
     "gg_ws_gather": (_SZ, [_I64, _I32, _I32]),
     "gg_sample_window": (C.c_int, [_P, _P, _P, _I32, _P, _I32, _U64, _I32, _I64, _P, _P, _P, _SZ,
                                    _P]),
     "gg_build_hotset": (C.c_int, [_P, _I32, _P, _I64, _P, _P, _I64, _P, _P, _P, _SZ, _P]),
     "gg_bucket_by_owner": (C.c_int, [_P, _P, _I64, _P, _P, _P, _P, _P, _SZ, _P]),
-    "gg_stage_bulk": (C.c_int, [_P, _P, _I64, _P, _P, _P, _I64, _I64, _P, _P, _P, _P, _P, _P]),
+    "gg_stage_bulk": (C.c_int, [_P, _P, _I64, _P, _P, _P, _I64, _I64, _P, _P, _P, _P, _P, _P, _SZ,
+                                _P]),
     "gg_gather_batch": (C.c_int, [_P, _P, _I32, _I64, _P, _P, _P, _I64, _I64, _P, _P, _I64, _P,
                                   _P, _P, _SZ, _P]),
     "gg_status_string": (C.c_char_p, [_I32]),
@@ -197,6 +199,10 @@ def gg_ws_bucket(cap, num_parts):
     return int(lib.gg_ws_bucket(cap, num_parts))
 
 
+def gg_ws_stage(cap, num_parts):
+    return int(lib.gg_ws_stage(cap, num_parts))
+
+
 def gg_ws_gather(n_cap, nseg, num_parts):
     return int(lib.gg_ws_gather(n_cap, nseg, num_parts))
 
@@ -229,11 +235,12 @@ def gg_bucket_by_owner(hot_ids, hot_count, cap, part, bucket_ids, owner_off, sta
 
 
 def gg_stage_bulk(bucket_ids, owner_off, cap, part, feat, cache, cache_stride, cache_rows, slot_of,
-                  prev_ids, prev_count, stats, status, stream=None):
+                  prev_ids, prev_count, stats, status, ws, stream=None):
     return check(lib.gg_stage_bulk(_ptr(bucket_ids), _ptr(owner_off), cap, C.byref(part),
                                    C.byref(feat), _ptr(cache), cache_stride, cache_rows,
                                    _ptr(slot_of), _ptr(prev_ids), _ptr(prev_count), _ptr(stats),
-                                   _ptr(status), _stream(stream)), "gg_stage_bulk")
+                                   _ptr(status), _ptr(ws), ws.numel(), _stream(stream)),
+                 "gg_stage_bulk")
 
 
 def gg_gather_batch(in_ids, bounds_ptr, nseg, n_cap, part, feat, cache, cache_stride, cache_rows,

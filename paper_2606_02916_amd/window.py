@@ -19,7 +19,7 @@ from . import gg
 class FetchPipeline:
     def __init__(self, row_ptr, col_idx, num_parts, part_kind, local_owner, range_start, shards,
                  shard_rows, row_bytes, stride, W, fanout, max_batch, n_hot=-1, device=None,
-                 out_buffers=2):
+                 out_buffers=2, cache_stride=None):
         self.device = torch.device(device if device is not None else "cuda")
         self.N = int(row_ptr.numel() - 1)
         self.W = int(W)
@@ -28,6 +28,9 @@ class FetchPipeline:
         self.P = int(num_parts)
         self.row_bytes = int(row_bytes)
         self.stride = int(stride)
+        # Cache rows are packed at the feature stride: neighbouring slots
+        # share HBM sectors, which a sparse ascending gather reuses.
+        self.cache_stride = int(cache_stride) if cache_stride else self.stride
         self.n_hot = int(n_hot)
         self.row_ptr, self.col_idx = row_ptr, col_idx
         self.shards = shards
@@ -59,11 +62,11 @@ class FetchPipeline:
         self.bucket_ids = [torch.empty(self.hot_cap, dtype=torch.int32, device=dev)
                            for _ in range(2)]
         self.owner_off = torch.zeros(self.P + 1, dtype=torch.int64, device=dev)
-        self.cache = torch.empty((self.hot_cap, self.stride), dtype=torch.uint8, device=dev)
+        self.cache = torch.empty((self.hot_cap, self.cache_stride), dtype=torch.uint8, device=dev)
         self.slot_of = torch.full((self.N,), -1, dtype=torch.int32, device=dev)
         self.win_cap = self.W * self.out_cap
         ws_bytes = max(gg.gg_ws_sample(self.N, self.W), gg.gg_ws_hotset(self.N, self.W),
-                       gg.gg_ws_bucket(self.hot_cap, self.P),
+                       gg.gg_ws_bucket(self.hot_cap, self.P), gg.gg_ws_stage(self.hot_cap, self.P),
                        gg.gg_ws_gather(self.out_cap, 1, self.P),
                        gg.gg_ws_gather(self.win_cap, self.W, self.P))
         self.ws = torch.empty(ws_bytes, dtype=torch.uint8, device=dev)
@@ -106,18 +109,18 @@ class FetchPipeline:
         prev = 1 - cur
         have_prev = self.k > 0
         gg.gg_stage_bulk(self.bucket_ids[cur], self.owner_off, self.hot_cap, self.part, self.feat,
-                         self.cache, self.stride, self.hot_cap, self.slot_of,
+                         self.cache, self.cache_stride, self.hot_cap, self.slot_of,
                          self.bucket_ids[prev] if have_prev else None,
                          self.hot_count[prev] if have_prev else None, self.stage_stats,
-                         self.status)
+                         self.status, self.ws)
 
     def gather(self, Wk, b, out):
         """Batch b of the window into out (one launch)."""
         bounds = self.frontier_off.data_ptr() + 8 * (self.L * Wk + b)
         stats = self.gather_stats.data_ptr() + b * gg.GATHER_STATS_BYTES
         gg.gg_gather_batch(self.frontier_ids, bounds, 1, out.shape[0], self.part, self.feat,
-                           self.cache, self.stride, self.hot_cap, self.slot_of, out, self.stride,
-                           stats, self.status, self.ws)
+                           self.cache, self.cache_stride, self.hot_cap, self.slot_of, out,
+                           self.stride, stats, self.status, self.ws)
 
     def gather_window(self, Wk, out=None):
         """All Wk batches of the window in one launch; batch b's rows start at
@@ -125,8 +128,8 @@ class FetchPipeline:
         out = self.win_out if out is None else out
         bounds = self.frontier_off.data_ptr() + 8 * (self.L * Wk)
         gg.gg_gather_batch(self.frontier_ids, bounds, Wk, out.shape[0], self.part, self.feat,
-                           self.cache, self.stride, self.hot_cap, self.slot_of, out, self.stride,
-                           self.gather_stats.data_ptr(), self.status, self.ws)
+                           self.cache, self.cache_stride, self.hot_cap, self.slot_of, out,
+                           self.stride, self.gather_stats.data_ptr(), self.status, self.ws)
         return out
 
     def window(self, seeds, seed_off, batch0, epoch=0, rng_seed=0, outs=None, events=None,

@@ -222,6 +222,25 @@ def full_features(wl: Workload):
 
 
 _cache = {}
+GEN_VERSION = 1
+
+
+def _disk_cache(name, what, make):
+    """Arrays of a workload, memoised under $SYNTH_CACHE_DIR when it is set
+    (the generator is deterministic, so a cached copy equals a fresh one)."""
+    d = os.environ.get("SYNTH_CACHE_DIR")
+    if not d:
+        return make()
+    path = os.path.join(d, f"{name}.v{GEN_VERSION}.{what}.npz")
+    if os.path.exists(path):
+        with np.load(path) as z:
+            return [z[k] for k in sorted(z.files, key=lambda k: int(k[1:]))]
+    arrs = make()
+    os.makedirs(d, exist_ok=True)
+    tmp = path + ".tmp.npz"
+    np.savez(tmp, **{f"a{i}": a for i, a in enumerate(arrs)})
+    os.replace(tmp, path)
+    return arrs
 
 
 def instance(name, with_features=True):
@@ -229,10 +248,13 @@ def instance(name, with_features=True):
     if key in _cache:
         return _cache[key]
     wl = WORKLOADS[name]
-    row_ptr, col_idx = rmat_csr(wl.num_nodes, wl.num_edges, relabel=wl.relabel,
-                                row_ptr_bits=wl.row_ptr_bits)
+    gname = "large_sparse" if name == "wsweep" else name
+    row_ptr, col_idx = _disk_cache(gname, "csr", lambda: list(rmat_csr(
+        wl.num_nodes, wl.num_edges, relabel=wl.relabel, row_ptr_bits=wl.row_ptr_bits)))
     seeds, boff = seed_batches(wl)
-    shards = [shard_features(wl, m) for m in range(wl.num_parts)] if with_features else []
+    shards = (_disk_cache(gname, "feat", lambda: [shard_features(wl, m)
+                                                  for m in range(wl.num_parts)])
+              if with_features else [])
     inst = Instance(wl, row_ptr, col_idx, seeds, boff, shards,
                     wl.range_start() if wl.part_kind == PART_RANGE else None)
     _cache[key] = inst

@@ -19,7 +19,7 @@ class World:
     """One workload instance on the GPU and its oracle counterpart."""
 
     def __init__(self, inst, W=None, n_hot=-1, local_owner=None, fanout=None, batch=None,
-                 device="cuda:0", shards=None, row_bytes=None, stride=None):
+                 device="cuda:0", shards=None, row_bytes=None, stride=None, cache_stride=None):
         wl = inst.wl
         self.inst = inst
         self.wl = wl
@@ -40,10 +40,12 @@ class World:
         rows = [s.shape[0] for s in self.shards]
         self.pipe = FetchPipeline(self.row_ptr_d, self.col_idx_d, self.P, wl.part_kind, self.local,
                                   self.rs, self.shards_d, rows, self.row_bytes, self.stride,
-                                  self.W, self.fanout, self.batch, n_hot=n_hot, device=self.dev)
+                                  self.W, self.fanout, self.batch, n_hot=n_hot, device=self.dev,
+                                  cache_stride=cache_stride)
         self.part_ref = ggref.make_part(self.P, wl.part_kind, self.local, wl.num_nodes, self.rs)
         self.feat_ref = ggref.make_feat(self.row_bytes, self.shards, [self.stride] * self.P)
-        self.cache_ref = np.zeros((self.pipe.hot_cap, self.stride), dtype=np.uint8)
+        self.cstride = self.pipe.cache_stride
+        self.cache_ref = np.zeros((self.pipe.hot_cap, self.cstride), dtype=np.uint8)
         self.slot_ref = np.full(wl.num_nodes, -1, dtype=np.int32)
         self.prev_ref = None
 
@@ -96,7 +98,7 @@ class World:
         assert np.array_equal(g_owner_off, owner_off)
         # stage
         sst = ggref.stage_bulk(bucket, owner_off, self.part_ref, self.feat_ref, self.cache_ref,
-                               st, self.slot_ref, self.prev_ref)
+                               self.cstride, self.slot_ref, self.prev_ref)
         self.prev_ref = bucket.copy()
         assert pipe.stage_stats_dict() == sst
         assert np.array_equal(pipe.slot_of.cpu().numpy(), self.slot_ref)
@@ -115,7 +117,7 @@ class World:
             ids = fids[foff[s]:foff[s + 1]]
             ref = np.zeros((len(ids), st), dtype=np.uint8)
             gs = ggref.gather_batch(ids, self.part_ref, self.feat_ref, self.cache_ref,
-                                    st, self.slot_ref, ref, st)
+                                    self.cstride, self.slot_ref, ref, st)
             assert pipe.gather_stats_dict(b) == gs
             gstats.append(gs)
             if check_outputs:

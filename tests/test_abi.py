@@ -96,7 +96,7 @@ def test_host_helpers(gg):
     assert fc == 2 * (600 + 1000) and nc == 2 * 600 * 3
     for f in (gg.gg_ws_sample, gg.gg_ws_hotset):
         assert f(10_000, 4) > 0 and f(10_000, 4) % 256 == 0
-    assert gg.gg_ws_bucket(0, 4) > 0 and gg.gg_ws_gather(0, 1, 4) > 0
+    assert gg.gg_ws_bucket(0, 4) > 0 and gg.gg_ws_gather(0, 1, 4) > 0 and gg.gg_ws_stage(0, 4) > 0
 
 
 class _FakeTensor:
@@ -135,7 +135,7 @@ def test_bad_arguments_are_rejected_on_the_host(gg):
     part = gg.make_part(4, gg.PART_MOD, 4, 100)                          # local owner >= P
     feat = gg.make_feat(256, [t] * 4, [256] * 4, [25] * 4)
     with pytest.raises(gg.GGError):
-        gg.gg_stage_bulk(t, t, 10, part, feat, t, 256, 10, t, None, None, t, t, stream=0)
+        gg.gg_stage_bulk(t, t, 10, part, feat, t, 256, 10, t, None, None, t, t, t, stream=0)
     part = gg.make_part(4, gg.PART_MOD, 0, 100)
     feat = gg.make_feat(250, [t] * 4, [256] * 4, [25] * 4)              # row_bytes % 4 != 0
     with pytest.raises(gg.GGError):

@@ -106,7 +106,7 @@ def test_unaligned_rows_use_the_word_path():
     inst = synth.instance("tiny")
     rng = np.random.default_rng(5)
     shards = [rng.integers(0, 256, size=(s.shape[0], 44), dtype=np.uint8) for s in inst.shards]
-    w = world(inst, shards=shards, row_bytes=44, stride=44)
+    w = world(inst, shards=shards, row_bytes=44, stride=44, cache_stride=44)
     w.run_and_compare(0)
 
 
@@ -162,3 +162,37 @@ def test_dense_mid_full_window_matches_oracle():
     log("dense_mid: 233K nodes, 114M edges, fp32x602 (stride 2416), fanout [25,10], W=8, window 0")
     w = world(synth.instance("dense_mid"))
     w.run_and_compare(0)
+
+
+@pytest.mark.parametrize("kind", [0, 1])
+@pytest.mark.parametrize("order", ["ascending", "shuffled", "one_descent"])
+def test_bucket_by_owner_direct(kind, order):
+    log(f"bucket_by_owner: kind={kind} order={order}")
+    import torch as T
+    from oracle import ggref
+    from paper_2606_02916_amd import gg
+    rng = np.random.default_rng(17)
+    N, P = 500_000, 5
+    rs = [0, 70_000, 70_000, 300_000, 420_001, N]
+    ids = np.sort(rng.choice(N, size=123_457, replace=False)).astype(np.int32)
+    if order == "shuffled":
+        rng.shuffle(ids)
+    elif order == "one_descent":
+        ids[[1000, 60_000]] = ids[[60_000, 1000]]
+    part_ref = ggref.make_part(P, kind, 0, N, rs if kind == 1 else None)
+    want, want_off = ggref.bucket_by_owner(ids, part_ref)
+    dev = T.device("cuda:0")
+    cap = ids.shape[0] + 1000
+    hot = T.zeros(cap, dtype=T.int32, device=dev)
+    hot[:ids.shape[0]] = T.from_numpy(ids).to(dev)
+    cnt = T.tensor([ids.shape[0], ids.shape[0]], dtype=T.int64, device=dev)
+    out = T.full((cap,), -7, dtype=T.int32, device=dev)
+    off = T.zeros(P + 1, dtype=T.int64, device=dev)
+    status = T.zeros(1, dtype=T.int32, device=dev)
+    ws = T.empty(gg.gg_ws_bucket(cap, P), dtype=T.uint8, device=dev)
+    part = gg.make_part(P, kind, 0, N, rs if kind == 1 else None)
+    gg.gg_bucket_by_owner(hot, cnt, cap, part, out, off, status, ws)
+    T.cuda.synchronize()
+    assert int(status.item()) == 0
+    assert np.array_equal(off.cpu().numpy(), want_off)
+    assert np.array_equal(out[:ids.shape[0]].cpu().numpy(), want)
