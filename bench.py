@@ -26,6 +26,8 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBS = 8000.0
+PROFILES = os.path.join(ROOT, "profiles")
+GATHER_SOURCES = ["paper_2606_02916_amd/csrc/gather.hip", "paper_2606_02916_amd/csrc/gg_dev.hpp"]
 
 
 def log(msg):
@@ -41,6 +43,88 @@ def cpu_model():
     except OSError:
         pass
     return platform.processor()
+
+
+def gather_source_sha():
+    import hashlib
+    h = hashlib.sha256()
+    for f in GATHER_SOURCES:
+        with open(os.path.join(ROOT, f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()[:16]
+
+
+def counters_path(workload):
+    return os.path.join(PROFILES, f"gather_{workload}_counters.txt")
+
+
+def measured_traffic(workload, per_batch):
+    """HBM bytes per gather launch from the committed counter summary, or
+    None when there is none for this workload or the kernel source changed."""
+    path = counters_path(workload)
+    if per_batch or not os.path.exists(path):
+        return None
+    with open(path) as f:
+        d = json.loads("".join(l for l in f if not l.startswith("#")))
+    if d.get("source_sha") != gather_source_sha():
+        return None
+    return int(d["traffic_bytes_per_launch"])
+
+
+def _short(name):
+    import re
+    m = re.search(r"(k_[a-z_0-9]+)(<[^>]*>)?", name)
+    return (m.group(1) + (m.group(2) or "")) if m else name.split("(")[0][:48]
+
+
+def summarize(args):
+    """Writes profiles/ summaries from rocprofv3 databases of bench runs."""
+    import sqlite3
+    wl = args.config
+    os.makedirs(PROFILES, exist_ok=True)
+    cmd = args.summary_command
+    if args.trace_db:
+        db = sqlite3.connect(args.trace_db)
+        rows = db.execute("select name, count(*), avg(end-start), min(end-start), max(end-start), "
+                          "sum(end-start) from kernels group by name order by sum(end-start) "
+                          "desc").fetchall()
+        tot = sum(r[5] for r in rows)
+        out = [f"# rocprofv3 kernel trace of bench.py, workload {wl}",
+               f"# command: {cmd}",
+               f"# gather source sha: {gather_source_sha()}",
+               f"{'kernel':40s} {'calls':>6s} {'avg_us':>9s} {'min_us':>9s} {'max_us':>9s} "
+               f"{'total_ms':>9s} {'share':>6s}"]
+        for n, c, a, mn, mx, sm in rows:
+            out.append(f"{_short(n):40s} {c:6d} {a / 1e3:9.2f} {mn / 1e3:9.2f} {mx / 1e3:9.2f} "
+                       f"{sm / 1e6:9.3f} {100 * sm / tot:5.1f}%")
+        with open(os.path.join(PROFILES, f"kernels_{wl}.txt"), "w") as f:
+            f.write("\n".join(out) + "\n")
+    if args.fetch_db and args.write_db:
+        def per_kernel(path, counter):
+            db = sqlite3.connect(path)
+            r = db.execute("select kernel_name, value from counters_collection where "
+                           "counter_name = ?", (counter,)).fetchall()
+            gather = [v for n, v in r if "k_gather_rows" in n]
+            copies = sorted((v for n, v in r if "copyBuffer" in n), reverse=True)[:3]
+            return sum(gather) / len(gather), sum(copies) / len(copies), len(gather)
+        f_g, f_c, n_g = per_kernel(args.fetch_db, "FETCH_SIZE")
+        w_g, w_c, _ = per_kernel(args.write_db, "WRITE_SIZE")
+        known_kib = args.copy_calibration_mib * 1024
+        fs, wsc = known_kib / f_c, known_kib / w_c
+        traffic = int(round((f_g * fs + w_g * wsc) * 1024))
+        d = {"kernel": "k_gather_rows", "workload": wl, "launches": n_g,
+             "source_sha": gather_source_sha(),
+             "fetch_kib_per_launch_raw": round(f_g, 1), "write_kib_per_launch_raw": round(w_g, 1),
+             "calibration": {"copy_mib": args.copy_calibration_mib,
+                             "fetch_kib_raw": round(f_c, 1), "write_kib_raw": round(w_c, 1)},
+             "fetch_scale": round(fs, 4), "write_scale": round(wsc, 4),
+             "traffic_bytes_per_launch": traffic}
+        with open(counters_path(wl), "w") as f:
+            f.write(f"# HBM counters of k_gather_rows (window-mode gather), workload {wl}\n")
+            f.write(f"# command (FETCH_SIZE, then WRITE_SIZE): {cmd}\n")
+            f.write("# scale = known bytes of a 1 GiB device-to-device copy / counter reading\n")
+            f.write(json.dumps(d, indent=1) + "\n")
+    print("summaries written", file=sys.stderr)
 
 
 def main():
@@ -59,7 +143,16 @@ def main():
     ap.add_argument("--copy-calibration-mib", type=int, default=0,
                     help="after the timed steps, copy this many MiB device to device three "
                          "times (a plain copy of known size for scaling HBM counters)")
+    ap.add_argument("--summarize", action="store_true",
+                    help="write profiles/ summaries from rocprofv3 databases instead of running")
+    ap.add_argument("--trace-db", default=None)
+    ap.add_argument("--fetch-db", default=None)
+    ap.add_argument("--write-db", default=None)
+    ap.add_argument("--summary-command", default="")
     args = ap.parse_args()
+    if args.summarize:
+        summarize(args)
+        return
 
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
@@ -194,7 +287,8 @@ def main():
                    "gather_launch": "per batch" if pb else "per window"},
         "roofline": {"bound": "hbm", "kernel": "gg_gather_batch",
                      "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                     "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": None,
+                     "frac": round(achieved / HBM_PEAK_GBS, 4),
+                     "traffic": measured_traffic(args.config, pb),
                      "bytes_per_launch": int(avg_bytes), "avg_launch_us": round(avg_ms * 1e3, 2)},
         "stage_roofline": {"kernel": "gg_stage_bulk", "achieved": round(stage_gbs, 1),
                            "frac": round(stage_gbs / HBM_PEAK_GBS, 4), "unit": "GB/s"},
