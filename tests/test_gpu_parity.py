@@ -196,3 +196,76 @@ def test_bucket_by_owner_direct(kind, order):
     assert int(status.item()) == 0
     assert np.array_equal(off.cpu().numpy(), want_off)
     assert np.array_equal(out[:ids.shape[0]].cpu().numpy(), want)
+
+
+@pytest.mark.timeout(900)
+def test_wsweep_batch4096_w2_matches_oracle():
+    log("wsweep graph: batch 4096, W=2, window 0, full compare")
+    w = world(synth.instance("wsweep"), W=2)
+    w.run_and_compare(0)
+
+
+@pytest.mark.timeout(900)
+def test_wsweep_batch4096_w32_sampled_batches_and_invariants():
+    log("wsweep graph: batch 4096, W=32, window 0: sampled batches vs oracle, invariants")
+    import torch as T
+    from oracle import ggref
+    inst = synth.instance("wsweep")
+    wl = inst.wl
+    w = world(inst, W=32)
+    p = w.pipe
+    seeds, so, b0 = w.window_inputs(0)
+    Wk = p.window(T.from_numpy(seeds).to(w.dev), so, b0)
+    T.cuda.synchronize()
+    assert p.read_status() == 0
+    L = len(wl.fanout)
+    fids, foff, nids, noff = p.sample_outputs(Wk)
+    base = int(foff[L * Wk])
+    rs = inst.range_start
+    full_rows = {}
+    # batches 0, 17 and 31 against the oracle run on that batch alone (N_b
+    # does not depend on the window it falls in)
+    for b in (0, 17, 31):
+        s = seeds[so[b]:so[b + 1]]
+        f1, o1, n1, no1 = ggref.sample_window(inst.row_ptr, inst.col_idx, s,
+                                              np.array([0, len(s)], np.int64), wl.fanout, 0, 0,
+                                              b0 + b)
+        for l in range(L + 1):
+            got = fids[foff[l * Wk + b]:foff[l * Wk + b + 1]]
+            assert np.array_equal(got, f1[o1[l]:o1[l + 1]]), (b, l)
+        for l in range(L):
+            got = nids[noff[l * Wk + b]:noff[l * Wk + b + 1]]
+            assert np.array_equal(got, n1[no1[l]:no1[l + 1]]), (b, l)
+    # hot set = union of the remote N_b, with per-batch frequencies
+    lo, hi = rs[0], rs[1]
+    allN = fids[foff[L * Wk]:foff[(L + 1) * Wk]]
+    remote = allN[(allN < lo) | (allN >= hi)]
+    uniq, cnt = np.unique(remote, return_counts=True)
+    hot, freq, hc, bucket, owner_off = p.hot_outputs()
+    assert np.array_equal(hot, uniq) and np.array_equal(freq, cnt)
+    assert np.array_equal(bucket, hot)                     # ranges: identity bucketing
+    for m in range(4):
+        assert owner_off[m] == np.searchsorted(hot, rs[m])
+    # staged rows and gathered rows equal the source rows, on a sample
+    rng = np.random.default_rng(1)
+    cache = p.cache
+    slots = rng.choice(len(hot), 2000, replace=False)
+    for s_ in slots.tolist():
+        u = int(bucket[s_])
+        m = int(np.searchsorted(rs, u, side="right") - 1)
+        want = inst.shards[m][u - rs[m], :wl.row_bytes]
+        assert np.array_equal(cache[s_, :wl.row_bytes].cpu().numpy(), want)
+    out = p.win_out
+    rows = rng.choice(foff[(L + 1) * Wk] - base, 5000, replace=False)
+    got = out[T.from_numpy(rows).to(w.dev)].cpu().numpy()
+    for r_, g in zip(rows.tolist(), got):
+        u = int(fids[base + r_])
+        m = int(np.searchsorted(rs, u, side="right") - 1)
+        assert np.array_equal(g[:wl.row_bytes], inst.shards[m][u - rs[m], :wl.row_bytes])
+    total = 0
+    for b in range(Wk):
+        gs = p.gather_stats_dict(b)
+        n = int(foff[L * Wk + b + 1] - foff[L * Wk + b])
+        assert gs["rows"] == n and gs["misses"] == 0 and gs["local"] + gs["hits"] == n
+        total += n
+    assert total == len(allN)
