@@ -175,13 +175,11 @@ def main():
         return wsweep(args, wl)
     W = args.W or wl.W
     t = time.time()
-    inst = synth.instance(args.config)
+    inst, row_ptr_d, col_idx_d, shards_d = synth.torch_instance(args.config, dev)
     log(f"generated {args.config}: N={wl.num_nodes} E={wl.num_edges} in {time.time() - t:.1f}s")
     P, L = wl.num_parts, len(wl.fanout)
-    row_ptr_d = torch.from_numpy(inst.row_ptr).to(dev)
-    col_idx_d = torch.from_numpy(inst.col_idx).to(dev)
-    shards_d = [torch.from_numpy(s).to(dev) for s in inst.shards]
     seeds_d = torch.from_numpy(inst.seeds).to(dev)
+    pcie = pcie_h2d_gbps(dev) if wl.remote_on_host else None
     pipe = FetchPipeline(row_ptr_d, col_idx_d, P, wl.part_kind, wl.local_owner, inst.range_start,
                          shards_d, [s.shape[0] for s in inst.shards], wl.row_bytes, wl.row_stride,
                          W, wl.fanout, wl.batch_size, device=dev)
@@ -198,7 +196,7 @@ def main():
     # Pass over every window once: per-window row counts for the metric and
     # per-batch local/remote counts for the gather's algorithmic bytes.
     rb = wl.row_bytes
-    rows_w, gbytes_w, hot_w, sbytes_w, req_w = [], [], [], [], []
+    rows_w, gbytes_w, hot_w, sbytes_w, req_w, hbytes_w = [], [], [], [], [], []
     pb = args.per_batch
     for k, (s, so, b0) in enumerate(wins):
         Wk = pipe.window(s, so, b0, per_batch=pb)
@@ -214,6 +212,7 @@ def main():
         hot_w.append(ss["rows_total"])
         sbytes_w.append(ss["rows_total"] * (2 * rb + 8) + ss["invalidated"] * 4)
         req_w.append(ss["requests_total"])
+        hbytes_w.append(sum(ss["bytes"][m] for m in range(P) if not shards_d[m].is_cuda))
     log(f"rows per window: {rows_w[:4]}... hot set: {hot_w[:4]}...")
 
     for i in range(args.warmup):
@@ -241,13 +240,14 @@ def main():
 
     g_ms, g_bytes, n_launch = 0.0, 0, 0
     stage_ms = {"sample": [], "hotset": [], "bucket": [], "stage": [], "gathers": []}
-    st_ms, st_bytes = 0.0, 0
+    st_ms, st_bytes, st_host_bytes = 0.0, 0, 0
     for i, k in enumerate(order):
         e = evs[i]
         for name, (a, b) in zip(stage_ms, [(0, 1), (1, 2), (2, 3), (3, 4), (4, 5)]):
             stage_ms[name].append(e[a].elapsed_time(e[b]))
         st_ms += e[3].elapsed_time(e[4])
         st_bytes += sbytes_w[k]
+        st_host_bytes += hbytes_w[k]
         for b in range(len(gbytes_w[k])):
             g_ms += gevs[i][b][0].elapsed_time(gevs[i][b][1])
             g_bytes += gbytes_w[k][b]
@@ -295,8 +295,16 @@ def main():
                      "frac": round(achieved / HBM_PEAK_GBS, 4),
                      "traffic": measured_traffic(args.config, pb),
                      "bytes_per_launch": int(avg_bytes), "avg_launch_us": round(avg_ms * 1e3, 2)},
-        "stage_roofline": {"kernel": "gg_stage_bulk", "achieved": round(stage_gbs, 1),
-                           "frac": round(stage_gbs / HBM_PEAK_GBS, 4), "unit": "GB/s"},
+        "stage_roofline": ({"kernel": "gg_stage_bulk", "bound": "hbm",
+                            "achieved": round(stage_gbs, 1),
+                            "frac": round(stage_gbs / HBM_PEAK_GBS, 4), "unit": "GB/s"}
+                           if pcie is None else
+                           {"kernel": "gg_stage_bulk", "bound": "pcie",
+                            "achieved": round(st_host_bytes / (st_ms * 1e-3) / 1e9, 2),
+                            "peak": round(pcie, 2), "unit": "GB/s",
+                            "frac": round(st_host_bytes / (st_ms * 1e-3) / 1e9 / pcie, 4),
+                            "note": "host bytes read by the staging kernel over PCIe vs a "
+                                    "measured pinned-to-device copy of 1 GiB"}),
         "stage_ms_median": {k: round(float(np.median(v)), 4) for k, v in stage_ms.items()},
         "rows_per_window": int(np.mean(rows_w)),
         "hot_set_rows_per_window": int(np.mean(hot_w)),
@@ -307,6 +315,24 @@ def main():
     print(json.dumps(line), flush=True)
 
 
+def pcie_h2d_gbps(dev):
+    """Pinned host to device copy rate of 1 GiB (best of 3), the PCIe ceiling
+    for staging rows that live in host memory."""
+    import torch
+    a = torch.empty(1 << 30, dtype=torch.uint8, pin_memory=True)
+    b = torch.empty(1 << 30, dtype=torch.uint8, device=dev)
+    best = 1e9
+    for _ in range(3):
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        b.copy_(a, non_blocking=True)
+        e1.record()
+        torch.cuda.synchronize()
+        best = min(best, e0.elapsed_time(e1))
+    del a, b
+    return (1 << 30) / (best * 1e-3) / 1e9
+
+
 def wsweep(args, wl):
     """One epoch per window size W on the same graph, seeds and features."""
     import numpy as np
@@ -315,11 +341,8 @@ def wsweep(args, wl):
     import synth
     from paper_2606_02916_amd import FetchPipeline
     dev = torch.device("cuda:0")
-    inst = synth.instance(args.config)
+    inst, row_ptr_d, col_idx_d, shards_d = synth.torch_instance(args.config, dev)
     P, rb = wl.num_parts, wl.row_bytes
-    row_ptr_d = torch.from_numpy(inst.row_ptr).to(dev)
-    col_idx_d = torch.from_numpy(inst.col_idx).to(dev)
-    shards_d = [torch.from_numpy(s).to(dev) for s in inst.shards]
     seeds_d = torch.from_numpy(inst.seeds).to(dev)
     boff = inst.batch_off
     results = []

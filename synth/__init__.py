@@ -222,7 +222,7 @@ def full_features(wl: Workload):
 
 
 _cache = {}
-GEN_VERSION = 1
+GEN_VERSION = 2
 
 
 def _disk_cache(name, what, make):
@@ -243,19 +243,80 @@ def _disk_cache(name, what, make):
     return arrs
 
 
-def instance(name, with_features=True):
-    key = (name, with_features)
+def _progress(msg):
+    import sys
+    import time
+    print(f"[synth {time.strftime('%H:%M:%S')}] {msg}", file=sys.stderr, flush=True)
+
+
+def instance(name, with_features=True, host_alloc=None):
+    """Generates (or returns the memoised) workload `name`.
+
+    host_alloc(m, rows, stride) -> uint8 array: when given, the shards of
+    remote owners of a workload that keeps them in host memory are written
+    straight into the arrays it returns (e.g. views of pinned host tensors).
+    """
+    key = (name, with_features, host_alloc is not None)
     if key in _cache:
         return _cache[key]
     wl = WORKLOADS[name]
     gname = "large_sparse" if name == "wsweep" else name
-    row_ptr, col_idx = _disk_cache(gname, "csr", lambda: list(rmat_csr(
-        wl.num_nodes, wl.num_edges, relabel=wl.relabel, row_ptr_bits=wl.row_ptr_bits)))
+    big = wl.num_edges > 500_000_000
+    if big:
+        _progress(f"{name}: R-MAT {wl.num_nodes} nodes, {wl.num_edges} edges")
+    make_csr = lambda: list(rmat_csr(wl.num_nodes, wl.num_edges, relabel=wl.relabel,  # noqa: E731
+                                     row_ptr_bits=wl.row_ptr_bits))
+    row_ptr, col_idx = make_csr() if big else _disk_cache(gname, "csr", make_csr)
     seeds, boff = seed_batches(wl)
-    shards = (_disk_cache(gname, "feat", lambda: [shard_features(wl, m)
-                                                  for m in range(wl.num_parts)])
-              if with_features else [])
+    shards = []
+    if with_features:
+        if wl.remote_on_host and host_alloc is not None:
+            for m in range(wl.num_parts):
+                rows = shard_rows(wl, m)
+                out = None if m == wl.local_owner else host_alloc(m, rows, wl.row_stride)
+                if big:
+                    _progress(f"{name}: features of owner {m} ({rows} rows)")
+                shards.append(shard_features(wl, m, out=out))
+        elif big:
+            for m in range(wl.num_parts):
+                _progress(f"{name}: features of owner {m}")
+                shards.append(shard_features(wl, m))
+        else:
+            shards = _disk_cache(gname, "feat", lambda: [shard_features(wl, m)
+                                                         for m in range(wl.num_parts)])
+    if big:
+        _progress(f"{name}: ready")
     inst = Instance(wl, row_ptr, col_idx, seeds, boff, shards,
                     wl.range_start() if wl.part_kind == PART_RANGE else None)
     _cache[key] = inst
     return inst
+
+
+def torch_instance(name, device):
+    """The workload with its CSR and feature shards as torch tensors:
+    device tensors, except the remote shards of a workload that keeps them
+    in host memory, which stay pinned host tensors (read by the GPU through
+    their device address).  Returns (inst, row_ptr_d, col_idx_d, shards_d)."""
+    import torch
+    wl = WORKLOADS[name]
+    pinned = {}
+
+    def alloc(m, rows, stride):
+        t = torch.empty((rows, stride), dtype=torch.uint8, pin_memory=True)
+        pinned[m] = t
+        return t.numpy()
+
+    key = ("torch", name)
+    if key in _cache:
+        return _cache[key]
+    inst = instance(name, host_alloc=alloc if wl.remote_on_host else None)
+    if wl.remote_on_host and not pinned:
+        raise RuntimeError("host-resident shards were generated without pinned memory")
+    dev = torch.device(device)
+    row_ptr_d = torch.from_numpy(inst.row_ptr).to(dev)
+    col_idx_d = torch.from_numpy(inst.col_idx).to(dev)
+    shards_d = [pinned[m] if m in pinned else torch.from_numpy(inst.shards[m]).to(dev)
+                for m in range(wl.num_parts)]
+    res = (inst, row_ptr_d, col_idx_d, shards_d)
+    _cache[key] = res
+    return res

@@ -30,8 +30,11 @@ inline uint64_t mix64(uint64_t z) {
 }
 
 // Word i of the stream (seed, stream).
+inline uint64_t stream_key(uint64_t seed, uint64_t stream) {
+  return mix64(seed * 0xD1B54A32D192ED03ULL ^ mix64(stream));
+}
 inline uint64_t word64(uint64_t seed, uint64_t stream, uint64_t i) {
-  return mix64(mix64(seed * 0xD1B54A32D192ED03ULL ^ mix64(stream)) + i);
+  return mix64(stream_key(seed, stream) + i);
 }
 
 int num_threads() {
@@ -40,13 +43,17 @@ int num_threads() {
   return (int)std::min<unsigned>(hc, 16u);
 }
 
+// Runs f(i) for i in [0, n) on the worker threads.  Items are handed out in
+// grains; `heavy` marks loops whose items are large chunks of work, which
+// are spread one at a time and never run serially.
 template <class F>
-void parallel_for(int64_t n, F f) {
+void parallel_for(int64_t n, F f, bool heavy = false) {
   int nt = num_threads();
-  if (n < 4096) nt = 1;
+  if (n < 4096 && !heavy) nt = 1;
   std::vector<std::thread> th;
   std::atomic<int64_t> next{0};
-  const int64_t grain = std::max<int64_t>(1, std::min<int64_t>(1 << 16, n / (nt * 8) + 1));
+  const int64_t grain =
+      heavy ? 1 : std::max<int64_t>(1, std::min<int64_t>(1 << 16, n / (nt * 8) + 1));
   for (int t = 0; t < nt; ++t) {
     th.emplace_back([&]() {
       for (;;) {
@@ -102,26 +109,18 @@ enum : uint64_t {
 
 // One R-MAT candidate edge.  Each level draws one 32-bit word and picks a
 // quadrant of the adjacency matrix with probabilities (a, b, c, 1-a-b-c).
-inline void rmat_candidate(uint64_t seed, uint64_t c, int scale, uint32_t t1, uint32_t t2,
+inline void rmat_candidate(uint64_t key, uint64_t c, int scale, uint32_t t1, uint32_t t2,
                            uint32_t t3, uint64_t* src, uint64_t* dst) {
   uint64_t s = 0, d = 0;
   uint64_t w = 0;
   const uint64_t base = c * (uint64_t)((scale + 1) / 2);
   for (int lv = 0; lv < scale; ++lv) {
-    if ((lv & 1) == 0) w = word64(seed, STREAM_RMAT, base + (uint64_t)(lv / 2));
-    uint32_t r = (lv & 1) ? (uint32_t)(w >> 32) : (uint32_t)w;
-    uint64_t sb, db;
-    if (r < t1) {
-      sb = 0; db = 0;
-    } else if (r < t2) {
-      sb = 0; db = 1;
-    } else if (r < t3) {
-      sb = 1; db = 0;
-    } else {
-      sb = 1; db = 1;
-    }
-    s = (s << 1) | sb;
-    d = (d << 1) | db;
+    if ((lv & 1) == 0) w = mix64(key + base + (uint64_t)(lv / 2));
+    const uint32_t r = (lv & 1) ? (uint32_t)(w >> 32) : (uint32_t)w;
+    // Quadrants in order (0,0), (0,1), (1,0), (1,1) below t1, t2, t3, 2^32.
+    const uint64_t g1 = r >= t1, g2 = r >= t2, g3 = r >= t3;
+    s = (s << 1) | g2;
+    d = (d << 1) | (g1 ^ g2 ^ g3);
   }
   *src = s;
   *dst = d;
@@ -156,6 +155,7 @@ int synth_rmat_csr(int64_t num_nodes, int64_t num_edges, double a, double b, dou
   const uint32_t t2 = (uint32_t)std::min(two32 - 1, (a + b) * two32);
   const uint32_t t3 = (uint32_t)std::min(two32 - 1, (a + b + c) * two32);
   const int64_t CH = 1 << 18;
+  const uint64_t rkey = stream_key(seed, STREAM_RMAT);
 
   // Pass 1: count accepted candidates per chunk until the budget covers E.
   std::vector<int64_t> chunk_cnt;
@@ -174,11 +174,11 @@ int synth_rmat_csr(int64_t num_nodes, int64_t num_edges, double a, double b, dou
       int64_t cnt = 0;
       for (int64_t i = 0; i < CH; ++i) {
         uint64_t s, d;
-        rmat_candidate(seed, (uint64_t)(ch * CH + i), scale, t1, t2, t3, &s, &d);
+        rmat_candidate(rkey, (uint64_t)(ch * CH + i), scale, t1, t2, t3, &s, &d);
         cnt += (s < (uint64_t)num_nodes && d < (uint64_t)num_nodes);
       }
       chunk_cnt[(size_t)ch] = cnt;
-    });
+    }, true);
     for (int64_t k = 0; k < add; ++k) have += chunk_cnt[(size_t)(first + k)];
     nchunks += add;
   }
@@ -194,7 +194,7 @@ int synth_rmat_csr(int64_t num_nodes, int64_t num_edges, double a, double b, dou
     int64_t pos = chunk_off[(size_t)ch];
     for (int64_t i = 0; i < CH && pos < num_edges; ++i) {
       uint64_t s, d;
-      rmat_candidate(seed, (uint64_t)(ch * CH + i), scale, t1, t2, t3, &s, &d);
+      rmat_candidate(rkey, (uint64_t)(ch * CH + i), scale, t1, t2, t3, &s, &d);
       if (s < (uint64_t)num_nodes && d < (uint64_t)num_nodes) {
         if (relabel) {
           s = perm_apply(rp, s);
@@ -205,7 +205,7 @@ int synth_rmat_csr(int64_t num_nodes, int64_t num_edges, double a, double b, dou
         ++pos;
       }
     }
-  });
+  }, true);
 
   // Counting sort by source, then sort each row.
   std::vector<std::atomic<int64_t>> deg((size_t)num_nodes);
@@ -248,31 +248,37 @@ static inline uint16_t f32_to_f16(float f) {
 
 // Feature rows for nodes [u_begin, u_end): row u is written at
 // out + (u - u_begin) * stride_bytes.  dtype 0 = fp32, 1 = fp16.
-// dist 0 = N(0,1) (Box-Muller), 1 = U(-1,1).  Padding bytes between
-// row_bytes and the stride are zero.
+// dist 0 = N(0,1) (Box-Muller, two values per draw), 1 = U(-1,1).
+// Padding bytes between row_bytes and the stride are zero.
 void synth_features(int64_t u_begin, int64_t u_end, int32_t dim, int32_t dtype, int32_t dist,
                     int64_t stride_bytes, uint64_t seed, void* out) {
-  const int elem = dtype == 0 ? 4 : 2;
-  const int64_t row_bytes = (int64_t)dim * elem;
+  const int64_t row_bytes = (int64_t)dim * (dtype == 0 ? 4 : 2);
+  const uint64_t key = stream_key(seed, STREAM_FEAT);
   parallel_for(u_end - u_begin, [&](int64_t k) {
     const int64_t u = u_begin + k;
     char* row = (char*)out + k * stride_bytes;
-    for (int32_t j = 0; j < dim; ++j) {
-      uint64_t w = word64(seed, STREAM_FEAT, (uint64_t)u * (uint64_t)dim + (uint64_t)j);
-      double u1 = ((double)(w >> 11) + 0.5) * (1.0 / 9007199254740992.0);
-      float v;
+    for (int32_t j = 0; j < dim; j += 2) {
+      const uint64_t w = mix64(key + (uint64_t)u * (uint64_t)dim + (uint64_t)j);
+      const double u1 = ((double)(w >> 11) + 0.5) * (1.0 / 9007199254740992.0);
+      float v[2];
       if (dist == 0) {
-        uint64_t w2 = mix64(w ^ 0x5851F42D4C957F2DULL);
-        double u2 = (double)(w2 >> 11) * (1.0 / 9007199254740992.0);
-        v = (float)(std::sqrt(-2.0 * std::log(u1)) * std::cos(6.283185307179586 * u2));
+        const uint64_t w2 = mix64(w ^ 0x5851F42D4C957F2DULL);
+        const double u2 = (double)(w2 >> 11) * (1.0 / 9007199254740992.0);
+        const double r = std::sqrt(-2.0 * std::log(u1)), th = 6.283185307179586 * u2;
+        v[0] = (float)(r * std::cos(th));
+        v[1] = (float)(r * std::sin(th));
       } else {
-        v = (float)(2.0 * u1 - 1.0);
+        const uint64_t w2 = mix64(w ^ 0x5851F42D4C957F2DULL);
+        v[0] = (float)(2.0 * u1 - 1.0);
+        v[1] = (float)(2.0 * (((double)(w2 >> 11) + 0.5) * (1.0 / 9007199254740992.0)) - 1.0);
       }
-      if (dtype == 0) {
-        std::memcpy(row + (int64_t)j * 4, &v, 4);
-      } else {
-        uint16_t h = f32_to_f16(v);
-        std::memcpy(row + (int64_t)j * 2, &h, 2);
+      for (int t = 0; t < 2 && j + t < dim; ++t) {
+        if (dtype == 0) {
+          std::memcpy(row + (int64_t)(j + t) * 4, &v[t], 4);
+        } else {
+          const uint16_t h = f32_to_f16(v[t]);
+          std::memcpy(row + (int64_t)(j + t) * 2, &h, 2);
+        }
       }
     }
     if (stride_bytes > row_bytes) std::memset(row + row_bytes, 0, (size_t)(stride_bytes - row_bytes));

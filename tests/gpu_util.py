@@ -19,7 +19,8 @@ class World:
     """One workload instance on the GPU and its oracle counterpart."""
 
     def __init__(self, inst, W=None, n_hot=-1, local_owner=None, fanout=None, batch=None,
-                 device="cuda:0", shards=None, row_bytes=None, stride=None, cache_stride=None):
+                 device="cuda:0", shards=None, row_bytes=None, stride=None, cache_stride=None,
+                 tensors=None):
         wl = inst.wl
         self.inst = inst
         self.wl = wl
@@ -34,9 +35,12 @@ class World:
         self.dev = torch.device(device)
         self.P = wl.num_parts
         self.rs = inst.range_start
-        self.row_ptr_d = torch.from_numpy(inst.row_ptr).to(self.dev)
-        self.col_idx_d = torch.from_numpy(inst.col_idx).to(self.dev)
-        self.shards_d = [torch.from_numpy(s).to(self.dev) for s in self.shards]
+        if tensors is not None:        # (row_ptr_d, col_idx_d, shards_d) already placed
+            self.row_ptr_d, self.col_idx_d, self.shards_d = tensors
+        else:
+            self.row_ptr_d = torch.from_numpy(inst.row_ptr).to(self.dev)
+            self.col_idx_d = torch.from_numpy(inst.col_idx).to(self.dev)
+            self.shards_d = [torch.from_numpy(s).to(self.dev) for s in self.shards]
         rows = [s.shape[0] for s in self.shards]
         self.pipe = FetchPipeline(self.row_ptr_d, self.col_idx_d, self.P, wl.part_kind, self.local,
                                   self.rs, self.shards_d, rows, self.row_bytes, self.stride,

@@ -269,3 +269,58 @@ def test_wsweep_batch4096_w32_sampled_batches_and_invariants():
         assert gs["rows"] == n and gs["misses"] == 0 and gs["local"] + gs["hits"] == n
         total += n
     assert total == len(allN)
+
+
+@pytest.mark.timeout(1800)
+def test_papers_share_sampled_batches_and_invariants():
+    log("papers_share: 111M nodes, 1.6B edges, fp16x128, remote shards in pinned host memory, "
+        "W=16 window 0: sampled batches vs oracle, hot set, staged and gathered rows")
+    import torch as T
+    from oracle import ggref
+    inst, rp_d, ci_d, sh_d = synth.torch_instance("papers_share", "cuda:0")
+    wl = inst.wl
+    assert all(not sh_d[m].is_cuda for m in (1, 2, 3)) and sh_d[0].is_cuda
+    w = world(inst, tensors=(rp_d, ci_d, sh_d))
+    p = w.pipe
+    seeds, so, b0 = w.window_inputs(0)
+    log(f"papers_share: running window 0 ({len(seeds)} seeds)")
+    Wk = p.window(T.from_numpy(seeds).to(w.dev), so, b0)
+    T.cuda.synchronize()
+    assert p.read_status() == 0
+    L = len(wl.fanout)
+    fids, foff, nids, noff = p.sample_outputs(Wk)
+    rs = inst.range_start
+    for b in (0, 9, 15):
+        log(f"papers_share: oracle on batch {b}")
+        s = seeds[so[b]:so[b + 1]]
+        f1, o1, n1, no1 = ggref.sample_window(inst.row_ptr, inst.col_idx, s,
+                                              np.array([0, len(s)], np.int64), wl.fanout, 0, 0,
+                                              b0 + b)
+        for l in range(L + 1):
+            assert np.array_equal(fids[foff[l * Wk + b]:foff[l * Wk + b + 1]], f1[o1[l]:o1[l + 1]])
+        for l in range(L):
+            assert np.array_equal(nids[noff[l * Wk + b]:noff[l * Wk + b + 1]], n1[no1[l]:no1[l + 1]])
+    allN = fids[foff[L * Wk]:foff[(L + 1) * Wk]]
+    remote = allN[(allN < rs[0]) | (allN >= rs[1])]
+    uniq, cnt = np.unique(remote, return_counts=True)
+    hot, freq, hc, bucket, owner_off = p.hot_outputs()
+    assert np.array_equal(hot, uniq) and np.array_equal(freq, cnt)
+    assert np.array_equal(bucket, hot)
+    st = p.stage_stats_dict()
+    assert st["requests"] == [0, 1, 1, 1] and st["rows_total"] == len(hot)
+    rng = np.random.default_rng(3)
+    rb = wl.row_bytes
+    for s_ in rng.choice(len(hot), 3000, replace=False).tolist():
+        u = int(bucket[s_])
+        m = int(np.searchsorted(rs, u, side="right") - 1)
+        assert np.array_equal(p.cache[s_, :rb].cpu().numpy(), inst.shards[m][u - rs[m], :rb])
+    base = int(foff[L * Wk])
+    rows = rng.choice(len(allN), 5000, replace=False)
+    got = p.win_out[T.from_numpy(rows).to(w.dev)].cpu().numpy()
+    for r_, g in zip(rows.tolist(), got):
+        u = int(fids[base + r_])
+        m = int(np.searchsorted(rs, u, side="right") - 1)
+        assert np.array_equal(g[:rb], inst.shards[m][u - rs[m], :rb])
+    for b in range(Wk):
+        gs = p.gather_stats_dict(b)
+        assert gs["misses"] == 0 and gs["local"] + gs["hits"] == gs["rows"]
