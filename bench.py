@@ -25,6 +25,7 @@ import time
 ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
+PCIE5_X16_GBS = 63.0   # 32 GT/s x 16 lanes x 128/130 encoding / 8 bits
 HBM_PEAK_GBS = 8000.0
 PROFILES = os.path.join(ROOT, "profiles")
 GATHER_SOURCES = ["paper_2606_02916_amd/csrc/gather.hip", "paper_2606_02916_amd/csrc/gg_dev.hpp"]
@@ -97,6 +98,26 @@ def summarize(args):
         for n, c, a, mn, mx, sm in rows:
             out.append(f"{_short(n):40s} {c:6d} {a / 1e3:9.2f} {mn / 1e3:9.2f} {mx / 1e3:9.2f} "
                        f"{sm / 1e6:9.3f} {100 * sm / tot:5.1f}%")
+        if args.phases:
+            # the gather call's kernels per launch, split into the bench's
+            # phases (pre-pass, warm-up, timed steps) by dispatch order
+            n_pre, n_warm, n_timed = (int(x) for x in args.phases.split(","))
+            per = {}
+            for part in ("k_gather_zero", "k_gather_rows", "k_gather_finish"):
+                per[part] = [r[0] for r in db.execute(
+                    "select end-start from kernels where name like ? order by start",
+                    (f"%{part}%",)).fetchall()]
+            n = len(per["k_gather_rows"])
+            calls = [sum(per[p][i] for p in per if i < len(per[p])) for i in range(n)]
+            out.append("")
+            out.append("# gg_gather_batch (zero + rows + finish) by bench phase, microseconds")
+            for label, lo, hi in (("pre-pass, one window at a time", 0, n_pre),
+                                  ("timed steps", n - n_timed, n)):
+                v = calls[lo:hi]
+                r = per["k_gather_rows"][lo:hi]
+                if v:
+                    out.append(f"{label:34s} launches {len(v):3d}  call avg {sum(v) / len(v) / 1e3:8.2f}"
+                               f"  k_gather_rows avg {sum(r) / len(r) / 1e3:8.2f}")
         with open(os.path.join(PROFILES, f"kernels_{wl}.txt"), "w") as f:
             f.write("\n".join(out) + "\n")
     if args.fetch_db and args.write_db:
@@ -139,10 +160,18 @@ def main():
     ap.add_argument("--cpu-seconds", type=float, default=10.0,
                     help="minimum oracle time for the CPU baseline sample")
     ap.add_argument("--per-batch", action="store_true",
-                    help="one gather launch per batch instead of one per window")
+                    help="one gather launch per batch instead of one per window (sequential "
+                         "driver only)")
+    ap.add_argument("--pipeline", default="lookahead", choices=["sequential", "delta", "lookahead"],
+                    help="sequential: the five calls per window on one stream, full restage; "
+                         "delta: the same with delta staging from the previous cache; "
+                         "lookahead: delta staging, window k+1 built on a second stream while "
+                         "window k is gathered")
     ap.add_argument("--copy-calibration-mib", type=int, default=0,
                     help="after the timed steps, copy this many MiB device to device three "
                          "times (a plain copy of known size for scaling HBM counters)")
+    ap.add_argument("--sets", type=int, default=2,
+                    help="buffer sets of the look-ahead pipeline (how far building may run ahead)")
     ap.add_argument("--wsweep", default=None,
                     help="comma-separated window sizes: run one epoch per W and report, per W, "
                          "hot-set size, bulk bytes per owner, rebuild delta and gather rate")
@@ -152,6 +181,9 @@ def main():
     ap.add_argument("--fetch-db", default=None)
     ap.add_argument("--write-db", default=None)
     ap.add_argument("--summary-command", default="")
+    ap.add_argument("--phases", default=None,
+                    help="with --trace-db: gather launches of the pre-pass, warm-up and timed "
+                         "steps, e.g. 12,1,12, to average the gather per phase")
     args = ap.parse_args()
     if args.summarize:
         summarize(args)
@@ -167,10 +199,12 @@ def main():
     import torch
 
     import synth
-    from paper_2606_02916_amd import FetchPipeline
+    from paper_2606_02916_amd import FetchPipeline, LookaheadPipeline
 
     dev = torch.device("cuda:0")
     wl = synth.WORKLOADS[args.config]
+    if args.per_batch and args.pipeline != "sequential":
+        ap.error("--per-batch needs --pipeline sequential")
     if args.wsweep:
         return wsweep(args, wl)
     W = args.W or wl.W
@@ -180,9 +214,14 @@ def main():
     P, L = wl.num_parts, len(wl.fanout)
     seeds_d = torch.from_numpy(inst.seeds).to(dev)
     pcie = pcie_h2d_gbps(dev) if wl.remote_on_host else None
-    pipe = FetchPipeline(row_ptr_d, col_idx_d, P, wl.part_kind, wl.local_owner, inst.range_start,
-                         shards_d, [s.shape[0] for s in inst.shards], wl.row_bytes, wl.row_stride,
-                         W, wl.fanout, wl.batch_size, device=dev)
+    pargs = (row_ptr_d, col_idx_d, P, wl.part_kind, wl.local_owner, inst.range_start, shards_d,
+             [s.shape[0] for s in inst.shards], wl.row_bytes, wl.row_stride, W, wl.fanout,
+             wl.batch_size)
+    look = args.pipeline == "lookahead"
+    if look:
+        pipe = LookaheadPipeline(*pargs, device=dev, nsets=args.sets)
+    else:
+        pipe = FetchPipeline(*pargs, device=dev, delta=args.pipeline == "delta")
     boff = inst.batch_off
     nwin = synth.n_windows(boff, W)
     wins = []
@@ -191,24 +230,37 @@ def main():
         so = boff[b0:b1 + 1] - boff[b0]
         wins.append((seeds_d[boff[b0]:boff[b1]], so, b0))
     torch.cuda.synchronize()
-    log(f"uploaded; {nwin} windows of W={W}; out_cap={pipe.out_cap} hot_cap={pipe.hot_cap}")
+    log(f"uploaded; {nwin} windows of W={W}; out_cap={pipe.geo.out_cap} "
+        f"hot_cap={pipe.geo.hot_cap}; driver {args.pipeline}")
+
+    def run_window(s, so, b0, events=None, gevs=None):
+        """Enqueues one window; returns (Wk, object holding its statistics)."""
+        if look:
+            return pipe.window(s, so, b0, events=events,
+                               gather_events=gevs[0] if gevs is not None else None)
+        Wk = pipe.window(s, so, b0, events=events, gather_events=gevs, per_batch=pb)
+        return Wk, pipe
 
     # Pass over every window once: per-window row counts for the metric and
     # per-batch local/remote counts for the gather's algorithmic bytes.
     rb = wl.row_bytes
+    mk = lambda: torch.cuda.Event(enable_timing=True)  # noqa: E731
     rows_w, gbytes_w, hot_w, sbytes_w, req_w, hbytes_w = [], [], [], [], [], []
     pb = args.per_batch
+    iso_ms = []      # gather launches of the pre-pass, each with the chip to itself
     for k, (s, so, b0) in enumerate(wins):
-        Wk = pipe.window(s, so, b0, per_batch=pb)
+        ge = [(mk(), mk()) for _ in range(W if pb else 1)]
+        Wk, sb = run_window(s, so, b0, gevs=ge)
         torch.cuda.synchronize()
+        iso_ms += [a.elapsed_time(b) for a, b in ge[:Wk if pb else 1]]
         st = pipe.read_status()
         if st != 0:
             raise RuntimeError(f"device status {st} in window {k}")
-        g = [pipe.gather_stats_dict(b) for b in range(Wk)]
+        g = [sb.gather_stats_dict(b) for b in range(Wk)]
         rows_w.append(sum(x["rows"] for x in g))
         gb = [x["rows"] * (2 * rb + 4) + (x["hits"] + x["misses"]) * 4 for x in g]
         gbytes_w.append(gb if pb else [sum(gb)])
-        ss = pipe.stage_stats_dict()
+        ss = sb.stage_stats_dict()
         hot_w.append(ss["rows_total"])
         sbytes_w.append(ss["rows_total"] * (2 * rb + 8) + ss["invalidated"] * 4)
         req_w.append(ss["requests_total"])
@@ -217,19 +269,18 @@ def main():
 
     for i in range(args.warmup):
         s, so, b0 = wins[i % nwin]
-        pipe.window(s, so, b0, per_batch=pb)
+        run_window(s, so, b0)
     torch.cuda.synchronize()
 
     K = args.steps
-    mk = lambda: torch.cuda.Event(enable_timing=True)  # noqa: E731
-    evs = [[mk() for _ in range(6)] for _ in range(K)]
+    evs = [[mk() for _ in range(5 if look else 6)] for _ in range(K)]
     gevs = [[(mk(), mk()) for _ in range(W if pb else 1)] for _ in range(K)]
     order = [(args.warmup + i) % nwin for i in range(K)]
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     for i, k in enumerate(order):
         s, so, b0 = wins[k]
-        pipe.window(s, so, b0, events=evs[i], gather_events=gevs[i], per_batch=pb)
+        run_window(s, so, b0, events=evs[i], gevs=gevs[i])
     torch.cuda.synchronize()
     t1 = time.perf_counter()
     if pipe.read_status() != 0:
@@ -238,23 +289,46 @@ def main():
     rows = sum(rows_w[k] for k in order)
     value = rows / elapsed
 
+    def gather_ms(gevs, i, b=None):
+        """Duration of gather launch b of step i (all launches when b is
+        None).  The look-ahead driver's start event marks the end of
+        staging; its gather begins at the later of that and the previous
+        gather's end on the same stream."""
+        if b is None:
+            return sum(gather_ms(gevs, i, j) for j in range(len(gevs[i])))
+        s, e = gevs[i][b]
+        t = s.elapsed_time(e)
+        if look and i > 0:
+            t = min(t, gevs[i - 1][-1][1].elapsed_time(e))
+        return t
+
     g_ms, g_bytes, n_launch = 0.0, 0, 0
     stage_ms = {"sample": [], "hotset": [], "bucket": [], "stage": [], "gathers": []}
     st_ms, st_bytes, st_host_bytes = 0.0, 0, 0
     for i, k in enumerate(order):
         e = evs[i]
-        for name, (a, b) in zip(stage_ms, [(0, 1), (1, 2), (2, 3), (3, 4), (4, 5)]):
+        for name, (a, b) in zip(stage_ms, [(0, 1), (1, 2), (2, 3)]):
             stage_ms[name].append(e[a].elapsed_time(e[b]))
-        st_ms += e[3].elapsed_time(e[4])
+        # staging starts once its window is built and the previous window's
+        # staging (same stream) has ended
+        t_st = e[3].elapsed_time(e[4])
+        if look and i > 0:
+            t_st = min(t_st, evs[i - 1][4].elapsed_time(e[4]))
+        stage_ms["stage"].append(t_st)
+        stage_ms["gathers"].append(gather_ms(gevs, i))
+        st_ms += t_st
         st_bytes += sbytes_w[k]
         st_host_bytes += hbytes_w[k]
         for b in range(len(gbytes_w[k])):
-            g_ms += gevs[i][b][0].elapsed_time(gevs[i][b][1])
+            g_ms += gather_ms(gevs, i, b)
             g_bytes += gbytes_w[k][b]
             n_launch += 1
     avg_ms = g_ms / n_launch
     avg_bytes = g_bytes / n_launch
     achieved = avg_bytes / (avg_ms * 1e-3) / 1e9
+    all_gb = [x for v in gbytes_w for x in v]
+    iso_avg_ms = float(np.mean(iso_ms))
+    iso_achieved = float(np.mean(all_gb)) / (iso_avg_ms * 1e-3) / 1e9
     stage_gbs = st_bytes / (st_ms * 1e-3) / 1e9
 
     if args.copy_calibration_mib:
@@ -289,22 +363,31 @@ def main():
                    "features": f"{wl.feat_dtype}x{wl.feat_dim}", "row_bytes": rb,
                    "fanout": list(wl.fanout), "batch": wl.batch_size, "W": W,
                    "partitions": P, "local_owner": wl.local_owner, "windows_per_epoch": nwin,
-                   "gather_launch": "per batch" if pb else "per window"},
+                   "gather_launch": "per batch" if pb else "per window",
+                   "driver": args.pipeline + (f" ({args.sets} buffer sets)" if look else "")},
         "roofline": {"bound": "hbm", "kernel": "gg_gather_batch",
                      "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
                      "frac": round(achieved / HBM_PEAK_GBS, 4),
                      "traffic": measured_traffic(args.config, pb),
-                     "bytes_per_launch": int(avg_bytes), "avg_launch_us": round(avg_ms * 1e3, 2)},
+                     "bytes_per_launch": int(avg_bytes), "avg_launch_us": round(avg_ms * 1e3, 2),
+                     "overlapped": look,
+                     "isolated": {"achieved": round(iso_achieved, 1),
+                                  "frac": round(iso_achieved / HBM_PEAK_GBS, 4),
+                                  "avg_launch_us": round(iso_avg_ms * 1e3, 2),
+                                  "launches": len(iso_ms),
+                                  "note": "pre-pass over every window, one window at a time"}},
         "stage_roofline": ({"kernel": "gg_stage_bulk", "bound": "hbm",
                             "achieved": round(stage_gbs, 1),
                             "frac": round(stage_gbs / HBM_PEAK_GBS, 4), "unit": "GB/s"}
                            if pcie is None else
                            {"kernel": "gg_stage_bulk", "bound": "pcie",
                             "achieved": round(st_host_bytes / (st_ms * 1e-3) / 1e9, 2),
-                            "peak": round(pcie, 2), "unit": "GB/s",
-                            "frac": round(st_host_bytes / (st_ms * 1e-3) / 1e9 / pcie, 4),
-                            "note": "host bytes read by the staging kernel over PCIe vs a "
-                                    "measured pinned-to-device copy of 1 GiB"}),
+                            "peak": PCIE5_X16_GBS, "unit": "GB/s",
+                            "frac": round(st_host_bytes / (st_ms * 1e-3) / 1e9 / PCIE5_X16_GBS, 4),
+                            "dma_copy_gbps": round(pcie, 2),
+                            "note": "host bytes the staging kernel reads over PCIe; peak is the "
+                                    "PCIe 5.0 x16 link rate, dma_copy_gbps a measured "
+                                    "pinned-to-device copy of 1 GiB"}),
         "stage_ms_median": {k: round(float(np.median(v)), 4) for k, v in stage_ms.items()},
         "rows_per_window": int(np.mean(rows_w)),
         "hot_set_rows_per_window": int(np.mean(hot_w)),

@@ -132,14 +132,14 @@ typedef struct gg_wsample {
 
 /* Per-window staging statistics (device). */
 typedef struct gg_stage_stats {
-  int64_t rows_total;
+  int64_t rows_total;        /* cache rows filled */
   int64_t requests_total;
-  int64_t invalidated;       /* previous-window entries cleared */
-  int64_t pad_;
-  int64_t requests[GG_MAX_PARTS];   /* 1 per non-empty owner bucket */
-  int64_t rows[GG_MAX_PARTS];
+  int64_t invalidated;       /* remap entries cleared */
+  int64_t retained;          /* rows copied from the source cache */
+  int64_t requests[GG_MAX_PARTS];   /* 1 per owner with rows requested */
+  int64_t rows[GG_MAX_PARTS];       /* rows requested from owner m */
   int64_t bytes[GG_MAX_PARTS];
-  int64_t delta_rows[GG_MAX_PARTS]; /* |bucket_m(H_k) \ H_{k-1}|, Sec. IV-A rebuild delta */
+  int64_t delta_rows[GG_MAX_PARTS]; /* |bucket_m(H_k) \ C_{k-1}|, Sec. IV-A rebuild delta */
 } gg_stage_stats_t;
 
 /* Per-batch gather statistics (device). */
@@ -208,20 +208,27 @@ int gg_bucket_by_owner(const int32_t* hot_ids_d, const int64_t* hot_count_d, int
                        const gg_part_t* part, int32_t* bucket_ids_d, int64_t* owner_off_d,
                        int32_t* status_d, void* ws, size_t ws_bytes, hipStream_t stream);
 
-/* Stages the window cache (Sec. IV-C; Algorithm 1 WarmCache): clears the
- * previous window's remap entries slot_of_d[prev_ids_d[i]] = -1 for
- * i < prev_count_d[0] (both may be NULL), then for every owner with a
- * non-empty bucket issues one bulk copy of its rows into cache slots
- * owner_off_d[m] .. owner_off_d[m+1] (slot s at cache_d + s * cache_stride)
- * and sets slot_of_d[u] = s.  slot_of_d has num_nodes entries, -1 where a
- * node is not cached; the caller sets it to -1 once before the first
- * window.  At most cap bucket entries and cache_rows slots are used.
- * stats_d->delta_rows counts the staged rows absent from the previous
- * window's cache (the rebuild delta); every hot row is copied. */
+/* Stages the window cache (Sec. IV-C; Algorithm 1 WarmCache).  The rows of
+ * the bucketed hot set (owner_off_d[P] <= cap entries of bucket_ids_d) go
+ * to cache slots in bucket order (slot s at cache_d + s * cache_stride,
+ * at most cache_rows) and slot_of_d[u] = s.  slot_of_d has num_nodes
+ * entries, -1 where a node is not cached; the caller sets it to -1 once,
+ * and every call first clears the entries clear_ids_d[0 .. clear_count_d[0])
+ * (both may be NULL), normally the ids the previous call staged.
+ * Without a source cache (src_cache_d == NULL) every row is requested from
+ * its owner: one bulk copy per owner with a non-empty bucket.  With one
+ * (same stride, at least cache_rows rows; its remap src_slot_of_d may be
+ * slot_of_d itself, read before the clearing), a row whose node the source
+ * remap holds is copied from the source cache in device memory and only
+ * the rebuild delta Delta_{k,m} = (H_k in owner m) \ C_{k-1} of Sec. IV-A is
+ * requested from the owners, one request per owner whose delta is
+ * non-empty (the indicator of Eq. (1)).  stats_d->delta_rows counts the
+ * rows of each bucket absent from the source (else the current) remap. */
 int gg_stage_bulk(const int32_t* bucket_ids_d, const int64_t* owner_off_d, int64_t cap,
                   const gg_part_t* part, const gg_feat_t* feat, void* cache_d,
                   int64_t cache_stride, int64_t cache_rows, int32_t* slot_of_d,
-                  const int32_t* prev_ids_d, const int64_t* prev_count_d,
+                  const int32_t* clear_ids_d, const int64_t* clear_count_d,
+                  const void* src_cache_d, const int32_t* src_slot_of_d,
                   gg_stage_stats_t* stats_d, int32_t* status_d, void* ws, size_t ws_bytes,
                   hipStream_t stream);
 

@@ -296,40 +296,54 @@ int ggref_bucket_by_owner(const int32_t* hot_ids, int64_t hot_count, const ggref
 }
 
 // Bulk staging of the window cache (Sec. IV-C; Algorithm 1 WarmCache).
-// The previous window's remap entries are cleared first; then, for every
-// owner with a non-empty bucket, one request copies that owner's rows into
-// the contiguous cache slots of its bucket and points slot_of at them.
-// delta_rows[m] = |bucket_m(H_k) \ H_{k-1}|, the rebuild delta of Sec. IV-A
-// (reported; the whole hot set is restaged).
+// The node's slot in the cache it came from is read first (the source remap
+// may be slot_of itself); then the listed remap entries are cleared; then,
+// for every owner, the bucket's rows are filled in bucket order.  Without a
+// source cache every row is one owner's bulk request; with one, rows the
+// source cache holds are copied from it and only the rebuild delta of
+// Sec. IV-A, Delta_{k,m} = (H_k in owner m) minus C_{k-1}, is requested,
+// one request per owner whose delta is non-empty (Eq. (1) indicator).
+// delta_rows[m] always counts the rows of bucket m absent from the source
+// (or, without one, from the current) remap.
 int ggref_stage_bulk(const int32_t* bucket_ids, const int64_t* owner_off,
                      const ggref_part_t* part, const ggref_feat_t* feat, void* cache,
                      int64_t cache_stride, int64_t cache_rows, int32_t* slot_of,
-                     const int32_t* prev_ids, int64_t prev_count, ggref_stage_stats_t* stats) {
+                     const int32_t* clear_ids, int64_t clear_count, const void* src_cache,
+                     const int32_t* src_slot_of, ggref_stage_stats_t* stats) {
   if (!part_ok(part) || !feat || feat->num_parts != part->num_parts) return GGREF_ERR_ARG;
   const int32_t P = part->num_parts;
   std::memset(stats, 0, sizeof(*stats));
-  for (int64_t i = 0; i < prev_count; ++i) slot_of[prev_ids[i]] = -1;
-  stats->invalidated = prev_count;
   const int64_t total = owner_off[P];
   if (total > cache_rows) return GGREF_ERR_CAPACITY;
-  std::set<int32_t> prev(prev_ids, prev_ids + prev_count);
+  const int32_t* before = src_slot_of ? src_slot_of : slot_of;
+  std::vector<int32_t> old_slot((size_t)total);
+  for (int64_t s = 0; s < total; ++s) old_slot[(size_t)s] = before[bucket_ids[s]];
+  for (int64_t i = 0; i < clear_count; ++i) slot_of[clear_ids[i]] = -1;
+  stats->invalidated = clear_count;
   for (int32_t m = 0; m < P; ++m) {
-    const int64_t n = owner_off[m + 1] - owner_off[m];
-    stats->rows[m] = n;
-    stats->bytes[m] = n * feat->row_bytes;
-    stats->requests[m] = n > 0 ? 1 : 0;
-    stats->rows_total += n;
-    stats->requests_total += stats->requests[m];
     for (int64_t s = owner_off[m]; s < owner_off[m + 1]; ++s) {
       const int32_t u = bucket_ids[s];
       if (ggref_owner(part, u) != m) return GGREF_ERR_RANGE;
       const int64_t r = ggref_row(part, u);
       if (r < 0 || r >= feat->shard_rows[m]) return GGREF_ERR_RANGE;
-      std::memcpy((char*)cache + s * cache_stride, src_row(feat, m, r), (size_t)feat->row_bytes);
+      const int32_t old = old_slot[(size_t)s];
+      if (old < 0) ++stats->delta_rows[m];
+      char* dst = (char*)cache + s * cache_stride;
+      if (src_cache && old >= 0) {
+        std::memcpy(dst, (const char*)src_cache + (int64_t)old * cache_stride,
+                    (size_t)feat->row_bytes);
+        ++stats->retained;
+      } else {
+        std::memcpy(dst, src_row(feat, m, r), (size_t)feat->row_bytes);
+        ++stats->rows[m];
+      }
       slot_of[u] = (int32_t)s;
-      if (!prev.count(u)) ++stats->delta_rows[m];
     }
+    stats->bytes[m] = stats->rows[m] * feat->row_bytes;
+    stats->requests[m] = stats->rows[m] > 0 ? 1 : 0;
+    stats->requests_total += stats->requests[m];
   }
+  stats->rows_total = total;
   return GGREF_OK;
 }
 

@@ -72,7 +72,7 @@ typedef struct ggref_stage_stats {
   int64_t rows_total;
   int64_t requests_total;
   int64_t invalidated;
-  int64_t pad_;
+  int64_t retained; /* rows copied from the source cache instead of an owner */
   int64_t requests[GGREF_MAX_PARTS];
   int64_t rows[GGREF_MAX_PARTS];
   int64_t bytes[GGREF_MAX_PARTS];
@@ -132,13 +132,21 @@ int ggref_build_hotset(const int32_t* frontier_ids, const int64_t* frontier_off,
 int ggref_bucket_by_owner(const int32_t* hot_ids, int64_t hot_count, const ggref_part_t* part,
                           int32_t* bucket_ids, int64_t* owner_off);
 
-/* One bulk request per non-empty owner bucket (Sec. IV-C): copies the rows
- * into cache slots in bucket order and points slot_of at them, after
- * clearing the previous window's entries prev_ids[0 .. prev_count). */
+/* Window cache rebuild (Sec. IV-A rebuild events, Eq. (1); Sec. IV-C;
+ * Algorithm 1 WarmCache).  The rows of the bucketed hot set go to cache
+ * slots in bucket order and slot_of points at them, after the entries
+ * clear_ids[0 .. clear_count) of slot_of are set to -1.  Without a source
+ * cache (src_cache == NULL) every row is requested from its owner.  With
+ * one, a row whose node the source remap src_slot_of (which may be slot_of
+ * itself, read before clearing) holds is copied from the source cache, and
+ * only the rebuild delta Delta_{k,m} = (H_k in owner m) \ C_{k-1} is
+ * requested from the owners: one request per owner whose delta is
+ * non-empty. */
 int ggref_stage_bulk(const int32_t* bucket_ids, const int64_t* owner_off,
                      const ggref_part_t* part, const ggref_feat_t* feat, void* cache,
                      int64_t cache_stride, int64_t cache_rows, int32_t* slot_of,
-                     const int32_t* prev_ids, int64_t prev_count, ggref_stage_stats_t* stats);
+                     const int32_t* clear_ids, int64_t clear_count, const void* src_cache,
+                     const int32_t* src_slot_of, ggref_stage_stats_t* stats);
 
 /* Assembles one batch's input features (Algorithm 1, cache lookup, residual
  * misses, on-demand fetch): out row i = feature row of in_ids[i]. */

@@ -38,7 +38,7 @@ class Feat(C.Structure):
 
 class StageStats(C.Structure):
     _fields_ = [("rows_total", C.c_int64), ("requests_total", C.c_int64),
-                ("invalidated", C.c_int64), ("pad_", C.c_int64),
+                ("invalidated", C.c_int64), ("retained", C.c_int64),
                 ("requests", C.c_int64 * MAX_PARTS), ("rows", C.c_int64 * MAX_PARTS),
                 ("bytes", C.c_int64 * MAX_PARTS), ("delta_rows", C.c_int64 * MAX_PARTS)]
 
@@ -77,7 +77,7 @@ def lib():
         L.ggref_build_hotset.restype = C.c_int
         L.ggref_bucket_by_owner.argtypes = [P, i64, P, P, P]
         L.ggref_bucket_by_owner.restype = C.c_int
-        L.ggref_stage_bulk.argtypes = [P, P, P, P, P, i64, i64, P, P, i64, P]
+        L.ggref_stage_bulk.argtypes = [P, P, P, P, P, i64, i64, P, P, i64, P, P, P]
         L.ggref_stage_bulk.restype = C.c_int
         L.ggref_gather_batch.argtypes = [P, i64, P, P, P, i64, i64, P, P, i64, P]
         L.ggref_gather_batch.restype = C.c_int
@@ -209,8 +209,11 @@ def bucket_by_owner(hot_ids, part):
     return out[:hot_ids.shape[0]], off
 
 
-def stage_bulk(bucket_ids, owner_off, part, feat, cache, cache_stride, slot_of, prev_ids=None):
-    """cache: uint8 array (rows x cache_stride); slot_of: int32[N], updated in place."""
+def stage_bulk(bucket_ids, owner_off, part, feat, cache, cache_stride, slot_of, prev_ids=None,
+               src_cache=None, src_slot_of=None):
+    """cache: uint8 array (rows x cache_stride); slot_of: int32[N], updated
+    in place.  prev_ids: remap entries to clear.  src_cache / src_slot_of:
+    the cache rows may be taken from (delta staging)."""
     st = StageStats()
     bucket_ids = np.ascontiguousarray(bucket_ids, dtype=np.int32)
     owner_off = np.ascontiguousarray(owner_off, dtype=np.int64)
@@ -218,7 +221,8 @@ def stage_bulk(bucket_ids, owner_off, part, feat, cache, cache_stride, slot_of, 
     npre = 0 if prev is None else prev.shape[0]
     _check(lib().ggref_stage_bulk(_p(bucket_ids), _p(owner_off), C.byref(part), C.byref(feat),
                                   _p(cache), cache_stride, cache.shape[0], _p(slot_of), _p(prev),
-                                  npre, C.byref(st)), "ggref_stage_bulk")
+                                  npre, _p(src_cache), _p(src_slot_of), C.byref(st)),
+           "ggref_stage_bulk")
     return stats_dict(st, part.num_parts)
 
 

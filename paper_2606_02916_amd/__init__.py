@@ -5,4 +5,4 @@ buffer set and call sequence of one window.  Importing the package loads the
 HIP library and fails loudly if it is not built.
 """
 from . import gg  # noqa: F401
-from .window import FetchPipeline  # noqa: F401
+from .window import FetchPipeline, LookaheadPipeline  # noqa: F401

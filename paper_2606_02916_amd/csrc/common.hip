@@ -66,6 +66,31 @@ int pack_feat(const gg_feat_t* feat, const gg_part_t* part, KFeat* out) {
   return GG_OK;
 }
 
+bool env_flag(const char* name, bool dflt) {
+  const char* v = getenv(name);
+  if (!v || !*v) return dflt;
+  return strcmp(v, "0") != 0;
+}
+
+int env_int(const char* name, int dflt) {
+  const char* v = getenv(name);
+  return (v && *v) ? atoi(v) : dflt;
+}
+
+int host_shards(const KFeat& f) {
+  int n = 0;
+  for (int m = 0; m < f.P; ++m) {
+    if (f.rows[m] == 0) continue;
+    hipPointerAttribute_t at;
+    if (hipPointerGetAttributes(&at, f.shard[m]) != hipSuccess) {
+      (void)hipGetLastError();   // not known to the runtime: plain host memory
+      continue;
+    }
+    if (at.type == hipMemoryTypeHost) ++n;
+  }
+  return n;
+}
+
 CopyGeom copy_geom(int32_t row_bytes, int vb) {
   CopyGeom g;
   g.row_bytes = row_bytes;

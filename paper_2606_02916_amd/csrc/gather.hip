@@ -206,17 +206,6 @@ __global__ void __launch_bounds__(kBlock) k_gather_finish(const int64_t* bounds,
   if (st) set_status(status, st);
 }
 
-bool env_flag(const char* name, bool dflt) {
-  const char* v = getenv(name);
-  if (!v || !*v) return dflt;
-  return strcmp(v, "0") != 0;
-}
-
-int env_int(const char* name, int dflt) {
-  const char* v = getenv(name);
-  return (v && *v) ? atoi(v) : dflt;
-}
-
 struct GatherWs {
   int64_t* miss_count;
   int32_t* blk_stat;

@@ -47,6 +47,14 @@ CopyGeom copy_geom(int32_t row_bytes, int vb);
 
 inline bool aligned16(const void* p) { return ((uintptr_t)p & 15u) == 0; }
 
+// Tuning switches read once from the environment: a flag is on unless "0".
+bool env_flag(const char* name, bool dflt);
+int env_int(const char* name, int dflt);
+
+// Number of shards with rows whose memory is pinned host memory (read by
+// the kernels over PCIe rather than from HBM).
+int host_shards(const KFeat& f);
+
 // Bump allocator over the caller's workspace.
 struct Carve {
   char* base;

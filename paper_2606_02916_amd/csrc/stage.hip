@@ -27,12 +27,13 @@ __device__ __forceinline__ int64_t stage_n(const int64_t* owner_off, int32_t P, 
   return n < a.cache_rows ? n : a.cache_rows;
 }
 
-// Rebuild delta: staged rows whose node is not in the previous window's
-// cache (slot_of still describes that cache here).  Every block writes its
-// per-owner counts to dcnt[block * P + m].
+// Old slots and the rebuild delta: old_slot[s] = the slot the source remap
+// (or, without a source cache, the current remap before clearing) gives
+// the node of bucket entry s; rows with none are the delta.  Every block
+// writes its per-owner delta counts to dcnt[block * P + m].
 __global__ void __launch_bounds__(kBlock) k_stage_delta(const int32_t* bucket, const int64_t* owner_off,
-                                                        KPart part, StageArgs a, const int32_t* slot_of,
-                                                        int32_t* dcnt) {
+                                                        KPart part, StageArgs a, const int32_t* before,
+                                                        int32_t* old_slot, int32_t* dcnt) {
   __shared__ int32_t hist[GG_MAX_PARTS];
   __shared__ int64_t s_start[GG_MAX_PARTS + 1];
   for (int t = threadIdx.x; t < GG_MAX_PARTS; t += blockDim.x) hist[t] = 0;
@@ -46,10 +47,15 @@ __global__ void __launch_bounds__(kBlock) k_stage_delta(const int32_t* bucket, c
     int32_t m = 0;
     if (s < n) {
       const int32_t u = bucket[s];
-      if (u >= 0 && (int64_t)u < part.N && slot_of[u] < 0) {
-        fresh = true;
-        m = owner_of(part, s_start, u);
+      int32_t old = -1;
+      if (u >= 0 && (int64_t)u < part.N) {
+        old = before[u];
+        if (old < 0) {
+          fresh = true;
+          m = owner_of(part, s_start, u);
+        }
       }
+      old_slot[s] = old;
     }
     wave_hist_add(hist, fresh, m);
   }
@@ -71,6 +77,7 @@ template <int VB, bool NT>
 __global__ void __launch_bounds__(kBlock) k_stage_rows(const int32_t* bucket, const int64_t* owner_off,
                                                        KPart part, KFeat feat, StageArgs a,
                                                        char* cache, int32_t* slot_of,
+                                                       const char* src_cache, const int32_t* old_slot,
                                                        int32_t* status) {
   __shared__ int64_t s_start[GG_MAX_PARTS + 1];
   for (int t = threadIdx.x; t <= GG_MAX_PARTS; t += blockDim.x) s_start[t] = part.start[t];
@@ -89,13 +96,20 @@ __global__ void __launch_bounds__(kBlock) k_stage_rows(const int32_t* bucket, co
       if (u < 0 || (int64_t)u >= part.N) {
         st |= GG_DEV_BAD_ID;
       } else {
-        const int32_t m = owner_of(part, s_start, u);
-        const int64_t r = row_of(part, s_start, u, m);
-        if (r >= feat.rows[m]) {
-          st |= GG_DEV_BAD_ROW;
-        } else {
-          src = feat.shard[m] + r * feat.stride[m];
+        const int32_t old = src_cache ? old_slot[s] : -1;
+        if (old >= 0 && (int64_t)old < a.cache_rows) {
+          src = src_cache + (int64_t)old * a.cache_stride;   // retained: device-local copy
           slot_of[u] = (int32_t)s;
+        } else {
+          if (old >= 0) st |= GG_DEV_BAD_ROW;
+          const int32_t m = owner_of(part, s_start, u);
+          const int64_t r = row_of(part, s_start, u, m);
+          if (r >= feat.rows[m]) {
+            st |= GG_DEV_BAD_ROW;
+          } else {
+            src = feat.shard[m] + r * feat.stride[m];          // requested from owner m
+            slot_of[u] = (int32_t)s;
+          }
         }
       }
     }
@@ -108,7 +122,8 @@ __global__ void __launch_bounds__(kBlock) k_stage_rows(const int32_t* bucket, co
 __global__ void __launch_bounds__(kBlock) k_stage_finish(const int64_t* owner_off, KPart part,
                                                          StageArgs a, const int64_t* prev_count,
                                                          int32_t row_bytes, const int32_t* dcnt,
-                                                         int32_t nblk_delta, gg_stage_stats_t* stats,
+                                                         int32_t nblk_delta, int32_t has_src,
+                                                         gg_stage_stats_t* stats,
                                                          int32_t* status) {
   __shared__ int32_t s_delta[GG_MAX_PARTS];
   for (int t = threadIdx.x; t < GG_MAX_PARTS; t += blockDim.x) s_delta[t] = 0;
@@ -121,6 +136,7 @@ __global__ void __launch_bounds__(kBlock) k_stage_finish(const int64_t* owner_of
   }
   __syncthreads();
   const int64_t n = stage_n(owner_off, part.P, a);
+  __shared__ int64_t s_req[GG_MAX_PARTS], s_rows[GG_MAX_PARTS];
   if (threadIdx.x < GG_MAX_PARTS) {
     const int m = threadIdx.x;
     int64_t rows = 0;
@@ -129,42 +145,41 @@ __global__ void __launch_bounds__(kBlock) k_stage_finish(const int64_t* owner_of
       lo = lo < n ? lo : n;
       hi = hi < n ? hi : n;
       rows = hi > lo ? hi - lo : 0;
+      if (has_src) rows = s_delta[m];    // only the delta is requested
     }
     stats->rows[m] = rows;
     stats->bytes[m] = rows * row_bytes;
     stats->requests[m] = rows > 0 ? 1 : 0;
     stats->delta_rows[m] = s_delta[m];
+    s_req[m] = rows > 0 ? 1 : 0;
+    s_rows[m] = rows;
   }
+  __syncthreads();
   if (threadIdx.x == 0) {
-    int64_t req = 0;
+    int64_t req = 0, fetched = 0;
     for (int m = 0; m < part.P; ++m) {
-      int64_t lo = owner_off[m] < n ? owner_off[m] : n, hi = owner_off[m + 1] < n ? owner_off[m + 1] : n;
-      req += hi > lo ? 1 : 0;
+      req += s_req[m];
+      fetched += s_rows[m];
     }
     stats->rows_total = n;
     stats->requests_total = req;
     stats->invalidated = prev_count ? prev_count[0] : 0;
-    stats->pad_ = 0;
+    stats->retained = has_src ? n - fetched : 0;
     if (owner_off[part.P] > n) set_status(status, GG_DEV_CAPACITY);
   }
-}
-
-bool env_flag(const char* name, bool dflt) {
-  const char* v = getenv(name);
-  if (!v || !*v) return dflt;
-  return strcmp(v, "0") != 0;
 }
 
 template <int VB>
 void launch_stage_rows(bool nt, int grid, hipStream_t stream, const int32_t* bucket,
                        const int64_t* owner_off, const KPart& kp, const KFeat& kf,
-                       const StageArgs& a, char* cache, int32_t* slot_of, int32_t* status) {
+                       const StageArgs& a, char* cache, int32_t* slot_of, const char* src_cache,
+                       const int32_t* old_slot, int32_t* status) {
   if (nt)
     hipLaunchKernelGGL((k_stage_rows<VB, true>), dim3(grid), dim3(kBlock), 0, stream, bucket,
-                       owner_off, kp, kf, a, cache, slot_of, status);
+                       owner_off, kp, kf, a, cache, slot_of, src_cache, old_slot, status);
   else
     hipLaunchKernelGGL((k_stage_rows<VB, false>), dim3(grid), dim3(kBlock), 0, stream, bucket,
-                       owner_off, kp, kf, a, cache, slot_of, status);
+                       owner_off, kp, kf, a, cache, slot_of, src_cache, old_slot, status);
 }
 
 int stage_delta_blocks(int64_t cap) {
@@ -177,21 +192,27 @@ int stage_delta_blocks(int64_t cap) {
 using namespace gg;
 
 extern "C" size_t gg_ws_stage(int64_t cap, int32_t num_parts) {
-  return align_up((size_t)stage_delta_blocks(cap) * (size_t)num_parts * sizeof(int32_t), 256);
+  return align_up((size_t)stage_delta_blocks(cap) * (size_t)num_parts * sizeof(int32_t), 256) +
+         align_up((size_t)std::max<int64_t>(cap, 1) * sizeof(int32_t), 256);
 }
 
 extern "C" int gg_stage_bulk(const int32_t* bucket_ids_d, const int64_t* owner_off_d, int64_t cap,
                              const gg_part_t* part, const gg_feat_t* feat, void* cache_d,
                              int64_t cache_stride, int64_t cache_rows, int32_t* slot_of_d,
-                             const int32_t* prev_ids_d, const int64_t* prev_count_d,
+                             const int32_t* clear_ids_d, const int64_t* clear_count_d,
+                             const void* src_cache_d, const int32_t* src_slot_of_d,
                              gg_stage_stats_t* stats_d, int32_t* status_d, void* ws,
                              size_t ws_bytes, hipStream_t stream) {
   GG_REQUIRE(owner_off_d && slot_of_d && stats_d && status_d, "NULL argument");
   GG_REQUIRE(cap >= 0 && cap < (1LL << 31) && cache_rows >= 0, "bad capacity");
   GG_REQUIRE(cap == 0 || bucket_ids_d, "bucket ids are NULL");
   GG_REQUIRE(cache_rows == 0 || cache_d, "cache is NULL");
-  GG_REQUIRE((prev_ids_d == nullptr) == (prev_count_d == nullptr),
-             "prev_ids and prev_count must both be given or both be NULL");
+  GG_REQUIRE((clear_ids_d == nullptr) == (clear_count_d == nullptr),
+             "clear_ids and clear_count must both be given or both be NULL");
+  GG_REQUIRE(src_cache_d == nullptr || src_slot_of_d != nullptr,
+             "a source cache needs its remap src_slot_of");
+  GG_REQUIRE(src_cache_d == nullptr || src_cache_d != cache_d,
+             "the source cache must be a different buffer from the cache being staged");
   KPart kp;
   int rc = pack_part(part, &kp);
   if (rc != GG_OK) return rc;
@@ -200,7 +221,8 @@ extern "C" int gg_stage_bulk(const int32_t* bucket_ids_d, const int64_t* owner_o
   if (rc != GG_OK) return rc;
   GG_REQUIRE(cache_stride >= kf.row_bytes && cache_stride % 4 == 0, "cache_stride %lld invalid",
              (long long)cache_stride);
-  bool v16 = aligned16(cache_d) && cache_stride % 16 == 0;
+  bool v16 = aligned16(cache_d) && cache_stride % 16 == 0 &&
+             (src_cache_d == nullptr || aligned16(src_cache_d));
   for (int m = 0; m < kf.P; ++m)
     if (kf.rows[m] > 0) v16 = v16 && aligned16(kf.shard[m]) && kf.stride[m] % 16 == 0;
   StageArgs a;
@@ -214,25 +236,35 @@ extern "C" int gg_stage_bulk(const int32_t* bucket_ids_d, const int64_t* owner_o
   GG_REQUIRE(ws && ws_bytes >= gg_ws_stage(cap, kp.P), "workspace of %zu bytes < %zu", ws_bytes,
              gg_ws_stage(cap, kp.P));
   int32_t* dcnt = (int32_t*)ws;
+  int32_t* old_slot =
+      (int32_t*)((char*)ws + align_up((size_t)gridd * (size_t)kp.P * sizeof(int32_t), 256));
+  const int32_t* before = src_slot_of_d ? src_slot_of_d : slot_of_d;
   hipLaunchKernelGGL(k_stage_delta, dim3(gridd), dim3(kBlock), 0, stream, bucket_ids_d, owner_off_d,
-                     kp, a, slot_of_d, dcnt);
+                     kp, a, before, old_slot, dcnt);
   GG_LAUNCH_CHECK("k_stage_delta");
-  if (prev_ids_d) {
-    hipLaunchKernelGGL(k_slot_reset, dim3(2048), dim3(kBlock), 0, stream, prev_ids_d, prev_count_d,
+  if (clear_ids_d) {
+    hipLaunchKernelGGL(k_slot_reset, dim3(2048), dim3(kBlock), 0, stream, clear_ids_d, clear_count_d,
                        kp.N, slot_of_d);
     GG_LAUNCH_CHECK("k_slot_reset");
   }
   const int64_t ntiles = cdiv(std::min(cap, cache_rows), kWave);
-  const int grid = (int)std::min<int64_t>(std::max<int64_t>(cdiv(ntiles, kBlock / kWave), 1), 16384);
+  // Rows read over PCIe need few waves in flight to keep the link busy; a
+  // full grid would hold every CU while it waits and starve kernels on
+  // other streams (the next window's sampling), so cap it then.
+  static const int host_cap = env_int("GG_STAGE_HOST_BLOCKS", 128);
+  int64_t gmax = 16384;
+  if (host_cap > 0 && host_shards(kf) > 0) gmax = host_cap;
+  const int grid = (int)std::min<int64_t>(std::max<int64_t>(cdiv(ntiles, kBlock / kWave), 1), gmax);
   if (v16)
     launch_stage_rows<16>(nt, grid, stream, bucket_ids_d, owner_off_d, kp, kf, a, (char*)cache_d,
-                          slot_of_d, status_d);
+                          slot_of_d, (const char*)src_cache_d, old_slot, status_d);
   else
     launch_stage_rows<4>(nt, grid, stream, bucket_ids_d, owner_off_d, kp, kf, a, (char*)cache_d,
-                         slot_of_d, status_d);
+                         slot_of_d, (const char*)src_cache_d, old_slot, status_d);
   GG_LAUNCH_CHECK("k_stage_rows");
   hipLaunchKernelGGL(k_stage_finish, dim3(1), dim3(kBlock), 0, stream, owner_off_d, kp, a,
-                     prev_count_d, kf.row_bytes, dcnt, gridd, stats_d, status_d);
+                     clear_count_d, kf.row_bytes, dcnt, gridd, src_cache_d ? 1 : 0, stats_d,
+                     status_d);
   GG_LAUNCH_CHECK("k_stage_finish");
   return GG_OK;
 }

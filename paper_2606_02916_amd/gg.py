@@ -60,7 +60,7 @@ class gg_wsample_t(C.Structure):
 
 class gg_stage_stats_t(C.Structure):
     _fields_ = [("rows_total", C.c_int64), ("requests_total", C.c_int64),
-                ("invalidated", C.c_int64), ("pad_", C.c_int64),
+                ("invalidated", C.c_int64), ("retained", C.c_int64),
                 ("requests", C.c_int64 * MAX_PARTS), ("rows", C.c_int64 * MAX_PARTS),
                 ("bytes", C.c_int64 * MAX_PARTS), ("delta_rows", C.c_int64 * MAX_PARTS)]
 
@@ -88,8 +88,8 @@ SIGNATURES = {
                                    _P]),
     "gg_build_hotset": (C.c_int, [_P, _I32, _P, _I64, _P, _P, _I64, _P, _P, _P, _SZ, _P]),
     "gg_bucket_by_owner": (C.c_int, [_P, _P, _I64, _P, _P, _P, _P, _P, _SZ, _P]),
-    "gg_stage_bulk": (C.c_int, [_P, _P, _I64, _P, _P, _P, _I64, _I64, _P, _P, _P, _P, _P, _P, _SZ,
-                                _P]),
+    "gg_stage_bulk": (C.c_int, [_P, _P, _I64, _P, _P, _P, _I64, _I64, _P, _P, _P, _P, _P, _P, _P,
+                                _P, _SZ, _P]),
     "gg_gather_batch": (C.c_int, [_P, _P, _I32, _I64, _P, _P, _P, _I64, _I64, _P, _P, _I64, _P,
                                   _P, _P, _SZ, _P]),
     "gg_status_string": (C.c_char_p, [_I32]),
@@ -235,10 +235,11 @@ def gg_bucket_by_owner(hot_ids, hot_count, cap, part, bucket_ids, owner_off, sta
 
 
 def gg_stage_bulk(bucket_ids, owner_off, cap, part, feat, cache, cache_stride, cache_rows, slot_of,
-                  prev_ids, prev_count, stats, status, ws, stream=None):
+                  clear_ids, clear_count, src_cache, src_slot_of, stats, status, ws, stream=None):
     return check(lib.gg_stage_bulk(_ptr(bucket_ids), _ptr(owner_off), cap, C.byref(part),
                                    C.byref(feat), _ptr(cache), cache_stride, cache_rows,
-                                   _ptr(slot_of), _ptr(prev_ids), _ptr(prev_count), _ptr(stats),
+                                   _ptr(slot_of), _ptr(clear_ids), _ptr(clear_count),
+                                   _ptr(src_cache), _ptr(src_slot_of), _ptr(stats),
                                    _ptr(status), _ptr(ws), ws.numel(), _stream(stream)),
                  "gg_stage_bulk")
 
@@ -279,8 +280,6 @@ def gather_stats_from_bytes(buf, P):
 def _stats_dict(st, P):
     d = {}
     for name, _ in st._fields_:
-        if name == "pad_":
-            continue
         v = getattr(st, name)
         d[name] = [int(x) for x in v][:P] if hasattr(v, "__len__") else int(v)
     return d

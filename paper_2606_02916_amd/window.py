@@ -1,25 +1,94 @@
-"""Window driver: device buffers (torch allocations) and the call sequence
-of one window through libgg.  Orchestration only; every step runs in the
-library's kernels, on one stream, with no host synchronisation inside a
-window.
+"""Window drivers: device buffers (torch allocations) and the call sequence
+of a window through libgg.  Orchestration only; every step runs in the
+library's kernels and no host synchronisation happens inside a window.
 
-Algorithm 1 of the paper (GreenGNN, arXiv 2606.02916) per window k:
-sample the W batches, build H_k, group it by owner, stage the cache with
-one bulk copy per owner (clearing window k-1's remap entries), then gather
-every batch's input rows through the remap with the miss path.
+Algorithm 1 of the paper (GreenGNN, arXiv 2606.02916) per window k: sample
+the W batches, build H_k, group it by owner, rebuild the cache with one
+bulk request per owner, then gather every batch's input rows through the
+ID-to-slot remap with the miss path.
+
+FetchPipeline runs the five calls in order on one stream.  With delta=True
+it keeps two caches and requests only the rebuild delta
+Delta_{k,m} = (H_k in owner m) minus C_{k-1} from the owners, copying the
+rows it retains from the previous cache (Sec. IV-A, Eq. (1)).
+LookaheadPipeline is the paper's pipelined runtime (Algorithm 1, Sec.
+IV-C): window k+1 is sampled, bucketed and delta-staged on one stream while
+window k is gathered on another.
 """
 from __future__ import annotations
 
-import numpy as np
 import torch
 
 from . import gg
 
 
+class _Geometry:
+    """Sizes shared by all buffer sets of a pipeline."""
+
+    def __init__(self, N, W, fanout, max_batch, P, local_owner, shard_rows, stride, cache_stride):
+        self.N, self.W, self.P = N, W, P
+        self.fanout = [int(k) for k in fanout]
+        self.L = len(self.fanout)
+        self.stride = stride
+        self.cache_stride = cache_stride
+        self.fcap, self.ncap = gg.gg_sample_caps(N, W, max_batch, self.fanout)
+        self.wpb = gg.gg_bits_words(N)
+        lev = min(max_batch, N)
+        for k in self.fanout:
+            lev = min(N, lev * (k + 1))
+        self.out_cap = max(lev, 1)                      # rows of one N_b
+        remote = N - (int(shard_rows[local_owner]) if local_owner >= 0 else 0)
+        self.hot_cap = max(1, min(remote, W * self.out_cap))
+        self.win_cap = W * self.out_cap                 # rows of a whole window
+        self.ws_bytes = max(gg.gg_ws_sample(N, W), gg.gg_ws_hotset(N, W),
+                            gg.gg_ws_bucket(self.hot_cap, P), gg.gg_ws_stage(self.hot_cap, P),
+                            gg.gg_ws_gather(self.out_cap, 1, P),
+                            gg.gg_ws_gather(self.win_cap, W, P))
+
+
+class _Buffers:
+    """Everything one window writes: sampling outputs, hot set, cache and
+    remap, workspace, statistics and (lazily) the window's gathered rows."""
+
+    def __init__(self, g: _Geometry, dev):
+        self.g, self.dev = g, dev
+        self.frontier_ids = torch.empty(max(g.fcap, 1), dtype=torch.int32, device=dev)
+        self.frontier_off = torch.zeros((g.L + 1) * g.W + 1, dtype=torch.int64, device=dev)
+        self.nbr_ids = torch.empty(max(g.ncap, 1), dtype=torch.int32, device=dev)
+        self.nbr_off = torch.zeros(g.L * g.W + 1, dtype=torch.int64, device=dev)
+        self.frontier_bits = torch.empty(g.W * g.wpb, dtype=torch.int32, device=dev)
+        self.need = torch.zeros(2, dtype=torch.int64, device=dev)
+        self.wsample = gg.make_wsample(self.frontier_ids, self.frontier_off, self.nbr_ids,
+                                       self.nbr_off, self.frontier_bits, self.need)
+        self.hot_ids = torch.empty(g.hot_cap, dtype=torch.int32, device=dev)
+        self.hot_freq = torch.empty(g.hot_cap, dtype=torch.int32, device=dev)
+        self.owner_off = torch.zeros(g.P + 1, dtype=torch.int64, device=dev)
+        self.cache = torch.empty((g.hot_cap, g.cache_stride), dtype=torch.uint8, device=dev)
+        self.slot_of = torch.full((g.N,), -1, dtype=torch.int32, device=dev)
+        self.ws = torch.empty(g.ws_bytes, dtype=torch.uint8, device=dev)
+        self.stage_stats = torch.zeros(gg.STAGE_STATS_BYTES, dtype=torch.uint8, device=dev)
+        self.gather_stats = torch.zeros((g.W, gg.GATHER_STATS_BYTES), dtype=torch.uint8,
+                                        device=dev)
+        self._win_out = None
+
+    def stage_stats_dict(self):
+        return gg.stage_stats_from_bytes(self.stage_stats.cpu().numpy().tobytes(), self.g.P)
+
+    def gather_stats_dict(self, b):
+        return gg.gather_stats_from_bytes(self.gather_stats[b].cpu().numpy().tobytes(), self.g.P)
+
+    @property
+    def win_out(self):
+        if self._win_out is None:
+            self._win_out = torch.empty((self.g.win_cap, self.g.stride), dtype=torch.uint8,
+                                        device=self.dev)
+        return self._win_out
+
+
 class FetchPipeline:
     def __init__(self, row_ptr, col_idx, num_parts, part_kind, local_owner, range_start, shards,
                  shard_rows, row_bytes, stride, W, fanout, max_batch, n_hot=-1, device=None,
-                 out_buffers=2, cache_stride=None):
+                 out_buffers=2, cache_stride=None, delta=False):
         self.device = torch.device(device if device is not None else "cuda")
         self.N = int(row_ptr.numel() - 1)
         self.W = int(W)
@@ -32,59 +101,41 @@ class FetchPipeline:
         # share HBM sectors, which a sparse ascending gather reuses.
         self.cache_stride = int(cache_stride) if cache_stride else self.stride
         self.n_hot = int(n_hot)
+        self.delta = bool(delta)
         self.row_ptr, self.col_idx = row_ptr, col_idx
         self.shards = shards
         self.csr = gg.make_csr(row_ptr, col_idx)
         self.part = gg.make_part(self.P, part_kind, local_owner, self.N, range_start)
         self.feat = gg.make_feat(self.row_bytes, shards, [self.stride] * self.P, shard_rows)
-        dev = self.device
-        fcap, ncap = gg.gg_sample_caps(self.N, self.W, max_batch, self.fanout)
-        self.frontier_ids = torch.empty(max(fcap, 1), dtype=torch.int32, device=dev)
-        self.frontier_off = torch.zeros((self.L + 1) * self.W + 1, dtype=torch.int64, device=dev)
-        self.nbr_ids = torch.empty(max(ncap, 1), dtype=torch.int32, device=dev)
-        self.nbr_off = torch.zeros(self.L * self.W + 1, dtype=torch.int64, device=dev)
-        self.wpb = gg.gg_bits_words(self.N)
-        self.frontier_bits = torch.empty(self.W * self.wpb, dtype=torch.int32, device=dev)
-        self.need = torch.zeros(2, dtype=torch.int64, device=dev)
+        self.geo = _Geometry(self.N, self.W, self.fanout, max_batch, self.P, local_owner,
+                             shard_rows, self.stride, self.cache_stride)
+        g, dev = self.geo, self.device
+        self.out_cap, self.hot_cap, self.win_cap, self.wpb = g.out_cap, g.hot_cap, g.win_cap, g.wpb
+        self.buf = _Buffers(g, dev)
+        b = self.buf
+        for name in ("frontier_ids", "frontier_off", "nbr_ids", "nbr_off", "frontier_bits", "need",
+                     "wsample", "hot_ids", "hot_freq", "owner_off", "slot_of", "ws",
+                     "stage_stats", "gather_stats"):
+            setattr(self, name, getattr(b, name))
         self.status = torch.zeros(1, dtype=torch.int32, device=dev)
-        self.wsample = gg.make_wsample(self.frontier_ids, self.frontier_off, self.nbr_ids,
-                                       self.nbr_off, self.frontier_bits, self.need)
-        # Per-batch bound of |N_b| and of the window's remote nodes.
-        lev = min(max_batch, self.N)
-        for k in self.fanout:
-            lev = min(self.N, lev * (k + 1))
-        self.out_cap = max(lev, 1)
-        remote = self.N - (int(shard_rows[local_owner]) if local_owner >= 0 else 0)
-        self.hot_cap = max(1, min(remote, self.W * self.out_cap))
-        self.hot_ids = torch.empty(self.hot_cap, dtype=torch.int32, device=dev)
-        self.hot_freq = torch.empty(self.hot_cap, dtype=torch.int32, device=dev)
         self.hot_count = [torch.zeros(2, dtype=torch.int64, device=dev) for _ in range(2)]
-        self.bucket_ids = [torch.empty(self.hot_cap, dtype=torch.int32, device=dev)
+        self.bucket_ids = [torch.empty(g.hot_cap, dtype=torch.int32, device=dev)
                            for _ in range(2)]
-        self.owner_off = torch.zeros(self.P + 1, dtype=torch.int64, device=dev)
-        self.cache = torch.empty((self.hot_cap, self.cache_stride), dtype=torch.uint8, device=dev)
-        self.slot_of = torch.full((self.N,), -1, dtype=torch.int32, device=dev)
-        self.win_cap = self.W * self.out_cap
-        ws_bytes = max(gg.gg_ws_sample(self.N, self.W), gg.gg_ws_hotset(self.N, self.W),
-                       gg.gg_ws_bucket(self.hot_cap, self.P), gg.gg_ws_stage(self.hot_cap, self.P),
-                       gg.gg_ws_gather(self.out_cap, 1, self.P),
-                       gg.gg_ws_gather(self.win_cap, self.W, self.P))
-        self.ws = torch.empty(ws_bytes, dtype=torch.uint8, device=dev)
-        self.stage_stats = torch.zeros(gg.STAGE_STATS_BYTES, dtype=torch.uint8, device=dev)
-        self.gather_stats = torch.zeros((self.W, gg.GATHER_STATS_BYTES), dtype=torch.uint8,
-                                        device=dev)
-        self.outs = [torch.empty((self.out_cap, self.stride), dtype=torch.uint8, device=dev)
+        # With delta staging the cache alternates between two buffers.
+        self.caches = [b.cache] + ([torch.empty_like(b.cache)] if self.delta else [])
+        self.outs = [torch.empty((g.out_cap, self.stride), dtype=torch.uint8, device=dev)
                      for _ in range(out_buffers)]
-        self._win_out = None
         self.k = 0
+
+    @property
+    def cache(self):
+        """The cache of the most recently staged window."""
+        return self.caches[(self.k - 1) % len(self.caches)] if self.k else self.caches[0]
 
     @property
     def win_out(self):
         """Output of a whole-window gather: the W batches' rows back to back."""
-        if self._win_out is None:
-            self._win_out = torch.empty((self.win_cap, self.stride), dtype=torch.uint8,
-                                        device=self.device)
-        return self._win_out
+        return self.buf.win_out
 
     def reset_cache(self):
         self.slot_of.fill_(-1)
@@ -106,21 +157,30 @@ class FetchPipeline:
                               self.bucket_ids[cur], self.owner_off, self.status, self.ws)
 
     def stage(self, cur):
+        """Rebuilds the cache for window k (= self.k, advanced by the caller)."""
         prev = 1 - cur
         have_prev = self.k > 0
+        nc = len(self.caches)
+        cache = self.caches[self.k % nc]
+        src = self.caches[(self.k - 1) % nc] if (self.delta and have_prev) else None
         gg.gg_stage_bulk(self.bucket_ids[cur], self.owner_off, self.hot_cap, self.part, self.feat,
-                         self.cache, self.cache_stride, self.hot_cap, self.slot_of,
+                         cache, self.cache_stride, self.hot_cap, self.slot_of,
                          self.bucket_ids[prev] if have_prev else None,
-                         self.hot_count[prev] if have_prev else None, self.stage_stats,
+                         self.hot_count[prev] if have_prev else None,
+                         src, self.slot_of if src is not None else None, self.stage_stats,
                          self.status, self.ws)
+
+    def staged_cache(self):
+        """The cache stage() just filled (valid until the window advances)."""
+        return self.caches[self.k % len(self.caches)]
 
     def gather(self, Wk, b, out):
         """Batch b of the window into out (one launch)."""
         bounds = self.frontier_off.data_ptr() + 8 * (self.L * Wk + b)
         stats = self.gather_stats.data_ptr() + b * gg.GATHER_STATS_BYTES
         gg.gg_gather_batch(self.frontier_ids, bounds, 1, out.shape[0], self.part, self.feat,
-                           self.cache, self.cache_stride, self.hot_cap, self.slot_of, out,
-                           self.stride, stats, self.status, self.ws)
+                           self.staged_cache(), self.cache_stride, self.hot_cap, self.slot_of,
+                           out, self.stride, stats, self.status, self.ws)
 
     def gather_window(self, Wk, out=None):
         """All Wk batches of the window in one launch; batch b's rows start at
@@ -128,8 +188,8 @@ class FetchPipeline:
         out = self.win_out if out is None else out
         bounds = self.frontier_off.data_ptr() + 8 * (self.L * Wk)
         gg.gg_gather_batch(self.frontier_ids, bounds, Wk, out.shape[0], self.part, self.feat,
-                           self.cache, self.cache_stride, self.hot_cap, self.slot_of, out,
-                           self.stride, self.gather_stats.data_ptr(), self.status, self.ws)
+                           self.staged_cache(), self.cache_stride, self.hot_cap, self.slot_of,
+                           out, self.stride, self.gather_stats.data_ptr(), self.status, self.ws)
         return out
 
     def window(self, seeds, seed_off, batch0, epoch=0, rng_seed=0, outs=None, events=None,
@@ -193,6 +253,137 @@ class FetchPipeline:
         return gg.gather_stats_from_bytes(self.gather_stats[b].cpu().numpy().tobytes(), self.P)
 
 
-def _rec(e):
+class LookaheadPipeline:
+    """Pipelined runtime in three stages on three streams: the build stream
+    samples window k and forms its hot set and owner buckets, the stage
+    stream rebuilds the cache (delta staging from window k-1's cache), the
+    gather stream gathers the window.  Window k+1 is built while window k
+    is staged, and window k is gathered while window k+1 is staged, so a
+    window costs about the longest stage instead of the sum.
+
+    `nsets` buffer sets rotate over the windows (window k uses set
+    k mod nsets).  Building window k waits for the gather of window
+    k - nsets, the last reader of its set; with more sets the build may run
+    further ahead.  Bucket lists and hot-set counts rotate over 2 * nsets
+    slots: staging window k reads slot k and clears its remap with the slot
+    of window k - nsets while windows up to k + nsets - 1 are being built.
+    Every other reuse is ordered through the build wait or stream order."""
+
+    def __init__(self, row_ptr, col_idx, num_parts, part_kind, local_owner, range_start, shards,
+                 shard_rows, row_bytes, stride, W, fanout, max_batch, n_hot=-1, device=None,
+                 cache_stride=None, nsets=2):
+        self.device = torch.device(device if device is not None else "cuda")
+        self.N = int(row_ptr.numel() - 1)
+        self.W = int(W)
+        self.fanout = [int(k) for k in fanout]
+        self.L = len(self.fanout)
+        self.P = int(num_parts)
+        self.row_bytes, self.stride = int(row_bytes), int(stride)
+        self.cache_stride = int(cache_stride) if cache_stride else self.stride
+        self.n_hot = int(n_hot)
+        self.csr = gg.make_csr(row_ptr, col_idx)
+        self.part = gg.make_part(self.P, part_kind, local_owner, self.N, range_start)
+        self.feat = gg.make_feat(self.row_bytes, shards, [self.stride] * self.P, shard_rows)
+        self.shards = shards
+        self.geo = g = _Geometry(self.N, self.W, self.fanout, max_batch, self.P, local_owner,
+                                 shard_rows, self.stride, self.cache_stride)
+        dev = self.device
+        if int(nsets) < 2:
+            raise ValueError("the look-ahead pipeline needs at least two buffer sets")
+        self.nsets = int(nsets)
+        self.NSLOT = 2 * self.nsets
+        self.sets = [_Buffers(g, dev) for _ in range(self.nsets)]
+        self.stage_ws = torch.empty(g.ws_bytes, dtype=torch.uint8, device=dev)
+        self.gather_ws = torch.empty(g.ws_bytes, dtype=torch.uint8, device=dev)
+        self.bucket_ids = [torch.empty(g.hot_cap, dtype=torch.int32, device=dev)
+                           for _ in range(self.NSLOT)]
+        self.hot_count = [torch.zeros(2, dtype=torch.int64, device=dev)
+                          for _ in range(self.NSLOT)]
+        self.status = torch.zeros(1, dtype=torch.int32, device=dev)
+        self.build_stream = torch.cuda.Stream(device=dev)
+        self.stage_stream = torch.cuda.Stream(device=dev)
+        self.gather_stream = torch.cuda.Stream(device=dev)
+        self.built = [torch.cuda.Event() for _ in range(self.nsets)]
+        self.staged = [torch.cuda.Event() for _ in range(self.nsets)]
+        self.gathered = [torch.cuda.Event() for _ in range(self.nsets)]
+        self.k = 0
+
+    def window(self, seeds, seed_off, batch0, epoch=0, rng_seed=0, out=None, events=None,
+               gather_events=None):
+        """Enqueues window k; returns (number of batches, buffer set).  The
+        window's rows land in the set's win_out (or `out`) on the gather
+        stream; wait on gathered_event(k) before reading them.  Inputs
+        uploaded on the caller's stream are visible to the build stream.
+        events: optional 5 torch events, four recorded on the build stream
+        around its three calls and one after staging on the stage stream
+        (the stage time is events[4] minus the later of events[3] and the
+        previous window's staging end); gather_events: optional (start, end)
+        pair recorded on the gather stream around the gather launch."""
+        k, g = self.k, self.geo
+        X, T = k % self.nsets, k % self.NSLOT
+        cur, prev = self.sets[X], self.sets[(k - 1) % self.nsets]
+        Wk = len(seed_off) - 1
+        bs, ss, gs = self.build_stream, self.stage_stream, self.gather_stream
+        ev = events if events is not None else [None] * 5
+        bs.wait_stream(torch.cuda.current_stream(self.device))
+        if k >= self.nsets:
+            bs.wait_event(self.gathered[X])      # window k - nsets read this set
+        s = bs.cuda_stream
+        _rec(ev[0], bs)
+        gg.gg_sample_window(self.csr, seeds, seed_off, Wk, self.fanout, self.L, rng_seed, epoch,
+                            batch0, cur.wsample, self.status, cur.ws, stream=s)
+        _rec(ev[1], bs)
+        gg.gg_build_hotset(cur.frontier_bits, Wk, self.part, self.n_hot, cur.hot_ids,
+                           cur.hot_freq, g.hot_cap, self.hot_count[T], self.status, cur.ws,
+                           stream=s)
+        _rec(ev[2], bs)
+        gg.gg_bucket_by_owner(cur.hot_ids, self.hot_count[T], g.hot_cap, self.part,
+                              self.bucket_ids[T], cur.owner_off, self.status, cur.ws, stream=s)
+        _rec(ev[3], bs)
+        self.built[X].record(bs)
+        ss.wait_event(self.built[X])
+        C = (k - self.nsets) % self.NSLOT
+        clear_ids = self.bucket_ids[C] if k >= self.nsets else None
+        clear_cnt = self.hot_count[C] if k >= self.nsets else None
+        src = prev if k >= 1 else None
+        gg.gg_stage_bulk(self.bucket_ids[T], cur.owner_off, g.hot_cap, self.part, self.feat,
+                         cur.cache, self.cache_stride, g.hot_cap, cur.slot_of, clear_ids,
+                         clear_cnt, src.cache if src else None, src.slot_of if src else None,
+                         cur.stage_stats, self.status, self.stage_ws,
+                         stream=ss.cuda_stream)
+        _rec(ev[4], ss)
+        if gather_events is not None:
+            # A timing event recorded on the gather stream right behind its
+            # cross-stream wait can take its timestamp before the wait ends,
+            # so the start is taken where staging ends; the gather begins
+            # at the later of this and the previous gather's end.
+            gather_events[0].record(ss)
+        self.staged[X].record(ss)
+        gs.wait_event(self.staged[X])
+        o = cur.win_out if out is None else out
+        bounds = cur.frontier_off.data_ptr() + 8 * (self.L * Wk)
+        gg.gg_gather_batch(cur.frontier_ids, bounds, Wk, o.shape[0], self.part, self.feat,
+                           cur.cache, self.cache_stride, g.hot_cap, cur.slot_of, o, self.stride,
+                           cur.gather_stats.data_ptr(), self.status, self.gather_ws,
+                           stream=gs.cuda_stream)
+        if gather_events is not None:
+            gather_events[1].record(gs)
+        self.gathered[X].record(gs)
+        self.k += 1
+        return Wk, cur
+
+    def gathered_event(self, k):
+        return self.gathered[k % self.nsets]
+
+    def synchronize(self):
+        for s in (self.build_stream, self.stage_stream, self.gather_stream):
+            s.synchronize()
+
+    def read_status(self):
+        self.synchronize()
+        return int(self.status.item())
+
+
+def _rec(e, stream=None):
     if e is not None:
-        e.record()
+        e.record(stream)

@@ -20,7 +20,7 @@ class World:
 
     def __init__(self, inst, W=None, n_hot=-1, local_owner=None, fanout=None, batch=None,
                  device="cuda:0", shards=None, row_bytes=None, stride=None, cache_stride=None,
-                 tensors=None):
+                 tensors=None, delta=False):
         wl = inst.wl
         self.inst = inst
         self.wl = wl
@@ -45,11 +45,13 @@ class World:
         self.pipe = FetchPipeline(self.row_ptr_d, self.col_idx_d, self.P, wl.part_kind, self.local,
                                   self.rs, self.shards_d, rows, self.row_bytes, self.stride,
                                   self.W, self.fanout, self.batch, n_hot=n_hot, device=self.dev,
-                                  cache_stride=cache_stride)
+                                  cache_stride=cache_stride, delta=delta)
         self.part_ref = ggref.make_part(self.P, wl.part_kind, self.local, wl.num_nodes, self.rs)
         self.feat_ref = ggref.make_feat(self.row_bytes, self.shards, [self.stride] * self.P)
         self.cstride = self.pipe.cache_stride
-        self.cache_ref = np.zeros((self.pipe.hot_cap, self.cstride), dtype=np.uint8)
+        self.delta = delta
+        self.cache_refs = [np.zeros((self.pipe.hot_cap, self.cstride), dtype=np.uint8)
+                           for _ in range(2 if delta else 1)]
         self.slot_ref = np.full(wl.num_nodes, -1, dtype=np.int32)
         self.prev_ref = None
 
@@ -100,15 +102,19 @@ class World:
         assert np.array_equal(g_freq, freq)
         assert np.array_equal(g_bucket, bucket)
         assert np.array_equal(g_owner_off, owner_off)
-        # stage
-        sst = ggref.stage_bulk(bucket, owner_off, self.part_ref, self.feat_ref, self.cache_ref,
-                               self.cstride, self.slot_ref, self.prev_ref)
+        # stage (delta mode: retained rows come from the previous cache)
+        kk, nc = pipe.k, len(self.cache_refs)
+        cache_ref = self.cache_refs[kk % nc]
+        src = self.cache_refs[(kk - 1) % nc] if (self.delta and kk > 0) else None
+        sst = ggref.stage_bulk(bucket, owner_off, self.part_ref, self.feat_ref, cache_ref,
+                               self.cstride, self.slot_ref, self.prev_ref, src_cache=src,
+                               src_slot_of=self.slot_ref if src is not None else None)
         self.prev_ref = bucket.copy()
         assert pipe.stage_stats_dict() == sst
         assert np.array_equal(pipe.slot_of.cpu().numpy(), self.slot_ref)
         H = len(hot)
-        g_cache = pipe.cache[:H].cpu().numpy()
-        assert np.array_equal(g_cache[:, :rb], self.cache_ref[:H, :rb])
+        g_cache = pipe.staged_cache()[:H].cpu().numpy()
+        assert np.array_equal(g_cache[:, :rb], cache_ref[:H, :rb])
         # gathers, one batch at a time, then the whole window in one launch
         refs, gstats = [], []
         for b in range(Wk):
@@ -120,7 +126,7 @@ class World:
             s = L * Wk + b
             ids = fids[foff[s]:foff[s + 1]]
             ref = np.zeros((len(ids), st), dtype=np.uint8)
-            gs = ggref.gather_batch(ids, self.part_ref, self.feat_ref, self.cache_ref,
+            gs = ggref.gather_batch(ids, self.part_ref, self.feat_ref, cache_ref,
                                     self.cstride, self.slot_ref, ref, st)
             assert pipe.gather_stats_dict(b) == gs
             gstats.append(gs)
@@ -141,4 +147,5 @@ class World:
                 got = win[lo:hi].cpu().numpy()
                 assert np.array_equal(got[:, :rb], refs[b][:, :rb]), f"window batch {b}"
         pipe.k += 1
-        return dict(Wk=Wk, fids=fids, foff=foff, hot=hot, stage=sst)
+        return dict(Wk=Wk, fids=fids, foff=foff, hot=hot, stage=sst,
+                    outs=refs if check_outputs else None)

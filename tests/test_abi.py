@@ -54,7 +54,7 @@ int main() {
   S(gg_feat_t) F(gg_feat_t, shard) F(gg_feat_t, row_stride) F(gg_feat_t, shard_rows)
   S(gg_wsample_t) F(gg_wsample_t, frontier_cap) F(gg_wsample_t, nbr_ids) F(gg_wsample_t, nbr_off)
   F(gg_wsample_t, frontier_bits) F(gg_wsample_t, need)
-  S(gg_stage_stats_t) F(gg_stage_stats_t, invalidated) F(gg_stage_stats_t, requests)
+  S(gg_stage_stats_t) F(gg_stage_stats_t, invalidated) F(gg_stage_stats_t, retained) F(gg_stage_stats_t, requests)
   F(gg_stage_stats_t, rows) F(gg_stage_stats_t, bytes) F(gg_stage_stats_t, delta_rows)
   S(gg_gather_stats_t) F(gg_gather_stats_t, misses) F(gg_gather_stats_t, miss_requests)
   F(gg_gather_stats_t, miss_rows)
@@ -135,7 +135,7 @@ def test_bad_arguments_are_rejected_on_the_host(gg):
     part = gg.make_part(4, gg.PART_MOD, 4, 100)                          # local owner >= P
     feat = gg.make_feat(256, [t] * 4, [256] * 4, [25] * 4)
     with pytest.raises(gg.GGError):
-        gg.gg_stage_bulk(t, t, 10, part, feat, t, 256, 10, t, None, None, t, t, t, stream=0)
+        gg.gg_stage_bulk(t, t, 10, part, feat, t, 256, 10, t, None, None, None, None, t, t, t, stream=0)
     part = gg.make_part(4, gg.PART_MOD, 0, 100)
     feat = gg.make_feat(250, [t] * 4, [256] * 4, [25] * 4)              # row_bytes % 4 != 0
     with pytest.raises(gg.GGError):
