@@ -111,7 +111,7 @@ def summarize(args):
             calls = [sum(per[p][i] for p in per if i < len(per[p])) for i in range(n)]
             out.append("")
             out.append("# gg_gather_batch (zero + rows + finish) by bench phase, microseconds")
-            for label, lo, hi in (("pre-pass, one window at a time", 0, n_pre),
+            for label, lo, hi in (("pre-pass, chip to itself", 0, n_pre),
                                   ("timed steps", n - n_timed, n)):
                 v = calls[lo:hi]
                 r = per["k_gather_rows"][lo:hi]
@@ -175,6 +175,12 @@ def main():
     ap.add_argument("--wsweep", default=None,
                     help="comma-separated window sizes: run one epoch per W and report, per W, "
                          "hot-set size, bulk bytes per owner, rebuild delta and gather rate")
+    ap.add_argument("--simulate", default=None,
+                    help="comma-separated window sizes: replay one epoch per W and per hot-set "
+                         "budget through the fetch path and report the simulator's event counts "
+                         "z(W) and energy estimate E_phy(W) (synthetic coefficients)")
+    ap.add_argument("--n-hot", default="-1",
+                    help="with --simulate: comma-separated hot-set budgets (-1 = union)")
     ap.add_argument("--summarize", action="store_true",
                     help="write profiles/ summaries from rocprofv3 databases instead of running")
     ap.add_argument("--trace-db", default=None)
@@ -182,8 +188,9 @@ def main():
     ap.add_argument("--write-db", default=None)
     ap.add_argument("--summary-command", default="")
     ap.add_argument("--phases", default=None,
-                    help="with --trace-db: gather launches of the pre-pass, warm-up and timed "
-                         "steps, e.g. 12,1,12, to average the gather per phase")
+                    help="with --trace-db: gather launches of the pre-pass (two per window "
+                         "with the look-ahead driver), warm-up and timed steps, e.g. 24,1,12, "
+                         "to average the gather per phase")
     args = ap.parse_args()
     if args.summarize:
         summarize(args)
@@ -207,6 +214,8 @@ def main():
         ap.error("--per-batch needs --pipeline sequential")
     if args.wsweep:
         return wsweep(args, wl)
+    if args.simulate:
+        return simulate(args, wl)
     W = args.W or wl.W
     t = time.time()
     inst, row_ptr_d, col_idx_d, shards_d = synth.torch_instance(args.config, dev)
@@ -247,11 +256,23 @@ def main():
     mk = lambda: torch.cuda.Event(enable_timing=True)  # noqa: E731
     rows_w, gbytes_w, hot_w, sbytes_w, req_w, hbytes_w = [], [], [], [], [], []
     pb = args.per_batch
-    iso_ms = []      # gather launches of the pre-pass, each with the chip to itself
+    iso_ms = []      # gather launches with the chip to themselves
+    flush = torch.empty(512 << 20, dtype=torch.uint8, device=dev) if look else None
     for k, (s, so, b0) in enumerate(wins):
         ge = [(mk(), mk()) for _ in range(W if pb else 1)]
-        Wk, sb = run_window(s, so, b0, gevs=ge)
+        Wk, sb = run_window(s, so, b0, gevs=None if look else ge)
         torch.cuda.synchronize()
+        if look:
+            # The same gather once more on one stream after the window is
+            # complete, so no cross-stream wait falls inside the interval.
+            # A 512 MiB fill first evicts the window's rows from the
+            # last-level cache and keeps the queue busy while the gather is
+            # enqueued behind it.
+            flush.fill_(k & 0xFF)
+            ge[0][0].record()
+            pipe.regather(sb, Wk)
+            ge[0][1].record()
+            torch.cuda.synchronize()
         iso_ms += [a.elapsed_time(b) for a, b in ge[:Wk if pb else 1]]
         st = pipe.read_status()
         if st != 0:
@@ -265,6 +286,7 @@ def main():
         sbytes_w.append(ss["rows_total"] * (2 * rb + 8) + ss["invalidated"] * 4)
         req_w.append(ss["requests_total"])
         hbytes_w.append(sum(ss["bytes"][m] for m in range(P) if not shards_d[m].is_cuda))
+    del flush
     log(f"rows per window: {rows_w[:4]}... hot set: {hot_w[:4]}...")
 
     for i in range(args.warmup):
@@ -375,7 +397,9 @@ def main():
                                   "frac": round(iso_achieved / HBM_PEAK_GBS, 4),
                                   "avg_launch_us": round(iso_avg_ms * 1e3, 2),
                                   "launches": len(iso_ms),
-                                  "note": "pre-pass over every window, one window at a time"}},
+                                  "note": "pre-pass over every window, one window at a "
+                                          "time" + ("; the look-ahead driver's gather launched "
+                                                    "again on one stream" if look else "")}},
         "stage_roofline": ({"kernel": "gg_stage_bulk", "bound": "hbm",
                             "achieved": round(stage_gbs, 1),
                             "frac": round(stage_gbs / HBM_PEAK_GBS, 4), "unit": "GB/s"}
@@ -487,6 +511,87 @@ def wsweep(args, wl):
                        "features": f"{wl.feat_dtype}x{wl.feat_dim}", "fanout": list(wl.fanout),
                        "batch": wl.batch_size, "W_reported": pick["W"]},
             "w_sweep": results}
+    print(json.dumps(line), flush=True)
+
+
+def sim_coefficients(wl):
+    """Synthetic coefficients of the analytical energy model, the same for
+    every owner: a 500 us request initiation at 50 W, rows at 1.25 GB/s
+    (one 10 GbE link) at 50 W, a 1.25 GB/s aggregate ceiling and 30 W idle
+    power.  A one-row request is then almost all initiation and a request
+    of about 1,500 rows of 400 B is half initiation."""
+    link = 1.25e9
+    lam_init, lam_row = 500e-6, wl.row_bytes / link
+    return dict(eps_init=50.0 * lam_init, eps_row=50.0 * lam_row, lam_init=lam_init,
+                lam_row=lam_row, bw_bytes_per_s=link, row_bytes=wl.row_bytes, p_idle=30.0)
+
+
+def simulate(args, wl):
+    """The window-size simulator on the GPU: one epoch per (budget, W)
+    through the fetch path, the per-window rebuild-delta and miss counters
+    priced into z(W) and E_phy(W) on the device."""
+    import numpy as np
+    import torch
+
+    import synth
+    from paper_2606_02916_amd import FetchPipeline, gg
+    dev = torch.device("cuda:0")
+    inst, row_ptr_d, col_idx_d, shards_d = synth.torch_instance(args.config, dev)
+    P, rb = wl.num_parts, wl.row_bytes
+    seeds_d = torch.from_numpy(inst.seeds).to(dev)
+    boff = inst.batch_off
+    cd = sim_coefficients(wl)
+    coeffs = gg.make_sim_coeffs(P, **cd)
+    results = []
+    for n_hot in [int(x) for x in args.n_hot.split(",")]:
+        for W in [int(x) for x in args.simulate.split(",")]:
+            pipe = FetchPipeline(row_ptr_d, col_idx_d, P, wl.part_kind, wl.local_owner,
+                                 inst.range_start, shards_d, [s.shape[0] for s in inst.shards],
+                                 rb, wl.row_stride, W, wl.fanout, wl.batch_size, n_hot=n_hot,
+                                 device=dev, delta=True)
+            nwin = synth.n_windows(boff, W)
+            wins = []
+            for k in range(nwin):
+                b0, b1 = synth.window_batches(boff, W, k)
+                wins.append((seeds_d[boff[b0]:boff[b1]], boff[b0:b1 + 1] - boff[b0], b0))
+            acc = torch.zeros(gg.SIM_ACC_BYTES, dtype=torch.uint8, device=dev)
+            for s, so, b0 in wins:                       # warm-up epoch
+                pipe.window(s, so, b0)
+            pipe.reset_cache()
+            torch.cuda.synchronize()
+            t0 = time.perf_counter()
+            for s, so, b0 in wins:
+                pipe.window(s, so, b0, sim=(coeffs, acc))
+            torch.cuda.synchronize()
+            el = time.perf_counter() - t0
+            if pipe.read_status() != 0:
+                raise RuntimeError(f"device status {pipe.read_status()} at W={W}")
+            a = gg.sim_acc_from_bytes(acc.cpu().numpy().tobytes())
+            r = {"n_hot": n_hot, "W": W, "windows": a["windows"],
+                 "z": {"rebuild_events": a["rebuild_events"], "miss_events": a["miss_events"],
+                       "t_stall_s": a["t_stall"],
+                       "hit_ratio": a["hits"] / a["remote_rows"] if a["remote_rows"] else 1.0},
+                 "rebuild_rows": a["rebuild_rows"], "miss_rows": a["miss_rows"],
+                 "E_rebuild_J": a["e_rebuild"], "E_miss_J": a["e_miss"],
+                 "E_stall_J": a["e_stall"], "E_phy_J": a["e_phy"],
+                 "epoch_ms": round(el * 1e3, 3)}
+            log(json.dumps(r))
+            results.append(r)
+            del pipe
+            torch.cuda.empty_cache()
+    best = {}
+    for r in results:
+        if r["n_hot"] not in best or r["E_phy_J"] < best[r["n_hot"]]["E_phy_J"]:
+            best[r["n_hot"]] = r
+    line = {"metric": "window-size simulator: z(W) and E_phy(W) per candidate W",
+            "value": round(sum(r["epoch_ms"] for r in results), 3), "unit": "ms (whole sweep)",
+            "n_gpus": 1, "higher_is_better": False, "dtype": "int64+f64",
+            "data": "synthetic R-MAT (a,b,c)=(0.57,0.19,0.19), seeded; synthetic cost coefficients",
+            "config": {"workload": args.config, "nodes": wl.num_nodes, "edges": wl.num_edges,
+                       "fanout": list(wl.fanout), "batch": wl.batch_size,
+                       "coefficients": cd},
+            "W_star": {str(k): v["W"] for k, v in best.items()},
+            "sweep": results}
     print(json.dumps(line), flush=True)
 
 

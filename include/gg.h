@@ -255,6 +255,66 @@ int gg_gather_batch(const int32_t* in_ids_d, const int64_t* bounds_d, int32_t ns
                     gg_gather_stats_t* stats_d, int32_t* status_d, void* ws, size_t ws_bytes,
                     hipStream_t stream);
 
+/* ---------------------------------------------------------------------------
+ * Window-size simulator counts.  The paper scores a candidate window size W
+ * by replaying one epoch's trace: per window k it counts the rebuild delta
+ * Delta_{k,m} = (H_k in owner m) minus C_{k-1} with C_{k-1} = H_{k-1}
+ * (C_0 empty), per batch the residual misses M_{b,m} = (N_b in owner m)
+ * minus H_k, over remote owners m (Sec. IV-A), and prices them with the
+ * analytical model of Sec. IV-B: Eq. (1) rebuild energy, Eq. (2) miss
+ * energy, Eq. (3) stall energy, E_phy = their sum.  Here the counts are the
+ * fetch path's own: one window's gg_stage_stats_t.delta_rows and its
+ * batches' gg_gather_stats_t.miss_rows, added to a running total.
+ * ------------------------------------------------------------------------- */
+
+/* Coefficients of the analytical model, per owner m.  A "row" is one
+ * node's feature row (the paper's x features of a transfer).  Payload terms
+ * are linear in the rows moved: eps_payload(m, x) = eps_row[m] * x and
+ * lam_payload(m, x) = lam_row[m] * x.  An event (one window's rebuild, or
+ * one batch's misses) lasts max(max over owners with x_m > 0 of
+ * lam_init[m] + lam_row[m] * x_m, (sum_m x_m) * row_bytes / bw_bytes_per_s):
+ * the slowest single-owner transfer or the aggregate bandwidth ceiling.
+ * Units are the caller's (e.g. J, s, B/s, W); bw_bytes_per_s must be > 0. */
+typedef struct gg_sim_coeffs {
+  double eps_init[GG_MAX_PARTS];
+  double eps_row[GG_MAX_PARTS];
+  double lam_init[GG_MAX_PARTS];
+  double lam_row[GG_MAX_PARTS];
+  double bw_bytes_per_s;
+  double row_bytes;
+  double p_idle;
+} gg_sim_coeffs_t;
+
+/* Running totals for one candidate W (device; the caller zeroes it before
+ * the first window).  z(W) of the paper's rank correction is (rebuild_events,
+ * miss_events, t_stall, hits / remote_rows). */
+typedef struct gg_sim_acc {
+  int64_t windows;
+  int64_t batches;
+  int64_t rebuild_events;  /* sum over k, m of I[Delta_{k,m} != empty] */
+  int64_t rebuild_rows;    /* sum over k, m of |Delta_{k,m}| */
+  int64_t miss_events;     /* sum over b, m of I[M_{b,m} != empty] */
+  int64_t miss_rows;       /* sum over b, m of |M_{b,m}| */
+  int64_t remote_rows;     /* remote members of the N_b, over all batches */
+  int64_t hits;            /* of those, served from the cache */
+  double e_rebuild;        /* Eq. (1) */
+  double e_miss;           /* Eq. (2) */
+  double t_stall;          /* summed event durations */
+  double e_stall;          /* Eq. (3): p_idle * t_stall */
+  double e_phy;            /* e_rebuild + e_miss + e_stall */
+} gg_sim_acc_t;
+
+/* Adds one window to acc_d: stage_d is the window's staging statistics,
+ * gather_d[0 .. nseg) its batches' gather statistics (one per batch, as a
+ * whole-window gg_gather_batch writes them).  Owners equal to
+ * part->local_owner are skipped.  The arithmetic is fp64 without fused
+ * multiply-adds, in a fixed order (owners ascending; the rebuild, then the
+ * batches in order), so totals are reproducible bit for bit.  One tiny
+ * launch on `stream`; no host synchronisation. */
+int gg_sim_accumulate(const gg_stage_stats_t* stage_d, const gg_gather_stats_t* gather_d,
+                      int32_t nseg, const gg_part_t* part, const gg_sim_coeffs_t* coeffs,
+                      gg_sim_acc_t* acc_d, hipStream_t stream);
+
 /* Helpers. */
 const char* gg_status_string(int32_t code);
 const char* gg_last_error(void);

@@ -10,6 +10,7 @@
 #include "ggref.h"
 
 #include <algorithm>
+#include <iterator>
 #include <cstring>
 #include <set>
 #include <vector>
@@ -394,3 +395,88 @@ int ggref_gather_batch(const int32_t* in_ids, int64_t n, const ggref_part_t* par
 }
 
 }  // extern "C"
+
+// ---------------------------------------------------------------------------
+// Trace simulator (Sec. IV-A simulation, Sec. IV-B, Sec. V).
+// ---------------------------------------------------------------------------
+namespace {
+
+// Prices one communication event whose owners move x[m] rows: every owner
+// with rows pays one initiation plus its linear payload (the summand of
+// Eq. (1) and Eq. (2)); the event lasts the longer of its slowest owner's
+// transfer and all its rows at the aggregate bandwidth ceiling.  Owners
+// are taken in ascending order.
+double price_event(const std::vector<int64_t>& x, const ggref_part_t* part,
+                   const ggref_sim_coeffs_t* c, int64_t* events, int64_t* rows, double* t) {
+  double energy = 0.0, slowest = 0.0;
+  int64_t moved = 0;
+  for (int32_t m = 0; m < part->num_parts; ++m) {
+    if (m == part->local_owner || x[m] == 0) continue;   // only remote owners with a transfer
+    const double xm = (double)x[m];
+    energy = energy + (c->eps_init[m] + c->eps_row[m] * xm);
+    const double tm = c->lam_init[m] + c->lam_row[m] * xm;
+    if (tm > slowest) slowest = tm;
+    moved += x[m];
+    *events += 1;
+  }
+  *rows += moved;
+  if (moved > 0) {
+    const double ceiling = (double)moved * c->row_bytes / c->bw_bytes_per_s;
+    *t = *t + (slowest > ceiling ? slowest : ceiling);
+  }
+  return energy;
+}
+
+}  // namespace
+
+int ggref_simulate_epoch(const int32_t* trace_ids, const int64_t* trace_off, int64_t n_batches,
+                         int32_t W, int64_t n_hot, const ggref_part_t* part,
+                         const ggref_sim_coeffs_t* coeffs, ggref_sim_acc_t* acc) {
+  if (!part_ok(part) || !coeffs || !acc || W < 1 || n_batches < 0 ||
+      !(coeffs->bw_bytes_per_s > 0.0))
+    return GGREF_ERR_ARG;
+  std::memset(acc, 0, sizeof(*acc));
+  const int32_t P = part->num_parts;
+  std::vector<int32_t> cache;   // C_{k-1}, ascending; C_0 is empty
+  const int64_t K = (n_batches + W - 1) / W;
+  for (int64_t k = 0; k < K; ++k) {
+    const int64_t b0 = k * W, b1 = std::min<int64_t>(n_batches, b0 + W);
+    const int32_t Wk = (int32_t)(b1 - b0);
+    // H_k from the window's N_b (level 0 of a one-level layout).
+    std::vector<int32_t> hot((size_t)std::max<int64_t>(trace_off[b1] - trace_off[b0], 1));
+    int64_t nh = 0;
+    int rc = ggref_build_hotset(trace_ids, trace_off + b0, Wk, 0, part, n_hot, hot.data(),
+                                nullptr, (int64_t)hot.size(), &nh);
+    if (rc != GGREF_OK) return rc;
+    hot.resize((size_t)nh);
+    // Rebuild event: Delta_{k,m} = (H_k in owner m) \ C_{k-1}.
+    std::vector<int32_t> delta;
+    std::set_difference(hot.begin(), hot.end(), cache.begin(), cache.end(),
+                        std::back_inserter(delta));
+    std::vector<int64_t> x(P, 0);
+    for (int32_t u : delta) ++x[ggref_owner(part, u)];
+    acc->e_rebuild = acc->e_rebuild + price_event(x, part, coeffs, &acc->rebuild_events,
+                                                  &acc->rebuild_rows, &acc->t_stall);
+    // Miss events: M_{b,m} = (N_b in owner m) \ H_k for remote m.
+    for (int64_t b = b0; b < b1; ++b) {
+      std::vector<int32_t> remote;
+      for (int64_t i = trace_off[b]; i < trace_off[b + 1]; ++i)
+        if (ggref_owner(part, trace_ids[i]) != part->local_owner) remote.push_back(trace_ids[i]);
+      std::vector<int32_t> miss;
+      std::set_difference(remote.begin(), remote.end(), hot.begin(), hot.end(),
+                          std::back_inserter(miss));
+      std::fill(x.begin(), x.end(), 0);
+      for (int32_t u : miss) ++x[ggref_owner(part, u)];
+      acc->e_miss = acc->e_miss + price_event(x, part, coeffs, &acc->miss_events,
+                                              &acc->miss_rows, &acc->t_stall);
+      acc->remote_rows += (int64_t)remote.size();
+      acc->hits += (int64_t)(remote.size() - miss.size());
+    }
+    cache = hot;   // C_k = H_k (Algorithm 1: the cache holds the window's hot set)
+    acc->windows += 1;
+    acc->batches += Wk;
+    acc->e_stall = coeffs->p_idle * acc->t_stall;
+    acc->e_phy = (acc->e_rebuild + acc->e_miss) + acc->e_stall;
+  }
+  return GGREF_OK;
+}

@@ -155,6 +155,49 @@ int ggref_gather_batch(const int32_t* in_ids, int64_t n, const ggref_part_t* par
                        int64_t cache_rows, const int32_t* slot_of, void* out, int64_t out_stride,
                        ggref_gather_stats_t* stats);
 
+/* Coefficients of the analytical energy model (Sec. IV-B), per owner m;
+ * a "row" is one node's feature row.  eps_payload(m, x) = eps_row[m] * x,
+ * lam_payload(m, x) = lam_row[m] * x. */
+typedef struct ggref_sim_coeffs {
+  double eps_init[GGREF_MAX_PARTS];
+  double eps_row[GGREF_MAX_PARTS];
+  double lam_init[GGREF_MAX_PARTS];
+  double lam_row[GGREF_MAX_PARTS];
+  double bw_bytes_per_s;
+  double row_bytes;
+  double p_idle;
+} ggref_sim_coeffs_t;
+
+typedef struct ggref_sim_acc {
+  int64_t windows;
+  int64_t batches;
+  int64_t rebuild_events;
+  int64_t rebuild_rows;
+  int64_t miss_events;
+  int64_t miss_rows;
+  int64_t remote_rows;
+  int64_t hits;
+  double e_rebuild;
+  double e_miss;
+  double t_stall;
+  double e_stall;
+  double e_phy;
+} ggref_sim_acc_t;
+
+/* The paper's trace simulator for one window size W (Sec. IV-A simulation,
+ * Sec. IV-B Eqs. (1)-(3), Sec. V trace simulator).  trace_ids /
+ * trace_off hold the epoch's N_b, batch b at [trace_off[b],
+ * trace_off[b+1]), each ascending and distinct.  For each window k: H_k =
+ * the n_hot most frequent remote nodes (the hot-set rule above); the
+ * rebuild delta Delta_{k,m} = (H_k in owner m) \ C_{k-1}, C_0 empty and
+ * C_k = H_k; per batch the misses M_{b,m} = (remote N_b in owner m) \ H_k.
+ * Every non-empty set is one event priced by Eq. (1) or (2); an event lasts
+ * the longer of its slowest owner's transfer and its rows at the aggregate
+ * bandwidth; E_stall = p_idle * total duration (Eq. (3)). */
+int ggref_simulate_epoch(const int32_t* trace_ids, const int64_t* trace_off, int64_t n_batches,
+                         int32_t W, int64_t n_hot, const ggref_part_t* part,
+                         const ggref_sim_coeffs_t* coeffs, ggref_sim_acc_t* acc);
+
 #ifdef __cplusplus
 }
 #endif

@@ -49,6 +49,22 @@ class GatherStats(C.Structure):
                 ("miss_rows", C.c_int64 * MAX_PARTS)]
 
 
+class SimCoeffs(C.Structure):
+    _fields_ = [("eps_init", C.c_double * MAX_PARTS), ("eps_row", C.c_double * MAX_PARTS),
+                ("lam_init", C.c_double * MAX_PARTS), ("lam_row", C.c_double * MAX_PARTS),
+                ("bw_bytes_per_s", C.c_double), ("row_bytes", C.c_double),
+                ("p_idle", C.c_double)]
+
+
+class SimAcc(C.Structure):
+    _fields_ = [("windows", C.c_int64), ("batches", C.c_int64),
+                ("rebuild_events", C.c_int64), ("rebuild_rows", C.c_int64),
+                ("miss_events", C.c_int64), ("miss_rows", C.c_int64),
+                ("remote_rows", C.c_int64), ("hits", C.c_int64),
+                ("e_rebuild", C.c_double), ("e_miss", C.c_double), ("t_stall", C.c_double),
+                ("e_stall", C.c_double), ("e_phy", C.c_double)]
+
+
 _lib = None
 
 
@@ -81,6 +97,8 @@ def lib():
         L.ggref_stage_bulk.restype = C.c_int
         L.ggref_gather_batch.argtypes = [P, i64, P, P, P, i64, i64, P, P, i64, P]
         L.ggref_gather_batch.restype = C.c_int
+        L.ggref_simulate_epoch.argtypes = [P, P, i64, i32, i64, P, P, P]
+        L.ggref_simulate_epoch.restype = C.c_int
         _lib = L
     return _lib
 
@@ -233,6 +251,37 @@ def gather_batch(in_ids, part, feat, cache, cache_stride, slot_of, out, out_stri
                                     _p(cache), cache_stride, cache.shape[0], _p(slot_of), _p(out),
                                     out_stride, C.byref(gs)), "ggref_gather_batch")
     return stats_dict(gs, part.num_parts)
+
+
+def sim_coeffs(P, eps_init, eps_row, lam_init, lam_row, bw_bytes_per_s, row_bytes, p_idle):
+    """Coefficients of the analytical model; per-owner terms are scalars
+    (the same for every owner) or sequences of P values."""
+    c = SimCoeffs()
+    for name, v in (("eps_init", eps_init), ("eps_row", eps_row), ("lam_init", lam_init),
+                    ("lam_row", lam_row)):
+        vals = list(v) if hasattr(v, "__len__") else [v] * P
+        arr = getattr(c, name)
+        for m in range(P):
+            arr[m] = float(vals[m])
+    c.bw_bytes_per_s, c.row_bytes, c.p_idle = float(bw_bytes_per_s), float(row_bytes), float(p_idle)
+    return c
+
+
+def simulate_epoch(trace_ids, trace_off, W, n_hot, part, coeffs):
+    """The trace simulator for window size W over the epoch's N_b (batch b
+    at trace_ids[trace_off[b]:trace_off[b+1]], ascending): event counts and
+    the energies of Eqs. (1)-(3)."""
+    ids = np.ascontiguousarray(trace_ids, dtype=np.int32)
+    off = np.ascontiguousarray(trace_off, dtype=np.int64)
+    acc = SimAcc()
+    _check(lib().ggref_simulate_epoch(_p(ids), _p(off), off.shape[0] - 1, W, n_hot, C.byref(part),
+                                      C.byref(coeffs), C.byref(acc)), "ggref_simulate_epoch")
+    return sim_dict(acc)
+
+
+def sim_dict(acc):
+    return {name: (float(getattr(acc, name)) if typ is C.c_double else int(getattr(acc, name)))
+            for name, typ in acc._fields_}
 
 
 def stats_dict(st, P):

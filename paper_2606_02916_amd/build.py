@@ -11,7 +11,8 @@ ROOT = os.path.dirname(HERE)
 CSRC = os.path.join(HERE, "csrc")
 BUILD = os.path.join(ROOT, "_build")
 LIB = os.path.join(HERE, "libgg.so")
-SOURCES = ["common.hip", "sample.hip", "hotset.hip", "bucket.hip", "stage.hip", "gather.hip"]
+SOURCES = ["common.hip", "sample.hip", "hotset.hip", "bucket.hip", "stage.hip", "gather.hip",
+           "sim.hip"]
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 
 FLAGS = [

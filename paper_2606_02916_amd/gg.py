@@ -71,8 +71,25 @@ class gg_gather_stats_t(C.Structure):
                 ("miss_rows", C.c_int64 * MAX_PARTS)]
 
 
+class gg_sim_coeffs_t(C.Structure):
+    _fields_ = [("eps_init", C.c_double * MAX_PARTS), ("eps_row", C.c_double * MAX_PARTS),
+                ("lam_init", C.c_double * MAX_PARTS), ("lam_row", C.c_double * MAX_PARTS),
+                ("bw_bytes_per_s", C.c_double), ("row_bytes", C.c_double),
+                ("p_idle", C.c_double)]
+
+
+class gg_sim_acc_t(C.Structure):
+    _fields_ = [("windows", C.c_int64), ("batches", C.c_int64),
+                ("rebuild_events", C.c_int64), ("rebuild_rows", C.c_int64),
+                ("miss_events", C.c_int64), ("miss_rows", C.c_int64),
+                ("remote_rows", C.c_int64), ("hits", C.c_int64),
+                ("e_rebuild", C.c_double), ("e_miss", C.c_double), ("t_stall", C.c_double),
+                ("e_stall", C.c_double), ("e_phy", C.c_double)]
+
+
 STAGE_STATS_BYTES = C.sizeof(gg_stage_stats_t)
 GATHER_STATS_BYTES = C.sizeof(gg_gather_stats_t)
+SIM_ACC_BYTES = C.sizeof(gg_sim_acc_t)
 
 # Every function include/gg.h declares, with its ctypes signature.
 _P, _I32, _I64, _U64, _SZ = C.c_void_p, C.c_int32, C.c_int64, C.c_uint64, C.c_size_t
@@ -92,6 +109,7 @@ SIGNATURES = {
                                 _P, _SZ, _P]),
     "gg_gather_batch": (C.c_int, [_P, _P, _I32, _I64, _P, _P, _P, _I64, _I64, _P, _P, _I64, _P,
                                   _P, _P, _SZ, _P]),
+    "gg_sim_accumulate": (C.c_int, [_P, _P, _I32, _P, _P, _P, _P]),
     "gg_status_string": (C.c_char_p, [_I32]),
     "gg_last_error": (C.c_char_p, []),
     "gg_version": (C.c_int, []),
@@ -253,6 +271,33 @@ def gg_gather_batch(in_ids, bounds_ptr, nseg, n_cap, part, feat, cache, cache_st
                                      _ptr(slot_of), _ptr(out), out_stride, stats_ptr,
                                      _ptr(status), _ptr(ws), ws.numel(), _stream(stream)),
                  "gg_gather_batch")
+
+
+def make_sim_coeffs(P, eps_init, eps_row, lam_init, lam_row, bw_bytes_per_s, row_bytes, p_idle):
+    """Coefficients of the analytical energy model; each per-owner term is a
+    scalar (every owner alike) or a sequence of P values."""
+    c = gg_sim_coeffs_t()
+    for name, v in (("eps_init", eps_init), ("eps_row", eps_row), ("lam_init", lam_init),
+                    ("lam_row", lam_row)):
+        vals = list(v) if hasattr(v, "__len__") else [v] * P
+        arr = getattr(c, name)
+        for m in range(P):
+            arr[m] = float(vals[m])
+    c.bw_bytes_per_s, c.row_bytes, c.p_idle = float(bw_bytes_per_s), float(row_bytes), float(p_idle)
+    return c
+
+
+def gg_sim_accumulate(stage_stats, gather_stats_ptr, nseg, part, coeffs, acc, stream=None):
+    """gather_stats_ptr is the device address of nseg gather statistics."""
+    return check(lib.gg_sim_accumulate(_ptr(stage_stats), gather_stats_ptr, nseg, C.byref(part),
+                                       C.byref(coeffs), _ptr(acc), _stream(stream)),
+                 "gg_sim_accumulate")
+
+
+def sim_acc_from_bytes(buf):
+    a = gg_sim_acc_t.from_buffer_copy(bytes(buf))
+    return {name: (float(getattr(a, name)) if typ is C.c_double else int(getattr(a, name)))
+            for name, typ in a._fields_}
 
 
 def gg_status_string(code):

@@ -192,13 +192,20 @@ class FetchPipeline:
                            out, self.stride, self.gather_stats.data_ptr(), self.status, self.ws)
         return out
 
+    def sim_accumulate(self, Wk, coeffs, acc):
+        """Adds the window just gathered to the simulator totals `acc` (a
+        device buffer of SIM_ACC_BYTES, zeroed before the first window)."""
+        gg.gg_sim_accumulate(self.stage_stats, self.gather_stats.data_ptr(), Wk, self.part,
+                             coeffs, acc)
+
     def window(self, seeds, seed_off, batch0, epoch=0, rng_seed=0, outs=None, events=None,
-               gather_events=None, per_batch=False):
+               gather_events=None, per_batch=False, sim=None):
         """Enqueues one window.  By default the W gathers run as one launch
         into win_out; with per_batch=True every batch is its own launch into
         outs[b] (default: the driver's ping-pong buffers).  events: optional
         list of 6 torch events recorded between the calls; gather_events:
-        optional list of (start, end) event pairs, one per gather launch."""
+        optional list of (start, end) event pairs, one per gather launch;
+        sim: optional (coeffs, acc) to add the window to simulator totals."""
         cur = self.k & 1
         ev = events if events is not None else [None] * 6
         _rec(ev[0])
@@ -225,6 +232,8 @@ class FetchPipeline:
             if gather_events is not None:
                 gather_events[0][1].record()
         _rec(ev[5])
+        if sim is not None:
+            self.sim_accumulate(Wk, *sim)
         self.k += 1
         return Wk
 
@@ -309,7 +318,7 @@ class LookaheadPipeline:
         self.k = 0
 
     def window(self, seeds, seed_off, batch0, epoch=0, rng_seed=0, out=None, events=None,
-               gather_events=None):
+               gather_events=None, sim=None):
         """Enqueues window k; returns (number of batches, buffer set).  The
         window's rows land in the set's win_out (or `out`) on the gather
         stream; wait on gathered_event(k) before reading them.  Inputs
@@ -318,7 +327,9 @@ class LookaheadPipeline:
         around its three calls and one after staging on the stage stream
         (the stage time is events[4] minus the later of events[3] and the
         previous window's staging end); gather_events: optional (start, end)
-        pair recorded on the gather stream around the gather launch."""
+        pair, the start recorded on the stage stream when staging ends and
+        the end on the gather stream after the gather; sim: optional
+        (coeffs, acc) to add the window to simulator totals."""
         k, g = self.k, self.geo
         X, T = k % self.nsets, k % self.NSLOT
         cur, prev = self.sets[X], self.sets[(k - 1) % self.nsets]
@@ -368,9 +379,24 @@ class LookaheadPipeline:
                            stream=gs.cuda_stream)
         if gather_events is not None:
             gather_events[1].record(gs)
+        if sim is not None:           # simulator totals, in window order on the gather stream
+            gg.gg_sim_accumulate(cur.stage_stats, cur.gather_stats.data_ptr(), Wk, self.part,
+                                 sim[0], sim[1], stream=gs.cuda_stream)
         self.gathered[X].record(gs)
         self.k += 1
         return Wk, cur
+
+    def regather(self, bufs, Wk, out=None, stream=None):
+        """Launches the gather of a finished window again (same inputs, same
+        output) on `stream` (default: the caller's current stream), e.g. to
+        time it with the chip to itself.  The window must be complete."""
+        o = bufs.win_out if out is None else out
+        bounds = bufs.frontier_off.data_ptr() + 8 * (self.L * Wk)
+        gg.gg_gather_batch(bufs.frontier_ids, bounds, Wk, o.shape[0], self.part, self.feat,
+                           bufs.cache, self.cache_stride, self.geo.hot_cap, bufs.slot_of, o,
+                           self.stride, bufs.gather_stats.data_ptr(), self.status,
+                           self.gather_ws, stream=stream)
+        return o
 
     def gathered_event(self, k):
         return self.gathered[k % self.nsets]

@@ -58,6 +58,11 @@ int main() {
   F(gg_stage_stats_t, rows) F(gg_stage_stats_t, bytes) F(gg_stage_stats_t, delta_rows)
   S(gg_gather_stats_t) F(gg_gather_stats_t, misses) F(gg_gather_stats_t, miss_requests)
   F(gg_gather_stats_t, miss_rows)
+  S(gg_sim_coeffs_t) F(gg_sim_coeffs_t, eps_row) F(gg_sim_coeffs_t, lam_init)
+  F(gg_sim_coeffs_t, lam_row) F(gg_sim_coeffs_t, bw_bytes_per_s) F(gg_sim_coeffs_t, row_bytes)
+  F(gg_sim_coeffs_t, p_idle)
+  S(gg_sim_acc_t) F(gg_sim_acc_t, rebuild_events) F(gg_sim_acc_t, miss_rows)
+  F(gg_sim_acc_t, hits) F(gg_sim_acc_t, e_rebuild) F(gg_sim_acc_t, t_stall) F(gg_sim_acc_t, e_phy)
   return 0;
 }
 """
@@ -146,3 +151,9 @@ def test_bad_arguments_are_rejected_on_the_host(gg):
         gg.gg_gather_batch(t, t.data_ptr(), 0, 10, part, feat, t, 256, 10, t, t, 256,
                            t.data_ptr(), t, t, stream=0)
     assert "nseg" in gg.gg_last_error()
+    c = gg.make_sim_coeffs(4, 1.0, 0.01, 1e-3, 1e-5, 0.0, 256, 30.0)    # no bandwidth ceiling
+    with pytest.raises(gg.GGError):
+        gg.gg_sim_accumulate(t, t.data_ptr(), 4, part, c, t, stream=0)
+    c = gg.make_sim_coeffs(4, 1.0, 0.01, 1e-3, 1e-5, 1e9, 256, 30.0)
+    with pytest.raises(gg.GGError):                                      # more batches than W max
+        gg.gg_sim_accumulate(t, t.data_ptr(), 65, part, c, t, stream=0)

@@ -392,3 +392,74 @@ def test_lookahead_pipeline_equals_sequential(name, n_hot, W, nsets):
                                            if k >= nsets else 0)
         e_st.pop("invalidated")
         assert g_st == e_st, f"window {k} staging statistics"
+
+
+def _oracle_trace(inst):
+    """The epoch's N_b from the oracle sampler, batch by batch (N_b does not
+    depend on W)."""
+    from oracle import ggref
+    wl = inst.wl
+    L = len(wl.fanout)
+    boff = inst.batch_off
+    nb = boff.shape[0] - 1
+    ids, off = [], [0]
+    for b0 in range(0, nb, 4):
+        b1 = min(nb, b0 + 4)
+        so = boff[b0:b1 + 1] - boff[b0]
+        fids, foff, _, _ = ggref.sample_window(inst.row_ptr, inst.col_idx,
+                                               inst.seeds[boff[b0]:boff[b1]], so, wl.fanout,
+                                               0, 0, b0)
+        Wk = b1 - b0
+        for b in range(Wk):
+            s = L * Wk + b
+            ids.append(fids[foff[s]:foff[s + 1]])
+            off.append(off[-1] + int(foff[s + 1] - foff[s]))
+    return np.concatenate(ids).astype(np.int32), np.array(off, np.int64)
+
+
+SIM_COEF = dict(eps_init=0.025, eps_row=1.6e-5, lam_init=5e-4, lam_row=3.2e-7,
+                bw_bytes_per_s=1.25e9, row_bytes=400.0, p_idle=30.0)
+
+
+@pytest.mark.parametrize("name,W,n_hot,driver", [
+    ("tiny", 1, -1, "seq"), ("tiny", 2, 2000, "seq"), ("tiny", 4, 0, "seq"),
+    ("small", 1, 3000, "seq"), ("small", 4, 3000, "delta"), ("small", 8, -1, "seq"),
+    ("small", 3, 0, "seq"), ("small", 4, 3000, "lookahead"), ("small", 2, 20000, "lookahead")])
+def test_simulator_counts_match_oracle(name, W, n_hot, driver):
+    log(f"{name}: simulator z(W), E_phy(W) over the epoch, W={W}, n_hot={n_hot}, {driver}")
+    import torch as T
+    from oracle import ggref
+    from paper_2606_02916_amd import LookaheadPipeline, gg
+    inst = synth.instance(name)
+    wl = inst.wl
+    w = world(inst, W=W, n_hot=n_hot, delta=driver == "delta")
+    P = wl.num_parts
+    coeffs = gg.make_sim_coeffs(P, **SIM_COEF)
+    acc = T.zeros(gg.SIM_ACC_BYTES, dtype=T.uint8, device=w.dev)
+    boff = inst.batch_off
+    nwin = synth.n_windows(boff, W)
+    seeds_d = T.from_numpy(inst.seeds).to(w.dev)
+    if driver == "lookahead":
+        pipe = LookaheadPipeline(w.row_ptr_d, w.col_idx_d, P, wl.part_kind, wl.local_owner,
+                                 inst.range_start, w.shards_d, [s.shape[0] for s in inst.shards],
+                                 wl.row_bytes, wl.row_stride, W, wl.fanout, wl.batch_size,
+                                 n_hot=n_hot, device=w.dev)
+    else:
+        pipe = w.pipe
+    for k in range(nwin):
+        b0, b1 = synth.window_batches(boff, W, k)
+        pipe.window(seeds_d[boff[b0]:boff[b1]], boff[b0:b1 + 1] - boff[b0], b0,
+                    sim=(coeffs, acc))
+    assert pipe.read_status() == 0
+    T.cuda.synchronize()
+    got = gg.sim_acc_from_bytes(acc.cpu().numpy().tobytes())
+    ids, off = _oracle_trace(inst)
+    part = ggref.make_part(P, wl.part_kind, wl.local_owner, wl.num_nodes, inst.range_start)
+    ref = ggref.simulate_epoch(ids, off, W, n_hot, part, ggref.sim_coeffs(P, **SIM_COEF))
+    # integer counts exactly; the fp64 energies are formed in the same order
+    # without fused multiply-adds on both sides, so they agree bit for bit
+    assert got == ref
+    if n_hot == 0:
+        assert got["rebuild_events"] == 0 and got["hits"] == 0
+    if n_hot < 0:
+        assert got["miss_events"] == 0
