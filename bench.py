@@ -100,7 +100,9 @@ def summarize(args):
                        f"{sm / 1e6:9.3f} {100 * sm / tot:5.1f}%")
         if args.phases:
             # the gather call's kernels per launch, split into the bench's
-            # phases (pre-pass, warm-up, timed steps) by dispatch order
+            # phases (pre-pass, warm-up, timed steps) by dispatch order; with
+            # the look-ahead driver the pre-pass alternates the pipeline's
+            # gather and the timed regather (the odd launches)
             n_pre, n_warm, n_timed = (int(x) for x in args.phases.split(","))
             per = {}
             for part in ("k_gather_zero", "k_gather_rows", "k_gather_finish"):
@@ -111,10 +113,11 @@ def summarize(args):
             calls = [sum(per[p][i] for p in per if i < len(per[p])) for i in range(n)]
             out.append("")
             out.append("# gg_gather_batch (zero + rows + finish) by bench phase, microseconds")
-            for label, lo, hi in (("pre-pass, chip to itself", 0, n_pre),
-                                  ("timed steps", n - n_timed, n)):
-                v = calls[lo:hi]
-                r = per["k_gather_rows"][lo:hi]
+            for label, lo, hi, step in (("pre-pass, all launches", 0, n_pre, 1),
+                                        ("pre-pass, odd launches", 1, n_pre, 2),
+                                        ("timed steps", n - n_timed, n, 1)):
+                v = calls[lo:hi:step]
+                r = per["k_gather_rows"][lo:hi:step]
                 if v:
                     out.append(f"{label:34s} launches {len(v):3d}  call avg {sum(v) / len(v) / 1e3:8.2f}"
                                f"  k_gather_rows avg {sum(r) / len(r) / 1e3:8.2f}")
@@ -181,6 +184,10 @@ def main():
                          "z(W) and energy estimate E_phy(W) (synthetic coefficients)")
     ap.add_argument("--n-hot", default="-1",
                     help="with --simulate: comma-separated hot-set budgets (-1 = union)")
+    ap.add_argument("--hot-frac", default=None,
+                    help="with --simulate: budgets relative to each window, e.g. 1/10,1/4: the "
+                         "top fraction of the window's distinct remote nodes; the hit ratio is "
+                         "then the share of remote requests that fraction covers")
     ap.add_argument("--summarize", action="store_true",
                     help="write profiles/ summaries from rocprofv3 databases instead of running")
     ap.add_argument("--trace-db", default=None)
@@ -543,12 +550,16 @@ def simulate(args, wl):
     cd = sim_coefficients(wl)
     coeffs = gg.make_sim_coeffs(P, **cd)
     results = []
-    for n_hot in [int(x) for x in args.n_hot.split(",")]:
+    if args.hot_frac:
+        budgets = [(-1, tuple(int(v) for v in f.split("/"))) for f in args.hot_frac.split(",")]
+    else:
+        budgets = [(int(x), None) for x in args.n_hot.split(",")]
+    for n_hot, frac in budgets:
         for W in [int(x) for x in args.simulate.split(",")]:
             pipe = FetchPipeline(row_ptr_d, col_idx_d, P, wl.part_kind, wl.local_owner,
                                  inst.range_start, shards_d, [s.shape[0] for s in inst.shards],
                                  rb, wl.row_stride, W, wl.fanout, wl.batch_size, n_hot=n_hot,
-                                 device=dev, delta=True)
+                                 device=dev, delta=True, hot_frac=frac)
             nwin = synth.n_windows(boff, W)
             wins = []
             for k in range(nwin):
@@ -567,11 +578,13 @@ def simulate(args, wl):
             if pipe.read_status() != 0:
                 raise RuntimeError(f"device status {pipe.read_status()} at W={W}")
             a = gg.sim_acc_from_bytes(acc.cpu().numpy().tobytes())
-            r = {"n_hot": n_hot, "W": W, "windows": a["windows"],
+            r = {"n_hot": n_hot if frac is None else f"{frac[0]}/{frac[1]} of each window",
+                 "W": W, "windows": a["windows"],
                  "z": {"rebuild_events": a["rebuild_events"], "miss_events": a["miss_events"],
                        "t_stall_s": a["t_stall"],
                        "hit_ratio": a["hits"] / a["remote_rows"] if a["remote_rows"] else 1.0},
                  "rebuild_rows": a["rebuild_rows"], "miss_rows": a["miss_rows"],
+                 "remote_requests": a["remote_rows"],
                  "E_rebuild_J": a["e_rebuild"], "E_miss_J": a["e_miss"],
                  "E_stall_J": a["e_stall"], "E_phy_J": a["e_phy"],
                  "epoch_ms": round(el * 1e3, 3)}

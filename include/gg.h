@@ -191,14 +191,18 @@ int gg_sample_window(const gg_csr_t* csr, const int32_t* seeds_d, const int64_t*
  * gg_sample_window (frontier_bits_d).  freq(u) = number of batches whose N_b
  * holds u; a node is remote when its owner is not part->local_owner.
  * n_hot < 0 keeps every remote node of the window (the union); n_hot >= 0
- * keeps the n_hot most frequent (ties: smaller id first).  hot_ids_d
+ * keeps the n_hot most frequent (ties: smaller id first).  A budget
+ * relative to the window (the "top 10%" of Sec. I): with hot_den > 0 the
+ * budget is ceil(U * hot_num / hot_den), U = the number of distinct remote
+ * nodes of the window, decided on the device (needs n_hot = -1 and
+ * 0 <= hot_num <= hot_den <= 2^31).  hot_ids_d
  * receives the chosen ids ascending, hot_freq_d (may be NULL) their freq;
  * hot_count_d[0] = entries written (<= cap), hot_count_d[1] = entries
  * required. */
 int gg_build_hotset(const uint32_t* frontier_bits_d, int32_t W, const gg_part_t* part,
-                    int64_t n_hot, int32_t* hot_ids_d, int32_t* hot_freq_d, int64_t cap,
-                    int64_t* hot_count_d, int32_t* status_d, void* ws, size_t ws_bytes,
-                    hipStream_t stream);
+                    int64_t n_hot, int64_t hot_num, int64_t hot_den, int32_t* hot_ids_d,
+                    int32_t* hot_freq_d, int64_t cap, int64_t* hot_count_d, int32_t* status_d,
+                    void* ws, size_t ws_bytes, hipStream_t stream);
 
 /* Groups the hot set by owner, one bucket per owner (Sec. IV-A: one bulk
  * request per partition owner): bucket_ids_d receives the hot_count_d[0]

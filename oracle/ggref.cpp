@@ -237,9 +237,13 @@ int ggref_sample_window(const ggref_csr_t* csr, const int32_t* seeds, const int6
 // node of the window (the union); otherwise the first n_hot in order of
 // decreasing freq, ties broken by smaller id.
 int ggref_build_hotset(const int32_t* frontier_ids, const int64_t* frontier_off, int32_t W,
-                       int32_t L, const ggref_part_t* part, int64_t n_hot, int32_t* hot_ids,
-                       int32_t* hot_freq, int64_t cap, int64_t* hot_count) {
+                       int32_t L, const ggref_part_t* part, int64_t n_hot, int64_t hot_num,
+                       int64_t hot_den, int32_t* hot_ids, int32_t* hot_freq, int64_t cap,
+                       int64_t* hot_count) {
   if (!part_ok(part) || W < 1 || L < 0) return GGREF_ERR_ARG;
+  if (hot_den < 0 || hot_den > (1LL << 31) ||
+      (hot_den > 0 && (n_hot != -1 || hot_num < 0 || hot_num > hot_den)))
+    return GGREF_ERR_ARG;
   std::vector<int32_t> remote;
   for (int32_t b = 0; b < W; ++b) {
     const int64_t s = (int64_t)L * W + b;
@@ -255,6 +259,10 @@ int ggref_build_hotset(const int32_t* frontier_ids, const int64_t* frontier_off,
     while (j < remote.size() && remote[j] == remote[i]) ++j;
     uf.push_back({remote[i], (int32_t)(j - i)});
     i = j;
+  }
+  if (hot_den > 0) {   // the top hot_num / hot_den of the U distinct remote nodes, rounded up
+    const int64_t U = (int64_t)uf.size();
+    n_hot = (U * hot_num + hot_den - 1) / hot_den;
   }
   if (n_hot >= 0 && n_hot < (int64_t)uf.size()) {
     std::stable_sort(uf.begin(), uf.end(),
@@ -430,8 +438,9 @@ double price_event(const std::vector<int64_t>& x, const ggref_part_t* part,
 }  // namespace
 
 int ggref_simulate_epoch(const int32_t* trace_ids, const int64_t* trace_off, int64_t n_batches,
-                         int32_t W, int64_t n_hot, const ggref_part_t* part,
-                         const ggref_sim_coeffs_t* coeffs, ggref_sim_acc_t* acc) {
+                         int32_t W, int64_t n_hot, int64_t hot_num, int64_t hot_den,
+                         const ggref_part_t* part, const ggref_sim_coeffs_t* coeffs,
+                         ggref_sim_acc_t* acc) {
   if (!part_ok(part) || !coeffs || !acc || W < 1 || n_batches < 0 ||
       !(coeffs->bw_bytes_per_s > 0.0))
     return GGREF_ERR_ARG;
@@ -445,8 +454,8 @@ int ggref_simulate_epoch(const int32_t* trace_ids, const int64_t* trace_off, int
     // H_k from the window's N_b (level 0 of a one-level layout).
     std::vector<int32_t> hot((size_t)std::max<int64_t>(trace_off[b1] - trace_off[b0], 1));
     int64_t nh = 0;
-    int rc = ggref_build_hotset(trace_ids, trace_off + b0, Wk, 0, part, n_hot, hot.data(),
-                                nullptr, (int64_t)hot.size(), &nh);
+    int rc = ggref_build_hotset(trace_ids, trace_off + b0, Wk, 0, part, n_hot, hot_num, hot_den,
+                                hot.data(), nullptr, (int64_t)hot.size(), &nh);
     if (rc != GGREF_OK) return rc;
     hot.resize((size_t)nh);
     // Rebuild event: Delta_{k,m} = (H_k in owner m) \ C_{k-1}.

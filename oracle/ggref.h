@@ -121,11 +121,14 @@ int ggref_sample_window(const ggref_csr_t* csr, const int32_t* seeds, const int6
 /* Hot set of a window (Sec. IV-A window simulation): the remote nodes of
  * the window's input sets N_b = frontier segment (L, b), with freq(u) = the
  * number of batches whose N_b holds u.  n_hot < 0 keeps all of them;
- * otherwise the n_hot most frequent (ties: smaller id first).  Output
- * ascending by id. */
+ * otherwise the n_hot most frequent (ties: smaller id first).  With
+ * hot_den > 0 (and n_hot = -1) the budget is the top hot_num / hot_den of
+ * the window's U distinct remote nodes, rounded up: ceil(U * hot_num /
+ * hot_den) (the "top 10%" of Sec. I).  Output ascending by id. */
 int ggref_build_hotset(const int32_t* frontier_ids, const int64_t* frontier_off, int32_t W,
-                       int32_t L, const ggref_part_t* part, int64_t n_hot, int32_t* hot_ids,
-                       int32_t* hot_freq, int64_t cap, int64_t* hot_count);
+                       int32_t L, const ggref_part_t* part, int64_t n_hot, int64_t hot_num,
+                       int64_t hot_den, int32_t* hot_ids, int32_t* hot_freq, int64_t cap,
+                       int64_t* hot_count);
 
 /* Stable partition of the hot set by owner: owner-major, input order kept
  * inside each owner; owner_off has P+1 entries. */
@@ -188,15 +191,16 @@ typedef struct ggref_sim_acc {
  * Sec. IV-B Eqs. (1)-(3), Sec. V trace simulator).  trace_ids /
  * trace_off hold the epoch's N_b, batch b at [trace_off[b],
  * trace_off[b+1]), each ascending and distinct.  For each window k: H_k =
- * the n_hot most frequent remote nodes (the hot-set rule above); the
+ * the hot set under the budget (n_hot, hot_num / hot_den) as above; the
  * rebuild delta Delta_{k,m} = (H_k in owner m) \ C_{k-1}, C_0 empty and
  * C_k = H_k; per batch the misses M_{b,m} = (remote N_b in owner m) \ H_k.
  * Every non-empty set is one event priced by Eq. (1) or (2); an event lasts
  * the longer of its slowest owner's transfer and its rows at the aggregate
  * bandwidth; E_stall = p_idle * total duration (Eq. (3)). */
 int ggref_simulate_epoch(const int32_t* trace_ids, const int64_t* trace_off, int64_t n_batches,
-                         int32_t W, int64_t n_hot, const ggref_part_t* part,
-                         const ggref_sim_coeffs_t* coeffs, ggref_sim_acc_t* acc);
+                         int32_t W, int64_t n_hot, int64_t hot_num, int64_t hot_den,
+                         const ggref_part_t* part, const ggref_sim_coeffs_t* coeffs,
+                         ggref_sim_acc_t* acc);
 
 #ifdef __cplusplus
 }

@@ -89,7 +89,7 @@ def lib():
         L.ggref_sample_window.argtypes = [P, P, P, i32, P, i32, u64, i32, i64, P, i64, P, P,
                                           i64, P, P]
         L.ggref_sample_window.restype = C.c_int
-        L.ggref_build_hotset.argtypes = [P, P, i32, i32, P, i64, P, P, i64, P]
+        L.ggref_build_hotset.argtypes = [P, P, i32, i32, P, i64, i64, i64, P, P, i64, P]
         L.ggref_build_hotset.restype = C.c_int
         L.ggref_bucket_by_owner.argtypes = [P, i64, P, P, P]
         L.ggref_bucket_by_owner.restype = C.c_int
@@ -97,7 +97,7 @@ def lib():
         L.ggref_stage_bulk.restype = C.c_int
         L.ggref_gather_batch.argtypes = [P, i64, P, P, P, i64, i64, P, P, i64, P]
         L.ggref_gather_batch.restype = C.c_int
-        L.ggref_simulate_epoch.argtypes = [P, P, i64, i32, i64, P, P, P]
+        L.ggref_simulate_epoch.argtypes = [P, P, i64, i32, i64, i64, i64, P, P, P]
         L.ggref_simulate_epoch.restype = C.c_int
         _lib = L
     return _lib
@@ -205,15 +205,18 @@ def sample_window(row_ptr, col_idx, seeds, seed_off, fanout, rng_seed, epoch, ba
     raise OracleError("sample_window capacity loop")
 
 
-def build_hotset(frontier_ids, frontier_off, W, L, part, n_hot=-1):
+def build_hotset(frontier_ids, frontier_off, W, L, part, n_hot=-1, hot_frac=None):
+    """hot_frac = (num, den): the top ceil(U * num / den) of the window's U
+    distinct remote nodes (n_hot must then be -1)."""
+    num, den = hot_frac if hot_frac is not None else (0, 0)
     cap = max(1, int(frontier_ids.shape[0]))
     hot = np.zeros(cap, dtype=np.int32)
     freq = np.zeros(cap, dtype=np.int32)
     cnt = np.zeros(1, dtype=np.int64)
     fids = np.ascontiguousarray(frontier_ids, dtype=np.int32)
     foff = np.ascontiguousarray(frontier_off, dtype=np.int64)
-    _check(lib().ggref_build_hotset(_p(fids), _p(foff), W, L, C.byref(part), n_hot, _p(hot),
-                                    _p(freq), cap, _p(cnt)), "ggref_build_hotset")
+    _check(lib().ggref_build_hotset(_p(fids), _p(foff), W, L, C.byref(part), n_hot, num, den,
+                                    _p(hot), _p(freq), cap, _p(cnt)), "ggref_build_hotset")
     n = int(cnt[0])
     return hot[:n], freq[:n]
 
@@ -267,15 +270,17 @@ def sim_coeffs(P, eps_init, eps_row, lam_init, lam_row, bw_bytes_per_s, row_byte
     return c
 
 
-def simulate_epoch(trace_ids, trace_off, W, n_hot, part, coeffs):
+def simulate_epoch(trace_ids, trace_off, W, n_hot, part, coeffs, hot_frac=None):
     """The trace simulator for window size W over the epoch's N_b (batch b
     at trace_ids[trace_off[b]:trace_off[b+1]], ascending): event counts and
     the energies of Eqs. (1)-(3)."""
+    num, den = hot_frac if hot_frac is not None else (0, 0)
     ids = np.ascontiguousarray(trace_ids, dtype=np.int32)
     off = np.ascontiguousarray(trace_off, dtype=np.int64)
     acc = SimAcc()
-    _check(lib().ggref_simulate_epoch(_p(ids), _p(off), off.shape[0] - 1, W, n_hot, C.byref(part),
-                                      C.byref(coeffs), C.byref(acc)), "ggref_simulate_epoch")
+    _check(lib().ggref_simulate_epoch(_p(ids), _p(off), off.shape[0] - 1, W, n_hot, num, den,
+                                      C.byref(part), C.byref(coeffs), C.byref(acc)),
+           "ggref_simulate_epoch")
     return sim_dict(acc)
 
 

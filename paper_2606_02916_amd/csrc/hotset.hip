@@ -135,8 +135,11 @@ __global__ void __launch_bounds__(kBlock) k_hot_hist(const uint32_t* bits, KPart
 }
 
 // One block: total histogram, then the threshold f* and remainder r.
+// With den > 0 the budget is ceil(total * num / den) of the window's total
+// distinct remote nodes (exact integer arithmetic).
 __global__ void __launch_bounds__(1024) k_hot_select(const int32_t* chunk_hist, int32_t nch,
-                                                     int32_t W, int64_t n_hot, int64_t* params) {
+                                                     int32_t W, int64_t n_hot, int64_t num,
+                                                     int64_t den, int64_t* params) {
   __shared__ int64_t hist[GG_MAX_W + 2];
   for (int t = threadIdx.x; t < GG_MAX_W + 2; t += blockDim.x) hist[t] = 0;
   __syncthreads();
@@ -149,6 +152,7 @@ __global__ void __launch_bounds__(1024) k_hot_select(const int32_t* chunk_hist, 
   if (threadIdx.x == 0) {
     int64_t total = 0;
     for (int32_t f = 1; f <= W; ++f) total += hist[f];
+    if (den > 0) n_hot = (total * num + den - 1) / den;
     int64_t fstar = 0, r = 0;
     if (n_hot >= total) {
       fstar = 0;
@@ -318,13 +322,18 @@ extern "C" size_t gg_ws_hotset(int64_t num_nodes, int32_t W) {
 }
 
 extern "C" int gg_build_hotset(const uint32_t* frontier_bits_d, int32_t W, const gg_part_t* part,
-                               int64_t n_hot, int32_t* hot_ids_d, int32_t* hot_freq_d,
-                               int64_t cap, int64_t* hot_count_d, int32_t* status_d, void* ws,
+                               int64_t n_hot, int64_t hot_num, int64_t hot_den,
+                               int32_t* hot_ids_d, int32_t* hot_freq_d, int64_t cap,
+                               int64_t* hot_count_d, int32_t* status_d, void* ws,
                                size_t ws_bytes, hipStream_t stream) {
   GG_REQUIRE(frontier_bits_d && hot_count_d && status_d && (cap == 0 || hot_ids_d),
              "NULL argument");
   GG_REQUIRE(W >= 1 && W <= GG_MAX_W, "W = %d outside 1..%d", W, GG_MAX_W);
   GG_REQUIRE(cap >= 0, "negative capacity");
+  GG_REQUIRE(hot_den >= 0 && hot_den <= (1LL << 31), "hot_den %lld outside 0..2^31",
+             (long long)hot_den);
+  GG_REQUIRE(hot_den == 0 || (n_hot == -1 && hot_num >= 0 && hot_num <= hot_den),
+             "a relative budget needs n_hot = -1 and 0 <= hot_num <= hot_den");
   GG_REQUIRE(aligned16(frontier_bits_d), "frontier_bits must be 16-byte aligned");
   KPart kp;
   int rc = pack_part(part, &kp);
@@ -344,12 +353,12 @@ extern "C" int gg_build_hotset(const uint32_t* frontier_bits_d, int32_t W, const
   const int64_t* params = nullptr;
   if (n_hot == 0) {
     a.fstar = W + 1;
-  } else if (n_hot > 0) {
+  } else if (n_hot > 0 || hot_den > 0) {
     hipLaunchKernelGGL(k_hot_hist, dim3(nch), dim3(kBlock), 0, stream, frontier_bits_d, kp, a,
                        hw.chunk_hist);
     GG_LAUNCH_CHECK("k_hot_hist");
     hipLaunchKernelGGL(k_hot_select, dim3(1), dim3(1024), 0, stream, hw.chunk_hist, nch, W, n_hot,
-                       hw.params);
+                       hot_num, hot_den, hw.params);
     GG_LAUNCH_CHECK("k_hot_select");
     params = hw.params;
   }

@@ -103,7 +103,8 @@ SIGNATURES = {
     "gg_ws_gather": (_SZ, [_I64, _I32, _I32]),
     "gg_sample_window": (C.c_int, [_P, _P, _P, _I32, _P, _I32, _U64, _I32, _I64, _P, _P, _P, _SZ,
                                    _P]),
-    "gg_build_hotset": (C.c_int, [_P, _I32, _P, _I64, _P, _P, _I64, _P, _P, _P, _SZ, _P]),
+    "gg_build_hotset": (C.c_int, [_P, _I32, _P, _I64, _I64, _I64, _P, _P, _I64, _P, _P, _P, _SZ,
+                                  _P]),
     "gg_bucket_by_owner": (C.c_int, [_P, _P, _I64, _P, _P, _P, _P, _P, _SZ, _P]),
     "gg_stage_bulk": (C.c_int, [_P, _P, _I64, _P, _P, _P, _I64, _I64, _P, _P, _P, _P, _P, _P, _P,
                                 _P, _SZ, _P]),
@@ -239,10 +240,14 @@ def gg_sample_window(csr, seeds, seed_off, W, fanout, L, rng_seed, epoch, batch0
 
 
 def gg_build_hotset(frontier_bits, W, part, n_hot, hot_ids, hot_freq, cap, hot_count, status, ws,
-                    stream=None):
-    return check(lib.gg_build_hotset(_ptr(frontier_bits), W, C.byref(part), n_hot, _ptr(hot_ids),
-                                     _ptr(hot_freq), cap, _ptr(hot_count), _ptr(status), _ptr(ws),
-                                     ws.numel(), _stream(stream)), "gg_build_hotset")
+                    stream=None, hot_frac=None):
+    """hot_frac = (num, den): budget ceil(U * num / den) of the window's U
+    distinct remote nodes (n_hot must then be -1)."""
+    num, den = hot_frac if hot_frac is not None else (0, 0)
+    return check(lib.gg_build_hotset(_ptr(frontier_bits), W, C.byref(part), n_hot, num, den,
+                                     _ptr(hot_ids), _ptr(hot_freq), cap, _ptr(hot_count),
+                                     _ptr(status), _ptr(ws), ws.numel(), _stream(stream)),
+                 "gg_build_hotset")
 
 
 def gg_bucket_by_owner(hot_ids, hot_count, cap, part, bucket_ids, owner_off, status, ws,

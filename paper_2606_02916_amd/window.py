@@ -88,7 +88,7 @@ class _Buffers:
 class FetchPipeline:
     def __init__(self, row_ptr, col_idx, num_parts, part_kind, local_owner, range_start, shards,
                  shard_rows, row_bytes, stride, W, fanout, max_batch, n_hot=-1, device=None,
-                 out_buffers=2, cache_stride=None, delta=False):
+                 out_buffers=2, cache_stride=None, delta=False, hot_frac=None):
         self.device = torch.device(device if device is not None else "cuda")
         self.N = int(row_ptr.numel() - 1)
         self.W = int(W)
@@ -101,6 +101,7 @@ class FetchPipeline:
         # share HBM sectors, which a sparse ascending gather reuses.
         self.cache_stride = int(cache_stride) if cache_stride else self.stride
         self.n_hot = int(n_hot)
+        self.hot_frac = hot_frac
         self.delta = bool(delta)
         self.row_ptr, self.col_idx = row_ptr, col_idx
         self.shards = shards
@@ -150,7 +151,8 @@ class FetchPipeline:
 
     def hotset(self, Wk, cur):
         gg.gg_build_hotset(self.frontier_bits, Wk, self.part, self.n_hot, self.hot_ids,
-                           self.hot_freq, self.hot_cap, self.hot_count[cur], self.status, self.ws)
+                           self.hot_freq, self.hot_cap, self.hot_count[cur], self.status, self.ws,
+                           hot_frac=self.hot_frac)
 
     def bucket(self, cur):
         gg.gg_bucket_by_owner(self.hot_ids, self.hot_count[cur], self.hot_cap, self.part,
@@ -280,7 +282,7 @@ class LookaheadPipeline:
 
     def __init__(self, row_ptr, col_idx, num_parts, part_kind, local_owner, range_start, shards,
                  shard_rows, row_bytes, stride, W, fanout, max_batch, n_hot=-1, device=None,
-                 cache_stride=None, nsets=2):
+                 cache_stride=None, nsets=2, hot_frac=None):
         self.device = torch.device(device if device is not None else "cuda")
         self.N = int(row_ptr.numel() - 1)
         self.W = int(W)
@@ -290,6 +292,7 @@ class LookaheadPipeline:
         self.row_bytes, self.stride = int(row_bytes), int(stride)
         self.cache_stride = int(cache_stride) if cache_stride else self.stride
         self.n_hot = int(n_hot)
+        self.hot_frac = hot_frac
         self.csr = gg.make_csr(row_ptr, col_idx)
         self.part = gg.make_part(self.P, part_kind, local_owner, self.N, range_start)
         self.feat = gg.make_feat(self.row_bytes, shards, [self.stride] * self.P, shard_rows)
@@ -346,7 +349,7 @@ class LookaheadPipeline:
         _rec(ev[1], bs)
         gg.gg_build_hotset(cur.frontier_bits, Wk, self.part, self.n_hot, cur.hot_ids,
                            cur.hot_freq, g.hot_cap, self.hot_count[T], self.status, cur.ws,
-                           stream=s)
+                           stream=s, hot_frac=self.hot_frac)
         _rec(ev[2], bs)
         gg.gg_bucket_by_owner(cur.hot_ids, self.hot_count[T], g.hot_cap, self.part,
                               self.bucket_ids[T], cur.owner_off, self.status, cur.ws, stream=s)

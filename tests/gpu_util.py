@@ -20,7 +20,7 @@ class World:
 
     def __init__(self, inst, W=None, n_hot=-1, local_owner=None, fanout=None, batch=None,
                  device="cuda:0", shards=None, row_bytes=None, stride=None, cache_stride=None,
-                 tensors=None, delta=False):
+                 tensors=None, delta=False, hot_frac=None):
         wl = inst.wl
         self.inst = inst
         self.wl = wl
@@ -45,11 +45,12 @@ class World:
         self.pipe = FetchPipeline(self.row_ptr_d, self.col_idx_d, self.P, wl.part_kind, self.local,
                                   self.rs, self.shards_d, rows, self.row_bytes, self.stride,
                                   self.W, self.fanout, self.batch, n_hot=n_hot, device=self.dev,
-                                  cache_stride=cache_stride, delta=delta)
+                                  cache_stride=cache_stride, delta=delta, hot_frac=hot_frac)
         self.part_ref = ggref.make_part(self.P, wl.part_kind, self.local, wl.num_nodes, self.rs)
         self.feat_ref = ggref.make_feat(self.row_bytes, self.shards, [self.stride] * self.P)
         self.cstride = self.pipe.cache_stride
         self.delta = delta
+        self.hot_frac = hot_frac
         self.cache_refs = [np.zeros((self.pipe.hot_cap, self.cstride), dtype=np.uint8)
                            for _ in range(2 if delta else 1)]
         self.slot_ref = np.full(wl.num_nodes, -1, dtype=np.int32)
@@ -94,7 +95,8 @@ class World:
             got = np.nonzero(np.unpackbits(row.view(np.uint8), bitorder="little"))[0]
             assert np.array_equal(got, ids)
         # hot set and buckets
-        hot, freq = ggref.build_hotset(fids, foff, Wk, L, self.part_ref, self.n_hot)
+        hot, freq = ggref.build_hotset(fids, foff, Wk, L, self.part_ref, self.n_hot,
+                                       hot_frac=self.hot_frac)
         bucket, owner_off = ggref.bucket_by_owner(hot, self.part_ref)
         g_hot, g_freq, g_cnt, g_bucket, g_owner_off = pipe.hot_outputs(cur)
         assert int(g_cnt[0]) == len(hot) == int(g_cnt[1])

@@ -134,6 +134,10 @@ def test_bad_arguments_are_rejected_on_the_host(gg):
     part = gg.make_part(0, gg.PART_MOD, 0, 100)
     with pytest.raises(gg.GGError):
         gg.gg_build_hotset(t, 4, part, -1, t, None, 10, t, t, t, stream=0)
+    part = gg.make_part(4, gg.PART_MOD, 0, 100)
+    for n_hot, frac in [(5, (1, 10)), (-1, (11, 10)), (-1, (-1, 10)), (-1, (1, 1 << 32))]:
+        with pytest.raises(gg.GGError):                                  # bad relative budgets
+            gg.gg_build_hotset(t, 4, part, n_hot, t, None, 10, t, t, t, stream=0, hot_frac=frac)
     part = gg.make_part(4, gg.PART_RANGE, 0, 100, [0, 10, 20, 30, 99])  # does not end at N
     with pytest.raises(gg.GGError):
         gg.gg_bucket_by_owner(t, t, 10, part, t, t, t, t, stream=0)

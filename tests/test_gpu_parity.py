@@ -64,6 +64,14 @@ def test_small_window_sizes(W):
     w.run_and_compare(1)
 
 
+@pytest.mark.parametrize("frac", [(1, 10), (1, 3), (0, 1), (1, 1), (999, 1000)])
+def test_relative_budget_window_matches_oracle(frac):
+    log(f"small: hot set = top {frac[0]}/{frac[1]} of the window's remote nodes, 2 windows")
+    w = world(synth.instance("small"), hot_frac=frac)
+    w.run_and_compare(0)
+    w.run_and_compare(1)
+
+
 def test_small_budget_misses_across_windows():
     log("small: n_hot=3000 over two windows")
     w = world(synth.instance("small"), n_hot=3000)
@@ -421,18 +429,22 @@ SIM_COEF = dict(eps_init=0.025, eps_row=1.6e-5, lam_init=5e-4, lam_row=3.2e-7,
                 bw_bytes_per_s=1.25e9, row_bytes=400.0, p_idle=30.0)
 
 
-@pytest.mark.parametrize("name,W,n_hot,driver", [
-    ("tiny", 1, -1, "seq"), ("tiny", 2, 2000, "seq"), ("tiny", 4, 0, "seq"),
-    ("small", 1, 3000, "seq"), ("small", 4, 3000, "delta"), ("small", 8, -1, "seq"),
-    ("small", 3, 0, "seq"), ("small", 4, 3000, "lookahead"), ("small", 2, 20000, "lookahead")])
-def test_simulator_counts_match_oracle(name, W, n_hot, driver):
-    log(f"{name}: simulator z(W), E_phy(W) over the epoch, W={W}, n_hot={n_hot}, {driver}")
+@pytest.mark.parametrize("name,W,n_hot,driver,frac", [
+    ("tiny", 1, -1, "seq", None), ("tiny", 2, 2000, "seq", None), ("tiny", 4, 0, "seq", None),
+    ("small", 1, 3000, "seq", None), ("small", 4, 3000, "delta", None),
+    ("small", 8, -1, "seq", None), ("small", 3, 0, "seq", None),
+    ("small", 4, 3000, "lookahead", None), ("small", 2, 20000, "lookahead", None),
+    ("small", 4, -1, "seq", (1, 10)), ("small", 16, -1, "lookahead", (1, 10)),
+    ("tiny", 3, -1, "seq", (7, 9)), ("small", 1, -1, "delta", (0, 5))])
+def test_simulator_counts_match_oracle(name, W, n_hot, driver, frac):
+    log(f"{name}: simulator z(W), E_phy(W) over the epoch, W={W}, n_hot={n_hot}, {driver}, "
+        f"relative budget {frac}")
     import torch as T
     from oracle import ggref
     from paper_2606_02916_amd import LookaheadPipeline, gg
     inst = synth.instance(name)
     wl = inst.wl
-    w = world(inst, W=W, n_hot=n_hot, delta=driver == "delta")
+    w = world(inst, W=W, n_hot=n_hot, delta=driver == "delta", hot_frac=frac)
     P = wl.num_parts
     coeffs = gg.make_sim_coeffs(P, **SIM_COEF)
     acc = T.zeros(gg.SIM_ACC_BYTES, dtype=T.uint8, device=w.dev)
@@ -443,7 +455,7 @@ def test_simulator_counts_match_oracle(name, W, n_hot, driver):
         pipe = LookaheadPipeline(w.row_ptr_d, w.col_idx_d, P, wl.part_kind, wl.local_owner,
                                  inst.range_start, w.shards_d, [s.shape[0] for s in inst.shards],
                                  wl.row_bytes, wl.row_stride, W, wl.fanout, wl.batch_size,
-                                 n_hot=n_hot, device=w.dev)
+                                 n_hot=n_hot, device=w.dev, hot_frac=frac)
     else:
         pipe = w.pipe
     for k in range(nwin):
@@ -455,11 +467,12 @@ def test_simulator_counts_match_oracle(name, W, n_hot, driver):
     got = gg.sim_acc_from_bytes(acc.cpu().numpy().tobytes())
     ids, off = _oracle_trace(inst)
     part = ggref.make_part(P, wl.part_kind, wl.local_owner, wl.num_nodes, inst.range_start)
-    ref = ggref.simulate_epoch(ids, off, W, n_hot, part, ggref.sim_coeffs(P, **SIM_COEF))
+    ref = ggref.simulate_epoch(ids, off, W, n_hot, part, ggref.sim_coeffs(P, **SIM_COEF),
+                               hot_frac=frac)
     # integer counts exactly; the fp64 energies are formed in the same order
     # without fused multiply-adds on both sides, so they agree bit for bit
     assert got == ref
-    if n_hot == 0:
+    if n_hot == 0 or (frac is not None and frac[0] == 0):
         assert got["rebuild_events"] == 0 and got["hits"] == 0
-    if n_hot < 0:
+    if n_hot < 0 and frac is None:
         assert got["miss_events"] == 0

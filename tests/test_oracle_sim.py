@@ -210,3 +210,59 @@ def test_simulator_rejects_bad_arguments():
     with pytest.raises(ggref.OracleError):
         ggref.simulate_epoch(IDS, OFF, 1, -1, PART,
                              ggref.sim_coeffs(4, 1.0, 0.0, 0.0, 0.0, 0.0, 400, 0.0))
+
+
+def test_top_fraction_budget_hand_worked():
+    # One window, owners by id mod 4, owner 0 local: b0 = {1,2,3}, b1 = {1,5},
+    # b2 = {1,6}.  7 remote requests over U = 5 distinct nodes; freq(1) = 3,
+    # every other node 1.
+    ids = np.array([1, 2, 3, 1, 5, 1, 6], np.int32)
+    off = np.array([0, 3, 5, 7], np.int64)
+    # top 10%: ceil(0.5) = 1 node -> {1}, which serves 3 of the 7 requests
+    a = ggref.simulate_epoch(ids, off, 3, -1, PART, COEF, hot_frac=(1, 10))
+    assert (a["hits"], a["remote_rows"], a["rebuild_rows"], a["miss_rows"]) == (3, 7, 1, 4)
+    # top 40%: exactly 2 nodes -> {1, 2} (ties by smaller id): 4 of 7
+    a = ggref.simulate_epoch(ids, off, 3, -1, PART, COEF, hot_frac=(2, 5))
+    assert (a["hits"], a["rebuild_rows"]) == (4, 2)
+    hot, freq = ggref.build_hotset(ids, off, 3, 0, PART, -1, hot_frac=(2, 5))
+    assert hot.tolist() == [1, 2] and freq.tolist() == [3, 1]
+    # top 41%: ceil(2.05) = 3 nodes -> {1, 2, 3}
+    hot, _ = ggref.build_hotset(ids, off, 3, 0, PART, -1, hot_frac=(41, 100))
+    assert hot.tolist() == [1, 2, 3]
+    # 0 and 1: nothing cached / the whole union
+    assert ggref.simulate_epoch(ids, off, 3, -1, PART, COEF, hot_frac=(0, 7))["hits"] == 0
+    assert ggref.simulate_epoch(ids, off, 3, -1, PART, COEF, hot_frac=(7, 7))["hits"] == 7
+
+
+def test_top_fraction_budget_brute_force():
+    rng = np.random.default_rng(5)
+    N = 50
+    part = ggref.make_part(4, ggref.PART_MOD, 2, N)
+    own = lambda u: ggref.owner(part, u)   # noqa: E731
+    for trial in range(15):
+        ids, off = _random_trace(rng, N, int(rng.integers(1, 7)), 14)
+        sets = _batch_sets(ids, off)
+        for num, den in ((1, 10), (1, 4), (3, 7), (1, 1), (0, 3)):
+            for W in (1, 2, 6):
+                hits = remote = 0
+                for k in range(0, len(sets), W):
+                    win = sets[k:k + W]
+                    freq = {}
+                    for s in win:
+                        for u in s:
+                            if own(u) != 2:
+                                freq[u] = freq.get(u, 0) + 1
+                    n = -(-len(freq) * num // den)          # ceil(U * num / den)
+                    hot = set(sorted(freq, key=lambda u: (-freq[u], u))[:n])
+                    for s in win:
+                        r = {u for u in s if own(u) != 2}
+                        remote += len(r)
+                        hits += len(r & hot)
+                a = ggref.simulate_epoch(ids, off, W, -1, part, COEF, hot_frac=(num, den))
+                assert (a["hits"], a["remote_rows"]) == (hits, remote), (trial, num, den, W)
+
+
+def test_relative_budget_argument_checks():
+    for n_hot, frac in ((3, (1, 10)), (-1, (11, 10)), (-1, (-1, 10)), (-1, (1, 1 << 32))):
+        with pytest.raises(ggref.OracleError):
+            ggref.build_hotset(IDS, OFF, 3, 0, PART, n_hot, hot_frac=frac)
