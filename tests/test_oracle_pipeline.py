@@ -367,6 +367,50 @@ def test_restaging_reports_the_rebuild_delta_and_clears_stale_slots():
         prev = win["bucket_ids"]
 
 
+@pytest.mark.parametrize("kind,local", [(ggref.PART_RANGE, 0), (ggref.PART_MOD, -1)])
+def test_delta_staging_requests_only_the_set_difference(kind, local):
+    """Sec. IV-A, Eq. (1): with the previous cache as a source only
+    Delta_{k,m} = (H_k in owner m) minus H_{k-1} is requested from owner m;
+    rows already cached are copied from the previous cache.  Ground truth is
+    the unsharded feature matrix and Python set algebra."""
+    rng = np.random.default_rng(43)
+    N = 500
+    row_ptr, col_idx = helpers.random_graph(N, 4000, rng)
+    part, feat, full, shards, rs = make_world(row_ptr, col_idx, kind, 4, local, 20, 32, rng)
+    caches = [np.zeros((N, 32), dtype=np.uint8) for _ in range(2)]
+    slot_of = np.full(N, -1, dtype=np.int32)
+    prev = None
+    for k in range(5):
+        seeds, soff = random_seeds(N, 3, 5, rng)
+        fids, foff, _, _ = ggref.sample_window(row_ptr, col_idx, seeds, soff, (3, 2), 5, 0, 3 * k)
+        hot, _ = ggref.build_hotset(fids, foff, 3, 2, part, -1)
+        bucket, owner_off = ggref.bucket_by_owner(hot, part)
+        cache, src = caches[k % 2], (caches[(k - 1) % 2] if k else None)
+        full_cache = np.zeros_like(cache)
+        full_slot = slot_of.copy()
+        ref = ggref.stage_bulk(bucket, owner_off, part, feat, full_cache, 32, full_slot, prev)
+        st = ggref.stage_bulk(bucket, owner_off, part, feat, cache, 32, slot_of, prev,
+                              src_cache=src, src_slot_of=slot_of if src is not None else None)
+        prev_set = set() if prev is None else set(prev.tolist())
+        H = bucket.tolist()
+        for m in range(4):
+            seg = H[owner_off[m]:owner_off[m + 1]]
+            delta = set(seg) - prev_set
+            assert st["rows"][m] == st["delta_rows"][m] == len(delta)
+            assert st["requests"][m] == (1 if delta else 0)
+            assert st["bytes"][m] == 20 * len(delta)
+        assert st["retained"] == len(set(H) & prev_set)
+        assert st["rows_total"] == len(H)
+        # the cache holds the rows of H_k, equal to a full restage's cache
+        for s_, u in enumerate(H):
+            assert slot_of[u] == s_
+            assert np.array_equal(cache[s_, :20], full[u, :20])
+        assert np.array_equal(cache[:len(H), :20], full_cache[:len(H), :20])
+        assert np.array_equal(slot_of, full_slot)
+        assert ref["delta_rows"] == st["delta_rows"]
+        prev = bucket
+
+
 def test_paper_consolidation_example():
     """Sec. IV-C: W = 16 batches over three remote owners turn up to
     16 x 3 = 48 per-batch requests into 3 bulk transfers."""
