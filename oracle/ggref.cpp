@@ -10,6 +10,7 @@
 #include "ggref.h"
 
 #include <algorithm>
+#include <cmath>
 #include <iterator>
 #include <cstring>
 #include <set>
@@ -486,6 +487,130 @@ int ggref_simulate_epoch(const int32_t* trace_ids, const int64_t* trace_off, int
     acc->batches += Wk;
     acc->e_stall = coeffs->p_idle * acc->t_stall;
     acc->e_phy = (acc->e_rebuild + acc->e_miss) + acc->e_stall;
+  }
+  return GGREF_OK;
+}
+
+// ---------------------------------------------------------------------------
+// GraphSAGE consumer of X_b (mean aggregator), in fp64.
+// ---------------------------------------------------------------------------
+namespace {
+
+// IEEE 754 binary16 to double, from the bit fields.
+double half_to_double(uint16_t h) {
+  const int sign = (h >> 15) & 1, exp = (h >> 10) & 31, man = h & 1023;
+  double v;
+  if (exp == 0)
+    v = std::ldexp((double)man, -24);                  // subnormal (or zero)
+  else if (exp == 31)
+    v = man ? std::nan("") : INFINITY;
+  else
+    v = std::ldexp((double)(1024 + man), exp - 25);    // (1 + man/1024) * 2^(exp-15)
+  return sign ? -v : v;
+}
+
+}  // namespace
+
+int ggref_sage_forward(const int32_t* frontier_ids, const int64_t* frontier_off,
+                       const int32_t* nbr_ids, const int64_t* nbr_off, int32_t W, int32_t L,
+                       const int32_t* fanout, const void* x, int32_t x_dtype, int64_t x_stride,
+                       const ggref_sage_layer_t* layers, double* out, double* out_abs) {
+  if (W < 1 || L < 1 || (x_dtype != 0 && x_dtype != 1) || !layers || !out) return GGREF_ERR_ARG;
+  for (int32_t j = 0; j < L; ++j) {
+    if (layers[j].d_in < 1 || layers[j].d_out < 1) return GGREF_ERR_ARG;
+    if (j > 0 && layers[j].d_in != layers[j - 1].d_out) return GGREF_ERR_ARG;
+  }
+  const int64_t esz = x_dtype == 0 ? 4 : 2;
+  if (x_stride < layers[0].d_in * esz) return GGREF_ERR_ARG;
+  const int32_t d_last = layers[L - 1].d_out;
+  for (int32_t b = 0; b < W; ++b) {
+    // h^0 = X_b over F_L(b)
+    const int64_t sL = (int64_t)L * W + b;
+    const int64_t nL = frontier_off[sL + 1] - frontier_off[sL];
+    const int64_t xrow0 = frontier_off[sL] - frontier_off[(int64_t)L * W];
+    int32_t d = layers[0].d_in;
+    std::vector<double> h((size_t)(nL * d)), ha((size_t)(nL * d));
+    for (int64_t i = 0; i < nL; ++i) {
+      const char* row = (const char*)x + (xrow0 + i) * x_stride;
+      for (int32_t c = 0; c < d; ++c) {
+        double v;
+        if (x_dtype == 0) {
+          float f;
+          std::memcpy(&f, row + 4 * c, 4);
+          v = f;
+        } else {
+          uint16_t bits;
+          std::memcpy(&bits, row + 2 * c, 2);
+          v = half_to_double(bits);
+        }
+        h[(size_t)(i * d + c)] = v;
+        ha[(size_t)(i * d + c)] = std::fabs(v);
+      }
+    }
+    for (int32_t j = 1; j <= L; ++j) {
+      const int32_t lvl = L - j;                      // output level; input level lvl + 1
+      const ggref_sage_layer_t& ly = layers[j - 1];
+      const int64_t sin = (int64_t)(lvl + 1) * W + b, sout = (int64_t)lvl * W + b;
+      const int32_t* Fin = frontier_ids + frontier_off[sin];
+      const int64_t nin = frontier_off[sin + 1] - frontier_off[sin];
+      const int32_t* Fout = frontier_ids + frontier_off[sout];
+      const int64_t nout = frontier_off[sout + 1] - frontier_off[sout];
+      const int32_t k = fanout[lvl];
+      const int32_t* S = nbr_ids + nbr_off[(int64_t)lvl * W + b];
+      if (nbr_off[(int64_t)lvl * W + b + 1] - nbr_off[(int64_t)lvl * W + b] != nout * k)
+        return GGREF_ERR_RANGE;
+      auto pos = [&](int32_t u) -> int64_t {          // row of u in h (F_in ascending)
+        const int32_t* p = std::lower_bound(Fin, Fin + nin, u);
+        return (p != Fin + nin && *p == u) ? (int64_t)(p - Fin) : -1;
+      };
+      const int32_t dout = ly.d_out;
+      std::vector<double> g((size_t)(nout * dout)), ga((size_t)(nout * dout));
+      std::vector<double> mean((size_t)d), meana((size_t)d);
+      for (int64_t i = 0; i < nout; ++i) {
+        const int64_t pv = pos(Fout[i]);
+        if (pv < 0) return GGREF_ERR_RANGE;
+        std::fill(mean.begin(), mean.end(), 0.0);
+        std::fill(meana.begin(), meana.end(), 0.0);
+        int32_t cnt = 0;
+        for (int32_t t = 0; t < k; ++t) {
+          const int32_t u = S[i * k + t];
+          if (u < 0) continue;
+          const int64_t pu = pos(u);
+          if (pu < 0) return GGREF_ERR_RANGE;
+          for (int32_t c = 0; c < d; ++c) {
+            mean[(size_t)c] += h[(size_t)(pu * d + c)];
+            meana[(size_t)c] += ha[(size_t)(pu * d + c)];
+          }
+          ++cnt;
+        }
+        if (cnt > 0)
+          for (int32_t c = 0; c < d; ++c) {
+            mean[(size_t)c] /= cnt;
+            meana[(size_t)c] /= cnt;
+          }
+        for (int32_t o = 0; o < dout; ++o) {
+          double y = ly.bias ? (double)ly.bias[o] : 0.0;
+          double ya = std::fabs(y);
+          for (int32_t c = 0; c < d; ++c) {
+            const double ws = ly.w_self[(size_t)c * dout + o], wn = ly.w_neigh[(size_t)c * dout + o];
+            y += ws * h[(size_t)(pv * d + c)] + wn * mean[(size_t)c];
+            ya += std::fabs(ws) * ha[(size_t)(pv * d + c)] + std::fabs(wn) * meana[(size_t)c];
+          }
+          if (ly.relu && y < 0) y = 0;
+          g[(size_t)(i * dout + o)] = y;
+          ga[(size_t)(i * dout + o)] = ya;
+        }
+      }
+      h.swap(g);
+      ha.swap(ga);
+      d = dout;
+    }
+    const int64_t n0 = frontier_off[b + 1] - frontier_off[b];
+    const int64_t orow0 = frontier_off[b] - frontier_off[0];
+    for (int64_t i = 0; i < n0 * d_last; ++i) {
+      out[orow0 * d_last + i] = h[(size_t)i];
+      if (out_abs) out_abs[orow0 * d_last + i] = ha[(size_t)i];
+    }
   }
   return GGREF_OK;
 }

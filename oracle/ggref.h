@@ -202,6 +202,35 @@ int ggref_simulate_epoch(const int32_t* trace_ids, const int64_t* trace_off, int
                          const ggref_part_t* part, const ggref_sim_coeffs_t* coeffs,
                          ggref_sim_acc_t* acc);
 
+/* One GraphSAGE layer with the mean aggregator: for a node v with sampled
+ * neighbours S(v), out = act(W_self^T h_v + W_neigh^T mean_{u in S(v)} h_u
+ * + bias), the mean of an empty S(v) being 0; act = ReLU when relu != 0.
+ * Weights are row-major [d_in][d_out]. */
+typedef struct ggref_sage_layer {
+  int32_t d_in;
+  int32_t d_out;
+  int32_t relu;
+  const float* w_self;
+  const float* w_neigh;
+  const float* bias;
+} ggref_sage_layer_t;
+
+/* The consumer of X_b (Algorithm 1: forward pass on the assembled tensor;
+ * Sec. VI-A: GraphSAGE): L mean-aggregator layers over each batch's sampled
+ * blocks.  Layer j (1..L) computes h^j for the nodes of F_{L-j} from h^{j-1}
+ * over F_{L-j+1}, with S(v) = v's sampled neighbours at hop L-j; h^0 = X_b.
+ * x holds the rows of N_b = F_L of all W batches back to back (batch b's at
+ * row frontier_off[L*W+b] - frontier_off[L*W]), layers[0].d_in elements of
+ * x_dtype (0 = fp32, 1 = fp16) per row at x_stride bytes.  out receives
+ * the rows of F_0 (the seeds) of all batches back to back, layers[L-1].d_out
+ * doubles per row; out_abs (may be NULL) the same forward pass on absolute
+ * values (|x|, |W|, |bias|, no activation), a magnitude bound used to size
+ * rounding-error tolerances.  Arithmetic in fp64. */
+int ggref_sage_forward(const int32_t* frontier_ids, const int64_t* frontier_off,
+                       const int32_t* nbr_ids, const int64_t* nbr_off, int32_t W, int32_t L,
+                       const int32_t* fanout, const void* x, int32_t x_dtype, int64_t x_stride,
+                       const ggref_sage_layer_t* layers, double* out, double* out_abs);
+
 #ifdef __cplusplus
 }
 #endif

@@ -65,6 +65,11 @@ class SimAcc(C.Structure):
                 ("e_stall", C.c_double), ("e_phy", C.c_double)]
 
 
+class SageLayer(C.Structure):
+    _fields_ = [("d_in", C.c_int32), ("d_out", C.c_int32), ("relu", C.c_int32),
+                ("w_self", C.c_void_p), ("w_neigh", C.c_void_p), ("bias", C.c_void_p)]
+
+
 _lib = None
 
 
@@ -99,6 +104,8 @@ def lib():
         L.ggref_gather_batch.restype = C.c_int
         L.ggref_simulate_epoch.argtypes = [P, P, i64, i32, i64, i64, i64, P, P, P]
         L.ggref_simulate_epoch.restype = C.c_int
+        L.ggref_sage_forward.argtypes = [P, P, P, P, i32, i32, P, P, i32, i64, P, P, P]
+        L.ggref_sage_forward.restype = C.c_int
         _lib = L
     return _lib
 
@@ -282,6 +289,39 @@ def simulate_epoch(trace_ids, trace_off, W, n_hot, part, coeffs, hot_frac=None):
                                       C.byref(part), C.byref(coeffs), C.byref(acc)),
            "ggref_simulate_epoch")
     return sim_dict(acc)
+
+
+def sage_forward(frontier_ids, frontier_off, nbr_ids, nbr_off, W, fanout, x, x_dtype, x_stride,
+                 layers):
+    """GraphSAGE (mean aggregator) over a window's sampled blocks.  x: the
+    window's N_b rows back to back as a uint8 array of rows at x_stride
+    bytes; x_dtype 0 = fp32, 1 = fp16; layers: list of (w_self [d_in, d_out],
+    w_neigh, bias [d_out], relu).  Returns (out, out_abs) over the rows of
+    F_0 of all batches."""
+    L = len(fanout)
+    fids = np.ascontiguousarray(frontier_ids, dtype=np.int32)
+    foff = np.ascontiguousarray(frontier_off, dtype=np.int64)
+    nids = np.ascontiguousarray(nbr_ids, dtype=np.int32)
+    noff = np.ascontiguousarray(nbr_off, dtype=np.int64)
+    fan = np.ascontiguousarray(fanout, dtype=np.int32)
+    xb = np.ascontiguousarray(x)
+    keep = []
+    arr = (SageLayer * L)()
+    for j, (ws, wn, b, relu) in enumerate(layers):
+        ws = np.ascontiguousarray(ws, dtype=np.float32)
+        wn = np.ascontiguousarray(wn, dtype=np.float32)
+        b = np.ascontiguousarray(b, dtype=np.float32)
+        keep += [ws, wn, b]
+        arr[j].d_in, arr[j].d_out, arr[j].relu = ws.shape[0], ws.shape[1], int(bool(relu))
+        arr[j].w_self, arr[j].w_neigh, arr[j].bias = ws.ctypes.data, wn.ctypes.data, b.ctypes.data
+    n0 = int(foff[W] - foff[0])
+    d = int(arr[L - 1].d_out)
+    out = np.zeros((n0, d), dtype=np.float64)
+    oab = np.zeros((n0, d), dtype=np.float64)
+    _check(lib().ggref_sage_forward(_p(fids), _p(foff), _p(nids), _p(noff), W, L, _p(fan),
+                                    _p(xb), x_dtype, x_stride, arr, _p(out), _p(oab)),
+           "ggref_sage_forward")
+    return out, oab
 
 
 def sim_dict(acc):
