@@ -173,6 +173,10 @@ def main():
     ap.add_argument("--copy-calibration-mib", type=int, default=0,
                     help="after the timed steps, copy this many MiB device to device three "
                          "times (a plain copy of known size for scaling HBM counters)")
+    ap.add_argument("--consumer", type=int, default=0, metavar="CLASSES",
+                    help="also run the GraphSAGE consumer (mean aggregator, 16 hidden units, "
+                         "CLASSES outputs, one layer per sampling hop) on every window's rows "
+                         "inside the step, and report its time and MFMA rate")
     ap.add_argument("--sets", type=int, default=2,
                     help="buffer sets of the look-ahead pipeline (how far building may run ahead)")
     ap.add_argument("--wsweep", default=None,
@@ -245,23 +249,40 @@ def main():
         b0, b1 = synth.window_batches(boff, W, k)
         so = boff[b0:b1 + 1] - boff[b0]
         wins.append((seeds_d[boff[b0]:boff[b1]], so, b0))
+    cons, cons_dims = None, None
+    if args.consumer:
+        from paper_2606_02916_amd import SageConsumer, gg
+        if args.per_batch:
+            ap.error("--consumer reads whole-window gathers; drop --per-batch")
+        gen = torch.Generator(device=dev).manual_seed(0)
+        cons_dims = [wl.feat_dim] + [16] * (L - 1) + [args.consumer]
+        layers = []
+        for j in range(L):
+            a, b = cons_dims[j], cons_dims[j + 1]
+            layers.append((torch.randn(a, b, device=dev, generator=gen) / a ** 0.5,
+                           torch.randn(a, b, device=dev, generator=gen) / a ** 0.5,
+                           0.1 * torch.randn(b, device=dev, generator=gen), j < L - 1))
+        cons = SageConsumer(pipe.geo, layers, device=dev,
+                            x_dtype=gg.GG_F16 if wl.feat_dtype == "fp16" else gg.GG_F32)
     torch.cuda.synchronize()
     log(f"uploaded; {nwin} windows of W={W}; out_cap={pipe.geo.out_cap} "
         f"hot_cap={pipe.geo.hot_cap}; driver {args.pipeline}")
 
-    def run_window(s, so, b0, events=None, gevs=None):
+    def run_window(s, so, b0, events=None, gevs=None, cevs=None):
         """Enqueues one window; returns (Wk, object holding its statistics)."""
         if look:
             return pipe.window(s, so, b0, events=events,
-                               gather_events=gevs[0] if gevs is not None else None)
-        Wk = pipe.window(s, so, b0, events=events, gather_events=gevs, per_batch=pb)
-        return Wk, pipe
+                               gather_events=gevs[0] if gevs is not None else None,
+                               consumer=cons, consumer_events=cevs)
+        Wk = pipe.window(s, so, b0, events=events, gather_events=gevs, per_batch=pb,
+                         consumer=cons, consumer_events=cevs)
+        return Wk, pipe.buf
 
     # Pass over every window once: per-window row counts for the metric and
     # per-batch local/remote counts for the gather's algorithmic bytes.
     rb = wl.row_bytes
     mk = lambda: torch.cuda.Event(enable_timing=True)  # noqa: E731
-    rows_w, gbytes_w, hot_w, sbytes_w, req_w, hbytes_w = [], [], [], [], [], []
+    rows_w, gbytes_w, hot_w, sbytes_w, req_w, hbytes_w, lev_w = [], [], [], [], [], [], []
     pb = args.per_batch
     iso_ms = []      # gather launches with the chip to themselves
     flush = torch.empty(512 << 20, dtype=torch.uint8, device=dev) if look else None
@@ -293,6 +314,8 @@ def main():
         sbytes_w.append(ss["rows_total"] * (2 * rb + 8) + ss["invalidated"] * 4)
         req_w.append(ss["requests_total"])
         hbytes_w.append(sum(ss["bytes"][m] for m in range(P) if not shards_d[m].is_cuda))
+        fo = sb.frontier_off[:(L + 1) * Wk + 1].cpu().numpy()
+        lev_w.append([int(fo[(l + 1) * Wk] - fo[l * Wk]) for l in range(L + 1)])
     del flush
     log(f"rows per window: {rows_w[:4]}... hot set: {hot_w[:4]}...")
 
@@ -304,12 +327,13 @@ def main():
     K = args.steps
     evs = [[mk() for _ in range(5 if look else 6)] for _ in range(K)]
     gevs = [[(mk(), mk()) for _ in range(W if pb else 1)] for _ in range(K)]
+    cevs = [(mk(), mk()) for _ in range(K)] if cons else [None] * K
     order = [(args.warmup + i) % nwin for i in range(K)]
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     for i, k in enumerate(order):
         s, so, b0 = wins[k]
-        run_window(s, so, b0, events=evs[i], gevs=gevs[i])
+        run_window(s, so, b0, events=evs[i], gevs=gevs[i], cevs=cevs[i])
     torch.cuda.synchronize()
     t1 = time.perf_counter()
     if pipe.read_status() != 0:
@@ -424,9 +448,34 @@ def main():
         "hot_set_rows_per_window": int(np.mean(hot_w)),
         "bulk_requests_per_window": float(np.mean(req_w)),
         "gather_rows_per_s": round(rows / (g_ms * 1e-3) if g_ms else 0.0, 1),
+        "consumer": consumer_report(cons_dims, lev_w, order, cevs, wl) if cons else None,
         "cpu_baseline": cpu,
     }
     print(json.dumps(line), flush=True)
+
+
+def consumer_report(dims, lev_w, order, cevs, wl):
+    """GraphSAGE consumer per window: time (HIP events on its stream), the
+    dense products' flops (layer j projects the rows of level L-j+1 from
+    d_in to 2 * d_out), their rate against the fp32 MFMA peak, and the rate
+    of the first layer's read of the gathered rows."""
+    import numpy as np
+    L = len(dims) - 1
+    ms, flops, xbytes = [], 0, 0
+    for i, k in enumerate(order):
+        ms.append(cevs[i][0].elapsed_time(cevs[i][1]))
+        lev = lev_w[k]
+        for j in range(1, L + 1):
+            flops += 2 * lev[L - j + 1] * dims[j - 1] * 2 * dims[j]
+        xbytes += lev[L] * wl.row_bytes
+    t = sum(ms) * 1e-3
+    return {"layers": dims, "aggregator": "mean", "ms_per_window_median": round(float(np.median(ms)), 4),
+            "flops_per_window": int(flops / len(order)),
+            "tflops": round(flops / t / 1e12, 3), "peak_tflops_fp32_mfma": 157.3,
+            "mfma_frac": round(flops / t / 1e12 / 157.3, 5),
+            "x_read_gbps": round(xbytes / t / 1e9, 1),
+            "note": "the consumer's time is on its own events; it overlaps the next window's "
+                    "build under the look-ahead driver"}
 
 
 def pcie_h2d_gbps(dev):

@@ -319,6 +319,57 @@ int gg_sim_accumulate(const gg_stage_stats_t* stage_d, const gg_gather_stats_t* 
                       int32_t nseg, const gg_part_t* part, const gg_sim_coeffs_t* coeffs,
                       gg_sim_acc_t* acc_d, hipStream_t stream);
 
+/* ---------------------------------------------------------------------------
+ * The consumer of X_b: GraphSAGE with the mean aggregator (Algorithm 1's
+ * forward pass on the assembled tensor; Sec. VI-A trains GraphSAGE).
+ * ------------------------------------------------------------------------- */
+
+#define GG_F32 0
+#define GG_F16 1
+#define GG_SAGE_MAX_DIM 128   /* d_out of every layer, and d_in of layers after the first */
+#define GG_SAGE_MAX_IN 4096   /* d_in of the first layer */
+
+/* One layer: for a node v with sampled neighbours S(v),
+ * out = act(W_self^T h_v + W_neigh^T mean_{u in S(v)} h_u + bias), the mean
+ * of an empty S(v) being 0, act = ReLU when relu != 0.  Weights are fp32,
+ * row-major [d_in][d_out], on the device; bias [d_out] may be NULL. */
+typedef struct gg_sage_layer {
+  int32_t d_in;
+  int32_t d_out;
+  int32_t relu;
+  const float* w_self;
+  const float* w_neigh;
+  const float* bias;
+} gg_sage_layer_t;
+
+/* Workspace bytes of gg_sage_forward for graphs of num_nodes nodes, windows
+ * of at most W batches and at most rows_cap rows per level (all batches
+ * together; the frontier capacity of N_b bounds it). */
+size_t gg_ws_sage(int64_t num_nodes, int32_t W, int64_t rows_cap, int32_t L,
+                  const gg_sage_layer_t* layers_h);
+
+/* Runs L = the sampling depth GraphSAGE layers over the W batches of a
+ * window sampled by gg_sample_window (smp) in one pass per layer.  Layer j
+ * (1..L) computes h^j for the nodes of F_{L-j} from h^{j-1} over F_{L-j+1},
+ * S(v) being v's neighbours drawn at hop L-j; h^0 = x_d, the rows of the
+ * window's N_b back to back as gg_gather_batch writes them for the whole
+ * window (layers_h[0].d_in elements of x_dtype per row at x_stride bytes;
+ * at least min(rows_cap, |N_b| summed over the window) rows).  The first
+ * layer finds rows of N_b by rank in smp->frontier_bits, which must still
+ * hold the window's N_b (num_nodes is the graph's node count).
+ * out_d receives the rows of F_0 (each batch's distinct seeds) of all
+ * batches back to back, layers_h[L-1].d_out fp32 per row; out_rows_cap
+ * bounds them.  The dense products run on MFMA in fp32 (each layer first
+ * projects its input by [W_self | W_neigh], then averages the projected
+ * neighbour rows: the same linear map in the other order).  A level with
+ * more rows than rows_cap, or seeds beyond out_rows_cap, set
+ * GG_DEV_CAPACITY and the excess is skipped. */
+int gg_sage_forward(const gg_wsample_t* smp, int64_t num_nodes, int32_t W, int32_t L,
+                    const int32_t* fanout_h,
+                    const void* x_d, int32_t x_dtype, int64_t x_stride, int64_t rows_cap,
+                    const gg_sage_layer_t* layers_h, float* out_d, int64_t out_rows_cap,
+                    int32_t* status_d, void* ws, size_t ws_bytes, hipStream_t stream);
+
 /* Helpers. */
 const char* gg_status_string(int32_t code);
 const char* gg_last_error(void);

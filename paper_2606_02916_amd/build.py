@@ -12,7 +12,7 @@ CSRC = os.path.join(HERE, "csrc")
 BUILD = os.path.join(ROOT, "_build")
 LIB = os.path.join(HERE, "libgg.so")
 SOURCES = ["common.hip", "sample.hip", "hotset.hip", "bucket.hip", "stage.hip", "gather.hip",
-           "sim.hip"]
+           "sim.hip", "sage.hip"]
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 
 FLAGS = [

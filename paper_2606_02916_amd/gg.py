@@ -87,6 +87,12 @@ class gg_sim_acc_t(C.Structure):
                 ("e_stall", C.c_double), ("e_phy", C.c_double)]
 
 
+class gg_sage_layer_t(C.Structure):
+    _fields_ = [("d_in", C.c_int32), ("d_out", C.c_int32), ("relu", C.c_int32),
+                ("w_self", C.c_void_p), ("w_neigh", C.c_void_p), ("bias", C.c_void_p)]
+
+
+GG_F32, GG_F16 = 0, 1
 STAGE_STATS_BYTES = C.sizeof(gg_stage_stats_t)
 GATHER_STATS_BYTES = C.sizeof(gg_gather_stats_t)
 SIM_ACC_BYTES = C.sizeof(gg_sim_acc_t)
@@ -111,6 +117,9 @@ SIGNATURES = {
     "gg_gather_batch": (C.c_int, [_P, _P, _I32, _I64, _P, _P, _P, _I64, _I64, _P, _P, _I64, _P,
                                   _P, _P, _SZ, _P]),
     "gg_sim_accumulate": (C.c_int, [_P, _P, _I32, _P, _P, _P, _P]),
+    "gg_ws_sage": (_SZ, [_I64, _I32, _I64, _I32, _P]),
+    "gg_sage_forward": (C.c_int, [_P, _I64, _I32, _I32, _P, _P, _I32, _I64, _I64, _P, _P, _I64, _P,
+                                  _P, _SZ, _P]),
     "gg_status_string": (C.c_char_p, [_I32]),
     "gg_last_error": (C.c_char_p, []),
     "gg_version": (C.c_int, []),
@@ -303,6 +312,35 @@ def sim_acc_from_bytes(buf):
     a = gg_sim_acc_t.from_buffer_copy(bytes(buf))
     return {name: (float(getattr(a, name)) if typ is C.c_double else int(getattr(a, name)))
             for name, typ in a._fields_}
+
+
+def make_sage_layers(layers):
+    """layers: sequence of (w_self [d_in, d_out], w_neigh, bias or None,
+    relu) with fp32 device tensors.  The tensors must outlive the calls."""
+    arr = (gg_sage_layer_t * len(layers))()
+    for j, (ws, wn, b, relu) in enumerate(layers):
+        if ws.dtype != wn.dtype or ws.shape != wn.shape or ws.dim() != 2:
+            raise GGError(f"layer {j}: w_self and w_neigh must be matching 2-d tensors")
+        if not (ws.is_contiguous() and wn.is_contiguous()):
+            raise GGError(f"layer {j}: weights must be contiguous")
+        arr[j].d_in, arr[j].d_out, arr[j].relu = int(ws.shape[0]), int(ws.shape[1]), int(bool(relu))
+        arr[j].w_self, arr[j].w_neigh = ws.data_ptr(), wn.data_ptr()
+        arr[j].bias = b.data_ptr() if b is not None else None
+    return arr
+
+
+def gg_ws_sage(num_nodes, W, rows_cap, layers_arr):
+    return int(lib.gg_ws_sage(num_nodes, W, rows_cap, len(layers_arr), layers_arr))
+
+
+def gg_sage_forward(wsample, num_nodes, W, fanout, x, x_dtype, x_stride, rows_cap, layers_arr, out,
+                    out_rows_cap, status, ws, stream=None):
+    fan = np.ascontiguousarray(fanout, dtype=np.int32)
+    return check(lib.gg_sage_forward(C.byref(wsample), num_nodes, W, len(fan), fan.ctypes.data,
+                                     _ptr(x),
+                                     x_dtype, x_stride, rows_cap, layers_arr, _ptr(out),
+                                     out_rows_cap, _ptr(status), _ptr(ws), ws.numel(),
+                                     _stream(stream)), "gg_sage_forward")
 
 
 def gg_status_string(code):

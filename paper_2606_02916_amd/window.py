@@ -40,6 +40,7 @@ class _Geometry:
         remote = N - (int(shard_rows[local_owner]) if local_owner >= 0 else 0)
         self.hot_cap = max(1, min(remote, W * self.out_cap))
         self.win_cap = W * self.out_cap                 # rows of a whole window
+        self.seed_cap = W * max(min(max_batch, N), 1)   # F_0 rows of a whole window
         self.ws_bytes = max(gg.gg_ws_sample(N, W), gg.gg_ws_hotset(N, W),
                             gg.gg_ws_bucket(self.hot_cap, P), gg.gg_ws_stage(self.hot_cap, P),
                             gg.gg_ws_gather(self.out_cap, 1, P),
@@ -201,13 +202,16 @@ class FetchPipeline:
                              coeffs, acc)
 
     def window(self, seeds, seed_off, batch0, epoch=0, rng_seed=0, outs=None, events=None,
-               gather_events=None, per_batch=False, sim=None):
+               gather_events=None, per_batch=False, sim=None, consumer=None,
+               consumer_events=None):
         """Enqueues one window.  By default the W gathers run as one launch
         into win_out; with per_batch=True every batch is its own launch into
         outs[b] (default: the driver's ping-pong buffers).  events: optional
         list of 6 torch events recorded between the calls; gather_events:
         optional list of (start, end) event pairs, one per gather launch;
-        sim: optional (coeffs, acc) to add the window to simulator totals."""
+        sim: optional (coeffs, acc) to add the window to simulator totals;
+        consumer: optional SageConsumer run on the window's rows (whole-window
+        gather only), bracketed by the optional event pair consumer_events."""
         cur = self.k & 1
         ev = events if events is not None else [None] * 6
         _rec(ev[0])
@@ -236,6 +240,13 @@ class FetchPipeline:
         _rec(ev[5])
         if sim is not None:
             self.sim_accumulate(Wk, *sim)
+        if consumer is not None:
+            if per_batch:
+                raise ValueError("the consumer reads a whole-window gather")
+            _rec(consumer_events[0] if consumer_events else None)
+            consumer.forward(self.buf, Wk, outs if outs is not None else self.win_out,
+                             self.stride, self.status)
+            _rec(consumer_events[1] if consumer_events else None)
         self.k += 1
         return Wk
 
@@ -321,7 +332,7 @@ class LookaheadPipeline:
         self.k = 0
 
     def window(self, seeds, seed_off, batch0, epoch=0, rng_seed=0, out=None, events=None,
-               gather_events=None, sim=None):
+               gather_events=None, sim=None, consumer=None, consumer_events=None):
         """Enqueues window k; returns (number of batches, buffer set).  The
         window's rows land in the set's win_out (or `out`) on the gather
         stream; wait on gathered_event(k) before reading them.  Inputs
@@ -332,7 +343,10 @@ class LookaheadPipeline:
         previous window's staging end); gather_events: optional (start, end)
         pair, the start recorded on the stage stream when staging ends and
         the end on the gather stream after the gather; sim: optional
-        (coeffs, acc) to add the window to simulator totals."""
+        (coeffs, acc) to add the window to simulator totals; consumer:
+        optional SageConsumer run on the gather stream after the gather
+        (so it overlaps the next window's build), bracketed by the optional
+        event pair consumer_events."""
         k, g = self.k, self.geo
         X, T = k % self.nsets, k % self.NSLOT
         cur, prev = self.sets[X], self.sets[(k - 1) % self.nsets]
@@ -385,6 +399,10 @@ class LookaheadPipeline:
         if sim is not None:           # simulator totals, in window order on the gather stream
             gg.gg_sim_accumulate(cur.stage_stats, cur.gather_stats.data_ptr(), Wk, self.part,
                                  sim[0], sim[1], stream=gs.cuda_stream)
+        if consumer is not None:      # reads the set's sampling outputs and rows
+            _rec(consumer_events[0] if consumer_events else None, gs)
+            consumer.forward(cur, Wk, o, self.stride, self.status, stream=gs.cuda_stream)
+            _rec(consumer_events[1] if consumer_events else None, gs)
         self.gathered[X].record(gs)
         self.k += 1
         return Wk, cur

@@ -149,5 +149,5 @@ class World:
                 got = win[lo:hi].cpu().numpy()
                 assert np.array_equal(got[:, :rb], refs[b][:, :rb]), f"window batch {b}"
         pipe.k += 1
-        return dict(Wk=Wk, fids=fids, foff=foff, hot=hot, stage=sst,
+        return dict(Wk=Wk, fids=fids, foff=foff, nids=nids, noff=noff, hot=hot, stage=sst,
                     outs=refs if check_outputs else None)

@@ -63,6 +63,8 @@ int main() {
   F(gg_sim_coeffs_t, p_idle)
   S(gg_sim_acc_t) F(gg_sim_acc_t, rebuild_events) F(gg_sim_acc_t, miss_rows)
   F(gg_sim_acc_t, hits) F(gg_sim_acc_t, e_rebuild) F(gg_sim_acc_t, t_stall) F(gg_sim_acc_t, e_phy)
+  S(gg_sage_layer_t) F(gg_sage_layer_t, relu) F(gg_sage_layer_t, w_self)
+  F(gg_sage_layer_t, w_neigh) F(gg_sage_layer_t, bias)
   return 0;
 }
 """
@@ -161,3 +163,17 @@ def test_bad_arguments_are_rejected_on_the_host(gg):
     c = gg.make_sim_coeffs(4, 1.0, 0.01, 1e-3, 1e-5, 1e9, 256, 30.0)
     with pytest.raises(gg.GGError):                                      # more batches than W max
         gg.gg_sim_accumulate(t, t.data_ptr(), 65, part, c, t, stream=0)
+    # GraphSAGE consumer: inconsistent layer shapes and bad dtypes
+    smp = gg.make_wsample(t, t, t, t, t, t)
+    w = _FakeTensor(1 << 21, 64 * 16)
+    for dtype, stride, dims in [(2, 256, [(64, 16), (16, 8)]),         # unknown dtype
+                                (gg.GG_F32, 128, [(64, 16), (16, 8)]),  # row wider than stride
+                                (gg.GG_F32, 256, [(64, 16), (15, 8)]),  # d_in != previous d_out
+                                (gg.GG_F32, 256, [(64, 16), (16, 129)])]:  # d_out > 128
+        arr = (gg.gg_sage_layer_t * 2)()
+        for j, (di, do) in enumerate(dims):
+            arr[j].d_in, arr[j].d_out, arr[j].relu = di, do, 1
+            arr[j].w_self = arr[j].w_neigh = w.data_ptr()
+        with pytest.raises(gg.GGError):
+            gg.gg_sage_forward(smp, 1000, 4, [3, 2], t, dtype, stride, 100, arr, t, 100, t, t,
+                               stream=0)

@@ -476,3 +476,116 @@ def test_simulator_counts_match_oracle(name, W, n_hot, driver, frac):
         assert got["rebuild_events"] == 0 and got["hits"] == 0
     if n_hot < 0 and frac is None:
         assert got["miss_events"] == 0
+
+
+def _sage_layers(rng, dims):
+    """Random GraphSAGE weights, scaled by 1/sqrt(d_in); ReLU on all but the
+    last layer."""
+    L = len(dims) - 1
+    return [((rng.standard_normal((dims[j], dims[j + 1])) / np.sqrt(dims[j])).astype(np.float32),
+             (rng.standard_normal((dims[j], dims[j + 1])) / np.sqrt(dims[j])).astype(np.float32),
+             (0.1 * rng.standard_normal(dims[j + 1])).astype(np.float32), j < L - 1)
+            for j in range(L)]
+
+
+def _sage_tolerance(layers, fanout, ab):
+    """Rounding bound of the fp32 kernels against the fp64 oracle: per layer
+    at most K + k + 5 roundings (a K-term product, a mean of up to k rows,
+    the reciprocal and its product, the self term and the bias), each of
+    relative size 2^-24 of the magnitudes the absolute-value pass bounds;
+    doubled for second-order terms."""
+    L = len(layers)
+    n = sum(layers[j][0].shape[0] + fanout[L - 1 - j] + 5 for j in range(L))
+    return 2.0 * n * 2.0 ** -24 * ab
+
+
+def _run_consumer(w, layers, x_dtype, stride, Wk):
+    import torch as T
+    from paper_2606_02916_amd import SageConsumer
+    lt = [(T.from_numpy(a).to(w.dev), T.from_numpy(b).to(w.dev), T.from_numpy(c).to(w.dev), r)
+          for a, b, c, r in layers]
+    cons = SageConsumer(w.pipe.geo, lt, x_dtype=x_dtype, device=w.dev)
+    out = cons.forward(w.pipe.buf, Wk, w.pipe.win_out, stride, w.pipe.status)
+    T.cuda.synchronize()
+    assert w.pipe.read_status() == 0
+    return out.cpu().numpy()
+
+
+@pytest.mark.parametrize("name,hidden,fp16,W", [
+    ("tiny", [16, 41], False, None), ("small", [16, 16, 47], False, None),
+    ("tiny", [128, 7], True, None), ("small", [40, 100, 3], False, 2),
+    ("tiny", [1, 1], False, 1)])
+def test_sage_consumer_matches_oracle(name, hidden, fp16, W):
+    log(f"{name}: GraphSAGE consumer, dims {hidden}, fp16={fp16}, W={W}")
+    from oracle import ggref
+    inst = synth.instance(name)
+    wl = inst.wl
+    kw = {}
+    d_in = wl.feat_dim
+    stride = wl.row_stride
+    if fp16:   # the same values rounded to fp16, 2-byte elements
+        kw["shards"] = [np.ascontiguousarray(
+            s[:, :wl.row_bytes].view(np.float32).astype(np.float16)).view(np.uint8)
+            for s in inst.shards]
+        kw["row_bytes"] = kw["stride"] = stride = 2 * d_in
+    w = world(inst, W=W, **kw)
+    r = w.run_and_compare(0)
+    Wk, fan = r["Wk"], list(wl.fanout)
+    rng = np.random.default_rng(len(hidden) * 100 + hidden[0])
+    layers = _sage_layers(rng, [d_in] + hidden)
+    x = np.concatenate(r["outs"])          # the oracle's own gathered rows
+    dt = 1 if fp16 else 0
+    ref, ab = ggref.sage_forward(r["fids"], r["foff"], r["nids"], r["noff"], Wk, fan, x, dt,
+                                 stride, layers)
+    got = _run_consumer(w, layers, dt, stride, Wk)[:ref.shape[0]]
+    tol = _sage_tolerance(layers, fan, ab)
+    err = np.abs(got.astype(np.float64) - ref)
+    assert np.all(err <= tol), (float(np.max(err - tol)), float(np.max(err)))
+    assert ref.shape[0] == int(r["foff"][Wk] - r["foff"][0])
+
+
+@pytest.mark.timeout(900)
+def test_sage_consumer_large_sparse_window_sampled_batches():
+    """The consumer over a whole 16-batch window of the 2.45M-node graph, as
+    the benchmark lays it out; the oracle recomputes two of the batches from
+    its own sampling and the feature shards."""
+    log("large_sparse: GraphSAGE consumer over a full window, batches 0 and 11 checked")
+    import torch as T
+    from oracle import ggref
+    inst = synth.instance("large_sparse")
+    wl = inst.wl
+    w = world(inst)
+    pipe, dev = w.pipe, w.dev
+    boff = inst.batch_off
+    b0, b1 = synth.window_batches(boff, wl.W, 3)
+    seeds_d = T.from_numpy(inst.seeds[boff[b0]:boff[b1]]).to(dev)
+    Wk = pipe.window(seeds_d, boff[b0:b1 + 1] - boff[b0], b0)
+    rng = np.random.default_rng(7)
+    layers = _sage_layers(rng, [wl.feat_dim, 16, 16, 47])
+    from paper_2606_02916_amd import SageConsumer
+    lt = [(T.from_numpy(a).to(dev), T.from_numpy(b).to(dev), T.from_numpy(c).to(dev), r_)
+          for a, b, c, r_ in layers]
+    cons = SageConsumer(pipe.geo, lt, device=dev)
+    out = cons.forward(pipe.buf, Wk, pipe.win_out, wl.row_stride, pipe.status)
+    T.cuda.synchronize()
+    assert pipe.read_status() == 0
+    foff_g = pipe.frontier_off[:(len(wl.fanout) + 1) * Wk + 1].cpu().numpy()
+    got_all = out.cpu().numpy()
+    part = ggref.make_part(wl.num_parts, wl.part_kind, wl.local_owner, wl.num_nodes,
+                           inst.range_start)
+    L = len(wl.fanout)
+    for b in (0, 11):
+        g = b0 + b
+        so = np.array([0, boff[g + 1] - boff[g]], np.int64)
+        fids, foff, nids, noff = ggref.sample_window(inst.row_ptr, inst.col_idx,
+                                                     inst.seeds[boff[g]:boff[g + 1]], so,
+                                                     wl.fanout, 0, 0, g)
+        ids = fids[foff[L]:foff[L + 1]]
+        x = np.stack([inst.shards[ggref.owner(part, int(u))][ggref.row(part, int(u))]
+                      for u in ids])
+        ref, ab = ggref.sage_forward(fids, foff, nids, noff, 1, wl.fanout, x, 0, wl.row_stride,
+                                     layers)
+        got = got_all[foff_g[b] - foff_g[0]:foff_g[b + 1] - foff_g[0]]
+        assert got.shape == ref.shape
+        tol = _sage_tolerance(layers, list(wl.fanout), ab)
+        assert np.all(np.abs(got.astype(np.float64) - ref) <= tol), b
