@@ -16,7 +16,9 @@ PART_MOD = 0
 PART_RANGE = 1
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
-LIB_PATH = os.path.join(_HERE, "libggref.so")
+# GGREF_LIB lets the oracle's own mutation tests load a deliberately broken
+# build of it; nothing else sets it.
+LIB_PATH = os.environ.get("GGREF_LIB") or os.path.join(_HERE, "libggref.so")
 
 
 class Csr(C.Structure):

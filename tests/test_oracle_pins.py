@@ -47,9 +47,9 @@ def test_philox_matches_independent_engine():
 @pytest.mark.parametrize("bound", [3, 7])
 def test_bounded_map_preimage_counts_exhaustive(bound):
     exe = helpers.build_helper("bounded_count.c",
-                               extra=["-fopenmp", "-L" + os.path.join(helpers.ROOT, "oracle"),
+                               extra=["-fopenmp", "-L" + os.path.dirname(ggref.LIB_PATH),
                                       "-lggref",
-                                      "-Wl,-rpath," + os.path.join(helpers.ROOT, "oracle")])
+                                      "-Wl,-rpath," + os.path.dirname(ggref.LIB_PATH)])
     out = subprocess.run([exe, str(bound)], capture_output=True, text=True, check=True)
     mn, mx, nv, mono, first, last, oor = (int(x) for x in out.stdout.split())
     assert oor == 0

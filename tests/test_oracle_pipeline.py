@@ -110,6 +110,31 @@ def test_sampler_equals_bfs_ball_when_fanout_covers_every_degree(gname):
             assert F[L][b] == helpers.bfs_ball(row_ptr, col_idx, seeds[soff[b]:soff[b + 1]], L)
 
 
+@pytest.mark.parametrize("d,k", [(6, 3), (5, 4), (9, 2)])
+def test_sampler_subsets_uniform_chi2(d, k):
+    """The whole draw chain (Philox words, bounded map, Floyd) on one node of
+    degree d > k: every k-subset of its neighbours is equally likely.
+    20,000 batches, chi-square over the C(d, k) subsets."""
+    import itertools
+    row_ptr, col_idx = helpers.csr_from_edges(d + 1, [(0, i) for i in range(1, d + 1)])
+    n_batches = 20000
+    seeds = np.zeros(n_batches, dtype=np.int32)
+    soff = np.arange(n_batches + 1, dtype=np.int64)
+    _, _, nids, _ = ggref.sample_window(row_ptr, col_idx, seeds, soff, [k], 99, 0, 0)
+    subsets = {c: i for i, c in enumerate(itertools.combinations(range(1, d + 1), k))}
+    per = nids.reshape(n_batches, k)
+    counts = np.zeros(len(subsets))
+    for r in per.tolist():
+        counts[subsets[tuple(r)]] += 1          # ascending and distinct, or KeyError
+    expected = n_batches / len(subsets)
+    chi2 = float(((counts - expected) ** 2 / expected).sum())
+    # chi-square quantile 1 - 1e-6 for C(d, k) - 1 <= 35 degrees of freedom is below 90
+    assert chi2 < 90.0, chi2
+    # every position kept with probability k / d
+    pos = np.bincount(per.ravel(), minlength=d + 1)[1:] / n_batches
+    assert np.all(np.abs(pos - k / d) < 6 * np.sqrt(k / d * (1 - k / d) / n_batches)), pos
+
+
 def test_sampler_star_leaves_uniform_chi2():
     # One hub with 100 leaves sampled at k = 10 across many batches: every
     # leaf must be kept with probability k / 100.
