@@ -71,6 +71,7 @@ extern "C" {
 #define GG_DEV_BAD_ID 2     /* a seed or neighbour id outside [0, num_nodes) */
 #define GG_DEV_BAD_ROW 4    /* a feature row or cache slot outside its shard or cache */
 #define GG_DEV_BAD_DEGREE 8 /* a node degree of 2^32 or more */
+#define GG_DEV_ORDER 16     /* ids declared owner-ordered were not; bucketing output invalid */
 
 /* Graph in CSR form (device): row u holds the sampled-from neighbours of u
  * at col_idx[row_ptr[u] .. row_ptr[u+1]). */
@@ -207,10 +208,19 @@ int gg_build_hotset(const uint32_t* frontier_bits_d, int32_t W, const gg_part_t*
 /* Groups the hot set by owner, one bucket per owner (Sec. IV-A: one bulk
  * request per partition owner): bucket_ids_d receives the hot_count_d[0]
  * (<= cap) ids owner-major, input order kept inside each owner;
- * owner_off_d[m] .. owner_off_d[m+1] is owner m's bucket (P+1 entries). */
+ * owner_off_d[m] .. owner_off_d[m+1] is owner m's bucket (P+1 entries).
+ * flags: 0, or GG_BUCKET_OWNER_ORDERED when the caller knows the owners of
+ * hot_ids_d never decrease along the list (true of gg_build_hotset's
+ * ascending output under a GG_PART_RANGE book).  Under a range book that
+ * list is its own bucketing, so the call is then a single copy pass; if the
+ * order does not hold after all, GG_DEV_ORDER is raised and bucket_ids_d /
+ * owner_off_d are not valid.  Under a GG_PART_MOD book the flag changes
+ * nothing.  Any other flag bit is GG_ERR_ARG. */
+#define GG_BUCKET_OWNER_ORDERED 1
 int gg_bucket_by_owner(const int32_t* hot_ids_d, const int64_t* hot_count_d, int64_t cap,
-                       const gg_part_t* part, int32_t* bucket_ids_d, int64_t* owner_off_d,
-                       int32_t* status_d, void* ws, size_t ws_bytes, hipStream_t stream);
+                       const gg_part_t* part, int32_t flags, int32_t* bucket_ids_d,
+                       int64_t* owner_off_d, int32_t* status_d, void* ws, size_t ws_bytes,
+                       hipStream_t stream);
 
 /* Stages the window cache (Sec. IV-C; Algorithm 1 WarmCache).  The rows of
  * the bucketed hot set (owner_off_d[P] <= cap entries of bucket_ids_d) go

@@ -214,7 +214,8 @@ struct GatherWs {
 };
 
 int32_t blocks_per_seg(int64_t n_cap, int32_t nseg) {
-  int64_t bx = std::max<int64_t>(kMaxBlocks / nseg, 8);
+  static const int max_blocks = env_int("GG_GATHER_BLOCKS", kMaxBlocks);
+  int64_t bx = std::max<int64_t>(max_blocks / nseg, 8);
   bx = std::min<int64_t>(bx, std::max<int64_t>(1, cdiv(n_cap, kBlock)));
   return (int32_t)bx;
 }

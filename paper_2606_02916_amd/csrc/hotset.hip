@@ -79,34 +79,34 @@ __device__ __forceinline__ uint32_t remote_mask(const KPart& p, int64_t w) {
   return ~local;
 }
 
-// Loads the 8 words of this thread for every batch and sums them into planes.
-__device__ __forceinline__ void load_planes(const uint32_t* bits, const HotArgs& a, int64_t w0,
-                                            uint32_t (&pl)[8][kPlanes]) {
+// One 32-node word per thread: a block covers kHotWords consecutive words,
+// so a window of N nodes spreads over N / 8192 blocks.
+constexpr int kHotWords = kBlock;
+constexpr int kHotMaxIds = kHotWords * 32;  // ids one block can emit
+
+// Sums word w of every batch's set into the planes, eight loads in flight.
+__device__ __forceinline__ void load_planes(const uint32_t* bits, const HotArgs& a, int64_t w,
+                                            uint32_t (&pl)[kPlanes]) {
 #pragma unroll
-  for (int j = 0; j < 8; ++j)
+  for (int p = 0; p < kPlanes; ++p) pl[p] = 0u;
+  int32_t b = 0;
+  for (; b + 8 <= a.W; b += 8) {
+    uint32_t x[8];
 #pragma unroll
-    for (int p = 0; p < kPlanes; ++p) pl[j][p] = 0u;
-  for (int32_t b = 0; b < a.W; ++b) {
-    const u32x4* q = (const u32x4*)(bits + (int64_t)b * a.wpb + w0);
-    const u32x4 x = q[0], y = q[1];
-    bs_add(pl[0], x.x);
-    bs_add(pl[1], x.y);
-    bs_add(pl[2], x.z);
-    bs_add(pl[3], x.w);
-    bs_add(pl[4], y.x);
-    bs_add(pl[5], y.y);
-    bs_add(pl[6], y.z);
-    bs_add(pl[7], y.w);
+    for (int j = 0; j < 8; ++j) x[j] = bits[(int64_t)(b + j) * a.wpb + w];
+#pragma unroll
+    for (int j = 0; j < 8; ++j) bs_add(pl, x[j]);
   }
+  for (; b < a.W; ++b) bs_add(pl, bits[(int64_t)b * a.wpb + w]);
 }
 
-__device__ __forceinline__ void mask_planes(const KPart& p, int64_t w0, uint32_t (&pl)[8][kPlanes]) {
+// The planes of word w restricted to remote nodes.
+__device__ __forceinline__ void remote_planes(const uint32_t* bits, const KPart& part,
+                                              const HotArgs& a, int64_t w, uint32_t (&pl)[kPlanes]) {
+  load_planes(bits, a, w, pl);
+  const uint32_t m = remote_mask(part, w);
 #pragma unroll
-  for (int j = 0; j < 8; ++j) {
-    const uint32_t m = remote_mask(p, w0 + j);
-#pragma unroll
-    for (int q = 0; q < kPlanes; ++q) pl[j][q] &= m;
-  }
+  for (int q = 0; q < kPlanes; ++q) pl[q] &= m;
 }
 
 // Per-chunk histogram of freq over the remote nodes of the window.
@@ -116,19 +116,13 @@ __global__ void __launch_bounds__(kBlock) k_hot_hist(const uint32_t* bits, KPart
   for (int t = threadIdx.x; t < GG_MAX_W + 2; t += blockDim.x) hist[t] = 0;
   __syncthreads();
   const int c = blockIdx.x;
-  const int64_t w0 = (int64_t)c * kChunkWords + threadIdx.x * kWordsPerThread;
-  uint32_t pl[8][kPlanes];
-  load_planes(bits, a, w0, pl);
-  mask_planes(part, w0, pl);
+  uint32_t pl[kPlanes];
+  remote_planes(bits, part, a, (int64_t)c * kHotWords + threadIdx.x, pl);
   for (int32_t f = 1; f <= a.W; ++f) {
-    int n = 0;
-#pragma unroll
-    for (int j = 0; j < 8; ++j) {
-      uint32_t g, e;
-      bs_cmp(pl[j], (uint32_t)f, &g, &e);
-      n += __popc(e);
-    }
-    if (n) atomicAdd(&hist[f], n);
+    uint32_t g, e;
+    bs_cmp(pl, (uint32_t)f, &g, &e);
+    const int n = wave_sum(__popc(e));
+    if (lane_id() == 0 && n) atomicAdd(&hist[f], n);
   }
   __syncthreads();
   for (int t = threadIdx.x; t <= a.W; t += blockDim.x) chunk_hist[(int64_t)c * (a.W + 1) + t] = hist[t];
@@ -143,11 +137,12 @@ __global__ void __launch_bounds__(1024) k_hot_select(const int32_t* chunk_hist, 
   __shared__ int64_t hist[GG_MAX_W + 2];
   for (int t = threadIdx.x; t < GG_MAX_W + 2; t += blockDim.x) hist[t] = 0;
   __syncthreads();
-  for (int64_t c = threadIdx.x; c < nch; c += blockDim.x)
-    for (int32_t f = 1; f <= W; ++f) {
-      const int32_t v = chunk_hist[c * (W + 1) + f];
-      if (v) atomicAdd((unsigned long long*)&hist[f], (unsigned long long)v);
-    }
+  for (int32_t f = 1; f <= W; ++f) {
+    int64_t v = 0;
+    for (int64_t c = threadIdx.x; c < nch; c += blockDim.x) v += chunk_hist[c * (W + 1) + f];
+    v = wave_sum(v);
+    if (lane_id() == 0 && v) atomicAdd((unsigned long long*)&hist[f], (unsigned long long)v);
+  }
   __syncthreads();
   if (threadIdx.x == 0) {
     int64_t total = 0;
@@ -185,30 +180,28 @@ __device__ __forceinline__ void get_sel(const HotArgs& a, const int64_t* params,
   }
 }
 
+// Masks of the remote nodes of a word with freq > f* and freq == f*.
+__device__ __forceinline__ void sel_masks(const uint32_t (&pl)[kPlanes], uint32_t fstar,
+                                          uint32_t* gm, uint32_t* em) {
+  bs_cmp(pl, fstar, gm, em);
+  if (fstar == 0) *em = 0u;  // freq == 0 is not a member
+}
+
 // Per-chunk counts of nodes with freq > f* and freq == f*.
 __global__ void __launch_bounds__(kBlock) k_hot_count(const uint32_t* bits, KPart part, HotArgs a,
                                                       const int64_t* params, int32_t* cnt_gt,
                                                       int32_t* cnt_eq) {
   __shared__ int32_t lds[2][kBlock / kWave];
   const int c = blockIdx.x;
-  const int64_t w0 = (int64_t)c * kChunkWords + threadIdx.x * kWordsPerThread;
   uint32_t fstar;
   int64_t r;
   get_sel(a, params, &fstar, &r);
-  uint32_t pl[8][kPlanes];
-  load_planes(bits, a, w0, pl);
-  mask_planes(part, w0, pl);
-  int ng = 0, ne = 0;
-#pragma unroll
-  for (int j = 0; j < 8; ++j) {
-    uint32_t g, e;
-    bs_cmp(pl[j], fstar, &g, &e);
-    if (fstar == 0) e = 0u;  // freq == 0 is not a member
-    ng += __popc(g);
-    ne += __popc(e);
-  }
-  ng = wave_sum(ng);
-  ne = wave_sum(ne);
+  uint32_t pl[kPlanes];
+  remote_planes(bits, part, a, (int64_t)c * kHotWords + threadIdx.x, pl);
+  uint32_t g, e;
+  sel_masks(pl, fstar, &g, &e);
+  const int ng = wave_sum(__popc(g));
+  const int ne = wave_sum(__popc(e));
   if (lane_id() == 0) {
     lds[0][threadIdx.x / kWave] = ng;
     lds[1][threadIdx.x / kWave] = ne;
@@ -238,54 +231,51 @@ __global__ void __launch_bounds__(1024) k_hot_scan(const int32_t* cnt_gt, const 
   }
 }
 
+// Writes the chunk's selected ids (and their freq) ascending.  Each thread
+// owns one word; the block's ids are assembled in LDS at their block-local
+// positions and then written out as one contiguous run.
 __global__ void __launch_bounds__(kBlock) k_hot_emit(const uint32_t* bits, KPart part, HotArgs a,
                                                      const int64_t* params, const int64_t* off_gt,
                                                      const int64_t* off_eq, int32_t* hot_ids,
                                                      int32_t* hot_freq) {
+  __shared__ int32_t s_out[kHotMaxIds];
   __shared__ int64_t lds[kBlock / kWave];
   const int c = blockIdx.x;
-  const int64_t w0 = (int64_t)c * kChunkWords + threadIdx.x * kWordsPerThread;
+  const int64_t w = (int64_t)c * kHotWords + threadIdx.x;
   uint32_t fstar;
   int64_t r;
   get_sel(a, params, &fstar, &r);
-  uint32_t pl[8][kPlanes];
-  load_planes(bits, a, w0, pl);
-  mask_planes(part, w0, pl);
-  uint32_t gm[8], em[8];
-  int64_t ng = 0, ne = 0;
-#pragma unroll
-  for (int j = 0; j < 8; ++j) {
-    bs_cmp(pl[j], fstar, &gm[j], &em[j]);
-    if (fstar == 0) em[j] = 0u;
-    ng += __popc(gm[j]);
-    ne += __popc(em[j]);
-  }
+  uint32_t pl[kPlanes];
+  remote_planes(bits, part, a, w, pl);
+  uint32_t gm, em;
+  sel_masks(pl, fstar, &gm, &em);
+  const int ne = __popc(em);
   int64_t tot;
-  const int64_t eq_rank0 = off_eq[c] + block_excl_scan<kBlock>(ne, lds, &tot);
-  int64_t take_eq = r - eq_rank0;
-  take_eq = take_eq < 0 ? 0 : (take_eq > ne ? ne : take_eq);
-  const int64_t sel_before_chunk = off_gt[c] + (off_eq[c] < r ? off_eq[c] : r);
-  int64_t pos = sel_before_chunk + block_excl_scan<kBlock>(ng + take_eq, lds, &tot);
-  int64_t eq_rank = eq_rank0;
-#pragma unroll
-  for (int j = 0; j < 8; ++j) {
-    uint32_t m = gm[j] | em[j];
-    while (m) {
+  // freq == f* nodes are taken in id order until r of them are in.
+  const int64_t eq_rank0 = off_eq[c] + block_excl_scan<kBlock>((int64_t)ne, lds, &tot);
+  int64_t take = r - eq_rank0;
+  take = take < 0 ? 0 : (take > ne ? ne : take);
+  uint32_t sel = gm;
+  for (uint32_t e = em; take > 0; --take) {
+    sel |= e & (0u - e);  // lowest remaining id
+    e &= e - 1u;
+  }
+  int64_t btot;
+  const int64_t lpos = block_excl_scan<kBlock>((int64_t)__popc(sel), lds, &btot);
+  const int64_t pos0 = off_gt[c] + (off_eq[c] < r ? off_eq[c] : r);
+  for (int pass = 0; pass < (hot_freq ? 2 : 1); ++pass) {
+    int32_t* dst = pass == 0 ? hot_ids : hot_freq;
+    int64_t p = lpos;
+    for (uint32_t m = sel; m; m &= m - 1u) {
       const int bit = __ffs(m) - 1;
-      m &= m - 1;
-      bool take = true;
-      if ((em[j] >> bit) & 1u) {
-        take = eq_rank < r;
-        ++eq_rank;
-      }
-      if (take) {
-        if (pos < a.cap) {
-          hot_ids[pos] = (int32_t)((w0 + j) * 32 + bit);
-          if (hot_freq) hot_freq[pos] = (int32_t)bs_freq(pl[j], bit);
-        }
-        ++pos;
-      }
+      s_out[p++] = pass == 0 ? (int32_t)(w * 32 + bit) : (int32_t)bs_freq(pl, bit);
     }
+    __syncthreads();
+    for (int64_t i = threadIdx.x; i < btot; i += kBlock) {
+      const int64_t o = pos0 + i;
+      if (o < a.cap) dst[o] = s_out[i];
+    }
+    __syncthreads();
   }
 }
 
@@ -299,7 +289,7 @@ struct HotWs {
 };
 
 size_t hot_ws_layout(int64_t num_nodes, int32_t W, char* base, HotWs* out) {
-  const int64_t nch = gg_bits_words(num_nodes) / kChunkWords;
+  const int64_t nch = gg_bits_words(num_nodes) / kHotWords;
   Carve cv{base, 0, ~(size_t)0};
   HotWs h;
   h.chunk_hist = cv.take<int32_t>((size_t)(nch * (W + 1)));
@@ -343,7 +333,7 @@ extern "C" int gg_build_hotset(const uint32_t* frontier_bits_d, int32_t W, const
   const size_t need_ws = hot_ws_layout(kp.N, W, (char*)ws, &hw);
   GG_REQUIRE(ws && ws_bytes >= need_ws, "workspace of %zu bytes < %zu", ws_bytes, need_ws);
   const int64_t wpb = gg_bits_words(kp.N);
-  const int32_t nch = (int32_t)(wpb / kChunkWords);
+  const int32_t nch = (int32_t)(wpb / kHotWords);
   HotArgs a;
   a.wpb = wpb;
   a.cap = cap;

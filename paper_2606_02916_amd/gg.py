@@ -26,10 +26,13 @@ GG_ERR_CAPACITY = 2
 GG_ERR_HIP = 3
 GG_ERR_UNSUPPORTED = 4
 
+GG_BUCKET_OWNER_ORDERED = 1
+
 DEV_CAPACITY = 1
 DEV_BAD_ID = 2
 DEV_BAD_ROW = 4
 DEV_BAD_DEGREE = 8
+DEV_ORDER = 16
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_HERE, "libgg.so")
@@ -111,7 +114,7 @@ SIGNATURES = {
                                    _P]),
     "gg_build_hotset": (C.c_int, [_P, _I32, _P, _I64, _I64, _I64, _P, _P, _I64, _P, _P, _P, _SZ,
                                   _P]),
-    "gg_bucket_by_owner": (C.c_int, [_P, _P, _I64, _P, _P, _P, _P, _P, _SZ, _P]),
+    "gg_bucket_by_owner": (C.c_int, [_P, _P, _I64, _P, _I32, _P, _P, _P, _P, _SZ, _P]),
     "gg_stage_bulk": (C.c_int, [_P, _P, _I64, _P, _P, _P, _I64, _I64, _P, _P, _P, _P, _P, _P, _P,
                                 _P, _SZ, _P]),
     "gg_gather_batch": (C.c_int, [_P, _P, _I32, _I64, _P, _P, _P, _I64, _I64, _P, _P, _I64, _P,
@@ -260,8 +263,10 @@ def gg_build_hotset(frontier_bits, W, part, n_hot, hot_ids, hot_freq, cap, hot_c
 
 
 def gg_bucket_by_owner(hot_ids, hot_count, cap, part, bucket_ids, owner_off, status, ws,
-                       stream=None):
-    return check(lib.gg_bucket_by_owner(_ptr(hot_ids), _ptr(hot_count), cap, C.byref(part),
+                       stream=None, flags=0):
+    """flags = GG_BUCKET_OWNER_ORDERED when hot_ids is known to be in owner
+    order (the ascending output of gg_build_hotset under a range book)."""
+    return check(lib.gg_bucket_by_owner(_ptr(hot_ids), _ptr(hot_count), cap, C.byref(part), flags,
                                         _ptr(bucket_ids), _ptr(owner_off), _ptr(status), _ptr(ws),
                                         ws.numel(), _stream(stream)), "gg_bucket_by_owner")
 

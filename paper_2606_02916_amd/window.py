@@ -22,6 +22,12 @@ import torch
 from . import gg
 
 
+def _bucket_flags(part):
+    """The hot set comes out ascending, which under a range book is owner
+    order: bucketing is then one copy pass."""
+    return gg.GG_BUCKET_OWNER_ORDERED if part.kind == gg.PART_RANGE else 0
+
+
 class _Geometry:
     """Sizes shared by all buffer sets of a pipeline."""
 
@@ -157,7 +163,8 @@ class FetchPipeline:
 
     def bucket(self, cur):
         gg.gg_bucket_by_owner(self.hot_ids, self.hot_count[cur], self.hot_cap, self.part,
-                              self.bucket_ids[cur], self.owner_off, self.status, self.ws)
+                              self.bucket_ids[cur], self.owner_off, self.status, self.ws,
+                              flags=_bucket_flags(self.part))
 
     def stage(self, cur):
         """Rebuilds the cache for window k (= self.k, advanced by the caller)."""
@@ -366,7 +373,8 @@ class LookaheadPipeline:
                            stream=s, hot_frac=self.hot_frac)
         _rec(ev[2], bs)
         gg.gg_bucket_by_owner(cur.hot_ids, self.hot_count[T], g.hot_cap, self.part,
-                              self.bucket_ids[T], cur.owner_off, self.status, cur.ws, stream=s)
+                              self.bucket_ids[T], cur.owner_off, self.status, cur.ws, stream=s,
+                              flags=_bucket_flags(self.part))
         _rec(ev[3], bs)
         self.built[X].record(bs)
         ss.wait_event(self.built[X])

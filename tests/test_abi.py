@@ -143,6 +143,9 @@ def test_bad_arguments_are_rejected_on_the_host(gg):
     part = gg.make_part(4, gg.PART_RANGE, 0, 100, [0, 10, 20, 30, 99])  # does not end at N
     with pytest.raises(gg.GGError):
         gg.gg_bucket_by_owner(t, t, 10, part, t, t, t, t, stream=0)
+    part = gg.make_part(4, gg.PART_RANGE, 0, 100, [0, 10, 20, 30, 100])
+    with pytest.raises(gg.GGError):                                      # unknown flag bit
+        gg.gg_bucket_by_owner(t, t, 10, part, t, t, t, t, stream=0, flags=2)
     part = gg.make_part(4, gg.PART_MOD, 4, 100)                          # local owner >= P
     feat = gg.make_feat(256, [t] * 4, [256] * 4, [25] * 4)
     with pytest.raises(gg.GGError):

@@ -172,10 +172,13 @@ def test_dense_mid_full_window_matches_oracle():
     w.run_and_compare(0)
 
 
+@pytest.mark.parametrize("flags", [0, 1])
 @pytest.mark.parametrize("kind", [0, 1])
 @pytest.mark.parametrize("order", ["ascending", "shuffled", "one_descent"])
-def test_bucket_by_owner_direct(kind, order):
-    log(f"bucket_by_owner: kind={kind} order={order}")
+def test_bucket_by_owner_direct(kind, order, flags):
+    """flags=1 is GG_BUCKET_OWNER_ORDERED: under a range book an input out of
+    owner order must raise GG_DEV_ORDER instead of being bucketed."""
+    log(f"bucket_by_owner: kind={kind} order={order} flags={flags}")
     import torch as T
     from oracle import ggref
     from paper_2606_02916_amd import gg
@@ -199,11 +202,15 @@ def test_bucket_by_owner_direct(kind, order):
     status = T.zeros(1, dtype=T.int32, device=dev)
     ws = T.empty(gg.gg_ws_bucket(cap, P), dtype=T.uint8, device=dev)
     part = gg.make_part(P, kind, 0, N, rs if kind == 1 else None)
-    gg.gg_bucket_by_owner(hot, cnt, cap, part, out, off, status, ws)
+    gg.gg_bucket_by_owner(hot, cnt, cap, part, out, off, status, ws, flags=flags)
     T.cuda.synchronize()
+    if flags and kind == 1 and order != "ascending":
+        assert int(status.item()) == gg.DEV_ORDER
+        return
     assert int(status.item()) == 0
     assert np.array_equal(off.cpu().numpy(), want_off)
     assert np.array_equal(out[:ids.shape[0]].cpu().numpy(), want)
+    assert np.all(out[ids.shape[0]:].cpu().numpy() == -7)
 
 
 @pytest.mark.timeout(900)
