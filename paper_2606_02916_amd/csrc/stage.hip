@@ -31,9 +31,15 @@ __device__ __forceinline__ int64_t stage_n(const int64_t* owner_off, int32_t P, 
 // (or, without a source cache, the current remap before clearing) gives
 // the node of bucket entry s; rows with none are the delta.  Every block
 // writes its per-owner delta counts to dcnt[block * P + m].
+// When the old slots come from a different remap than the one being
+// rebuilt, the same launch also clears the rebuilt remap's entries
+// clear[0 .. clear_count[0]) (otherwise k_slot_reset does, afterwards).
 __global__ void __launch_bounds__(kBlock) k_stage_delta(const int32_t* bucket, const int64_t* owner_off,
                                                         KPart part, StageArgs a, const int32_t* before,
-                                                        int32_t* old_slot, int32_t* dcnt) {
+                                                        int32_t* old_slot, int32_t* dcnt,
+                                                        const int32_t* clear,
+                                                        const int64_t* clear_count,
+                                                        int32_t* slot_of) {
   __shared__ int32_t hist[GG_MAX_PARTS];
   __shared__ int64_t s_start[GG_MAX_PARTS + 1];
   for (int t = threadIdx.x; t < GG_MAX_PARTS; t += blockDim.x) hist[t] = 0;
@@ -59,6 +65,14 @@ __global__ void __launch_bounds__(kBlock) k_stage_delta(const int32_t* bucket, c
     }
     wave_hist_add(hist, fresh, m);
   }
+  if (clear) {
+    const int64_t nc = clear_count[0];
+    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < nc;
+         i += (int64_t)gridDim.x * blockDim.x) {
+      const int32_t u = clear[i];
+      if (u >= 0 && (int64_t)u < part.N) slot_of[u] = -1;
+    }
+  }
   __syncthreads();
   for (int m = threadIdx.x; m < part.P; m += blockDim.x) dcnt[(int64_t)blockIdx.x * part.P + m] = hist[m];
 }
@@ -73,58 +87,24 @@ __global__ void __launch_bounds__(kBlock) k_slot_reset(const int32_t* prev, cons
   }
 }
 
-template <int VB, bool NT>
-__global__ void __launch_bounds__(kBlock) k_stage_rows(const int32_t* bucket, const int64_t* owner_off,
-                                                       KPart part, KFeat feat, StageArgs a,
-                                                       char* cache, int32_t* slot_of,
-                                                       const char* src_cache, const int32_t* old_slot,
-                                                       int32_t* status) {
-  __shared__ int64_t s_start[GG_MAX_PARTS + 1];
-  for (int t = threadIdx.x; t <= GG_MAX_PARTS; t += blockDim.x) s_start[t] = part.start[t];
-  __syncthreads();
-  const int64_t n = stage_n(owner_off, part.P, a);
-  const int64_t ntiles = (n + kWave - 1) / kWave;
-  const int lane = lane_id();
-  int32_t st = 0;
-  for (int64_t tile = (int64_t)blockIdx.x * (kBlock / kWave) + threadIdx.x / kWave; tile < ntiles;
-       tile += (int64_t)gridDim.x * (kBlock / kWave)) {
-    const int64_t s0 = tile * kWave;
-    const int64_t s = s0 + lane;
-    const char* src = nullptr;
-    if (s < n) {
-      const int32_t u = bucket[s];
-      if (u < 0 || (int64_t)u >= part.N) {
-        st |= GG_DEV_BAD_ID;
-      } else {
-        const int32_t old = src_cache ? old_slot[s] : -1;
-        if (old >= 0 && (int64_t)old < a.cache_rows) {
-          src = src_cache + (int64_t)old * a.cache_stride;   // retained: device-local copy
-          slot_of[u] = (int32_t)s;
-        } else {
-          if (old >= 0) st |= GG_DEV_BAD_ROW;
-          const int32_t m = owner_of(part, s_start, u);
-          const int64_t r = row_of(part, s_start, u, m);
-          if (r >= feat.rows[m]) {
-            st |= GG_DEV_BAD_ROW;
-          } else {
-            src = feat.shard[m] + r * feat.stride[m];          // requested from owner m
-            slot_of[u] = (int32_t)s;
-          }
-        }
-      }
-    }
-    const int nrows = (int)((n - s0) < kWave ? (n - s0) : kWave);
-    wave_copy_rows<VB, NT>(src, cache + s0 * a.cache_stride, a.cache_stride, nrows, a.geom);
-  }
-  if (st) set_status(status, st);
-}
+// Statistics of the call: per-owner requests, rows and bytes and the
+// rebuild delta.  Their inputs (owner_off, the delta counts of
+// k_stage_delta) are complete before k_stage_rows starts, so its block 0
+// computes them.
+struct StageStatsArgs {
+  const int64_t* prev_count;
+  const int32_t* dcnt;
+  gg_stage_stats_t* stats;
+  int32_t nblk_delta;
+  int32_t has_src;
+};
 
-__global__ void __launch_bounds__(kBlock) k_stage_finish(const int64_t* owner_off, KPart part,
-                                                         StageArgs a, const int64_t* prev_count,
-                                                         int32_t row_bytes, const int32_t* dcnt,
-                                                         int32_t nblk_delta, int32_t has_src,
-                                                         gg_stage_stats_t* stats,
-                                                         int32_t* status) {
+__device__ void stage_stats(const int64_t* owner_off, const KPart& part, const StageArgs& a,
+                            int32_t row_bytes, const StageStatsArgs& sa, int32_t* status) {
+  const int64_t* prev_count = sa.prev_count;
+  const int32_t* dcnt = sa.dcnt;
+  const int32_t nblk_delta = sa.nblk_delta, has_src = sa.has_src;
+  gg_stage_stats_t* stats = sa.stats;
   __shared__ int32_t s_delta[GG_MAX_PARTS];
   for (int t = threadIdx.x; t < GG_MAX_PARTS; t += blockDim.x) s_delta[t] = 0;
   __syncthreads();
@@ -169,17 +149,64 @@ __global__ void __launch_bounds__(kBlock) k_stage_finish(const int64_t* owner_of
   }
 }
 
+template <int VB, bool NT>
+__global__ void __launch_bounds__(kBlock) k_stage_rows(const int32_t* bucket, const int64_t* owner_off,
+                                                       KPart part, KFeat feat, StageArgs a,
+                                                       char* cache, int32_t* slot_of,
+                                                       const char* src_cache, const int32_t* old_slot,
+                                                       StageStatsArgs sa, int32_t* status) {
+  if (blockIdx.x == 0) stage_stats(owner_off, part, a, feat.row_bytes, sa, status);
+  __shared__ int64_t s_start[GG_MAX_PARTS + 1];
+  for (int t = threadIdx.x; t <= GG_MAX_PARTS; t += blockDim.x) s_start[t] = part.start[t];
+  __syncthreads();
+  const int64_t n = stage_n(owner_off, part.P, a);
+  const int64_t ntiles = (n + kWave - 1) / kWave;
+  const int lane = lane_id();
+  int32_t st = 0;
+  for (int64_t tile = (int64_t)blockIdx.x * (kBlock / kWave) + threadIdx.x / kWave; tile < ntiles;
+       tile += (int64_t)gridDim.x * (kBlock / kWave)) {
+    const int64_t s0 = tile * kWave;
+    const int64_t s = s0 + lane;
+    const char* src = nullptr;
+    if (s < n) {
+      const int32_t u = bucket[s];
+      if (u < 0 || (int64_t)u >= part.N) {
+        st |= GG_DEV_BAD_ID;
+      } else {
+        const int32_t old = src_cache ? old_slot[s] : -1;
+        if (old >= 0 && (int64_t)old < a.cache_rows) {
+          src = src_cache + (int64_t)old * a.cache_stride;   // retained: device-local copy
+          slot_of[u] = (int32_t)s;
+        } else {
+          if (old >= 0) st |= GG_DEV_BAD_ROW;
+          const int32_t m = owner_of(part, s_start, u);
+          const int64_t r = row_of(part, s_start, u, m);
+          if (r >= feat.rows[m]) {
+            st |= GG_DEV_BAD_ROW;
+          } else {
+            src = feat.shard[m] + r * feat.stride[m];          // requested from owner m
+            slot_of[u] = (int32_t)s;
+          }
+        }
+      }
+    }
+    const int nrows = (int)((n - s0) < kWave ? (n - s0) : kWave);
+    wave_copy_rows<VB, NT>(src, cache + s0 * a.cache_stride, a.cache_stride, nrows, a.geom);
+  }
+  if (st) set_status(status, st);
+}
+
 template <int VB>
 void launch_stage_rows(bool nt, int grid, hipStream_t stream, const int32_t* bucket,
                        const int64_t* owner_off, const KPart& kp, const KFeat& kf,
                        const StageArgs& a, char* cache, int32_t* slot_of, const char* src_cache,
-                       const int32_t* old_slot, int32_t* status) {
+                       const int32_t* old_slot, const StageStatsArgs& sa, int32_t* status) {
   if (nt)
     hipLaunchKernelGGL((k_stage_rows<VB, true>), dim3(grid), dim3(kBlock), 0, stream, bucket,
-                       owner_off, kp, kf, a, cache, slot_of, src_cache, old_slot, status);
+                       owner_off, kp, kf, a, cache, slot_of, src_cache, old_slot, sa, status);
   else
     hipLaunchKernelGGL((k_stage_rows<VB, false>), dim3(grid), dim3(kBlock), 0, stream, bucket,
-                       owner_off, kp, kf, a, cache, slot_of, src_cache, old_slot, status);
+                       owner_off, kp, kf, a, cache, slot_of, src_cache, old_slot, sa, status);
 }
 
 int stage_delta_blocks(int64_t cap) {
@@ -239,10 +266,14 @@ extern "C" int gg_stage_bulk(const int32_t* bucket_ids_d, const int64_t* owner_o
   int32_t* old_slot =
       (int32_t*)((char*)ws + align_up((size_t)gridd * (size_t)kp.P * sizeof(int32_t), 256));
   const int32_t* before = src_slot_of_d ? src_slot_of_d : slot_of_d;
+  // The remap is cleared in the same launch when the old slots are read
+  // from another remap; reading and clearing one remap need two launches.
+  const bool fuse_clear = clear_ids_d && before != slot_of_d;
   hipLaunchKernelGGL(k_stage_delta, dim3(gridd), dim3(kBlock), 0, stream, bucket_ids_d, owner_off_d,
-                     kp, a, before, old_slot, dcnt);
+                     kp, a, before, old_slot, dcnt, fuse_clear ? clear_ids_d : nullptr,
+                     clear_count_d, slot_of_d);
   GG_LAUNCH_CHECK("k_stage_delta");
-  if (clear_ids_d) {
+  if (clear_ids_d && !fuse_clear) {
     hipLaunchKernelGGL(k_slot_reset, dim3(2048), dim3(kBlock), 0, stream, clear_ids_d, clear_count_d,
                        kp.N, slot_of_d);
     GG_LAUNCH_CHECK("k_slot_reset");
@@ -255,16 +286,18 @@ extern "C" int gg_stage_bulk(const int32_t* bucket_ids_d, const int64_t* owner_o
   int64_t gmax = 16384;
   if (host_cap > 0 && host_shards(kf) > 0) gmax = host_cap;
   const int grid = (int)std::min<int64_t>(std::max<int64_t>(cdiv(ntiles, kBlock / kWave), 1), gmax);
+  StageStatsArgs sa;
+  sa.prev_count = clear_count_d;
+  sa.dcnt = dcnt;
+  sa.stats = stats_d;
+  sa.nblk_delta = gridd;
+  sa.has_src = src_cache_d ? 1 : 0;
   if (v16)
     launch_stage_rows<16>(nt, grid, stream, bucket_ids_d, owner_off_d, kp, kf, a, (char*)cache_d,
-                          slot_of_d, (const char*)src_cache_d, old_slot, status_d);
+                          slot_of_d, (const char*)src_cache_d, old_slot, sa, status_d);
   else
     launch_stage_rows<4>(nt, grid, stream, bucket_ids_d, owner_off_d, kp, kf, a, (char*)cache_d,
-                         slot_of_d, (const char*)src_cache_d, old_slot, status_d);
+                         slot_of_d, (const char*)src_cache_d, old_slot, sa, status_d);
   GG_LAUNCH_CHECK("k_stage_rows");
-  hipLaunchKernelGGL(k_stage_finish, dim3(1), dim3(kBlock), 0, stream, owner_off_d, kp, a,
-                     clear_count_d, kf.row_bytes, dcnt, gridd, src_cache_d ? 1 : 0, stats_d,
-                     status_d);
-  GG_LAUNCH_CHECK("k_stage_finish");
   return GG_OK;
 }
