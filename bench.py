@@ -121,6 +121,17 @@ def summarize(args):
                 if v:
                     out.append(f"{label:34s} launches {len(v):3d}  call avg {sum(v) / len(v) / 1e3:8.2f}"
                                f"  k_gather_rows avg {sum(r) / len(r) / 1e3:8.2f}")
+        if args.bench_json:
+            # the JSON line bench.py printed in the traced run: its HIP-event
+            # gather durations, to set beside rocprofv3's
+            with open(args.bench_json) as f:
+                b = json.loads(f.read().strip().splitlines()[-1])
+            r = b["roofline"]
+            out.append("")
+            out.append(f"# bench.py line of the traced run: ms_per_step {b['ms_per_step']}, "
+                       f"gg_gather_batch {r['avg_launch_us']} us per launch over the timed steps "
+                       f"(HIP events, frac {r['frac']}), {r['isolated']['avg_launch_us']} us "
+                       f"isolated (frac {r['isolated']['frac']})")
         with open(os.path.join(PROFILES, f"kernels_{wl}.txt"), "w") as f:
             f.write("\n".join(out) + "\n")
     if args.fetch_db and args.write_db:
@@ -198,6 +209,8 @@ def main():
     ap.add_argument("--fetch-db", default=None)
     ap.add_argument("--write-db", default=None)
     ap.add_argument("--summary-command", default="")
+    ap.add_argument("--bench-json", default=None,
+                    help="with --summarize: the JSON line bench.py printed in the traced run")
     ap.add_argument("--phases", default=None,
                     help="with --trace-db: gather launches of the pre-pass (two per window "
                          "with the look-ahead driver), warm-up and timed steps, e.g. 24,1,12, "
