@@ -3,7 +3,8 @@
 //
 // Grid (bx, nseg): blocks (., s) serve segment (batch) s, so every block's
 // statistics belong to one batch and reduce without atomics.  Each
-// wavefront takes 64 consecutive output rows at a time; every lane resolves
+// wavefront takes a tile of consecutive output rows at a time (64, fewer
+// for rows wider than 512 bytes); every lane of the tile resolves
 // its row (local shard, cache slot, or miss) and the wave copies the
 // resolved rows with the row copy engine.  Misses are appended to a queue in
 // the workspace (one atomic per wave that has any) and served afterwards
@@ -26,6 +27,8 @@ struct GatherArgs {
   int64_t out_stride;
   int32_t nseg;
   int32_t nstat;        // 2 + P counters per block
+  int32_t tile;         // rows per wave step (tile_rows)
+  int32_t pad_;
   CopyGeom geom;
 };
 
@@ -61,17 +64,17 @@ __global__ void __launch_bounds__(kBlock) k_gather_rows(const int32_t* in_ids, c
   seg_range(bounds, seg, a, &lo, &hi);
   const int64_t begin = bounds[0];
   const int lane = lane_id();
-  const int64_t ntiles = (hi - lo + kWave - 1) / kWave;
+  const int64_t ntiles = (hi - lo + a.tile - 1) / a.tile;
   int32_t st = 0;
   int32_t c_local = 0, c_hit = 0;
   for (int64_t t = (int64_t)blockIdx.x * kTilesPerBlock + threadIdx.x / kWave; t < ntiles;
        t += (int64_t)gridDim.x * kTilesPerBlock) {
-    const int64_t r0 = lo + t * kWave;
+    const int64_t r0 = lo + t * a.tile;
     const int64_t i = r0 + lane;
     const char* src = nullptr;
     bool miss = false, is_local = false, is_hit = false;
     int32_t u = -1, m = -1;
-    if (i < hi) {
+    if (lane < a.tile && i < hi) {
       u = in_ids[begin + i];
       if (u < 0 || (int64_t)u >= part.N) {
         st |= GG_DEV_BAD_ID;
@@ -120,7 +123,7 @@ __global__ void __launch_bounds__(kBlock) k_gather_rows(const int32_t* in_ids, c
       }
     }
     const int64_t left = hi - r0;
-    const int nrows = left < kWave ? (int)left : kWave;
+    const int nrows = left < a.tile ? (int)left : a.tile;
     wave_copy_rows<VB, NT, U>(src, out + r0 * a.out_stride, a.out_stride, nrows, a.geom);
   }
   if (lane == 0) {
@@ -303,6 +306,8 @@ extern "C" int gg_gather_batch(const int32_t* in_ids_d, const int64_t* bounds_d,
   a.out_stride = out_stride;
   a.nseg = nseg;
   a.nstat = 2 + kp.P;
+  a.tile = tile_rows(kf.row_bytes);
+  a.pad_ = 0;
   a.geom = copy_geom(kf.row_bytes, v16 ? 16 : 4);
   const int32_t bx = blocks_per_seg(n_cap, nseg);
   static const bool nt = env_flag("GG_NT_GATHER", true);

@@ -45,6 +45,15 @@ int pack_feat(const gg_feat_t* feat, const gg_part_t* part, KFeat* out);
 // Geometry of the row copy for row_bytes and the vector width vb (16 or 4).
 CopyGeom copy_geom(int32_t row_bytes, int vb);
 
+// Rows a wavefront takes per step of a row copy: 64 for rows up to 512
+// bytes, fewer for wider rows so that a window's rows still spread over
+// every wave of the grid (the largest power of two <= 32 KB / row_bytes).
+inline int32_t tile_rows(int32_t row_bytes) {
+  int32_t t = 64;
+  while (t > 1 && (int64_t)t * row_bytes > 32768) t >>= 1;
+  return t;
+}
+
 inline bool aligned16(const void* p) { return ((uintptr_t)p & 15u) == 0; }
 
 // Tuning switches read once from the environment: a flag is on unless "0".

@@ -18,6 +18,8 @@ struct StageArgs {
   int64_t cap;         // bucket entries usable
   int64_t cache_rows;
   int64_t cache_stride;
+  int32_t tile;        // slots per wave step (tile_rows)
+  int32_t pad_;
   CopyGeom geom;
 };
 
@@ -160,15 +162,15 @@ __global__ void __launch_bounds__(kBlock) k_stage_rows(const int32_t* bucket, co
   for (int t = threadIdx.x; t <= GG_MAX_PARTS; t += blockDim.x) s_start[t] = part.start[t];
   __syncthreads();
   const int64_t n = stage_n(owner_off, part.P, a);
-  const int64_t ntiles = (n + kWave - 1) / kWave;
+  const int64_t ntiles = (n + a.tile - 1) / a.tile;
   const int lane = lane_id();
   int32_t st = 0;
   for (int64_t tile = (int64_t)blockIdx.x * (kBlock / kWave) + threadIdx.x / kWave; tile < ntiles;
        tile += (int64_t)gridDim.x * (kBlock / kWave)) {
-    const int64_t s0 = tile * kWave;
+    const int64_t s0 = tile * a.tile;
     const int64_t s = s0 + lane;
     const char* src = nullptr;
-    if (s < n) {
+    if (lane < a.tile && s < n) {
       const int32_t u = bucket[s];
       if (u < 0 || (int64_t)u >= part.N) {
         st |= GG_DEV_BAD_ID;
@@ -190,7 +192,7 @@ __global__ void __launch_bounds__(kBlock) k_stage_rows(const int32_t* bucket, co
         }
       }
     }
-    const int nrows = (int)((n - s0) < kWave ? (n - s0) : kWave);
+    const int nrows = (int)((n - s0) < a.tile ? (n - s0) : a.tile);
     wave_copy_rows<VB, NT>(src, cache + s0 * a.cache_stride, a.cache_stride, nrows, a.geom);
   }
   if (st) set_status(status, st);
@@ -256,6 +258,8 @@ extern "C" int gg_stage_bulk(const int32_t* bucket_ids_d, const int64_t* owner_o
   a.cap = cap;
   a.cache_rows = cache_rows;
   a.cache_stride = cache_stride;
+  a.tile = tile_rows(kf.row_bytes);
+  a.pad_ = 0;
   a.geom = copy_geom(kf.row_bytes, v16 ? 16 : 4);
   static const bool nt = env_flag("GG_NT_STAGE", false);
 
@@ -278,7 +282,7 @@ extern "C" int gg_stage_bulk(const int32_t* bucket_ids_d, const int64_t* owner_o
                        kp.N, slot_of_d);
     GG_LAUNCH_CHECK("k_slot_reset");
   }
-  const int64_t ntiles = cdiv(std::min(cap, cache_rows), kWave);
+  const int64_t ntiles = cdiv(std::min(cap, cache_rows), a.tile);
   // Rows read over PCIe need few waves in flight to keep the link busy; a
   // full grid would hold every CU while it waits and starve kernels on
   // other streams (the next window's sampling), so cap it then.
