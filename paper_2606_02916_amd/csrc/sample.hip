@@ -4,8 +4,9 @@
 // starts as the batch's seeds; hop l samples the neighbours of every node of
 // the current frontier F_l and ORs them in, so the set becomes F_{l+1} =
 // F_l plus the sampled neighbours.  After each hop the sets are compacted
-// into ascending id lists: a per-chunk popcount, one device-wide exclusive
-// scan, and an emit pass.  Deduplication therefore costs one streaming pass
+// into ascending id lists in two launches: a per-chunk popcount (with
+// per-batch totals), then an emit pass in which every block finds its own
+// place from those counts.  Deduplication therefore costs streaming passes
 // over N/8 bytes per batch and hop instead of a sort of the sampled ids.
 #include <limits.h>
 
@@ -23,6 +24,15 @@ struct LevelArgs {
   int32_t nch;
   int32_t pad_;
   int64_t fcap, ncap;
+};
+
+// Raw (unclamped) running ends of the window's frontier and neighbour
+// lists, one slot per level, so a level reads its predecessor's while it
+// writes its own.
+struct LevelState {
+  int64_t fend[GG_MAX_LAYERS + 1];   // frontier entries up to and including level l
+  int64_t nend[GG_MAX_LAYERS + 1];   // neighbour slots up to and including level l
+  int64_t nbase[GG_MAX_LAYERS + 1];  // first neighbour slot of level l
 };
 
 struct SampleArgs {
@@ -43,7 +53,11 @@ __device__ __forceinline__ int find_batch(const int64_t* off, int64_t x) {
   return idx;
 }
 
-__global__ void __launch_bounds__(kBlock) k_zero_words(uint32_t* p, int64_t n4) {
+// Zeroes the window's bit sets and the per-level batch totals.
+__global__ void __launch_bounds__(kBlock) k_zero_words(uint32_t* p, int64_t n4, int32_t* btot,
+                                                       int32_t nbtot) {
+  if (blockIdx.x == 0)
+    for (int t = threadIdx.x; t < nbtot; t += blockDim.x) btot[t] = 0;
   u32x4* q = (u32x4*)p;
   const u32x4 z = {0u, 0u, 0u, 0u};
   for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n4;
@@ -67,9 +81,12 @@ __global__ void __launch_bounds__(kBlock) k_mark_seeds(const int32_t* seeds, See
   }
 }
 
-// Popcount of one chunk (kChunkWords words) of one batch's bit set.
+// Popcount of one chunk (kChunkWords words) of one batch's bit set; the
+// chunk's count goes to cnt and is added to one of the batch's kTotLanes
+// partial totals (spread so that few blocks add to one word).
+constexpr int kTotLanes = 8;
 __global__ void __launch_bounds__(kBlock) k_bits_count(const uint32_t* bits, int64_t wpb,
-                                                       int32_t* cnt) {
+                                                       int32_t* cnt, int32_t* btot) {
   __shared__ int32_t lds[kBlock / kWave];
   const int c = blockIdx.x, b = blockIdx.y, nch = gridDim.x;
   const u32x4* p = (const u32x4*)(bits + (int64_t)b * wpb + (int64_t)c * kChunkWords +
@@ -80,82 +97,101 @@ __global__ void __launch_bounds__(kBlock) k_bits_count(const uint32_t* bits, int
   s = wave_sum(s);
   if (lane_id() == 0) lds[threadIdx.x / kWave] = s;
   __syncthreads();
-  if (threadIdx.x == 0) cnt[(int64_t)b * nch + c] = lds[0] + lds[1] + lds[2] + lds[3];
-}
-
-// One block of 1024 threads: scans the chunk counts of level lv and writes
-// the level's frontier and neighbour offsets (clamped to the capacities).
-// lvl[0] = raw frontier end, lvl[1] = raw neighbour end, lvl[2+l] = raw
-// neighbour base of level l.
-__global__ void __launch_bounds__(1024) k_level_scan(const int32_t* cnt, int64_t* chunk_off,
-                                                     int64_t* frontier_off, int64_t* nbr_off,
-                                                     int64_t* lvl, int64_t* need, int32_t* status,
-                                                     LevelArgs a) {
-  __shared__ int64_t lds[16];
-  __shared__ int64_t s_base[2];
   if (threadIdx.x == 0) {
-    s_base[0] = a.lv == 0 ? 0 : lvl[0];
-    s_base[1] = a.lv == 0 ? 0 : lvl[1];
-  }
-  __syncthreads();
-  const int64_t raw_base = s_base[0];
-  const int64_t raw_nbase = s_base[1];
-  const int64_t n = (int64_t)a.W * a.nch;
-  const int64_t total = block_scan_large(cnt, chunk_off, n, raw_base, lds);
-  __syncthreads();
-  const int64_t raw_end = raw_base + total;
-  const int64_t cb = raw_base < a.fcap ? raw_base : a.fcap;
-  const int64_t ce = raw_end < a.fcap ? raw_end : a.fcap;
-  const int t = threadIdx.x;
-  if (t < a.W) {
-    int64_t v = chunk_off[(int64_t)t * a.nch];
-    v = v < a.fcap ? v : a.fcap;
-    frontier_off[(int64_t)a.lv * a.W + t] = v;
-    if (a.lv < a.L) {
-      int64_t nv = raw_nbase + (v - cb) * a.k;
-      nbr_off[(int64_t)a.lv * a.W + t] = nv < a.ncap ? nv : a.ncap;
-    }
-  }
-  if (t == 0) {
-    frontier_off[(int64_t)(a.lv + 1) * a.W] = ce;
-    lvl[0] = raw_end;
-    need[0] = raw_end;
-    int32_t st = raw_end > a.fcap ? GG_DEV_CAPACITY : 0;
-    if (a.lv < a.L) {
-      const int64_t nend = raw_nbase + (ce - cb) * a.k;
-      nbr_off[(int64_t)(a.lv + 1) * a.W] = nend < a.ncap ? nend : a.ncap;
-      lvl[2 + a.lv] = raw_nbase;
-      lvl[1] = nend;
-      need[1] = nend;
-      if (nend > a.ncap) st |= GG_DEV_CAPACITY;
-    }
-    if (st) set_status(status, st);
+    const int32_t n = lds[0] + lds[1] + lds[2] + lds[3];
+    cnt[(int64_t)b * nch + c] = n;
+    if (n) atomicAdd(btot + b * kTotLanes + (c & (kTotLanes - 1)), n);
   }
 }
 
-// Writes the ids of one chunk of one batch's bit set, ascending.
+// Sums of three values over the block.
+__device__ __forceinline__ void block_sum3(int64_t (&v)[3], int64_t (*lds)[3]) {
+  const int w = threadIdx.x / kWave;
+#pragma unroll
+  for (int j = 0; j < 3; ++j) v[j] = wave_sum(v[j]);
+  if (lane_id() == 0)
+#pragma unroll
+    for (int j = 0; j < 3; ++j) lds[w][j] = v[j];
+  __syncthreads();
+#pragma unroll
+  for (int j = 0; j < 3; ++j) {
+    int64_t t = 0;
+    for (int q = 0; q < kBlock / kWave; ++q) t += lds[q][j];
+    v[j] = t;
+  }
+  __syncthreads();
+}
+
+// Writes the ids of one chunk of one batch's bit set, ascending, at its
+// place in the level's list.  The place comes from the counts of the
+// previous launch: the totals of the batches before b plus the counts of
+// the chunks before c, summed by the block itself (no separate scan
+// launch).  Block (0, b) writes batch b's frontier and neighbour offsets;
+// block (0, 0) also the level's ends and capacity checks.
 __global__ void __launch_bounds__(kBlock) k_bits_emit(const uint32_t* bits, int64_t wpb,
-                                                      const int64_t* chunk_off, int32_t* ids,
-                                                      int64_t fcap) {
+                                                      const int32_t* cnt, const int32_t* btot,
+                                                      int32_t* ids, int64_t* frontier_off,
+                                                      int64_t* nbr_off, LevelState* ls,
+                                                      int64_t* need, int32_t* status,
+                                                      LevelArgs a) {
+  __shared__ int64_t lds3[kBlock / kWave][3];
   __shared__ int32_t lds[kBlock / kWave];
+  __shared__ int64_t s_off;
   const int c = blockIdx.x, b = blockIdx.y, nch = gridDim.x;
   const int64_t w0 = (int64_t)c * kChunkWords + threadIdx.x * kWordsPerThread;
   const u32x4* p = (const u32x4*)(bits + (int64_t)b * wpb + w0);
-  const u32x4 x = p[0], y = p[1];
+  const u32x4 x = p[0], y = p[1];      // in flight while the offsets are summed
+  const int64_t raw_base = a.lv == 0 ? 0 : ls->fend[a.lv - 1];
+  const int64_t raw_nbase = a.lv == 0 ? 0 : ls->nend[a.lv - 1];
+  int64_t v[3] = {0, 0, 0};  // batches before b, all batches, chunks before c
+  for (int t = threadIdx.x; t < a.W * kTotLanes; t += kBlock) {
+    const int64_t x = btot[t];
+    v[1] += x;
+    if (t < b * kTotLanes) v[0] += x;
+  }
+  for (int t = threadIdx.x; t < c; t += kBlock) v[2] += cnt[(int64_t)b * nch + t];
+  block_sum3(v, lds3);
+  const int64_t cb = raw_base < a.fcap ? raw_base : a.fcap;
+  if (threadIdx.x == 0) {
+    s_off = raw_base + v[0] + v[2];
+    if (c == 0) {
+      int64_t fo = raw_base + v[0];
+      fo = fo < a.fcap ? fo : a.fcap;
+      frontier_off[(int64_t)a.lv * a.W + b] = fo;
+      if (a.lv < a.L) {
+        const int64_t nv = raw_nbase + (fo - cb) * a.k;
+        nbr_off[(int64_t)a.lv * a.W + b] = nv < a.ncap ? nv : a.ncap;
+      }
+      if (b == 0) {
+        const int64_t raw_end = raw_base + v[1];
+        const int64_t ce = raw_end < a.fcap ? raw_end : a.fcap;
+        frontier_off[(int64_t)(a.lv + 1) * a.W] = ce;
+        ls->fend[a.lv] = raw_end;
+        need[0] = raw_end;
+        int32_t st = raw_end > a.fcap ? GG_DEV_CAPACITY : 0;
+        if (a.lv < a.L) {
+          const int64_t nend = raw_nbase + (ce - cb) * a.k;
+          nbr_off[(int64_t)(a.lv + 1) * a.W] = nend < a.ncap ? nend : a.ncap;
+          ls->nbase[a.lv] = raw_nbase;
+          ls->nend[a.lv] = nend;
+          need[1] = nend;
+          if (nend > a.ncap) st |= GG_DEV_CAPACITY;
+        }
+        if (st) set_status(status, st);
+      }
+    }
+  }
+  __syncthreads();
   const uint32_t w[8] = {x.x, x.y, x.z, x.w, y.x, y.y, y.z, y.w};
   int n = 0;
 #pragma unroll
   for (int j = 0; j < 8; ++j) n += __popc(w[j]);
   int32_t tot;
-  const int32_t ex = block_excl_scan<kBlock>(n, lds, &tot);
-  int64_t pos = chunk_off[(int64_t)b * nch + c] + ex;
+  int64_t pos = s_off + block_excl_scan<kBlock>(n, lds, &tot);
 #pragma unroll
   for (int j = 0; j < 8; ++j) {
-    uint32_t m = w[j];
-    while (m) {
-      const int bit = __ffs(m) - 1;
-      m &= m - 1;
-      if (pos < fcap) ids[pos] = (int32_t)((w0 + j) * 32 + bit);
+    for (uint32_t m = w[j]; m; m &= m - 1u) {
+      if (pos < a.fcap) ids[pos] = (int32_t)((w0 + j) * 32 + (__ffs(m) - 1));
       ++pos;
     }
   }
@@ -259,13 +295,13 @@ __device__ __forceinline__ void sample_one(const RowT* row_ptr, const int32_t* c
 template <typename RowT, int KMAX>
 __global__ void __launch_bounds__(kBlock) k_sample(const RowT* row_ptr, const int32_t* col_idx,
                                                    const int32_t* fids, const int64_t* frontier_off,
-                                                   const int64_t* lvl, int32_t* nbr, uint32_t* bits,
+                                                   const LevelState* ls, int32_t* nbr, uint32_t* bits,
                                                    int32_t* status, SampleArgs a) {
   __shared__ int64_t so[GG_MAX_W + 1];
   __shared__ int64_t s_nbase;
   for (int t = threadIdx.x; t <= GG_MAX_W; t += blockDim.x)
     so[t] = t <= a.W ? frontier_off[(int64_t)a.l * a.W + t] : INT64_MAX;
-  if (threadIdx.x == 0) s_nbase = lvl[2 + a.l];
+  if (threadIdx.x == 0) s_nbase = ls->nbase[a.l];
   __syncthreads();
   const int64_t begin = so[0], end = so[a.W];
   const int64_t nbase = s_nbase;
@@ -278,9 +314,9 @@ __global__ void __launch_bounds__(kBlock) k_sample(const RowT* row_ptr, const in
 }
 
 struct SampleWs {
-  int32_t* cnt;
-  int64_t* chunk_off;
-  int64_t* lvl;
+  int32_t* cnt;       // per (batch, chunk) counts of the current level
+  int32_t* btot;      // per (level, batch) totals, zeroed by k_zero_words
+  LevelState* lvl;
 };
 
 size_t sample_ws_layout(int64_t num_nodes, int32_t W, char* base, SampleWs* out) {
@@ -288,8 +324,8 @@ size_t sample_ws_layout(int64_t num_nodes, int32_t W, char* base, SampleWs* out)
   Carve cv{base, 0, ~(size_t)0};
   SampleWs s;
   s.cnt = cv.take<int32_t>((size_t)(W * nch));
-  s.chunk_off = cv.take<int64_t>((size_t)(W * nch));
-  s.lvl = cv.take<int64_t>(2 + GG_MAX_LAYERS);
+  s.btot = cv.take<int32_t>((size_t)(GG_MAX_LAYERS + 1) * GG_MAX_W * kTotLanes);
+  s.lvl = cv.take<LevelState>(1);
   if (out) *out = s;
   return align_up(cv.used, 256);
 }
@@ -359,7 +395,8 @@ extern "C" int gg_sample_window(const gg_csr_t* csr, const int32_t* seeds_d,
   const int32_t nch = (int32_t)(wpb / kChunkWords);
 
   hipLaunchKernelGGL(k_zero_words, dim3((unsigned)std::min<int64_t>(cdiv(W * wpb / 4, kBlock), 4096)),
-                     dim3(kBlock), 0, stream, out->frontier_bits, W * wpb / 4);
+                     dim3(kBlock), 0, stream, out->frontier_bits, W * wpb / 4, sw.btot,
+                     (L + 1) * GG_MAX_W * kTotLanes);
   GG_LAUNCH_CHECK("k_zero_words");
   SeedOff so;
   for (int b = 0; b <= GG_MAX_W; ++b) so.off[b] = b <= W ? seed_off_h[b] : INT64_MAX;
@@ -399,8 +436,9 @@ extern "C" int gg_sample_window(const gg_csr_t* csr, const int32_t* seeds_d,
                    : launch_sample<int32_t>(csr, out, sw, status_d, a, bnd, stream);
       if (rc != GG_OK) return rc;
     }
+    int32_t* btot = sw.btot + (int64_t)lv * GG_MAX_W * kTotLanes;
     hipLaunchKernelGGL(k_bits_count, dim3(nch, W), dim3(kBlock), 0, stream, out->frontier_bits, wpb,
-                       sw.cnt);
+                       sw.cnt, btot);
     GG_LAUNCH_CHECK("k_bits_count");
     LevelArgs la;
     la.lv = lv;
@@ -411,11 +449,9 @@ extern "C" int gg_sample_window(const gg_csr_t* csr, const int32_t* seeds_d,
     la.pad_ = 0;
     la.fcap = out->frontier_cap;
     la.ncap = out->nbr_cap;
-    hipLaunchKernelGGL(k_level_scan, dim3(1), dim3(1024), 0, stream, sw.cnt, sw.chunk_off,
-                       out->frontier_off, out->nbr_off, sw.lvl, out->need, status_d, la);
-    GG_LAUNCH_CHECK("k_level_scan");
     hipLaunchKernelGGL(k_bits_emit, dim3(nch, W), dim3(kBlock), 0, stream, out->frontier_bits, wpb,
-                       sw.chunk_off, out->frontier_ids, out->frontier_cap);
+                       sw.cnt, btot, out->frontier_ids, out->frontier_off, out->nbr_off, sw.lvl,
+                       out->need, status_d, la);
     GG_LAUNCH_CHECK("k_bits_emit");
   }
   return GG_OK;
