@@ -357,16 +357,11 @@ def main():
 
     def gather_ms(gevs, i, b=None):
         """Duration of gather launch b of step i (all launches when b is
-        None).  The look-ahead driver's start event marks the end of
-        staging; its gather begins at the later of that and the previous
-        gather's end on the same stream."""
+        None), between HIP events on the stream the gather runs on."""
         if b is None:
             return sum(gather_ms(gevs, i, j) for j in range(len(gevs[i])))
         s, e = gevs[i][b]
-        t = s.elapsed_time(e)
-        if look and i > 0:
-            t = min(t, gevs[i - 1][-1][1].elapsed_time(e))
-        return t
+        return s.elapsed_time(e)
 
     g_ms, g_bytes, n_launch = 0.0, 0, 0
     stage_ms = {"sample": [], "hotset": [], "bucket": [], "stage": [], "gathers": []}
@@ -375,11 +370,11 @@ def main():
         e = evs[i]
         for name, (a, b) in zip(stage_ms, [(0, 1), (1, 2), (2, 3)]):
             stage_ms[name].append(e[a].elapsed_time(e[b]))
-        # staging starts once its window is built and the previous window's
-        # staging (same stream) has ended
+        # staging starts once its window is built and, under the look-ahead,
+        # the previous window's gather (same stream) has ended
         t_st = e[3].elapsed_time(e[4])
         if look and i > 0:
-            t_st = min(t_st, evs[i - 1][4].elapsed_time(e[4]))
+            t_st = min(t_st, gevs[i - 1][-1][1].elapsed_time(e[4]))
         stage_ms["stage"].append(t_st)
         stage_ms["gathers"].append(gather_ms(gevs, i))
         st_ms += t_st

@@ -12,8 +12,8 @@ it keeps two caches and requests only the rebuild delta
 Delta_{k,m} = (H_k in owner m) minus C_{k-1} from the owners, copying the
 rows it retains from the previous cache (Sec. IV-A, Eq. (1)).
 LookaheadPipeline is the paper's pipelined runtime (Algorithm 1, Sec.
-IV-C): window k+1 is sampled, bucketed and delta-staged on one stream while
-window k is gathered on another.
+IV-C): window k+1 is sampled and bucketed on one stream while window k is
+delta-staged and gathered on another.
 """
 from __future__ import annotations
 
@@ -283,12 +283,14 @@ class FetchPipeline:
 
 
 class LookaheadPipeline:
-    """Pipelined runtime in three stages on three streams: the build stream
-    samples window k and forms its hot set and owner buckets, the stage
-    stream rebuilds the cache (delta staging from window k-1's cache), the
-    gather stream gathers the window.  Window k+1 is built while window k
-    is staged, and window k is gathered while window k+1 is staged, so a
-    window costs about the longest stage instead of the sum.
+    """Pipelined runtime on two streams: the build stream samples window k
+    and forms its hot set and owner buckets; the fetch stream rebuilds the
+    cache (delta staging from window k-1's cache) and then gathers the
+    window.  Window k+1 is built while window k is staged and gathered, so a
+    window costs about the longer of the two streams' work instead of the
+    sum.  (Staging and gathering on separate streams gained nothing: both
+    are bound by HBM bandwidth, and every cross-stream wait costs a few
+    microseconds in the queues.)
 
     `nsets` buffer sets rotate over the windows (window k uses set
     k mod nsets).  Building window k waits for the gather of window
@@ -331,34 +333,31 @@ class LookaheadPipeline:
                           for _ in range(self.NSLOT)]
         self.status = torch.zeros(1, dtype=torch.int32, device=dev)
         self.build_stream = torch.cuda.Stream(device=dev)
-        self.stage_stream = torch.cuda.Stream(device=dev)
-        self.gather_stream = torch.cuda.Stream(device=dev)
+        self.fetch_stream = torch.cuda.Stream(device=dev)
         self.built = [torch.cuda.Event() for _ in range(self.nsets)]
-        self.staged = [torch.cuda.Event() for _ in range(self.nsets)]
         self.gathered = [torch.cuda.Event() for _ in range(self.nsets)]
         self.k = 0
 
     def window(self, seeds, seed_off, batch0, epoch=0, rng_seed=0, out=None, events=None,
                gather_events=None, sim=None, consumer=None, consumer_events=None):
         """Enqueues window k; returns (number of batches, buffer set).  The
-        window's rows land in the set's win_out (or `out`) on the gather
+        window's rows land in the set's win_out (or `out`) on the fetch
         stream; wait on gathered_event(k) before reading them.  Inputs
         uploaded on the caller's stream are visible to the build stream.
         events: optional 5 torch events, four recorded on the build stream
-        around its three calls and one after staging on the stage stream
-        (the stage time is events[4] minus the later of events[3] and the
-        previous window's staging end); gather_events: optional (start, end)
-        pair, the start recorded on the stage stream when staging ends and
-        the end on the gather stream after the gather; sim: optional
+        around its three calls and one after staging on the fetch stream
+        (staging starts at the later of events[3] and the end of the
+        previous window's gather); gather_events: optional (start, end)
+        pair around the gather on the fetch stream; sim: optional
         (coeffs, acc) to add the window to simulator totals; consumer:
-        optional SageConsumer run on the gather stream after the gather
+        optional SageConsumer run on the fetch stream after the gather
         (so it overlaps the next window's build), bracketed by the optional
         event pair consumer_events."""
         k, g = self.k, self.geo
         X, T = k % self.nsets, k % self.NSLOT
         cur, prev = self.sets[X], self.sets[(k - 1) % self.nsets]
         Wk = len(seed_off) - 1
-        bs, ss, gs = self.build_stream, self.stage_stream, self.gather_stream
+        bs, fs = self.build_stream, self.fetch_stream
         ev = events if events is not None else [None] * 5
         bs.wait_stream(torch.cuda.current_stream(self.device))
         if k >= self.nsets:
@@ -377,7 +376,7 @@ class LookaheadPipeline:
                               flags=_bucket_flags(self.part))
         _rec(ev[3], bs)
         self.built[X].record(bs)
-        ss.wait_event(self.built[X])
+        fs.wait_event(self.built[X])
         C = (k - self.nsets) % self.NSLOT
         clear_ids = self.bucket_ids[C] if k >= self.nsets else None
         clear_cnt = self.hot_count[C] if k >= self.nsets else None
@@ -386,32 +385,26 @@ class LookaheadPipeline:
                          cur.cache, self.cache_stride, g.hot_cap, cur.slot_of, clear_ids,
                          clear_cnt, src.cache if src else None, src.slot_of if src else None,
                          cur.stage_stats, self.status, self.stage_ws,
-                         stream=ss.cuda_stream)
-        _rec(ev[4], ss)
+                         stream=fs.cuda_stream)
+        _rec(ev[4], fs)
         if gather_events is not None:
-            # A timing event recorded on the gather stream right behind its
-            # cross-stream wait can take its timestamp before the wait ends,
-            # so the start is taken where staging ends; the gather begins
-            # at the later of this and the previous gather's end.
-            gather_events[0].record(ss)
-        self.staged[X].record(ss)
-        gs.wait_event(self.staged[X])
+            gather_events[0].record(fs)
         o = cur.win_out if out is None else out
         bounds = cur.frontier_off.data_ptr() + 8 * (self.L * Wk)
         gg.gg_gather_batch(cur.frontier_ids, bounds, Wk, o.shape[0], self.part, self.feat,
                            cur.cache, self.cache_stride, g.hot_cap, cur.slot_of, o, self.stride,
                            cur.gather_stats.data_ptr(), self.status, self.gather_ws,
-                           stream=gs.cuda_stream)
+                           stream=fs.cuda_stream)
         if gather_events is not None:
-            gather_events[1].record(gs)
-        if sim is not None:           # simulator totals, in window order on the gather stream
+            gather_events[1].record(fs)
+        if sim is not None:           # simulator totals, in window order on the fetch stream
             gg.gg_sim_accumulate(cur.stage_stats, cur.gather_stats.data_ptr(), Wk, self.part,
-                                 sim[0], sim[1], stream=gs.cuda_stream)
+                                 sim[0], sim[1], stream=fs.cuda_stream)
         if consumer is not None:      # reads the set's sampling outputs and rows
-            _rec(consumer_events[0] if consumer_events else None, gs)
-            consumer.forward(cur, Wk, o, self.stride, self.status, stream=gs.cuda_stream)
-            _rec(consumer_events[1] if consumer_events else None, gs)
-        self.gathered[X].record(gs)
+            _rec(consumer_events[0] if consumer_events else None, fs)
+            consumer.forward(cur, Wk, o, self.stride, self.status, stream=fs.cuda_stream)
+            _rec(consumer_events[1] if consumer_events else None, fs)
+        self.gathered[X].record(fs)
         self.k += 1
         return Wk, cur
 
@@ -431,7 +424,7 @@ class LookaheadPipeline:
         return self.gathered[k % self.nsets]
 
     def synchronize(self):
-        for s in (self.build_stream, self.stage_stream, self.gather_stream):
+        for s in (self.build_stream, self.fetch_stream):
             s.synchronize()
 
     def read_status(self):

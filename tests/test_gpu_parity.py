@@ -360,7 +360,7 @@ def test_delta_staging_matches_oracle(name, n_hot, W):
                                                 ("tiny", -1, 1, 2), ("small", -1, None, 3),
                                                 ("tiny", 2000, 1, 3)])
 def test_lookahead_pipeline_equals_sequential(name, n_hot, W, nsets):
-    log(f"{name}: three-stream look-ahead pipeline vs sequential delta windows, n_hot={n_hot}, "
+    log(f"{name}: two-stream look-ahead pipeline vs sequential delta windows, n_hot={n_hot}, "
         f"W={W}, nsets={nsets}")
     import torch as T
     from paper_2606_02916_amd import LookaheadPipeline
