@@ -6,9 +6,12 @@
 // wavefront takes a tile of consecutive output rows at a time (64, fewer
 // for rows wider than 512 bytes); every lane of the tile resolves
 // its row (local shard, cache slot, or miss) and the wave copies the
-// resolved rows with the row copy engine.  Misses are appended to a queue in
-// the workspace (one atomic per wave that has any) and served afterwards
-// from the owners' shards, straight into their output rows.
+// resolved rows with the row copy engine.  Misses are only counted, per
+// block and owner.  A second launch serves them: one block per row block
+// of the first launch, which returns at once when that block counted no
+// miss and otherwise walks the same tiles again and copies the missed rows
+// from their owners' shards straight into their output rows.  No queue and
+// no counter need clearing between calls.
 #include <stdlib.h>
 #include <string.h>
 
@@ -43,17 +46,12 @@ __device__ __forceinline__ void seg_range(const int64_t* bounds, int s, const Ga
   *hi = h;
 }
 
-__global__ void k_gather_zero(int64_t* miss_count) {
-  if (threadIdx.x == 0) miss_count[0] = 0;
-}
-
 template <int VB, bool NT, int U>
 __global__ void __launch_bounds__(kBlock) k_gather_rows(const int32_t* in_ids, const int64_t* bounds,
                                                         KPart part, KFeat feat, GatherArgs a,
                                                         const char* cache, const int32_t* slot_of,
                                                         char* out, int32_t* blk_stat,
-                                                        int64_t* miss_count, int32_t* miss_pos,
-                                                        int32_t* miss_id, int32_t* status) {
+                                                        int32_t* status) {
   __shared__ int64_t s_start[GG_MAX_PARTS + 1];
   __shared__ int32_t s_cnt[2 + GG_MAX_PARTS];  // local, hits, misses per owner
   for (int t = threadIdx.x; t <= GG_MAX_PARTS; t += blockDim.x) s_start[t] = part.start[t];
@@ -103,24 +101,13 @@ __global__ void __launch_bounds__(kBlock) k_gather_rows(const int32_t* in_ids, c
     const uint64_t ml = __ballot(is_local), mh = __ballot(is_hit), mm = __ballot(miss);
     c_local += (int32_t)__popcll(ml);
     c_hit += (int32_t)__popcll(mh);
-    if (mm) {
-      // Per-owner miss counts (one ballot per owner present) and the queue.
-      for (uint64_t act = mm; act;) {
-        const int leader = __ffsll((unsigned long long)act) - 1;
-        const int32_t ol = __shfl(m, leader, kWave);
-        const uint64_t sel = __ballot(miss && m == ol);
-        if (lane == leader) atomicAdd(&s_cnt[2 + ol], (int32_t)__popcll(sel));
-        act &= ~sel;
-      }
-      int64_t q0 = 0;
-      if (lane == 0) q0 = (int64_t)atomicAdd((unsigned long long*)miss_count,
-                                             (unsigned long long)__popcll(mm));
-      q0 = __shfl(q0, 0, kWave);
-      if (miss) {
-        const int64_t q = q0 + lanes_below(mm);
-        miss_pos[q] = (int32_t)i;
-        miss_id[q] = u;
-      }
+    // Per-owner miss counts: one ballot per owner present.
+    for (uint64_t act = mm; act;) {
+      const int leader = __ffsll((unsigned long long)act) - 1;
+      const int32_t ol = __shfl(m, leader, kWave);
+      const uint64_t sel = __ballot(miss && m == ol);
+      if (lane == leader) atomicAdd(&s_cnt[2 + ol], (int32_t)__popcll(sel));
+      act &= ~sel;
     }
     const int64_t left = hi - r0;
     const int nrows = left < a.tile ? (int)left : a.tile;
@@ -136,15 +123,13 @@ __global__ void __launch_bounds__(kBlock) k_gather_rows(const int32_t* in_ids, c
   for (int t = threadIdx.x; t < a.nstat; t += blockDim.x) dst[t] = s_cnt[t];
 }
 
-// Blocks 0 .. nseg-1: statistics of batch s.  The remaining blocks serve
-// the queued misses from the owners' shards.
+// Blocks 0 .. nseg-1: statistics of batch s.  Block nseg + s * bx + x
+// serves the misses of row block (x, s) of k_gather_rows, if it had any.
 template <int VB, bool NT>
-__global__ void __launch_bounds__(kBlock) k_gather_finish(const int64_t* bounds, KPart part, KFeat feat,
-                                                          GatherArgs a, int32_t bx,
-                                                          const int32_t* blk_stat,
-                                                          const int64_t* miss_count,
-                                                          const int32_t* miss_pos,
-                                                          const int32_t* miss_id, char* out,
+__global__ void __launch_bounds__(kBlock) k_gather_finish(const int32_t* in_ids, const int64_t* bounds,
+                                                          KPart part, KFeat feat, GatherArgs a,
+                                                          int32_t bx, const int32_t* blk_stat,
+                                                          const int32_t* slot_of, char* out,
                                                           gg_gather_stats_t* stats,
                                                           int32_t* status) {
   const int P = part.P;
@@ -180,40 +165,54 @@ __global__ void __launch_bounds__(kBlock) k_gather_finish(const int64_t* bounds,
     }
     return;
   }
+  const int64_t rb = blockIdx.x - a.nseg;    // row block (x, seg) of k_gather_rows
+  const int seg = (int)(rb / bx), x = (int)(rb % bx);
+  const int32_t* bs = blk_stat + rb * a.nstat;
+  int32_t nmiss = 0;
+  for (int m = 0; m < P; ++m) nmiss += bs[2 + m];
+  if (nmiss == 0) return;
   __shared__ int64_t s_start[GG_MAX_PARTS + 1];
   for (int t = threadIdx.x; t <= GG_MAX_PARTS; t += blockDim.x) s_start[t] = part.start[t];
   __syncthreads();
-  const int64_t nm = miss_count[0];
-  const int64_t mb = blockIdx.x - a.nseg, nmb = gridDim.x - a.nseg;
+  int64_t lo, hi;
+  seg_range(bounds, seg, a, &lo, &hi);
+  const int64_t begin = bounds[0];
   const int lane = lane_id();
+  const int64_t ntiles = (hi - lo + a.tile - 1) / a.tile;
   int32_t st = 0;
-  for (int64_t j0 = (mb * kTilesPerBlock + threadIdx.x / kWave) * kWave; j0 < nm;
-       j0 += nmb * kBlock) {
-    const int64_t j = j0 + lane;
+  // The tiles k_gather_rows gave this row block, in the same order.
+  for (int64_t t = (int64_t)x * kTilesPerBlock + threadIdx.x / kWave; t < ntiles;
+       t += (int64_t)bx * kTilesPerBlock) {
+    const int64_t r0 = lo + t * a.tile;
+    const int64_t i = r0 + lane;
     const char* src = nullptr;
-    char* dst = nullptr;
-    if (j < nm) {
-      const int32_t u = miss_id[j];
-      const int32_t m = owner_of(part, s_start, u);
-      const int64_t r = row_of(part, s_start, u, m);
-      if (r < feat.rows[m]) {
-        src = feat.shard[m] + r * feat.stride[m];
-        dst = out + (int64_t)miss_pos[j] * a.out_stride;
-      } else {
-        st |= GG_DEV_BAD_ROW;
+    if (lane < a.tile && i < hi) {
+      const int32_t u = in_ids[begin + i];
+      if (u >= 0 && (int64_t)u < part.N) {
+        const int32_t m = owner_of(part, s_start, u);
+        if (m != part.local) {
+          const int32_t sl = slot_of[u];
+          if (!(sl >= 0 && (int64_t)sl < a.cache_rows)) {
+            const int64_t r = row_of(part, s_start, u, m);
+            if (r < feat.rows[m])
+              src = feat.shard[m] + r * feat.stride[m];
+            else
+              st |= GG_DEV_BAD_ROW;
+          }
+        }
       }
     }
-    const int64_t left = nm - j0;
-    wave_copy_rows_scatter<VB, NT>(src, dst, left < kWave ? (int)left : kWave, a.geom);
+    if (__ballot(src != nullptr)) {
+      const int64_t left = hi - r0;
+      wave_copy_rows<VB, NT>(src, out + r0 * a.out_stride, a.out_stride,
+                             left < a.tile ? (int)left : a.tile, a.geom);
+    }
   }
   if (st) set_status(status, st);
 }
 
 struct GatherWs {
-  int64_t* miss_count;
-  int32_t* blk_stat;
-  int32_t* miss_pos;
-  int32_t* miss_id;
+  int32_t* blk_stat;   // per row block: local, hits, misses per owner
 };
 
 int32_t blocks_per_seg(int64_t n_cap, int32_t nseg) {
@@ -227,10 +226,7 @@ size_t gather_ws_layout(int64_t n_cap, int32_t nseg, int32_t P, char* base, Gath
   const int64_t bx = blocks_per_seg(n_cap, nseg);
   Carve cv{base, 0, ~(size_t)0};
   GatherWs g;
-  g.miss_count = cv.take<int64_t>(1);
   g.blk_stat = cv.take<int32_t>((size_t)(nseg * bx * (2 + P)));
-  g.miss_pos = cv.take<int32_t>((size_t)std::max<int64_t>(n_cap, 1));
-  g.miss_id = cv.take<int32_t>((size_t)std::max<int64_t>(n_cap, 1));
   if (out) *out = g;
   return align_up(cv.used, 256);
 }
@@ -240,23 +236,17 @@ void launch_gather(hipStream_t stream, int unroll, int32_t bx, const int32_t* in
                    const KPart& kp, const KFeat& kf, const GatherArgs& a, const char* cache,
                    const int32_t* slot_of, char* out, const GatherWs& w, gg_gather_stats_t* stats,
                    int32_t* status) {
-  hipLaunchKernelGGL(k_gather_zero, dim3(1), dim3(64), 0, stream, w.miss_count);
   if (VB == 16 && unroll == 8)
     hipLaunchKernelGGL((k_gather_rows<VB, NT, 8>), dim3(bx, a.nseg), dim3(kBlock), 0, stream, in_ids,
-                       bounds, kp, kf, a, cache, slot_of, out, w.blk_stat, w.miss_count, w.miss_pos,
-                       w.miss_id, status);
+                       bounds, kp, kf, a, cache, slot_of, out, w.blk_stat, status);
   else if (VB == 16 && unroll == 2)
     hipLaunchKernelGGL((k_gather_rows<VB, NT, 2>), dim3(bx, a.nseg), dim3(kBlock), 0, stream, in_ids,
-                       bounds, kp, kf, a, cache, slot_of, out, w.blk_stat, w.miss_count, w.miss_pos,
-                       w.miss_id, status);
+                       bounds, kp, kf, a, cache, slot_of, out, w.blk_stat, status);
   else
     hipLaunchKernelGGL((k_gather_rows<VB, NT, VB == 16 ? 4 : 8>), dim3(bx, a.nseg), dim3(kBlock), 0,
-                       stream, in_ids, bounds, kp, kf, a, cache, slot_of, out, w.blk_stat,
-                       w.miss_count, w.miss_pos, w.miss_id, status);
-  const int miss_blocks = (int)std::min<int64_t>(std::max<int64_t>(cdiv(a.n_cap, kBlock), 1), 1024);
-  hipLaunchKernelGGL((k_gather_finish<VB, NT>), dim3(a.nseg + miss_blocks), dim3(kBlock), 0, stream,
-                     bounds, kp, kf, a, bx, w.blk_stat, w.miss_count, w.miss_pos, w.miss_id, out,
-                     stats, status);
+                       stream, in_ids, bounds, kp, kf, a, cache, slot_of, out, w.blk_stat, status);
+  hipLaunchKernelGGL((k_gather_finish<VB, NT>), dim3(a.nseg + a.nseg * bx), dim3(kBlock), 0, stream,
+                     in_ids, bounds, kp, kf, a, bx, w.blk_stat, slot_of, out, stats, status);
 }
 
 }  // namespace
@@ -329,6 +319,6 @@ extern "C" int gg_gather_batch(const int32_t* in_ids_d, const int64_t* bounds_d,
       launch_gather<4, false>(stream, unroll, bx, in_ids_d, bounds_d, kp, kf, a, cache, slot_of_d, out, gw,
                               stats_d, status_d);
   }
-  GG_LAUNCH_CHECK("k_gather_zero/k_gather_rows/k_gather_finish");
+  GG_LAUNCH_CHECK("k_gather_rows/k_gather_finish");
   return GG_OK;
 }

@@ -272,40 +272,4 @@ __device__ __forceinline__ void wave_copy_rows(const char* src, char* dst0, int6
 }
 
 
-// As wave_copy_rows, but lane r also supplies row r's destination (rows that
-// land at scattered output positions, e.g. residual misses).
-template <int VB, bool NT>
-__device__ __forceinline__ void wave_copy_rows_scatter(const char* src, char* dst, int nrows,
-                                                       const CopyGeom& g) {
-  const int lane = lane_id();
-  const uint32_t total = (uint32_t)nrows * g.cpr;
-  const long long srcl = (long long)src, dstl = (long long)dst;
-  for (uint32_t base = 0; base < total; base += kWave) {
-    const uint32_t c = base + (uint32_t)lane;
-    const uint32_t r = __umulhi(c, g.magic);
-    const uint32_t col = c - r * g.cpr;
-    const char* sp = (const char*)__shfl(srcl, (int)(r & 63u), kWave);
-    char* dp = (char*)__shfl(dstl, (int)(r & 63u), kWave);
-    if (c < total && sp != nullptr) {
-      if (VB == 16)
-        st16<NT>(dp + (int64_t)col * 16, *(const u32x4*)(sp + (int64_t)col * 16));
-      else
-        st4<NT>(dp + (int64_t)col * 4, *(const uint32_t*)(sp + (int64_t)col * 4));
-    }
-  }
-  if (VB == 16 && g.tail) {
-    const uint32_t ttotal = (uint32_t)nrows * g.tail;
-    const int64_t off0 = (int64_t)g.cpr * 16;
-    for (uint32_t base = 0; base < ttotal; base += kWave) {
-      const uint32_t c = base + (uint32_t)lane;
-      const uint32_t r = __umulhi(c, g.tmagic);
-      const uint32_t w = c - r * g.tail;
-      const char* sp = (const char*)__shfl(srcl, (int)(r & 63u), kWave);
-      char* dp = (char*)__shfl(dstl, (int)(r & 63u), kWave);
-      if (c < ttotal && sp != nullptr)
-        st4<NT>(dp + off0 + (int64_t)w * 4, *(const uint32_t*)(sp + off0 + (int64_t)w * 4));
-    }
-  }
-}
-
 }  // namespace gg
