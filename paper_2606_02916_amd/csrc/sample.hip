@@ -42,7 +42,20 @@ struct SampleArgs {
   int64_t batch0;
   int32_t W, l, k;
   uint32_t key0, key1, epoch;
+  uint8_t* bytemap;   // non-null: marks go to one byte per node (bytes per batch: 32 * wpb)
 };
+
+// The last hop marks its draws with byte stores into a byte map instead of
+// atomic ORs into the bit sets when the map (one byte per node and batch)
+// is at most this large: a random byte store costs about a third of a
+// random atomic, and folding the map into the bit sets is one streaming
+// pass.  Above it (the 111M-node graph) the pass would cost more than the
+// atomics it saves.
+constexpr int64_t kByteMapMaxBytes = 512LL << 20;
+
+inline bool use_bytemap(int64_t num_nodes, int32_t W) {
+  return (int64_t)W * gg_bits_words(num_nodes) * 32 <= kByteMapMaxBytes;
+}
 
 // Largest b in [0, 64) with off[b] <= x, for a table padded with INT64_MAX.
 __device__ __forceinline__ int find_batch(const int64_t* off, int64_t x) {
@@ -53,16 +66,30 @@ __device__ __forceinline__ int find_batch(const int64_t* off, int64_t x) {
   return idx;
 }
 
-// Zeroes the window's bit sets and the per-level batch totals.
-__global__ void __launch_bounds__(kBlock) k_zero_words(uint32_t* p, int64_t n4, int32_t* btot,
-                                                       int32_t nbtot) {
+// Zeroes the window's bit sets (n4 16-byte words), the byte map (m4
+// 16-byte words, if any) and the per-level batch totals.
+__global__ void __launch_bounds__(kBlock) k_zero_words(uint32_t* p, int64_t n4, uint8_t* map,
+                                                       int64_t m4, int32_t* btot, int32_t nbtot) {
   if (blockIdx.x == 0)
     for (int t = threadIdx.x; t < nbtot; t += blockDim.x) btot[t] = 0;
-  u32x4* q = (u32x4*)p;
   const u32x4 z = {0u, 0u, 0u, 0u};
+  u32x4* q = (u32x4*)p;
   for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n4;
        i += (int64_t)gridDim.x * blockDim.x)
     q[i] = z;
+  u32x4* r = (u32x4*)map;
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < m4;
+       i += (int64_t)gridDim.x * blockDim.x)
+    r[i] = z;
+}
+
+// Bits of four bytes that are each 0 or 1: byte i gives bit i.
+__device__ __forceinline__ uint32_t pack4(uint32_t v) {
+  return (v & 1u) | ((v >> 7) & 2u) | ((v >> 14) & 4u) | ((v >> 21) & 8u);
+}
+
+__device__ __forceinline__ uint32_t pack16(u32x4 v) {
+  return pack4(v.x) | (pack4(v.y) << 4) | (pack4(v.z) << 8) | (pack4(v.w) << 12);
 }
 
 __global__ void __launch_bounds__(kBlock) k_mark_seeds(const int32_t* seeds, SeedOff so, int32_t W,
@@ -83,15 +110,34 @@ __global__ void __launch_bounds__(kBlock) k_mark_seeds(const int32_t* seeds, See
 
 // Popcount of one chunk (kChunkWords words) of one batch's bit set; the
 // chunk's count goes to cnt and is added to one of the batch's kTotLanes
-// partial totals (spread so that few blocks add to one word).
+// partial totals (spread so that few blocks add to one word).  With a byte
+// map (after a hop that marked bytes) the chunk's bytes are first folded
+// into its bit-set words.
 constexpr int kTotLanes = 8;
-__global__ void __launch_bounds__(kBlock) k_bits_count(const uint32_t* bits, int64_t wpb,
-                                                       int32_t* cnt, int32_t* btot) {
+__global__ void __launch_bounds__(kBlock) k_bits_count(uint32_t* bits, int64_t wpb,
+                                                       const uint8_t* map, int32_t* cnt,
+                                                       int32_t* btot) {
   __shared__ int32_t lds[kBlock / kWave];
   const int c = blockIdx.x, b = blockIdx.y, nch = gridDim.x;
-  const u32x4* p = (const u32x4*)(bits + (int64_t)b * wpb + (int64_t)c * kChunkWords +
-                                  threadIdx.x * kWordsPerThread);
-  const u32x4 x = p[0], y = p[1];
+  const int64_t w0 = (int64_t)c * kChunkWords + threadIdx.x * kWordsPerThread;
+  u32x4* p = (u32x4*)(bits + (int64_t)b * wpb + w0);
+  u32x4 x = p[0], y = p[1];
+  if (map) {
+    const u32x4* q = (const u32x4*)(map + ((int64_t)b * wpb + w0) * 32);
+    u32x4 m[16];
+#pragma unroll
+    for (int j = 0; j < 16; ++j) m[j] = q[j];
+    x.x |= pack16(m[0]) | (pack16(m[1]) << 16);
+    x.y |= pack16(m[2]) | (pack16(m[3]) << 16);
+    x.z |= pack16(m[4]) | (pack16(m[5]) << 16);
+    x.w |= pack16(m[6]) | (pack16(m[7]) << 16);
+    y.x |= pack16(m[8]) | (pack16(m[9]) << 16);
+    y.y |= pack16(m[10]) | (pack16(m[11]) << 16);
+    y.z |= pack16(m[12]) | (pack16(m[13]) << 16);
+    y.w |= pack16(m[14]) | (pack16(m[15]) << 16);
+    p[0] = x;
+    p[1] = y;
+  }
   int s = __popc(x.x) + __popc(x.y) + __popc(x.z) + __popc(x.w) + __popc(y.x) + __popc(y.y) +
           __popc(y.z) + __popc(y.w);
   s = wave_sum(s);
@@ -285,7 +331,12 @@ __device__ __forceinline__ void sample_one(const RowT* row_ptr, const int32_t* c
   for (int i = 0; i < KMAX; ++i) {
     if (i < k) {
       const int32_t x = v[i];
-      if (x >= 0) atomicOr(brow + (x >> 5), 1u << (x & 31));
+      if (x >= 0) {
+        if (a.bytemap)
+          a.bytemap[(int64_t)b * a.wpb * 32 + x] = 1;
+        else
+          atomicOr(brow + (x >> 5), 1u << (x & 31));
+      }
       out[i] = (i < cnt) ? x : -1;
     }
   }
@@ -317,6 +368,7 @@ struct SampleWs {
   int32_t* cnt;       // per (batch, chunk) counts of the current level
   int32_t* btot;      // per (level, batch) totals, zeroed by k_zero_words
   LevelState* lvl;
+  uint8_t* map;       // the last hop's byte map (32 * wpb bytes per batch), or null
 };
 
 size_t sample_ws_layout(int64_t num_nodes, int32_t W, char* base, SampleWs* out) {
@@ -326,6 +378,9 @@ size_t sample_ws_layout(int64_t num_nodes, int32_t W, char* base, SampleWs* out)
   s.cnt = cv.take<int32_t>((size_t)(W * nch));
   s.btot = cv.take<int32_t>((size_t)(GG_MAX_LAYERS + 1) * GG_MAX_W * kTotLanes);
   s.lvl = cv.take<LevelState>(1);
+  s.map = use_bytemap(num_nodes, W)
+              ? cv.take<uint8_t>((size_t)W * (size_t)gg_bits_words(num_nodes) * 32)
+              : nullptr;
   if (out) *out = s;
   return align_up(cv.used, 256);
 }
@@ -394,8 +449,9 @@ extern "C" int gg_sample_window(const gg_csr_t* csr, const int32_t* seeds_d,
   const int64_t wpb = gg_bits_words(N);
   const int32_t nch = (int32_t)(wpb / kChunkWords);
 
+  const int64_t map4 = sw.map ? W * wpb * 2 : 0;   // 32 bytes per word, 16 per store
   hipLaunchKernelGGL(k_zero_words, dim3((unsigned)std::min<int64_t>(cdiv(W * wpb / 4, kBlock), 4096)),
-                     dim3(kBlock), 0, stream, out->frontier_bits, W * wpb / 4, sw.btot,
+                     dim3(kBlock), 0, stream, out->frontier_bits, W * wpb / 4, sw.map, map4, sw.btot,
                      (L + 1) * GG_MAX_W * kTotLanes);
   GG_LAUNCH_CHECK("k_zero_words");
   SeedOff so;
@@ -430,6 +486,7 @@ extern "C" int gg_sample_window(const gg_csr_t* csr, const int32_t* seeds_d,
       a.key0 = (uint32_t)rng_seed;
       a.key1 = (uint32_t)(rng_seed >> 32);
       a.epoch = (uint32_t)epoch;
+      a.bytemap = lv == L ? sw.map : nullptr;
       const int64_t bnd = std::min<int64_t>(bound[lv - 1], out->frontier_cap);
       int rc = csr->row_ptr_bits == 64
                    ? launch_sample<int64_t>(csr, out, sw, status_d, a, bnd, stream)
@@ -438,7 +495,7 @@ extern "C" int gg_sample_window(const gg_csr_t* csr, const int32_t* seeds_d,
     }
     int32_t* btot = sw.btot + (int64_t)lv * GG_MAX_W * kTotLanes;
     hipLaunchKernelGGL(k_bits_count, dim3(nch, W), dim3(kBlock), 0, stream, out->frontier_bits, wpb,
-                       sw.cnt, btot);
+                       lv == L ? sw.map : nullptr, sw.cnt, btot);
     GG_LAUNCH_CHECK("k_bits_count");
     LevelArgs la;
     la.lv = lv;
