@@ -105,14 +105,14 @@ def summarize(args):
             # gather and the timed regather (the odd launches)
             n_pre, n_warm, n_timed = (int(x) for x in args.phases.split(","))
             per = {}
-            for part in ("k_gather_zero", "k_gather_rows", "k_gather_finish"):
+            for part in ("k_gather_rows", "k_gather_finish"):
                 per[part] = [r[0] for r in db.execute(
                     "select end-start from kernels where name like ? order by start",
                     (f"%{part}%",)).fetchall()]
             n = len(per["k_gather_rows"])
             calls = [sum(per[p][i] for p in per if i < len(per[p])) for i in range(n)]
             out.append("")
-            out.append("# gg_gather_batch (zero + rows + finish) by bench phase, microseconds")
+            out.append("# gg_gather_batch (rows + finish) by bench phase, microseconds")
             for label, lo, hi, step in (("pre-pass, all launches", 0, n_pre, 1),
                                         ("pre-pass, odd launches", 1, n_pre, 2),
                                         ("timed steps", n - n_timed, n, 1)):
