@@ -181,7 +181,10 @@ size_t gg_ws_gather(int64_t n_cap, int32_t nseg, int32_t num_parts);
  * (l << 16) | i/4), word i mod 4 for draw i, mapped onto [0, d-k+i] by
  * floor(r * (d-k+i+1) / 2^32)), ascending.  F_{l+1} is F_l together with
  * the neighbours drawn at hop l.  batch0 is the epoch-global index of the
- * window's first batch, so N_b does not depend on W. */
+ * window's first batch, so N_b does not depend on W.  When W * 32 *
+ * gg_bits_words(num_nodes) is at most 512 MB the workspace also holds a
+ * byte map (one byte per node and batch) into which the last hop marks its
+ * draws; gg_ws_sample includes it. */
 int gg_sample_window(const gg_csr_t* csr, const int32_t* seeds_d, const int64_t* seed_off_h,
                      int32_t W, const int32_t* fanout_h, int32_t L, uint64_t rng_seed,
                      int32_t epoch, int64_t batch0, const gg_wsample_t* out, int32_t* status_d,

@@ -127,6 +127,20 @@ def test_row_with_tail_words():
     w.run_and_compare(0)
 
 
+@pytest.mark.parametrize("n_hot", [0, 700, -1])
+def test_wide_rows_with_misses(n_hot):
+    """2,408-byte rows at a 2,416-byte stride (eight rows per wave step)
+    through both gathers and the miss path: with n_hot = 0 every remote row
+    is a miss, with 700 some are."""
+    log(f"tiny: 2408-byte rows (tiles of 8), n_hot={n_hot}, consecutive windows")
+    inst = synth.instance("tiny")
+    rng = np.random.default_rng(8)
+    shards = [rng.integers(0, 256, size=(s.shape[0], 2416), dtype=np.uint8) for s in inst.shards]
+    w = world(inst, shards=shards, row_bytes=2408, stride=2416, n_hot=n_hot, W=2)
+    for k in range(2):
+        w.run_and_compare(k)
+
+
 def test_repeat_runs_are_identical():
     log("small: determinism across two pipelines")
     inst = synth.instance("small")
