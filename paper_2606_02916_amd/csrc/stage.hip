@@ -287,7 +287,8 @@ extern "C" int gg_stage_bulk(const int32_t* bucket_ids_d, const int64_t* owner_o
   // full grid would hold every CU while it waits and starve kernels on
   // other streams (the next window's sampling), so cap it then.
   static const int host_cap = env_int("GG_STAGE_HOST_BLOCKS", 128);
-  int64_t gmax = 16384;
+  static const int hbm_cap = env_int("GG_STAGE_BLOCKS", 16384);
+  int64_t gmax = hbm_cap;
   if (host_cap > 0 && host_shards(kf) > 0) gmax = host_cap;
   const int grid = (int)std::min<int64_t>(std::max<int64_t>(cdiv(ntiles, kBlock / kWave), 1), gmax);
   StageStatsArgs sa;
