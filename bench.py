@@ -222,8 +222,9 @@ def main():
 
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
-        print("bench.py runs the per-window fetch path on one GPU only; multi-GPU runs are not "
-              "part of this build (see DESIGN.md for how the path would shard)", file=sys.stderr)
+        print("bench.py runs the per-window fetch path on one GPU only; with several GPUs each "
+              "would run its own partition's windows, which is not implemented here",
+              file=sys.stderr)
         sys.exit(2)
 
     import numpy as np
