@@ -180,6 +180,69 @@ def test_large_sparse_full_window_matches_oracle():
 
 
 @pytest.mark.timeout(900)
+def test_large_sparse_lookahead_as_benchmarked():
+    """The benchmark's launch configuration: the look-ahead driver with two
+    buffer sets over three consecutive windows of large_sparse.  Every
+    gathered row equals the row of the unsharded feature matrix (the
+    ground truth independent of the cache), N_b of the first and last batch
+    of every window equals the oracle's, and the hot set is the union of the
+    window's remote N_b."""
+    log("large_sparse: look-ahead driver (2 buffer sets), windows 0-2, every gathered row")
+    import torch as T
+    from oracle import ggref
+    from paper_2606_02916_amd import LookaheadPipeline
+    inst, rp_d, ci_d, sh_d = synth.torch_instance("large_sparse", "cuda:0")
+    wl = inst.wl
+    P, L, W = wl.num_parts, len(wl.fanout), wl.W
+    dev = T.device("cuda:0")
+    look = LookaheadPipeline(rp_d, ci_d, P, wl.part_kind, wl.local_owner, inst.range_start, sh_d,
+                             [s.shape[0] for s in inst.shards], wl.row_bytes, wl.row_stride, W,
+                             wl.fanout, wl.batch_size, device=dev, nsets=2)
+    seeds_d = T.from_numpy(inst.seeds).to(dev)
+    boff, rs, rb = inst.batch_off, inst.range_start, wl.row_bytes
+    feats = np.concatenate([s[:, :rb] for s in inst.shards])      # row u = node u
+
+    def check(k, Wk, bufs, b0, hot_slot):
+        look.gathered_event(k).synchronize()
+        foff = bufs.frontier_off[:(L + 1) * Wk + 1].cpu().numpy()
+        fids = bufs.frontier_ids[:int(foff[-1])].cpu().numpy()
+        base = int(foff[L * Wk])
+        n = int(foff[-1]) - base
+        allN = fids[base:]
+        got = bufs.win_out[:n, :rb].cpu().numpy()
+        assert np.array_equal(got, feats[allN]), f"window {k} rows"
+        for b in (0, Wk - 1):
+            s = inst.seeds[boff[b0 + b]:boff[b0 + b + 1]]
+            f1, o1, _, _ = ggref.sample_window(inst.row_ptr, inst.col_idx, s,
+                                               np.array([0, len(s)], np.int64), wl.fanout, 0, 0,
+                                               b0 + b)
+            for l in range(L + 1):
+                assert np.array_equal(fids[foff[l * Wk + b]:foff[l * Wk + b + 1]],
+                                      f1[o1[l]:o1[l + 1]]), (k, b, l)
+        remote = allN[(allN < rs[0]) | (allN >= rs[1])]
+        uniq = np.unique(remote)
+        cnt = look.hot_count[hot_slot].cpu().numpy()
+        assert int(cnt[0]) == len(uniq)
+        assert np.array_equal(bufs.hot_ids[:len(uniq)].cpu().numpy(), uniq)
+        for b in range(Wk):
+            gs = bufs.gather_stats_dict(b)
+            assert gs["misses"] == 0 and gs["local"] + gs["hits"] == gs["rows"]
+        st = bufs.stage_stats_dict()
+        assert st["rows_total"] == len(uniq)
+        assert st["retained"] + sum(st["rows"]) == st["rows_total"]
+
+    pending = None
+    for k in range(3):
+        b0, b1 = synth.window_batches(boff, W, k)
+        Wk, bufs = look.window(seeds_d[boff[b0]:boff[b1]], boff[b0:b1 + 1] - boff[b0], b0)
+        if pending is not None:
+            check(*pending)
+        pending = (k, Wk, bufs, b0, k % look.NSLOT)
+    check(*pending)
+    assert look.read_status() == 0
+
+
+@pytest.mark.timeout(900)
 def test_dense_mid_full_window_matches_oracle():
     log("dense_mid: 233K nodes, 114M edges, fp32x602 (stride 2416), fanout [25,10], W=8, window 0")
     w = world(synth.instance("dense_mid"))
