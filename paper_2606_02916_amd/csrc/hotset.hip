@@ -8,6 +8,8 @@
 // the r smallest ids with freq == f*, which is the n_hot most frequent with
 // ties broken by smaller id.  Ids come out ascending because words are
 // visited in id order.
+#include <stdlib.h>
+
 #include "gg_host.hpp"
 
 namespace gg {
@@ -21,6 +23,8 @@ struct HotArgs {
   int32_t W;
   int32_t fstar;   // used when params == nullptr
   int64_t r;       // used when params == nullptr
+  int32_t passes;  // kHotWords-word passes per chunk
+  int32_t nch;     // chunks (at most kHotMaxChunks)
 };
 
 __device__ __forceinline__ void bs_add(uint32_t (&pl)[kPlanes], uint32_t x) {
@@ -79,10 +83,13 @@ __device__ __forceinline__ uint32_t remote_mask(const KPart& p, int64_t w) {
   return ~local;
 }
 
-// One 32-node word per thread: a block covers kHotWords consecutive words,
-// so a window of N nodes spreads over N / 8192 blocks.
+// One 32-node word per thread and pass: a block (chunk) covers `passes`
+// runs of kHotWords consecutive words.  Chunks stay at most kHotMaxChunks,
+// so every emit block can sum the counts of the chunks before it itself;
+// a 2.45M-node window is 304 chunks of one pass.
 constexpr int kHotWords = kBlock;
-constexpr int kHotMaxIds = kHotWords * 32;  // ids one block can emit
+constexpr int kHotMaxIds = kHotWords * 32;  // ids one pass can emit
+constexpr int kHotMaxChunks = 1024;
 
 // Sums word w of every batch's set into the planes, eight loads in flight.
 __device__ __forceinline__ void load_planes(const uint32_t* bits, const HotArgs& a, int64_t w,
@@ -116,13 +123,21 @@ __global__ void __launch_bounds__(kBlock) k_hot_hist(const uint32_t* bits, KPart
   for (int t = threadIdx.x; t < GG_MAX_W + 2; t += blockDim.x) hist[t] = 0;
   __syncthreads();
   const int c = blockIdx.x;
-  uint32_t pl[kPlanes];
-  remote_planes(bits, part, a, (int64_t)c * kHotWords + threadIdx.x, pl);
-  for (int32_t f = 1; f <= a.W; ++f) {
-    uint32_t g, e;
-    bs_cmp(pl, (uint32_t)f, &g, &e);
-    const int n = wave_sum(__popc(e));
-    if (lane_id() == 0 && n) atomicAdd(&hist[f], n);
+  for (int32_t q = 0; q < a.passes; ++q) {
+    const int64_t w = ((int64_t)c * a.passes + q) * kHotWords + threadIdx.x;
+    uint32_t pl[kPlanes];
+    if (w < a.wpb) {
+      remote_planes(bits, part, a, w, pl);
+    } else {
+#pragma unroll
+      for (int p = 0; p < kPlanes; ++p) pl[p] = 0u;
+    }
+    for (int32_t f = 1; f <= a.W; ++f) {
+      uint32_t g, e;
+      bs_cmp(pl, (uint32_t)f, &g, &e);
+      const int n = wave_sum(__popc(e));
+      if (lane_id() == 0 && n) atomicAdd(&hist[f], n);
+    }
   }
   __syncthreads();
   for (int t = threadIdx.x; t <= a.W; t += blockDim.x) chunk_hist[(int64_t)c * (a.W + 1) + t] = hist[t];
@@ -187,6 +202,20 @@ __device__ __forceinline__ void sel_masks(const uint32_t (&pl)[kPlanes], uint32_
   if (fstar == 0) *em = 0u;  // freq == 0 is not a member
 }
 
+// The planes of word w restricted to remote nodes, or none past the set.
+__device__ __forceinline__ void word_masks(const uint32_t* bits, const KPart& part,
+                                           const HotArgs& a, int64_t w, uint32_t fstar,
+                                           uint32_t (&pl)[kPlanes], uint32_t* gm, uint32_t* em) {
+  if (w < a.wpb) {
+    remote_planes(bits, part, a, w, pl);
+    sel_masks(pl, fstar, gm, em);
+  } else {
+#pragma unroll
+    for (int p = 0; p < kPlanes; ++p) pl[p] = 0u;
+    *gm = *em = 0u;
+  }
+}
+
 // Per-chunk counts of nodes with freq > f* and freq == f*.
 __global__ void __launch_bounds__(kBlock) k_hot_count(const uint32_t* bits, KPart part, HotArgs a,
                                                       const int64_t* params, int32_t* cnt_gt,
@@ -196,12 +225,16 @@ __global__ void __launch_bounds__(kBlock) k_hot_count(const uint32_t* bits, KPar
   uint32_t fstar;
   int64_t r;
   get_sel(a, params, &fstar, &r);
-  uint32_t pl[kPlanes];
-  remote_planes(bits, part, a, (int64_t)c * kHotWords + threadIdx.x, pl);
-  uint32_t g, e;
-  sel_masks(pl, fstar, &g, &e);
-  const int ng = wave_sum(__popc(g));
-  const int ne = wave_sum(__popc(e));
+  int ng = 0, ne = 0;
+  for (int32_t q = 0; q < a.passes; ++q) {
+    uint32_t pl[kPlanes], g, e;
+    word_masks(bits, part, a, ((int64_t)c * a.passes + q) * kHotWords + threadIdx.x, fstar, pl,
+               &g, &e);
+    ng += __popc(g);
+    ne += __popc(e);
+  }
+  ng = wave_sum(ng);
+  ne = wave_sum(ne);
   if (lane_id() == 0) {
     lds[0][threadIdx.x / kWave] = ng;
     lds[1][threadIdx.x / kWave] = ne;
@@ -213,69 +246,93 @@ __global__ void __launch_bounds__(kBlock) k_hot_count(const uint32_t* bits, KPar
   }
 }
 
-__global__ void __launch_bounds__(1024) k_hot_scan(const int32_t* cnt_gt, const int32_t* cnt_eq,
-                                                   int32_t nch, HotArgs a, const int64_t* params,
-                                                   int64_t* off_gt, int64_t* off_eq,
-                                                   int64_t* hot_count, int32_t* status) {
-  __shared__ int64_t lds[16];
-  uint32_t fstar;
-  int64_t r;
-  get_sel(a, params, &fstar, &r);
-  const int64_t tg = block_scan_large(cnt_gt, off_gt, nch, 0, lds);
-  const int64_t te = block_scan_large(cnt_eq, off_eq, nch, 0, lds);
-  if (threadIdx.x == 0) {
-    const int64_t total = tg + (te < r ? te : r);
-    hot_count[0] = total < a.cap ? total : a.cap;
-    hot_count[1] = total;
-    if (total > a.cap) set_status(status, GG_DEV_CAPACITY);
+// Sums of two values over the block.
+__device__ __forceinline__ void block_sum2(int64_t& x, int64_t& y, int64_t (*lds)[2]) {
+  x = wave_sum(x);
+  y = wave_sum(y);
+  const int w = threadIdx.x / kWave;
+  if (lane_id() == 0) {
+    lds[w][0] = x;
+    lds[w][1] = y;
   }
+  __syncthreads();
+  x = y = 0;
+  for (int q = 0; q < kBlock / kWave; ++q) {
+    x += lds[q][0];
+    y += lds[q][1];
+  }
+  __syncthreads();
 }
 
-// Writes the chunk's selected ids (and their freq) ascending.  Each thread
-// owns one word; the block's ids are assembled in LDS at their block-local
-// positions and then written out as one contiguous run.
+// Writes the chunk's selected ids (and their freq) ascending.  The block
+// first sums the counts of the chunks before its own (its place in the
+// list; block 0 sums them all and writes the hot-set count).  Each thread
+// owns one word per pass; a pass's ids are assembled in LDS at their
+// block-local positions and then written out as one contiguous run.
 __global__ void __launch_bounds__(kBlock) k_hot_emit(const uint32_t* bits, KPart part, HotArgs a,
-                                                     const int64_t* params, const int64_t* off_gt,
-                                                     const int64_t* off_eq, int32_t* hot_ids,
-                                                     int32_t* hot_freq) {
+                                                     const int64_t* params, const int32_t* cnt_gt,
+                                                     const int32_t* cnt_eq, int32_t* hot_ids,
+                                                     int32_t* hot_freq, int64_t* hot_count,
+                                                     int32_t* status) {
   __shared__ int32_t s_out[kHotMaxIds];
   __shared__ int64_t lds[kBlock / kWave];
+  __shared__ int64_t lds2[kBlock / kWave][2];
   const int c = blockIdx.x;
-  const int64_t w = (int64_t)c * kHotWords + threadIdx.x;
   uint32_t fstar;
   int64_t r;
   get_sel(a, params, &fstar, &r);
-  uint32_t pl[kPlanes];
-  remote_planes(bits, part, a, w, pl);
-  uint32_t gm, em;
-  sel_masks(pl, fstar, &gm, &em);
-  const int ne = __popc(em);
-  int64_t tot;
-  // freq == f* nodes are taken in id order until r of them are in.
-  const int64_t eq_rank0 = off_eq[c] + block_excl_scan<kBlock>((int64_t)ne, lds, &tot);
-  int64_t take = r - eq_rank0;
-  take = take < 0 ? 0 : (take > ne ? ne : take);
-  uint32_t sel = gm;
-  for (uint32_t e = em; take > 0; --take) {
-    sel |= e & (0u - e);  // lowest remaining id
-    e &= e - 1u;
+  // chunks before c (all chunks for block 0's totals)
+  const int upto = c == 0 ? a.nch : c;
+  int64_t pg = 0, pe = 0;
+  for (int t = threadIdx.x; t < upto; t += kBlock) {
+    pg += cnt_gt[t];
+    pe += cnt_eq[t];
   }
-  int64_t btot;
-  const int64_t lpos = block_excl_scan<kBlock>((int64_t)__popc(sel), lds, &btot);
-  const int64_t pos0 = off_gt[c] + (off_eq[c] < r ? off_eq[c] : r);
-  for (int pass = 0; pass < (hot_freq ? 2 : 1); ++pass) {
-    int32_t* dst = pass == 0 ? hot_ids : hot_freq;
-    int64_t p = lpos;
-    for (uint32_t m = sel; m; m &= m - 1u) {
-      const int bit = __ffs(m) - 1;
-      s_out[p++] = pass == 0 ? (int32_t)(w * 32 + bit) : (int32_t)bs_freq(pl, bit);
+  block_sum2(pg, pe, lds2);
+  if (c == 0) {
+    if (threadIdx.x == 0) {
+      const int64_t total = pg + (pe < r ? pe : r);
+      hot_count[0] = total < a.cap ? total : a.cap;
+      hot_count[1] = total;
+      if (total > a.cap) set_status(status, GG_DEV_CAPACITY);
     }
-    __syncthreads();
-    for (int64_t i = threadIdx.x; i < btot; i += kBlock) {
-      const int64_t o = pos0 + i;
-      if (o < a.cap) dst[o] = s_out[i];
+    pg = pe = 0;
+  }
+  int64_t eq_before = pe;                          // freq == f* ids before this pass
+  int64_t pos0 = pg + (pe < r ? pe : r);           // output position of this pass
+  for (int32_t q = 0; q < a.passes; ++q) {
+    const int64_t w = ((int64_t)c * a.passes + q) * kHotWords + threadIdx.x;
+    uint32_t pl[kPlanes], gm, em;
+    word_masks(bits, part, a, w, fstar, pl, &gm, &em);
+    const int ne = __popc(em);
+    int64_t etot;
+    // freq == f* nodes are taken in id order until r of them are in.
+    const int64_t eq_rank0 = eq_before + block_excl_scan<kBlock>((int64_t)ne, lds, &etot);
+    int64_t take = r - eq_rank0;
+    take = take < 0 ? 0 : (take > ne ? ne : take);
+    uint32_t sel = gm;
+    for (uint32_t e = em; take > 0; --take) {
+      sel |= e & (0u - e);  // lowest remaining id
+      e &= e - 1u;
     }
-    __syncthreads();
+    int64_t btot;
+    const int64_t lpos = block_excl_scan<kBlock>((int64_t)__popc(sel), lds, &btot);
+    for (int pass = 0; pass < (hot_freq ? 2 : 1); ++pass) {
+      int32_t* dst = pass == 0 ? hot_ids : hot_freq;
+      int64_t p = lpos;
+      for (uint32_t m = sel; m; m &= m - 1u) {
+        const int bit = __ffs(m) - 1;
+        s_out[p++] = pass == 0 ? (int32_t)(w * 32 + bit) : (int32_t)bs_freq(pl, bit);
+      }
+      __syncthreads();
+      for (int64_t i = threadIdx.x; i < btot; i += kBlock) {
+        const int64_t o = pos0 + i;
+        if (o < a.cap) dst[o] = s_out[i];
+      }
+      __syncthreads();
+    }
+    eq_before += etot;
+    pos0 += btot;
   }
 }
 
@@ -283,20 +340,31 @@ struct HotWs {
   int32_t* chunk_hist;
   int32_t* cnt_gt;
   int32_t* cnt_eq;
-  int64_t* off_gt;
-  int64_t* off_eq;
   int64_t* params;
 };
 
+// Passes per chunk and chunks for a window of num_nodes nodes.  The chunk
+// limit can be lowered through GG_HOT_MAX_CHUNKS (read at every call), which
+// lets small graphs exercise multi-pass chunks; it must not change between a
+// gg_ws_hotset call and the calls that use that workspace.
+void hot_chunks(int64_t num_nodes, int32_t* passes, int32_t* nch) {
+  const int64_t runs = gg_bits_words(num_nodes) / kHotWords;
+  const char* e = getenv("GG_HOT_MAX_CHUNKS");
+  int64_t maxc = (e && *e) ? atoll(e) : kHotMaxChunks;
+  maxc = std::min<int64_t>(std::max<int64_t>(maxc, 1), kHotMaxChunks);
+  const int64_t p = std::max<int64_t>(1, cdiv(runs, maxc));
+  *passes = (int32_t)p;
+  *nch = (int32_t)cdiv(runs, p);
+}
+
 size_t hot_ws_layout(int64_t num_nodes, int32_t W, char* base, HotWs* out) {
-  const int64_t nch = gg_bits_words(num_nodes) / kHotWords;
+  int32_t passes, nch;
+  hot_chunks(num_nodes, &passes, &nch);
   Carve cv{base, 0, ~(size_t)0};
   HotWs h;
-  h.chunk_hist = cv.take<int32_t>((size_t)(nch * (W + 1)));
+  h.chunk_hist = cv.take<int32_t>((size_t)nch * (W + 1));
   h.cnt_gt = cv.take<int32_t>((size_t)nch);
   h.cnt_eq = cv.take<int32_t>((size_t)nch);
-  h.off_gt = cv.take<int64_t>((size_t)nch);
-  h.off_eq = cv.take<int64_t>((size_t)nch);
   h.params = cv.take<int64_t>(4);
   if (out) *out = h;
   return align_up(cv.used, 256);
@@ -333,13 +401,16 @@ extern "C" int gg_build_hotset(const uint32_t* frontier_bits_d, int32_t W, const
   const size_t need_ws = hot_ws_layout(kp.N, W, (char*)ws, &hw);
   GG_REQUIRE(ws && ws_bytes >= need_ws, "workspace of %zu bytes < %zu", ws_bytes, need_ws);
   const int64_t wpb = gg_bits_words(kp.N);
-  const int32_t nch = (int32_t)(wpb / kHotWords);
+  int32_t passes, nch;
+  hot_chunks(kp.N, &passes, &nch);
   HotArgs a;
   a.wpb = wpb;
   a.cap = cap;
   a.W = W;
   a.fstar = 0;
   a.r = 0;
+  a.passes = passes;
+  a.nch = nch;
   const int64_t* params = nullptr;
   if (n_hot == 0) {
     a.fstar = W + 1;
@@ -355,11 +426,8 @@ extern "C" int gg_build_hotset(const uint32_t* frontier_bits_d, int32_t W, const
   hipLaunchKernelGGL(k_hot_count, dim3(nch), dim3(kBlock), 0, stream, frontier_bits_d, kp, a, params,
                      hw.cnt_gt, hw.cnt_eq);
   GG_LAUNCH_CHECK("k_hot_count");
-  hipLaunchKernelGGL(k_hot_scan, dim3(1), dim3(1024), 0, stream, hw.cnt_gt, hw.cnt_eq, nch, a,
-                     params, hw.off_gt, hw.off_eq, hot_count_d, status_d);
-  GG_LAUNCH_CHECK("k_hot_scan");
   hipLaunchKernelGGL(k_hot_emit, dim3(nch), dim3(kBlock), 0, stream, frontier_bits_d, kp, a, params,
-                     hw.off_gt, hw.off_eq, hot_ids_d, hot_freq_d);
+                     hw.cnt_gt, hw.cnt_eq, hot_ids_d, hot_freq_d, hot_count_d, status_d);
   GG_LAUNCH_CHECK("k_hot_emit");
   return GG_OK;
 }

@@ -64,6 +64,18 @@ def test_small_window_sizes(W):
     w.run_and_compare(1)
 
 
+@pytest.mark.parametrize("n_hot", [-1, 0, 1, 2000])
+def test_hot_set_in_multi_pass_chunks(n_hot, monkeypatch):
+    """The hot set's chunks span several 256-word passes once a graph has
+    more than 1024 of them (the 111M-node graph); GG_HOT_MAX_CHUNKS=2
+    forces that layout on the small graph, with and without a budget."""
+    log(f"small: hot set in two chunks of several passes, n_hot={n_hot}")
+    monkeypatch.setenv("GG_HOT_MAX_CHUNKS", "2")
+    w = world(synth.instance("small"), n_hot=n_hot)
+    w.run_and_compare(0)
+    w.run_and_compare(1)
+
+
 @pytest.mark.parametrize("frac", [(1, 10), (1, 3), (0, 1), (1, 1), (999, 1000)])
 def test_relative_budget_window_matches_oracle(frac):
     log(f"small: hot set = top {frac[0]}/{frac[1]} of the window's remote nodes, 2 windows")
