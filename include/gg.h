@@ -264,11 +264,17 @@ int gg_stage_bulk(const int32_t* bucket_ids_d, const int64_t* owner_off_d, int64
  * bounds_d = frontier_off + L*W + b with nseg = 1 gathers N_b; with
  * bounds_d = frontier_off + L*W and nseg = W it gathers the whole window.
  * No host synchronisation is needed.  Rows past n_cap are dropped and set
- * GG_DEV_CAPACITY. */
+ * GG_DEV_CAPACITY.  flags: 0, or GG_GATHER_SHARED when other streams run
+ * latency-bound work (sampling) on the device at the same time: each lane
+ * then keeps half as many row loads in flight, which costs the gather a few
+ * percent alone and leaves the memory system's queues short enough for the
+ * concurrent work.  Results are identical either way; any other flag bit is
+ * GG_ERR_ARG. */
+#define GG_GATHER_SHARED 1
 int gg_gather_batch(const int32_t* in_ids_d, const int64_t* bounds_d, int32_t nseg,
                     int64_t n_cap, const gg_part_t* part, const gg_feat_t* feat,
                     const void* cache_d, int64_t cache_stride, int64_t cache_rows,
-                    const int32_t* slot_of_d, void* out_d, int64_t out_stride,
+                    const int32_t* slot_of_d, void* out_d, int64_t out_stride, int32_t flags,
                     gg_gather_stats_t* stats_d, int32_t* status_d, void* ws, size_t ws_bytes,
                     hipStream_t stream);
 

@@ -85,11 +85,12 @@ __device__ __forceinline__ uint32_t remote_mask(const KPart& p, int64_t w) {
 
 // One 32-node word per thread and pass: a block (chunk) covers `passes`
 // runs of kHotWords consecutive words.  Chunks stay at most kHotMaxChunks,
-// so every emit block can sum the counts of the chunks before it itself;
-// a 2.45M-node window is 304 chunks of one pass.
+// so every emit block can sum the counts of the chunks before it itself
+// (at most 16 loads per thread and array); a 2.45M-node window is 304
+// chunks of one pass, a 111M-node one 3,388 chunks of four.
 constexpr int kHotWords = kBlock;
 constexpr int kHotMaxIds = kHotWords * 32;  // ids one pass can emit
-constexpr int kHotMaxChunks = 1024;
+constexpr int kHotMaxChunks = 4096;
 
 // Sums word w of every batch's set into the planes, eight loads in flight.
 __device__ __forceinline__ void load_planes(const uint32_t* bits, const HotArgs& a, int64_t w,

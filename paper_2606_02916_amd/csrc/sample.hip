@@ -67,11 +67,12 @@ __device__ __forceinline__ int find_batch(const int64_t* off, int64_t x) {
 }
 
 // Zeroes the window's bit sets (n4 16-byte words), the byte map (m4
-// 16-byte words, if any) and the per-level batch totals.
+// 16-byte words, if any) and the per-level partial totals (nbtot).
 __global__ void __launch_bounds__(kBlock) k_zero_words(uint32_t* p, int64_t n4, uint8_t* map,
                                                        int64_t m4, int32_t* btot, int32_t nbtot) {
-  if (blockIdx.x == 0)
-    for (int t = threadIdx.x; t < nbtot; t += blockDim.x) btot[t] = 0;
+  for (int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; t < nbtot;
+       t += (int64_t)gridDim.x * blockDim.x)
+    btot[t] = 0;
   const u32x4 z = {0u, 0u, 0u, 0u};
   u32x4* q = (u32x4*)p;
   for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n4;
@@ -108,15 +109,27 @@ __global__ void __launch_bounds__(kBlock) k_mark_seeds(const int32_t* seeds, See
   }
 }
 
-// Popcount of one chunk (kChunkWords words) of one batch's bit set; the
-// chunk's count goes to cnt and is added to one of the batch's kTotLanes
-// partial totals (spread so that few blocks add to one word).  With a byte
-// map (after a hop that marked bytes) the chunk's bytes are first folded
-// into its bit-set words.
+// Popcount of one chunk (kChunkWords words) of one batch's bit set.  The
+// chunk's count goes to cnt and is added to its group's partial total (a
+// group is kGroupChunks consecutive chunks of one batch), spread over
+// kTotLanes words so that at most eight blocks add to one word (one total
+// per batch had 212 blocks contending for a word on the 111M-node graph).
+// An emit block then finds its place from the group totals of the batches
+// before its own, those of its batch before its group, and the counts of
+// its group's chunks before it: a few KB that stay in the caches.  With a
+// byte map (after a hop that marked bytes) the chunk's bytes are first
+// folded into its bit-set words.
 constexpr int kTotLanes = 8;
+constexpr int kGroupChunks = 64;
+
+struct Totals {
+  int32_t* gtot;   // [W][ngroups][kTotLanes]
+  int32_t ngroups;
+};
+
 __global__ void __launch_bounds__(kBlock) k_bits_count(uint32_t* bits, int64_t wpb,
                                                        const uint8_t* map, int32_t* cnt,
-                                                       int32_t* btot) {
+                                                       Totals tt) {
   __shared__ int32_t lds[kBlock / kWave];
   const int c = blockIdx.x, b = blockIdx.y, nch = gridDim.x;
   const int64_t w0 = (int64_t)c * kChunkWords + threadIdx.x * kWordsPerThread;
@@ -146,7 +159,10 @@ __global__ void __launch_bounds__(kBlock) k_bits_count(uint32_t* bits, int64_t w
   if (threadIdx.x == 0) {
     const int32_t n = lds[0] + lds[1] + lds[2] + lds[3];
     cnt[(int64_t)b * nch + c] = n;
-    if (n) atomicAdd(btot + b * kTotLanes + (c & (kTotLanes - 1)), n);
+    if (n)
+      atomicAdd(tt.gtot + ((int64_t)b * tt.ngroups + c / kGroupChunks) * kTotLanes +
+                    (c & (kTotLanes - 1)),
+                n);
   }
 }
 
@@ -175,7 +191,7 @@ __device__ __forceinline__ void block_sum3(int64_t (&v)[3], int64_t (*lds)[3]) {
 // launch).  Block (0, b) writes batch b's frontier and neighbour offsets;
 // block (0, 0) also the level's ends and capacity checks.
 __global__ void __launch_bounds__(kBlock) k_bits_emit(const uint32_t* bits, int64_t wpb,
-                                                      const int32_t* cnt, const int32_t* btot,
+                                                      const int32_t* cnt, Totals tt,
                                                       int32_t* ids, int64_t* frontier_off,
                                                       int64_t* nbr_off, LevelState* ls,
                                                       int64_t* need, int32_t* status,
@@ -189,13 +205,18 @@ __global__ void __launch_bounds__(kBlock) k_bits_emit(const uint32_t* bits, int6
   const u32x4 x = p[0], y = p[1];      // in flight while the offsets are summed
   const int64_t raw_base = a.lv == 0 ? 0 : ls->fend[a.lv - 1];
   const int64_t raw_nbase = a.lv == 0 ? 0 : ls->nend[a.lv - 1];
-  int64_t v[3] = {0, 0, 0};  // batches before b, all batches, chunks before c
-  for (int t = threadIdx.x; t < a.W * kTotLanes; t += kBlock) {
-    const int64_t x = btot[t];
+  int64_t v[3] = {0, 0, 0};  // batches before b, all batches (block (0, 0)), chunks of b before c
+  const int64_t per_batch = (int64_t)tt.ngroups * kTotLanes;
+  const int64_t upto = (b == 0 && c == 0) ? a.W * per_batch : b * per_batch;
+  for (int64_t t = threadIdx.x; t < upto; t += kBlock) {
+    const int64_t x = tt.gtot[t];
     v[1] += x;
-    if (t < b * kTotLanes) v[0] += x;
+    if (t < b * per_batch) v[0] += x;
   }
-  for (int t = threadIdx.x; t < c; t += kBlock) v[2] += cnt[(int64_t)b * nch + t];
+  const int g = c / kGroupChunks;
+  const int32_t* gb = tt.gtot + b * per_batch;
+  for (int t = threadIdx.x; t < g * kTotLanes; t += kBlock) v[2] += gb[t];
+  for (int t = g * kGroupChunks + threadIdx.x; t < c; t += kBlock) v[2] += cnt[(int64_t)b * nch + t];
   block_sum3(v, lds3);
   const int64_t cb = raw_base < a.fcap ? raw_base : a.fcap;
   if (threadIdx.x == 0) {
@@ -366,7 +387,9 @@ __global__ void __launch_bounds__(kBlock) k_sample(const RowT* row_ptr, const in
 
 struct SampleWs {
   int32_t* cnt;       // per (batch, chunk) counts of the current level
-  int32_t* btot;      // per (level, batch) totals, zeroed by k_zero_words
+  int32_t* tot;       // per level: group totals; zeroed by k_zero_words
+  int32_t ngroups;    // groups of kGroupChunks chunks per batch
+  int64_t tot_level;  // entries of tot per level
   LevelState* lvl;
   uint8_t* map;       // the last hop's byte map (32 * wpb bytes per batch), or null
 };
@@ -376,7 +399,9 @@ size_t sample_ws_layout(int64_t num_nodes, int32_t W, char* base, SampleWs* out)
   Carve cv{base, 0, ~(size_t)0};
   SampleWs s;
   s.cnt = cv.take<int32_t>((size_t)(W * nch));
-  s.btot = cv.take<int32_t>((size_t)(GG_MAX_LAYERS + 1) * GG_MAX_W * kTotLanes);
+  s.ngroups = (int32_t)std::max<int64_t>(1, cdiv(nch, kGroupChunks));
+  s.tot_level = (int64_t)W * kTotLanes * s.ngroups;
+  s.tot = cv.take<int32_t>((size_t)(GG_MAX_LAYERS + 1) * s.tot_level);
   s.lvl = cv.take<LevelState>(1);
   s.map = use_bytemap(num_nodes, W)
               ? cv.take<uint8_t>((size_t)W * (size_t)gg_bits_words(num_nodes) * 32)
@@ -451,8 +476,8 @@ extern "C" int gg_sample_window(const gg_csr_t* csr, const int32_t* seeds_d,
 
   const int64_t map4 = sw.map ? W * wpb * 2 : 0;   // 32 bytes per word, 16 per store
   hipLaunchKernelGGL(k_zero_words, dim3((unsigned)std::min<int64_t>(cdiv(W * wpb / 4, kBlock), 4096)),
-                     dim3(kBlock), 0, stream, out->frontier_bits, W * wpb / 4, sw.map, map4, sw.btot,
-                     (L + 1) * GG_MAX_W * kTotLanes);
+                     dim3(kBlock), 0, stream, out->frontier_bits, W * wpb / 4, sw.map, map4, sw.tot,
+                     (int32_t)((L + 1) * sw.tot_level));
   GG_LAUNCH_CHECK("k_zero_words");
   SeedOff so;
   for (int b = 0; b <= GG_MAX_W; ++b) so.off[b] = b <= W ? seed_off_h[b] : INT64_MAX;
@@ -493,9 +518,11 @@ extern "C" int gg_sample_window(const gg_csr_t* csr, const int32_t* seeds_d,
                    : launch_sample<int32_t>(csr, out, sw, status_d, a, bnd, stream);
       if (rc != GG_OK) return rc;
     }
-    int32_t* btot = sw.btot + (int64_t)lv * GG_MAX_W * kTotLanes;
+    Totals tt;
+    tt.gtot = sw.tot + (int64_t)lv * sw.tot_level;
+    tt.ngroups = sw.ngroups;
     hipLaunchKernelGGL(k_bits_count, dim3(nch, W), dim3(kBlock), 0, stream, out->frontier_bits, wpb,
-                       lv == L ? sw.map : nullptr, sw.cnt, btot);
+                       lv == L ? sw.map : nullptr, sw.cnt, tt);
     GG_LAUNCH_CHECK("k_bits_count");
     LevelArgs la;
     la.lv = lv;
@@ -507,7 +534,7 @@ extern "C" int gg_sample_window(const gg_csr_t* csr, const int32_t* seeds_d,
     la.fcap = out->frontier_cap;
     la.ncap = out->nbr_cap;
     hipLaunchKernelGGL(k_bits_emit, dim3(nch, W), dim3(kBlock), 0, stream, out->frontier_bits, wpb,
-                       sw.cnt, btot, out->frontier_ids, out->frontier_off, out->nbr_off, sw.lvl,
+                       sw.cnt, tt, out->frontier_ids, out->frontier_off, out->nbr_off, sw.lvl,
                        out->need, status_d, la);
     GG_LAUNCH_CHECK("k_bits_emit");
   }

@@ -27,6 +27,7 @@ GG_ERR_HIP = 3
 GG_ERR_UNSUPPORTED = 4
 
 GG_BUCKET_OWNER_ORDERED = 1
+GG_GATHER_SHARED = 1
 
 DEV_CAPACITY = 1
 DEV_BAD_ID = 2
@@ -117,8 +118,8 @@ SIGNATURES = {
     "gg_bucket_by_owner": (C.c_int, [_P, _P, _I64, _P, _I32, _P, _P, _P, _P, _SZ, _P]),
     "gg_stage_bulk": (C.c_int, [_P, _P, _I64, _P, _P, _P, _I64, _I64, _P, _P, _P, _P, _P, _P, _P,
                                 _P, _SZ, _P]),
-    "gg_gather_batch": (C.c_int, [_P, _P, _I32, _I64, _P, _P, _P, _I64, _I64, _P, _P, _I64, _P,
-                                  _P, _P, _SZ, _P]),
+    "gg_gather_batch": (C.c_int, [_P, _P, _I32, _I64, _P, _P, _P, _I64, _I64, _P, _P, _I64, _I32,
+                                  _P, _P, _P, _SZ, _P]),
     "gg_sim_accumulate": (C.c_int, [_P, _P, _I32, _P, _P, _P, _P]),
     "gg_ws_sage": (_SZ, [_I64, _I32, _I64, _I32, _P]),
     "gg_sage_forward": (C.c_int, [_P, _I64, _I32, _I32, _P, _P, _I32, _I64, _I64, _P, _P, _I64, _P,
@@ -282,12 +283,13 @@ def gg_stage_bulk(bucket_ids, owner_off, cap, part, feat, cache, cache_stride, c
 
 
 def gg_gather_batch(in_ids, bounds_ptr, nseg, n_cap, part, feat, cache, cache_stride, cache_rows,
-                    slot_of, out, out_stride, stats_ptr, status, ws, stream=None):
+                    slot_of, out, out_stride, stats_ptr, status, ws, stream=None, flags=0):
     """bounds_ptr and stats_ptr are raw device addresses (e.g. an offset into
-    frontier_off, or into an array of nseg statistics structures)."""
+    frontier_off, or into an array of nseg statistics structures).  flags =
+    GG_GATHER_SHARED when other streams sample on the device meanwhile."""
     return check(lib.gg_gather_batch(_ptr(in_ids), bounds_ptr, nseg, n_cap, C.byref(part),
                                      C.byref(feat), _ptr(cache), cache_stride, cache_rows,
-                                     _ptr(slot_of), _ptr(out), out_stride, stats_ptr,
+                                     _ptr(slot_of), _ptr(out), out_stride, flags, stats_ptr,
                                      _ptr(status), _ptr(ws), ws.numel(), _stream(stream)),
                  "gg_gather_batch")
 

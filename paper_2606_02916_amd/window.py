@@ -283,14 +283,17 @@ class FetchPipeline:
 
 
 class LookaheadPipeline:
-    """Pipelined runtime on two streams: the build stream samples window k
-    and forms its hot set and owner buckets; the fetch stream rebuilds the
-    cache (delta staging from window k-1's cache) and then gathers the
-    window.  Window k+1 is built while window k is staged and gathered, so a
-    window costs about the longer of the two streams' work instead of the
-    sum.  (Staging and gathering on separate streams gained nothing: both
-    are bound by HBM bandwidth, and every cross-stream wait costs a few
-    microseconds in the queues.)
+    """Pipelined runtime: the build stream samples window k and forms its
+    hot set and owner buckets; the fetch stream rebuilds the cache (delta
+    staging from window k-1's cache) and then gathers the window.  Window
+    k+1 is built while window k is staged and gathered, so a window costs
+    about the longer of the two streams' work instead of the sum.  Staging
+    and gathering share a stream when every shard is in device memory: both
+    are bound by HBM bandwidth, so they gain nothing from overlapping, and
+    every cross-stream wait costs a few microseconds in the queues.  When
+    shards live in pinned host memory, staging is bound by PCIe instead,
+    and the gather gets a stream of its own so that it runs beside the next
+    window's staging.
 
     `nsets` buffer sets rotate over the windows (window k uses set
     k mod nsets).  Building window k waits for the gather of window
@@ -334,7 +337,13 @@ class LookaheadPipeline:
         self.status = torch.zeros(1, dtype=torch.int32, device=dev)
         self.build_stream = torch.cuda.Stream(device=dev)
         self.fetch_stream = torch.cuda.Stream(device=dev)
+        # Staging that reads shards in pinned host memory is bound by PCIe,
+        # not HBM: the gather then gets a stream of its own, so that it runs
+        # beside the next window's staging.
+        on_host = any(t is not None and not t.is_cuda for t in shards)
+        self.gather_stream = torch.cuda.Stream(device=dev) if on_host else self.fetch_stream
         self.built = [torch.cuda.Event() for _ in range(self.nsets)]
+        self.staged = [torch.cuda.Event() for _ in range(self.nsets)]
         self.gathered = [torch.cuda.Event() for _ in range(self.nsets)]
         self.k = 0
 
@@ -389,42 +398,47 @@ class LookaheadPipeline:
         _rec(ev[4], fs)
         if gather_events is not None:
             gather_events[0].record(fs)
+        gs = self.gather_stream
+        if gs is not fs:
+            self.staged[X].record(fs)
+            gs.wait_event(self.staged[X])
         o = cur.win_out if out is None else out
         bounds = cur.frontier_off.data_ptr() + 8 * (self.L * Wk)
         gg.gg_gather_batch(cur.frontier_ids, bounds, Wk, o.shape[0], self.part, self.feat,
                            cur.cache, self.cache_stride, g.hot_cap, cur.slot_of, o, self.stride,
                            cur.gather_stats.data_ptr(), self.status, self.gather_ws,
-                           stream=fs.cuda_stream)
+                           stream=gs.cuda_stream, flags=gg.GG_GATHER_SHARED)
         if gather_events is not None:
-            gather_events[1].record(fs)
-        if sim is not None:           # simulator totals, in window order on the fetch stream
+            gather_events[1].record(gs)
+        if sim is not None:           # simulator totals, in window order on the gather stream
             gg.gg_sim_accumulate(cur.stage_stats, cur.gather_stats.data_ptr(), Wk, self.part,
-                                 sim[0], sim[1], stream=fs.cuda_stream)
+                                 sim[0], sim[1], stream=gs.cuda_stream)
         if consumer is not None:      # reads the set's sampling outputs and rows
-            _rec(consumer_events[0] if consumer_events else None, fs)
-            consumer.forward(cur, Wk, o, self.stride, self.status, stream=fs.cuda_stream)
-            _rec(consumer_events[1] if consumer_events else None, fs)
-        self.gathered[X].record(fs)
+            _rec(consumer_events[0] if consumer_events else None, gs)
+            consumer.forward(cur, Wk, o, self.stride, self.status, stream=gs.cuda_stream)
+            _rec(consumer_events[1] if consumer_events else None, gs)
+        self.gathered[X].record(gs)
         self.k += 1
         return Wk, cur
 
     def regather(self, bufs, Wk, out=None, stream=None):
         """Launches the gather of a finished window again (same inputs, same
-        output) on `stream` (default: the caller's current stream), e.g. to
-        time it with the chip to itself.  The window must be complete."""
+        output, same flags) on `stream` (default: the caller's current
+        stream), e.g. to time it with the chip to itself.  The window must be
+        complete."""
         o = bufs.win_out if out is None else out
         bounds = bufs.frontier_off.data_ptr() + 8 * (self.L * Wk)
         gg.gg_gather_batch(bufs.frontier_ids, bounds, Wk, o.shape[0], self.part, self.feat,
                            bufs.cache, self.cache_stride, self.geo.hot_cap, bufs.slot_of, o,
                            self.stride, bufs.gather_stats.data_ptr(), self.status,
-                           self.gather_ws, stream=stream)
+                           self.gather_ws, stream=stream, flags=gg.GG_GATHER_SHARED)
         return o
 
     def gathered_event(self, k):
         return self.gathered[k % self.nsets]
 
     def synchronize(self):
-        for s in (self.build_stream, self.fetch_stream):
+        for s in (self.build_stream, self.fetch_stream, self.gather_stream):
             s.synchronize()
 
     def read_status(self):

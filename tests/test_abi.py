@@ -160,6 +160,10 @@ def test_bad_arguments_are_rejected_on_the_host(gg):
         gg.gg_gather_batch(t, t.data_ptr(), 0, 10, part, feat, t, 256, 10, t, t, 256,
                            t.data_ptr(), t, t, stream=0)
     assert "nseg" in gg.gg_last_error()
+    with pytest.raises(gg.GGError):                                      # unknown gather flag
+        gg.gg_gather_batch(t, t.data_ptr(), 1, 10, part, feat, t, 256, 10, t, t, 256,
+                           t.data_ptr(), t, t, stream=0, flags=2)
+    assert "flags" in gg.gg_last_error()
     c = gg.make_sim_coeffs(4, 1.0, 0.01, 1e-3, 1e-5, 0.0, 256, 30.0)    # no bandwidth ceiling
     with pytest.raises(gg.GGError):
         gg.gg_sim_accumulate(t, t.data_ptr(), 4, part, c, t, stream=0)
