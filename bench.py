@@ -356,13 +356,22 @@ def main():
     rows = sum(rows_w[k] for k in order)
     value = rows / elapsed
 
+    # Under the look-ahead the gather follows staging on the fetch stream, or
+    # (shards in host memory) runs on a stream of its own after staging.
+    own_gather_stream = look and pipe.gather_stream is not pipe.fetch_stream
+
     def gather_ms(gevs, i, b=None):
         """Duration of gather launch b of step i (all launches when b is
-        None), between HIP events on the stream the gather runs on."""
+        None).  Its start event is recorded where its window's staging ends;
+        on a stream of its own the gather starts at the later of that and
+        the previous gather's end."""
         if b is None:
             return sum(gather_ms(gevs, i, j) for j in range(len(gevs[i])))
         s, e = gevs[i][b]
-        return s.elapsed_time(e)
+        t = s.elapsed_time(e)
+        if own_gather_stream and i > 0:
+            t = min(t, gevs[i - 1][-1][1].elapsed_time(e))
+        return t
 
     g_ms, g_bytes, n_launch = 0.0, 0, 0
     stage_ms = {"sample": [], "hotset": [], "bucket": [], "stage": [], "gathers": []}
@@ -371,11 +380,13 @@ def main():
         e = evs[i]
         for name, (a, b) in zip(stage_ms, [(0, 1), (1, 2), (2, 3)]):
             stage_ms[name].append(e[a].elapsed_time(e[b]))
-        # staging starts once its window is built and, under the look-ahead,
-        # the previous window's gather (same stream) has ended
+        # staging starts once its window is built and the fetch stream's
+        # previous work has ended: the previous window's gather, or its
+        # staging when the gather has a stream of its own
         t_st = e[3].elapsed_time(e[4])
         if look and i > 0:
-            t_st = min(t_st, gevs[i - 1][-1][1].elapsed_time(e[4]))
+            prev = evs[i - 1][4] if own_gather_stream else gevs[i - 1][-1][1]
+            t_st = min(t_st, prev.elapsed_time(e[4]))
         stage_ms["stage"].append(t_st)
         stage_ms["gathers"].append(gather_ms(gevs, i))
         st_ms += t_st
