@@ -9,6 +9,7 @@
 // place from those counts.  Deduplication therefore costs streaming passes
 // over N/8 bytes per batch and hop instead of a sort of the sampled ids.
 #include <limits.h>
+#include <stdlib.h>
 
 #include "gg_host.hpp"
 
@@ -51,10 +52,15 @@ struct SampleArgs {
 // random atomic, and folding the map into the bit sets is one streaming
 // pass.  Above it (the 111M-node graph) the pass would cost more than the
 // atomics it saves.
+// GG_BYTEMAP_MAX_MB overrides the limit (0 turns the map off); it is read
+// at every call and must not change between gg_ws_sample and the calls
+// that use that workspace.
 constexpr int64_t kByteMapMaxBytes = 512LL << 20;
 
 inline bool use_bytemap(int64_t num_nodes, int32_t W) {
-  return (int64_t)W * gg_bits_words(num_nodes) * 32 <= kByteMapMaxBytes;
+  const char* e = getenv("GG_BYTEMAP_MAX_MB");
+  const int64_t lim = (e && *e) ? (int64_t)atoll(e) << 20 : kByteMapMaxBytes;
+  return (int64_t)W * gg_bits_words(num_nodes) * 32 <= lim;
 }
 
 // Largest b in [0, 64) with off[b] <= x, for a table padded with INT64_MAX.
