@@ -153,6 +153,24 @@ def test_wide_rows_with_misses(n_hot):
         w.run_and_compare(k)
 
 
+@pytest.mark.parametrize("n_hot", [-1, 200])
+def test_every_limit_at_once(n_hot):
+    """The ABI's limits together: W = 64 batches (of 16 seeds), L = 4 hops
+    with a fan-out of 32 at the first (the widest Floyd network), and 64
+    owners by node id mod 64 with local owner 5; with the union and with a
+    budget (the miss path over 64 owners)."""
+    log(f"tiny graph: W=64, L=4, fanout [32,3,2,1], 64 owners (mod), local 5, n_hot={n_hot}")
+    import dataclasses
+    base = synth.instance("tiny")
+    wl = dataclasses.replace(base.wl, name="tiny_limits", num_parts=64, local_owner=5,
+                             fanout=(32, 3, 2, 1), batch_size=16, W=64)
+    shards = [synth.shard_features(wl, m) for m in range(wl.num_parts)]
+    inst = synth.Instance(wl, base.row_ptr, base.col_idx, *synth.seed_batches(wl), shards, None)
+    w = world(inst, n_hot=n_hot)
+    r = w.run_and_compare(0)
+    assert r["Wk"] == 64
+
+
 def test_repeat_runs_are_identical():
     log("small: determinism across two pipelines")
     inst = synth.instance("small")
