@@ -34,28 +34,29 @@ constexpr int kRankChunk = 2048;         // bit-set words per rank chunk (divide
 // Rank of a node in its batch's N_b bit set.
 // ---------------------------------------------------------------------------
 
-// pre[w] = set bits of the words before w inside w's chunk; csum[b][c] =
-// bits of chunk c of batch b.
+// rank[w] = {set bits of the words before w inside w's chunk, word w}: the
+// word travels with its prefix so that a rank lookup is one 8-byte load;
+// csum[b][c] = bits of chunk c of batch b.
 __global__ void __launch_bounds__(kSageBlock) k_rank_local(const uint32_t* bits, int64_t wpb,
-                                                           int64_t nch, int32_t* pre,
+                                                           int64_t nch, int2* rank,
                                                            int32_t* csum) {
   __shared__ int32_t lds[kSageBlock / kWave];
   const int b = blockIdx.y;
   const int64_t c = blockIdx.x;
   const int64_t w0 = (int64_t)b * wpb + c * kRankChunk + (int64_t)threadIdx.x * 8;
-  int32_t cnt[8];
+  uint32_t wd[8];
   int32_t s = 0;
 #pragma unroll
   for (int j = 0; j < 8; ++j) {
-    cnt[j] = __popc(bits[w0 + j]);
-    s += cnt[j];
+    wd[j] = bits[w0 + j];
+    s += __popc(wd[j]);
   }
   int32_t tot;
   int32_t run = block_excl_scan<kSageBlock>(s, lds, &tot);
 #pragma unroll
   for (int j = 0; j < 8; ++j) {
-    pre[w0 + j] = run;
-    run += cnt[j];
+    rank[w0 + j] = make_int2(run, (int32_t)wd[j]);
+    run += __popc(wd[j]);
   }
   if (threadIdx.x == 0) csum[(int64_t)b * nch + c] = tot;
 }
@@ -228,8 +229,7 @@ struct AggArgs {
   int64_t out_cap;
   // rank lookup in the N_b bit sets (input level = N_b), else binary search
   int32_t use_rank;
-  const uint32_t* bits;
-  const int32_t* pre;
+  const int2* rank;     // {prefix in chunk, word} per bit-set word
   const int32_t* cpre;
   int64_t wpb;
   int64_t nch;
@@ -254,9 +254,11 @@ __device__ __forceinline__ int32_t row_in_level(const AggArgs& a, int b, const i
     const int64_t wi = (int64_t)(uint32_t)u >> 5;
     if (u < 0 || wi >= a.wpb) return -1;
     const int64_t w = (int64_t)b * a.wpb + wi;
-    const uint32_t word = a.bits[w], bit = 1u << (u & 31);
+    const int2 rw = a.rank[w];
+    const int32_t cpre = a.cpre[(int64_t)b * a.nch + wi / kRankChunk];
+    const uint32_t word = (uint32_t)rw.y, bit = 1u << (u & 31);
     if (!(word & bit)) return -1;
-    p = (int64_t)a.pre[w] + a.cpre[(int64_t)b * a.nch + wi / kRankChunk] + __popc(word & (bit - 1u));
+    p = (int64_t)rw.x + cpre + __popc(word & (bit - 1u));
     if (p >= nin) return -1;
   } else {
     p = find_sorted(Fin, nin, u);
@@ -266,7 +268,10 @@ __device__ __forceinline__ int32_t row_in_level(const AggArgs& a, int b, const i
 
 // Grid (blocks, W): block column b serves batch b.  Sixteen lanes per output
 // node: lane j of the group resolves neighbour slots j and j + 16, then the
-// group sums the projected neighbour rows, 16 columns at a time.
+// group sums the projected neighbour rows, 16 columns at a time.  The
+// neighbour loop is unrolled to KMAX >= k so that all of a column's row
+// loads are in flight together; the sum still runs in slot order.
+template <int KMAX>
 __global__ void __launch_bounds__(kSageBlock) k_sage_aggregate(AggArgs a, int32_t* status) {
   const int b = blockIdx.y;
   const int64_t sout = (int64_t)a.lvl * a.W + b, sin = sout + a.W;
@@ -304,22 +309,30 @@ __global__ void __launch_bounds__(kSageBlock) k_sage_aggregate(AggArgs a, int32_
     if (zrow0 + pv >= a.z_cap) pv = -1;
     if (p0 >= 0 && zrow0 + p0 >= a.z_cap) p0 = -1;
     if (p1 >= 0 && zrow0 + p1 >= a.z_cap) p1 = -1;
+    int32_t pt[KMAX];
     int cnt = 0;
-    for (int t = 0; t < a.k; ++t) {
-      const int32_t p = __shfl(t < 16 ? p0 : p1, gbase + (t & 15), kWave);
-      cnt += p >= 0;
+#pragma unroll
+    for (int t = 0; t < KMAX; ++t) {
+      pt[t] = __shfl(t < 16 ? p0 : p1, gbase + (t & 15), kWave);
+      if (t >= a.k) pt[t] = -1;
+      cnt += pt[t] >= 0;
     }
     const float inv = cnt ? 1.0f / (float)cnt : 0.f;
     const int64_t orow = orow0 + i;
     for (int c0 = 0; c0 < a.d_out; c0 += 16) {
       const int c = c0 + sl;
+      const bool cok = c < a.d_out;
+      const float self = (cok && pv >= 0) ? a.z[(zrow0 + pv) * a.ldz + c] : 0.f;
+      float v[KMAX];
+#pragma unroll
+      for (int t = 0; t < KMAX; ++t)
+        v[t] = (cok && pt[t] >= 0) ? a.z[(zrow0 + pt[t]) * a.ldz + a.d_out + c] : 0.f;
       float sum = 0.f;
-      for (int t = 0; t < a.k; ++t) {
-        const int32_t p = __shfl(t < 16 ? p0 : p1, gbase + (t & 15), kWave);
-        if (p >= 0 && c < a.d_out) sum += a.z[(zrow0 + p) * a.ldz + a.d_out + c];
-      }
-      if (c < a.d_out && pv >= 0) {
-        float y = a.z[(zrow0 + pv) * a.ldz + c] + sum * inv + (a.bias ? a.bias[c] : 0.f);
+#pragma unroll
+      for (int t = 0; t < KMAX; ++t)
+        if (pt[t] >= 0) sum += v[t];
+      if (cok && pv >= 0) {
+        float y = self + sum * inv + (a.bias ? a.bias[c] : 0.f);
         if (a.relu && y < 0.f) y = 0.f;
         if (orow < a.out_cap) a.out[orow * a.d_out + c] = y;
       }
@@ -339,7 +352,7 @@ int ldz_tiles(int32_t d_out) {
 struct SageWs {
   float* z;
   float* h[2];
-  int32_t* pre;
+  int2* rank;
   int32_t* csum;
 };
 
@@ -357,9 +370,9 @@ size_t sage_ws_layout(int64_t num_nodes, int32_t W, int64_t rows_cap, int32_t L,
   float* z = cv.take<float>(r * (size_t)ntmax * 16);
   float* h0 = cv.take<float>(r * (size_t)dmax);
   float* h1 = cv.take<float>(r * (size_t)dmax);
-  int32_t* pre = cv.take<int32_t>((size_t)W * (size_t)wpb);
+  int2* rank = cv.take<int2>((size_t)W * (size_t)wpb);
   int32_t* csum = cv.take<int32_t>((size_t)W * (size_t)std::max<int64_t>(nch, 1));
-  if (out) *out = SageWs{z, {h0, h1}, pre, csum};
+  if (out) *out = SageWs{z, {h0, h1}, rank, csum};
   return align_up(cv.used, 256);
 }
 
@@ -440,7 +453,7 @@ extern "C" int gg_sage_forward(const gg_wsample_t* smp, int64_t num_nodes, int32
 
   // ranks in the N_b bit sets
   hipLaunchKernelGGL(k_rank_local, dim3((unsigned)nch, W), dim3(kSageBlock), 0, stream,
-                     smp->frontier_bits, wpb, nch, sw.pre, sw.csum);
+                     smp->frontier_bits, wpb, nch, sw.rank, sw.csum);
   GG_LAUNCH_CHECK("k_rank_local");
   hipLaunchKernelGGL(k_rank_chunks, dim3(W), dim3(kSageBlock), 0, stream, sw.csum, nch);
   GG_LAUNCH_CHECK("k_rank_chunks");
@@ -509,13 +522,19 @@ extern "C" int gg_sage_forward(const gg_wsample_t* smp, int64_t num_nodes, int32
       aa.out_cap = out_rows_cap;
     }
     aa.use_rank = j == 1 ? 1 : 0;   // the first layer's input level is N_b
-    aa.bits = smp->frontier_bits;
-    aa.pre = sw.pre;
+    aa.rank = sw.rank;
     aa.cpre = sw.csum;
     aa.wpb = wpb;
     aa.nch = nch;
-    hipLaunchKernelGGL(k_sage_aggregate, dim3(agg_bx, W), dim3(kSageBlock), 0, stream, aa,
-                       status_d);
+    if (aa.k <= 8)
+      hipLaunchKernelGGL(k_sage_aggregate<8>, dim3(agg_bx, W), dim3(kSageBlock), 0, stream, aa,
+                         status_d);
+    else if (aa.k <= 16)
+      hipLaunchKernelGGL(k_sage_aggregate<16>, dim3(agg_bx, W), dim3(kSageBlock), 0, stream, aa,
+                         status_d);
+    else
+      hipLaunchKernelGGL(k_sage_aggregate<32>, dim3(agg_bx, W), dim3(kSageBlock), 0, stream, aa,
+                         status_d);
     GG_LAUNCH_CHECK("k_sage_aggregate");
   }
   return GG_OK;
