@@ -203,6 +203,12 @@ def main():
                     help="with --simulate: budgets relative to each window, e.g. 1/10,1/4: the "
                          "top fraction of the window's distinct remote nodes; the hit ratio is "
                          "then the share of remote requests that fraction covers")
+    ap.add_argument("--ablation", action="store_true",
+                    help="measure per-row requests against bulk requests, rows per wavefront "
+                         "copy step, and (host-resident shards) zero-copy staging against "
+                         "pack + DMA, on the first window; prints one JSON line")
+    ap.add_argument("--ablation-rows", type=int, default=100_000,
+                    help="with --ablation: staged rows copied one request each")
     ap.add_argument("--summarize", action="store_true",
                     help="write profiles/ summaries from rocprofv3 databases instead of running")
     ap.add_argument("--trace-db", default=None)
@@ -241,6 +247,8 @@ def main():
         return wsweep(args, wl)
     if args.simulate:
         return simulate(args, wl)
+    if args.ablation:
+        return ablation(args, wl)
     W = args.W or wl.W
     t = time.time()
     inst, row_ptr_d, col_idx_d, shards_d = synth.torch_instance(args.config, dev)
@@ -514,6 +522,232 @@ def pcie_h2d_gbps(dev):
         best = min(best, e0.elapsed_time(e1))
     del a, b
     return (1 << 30) / (best * 1e-3) / 1e9
+
+
+def _hip_runtime():
+    """The HIP runtime this process already uses (torch and libgg bind the
+    same one), opened again by the path it is mapped from."""
+    import ctypes as C
+    paths = set()
+    with open("/proc/self/maps") as f:
+        for line in f:
+            parts = line.split()
+            if len(parts) >= 6 and os.path.basename(parts[5]).startswith("libamdhip64.so"):
+                paths.add(parts[5])
+    if len(paths) != 1:
+        raise RuntimeError(f"expected one mapped HIP runtime, found {sorted(paths)}")
+    hip = C.CDLL(paths.pop())
+    hip.hipMemcpyAsync.restype = C.c_int
+    hip.hipMemcpyAsync.argtypes = [C.c_void_p, C.c_void_p, C.c_size_t, C.c_int, C.c_void_p]
+    return hip
+
+
+def ablation(args, wl):
+    """Measurements of three design choices on the workload's first window
+    (built twice first, so everything is warm):
+    - requests: one hipMemcpyAsync per staged row, on an evenly spaced
+      sample of the window's hot set, against the staging call on the same
+      rows (one bulk request per owner);
+    - tile: rows a wavefront takes per copy step in the gather and the
+      stage (1 = one wavefront per row);
+    - host shards only: zero-copy staging (the kernel reads pinned host
+      memory) against packing each owner's rows on the host plus one DMA
+      per owner.
+    Every variant's bytes are compared with the staging call's."""
+    import numpy as np
+    import torch
+
+    import synth
+    from paper_2606_02916_amd import FetchPipeline, gg
+
+    dev = torch.device("cuda:0")
+    inst, row_ptr_d, col_idx_d, shards_d = synth.torch_instance(args.config, dev)
+    P, W, rb, stride = wl.num_parts, args.W or wl.W, wl.row_bytes, wl.row_stride
+    pipe = FetchPipeline(row_ptr_d, col_idx_d, P, wl.part_kind, wl.local_owner, inst.range_start,
+                         shards_d, [s.shape[0] for s in inst.shards], rb, stride, W, wl.fanout,
+                         wl.batch_size, device=dev)
+    seeds_d = torch.from_numpy(inst.seeds).to(dev)
+    boff = inst.batch_off
+    b0, b1 = synth.window_batches(boff, W, 0)
+    so = boff[b0:b1 + 1] - boff[b0]
+    seeds = seeds_d[boff[b0]:boff[b1]]
+    for _ in range(2):
+        pipe.reset_cache()
+        Wk = pipe.window(seeds, so, b0)
+    torch.cuda.synchronize()
+    if pipe.read_status() != 0:
+        raise RuntimeError(f"device status {pipe.read_status()}")
+    cur = (pipe.k - 1) & 1
+    H = int(pipe.hot_count[cur][0].item())
+    bucket, owner_off, cache = pipe.bucket_ids[cur], pipe.owner_off, pipe.staged_cache()
+    g = [pipe.buf.gather_stats_dict(b) for b in range(Wk)]
+    g_rows = sum(x["rows"] for x in g)
+    g_bytes = sum(x["rows"] * (2 * rb + 4) + (x["hits"] + x["misses"]) * 4 for x in g)
+    s_bytes = H * (2 * rb + 8)
+    mk = lambda: torch.cuda.Event(enable_timing=True)  # noqa: E731
+    log(f"{args.config}: window 0 has {g_rows} rows, hot set {H}")
+
+    def timed(fn, reps):
+        ts = []
+        for _ in range(reps):
+            e0, e1 = mk(), mk()
+            e0.record()
+            fn()
+            e1.record()
+            torch.cuda.synchronize()
+            ts.append(e0.elapsed_time(e1))
+        return float(np.median(ts))
+
+    def stage(ids, off, n, out, slot, stats):
+        gg.gg_stage_bulk(ids, off, n, pipe.part, pipe.feat, out, stride, n, slot, None, None,
+                         None, None, stats, pipe.status, pipe.ws)
+
+    def stage_full():
+        stage(bucket, owner_off, pipe.hot_cap, cache, pipe.slot_of, pipe.stage_stats)
+
+    res = {}
+    # -- per-row requests against one bulk request per owner ---------------
+    off_h = owner_off.cpu().numpy()
+    pick = np.unique(np.linspace(0, H - 1, min(args.ablation_rows, H)).astype(np.int64))
+    n = len(pick)
+    own = np.searchsorted(off_h, pick, side="right") - 1
+    u = bucket[:H].cpu().numpy()[pick].astype(np.int64)
+    if wl.part_kind == synth.PART_RANGE:
+        rows = u - np.asarray(inst.range_start, dtype=np.int64)[own]
+    else:
+        rows = u // P
+    base = np.array([shards_d[m].data_ptr() for m in range(P)], dtype=np.int64)
+    src = (base[own] + rows * stride).tolist()
+    dst = torch.empty((n, stride), dtype=torch.uint8, device=dev)
+    dl = (dst.data_ptr() + np.arange(n, dtype=np.int64) * stride).tolist()
+    hip = _hip_runtime()
+    hs = torch.cuda.current_stream().cuda_stream
+
+    def per_row(k):
+        for j in range(k):
+            rc = hip.hipMemcpyAsync(dl[j], src[j], rb, 4, hs)   # hipMemcpyDefault
+            if rc:
+                raise RuntimeError(f"hipMemcpyAsync returned {rc}")
+
+    per_row(min(n, 2000))
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(n):
+        gg.lib.gg_version()
+    loop_us = (time.perf_counter() - t0) / n * 1e6
+    e0, e1 = mk(), mk()
+    t0 = time.perf_counter()
+    e0.record()
+    per_row(n)
+    t_enq = time.perf_counter()
+    e1.record()
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    sub_ids = torch.from_numpy(u.astype(np.int32)).to(dev)
+    cnt = np.bincount(own, minlength=P)
+    sub_off = torch.from_numpy(np.concatenate([[0], np.cumsum(cnt)]).astype(np.int64)).to(dev)
+    sub_cache = torch.empty((n, stride), dtype=torch.uint8, device=dev)
+    sub_slot = torch.full((wl.num_nodes,), -1, dtype=torch.int32, device=dev)
+    sub_stats = torch.zeros(gg.STAGE_STATS_BYTES, dtype=torch.uint8, device=dev)
+    bulk_ms = timed(lambda: stage(sub_ids, sub_off, n, sub_cache, sub_slot, sub_stats), 20)
+    ss = gg.stage_stats_from_bytes(sub_stats.cpu().numpy().tobytes(), P)
+    same = bool(torch.equal(dst[:, :rb], sub_cache[:, :rb]))
+    if not same:
+        raise RuntimeError("per-row copies differ from the staging call")
+    res["requests"] = {
+        "rows": n, "row_bytes": rb,
+        "per_row": {"requests": n, "wall_ms": round((t1 - t0) * 1e3, 3),
+                    "enqueue_us_per_request": round((t_enq - t0) / n * 1e6, 3),
+                    "host_loop_us_per_call": round(loop_us, 3),
+                    "gpu_span_ms": round(e0.elapsed_time(e1), 3),
+                    "rows_per_s": round(n / (t1 - t0), 1)},
+        "bulk": {"requests": ss["requests_total"], "ms": round(bulk_ms, 4),
+                 "rows_per_s": round(n / (bulk_ms * 1e-3), 1)},
+        "speedup": round((t1 - t0) / (bulk_ms * 1e-3), 1)}
+    log(json.dumps(res["requests"]))
+    del dst, sub_cache, sub_slot
+
+    # -- rows per wavefront copy step ---------------------------------------
+    def tile_rows(max_bytes):
+        t = 64
+        while t > 1 and t * rb > max_bytes:
+            t //= 2
+        return t
+
+    defaults = {"gather": tile_rows(8192), "stage": tile_rows(32768)}
+    ref_out, ref_cache, tiles = None, None, []
+    try:
+        for t in sorted({64, 16, 4, 1, *defaults.values()}, reverse=True):
+            os.environ["GG_TILE_ROWS"] = str(t)
+            gm = timed(lambda: pipe.gather_window(Wk), 10)
+            sm = timed(stage_full, 10)
+            out = pipe.win_out[:g_rows, :rb]
+            if ref_out is None:
+                ref_out, ref_cache = out.clone(), cache[:H, :rb].clone()
+            elif not (torch.equal(out, ref_out) and torch.equal(cache[:H, :rb], ref_cache)):
+                raise RuntimeError(f"rows differ with {t} rows per wave step")
+            tiles.append({"rows_per_wave_step": t,
+                          "default_for": [k for k, v in defaults.items() if v == t],
+                          "gather_ms": round(gm, 4),
+                          "gather_GBps": round(g_bytes / (gm * 1e-3) / 1e9, 1),
+                          "stage_ms": round(sm, 4),
+                          "stage_GBps": round(s_bytes / (sm * 1e-3) / 1e9, 1)})
+            log(json.dumps(tiles[-1]))
+    finally:
+        os.environ.pop("GG_TILE_ROWS", None)
+    res["tile"] = tiles
+    del ref_out, ref_cache
+
+    # -- host shards: zero-copy against pack + DMA --------------------------
+    host = [m for m in range(P) if not shards_d[m].is_cuda]
+    if host:
+        zc_ms = timed(stage_full, 5)
+        full_own = np.searchsorted(off_h, np.arange(H), side="right") - 1
+        u_all = bucket[:H].cpu().numpy().astype(np.int64)
+        r_all = u_all - np.asarray(inst.range_start, dtype=np.int64)[full_own] \
+            if wl.part_kind == synth.PART_RANGE else u_all // P
+        host_rows = int(sum(off_h[m + 1] - off_h[m] for m in host))
+        pack = torch.empty((max(host_rows, 1), stride), dtype=torch.uint8, pin_memory=True)
+        dma = torch.empty((max(host_rows, 1), stride), dtype=torch.uint8, device=dev)
+        idx = {m: torch.from_numpy(r_all[off_h[m]:off_h[m + 1]]) for m in host}
+        best = None
+        for _ in range(3):
+            t0 = time.perf_counter()
+            o = 0
+            for m in host:
+                k = len(idx[m])
+                torch.index_select(shards_d[m], 0, idx[m], out=pack[o:o + k])
+                o += k
+            t_pack = time.perf_counter() - t0
+            e0, e1 = mk(), mk()
+            e0.record()
+            o = 0
+            for m in host:
+                k = len(idx[m])
+                dma[o:o + k].copy_(pack[o:o + k], non_blocking=True)
+                o += k
+            e1.record()
+            torch.cuda.synchronize()
+            t_all = time.perf_counter() - t0
+            r = (t_all, t_pack, e0.elapsed_time(e1))
+            best = r if best is None or r[0] < best[0] else best
+        o = 0
+        for m in host:
+            k = len(idx[m])
+            if not torch.equal(dma[o:o + k, :rb], cache[off_h[m]:off_h[m] + k, :rb]):
+                raise RuntimeError(f"packed rows of owner {m} differ from the staged cache")
+            o += k
+        res["host_staging"] = {
+            "host_rows": host_rows, "owners": host, "pack_threads": torch.get_num_threads(),
+            "zero_copy_stage_ms": round(zc_ms, 3),
+            "zero_copy_note": "the whole staging call, device-resident owners included",
+            "pack_ms": round(best[1] * 1e3, 3), "dma_ms": round(best[2], 3),
+            "pack_dma_ms": round(best[0] * 1e3, 3),
+            "dma_GBps": round(host_rows * stride / (best[2] * 1e-3) / 1e9, 1)}
+        log(json.dumps(res["host_staging"]))
+        del pack, dma
+    print(json.dumps({"ablation": args.config, "W": W, "window_rows": g_rows, "hot_set": H,
+                      **res}), flush=True)
 
 
 def wsweep(args, wl):

@@ -390,6 +390,17 @@ int gg_sage_forward(const gg_wsample_t* smp, int64_t num_nodes, int32_t W, int32
                     int32_t* status_d, void* ws, size_t ws_bytes, hipStream_t stream);
 
 /* Helpers. */
+
+/* Reads the sticky device status word once the work queued so far on
+ * `stream` has finished: the one call of the library that waits, meant for
+ * the once-per-window check of data-dependent failures (the caller's side
+ * of the per-window barrier of Algorithm 1).  status_d: the int32 word
+ * passed to the other calls; *out_h receives its GG_DEV_* bits.  The word
+ * is not cleared.  Returns GG_ERR_ARG for a null pointer, GG_ERR_HIP when
+ * the copy or the wait fails (a fault of earlier work on the stream is
+ * reported here). */
+int gg_read_status(const int32_t* status_d, int32_t* out_h, hipStream_t stream);
+
 const char* gg_status_string(int32_t code);
 const char* gg_last_error(void);
 int gg_version(void);

@@ -77,6 +77,14 @@ int env_int(const char* name, int dflt) {
   return (v && *v) ? atoi(v) : dflt;
 }
 
+int32_t copy_tile(int32_t row_bytes, int32_t max_bytes) {
+  const int v = env_int("GG_TILE_ROWS", 0);
+  if (v <= 0) return tile_rows(row_bytes, max_bytes);
+  int32_t p = 1;
+  while (p * 2 <= v && p * 2 <= kWave) p *= 2;
+  return p;
+}
+
 int host_shards(const KFeat& f) {
   int n = 0;
   for (int m = 0; m < f.P; ++m) {
@@ -108,6 +116,19 @@ extern "C" {
 const char* gg_last_error(void) { return gg::g_err; }
 
 int gg_version(void) { return GG_VERSION; }
+
+int gg_read_status(const int32_t* status_d, int32_t* out_h, hipStream_t stream) {
+  GG_REQUIRE(status_d && out_h, "gg_read_status: null pointer");
+  int32_t v = 0;
+  hipError_t e = hipMemcpyAsync(&v, status_d, sizeof(v), hipMemcpyDeviceToHost, stream);
+  if (e == hipSuccess) e = hipStreamSynchronize(stream);
+  if (e != hipSuccess) {
+    gg::set_error("gg_read_status: %s", hipGetErrorString(e));
+    return GG_ERR_HIP;
+  }
+  *out_h = v;
+  return GG_OK;
+}
 
 const char* gg_status_string(int32_t code) {
   switch (code) {

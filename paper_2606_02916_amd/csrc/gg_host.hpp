@@ -45,14 +45,19 @@ int pack_feat(const gg_feat_t* feat, const gg_part_t* part, KFeat* out);
 // Geometry of the row copy for row_bytes and the vector width vb (16 or 4).
 CopyGeom copy_geom(int32_t row_bytes, int vb);
 
-// Rows a wavefront takes per step of a row copy: 64 for rows up to 512
-// bytes, fewer for wider rows so that a window's rows still spread over
-// every wave of the grid (the largest power of two <= 32 KB / row_bytes).
-inline int32_t tile_rows(int32_t row_bytes) {
+// Rows a wavefront takes per step of a row copy: the largest power of two
+// up to 64 whose rows fit in max_bytes, so that wide rows still spread over
+// every wave of the grid.
+inline int32_t tile_rows(int32_t row_bytes, int32_t max_bytes) {
   int32_t t = 64;
-  while (t > 1 && (int64_t)t * row_bytes > 32768) t >>= 1;
+  while (t > 1 && (int64_t)t * row_bytes > max_bytes) t >>= 1;
   return t;
 }
+
+// tile_rows(row_bytes, max_bytes), or, when GG_TILE_ROWS is set (read at
+// every call), the largest power of two at most that and 64 (1 makes a
+// wavefront copy one row per step).
+int32_t copy_tile(int32_t row_bytes, int32_t max_bytes);
 
 inline bool aligned16(const void* p) { return ((uintptr_t)p & 15u) == 0; }
 

@@ -18,7 +18,7 @@ struct StageArgs {
   int64_t cap;         // bucket entries usable
   int64_t cache_rows;
   int64_t cache_stride;
-  int32_t tile;        // slots per wave step (tile_rows)
+  int32_t tile;        // slots per wave step (copy_tile)
   int32_t pad_;
   CopyGeom geom;
 };
@@ -258,7 +258,7 @@ extern "C" int gg_stage_bulk(const int32_t* bucket_ids_d, const int64_t* owner_o
   a.cap = cap;
   a.cache_rows = cache_rows;
   a.cache_stride = cache_stride;
-  a.tile = tile_rows(kf.row_bytes);
+  a.tile = copy_tile(kf.row_bytes, 32768);
   a.pad_ = 0;
   a.geom = copy_geom(kf.row_bytes, v16 ? 16 : 4);
   static const bool nt = env_flag("GG_NT_STAGE", false);

@@ -124,6 +124,7 @@ SIGNATURES = {
     "gg_ws_sage": (_SZ, [_I64, _I32, _I64, _I32, _P]),
     "gg_sage_forward": (C.c_int, [_P, _I64, _I32, _I32, _P, _P, _I32, _I64, _I64, _P, _P, _I64, _P,
                                   _P, _SZ, _P]),
+    "gg_read_status": (C.c_int, [_P, _P, _P]),
     "gg_status_string": (C.c_char_p, [_I32]),
     "gg_last_error": (C.c_char_p, []),
     "gg_version": (C.c_int, []),
@@ -348,6 +349,13 @@ def gg_sage_forward(wsample, num_nodes, W, fanout, x, x_dtype, x_stride, rows_ca
                                      x_dtype, x_stride, rows_cap, layers_arr, _ptr(out),
                                      out_rows_cap, _ptr(status), _ptr(ws), ws.numel(),
                                      _stream(stream)), "gg_sage_forward")
+
+
+def gg_read_status(status, stream=None):
+    """Waits for `stream` and returns the GG_DEV_* bits of the status word."""
+    out = C.c_int32(0)
+    check(lib.gg_read_status(_ptr(status), C.byref(out), _stream(stream)), "gg_read_status")
+    return int(out.value)
 
 
 def gg_status_string(code):

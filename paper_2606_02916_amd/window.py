@@ -259,7 +259,7 @@ class FetchPipeline:
 
     # -- host copies for checking ------------------------------------------
     def read_status(self):
-        return int(self.status.item())
+        return gg.gg_read_status(self.status)
 
     def sample_outputs(self, Wk):
         foff = self.frontier_off[:(self.L + 1) * Wk + 1].cpu().numpy()
@@ -443,7 +443,7 @@ class LookaheadPipeline:
 
     def read_status(self):
         self.synchronize()
-        return int(self.status.item())
+        return gg.gg_read_status(self.status)
 
 
 def _rec(e, stream=None):

@@ -104,6 +104,9 @@ def test_host_helpers(gg):
     for f in (gg.gg_ws_sample, gg.gg_ws_hotset):
         assert f(10_000, 4) > 0 and f(10_000, 4) % 256 == 0
     assert gg.gg_ws_bucket(0, 4) > 0 and gg.gg_ws_gather(0, 1, 4) > 0 and gg.gg_ws_stage(0, 4) > 0
+    # the status read checks its pointers before any HIP call
+    with pytest.raises(gg.GGError, match="null"):
+        gg.gg_read_status(None, stream=0)
 
 
 class _FakeTensor:

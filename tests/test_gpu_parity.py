@@ -76,6 +76,19 @@ def test_hot_set_in_multi_pass_chunks(n_hot, monkeypatch):
     w.run_and_compare(1)
 
 
+@pytest.mark.parametrize("tile", [1, 4, 16])
+@pytest.mark.parametrize("n_hot", [-1, 300])
+def test_fewer_rows_per_wave_step(tile, n_hot, monkeypatch):
+    """GG_TILE_ROWS shrinks the rows a wavefront copies per step in the
+    stage and the gather (1 = one row per wavefront step), the variants the
+    benchmark's ablation times: same bytes, with and without misses."""
+    log(f"small: {tile} rows per wave step, n_hot={n_hot}")
+    monkeypatch.setenv("GG_TILE_ROWS", str(tile))
+    w = world(synth.instance("small"), n_hot=n_hot)
+    w.run_and_compare(0)
+    w.run_and_compare(1)
+
+
 @pytest.mark.parametrize("frac", [(1, 10), (1, 3), (0, 1), (1, 1), (999, 1000)])
 def test_relative_budget_window_matches_oracle(frac):
     log(f"small: hot set = top {frac[0]}/{frac[1]} of the window's remote nodes, 2 windows")
@@ -139,12 +152,16 @@ def test_row_with_tail_words():
     w.run_and_compare(0)
 
 
+@pytest.mark.parametrize("tile", [None, 64])
 @pytest.mark.parametrize("n_hot", [0, 700, -1])
-def test_wide_rows_with_misses(n_hot):
-    """2,408-byte rows at a 2,416-byte stride (eight rows per wave step)
+def test_wide_rows_with_misses(n_hot, tile, monkeypatch):
+    """2,408-byte rows at a 2,416-byte stride (by default eight rows per
+    staging step and two per gather step; GG_TILE_ROWS=64 makes both 64)
     through both gathers and the miss path: with n_hot = 0 every remote row
     is a miss, with 700 some are."""
-    log(f"tiny: 2408-byte rows (tiles of 8), n_hot={n_hot}, consecutive windows")
+    log(f"tiny: 2408-byte rows, tile {tile or 'default'}, n_hot={n_hot}, consecutive windows")
+    if tile:
+        monkeypatch.setenv("GG_TILE_ROWS", str(tile))
     inst = synth.instance("tiny")
     rng = np.random.default_rng(8)
     shards = [rng.integers(0, 256, size=(s.shape[0], 2416), dtype=np.uint8) for s in inst.shards]
