@@ -188,7 +188,10 @@ def main():
                     help="also run the GraphSAGE consumer (mean aggregator, 16 hidden units, "
                          "CLASSES outputs, one layer per sampling hop) on every window's rows "
                          "inside the step, and report its time and MFMA rate")
-    ap.add_argument("--sets", type=int, default=2,
+    ap.add_argument("--breakdown", action="store_true",
+                    help="record events between sampling, hot set and bucketing as well (each "
+                         "event on the build stream costs a few us per window)")
+    ap.add_argument("--sets", type=int, default=None,
                     help="buffer sets of the look-ahead pipeline (how far building may run ahead)")
     ap.add_argument("--wsweep", default=None,
                     help="comma-separated window sizes: run one epoch per W and report, per W, "
@@ -347,8 +350,20 @@ def main():
     torch.cuda.synchronize()
 
     K = args.steps
-    evs = [[mk() for _ in range(5 if look else 6)] for _ in range(K)]
-    gevs = [[(mk(), mk()) for _ in range(W if pb else 1)] for _ in range(K)]
+    # With staging on the build stream, the gather stream's queue holds only
+    # the gathers and one end event each: the gather then starts at the
+    # later of its window's staging end (events[4]) and the previous
+    # gather's end, and every marker left out of that queue saves a few us.
+    stage_on_build = look and pipe.stage_stream is pipe.build_stream
+    # The build stream then carries the critical chain (build, staging) and
+    # each event on it costs a few us too: by default only the build's end
+    # and the staging's end are recorded there, and a build is taken to run
+    # from the previous window's staging end (--breakdown: every call).
+    lean = stage_on_build and not args.breakdown
+    evs = [[None if lean and j < 3 else mk() for j in range(5 if look else 6)]
+           for _ in range(K)]
+    gevs = [[(None if stage_on_build else mk(), mk()) for _ in range(W if pb else 1)]
+            for _ in range(K)]
     cevs = [(mk(), mk()) for _ in range(K)] if cons else [None] * K
     order = [(args.warmup + i) % nwin for i in range(K)]
     torch.cuda.synchronize()
@@ -364,37 +379,39 @@ def main():
     rows = sum(rows_w[k] for k in order)
     value = rows / elapsed
 
-    # Under the look-ahead the gather follows staging on the fetch stream, or
-    # (shards in host memory) runs on a stream of its own after staging.
-    own_gather_stream = look and pipe.gather_stream is not pipe.fetch_stream
-
     def gather_ms(gevs, i, b=None):
         """Duration of gather launch b of step i (all launches when b is
-        None).  Its start event is recorded where its window's staging ends;
-        on a stream of its own the gather starts at the later of that and
-        the previous gather's end."""
+        None).  Without a start event the gather began at the later of its
+        window's staging end and the previous gather's end (the first timed
+        gather is charged from its staging end)."""
         if b is None:
             return sum(gather_ms(gevs, i, j) for j in range(len(gevs[i])))
         s, e = gevs[i][b]
-        t = s.elapsed_time(e)
-        if own_gather_stream and i > 0:
+        if s is not None:
+            return s.elapsed_time(e)
+        t = evs[i][4].elapsed_time(e)
+        if i > 0:
             t = min(t, gevs[i - 1][-1][1].elapsed_time(e))
         return t
 
     g_ms, g_bytes, n_launch = 0.0, 0, 0
-    stage_ms = {"sample": [], "hotset": [], "bucket": [], "stage": [], "gathers": []}
+    stage_ms = ({"build": [], "stage": [], "gathers": []} if lean else
+                {"sample": [], "hotset": [], "bucket": [], "stage": [], "gathers": []})
     st_ms, st_bytes, st_host_bytes = 0.0, 0, 0
     for i, k in enumerate(order):
         e = evs[i]
-        for name, (a, b) in zip(stage_ms, [(0, 1), (1, 2), (2, 3)]):
-            stage_ms[name].append(e[a].elapsed_time(e[b]))
-        # staging starts once its window is built and the fetch stream's
-        # previous work has ended: the previous window's gather, or its
-        # staging when the gather has a stream of its own
+        if lean:
+            if i > 0:
+                stage_ms["build"].append(evs[i - 1][4].elapsed_time(e[3]))
+        else:
+            for name, (a, b) in zip(stage_ms, [(0, 1), (1, 2), (2, 3)]):
+                stage_ms[name].append(e[a].elapsed_time(e[b]))
+        # staging follows the build on the build stream; on the fetch stream
+        # (shards in host memory) it starts at the later of the build's end
+        # and the previous window's staging end
         t_st = e[3].elapsed_time(e[4])
-        if look and i > 0:
-            prev = evs[i - 1][4] if own_gather_stream else gevs[i - 1][-1][1]
-            t_st = min(t_st, prev.elapsed_time(e[4]))
+        if look and not stage_on_build and i > 0:
+            t_st = min(t_st, evs[i - 1][4].elapsed_time(e[4]))
         stage_ms["stage"].append(t_st)
         stage_ms["gathers"].append(gather_ms(gevs, i))
         st_ms += t_st
@@ -404,6 +421,7 @@ def main():
             g_ms += gather_ms(gevs, i, b)
             g_bytes += gbytes_w[k][b]
             n_launch += 1
+    win_bytes = (g_bytes + (st_bytes if pcie is None else 0)) / K
     avg_ms = g_ms / n_launch
     avg_bytes = g_bytes / n_launch
     achieved = avg_bytes / (avg_ms * 1e-3) / 1e9
@@ -445,13 +463,17 @@ def main():
                    "fanout": list(wl.fanout), "batch": wl.batch_size, "W": W,
                    "partitions": P, "local_owner": wl.local_owner, "windows_per_epoch": nwin,
                    "gather_launch": "per batch" if pb else "per window",
-                   "driver": args.pipeline + (f" ({args.sets} buffer sets)" if look else "")},
+                   "driver": args.pipeline + (f" ({pipe.nsets} buffer sets, staging on the "
+                                              f"{'build' if stage_on_build else 'fetch'} stream)"
+                                              if look else "")},
         "roofline": {"bound": "hbm", "kernel": "gg_gather_batch",
                      "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
                      "frac": round(achieved / HBM_PEAK_GBS, 4),
                      "traffic": measured_traffic(args.config, pb),
                      "bytes_per_launch": int(avg_bytes), "avg_launch_us": round(avg_ms * 1e3, 2),
                      "overlapped": look,
+                     "start": ("later of the window's staging end and the previous gather's end "
+                               "(HIP events)" if stage_on_build else "HIP event before the launch"),
                      "isolated": {"achieved": round(iso_achieved, 1),
                                   "frac": round(iso_achieved / HBM_PEAK_GBS, 4),
                                   "avg_launch_us": round(iso_avg_ms * 1e3, 2),
@@ -459,6 +481,14 @@ def main():
                                   "note": "pre-pass over every window, one window at a "
                                           "time" + ("; the look-ahead driver's gather launched "
                                                     "again on one stream" if look else "")}},
+        "window_hbm": {"bytes_per_window": int(win_bytes),
+                       "achieved": round(win_bytes / (elapsed / K) / 1e9, 1),
+                       "frac": round(win_bytes / (elapsed / K) / 1e9 / HBM_PEAK_GBS, 4),
+                       "unit": "GB/s",
+                       "note": "algorithmic bytes of the gathers and of staging from HBM "
+                               "shards over the whole window time (sampling, hot set and "
+                               "bucketing not counted): the share of HBM the overlapped kernels "
+                               "use together"},
         "stage_roofline": ({"kernel": "gg_stage_bulk", "bound": "hbm",
                             "achieved": round(stage_gbs, 1),
                             "frac": round(stage_gbs / HBM_PEAK_GBS, 4), "unit": "GB/s"}
@@ -471,7 +501,7 @@ def main():
                             "note": "host bytes the staging kernel reads over PCIe; peak is the "
                                     "PCIe 5.0 x16 link rate, dma_copy_gbps a measured "
                                     "pinned-to-device copy of 1 GiB"}),
-        "stage_ms_median": {k: round(float(np.median(v)), 4) for k, v in stage_ms.items()},
+        "stage_ms_median": {k: round(float(np.median(v)), 4) for k, v in stage_ms.items() if v},
         "rows_per_window": int(np.mean(rows_w)),
         "hot_set_rows_per_window": int(np.mean(hot_w)),
         "bulk_requests_per_window": float(np.mean(req_w)),

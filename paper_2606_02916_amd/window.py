@@ -283,29 +283,31 @@ class FetchPipeline:
 
 
 class LookaheadPipeline:
-    """Pipelined runtime: the build stream samples window k and forms its
-    hot set and owner buckets; the fetch stream rebuilds the cache (delta
-    staging from window k-1's cache) and then gathers the window.  Window
-    k+1 is built while window k is staged and gathered, so a window costs
-    about the longer of the two streams' work instead of the sum.  Staging
-    and gathering share a stream when every shard is in device memory: both
-    are bound by HBM bandwidth, so they gain nothing from overlapping, and
-    every cross-stream wait costs a few microseconds in the queues.  When
-    shards live in pinned host memory, staging is bound by PCIe instead,
-    and the gather gets a stream of its own so that it runs beside the next
-    window's staging.
+    """Pipelined runtime: window k+1 is built (sampled, its hot set formed
+    and bucketed by owner) and its cache staged while window k is gathered,
+    so a window costs about the longer of the two chains instead of their
+    sum.
+
+    With every shard in device memory, staging follows the build on the
+    build stream and the fetch stream only gathers: staging window k+1
+    (which writes its own buffer set and reads window k's cache) runs beside
+    window k's gather.  When shards live in pinned host memory, staging is
+    bound by PCIe rather than HBM and would hold up the next build, so it
+    runs on the fetch stream and the gather gets a stream of its own,
+    running beside the next window's staging.
 
     `nsets` buffer sets rotate over the windows (window k uses set
-    k mod nsets).  Building window k waits for the gather of window
-    k - nsets, the last reader of its set; with more sets the build may run
-    further ahead.  Bucket lists and hot-set counts rotate over 2 * nsets
-    slots: staging window k reads slot k and clears its remap with the slot
-    of window k - nsets while windows up to k + nsets - 1 are being built.
+    k mod nsets); the default is three with shards in device memory and two
+    otherwise.  Building window k waits for the gather of window k - nsets,
+    the last reader of its set; with more sets the build may run further
+    ahead.  Bucket lists and hot-set counts rotate over 2 * nsets slots:
+    staging window k reads slot k and clears its remap with the slot of
+    window k - nsets while windows up to k + nsets - 1 are being built.
     Every other reuse is ordered through the build wait or stream order."""
 
     def __init__(self, row_ptr, col_idx, num_parts, part_kind, local_owner, range_start, shards,
                  shard_rows, row_bytes, stride, W, fanout, max_batch, n_hot=-1, device=None,
-                 cache_stride=None, nsets=2, hot_frac=None):
+                 cache_stride=None, nsets=None, hot_frac=None):
         self.device = torch.device(device if device is not None else "cuda")
         self.N = int(row_ptr.numel() - 1)
         self.W = int(W)
@@ -323,6 +325,9 @@ class LookaheadPipeline:
         self.geo = g = _Geometry(self.N, self.W, self.fanout, max_batch, self.P, local_owner,
                                  shard_rows, self.stride, self.cache_stride)
         dev = self.device
+        on_host = any(t is not None and not t.is_cuda for t in shards)
+        if nsets is None:
+            nsets = 2 if on_host else 3
         if int(nsets) < 2:
             raise ValueError("the look-ahead pipeline needs at least two buffer sets")
         self.nsets = int(nsets)
@@ -337,36 +342,41 @@ class LookaheadPipeline:
         self.status = torch.zeros(1, dtype=torch.int32, device=dev)
         self.build_stream = torch.cuda.Stream(device=dev)
         self.fetch_stream = torch.cuda.Stream(device=dev)
-        # Staging that reads shards in pinned host memory is bound by PCIe,
-        # not HBM: the gather then gets a stream of its own, so that it runs
-        # beside the next window's staging.
-        on_host = any(t is not None and not t.is_cuda for t in shards)
-        self.gather_stream = torch.cuda.Stream(device=dev) if on_host else self.fetch_stream
+        if on_host:
+            self.stage_stream = self.fetch_stream
+            self.gather_stream = torch.cuda.Stream(device=dev)
+        else:
+            self.stage_stream = self.build_stream
+            self.gather_stream = self.fetch_stream
         self.built = [torch.cuda.Event() for _ in range(self.nsets)]
         self.staged = [torch.cuda.Event() for _ in range(self.nsets)]
-        self.gathered = [torch.cuda.Event() for _ in range(self.nsets)]
+        self._released = [torch.cuda.Event() for _ in range(self.nsets)]
+        self.gathered = list(self._released)
         self.k = 0
 
     def window(self, seeds, seed_off, batch0, epoch=0, rng_seed=0, out=None, events=None,
                gather_events=None, sim=None, consumer=None, consumer_events=None):
         """Enqueues window k; returns (number of batches, buffer set).  The
-        window's rows land in the set's win_out (or `out`) on the fetch
+        window's rows land in the set's win_out (or `out`) on the gather
         stream; wait on gathered_event(k) before reading them.  Inputs
         uploaded on the caller's stream are visible to the build stream.
         events: optional 5 torch events, four recorded on the build stream
-        around its three calls and one after staging on the fetch stream
-        (staging starts at the later of events[3] and the end of the
-        previous window's gather); gather_events: optional (start, end)
-        pair around the gather on the fetch stream; sim: optional
-        (coeffs, acc) to add the window to simulator totals; consumer:
-        optional SageConsumer run on the fetch stream after the gather
-        (so it overlaps the next window's build), bracketed by the optional
-        event pair consumer_events."""
+        around its three calls and one after staging on the staging stream.
+        gather_events: optional (start, end) pair recorded around the gather
+        on the gather stream; start may be None, which keeps one marker out
+        of that stream's queue (the gather then starts at the later of
+        events[4] and the previous window's gather end).  Without sim and
+        consumer, `end` also serves as the buffer set's release, which the
+        build of window k + nsets waits for: record it nowhere else before
+        that build is enqueued.  sim: optional (coeffs, acc) to add the
+        window to simulator totals; consumer: optional SageConsumer run on
+        the gather stream after the gather (so it overlaps the next window's
+        build), bracketed by the optional event pair consumer_events."""
         k, g = self.k, self.geo
         X, T = k % self.nsets, k % self.NSLOT
         cur, prev = self.sets[X], self.sets[(k - 1) % self.nsets]
         Wk = len(seed_off) - 1
-        bs, fs = self.build_stream, self.fetch_stream
+        bs, ss, gs = self.build_stream, self.stage_stream, self.gather_stream
         ev = events if events is not None else [None] * 5
         bs.wait_stream(torch.cuda.current_stream(self.device))
         if k >= self.nsets:
@@ -384,8 +394,9 @@ class LookaheadPipeline:
                               self.bucket_ids[T], cur.owner_off, self.status, cur.ws, stream=s,
                               flags=_bucket_flags(self.part))
         _rec(ev[3], bs)
-        self.built[X].record(bs)
-        fs.wait_event(self.built[X])
+        if ss is not bs:
+            self.built[X].record(bs)
+            ss.wait_event(self.built[X])
         C = (k - self.nsets) % self.NSLOT
         clear_ids = self.bucket_ids[C] if k >= self.nsets else None
         clear_cnt = self.hot_count[C] if k >= self.nsets else None
@@ -394,22 +405,20 @@ class LookaheadPipeline:
                          cur.cache, self.cache_stride, g.hot_cap, cur.slot_of, clear_ids,
                          clear_cnt, src.cache if src else None, src.slot_of if src else None,
                          cur.stage_stats, self.status, self.stage_ws,
-                         stream=fs.cuda_stream)
-        _rec(ev[4], fs)
-        if gather_events is not None:
-            gather_events[0].record(fs)
-        gs = self.gather_stream
-        if gs is not fs:
-            self.staged[X].record(fs)
+                         stream=ss.cuda_stream)
+        _rec(ev[4], ss)
+        if gs is not ss:
+            self.staged[X].record(ss)
             gs.wait_event(self.staged[X])
+        start, end = gather_events if gather_events is not None else (None, None)
+        _rec(start, gs)
         o = cur.win_out if out is None else out
         bounds = cur.frontier_off.data_ptr() + 8 * (self.L * Wk)
         gg.gg_gather_batch(cur.frontier_ids, bounds, Wk, o.shape[0], self.part, self.feat,
                            cur.cache, self.cache_stride, g.hot_cap, cur.slot_of, o, self.stride,
                            cur.gather_stats.data_ptr(), self.status, self.gather_ws,
                            stream=gs.cuda_stream, flags=gg.GG_GATHER_SHARED)
-        if gather_events is not None:
-            gather_events[1].record(gs)
+        _rec(end, gs)
         if sim is not None:           # simulator totals, in window order on the gather stream
             gg.gg_sim_accumulate(cur.stage_stats, cur.gather_stats.data_ptr(), Wk, self.part,
                                  sim[0], sim[1], stream=gs.cuda_stream)
@@ -417,7 +426,13 @@ class LookaheadPipeline:
             _rec(consumer_events[0] if consumer_events else None, gs)
             consumer.forward(cur, Wk, o, self.stride, self.status, stream=gs.cuda_stream)
             _rec(consumer_events[1] if consumer_events else None, gs)
-        self.gathered[X].record(gs)
+        if end is not None and sim is None and consumer is None:
+            # the gather's end marks the set free: every marker in the
+            # gather stream's queue delays the next gather by a few us
+            self.gathered[X] = end
+        else:
+            self.gathered[X] = self._released[X]
+            self.gathered[X].record(gs)
         self.k += 1
         return Wk, cur
 

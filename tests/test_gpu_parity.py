@@ -228,13 +228,14 @@ def test_large_sparse_full_window_matches_oracle():
 
 @pytest.mark.timeout(900)
 def test_large_sparse_lookahead_as_benchmarked():
-    """The benchmark's launch configuration: the look-ahead driver with two
-    buffer sets over three consecutive windows of large_sparse.  Every
+    """The benchmark's launch configuration: the look-ahead driver with
+    its default three buffer sets and only a gather end event per window,
+    over four consecutive windows of large_sparse.  Every
     gathered row equals the row of the unsharded feature matrix (the
     ground truth independent of the cache), N_b of the first and last batch
     of every window equals the oracle's, and the hot set is the union of the
     window's remote N_b."""
-    log("large_sparse: look-ahead driver (2 buffer sets), windows 0-2, every gathered row")
+    log("large_sparse: look-ahead driver (default buffer sets), windows 0-3, every gathered row")
     import torch as T
     from oracle import ggref
     from paper_2606_02916_amd import LookaheadPipeline
@@ -244,7 +245,8 @@ def test_large_sparse_lookahead_as_benchmarked():
     dev = T.device("cuda:0")
     look = LookaheadPipeline(rp_d, ci_d, P, wl.part_kind, wl.local_owner, inst.range_start, sh_d,
                              [s.shape[0] for s in inst.shards], wl.row_bytes, wl.row_stride, W,
-                             wl.fanout, wl.batch_size, device=dev, nsets=2)
+                             wl.fanout, wl.batch_size, device=dev)
+    assert look.nsets == 3 and look.stage_stream is look.build_stream
     seeds_d = T.from_numpy(inst.seeds).to(dev)
     boff, rs, rb = inst.batch_off, inst.range_start, wl.row_bytes
     feats = np.concatenate([s[:, :rb] for s in inst.shards])      # row u = node u
@@ -279,9 +281,10 @@ def test_large_sparse_lookahead_as_benchmarked():
         assert st["retained"] + sum(st["rows"]) == st["rows_total"]
 
     pending = None
-    for k in range(3):
+    for k in range(4):
         b0, b1 = synth.window_batches(boff, W, k)
-        Wk, bufs = look.window(seeds_d[boff[b0]:boff[b1]], boff[b0:b1 + 1] - boff[b0], b0)
+        Wk, bufs = look.window(seeds_d[boff[b0]:boff[b1]], boff[b0:b1 + 1] - boff[b0], b0,
+                               gather_events=(None, T.cuda.Event(enable_timing=True)))
         if pending is not None:
             check(*pending)
         pending = (k, Wk, bufs, b0, k % look.NSLOT)
@@ -480,12 +483,20 @@ def test_delta_staging_matches_oracle(name, n_hot, W):
             assert st["retained"] + sum(st["rows"]) == st["rows_total"]
 
 
-@pytest.mark.parametrize("name,n_hot,W,nsets", [("small", -1, None, 2), ("small", 3000, None, 2),
-                                                ("tiny", -1, 1, 2), ("small", -1, None, 3),
-                                                ("tiny", 2000, 1, 3)])
-def test_lookahead_pipeline_equals_sequential(name, n_hot, W, nsets):
-    log(f"{name}: two-stream look-ahead pipeline vs sequential delta windows, n_hot={n_hot}, "
-        f"W={W}, nsets={nsets}")
+@pytest.mark.parametrize("name,n_hot,W,nsets,host,gev", [
+    ("small", -1, None, 2, False, None), ("small", 3000, None, 2, False, "both"),
+    ("tiny", -1, 1, 2, False, None), ("small", -1, None, None, False, "end"),
+    ("tiny", 2000, 1, 3, False, "end"), ("small", 3000, None, 4, False, "both"),
+    ("small", -1, None, None, True, "both"), ("small", 3000, None, 3, True, "end")])
+def test_lookahead_pipeline_equals_sequential(name, n_hot, W, nsets, host, gev):
+    """The look-ahead driver against the sequential delta-staging driver,
+    window by window: with shards in device memory (staging on the build
+    stream) and with the remote shards in pinned host memory (staging on
+    the fetch stream, gathers on a third stream); without gather events,
+    with both, and with only the end event, which then also releases the
+    buffer set (the benchmark's configuration)."""
+    log(f"{name}: look-ahead pipeline vs sequential delta windows, n_hot={n_hot}, W={W}, "
+        f"nsets={nsets}, host shards={host}, gather events={gev}")
     import torch as T
     from paper_2606_02916_amd import LookaheadPipeline
     inst = synth.instance(name)
@@ -493,10 +504,18 @@ def test_lookahead_pipeline_equals_sequential(name, n_hot, W, nsets):
     seq = world(inst, n_hot=n_hot, W=W, delta=True)
     W = seq.W
     dev = seq.dev
+    shards = seq.shards_d
+    if host:
+        shards = [s if m == wl.local_owner else s.cpu().pin_memory()
+                  for m, s in enumerate(seq.shards_d)]
     look = LookaheadPipeline(seq.row_ptr_d, seq.col_idx_d, wl.num_parts, wl.part_kind,
-                             wl.local_owner, inst.range_start, seq.shards_d,
+                             wl.local_owner, inst.range_start, shards,
                              [s.shape[0] for s in inst.shards], wl.row_bytes, wl.row_stride, W,
                              wl.fanout, wl.batch_size, n_hot=n_hot, device=dev, nsets=nsets)
+    assert (look.stage_stream is look.fetch_stream) == host
+    assert (look.gather_stream is look.fetch_stream) != host
+    nsets = look.nsets
+    mk = lambda: T.cuda.Event(enable_timing=True)  # noqa: E731
     seeds_d = T.from_numpy(inst.seeds).to(dev)
     boff = inst.batch_off
     nwin = synth.n_windows(boff, W)
@@ -515,7 +534,11 @@ def test_lookahead_pipeline_equals_sequential(name, n_hot, W, nsets):
     got, pending = [], None
     for k in range(nwin):
         b0, b1 = synth.window_batches(boff, W, k)
-        Wk, bufs = look.window(seeds_d[boff[b0]:boff[b1]], boff[b0:b1 + 1] - boff[b0], b0)
+        ge = None if gev is None else (None if gev == "end" else mk(), mk())
+        Wk, bufs = look.window(seeds_d[boff[b0]:boff[b1]], boff[b0:b1 + 1] - boff[b0], b0,
+                               gather_events=ge)
+        if ge is not None:
+            assert (look.gathered_event(k) is ge[1])
         if pending is not None:                 # read window k-1 while k is in flight
             got.append(read(*pending))
         pending = (k, Wk, bufs)
