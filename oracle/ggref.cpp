@@ -357,6 +357,60 @@ int ggref_stage_bulk(const int32_t* bucket_ids, const int64_t* owner_off,
   return GGREF_OK;
 }
 
+// Delta staging into one persistent cache (Sec. IV-A; Algorithm 1
+// WarmCache(H_{k+1} \ C)): what the previous window cached stays in place,
+// and only the rebuild delta is fetched, into the lowest free slots.
+int ggref_stage_inplace(const int32_t* bucket_ids, const int64_t* owner_off,
+                        const ggref_part_t* part, const ggref_feat_t* feat, void* cache,
+                        int64_t cache_stride, int64_t cache_rows, int32_t* slot_of,
+                        const int32_t* clear_ids, int64_t clear_count,
+                        const int32_t* prev_slot_of, ggref_stage_stats_t* stats) {
+  if (!part_ok(part) || !feat || feat->num_parts != part->num_parts) return GGREF_ERR_ARG;
+  if (prev_slot_of == slot_of) return GGREF_ERR_ARG;
+  const int32_t P = part->num_parts;
+  const int64_t N = part->num_nodes;
+  std::memset(stats, 0, sizeof(*stats));
+  // The slots the previous window occupies; the rest are free, ascending.
+  std::vector<char> used((size_t)cache_rows, 0);
+  if (prev_slot_of)
+    for (int64_t u = 0; u < N; ++u) {
+      const int32_t s = prev_slot_of[u];
+      if (s >= cache_rows) return GGREF_ERR_RANGE;
+      if (s >= 0) used[(size_t)s] = 1;
+    }
+  std::vector<int64_t> free_slots;
+  for (int64_t s = 0; s < cache_rows; ++s)
+    if (!used[(size_t)s]) free_slots.push_back(s);
+  for (int64_t i = 0; i < clear_count; ++i) slot_of[clear_ids[i]] = -1;
+  stats->invalidated = clear_count;
+  size_t next_free = 0;
+  for (int32_t m = 0; m < P; ++m) {
+    for (int64_t s = owner_off[m]; s < owner_off[m + 1]; ++s) {
+      const int32_t u = bucket_ids[s];
+      if (ggref_owner(part, u) != m) return GGREF_ERR_RANGE;
+      const int64_t r = ggref_row(part, u);
+      if (r < 0 || r >= feat->shard_rows[m]) return GGREF_ERR_RANGE;
+      const int32_t old = prev_slot_of ? prev_slot_of[u] : -1;
+      if (old >= 0) {
+        slot_of[u] = old;
+        ++stats->retained;
+        continue;
+      }
+      if (next_free == free_slots.size()) return GGREF_ERR_CAPACITY;
+      const int64_t slot = free_slots[next_free++];
+      std::memcpy((char*)cache + slot * cache_stride, src_row(feat, m, r), (size_t)feat->row_bytes);
+      slot_of[u] = (int32_t)slot;
+      ++stats->rows[m];
+      ++stats->delta_rows[m];
+    }
+    stats->bytes[m] = stats->rows[m] * feat->row_bytes;
+    stats->requests[m] = (stats->rows[m] > 0) ? 1 : 0;
+    stats->requests_total += stats->requests[m];
+  }
+  stats->rows_total = owner_off[P];
+  return GGREF_OK;
+}
+
 // Per-batch feature assembly (Algorithm 1, inner loop): a local node is
 // read from the local shard, a cached remote node from its cache slot, and
 // every other node is a residual miss.  Misses are grouped by owner, input

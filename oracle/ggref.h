@@ -151,6 +151,22 @@ int ggref_stage_bulk(const int32_t* bucket_ids, const int64_t* owner_off,
                      const int32_t* clear_ids, int64_t clear_count, const void* src_cache,
                      const int32_t* src_slot_of, ggref_stage_stats_t* stats);
 
+/* Delta staging into one persistent cache (Sec. IV-A rebuild events,
+ * Eq. (1); Algorithm 1 WarmCache(H_{k+1} \ C)).  The entries
+ * clear_ids[0 .. clear_count) of slot_of are set to -1 first.  A node of
+ * the bucketed hot set that the previous window's remap prev_slot_of
+ * (num_nodes entries, or NULL for a first window) holds keeps that slot,
+ * and its row stays where it is.  Every other node is the rebuild delta: it
+ * is requested from its owner (one request per owner whose delta is
+ * non-empty) and takes, in bucket order, the lowest cache slot that
+ * prev_slot_of does not hold.  Returns GGREF_ERR_CAPACITY when the free
+ * slots run out. */
+int ggref_stage_inplace(const int32_t* bucket_ids, const int64_t* owner_off,
+                        const ggref_part_t* part, const ggref_feat_t* feat, void* cache,
+                        int64_t cache_stride, int64_t cache_rows, int32_t* slot_of,
+                        const int32_t* clear_ids, int64_t clear_count,
+                        const int32_t* prev_slot_of, ggref_stage_stats_t* stats);
+
 /* Assembles one batch's input features (Algorithm 1, cache lookup, residual
  * misses, on-demand fetch): out row i = feature row of in_ids[i]. */
 int ggref_gather_batch(const int32_t* in_ids, int64_t n, const ggref_part_t* part,

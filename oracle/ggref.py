@@ -102,6 +102,8 @@ def lib():
         L.ggref_bucket_by_owner.restype = C.c_int
         L.ggref_stage_bulk.argtypes = [P, P, P, P, P, i64, i64, P, P, i64, P, P, P]
         L.ggref_stage_bulk.restype = C.c_int
+        L.ggref_stage_inplace.argtypes = [P, P, P, P, P, i64, i64, P, P, i64, P, P]
+        L.ggref_stage_inplace.restype = C.c_int
         L.ggref_gather_batch.argtypes = [P, i64, P, P, P, i64, i64, P, P, i64, P]
         L.ggref_gather_batch.restype = C.c_int
         L.ggref_simulate_epoch.argtypes = [P, P, i64, i32, i64, i64, i64, P, P, P]
@@ -253,6 +255,24 @@ def stage_bulk(bucket_ids, owner_off, part, feat, cache, cache_stride, slot_of, 
                                   _p(cache), cache_stride, cache.shape[0], _p(slot_of), _p(prev),
                                   npre, _p(src_cache), _p(src_slot_of), C.byref(st)),
            "ggref_stage_bulk")
+    return stats_dict(st, part.num_parts)
+
+
+def stage_inplace(bucket_ids, owner_off, part, feat, cache, cache_stride, slot_of, prev_slot_of,
+                  clear_ids=None):
+    """Delta staging into one persistent cache: cache (rows x cache_stride,
+    uint8) and slot_of (int32[N], this window's remap) are updated in place;
+    prev_slot_of is the previous window's remap (None for a first window);
+    clear_ids: entries of slot_of to clear first."""
+    st = StageStats()
+    bucket_ids = np.ascontiguousarray(bucket_ids, dtype=np.int32)
+    owner_off = np.ascontiguousarray(owner_off, dtype=np.int64)
+    clr = None if clear_ids is None else np.ascontiguousarray(clear_ids, dtype=np.int32)
+    ncl = 0 if clr is None else clr.shape[0]
+    _check(lib().ggref_stage_inplace(_p(bucket_ids), _p(owner_off), C.byref(part), C.byref(feat),
+                                     _p(cache), cache_stride, cache.shape[0], _p(slot_of),
+                                     _p(clr), ncl, _p(prev_slot_of), C.byref(st)),
+           "ggref_stage_inplace")
     return stats_dict(st, part.num_parts)
 
 

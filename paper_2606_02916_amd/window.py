@@ -395,8 +395,12 @@ class LookaheadPipeline:
                               flags=_bucket_flags(self.part))
         _rec(ev[3], bs)
         if ss is not bs:
-            self.built[X].record(bs)
-            ss.wait_event(self.built[X])
+            # a caller's event recorded at the same point serves as the
+            # marker to wait on (one marker fewer in the queue)
+            built = ev[3] if ev[3] is not None else self.built[X]
+            if built is self.built[X]:
+                built.record(bs)
+            ss.wait_event(built)
         C = (k - self.nsets) % self.NSLOT
         clear_ids = self.bucket_ids[C] if k >= self.nsets else None
         clear_cnt = self.hot_count[C] if k >= self.nsets else None
@@ -408,8 +412,10 @@ class LookaheadPipeline:
                          stream=ss.cuda_stream)
         _rec(ev[4], ss)
         if gs is not ss:
-            self.staged[X].record(ss)
-            gs.wait_event(self.staged[X])
+            staged = ev[4] if ev[4] is not None else self.staged[X]
+            if staged is self.staged[X]:
+                staged.record(ss)
+            gs.wait_event(staged)
         start, end = gather_events if gather_events is not None else (None, None)
         _rec(start, gs)
         o = cur.win_out if out is None else out

@@ -51,6 +51,13 @@ MUTANTS = [
     ("stage clears before reading old slots",
      "  for (int64_t s = 0; s < total; ++s) old_slot[(size_t)s] = before[bucket_ids[s]];\n  for (int64_t i = 0; i < clear_count; ++i) slot_of[clear_ids[i]] = -1;",
      "  for (int64_t i = 0; i < clear_count; ++i) slot_of[clear_ids[i]] = -1;\n  for (int64_t s = 0; s < total; ++s) old_slot[(size_t)s] = before[bucket_ids[s]];"),
+    ("in-place delta takes the highest free slots",
+     "for (int64_t s = 0; s < cache_rows; ++s)\n    if (!used[(size_t)s]) free_slots.push_back(s);",
+     "for (int64_t s = cache_rows - 1; s >= 0; --s)\n    if (!used[(size_t)s]) free_slots.push_back(s);"),
+    ("in-place staging requests retained rows", "        ++stats->retained;\n        continue;",
+     "        ++stats->retained;\n        ++stats->rows[m];\n        continue;"),
+    ("in-place staging ignores the previous slots", "if (s >= 0) used[(size_t)s] = 1;",
+     "(void)s;"),
     ("miss request counts rows", "stats->miss_requests[m] = miss[m].empty() ? 0 : 1;",
      "stats->miss_requests[m] = (int64_t)miss[m].size();"),
     ("slot 0 treated as a miss", "} else if (slot_of[u] >= 0) {", "} else if (slot_of[u] > 0) {"),

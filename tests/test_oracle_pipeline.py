@@ -436,6 +436,92 @@ def test_delta_staging_requests_only_the_set_difference(kind, local):
         prev = bucket
 
 
+@pytest.mark.parametrize("kind,local", [(ggref.PART_MOD, 0), (ggref.PART_RANGE, 2),
+                                        (ggref.PART_RANGE, -1)])
+def test_inplace_staging_keeps_cached_rows_and_fills_lowest_free_slots(kind, local):
+    """Algorithm 1 WarmCache(H_{k+1} minus C) on one persistent cache: a node
+    the previous window cached keeps its slot and its bytes are not
+    touched; only Delta_{k,m} = (H_k in owner m) minus H_{k-1} is requested,
+    one request per owner with a non-empty delta, and the delta takes the
+    lowest slots the previous window does not hold, in bucket order.  Ground
+    truth: Python sets, sorted lists and the unsharded feature matrix."""
+    rng = np.random.default_rng(47)
+    N = 500
+    row_ptr, col_idx = helpers.random_graph(N, 4000, rng)
+    part, feat, full, shards, rs = make_world(row_ptr, col_idx, kind, 4, local, 20, 32, rng)
+    cache_rows = N
+    cache = np.zeros((cache_rows, 32), dtype=np.uint8)
+    remaps = [np.full(N, -1, dtype=np.int32) for _ in range(2)]
+    held = [None, None]                    # hot set each remap last held
+    prev = None
+    for k in range(6):
+        seeds, soff = random_seeds(N, 3, 5, rng)
+        fids, foff, _, _ = ggref.sample_window(row_ptr, col_idx, seeds, soff, (3, 2), 5, 0, 3 * k)
+        hot, _ = ggref.build_hotset(fids, foff, 3, 2, part, -1)
+        bucket, owner_off = ggref.bucket_by_owner(hot, part)
+        cur, old = remaps[k % 2], (remaps[(k - 1) % 2] if k else None)
+        before = cache.copy()
+        old_map = None if old is None else old.copy()
+        cleared = held[k % 2]
+        st = ggref.stage_inplace(bucket, owner_off, part, feat, cache, 32, cur, old,
+                                 clear_ids=cleared)
+        held[k % 2] = bucket.copy()
+        H = bucket.tolist()
+        prev_set = set() if prev is None else set(prev)
+        taken = set() if old_map is None else {int(x) for x in old_map if x >= 0}
+        free = [x for x in range(cache_rows) if x not in taken]
+        delta = [u for u in H if u not in prev_set]          # bucket order
+        for j, u in enumerate(delta):
+            assert cur[u] == free[j]
+        for u in H:
+            if u in prev_set:
+                assert cur[u] == old_map[u]
+                assert np.array_equal(cache[cur[u]], before[cur[u]])   # not rewritten
+            assert np.array_equal(cache[cur[u], :20], full[u, :20])
+        mask = np.ones(N, bool)
+        mask[H] = False
+        assert np.all(cur[mask] == -1)
+        assert len({int(cur[u]) for u in H}) == len(H)
+        for m in range(4):
+            seg = set(H[owner_off[m]:owner_off[m + 1]]) - prev_set
+            assert st["rows"][m] == st["delta_rows"][m] == len(seg)
+            assert st["requests"][m] == (1 if seg else 0)
+            assert st["bytes"][m] == 20 * len(seg)
+        assert st["retained"] == len(set(H) & prev_set)
+        assert st["rows_total"] == len(H)
+        assert st["invalidated"] == (0 if cleared is None else len(cleared))
+        if k == 0:                      # a first window takes slot = bucket position
+            assert [int(cur[u]) for u in H] == list(range(len(H)))
+        prev = H
+
+
+def test_inplace_staging_capacity_is_the_union_of_two_windows():
+    """The free slots run out exactly when the cache is smaller than the
+    union of the previous and the current hot set."""
+    rng = np.random.default_rng(53)
+    N = 300
+    row_ptr, col_idx = helpers.random_graph(N, 2000, rng)
+    part, feat, full, shards, rs = make_world(row_ptr, col_idx, ggref.PART_MOD, 4, 0, 8, 8, rng)
+    hs = []
+    for k in range(2):
+        seeds, soff = random_seeds(N, 2, 4, rng)
+        fids, foff, _, _ = ggref.sample_window(row_ptr, col_idx, seeds, soff, (2, 2), 1, 0, 2 * k)
+        hot, _ = ggref.build_hotset(fids, foff, 2, 2, part, -1)
+        hs.append(ggref.bucket_by_owner(hot, part))
+    union = len(set(hs[0][0].tolist()) | set(hs[1][0].tolist()))
+    assert union > len(hs[1][0])
+    for rows, ok in [(union, True), (union - 1, False)]:
+        cache = np.zeros((rows, 8), dtype=np.uint8)
+        r0, r1 = np.full(N, -1, np.int32), np.full(N, -1, np.int32)
+        ggref.stage_inplace(hs[0][0], hs[0][1], part, feat, cache, 8, r0, None)
+        if ok:
+            ggref.stage_inplace(hs[1][0], hs[1][1], part, feat, cache, 8, r1, r0)
+            assert max(int(r1[u]) for u in hs[1][0]) < rows
+        else:
+            with pytest.raises(ggref.OracleError, match="-2"):
+                ggref.stage_inplace(hs[1][0], hs[1][1], part, feat, cache, 8, r1, r0)
+
+
 def test_paper_consolidation_example():
     """Sec. IV-C: W = 16 batches over three remote owners turn up to
     16 x 3 = 48 per-batch requests into 3 bulk transfers."""
