@@ -176,11 +176,13 @@ def main():
     ap.add_argument("--per-batch", action="store_true",
                     help="one gather launch per batch instead of one per window (sequential "
                          "driver only)")
-    ap.add_argument("--pipeline", default="lookahead", choices=["sequential", "delta", "lookahead"],
+    ap.add_argument("--pipeline", default="lookahead",
+                    choices=["sequential", "delta", "inplace", "lookahead"],
                     help="sequential: the five calls per window on one stream, full restage; "
-                         "delta: the same with delta staging from the previous cache; "
-                         "lookahead: delta staging, window k+1 built on a second stream while "
-                         "window k is gathered")
+                         "delta: the same with delta staging, retained rows copied from the "
+                         "previous cache; inplace: delta staging into one persistent cache; "
+                         "lookahead: in-place staging, window k+1 built and staged on a second "
+                         "stream while window k is gathered")
     ap.add_argument("--copy-calibration-mib", type=int, default=0,
                     help="after the timed steps, copy this many MiB device to device three "
                          "times (a plain copy of known size for scaling HBM counters)")
@@ -263,10 +265,12 @@ def main():
              [s.shape[0] for s in inst.shards], wl.row_bytes, wl.row_stride, W, wl.fanout,
              wl.batch_size)
     look = args.pipeline == "lookahead"
+    inplace_cache = args.pipeline in ("lookahead", "inplace")
     if look:
         pipe = LookaheadPipeline(*pargs, device=dev, nsets=args.sets)
     else:
-        pipe = FetchPipeline(*pargs, device=dev, delta=args.pipeline == "delta")
+        pipe = FetchPipeline(*pargs, device=dev, delta=args.pipeline == "delta",
+                             inplace=args.pipeline == "inplace")
     boff = inst.batch_off
     nwin = synth.n_windows(boff, W)
     wins = []
@@ -336,7 +340,11 @@ def main():
         gbytes_w.append(gb if pb else [sum(gb)])
         ss = sb.stage_stats_dict()
         hot_w.append(ss["rows_total"])
-        sbytes_w.append(ss["rows_total"] * (2 * rb + 8) + ss["invalidated"] * 4)
+        # a staged row moves 2 * row_bytes and its id and remap entry; a row
+        # kept in place only its id, old and new remap entries
+        kept = ss["retained"] if inplace_cache else 0
+        sbytes_w.append((ss["rows_total"] - kept) * (2 * rb + 8) + kept * 12 +
+                        ss["invalidated"] * 4)
         req_w.append(ss["requests_total"])
         hbytes_w.append(sum(ss["bytes"][m] for m in range(P) if not shards_d[m].is_cuda))
         fo = sb.frontier_off[:(L + 1) * Wk + 1].cpu().numpy()

@@ -168,6 +168,7 @@ size_t gg_ws_sample(int64_t num_nodes, int32_t W);
 size_t gg_ws_hotset(int64_t num_nodes, int32_t W);
 size_t gg_ws_bucket(int64_t cap, int32_t num_parts);
 size_t gg_ws_stage(int64_t cap, int32_t num_parts);
+size_t gg_ws_stage_inplace(int64_t cap, int64_t cache_rows, int32_t num_parts);
 size_t gg_ws_gather(int64_t n_cap, int32_t nseg, int32_t num_parts);
 
 /* Neighbour sampling of one window (Sec. IV-A step 2: one epoch of
@@ -248,6 +249,38 @@ int gg_stage_bulk(const int32_t* bucket_ids_d, const int64_t* owner_off_d, int64
                   const void* src_cache_d, const int32_t* src_slot_of_d,
                   gg_stage_stats_t* stats_d, int32_t* status_d, void* ws, size_t ws_bytes,
                   hipStream_t stream);
+
+/* Delta staging into one persistent cache (Sec. IV-A rebuild events,
+ * Eq. (1); Algorithm 1 WarmCache(H_{k+1} \ C)): rows the previous window
+ * cached stay where they are, and only the rebuild delta is requested.
+ * First the entries clear_ids_d[0 .. clear_count_d[0]) of slot_of_d (this
+ * window's remap, num_nodes entries) are set to -1; both may be NULL.  A
+ * node of the bucketed hot set (owner_off_d[P] <= cap entries of
+ * bucket_ids_d) that prev_slot_of_d (the previous window's remap, another
+ * buffer) holds keeps that slot in slot_of_d, and its cache row is not
+ * touched.  Every other node is the delta Delta_{k,m}: it is requested from
+ * its owner m (one request per owner with a non-empty delta, the indicator
+ * of Eq. (1)) and takes, in bucket order, the lowest slot below cache_rows
+ * that the previous window does not occupy.  occ_prev_d is that occupancy,
+ * one byte per slot (non-zero = in use; cache_rows rounded up to a multiple
+ * of 32 bytes, 16-byte aligned) that the previous call wrote as occ_d;
+ * occ_d (another buffer of the same size) receives this window's.  With
+ * prev_slot_of_d and occ_prev_d
+ * both NULL (a first window) every row is requested and takes slot = its
+ * bucket position.  Only free slots are written, so the previous window's
+ * gathers may run concurrently; the window before it must be finished.
+ * The cache must hold both windows: when the free slots run out,
+ * GG_DEV_CAPACITY is raised and the rows left over are not staged (their
+ * remap entries stay -1, so a gather serves them as misses).  Statistics
+ * as gg_stage_bulk's with a source cache: rows, bytes and requests count
+ * the delta, retained the rows kept in place. */
+int gg_stage_inplace(const int32_t* bucket_ids_d, const int64_t* owner_off_d, int64_t cap,
+                     const gg_part_t* part, const gg_feat_t* feat, void* cache_d,
+                     int64_t cache_stride, int64_t cache_rows, int32_t* slot_of_d,
+                     const int32_t* clear_ids_d, const int64_t* clear_count_d,
+                     const int32_t* prev_slot_of_d, const uint8_t* occ_prev_d, uint8_t* occ_d,
+                     gg_stage_stats_t* stats_d, int32_t* status_d, void* ws, size_t ws_bytes,
+                     hipStream_t stream);
 
 /* Assembles the input features of nseg consecutive batches (Algorithm 1
  * inner loop) in one launch.  Segment s (s < nseg) is batch s: its ids are

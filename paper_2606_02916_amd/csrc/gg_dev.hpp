@@ -94,6 +94,18 @@ __device__ __forceinline__ int lanes_below(uint64_t mask) {
                                         __builtin_amdgcn_mbcnt_lo((uint32_t)mask, 0u));
 }
 
+// Lane index of the (r+1)-th set bit of mask (r < popcount(mask)).
+__device__ __forceinline__ int nth_set_lane(uint64_t mask, int r) {
+  int lo = 0;
+#pragma unroll
+  for (int w = 32; w >= 1; w >>= 1) {
+    // set bits below lane lo + w
+    const uint64_t below = (lo + w >= 64) ? mask : (mask & ((1ull << (lo + w)) - 1ull));
+    if (__popcll(below) <= r) lo += w;
+  }
+  return lo;
+}
+
 template <typename T>
 __device__ __forceinline__ T wave_incl_scan(T v) {
   const int lane = lane_id();
@@ -134,10 +146,12 @@ __device__ __forceinline__ T block_excl_scan(T v, T* lds, T* total) {
 }
 
 // Exclusive scan of in[0..n) into out[0..n) plus `base`, by one block of
-// 1024 threads, 16 consecutive items per thread per tile.  Returns the sum.
+// NT threads, 16 consecutive items per thread per tile; lds holds NT/64
+// entries.  Returns the sum.
+template <int NT = 1024>
 __device__ __forceinline__ int64_t block_scan_large(const int32_t* in, int64_t* out, int64_t n,
                                                     int64_t base, int64_t* lds16) {
-  constexpr int NT = 1024, IT = 16;
+  constexpr int IT = 16;
   int64_t carry = base;
   for (int64_t t0 = 0; t0 < n; t0 += (int64_t)NT * IT) {
     int32_t loc[IT];
@@ -271,5 +285,66 @@ __device__ __forceinline__ void wave_copy_rows(const char* src, char* dst0, int6
   }
 }
 
+// As wave_copy_rows, with a destination per row: lane r supplies both the
+// source and the destination of row r (a nullptr source skips the row).
+template <int VB, bool NT, int U = (VB == 16 ? 4 : 8)>
+__device__ __forceinline__ void wave_copy_rows_to(const char* src, char* dst, int nrows,
+                                                  const CopyGeom& g) {
+  const int lane = lane_id();
+  const uint32_t total = (uint32_t)nrows * g.cpr;
+  const long long srcl = (long long)src, dstl = (long long)dst;
+  for (uint32_t base = 0; base < total; base += kWave * U) {
+    if (VB == 16) {
+      u32x4 v[U];
+      char* dp[U];
+      bool ok[U];
+#pragma unroll
+      for (int j = 0; j < U; ++j) {
+        const uint32_t c = base + (uint32_t)(j * kWave + lane);
+        const uint32_t r = __umulhi(c, g.magic);
+        const uint32_t col = c - r * g.cpr;
+        const char* sp = (const char*)__shfl(srcl, (int)(r & 63u), kWave);
+        dp[j] = (char*)__shfl(dstl, (int)(r & 63u), kWave) + (int64_t)col * 16;
+        ok[j] = (c < total) && (sp != nullptr);
+        if (ok[j]) v[j] = *(const u32x4*)(sp + (int64_t)col * 16);
+      }
+#pragma unroll
+      for (int j = 0; j < U; ++j)
+        if (ok[j]) st16<NT>(dp[j], v[j]);
+    } else {
+      uint32_t v[U];
+      char* dp[U];
+      bool ok[U];
+#pragma unroll
+      for (int j = 0; j < U; ++j) {
+        const uint32_t c = base + (uint32_t)(j * kWave + lane);
+        const uint32_t r = __umulhi(c, g.magic);
+        const uint32_t col = c - r * g.cpr;
+        const char* sp = (const char*)__shfl(srcl, (int)(r & 63u), kWave);
+        dp[j] = (char*)__shfl(dstl, (int)(r & 63u), kWave) + (int64_t)col * 4;
+        ok[j] = (c < total) && (sp != nullptr);
+        if (ok[j]) v[j] = *(const uint32_t*)(sp + (int64_t)col * 4);
+      }
+#pragma unroll
+      for (int j = 0; j < U; ++j)
+        if (ok[j]) st4<NT>(dp[j], v[j]);
+    }
+  }
+  if (VB == 16 && g.tail) {
+    const uint32_t ttotal = (uint32_t)nrows * g.tail;
+    const int64_t off0 = (int64_t)g.cpr * 16;
+    for (uint32_t base = 0; base < ttotal; base += kWave) {
+      const uint32_t c = base + (uint32_t)lane;
+      const uint32_t r = __umulhi(c, g.tmagic);
+      const uint32_t w = c - r * g.tail;
+      const char* sp = (const char*)__shfl(srcl, (int)(r & 63u), kWave);
+      char* dp = (char*)__shfl(dstl, (int)(r & 63u), kWave);
+      if (c < ttotal && sp != nullptr) {
+        const uint32_t v = *(const uint32_t*)(sp + off0 + (int64_t)w * 4);
+        st4<NT>(dp + off0 + (int64_t)w * 4, v);
+      }
+    }
+  }
+}
 
 }  // namespace gg

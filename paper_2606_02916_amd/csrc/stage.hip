@@ -14,6 +14,8 @@
 namespace gg {
 namespace {
 
+__device__ __forceinline__ int64_t cdiv_dev(int64_t a, int64_t b) { return (a + b - 1) / b; }
+
 struct StageArgs {
   int64_t cap;         // bucket entries usable
   int64_t cache_rows;
@@ -215,6 +217,308 @@ int stage_delta_blocks(int64_t cap) {
   return (int)std::min<int64_t>(std::max<int64_t>(cdiv(cap, kBlock), 1), 1024);
 }
 
+// ---------------------------------------------------------------------------
+// In-place staging into one persistent cache.  The delta rows of window k
+// take, in bucket order, the lowest slots that window k-1 does not occupy;
+// rows window k-1 cached keep their slot and are not copied.  Occupancy is
+// one byte per slot (plain byte stores, no atomics).
+//   k_inplace_prep  old slot of every bucket entry (-1: delta, -2: bad id),
+//                   the delta count of every range of 64 entries and of
+//                   every block (block b takes ranges b*R .. b*R+R-1),
+//                   the per-owner delta counts and the free slots per chunk
+//                   of the previous occupancy; clears the remap's stale
+//                   entries and the new occupancy.
+//   k_inplace_emit  the prefix of the block counts, and the ascending list
+//                   of the first |delta| free slots, one block per chunk
+//                   (chunks past them return at once).
+//   k_inplace_rows  remap, occupancy and the delta rows' copies (the
+//                   requests); a tile's first delta rank is the prefix of
+//                   its range's block plus that block's range counts before
+//                   its range.
+// ---------------------------------------------------------------------------
+constexpr int kRange = kWave;          // bucket entries per delta count (one wave)
+constexpr int kOccChunk = kBlock * 32; // slots per free-list block (one 32-slot group a thread)
+constexpr int kPrepBlocks = 1024;      // most prep blocks (block counts a rank sums)
+
+struct InplaceWs {
+  int32_t* old_slot;   // [cap]
+  int32_t* dcnt;       // [prep blocks][P]
+  int32_t* dr;         // [ranges]
+  int32_t* btot;       // [prep blocks]
+  int64_t* bpre;       // [prep blocks]
+  int32_t* fcnt;       // [occupancy chunks]
+  int32_t* freel;      // [cache_rows]
+  int64_t* nfree;      // [1]
+};
+
+int inplace_prep_blocks(int64_t cap, int64_t cache_rows) {
+  const int64_t need = std::max<int64_t>(cdiv(cap, kBlock), cdiv(cache_rows, kOccChunk));
+  return (int)std::min<int64_t>(std::max<int64_t>(need, 1), kPrepBlocks);
+}
+
+size_t inplace_ws_layout(int64_t cap, int64_t cache_rows, int32_t P, char* base, InplaceWs* out) {
+  const int64_t nr = std::max<int64_t>(cdiv(cap, kRange), 1);
+  const int64_t nch = std::max<int64_t>(cdiv(cache_rows, kOccChunk), 1);
+  const int gp = inplace_prep_blocks(cap, cache_rows);
+  Carve cv{base, 0, ~(size_t)0};
+  InplaceWs w;
+  w.old_slot = cv.take<int32_t>((size_t)std::max<int64_t>(cap, 1));
+  w.dcnt = cv.take<int32_t>((size_t)gp * (size_t)P);
+  w.dr = cv.take<int32_t>((size_t)nr);
+  w.btot = cv.take<int32_t>((size_t)gp);
+  w.bpre = cv.take<int64_t>((size_t)gp);
+  w.fcnt = cv.take<int32_t>((size_t)nch);
+  w.freel = cv.take<int32_t>((size_t)std::max<int64_t>(cache_rows, 1));
+  w.nfree = cv.take<int64_t>(1);
+  if (out) *out = w;
+  return align_up(cv.used, 256);
+}
+
+// Free-slot mask of the 32 slots q*32 .. q*32+31 (bit i = slot q*32+i is
+// below cache_rows and its occupancy byte is 0).
+__device__ __forceinline__ uint32_t free_mask(const uint8_t* occ, int64_t q, int64_t cache_rows) {
+  const int64_t lim = cache_rows - q * 32;
+  if (lim <= 0) return 0u;
+  const u32x4* p = (const u32x4*)(occ + q * 32);
+  const u32x4 a = p[0], b = p[1];
+  const uint32_t w[8] = {a.x, a.y, a.z, a.w, b.x, b.y, b.z, b.w};
+  uint32_t m = 0;
+#pragma unroll
+  for (int i = 0; i < 8; ++i)
+#pragma unroll
+    for (int j = 0; j < 4; ++j)
+      m |= (((w[i] >> (8 * j)) & 0xFFu) == 0u ? 1u : 0u) << (4 * i + j);
+  if (lim < 32) m &= (1u << lim) - 1u;
+  return m;
+}
+
+// Sum of v over a block of kBlock threads (every thread gets it).
+__device__ __forceinline__ int64_t block_sum(int64_t v, int64_t* lds) {
+  v = wave_sum(v);
+  if (lane_id() == 0) lds[threadIdx.x / kWave] = v;
+  __syncthreads();
+  int64_t t = 0;
+#pragma unroll
+  for (int q = 0; q < kBlock / kWave; ++q) t += lds[q];
+  __syncthreads();
+  return t;
+}
+
+// Ranges per prep block for n bucket entries and gp prep blocks.
+__device__ __forceinline__ int64_t ranges_per_block(int64_t n, int gp) {
+  return cdiv_dev(cdiv_dev(n, kRange), gp);
+}
+
+__global__ void __launch_bounds__(kBlock) k_inplace_prep(
+    const int32_t* bucket, const int64_t* owner_off, KPart part, StageArgs a, const int32_t* prev,
+    int32_t* old_slot, int32_t* dcnt, int32_t* dr, int32_t* btot, const int32_t* clear,
+    const int64_t* clear_count, int32_t* slot_of, const uint8_t* occ_prev, int32_t* fcnt,
+    uint8_t* occ, int32_t* status) {
+  __shared__ int32_t hist[GG_MAX_PARTS];
+  __shared__ int64_t s_start[GG_MAX_PARTS + 1];
+  __shared__ int64_t lds[kBlock / kWave];
+  __shared__ int32_t s_fresh;
+  for (int t = threadIdx.x; t < GG_MAX_PARTS; t += blockDim.x) hist[t] = 0;
+  for (int t = threadIdx.x; t <= GG_MAX_PARTS; t += blockDim.x) s_start[t] = part.start[t];
+  if (threadIdx.x == 0) s_fresh = 0;
+  __syncthreads();
+  const int64_t n = stage_n(owner_off, part.P, a);
+  const int64_t nr = cdiv_dev(n, kRange);
+  const int64_t R = ranges_per_block(n, gridDim.x);
+  const int64_t rend = (int64_t)(blockIdx.x + 1) * R < nr ? (int64_t)(blockIdx.x + 1) * R : nr;
+  const int lane = lane_id();
+  int32_t st = 0;
+  for (int64_t r = (int64_t)blockIdx.x * R + threadIdx.x / kWave; r < rend; r += kBlock / kWave) {
+    const int64_t s = r * kRange + lane;
+    bool fresh = false;
+    int32_t m = 0;
+    if (s < n) {
+      const int32_t u = bucket[s];
+      int32_t old = -2;
+      if (u >= 0 && (int64_t)u < part.N) {
+        old = prev ? prev[u] : -1;
+        if ((int64_t)old >= a.cache_rows) {
+          st |= GG_DEV_BAD_ROW;
+          old = -1;
+        }
+        if (old < 0) {
+          old = -1;
+          fresh = true;
+          m = owner_of(part, s_start, u);
+        }
+      }
+      old_slot[s] = old;
+    }
+    wave_hist_add(hist, fresh, m);
+    const int32_t c = (int32_t)__popcll(__ballot(fresh));
+    if (lane == 0) {
+      dr[r] = c;
+      if (c) atomicAdd(&s_fresh, c);
+    }
+  }
+  if (clear) {
+    const int64_t nc = clear_count[0];
+    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < nc;
+         i += (int64_t)gridDim.x * blockDim.x) {
+      const int32_t u = clear[i];
+      if (u >= 0 && (int64_t)u < part.N) slot_of[u] = -1;
+    }
+  }
+  const int64_t groups = cdiv_dev(a.cache_rows, 32);     // 32-slot groups
+  if (occ_prev) {
+    const int64_t nch = cdiv_dev(a.cache_rows, kOccChunk);
+    for (int64_t c = blockIdx.x; c < nch; c += gridDim.x) {
+      const int64_t g = c * kBlock + threadIdx.x;
+      const int64_t f = block_sum(g < groups ? __popc(free_mask(occ_prev, g, a.cache_rows)) : 0,
+                                  lds);
+      if (threadIdx.x == 0) fcnt[c] = (int32_t)f;
+    }
+  }
+  const u32x4 z = {0u, 0u, 0u, 0u};
+  for (int64_t q = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; q < groups * 2;
+       q += (int64_t)gridDim.x * blockDim.x)
+    ((u32x4*)occ)[q] = z;
+  if (st) set_status(status, st);
+  __syncthreads();
+  for (int m = threadIdx.x; m < part.P; m += blockDim.x) dcnt[(int64_t)blockIdx.x * part.P + m] = hist[m];
+  if (threadIdx.x == 0) btot[blockIdx.x] = s_fresh;
+}
+
+// Block 0 writes the exclusive prefix of the prep blocks' delta counts
+// (bpre) and the number of free slots.  With a previous occupancy, block b
+// also writes the free slots of occupancy chunk b at their place in the
+// ascending free list, as far as the delta needs: staged in LDS, then
+// stored contiguously; chunks past the delta's last slot return at once.
+__global__ void __launch_bounds__(kBlock) k_inplace_emit(const uint8_t* occ_prev,
+                                                         const int32_t* fcnt, int32_t nch,
+                                                         const int32_t* btot, int32_t gp,
+                                                         int64_t* bpre, int32_t* freel,
+                                                         int64_t* nfree, StageArgs a) {
+  __shared__ int64_t lds[kBlock / kWave];
+  __shared__ int32_t buf[kOccChunk];
+  constexpr int PT = kPrepBlocks / kBlock;     // block counts per thread
+  const int b = blockIdx.x;
+  int32_t bt[PT];
+  int64_t v = 0;
+#pragma unroll
+  for (int q = 0; q < PT; ++q) {
+    const int i = threadIdx.x * PT + q;
+    bt[q] = i < gp ? btot[i] : 0;
+    v += bt[q];
+  }
+  int64_t need;
+  int64_t run = block_excl_scan<kBlock>(v, lds, &need);
+  if (b == 0) {
+#pragma unroll
+    for (int q = 0; q < PT; ++q) {
+      const int i = threadIdx.x * PT + q;
+      if (i < gp) bpre[i] = run;
+      run += bt[q];
+    }
+  }
+  if (!occ_prev) {
+    if (b == 0 && threadIdx.x == 0) *nfree = a.cache_rows;
+    return;
+  }
+  int64_t w = 0, all = 0;
+  for (int c = threadIdx.x; c < nch; c += blockDim.x) {
+    const int64_t x = fcnt[c];
+    all += x;
+    if (c < b) w += x;
+  }
+  const int64_t before = block_sum(w, lds);
+  if (b == 0) {
+    all = block_sum(all, lds);
+    if (threadIdx.x == 0) *nfree = all;
+  }
+  if (before >= need) return;                      // the delta's slots lie before this chunk
+  const int64_t g = (int64_t)b * kBlock + threadIdx.x;
+  uint32_t f = free_mask(occ_prev, g, a.cache_rows);
+  int64_t tot;
+  int64_t pos = block_excl_scan<kBlock>((int64_t)__popc(f), lds, &tot);
+  for (; f; f &= f - 1u) buf[pos++] = (int32_t)(g * 32 + (__ffs(f) - 1));
+  __syncthreads();
+  const int64_t lim = need - before < tot ? need - before : tot;
+  for (int64_t i = threadIdx.x; i < lim; i += blockDim.x) freel[before + i] = buf[i];
+}
+
+template <int VB, bool NT>
+__global__ void __launch_bounds__(kBlock) k_inplace_rows(
+    const int32_t* bucket, const int64_t* owner_off, KPart part, KFeat feat, StageArgs a,
+    char* cache, int32_t* slot_of, const int32_t* old_slot, const int32_t* dr,
+    const int64_t* bpre, int32_t gp, const int32_t* freel, const int64_t* nfree_p,
+    bool have_free_list, uint8_t* occ, StageStatsArgs sa, int32_t* status) {
+  if (blockIdx.x == 0) stage_stats(owner_off, part, a, feat.row_bytes, sa, status);
+  __shared__ int64_t s_start[GG_MAX_PARTS + 1];
+  for (int t = threadIdx.x; t <= GG_MAX_PARTS; t += blockDim.x) s_start[t] = part.start[t];
+  __syncthreads();
+  const int64_t n = stage_n(owner_off, part.P, a);
+  const int64_t R = ranges_per_block(n, gp);
+  const int64_t nfree = *nfree_p;
+  const int64_t ntiles = (n + a.tile - 1) / a.tile;
+  const int lane = lane_id();
+  int32_t st = 0;
+  for (int64_t tile = (int64_t)blockIdx.x * (kBlock / kWave) + threadIdx.x / kWave; tile < ntiles;
+       tile += (int64_t)gridDim.x * (kBlock / kWave)) {
+    const int64_t s0 = tile * a.tile;
+    const int64_t s = s0 + lane;
+    const bool live = lane < a.tile && s < n;
+    const int32_t old = live ? old_slot[s] : -2;
+    const int32_t u = live ? bucket[s] : -1;
+    // delta rank of the tile's first entry: the counts of the prep blocks
+    // before its range's block, of that block's ranges before its range,
+    // and of the range's entries before the tile
+    const int64_t rg = s0 / kRange;
+    const int64_t pb = rg / R;
+    int64_t j = 0;
+    for (int64_t q = pb * R + lane; q < rg; q += kWave) j += dr[q];
+    const int64_t r0 = rg * kRange;
+    if (r0 < s0) {
+      const int64_t p = r0 + lane;
+      j += (p < s0 && old_slot[p] == -1) ? 1 : 0;
+    }
+    j = bpre[pb] + wave_sum(j);
+    const uint64_t fm = __ballot(old == -1);
+    long long src = 0, dst = 0;
+    if (live) {
+      if (old == -2) {
+        st |= GG_DEV_BAD_ID;
+      } else if (old >= 0) {
+        slot_of[u] = old;                                    // retained in place
+        occ[old] = 1;
+      } else {
+        const int64_t jj = j + lanes_below(fm);
+        int64_t slot = -1;
+        if (jj < nfree) slot = have_free_list ? (int64_t)freel[jj] : jj;
+        if (slot < 0 || slot >= a.cache_rows) {
+          st |= GG_DEV_CAPACITY;
+        } else {
+          const int32_t m = owner_of(part, s_start, u);
+          const int64_t r = row_of(part, s_start, u, m);
+          if (r >= feat.rows[m]) {
+            st |= GG_DEV_BAD_ROW;
+          } else {
+            src = (long long)(feat.shard[m] + r * feat.stride[m]);   // requested from owner m
+            dst = (long long)(cache + slot * a.cache_stride);
+            slot_of[u] = (int32_t)slot;
+            occ[slot] = 1;
+          }
+        }
+      }
+    }
+    // the tile's requested rows, packed to the front of the wave
+    const uint64_t cm = __ballot(src != 0);
+    const int nc = (int)__popcll(cm);
+    if (nc) {
+      const int from = lane < nc ? nth_set_lane(cm, lane) : 0;
+      const long long cs = __shfl(src, from, kWave), cd = __shfl(dst, from, kWave);
+      wave_copy_rows_to<VB, NT>(lane < nc ? (const char*)cs : nullptr,
+                                lane < nc ? (char*)cd : nullptr, nc, a.geom);
+    }
+  }
+  if (st) set_status(status, st);
+}
+
 }  // namespace
 }  // namespace gg
 
@@ -304,5 +608,98 @@ extern "C" int gg_stage_bulk(const int32_t* bucket_ids_d, const int64_t* owner_o
     launch_stage_rows<4>(nt, grid, stream, bucket_ids_d, owner_off_d, kp, kf, a, (char*)cache_d,
                          slot_of_d, (const char*)src_cache_d, old_slot, sa, status_d);
   GG_LAUNCH_CHECK("k_stage_rows");
+  return GG_OK;
+}
+
+extern "C" size_t gg_ws_stage_inplace(int64_t cap, int64_t cache_rows, int32_t num_parts) {
+  return inplace_ws_layout(std::max<int64_t>(cap, 0), std::max<int64_t>(cache_rows, 0),
+                           std::max(num_parts, 1), nullptr, nullptr);
+}
+
+extern "C" int gg_stage_inplace(const int32_t* bucket_ids_d, const int64_t* owner_off_d,
+                                int64_t cap, const gg_part_t* part, const gg_feat_t* feat,
+                                void* cache_d, int64_t cache_stride, int64_t cache_rows,
+                                int32_t* slot_of_d, const int32_t* clear_ids_d,
+                                const int64_t* clear_count_d, const int32_t* prev_slot_of_d,
+                                const uint8_t* occ_prev_d, uint8_t* occ_d,
+                                gg_stage_stats_t* stats_d, int32_t* status_d, void* ws,
+                                size_t ws_bytes, hipStream_t stream) {
+  GG_REQUIRE(owner_off_d && slot_of_d && occ_d && stats_d && status_d, "NULL argument");
+  GG_REQUIRE(cap >= 0 && cap < (1LL << 31), "bad capacity");
+  GG_REQUIRE(cache_rows >= 0 && cache_rows < (1LL << 31), "bad cache_rows");
+  GG_REQUIRE(cap == 0 || bucket_ids_d, "bucket ids are NULL");
+  GG_REQUIRE(cache_rows == 0 || cache_d, "cache is NULL");
+  GG_REQUIRE((clear_ids_d == nullptr) == (clear_count_d == nullptr),
+             "clear_ids and clear_count must both be given or both be NULL");
+  GG_REQUIRE((prev_slot_of_d == nullptr) == (occ_prev_d == nullptr),
+             "prev_slot_of and occ_prev must both be given or both be NULL");
+  GG_REQUIRE(prev_slot_of_d != slot_of_d, "the previous remap must be another buffer");
+  GG_REQUIRE(occ_prev_d != occ_d, "the previous occupancy must be another buffer");
+  KPart kp;
+  int rc = pack_part(part, &kp);
+  if (rc != GG_OK) return rc;
+  KFeat kf;
+  rc = pack_feat(feat, part, &kf);
+  if (rc != GG_OK) return rc;
+  GG_REQUIRE(cache_stride >= kf.row_bytes && cache_stride % 4 == 0, "cache_stride %lld invalid",
+             (long long)cache_stride);
+  InplaceWs w;
+  const size_t need_ws = inplace_ws_layout(cap, cache_rows, kp.P, (char*)ws, &w);
+  GG_REQUIRE(ws && ws_bytes >= need_ws, "workspace of %zu bytes < %zu", ws_bytes, need_ws);
+  bool v16 = aligned16(cache_d) && cache_stride % 16 == 0;
+  for (int m = 0; m < kf.P; ++m)
+    if (kf.rows[m] > 0) v16 = v16 && aligned16(kf.shard[m]) && kf.stride[m] % 16 == 0;
+  StageArgs a;
+  a.cap = cap;
+  a.cache_rows = cache_rows;
+  a.cache_stride = cache_stride;
+  a.tile = copy_tile(kf.row_bytes, 32768);
+  a.pad_ = 0;
+  a.geom = copy_geom(kf.row_bytes, v16 ? 16 : 4);
+  static const bool nt = env_flag("GG_NT_STAGE", false);
+  GG_REQUIRE(((uintptr_t)occ_d & 15u) == 0 && ((uintptr_t)occ_prev_d & 15u) == 0,
+             "occupancy maps must be 16-byte aligned");
+  const int gridp = inplace_prep_blocks(cap, cache_rows);
+  hipLaunchKernelGGL(k_inplace_prep, dim3(gridp), dim3(kBlock), 0, stream, bucket_ids_d,
+                     owner_off_d, kp, a, prev_slot_of_d, w.old_slot, w.dcnt, w.dr, w.btot,
+                     clear_ids_d, clear_count_d, slot_of_d, occ_prev_d, w.fcnt, occ_d, status_d);
+  GG_LAUNCH_CHECK("k_inplace_prep");
+  const int32_t nch = occ_prev_d ? (int32_t)cdiv(cache_rows, kOccChunk) : 0;
+  hipLaunchKernelGGL(k_inplace_emit, dim3(std::max(nch, 1)), dim3(kBlock), 0, stream, occ_prev_d,
+                     w.fcnt, nch, w.btot, gridp, w.bpre, w.freel, w.nfree, a);
+  GG_LAUNCH_CHECK("k_inplace_emit");
+  const int64_t ntiles = cdiv(std::min(cap, cache_rows), a.tile);
+  static const int host_cap = env_int("GG_STAGE_HOST_BLOCKS", 128);
+  static const int hbm_cap = env_int("GG_STAGE_BLOCKS", 16384);
+  int64_t gmax = hbm_cap;
+  if (host_cap > 0 && host_shards(kf) > 0) gmax = host_cap;
+  const int grid = (int)std::min<int64_t>(std::max<int64_t>(cdiv(ntiles, kBlock / kWave), 1), gmax);
+  StageStatsArgs sa;
+  sa.prev_count = clear_count_d;
+  sa.dcnt = w.dcnt;
+  sa.stats = stats_d;
+  sa.nblk_delta = gridp;
+  sa.has_src = prev_slot_of_d ? 1 : 0;
+  const bool fl = occ_prev_d != nullptr;
+  if (v16) {
+    if (nt)
+      hipLaunchKernelGGL((k_inplace_rows<16, true>), dim3(grid), dim3(kBlock), 0, stream,
+                         bucket_ids_d, owner_off_d, kp, kf, a, (char*)cache_d, slot_of_d,
+                         w.old_slot, w.dr, w.bpre, gridp, w.freel, w.nfree, fl, occ_d, sa, status_d);
+    else
+      hipLaunchKernelGGL((k_inplace_rows<16, false>), dim3(grid), dim3(kBlock), 0, stream,
+                         bucket_ids_d, owner_off_d, kp, kf, a, (char*)cache_d, slot_of_d,
+                         w.old_slot, w.dr, w.bpre, gridp, w.freel, w.nfree, fl, occ_d, sa, status_d);
+  } else {
+    if (nt)
+      hipLaunchKernelGGL((k_inplace_rows<4, true>), dim3(grid), dim3(kBlock), 0, stream,
+                         bucket_ids_d, owner_off_d, kp, kf, a, (char*)cache_d, slot_of_d,
+                         w.old_slot, w.dr, w.bpre, gridp, w.freel, w.nfree, fl, occ_d, sa, status_d);
+    else
+      hipLaunchKernelGGL((k_inplace_rows<4, false>), dim3(grid), dim3(kBlock), 0, stream,
+                         bucket_ids_d, owner_off_d, kp, kf, a, (char*)cache_d, slot_of_d,
+                         w.old_slot, w.dr, w.bpre, gridp, w.freel, w.nfree, fl, occ_d, sa, status_d);
+  }
+  GG_LAUNCH_CHECK("k_inplace_rows");
   return GG_OK;
 }

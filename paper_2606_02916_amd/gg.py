@@ -110,6 +110,7 @@ SIGNATURES = {
     "gg_ws_hotset": (_SZ, [_I64, _I32]),
     "gg_ws_bucket": (_SZ, [_I64, _I32]),
     "gg_ws_stage": (_SZ, [_I64, _I32]),
+    "gg_ws_stage_inplace": (_SZ, [_I64, _I64, _I32]),
     "gg_ws_gather": (_SZ, [_I64, _I32, _I32]),
     "gg_sample_window": (C.c_int, [_P, _P, _P, _I32, _P, _I32, _U64, _I32, _I64, _P, _P, _P, _SZ,
                                    _P]),
@@ -118,6 +119,8 @@ SIGNATURES = {
     "gg_bucket_by_owner": (C.c_int, [_P, _P, _I64, _P, _I32, _P, _P, _P, _P, _SZ, _P]),
     "gg_stage_bulk": (C.c_int, [_P, _P, _I64, _P, _P, _P, _I64, _I64, _P, _P, _P, _P, _P, _P, _P,
                                 _P, _SZ, _P]),
+    "gg_stage_inplace": (C.c_int, [_P, _P, _I64, _P, _P, _P, _I64, _I64, _P, _P, _P, _P, _P,
+                                   _P, _P, _P, _P, _SZ, _P]),
     "gg_gather_batch": (C.c_int, [_P, _P, _I32, _I64, _P, _P, _P, _I64, _I64, _P, _P, _I64, _I32,
                                   _P, _P, _P, _SZ, _P]),
     "gg_sim_accumulate": (C.c_int, [_P, _P, _I32, _P, _P, _P, _P]),
@@ -281,6 +284,27 @@ def gg_stage_bulk(bucket_ids, owner_off, cap, part, feat, cache, cache_stride, c
                                    _ptr(src_cache), _ptr(src_slot_of), _ptr(stats),
                                    _ptr(status), _ptr(ws), ws.numel(), _stream(stream)),
                  "gg_stage_bulk")
+
+
+def gg_ws_stage_inplace(cap, cache_rows, num_parts):
+    return int(lib.gg_ws_stage_inplace(cap, cache_rows, num_parts))
+
+
+def gg_stage_inplace(bucket_ids, owner_off, cap, part, feat, cache, cache_stride, cache_rows,
+                     slot_of, clear_ids, clear_count, prev_slot_of, occ_prev, occ, stats, status,
+                     ws, stream=None):
+    return check(lib.gg_stage_inplace(_ptr(bucket_ids), _ptr(owner_off), cap, C.byref(part),
+                                      C.byref(feat), _ptr(cache), cache_stride, cache_rows,
+                                      _ptr(slot_of), _ptr(clear_ids), _ptr(clear_count),
+                                      _ptr(prev_slot_of), _ptr(occ_prev), _ptr(occ), _ptr(stats),
+                                      _ptr(status), _ptr(ws), ws.numel(), _stream(stream)),
+                 "gg_stage_inplace")
+
+
+def occ_bytes(cache_rows):
+    """Bytes of a cache occupancy map (gg_stage_inplace): one per slot,
+    rounded up to a multiple of 32."""
+    return (int(cache_rows) + 31) // 32 * 32
 
 
 def gg_gather_batch(in_ids, bounds_ptr, nseg, n_cap, part, feat, cache, cache_stride, cache_rows,

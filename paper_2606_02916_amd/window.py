@@ -10,10 +10,11 @@ ID-to-slot remap with the miss path.
 FetchPipeline runs the five calls in order on one stream.  With delta=True
 it keeps two caches and requests only the rebuild delta
 Delta_{k,m} = (H_k in owner m) minus C_{k-1} from the owners, copying the
-rows it retains from the previous cache (Sec. IV-A, Eq. (1)).
-LookaheadPipeline is the paper's pipelined runtime (Algorithm 1, Sec.
-IV-C): window k+1 is sampled and bucketed on one stream while window k is
-delta-staged and gathered on another.
+rows it retains from the previous cache (Sec. IV-A, Eq. (1)); with
+inplace=True it keeps one persistent cache in which those rows stay where
+they are.  LookaheadPipeline is the paper's pipelined runtime (Algorithm 1,
+Sec. IV-C) on a persistent cache: window k+1 is sampled, bucketed and
+staged while window k is gathered.
 """
 from __future__ import annotations
 
@@ -45,6 +46,8 @@ class _Geometry:
         self.out_cap = max(lev, 1)                      # rows of one N_b
         remote = N - (int(shard_rows[local_owner]) if local_owner >= 0 else 0)
         self.hot_cap = max(1, min(remote, W * self.out_cap))
+        # a persistent cache holds two consecutive windows' hot sets
+        self.inplace_rows = max(1, min(remote, 2 * W * self.out_cap))
         self.win_cap = W * self.out_cap                 # rows of a whole window
         self.seed_cap = W * max(min(max_batch, N), 1)   # F_0 rows of a whole window
         self.ws_bytes = max(gg.gg_ws_sample(N, W), gg.gg_ws_hotset(N, W),
@@ -55,9 +58,11 @@ class _Geometry:
 
 class _Buffers:
     """Everything one window writes: sampling outputs, hot set, cache and
-    remap, workspace, statistics and (lazily) the window's gathered rows."""
+    remap, workspace, statistics and (lazily) the window's gathered rows.
+    With own_cache=False the cache is the pipeline's persistent one and the
+    set holds an occupancy bitmap of it instead."""
 
-    def __init__(self, g: _Geometry, dev):
+    def __init__(self, g: _Geometry, dev, own_cache=True):
         self.g, self.dev = g, dev
         self.frontier_ids = torch.empty(max(g.fcap, 1), dtype=torch.int32, device=dev)
         self.frontier_off = torch.zeros((g.L + 1) * g.W + 1, dtype=torch.int64, device=dev)
@@ -70,7 +75,10 @@ class _Buffers:
         self.hot_ids = torch.empty(g.hot_cap, dtype=torch.int32, device=dev)
         self.hot_freq = torch.empty(g.hot_cap, dtype=torch.int32, device=dev)
         self.owner_off = torch.zeros(g.P + 1, dtype=torch.int64, device=dev)
-        self.cache = torch.empty((g.hot_cap, g.cache_stride), dtype=torch.uint8, device=dev)
+        self.cache = (torch.empty((g.hot_cap, g.cache_stride), dtype=torch.uint8, device=dev)
+                      if own_cache else None)
+        self.occ = (None if own_cache else
+                    torch.zeros(gg.occ_bytes(g.inplace_rows), dtype=torch.uint8, device=dev))
         self.slot_of = torch.full((g.N,), -1, dtype=torch.int32, device=dev)
         self.ws = torch.empty(g.ws_bytes, dtype=torch.uint8, device=dev)
         self.stage_stats = torch.zeros(gg.STAGE_STATS_BYTES, dtype=torch.uint8, device=dev)
@@ -95,7 +103,12 @@ class _Buffers:
 class FetchPipeline:
     def __init__(self, row_ptr, col_idx, num_parts, part_kind, local_owner, range_start, shards,
                  shard_rows, row_bytes, stride, W, fanout, max_batch, n_hot=-1, device=None,
-                 out_buffers=2, cache_stride=None, delta=False, hot_frac=None):
+                 out_buffers=2, cache_stride=None, delta=False, hot_frac=None, inplace=False):
+        """delta: rebuild the cache from the previous window's, requesting only
+        the rebuild delta; the cache then alternates between two buffers and
+        the rows still wanted are copied across.  inplace (implies delta):
+        one persistent cache in which those rows stay put (gg_stage_inplace);
+        the remap then alternates between two buffers."""
         self.device = torch.device(device if device is not None else "cuda")
         self.N = int(row_ptr.numel() - 1)
         self.W = int(W)
@@ -109,7 +122,8 @@ class FetchPipeline:
         self.cache_stride = int(cache_stride) if cache_stride else self.stride
         self.n_hot = int(n_hot)
         self.hot_frac = hot_frac
-        self.delta = bool(delta)
+        self.inplace = bool(inplace)
+        self.delta = bool(delta) or self.inplace
         self.row_ptr, self.col_idx = row_ptr, col_idx
         self.shards = shards
         self.csr = gg.make_csr(row_ptr, col_idx)
@@ -119,18 +133,35 @@ class FetchPipeline:
                              shard_rows, self.stride, self.cache_stride)
         g, dev = self.geo, self.device
         self.out_cap, self.hot_cap, self.win_cap, self.wpb = g.out_cap, g.hot_cap, g.win_cap, g.wpb
-        self.buf = _Buffers(g, dev)
+        self.buf = _Buffers(g, dev, own_cache=not self.inplace)
         b = self.buf
         for name in ("frontier_ids", "frontier_off", "nbr_ids", "nbr_off", "frontier_bits", "need",
-                     "wsample", "hot_ids", "hot_freq", "owner_off", "slot_of", "ws",
+                     "wsample", "hot_ids", "hot_freq", "owner_off", "ws",
                      "stage_stats", "gather_stats"):
             setattr(self, name, getattr(b, name))
         self.status = torch.zeros(1, dtype=torch.int32, device=dev)
-        self.hot_count = [torch.zeros(2, dtype=torch.int64, device=dev) for _ in range(2)]
+        # Hot-set counts and bucket lists of the last nslot windows: the
+        # in-place remap of window k last held window k - 2, whose list
+        # clears it.
+        self.nslot = 3 if self.inplace else 2
+        self.hot_count = [torch.zeros(2, dtype=torch.int64, device=dev)
+                          for _ in range(self.nslot)]
         self.bucket_ids = [torch.empty(g.hot_cap, dtype=torch.int32, device=dev)
-                           for _ in range(2)]
-        # With delta staging the cache alternates between two buffers.
-        self.caches = [b.cache] + ([torch.empty_like(b.cache)] if self.delta else [])
+                           for _ in range(self.nslot)]
+        if self.inplace:
+            self.cache_rows = g.inplace_rows
+            self.caches = [torch.empty((g.inplace_rows, self.cache_stride), dtype=torch.uint8,
+                                       device=dev)]
+            self.slot_ofs = [b.slot_of, torch.full_like(b.slot_of, -1)]
+            self.occs = [torch.zeros(gg.occ_bytes(g.inplace_rows), dtype=torch.uint8,
+                                     device=dev) for _ in range(2)]
+            self.stage_ws = torch.empty(gg.gg_ws_stage_inplace(g.hot_cap, g.inplace_rows, self.P),
+                                        dtype=torch.uint8, device=dev)
+        else:
+            # With delta staging the cache alternates between two buffers.
+            self.cache_rows = g.hot_cap
+            self.caches = [b.cache] + ([torch.empty_like(b.cache)] if self.delta else [])
+            self.slot_ofs = [b.slot_of]
         self.outs = [torch.empty((g.out_cap, self.stride), dtype=torch.uint8, device=dev)
                      for _ in range(out_buffers)]
         self.k = 0
@@ -141,12 +172,18 @@ class FetchPipeline:
         return self.caches[(self.k - 1) % len(self.caches)] if self.k else self.caches[0]
 
     @property
+    def slot_of(self):
+        """The remap of window k (= self.k, advanced after the gathers)."""
+        return self.slot_ofs[self.k % len(self.slot_ofs)]
+
+    @property
     def win_out(self):
         """Output of a whole-window gather: the W batches' rows back to back."""
         return self.buf.win_out
 
     def reset_cache(self):
-        self.slot_of.fill_(-1)
+        for r in self.slot_ofs:
+            r.fill_(-1)
         self.k = 0
 
     # -- the five calls of one window ------------------------------------
@@ -166,9 +203,25 @@ class FetchPipeline:
                               self.bucket_ids[cur], self.owner_off, self.status, self.ws,
                               flags=_bucket_flags(self.part))
 
+    def slot_index(self):
+        """Hot-set and bucket slot of window k (= self.k)."""
+        return self.k % self.nslot
+
     def stage(self, cur):
         """Rebuilds the cache for window k (= self.k, advanced by the caller)."""
-        prev = 1 - cur
+        if self.inplace:
+            k = self.k
+            X = k % 2
+            old = (k - 2) % self.nslot          # the window this remap held
+            gg.gg_stage_inplace(self.bucket_ids[cur], self.owner_off, self.hot_cap, self.part,
+                                self.feat, self.caches[0], self.cache_stride, self.cache_rows,
+                                self.slot_ofs[X], self.bucket_ids[old] if k >= 2 else None,
+                                self.hot_count[old] if k >= 2 else None,
+                                self.slot_ofs[1 - X] if k >= 1 else None,
+                                self.occs[1 - X] if k >= 1 else None, self.occs[X],
+                                self.stage_stats, self.status, self.stage_ws)
+            return
+        prev = (cur - 1) % self.nslot
         have_prev = self.k > 0
         nc = len(self.caches)
         cache = self.caches[self.k % nc]
@@ -189,7 +242,7 @@ class FetchPipeline:
         bounds = self.frontier_off.data_ptr() + 8 * (self.L * Wk + b)
         stats = self.gather_stats.data_ptr() + b * gg.GATHER_STATS_BYTES
         gg.gg_gather_batch(self.frontier_ids, bounds, 1, out.shape[0], self.part, self.feat,
-                           self.staged_cache(), self.cache_stride, self.hot_cap, self.slot_of,
+                           self.staged_cache(), self.cache_stride, self.cache_rows, self.slot_of,
                            out, self.stride, stats, self.status, self.ws)
 
     def gather_window(self, Wk, out=None):
@@ -198,7 +251,7 @@ class FetchPipeline:
         out = self.win_out if out is None else out
         bounds = self.frontier_off.data_ptr() + 8 * (self.L * Wk)
         gg.gg_gather_batch(self.frontier_ids, bounds, Wk, out.shape[0], self.part, self.feat,
-                           self.staged_cache(), self.cache_stride, self.hot_cap, self.slot_of,
+                           self.staged_cache(), self.cache_stride, self.cache_rows, self.slot_of,
                            out, self.stride, self.gather_stats.data_ptr(), self.status, self.ws)
         return out
 
@@ -219,7 +272,7 @@ class FetchPipeline:
         sim: optional (coeffs, acc) to add the window to simulator totals;
         consumer: optional SageConsumer run on the window's rows (whole-window
         gather only), bracketed by the optional event pair consumer_events."""
-        cur = self.k & 1
+        cur = self.slot_index()
         ev = events if events is not None else [None] * 6
         _rec(ev[0])
         Wk = self.sample(seeds, seed_off, batch0, epoch, rng_seed)
@@ -269,7 +322,7 @@ class FetchPipeline:
         return fids, foff, nids, noff
 
     def hot_outputs(self, cur=None):
-        cur = ((self.k - 1) & 1) if cur is None else cur
+        cur = ((self.k - 1) % self.nslot) if cur is None else cur
         cnt = self.hot_count[cur].cpu().numpy()
         n = int(cnt[0])
         return (self.hot_ids[:n].cpu().numpy(), self.hot_freq[:n].cpu().numpy(), cnt,
@@ -296,14 +349,19 @@ class LookaheadPipeline:
     runs on the fetch stream and the gather gets a stream of its own,
     running beside the next window's staging.
 
-    `nsets` buffer sets rotate over the windows (window k uses set
-    k mod nsets); the default is three with shards in device memory and two
-    otherwise.  Building window k waits for the gather of window k - nsets,
-    the last reader of its set; with more sets the build may run further
-    ahead.  Bucket lists and hot-set counts rotate over 2 * nsets slots:
-    staging window k reads slot k and clears its remap with the slot of
-    window k - nsets while windows up to k + nsets - 1 are being built.
-    Every other reuse is ordered through the build wait or stream order."""
+    The cache is one persistent buffer (gg_stage_inplace): a row window k
+    shares with window k-1 stays in its slot, and only the delta is
+    fetched, into slots window k-1 does not occupy.  `nsets` buffer sets
+    (remap, occupancy map, sampling outputs) rotate over the windows (window
+    k uses set k mod nsets); the default is three with shards in device
+    memory and two otherwise.  Building window k waits for the gather of
+    window k - nsets, the last reader of its set; with more sets the build
+    may run further ahead.  Staging window k waits for the gather of window
+    k - 2, whose slots it may reuse.  Bucket lists and hot-set counts rotate
+    over 2 * nsets slots: staging window k reads slot k and clears its remap
+    with the slot of window k - nsets while windows up to k + nsets - 1 are
+    being built.  Every other reuse is ordered through these waits or stream
+    order."""
 
     def __init__(self, row_ptr, col_idx, num_parts, part_kind, local_owner, range_start, shards,
                  shard_rows, row_bytes, stride, W, fanout, max_batch, n_hot=-1, device=None,
@@ -332,8 +390,15 @@ class LookaheadPipeline:
             raise ValueError("the look-ahead pipeline needs at least two buffer sets")
         self.nsets = int(nsets)
         self.NSLOT = 2 * self.nsets
-        self.sets = [_Buffers(g, dev) for _ in range(self.nsets)]
-        self.stage_ws = torch.empty(g.ws_bytes, dtype=torch.uint8, device=dev)
+        self.sets = [_Buffers(g, dev, own_cache=False) for _ in range(self.nsets)]
+        # One persistent cache (gg_stage_inplace): rows a window shares with
+        # the previous one stay in their slot; each set keeps its remap and
+        # occupancy bitmap.
+        self.cache_rows = g.inplace_rows
+        self.cache = torch.empty((g.inplace_rows, self.cache_stride), dtype=torch.uint8,
+                                 device=dev)
+        self.stage_ws = torch.empty(gg.gg_ws_stage_inplace(g.hot_cap, g.inplace_rows, self.P),
+                                    dtype=torch.uint8, device=dev)
         self.gather_ws = torch.empty(g.ws_bytes, dtype=torch.uint8, device=dev)
         self.bucket_ids = [torch.empty(g.hot_cap, dtype=torch.int32, device=dev)
                            for _ in range(self.NSLOT)]
@@ -401,15 +466,18 @@ class LookaheadPipeline:
             if built is self.built[X]:
                 built.record(bs)
             ss.wait_event(built)
+        if k >= 2 and self.nsets > 2:
+            # staging may reuse the slots of window k-2's rows (with two sets
+            # the build already waited for that gather)
+            ss.wait_event(self.gathered[(k - 2) % self.nsets])
         C = (k - self.nsets) % self.NSLOT
         clear_ids = self.bucket_ids[C] if k >= self.nsets else None
         clear_cnt = self.hot_count[C] if k >= self.nsets else None
-        src = prev if k >= 1 else None
-        gg.gg_stage_bulk(self.bucket_ids[T], cur.owner_off, g.hot_cap, self.part, self.feat,
-                         cur.cache, self.cache_stride, g.hot_cap, cur.slot_of, clear_ids,
-                         clear_cnt, src.cache if src else None, src.slot_of if src else None,
-                         cur.stage_stats, self.status, self.stage_ws,
-                         stream=ss.cuda_stream)
+        gg.gg_stage_inplace(self.bucket_ids[T], cur.owner_off, g.hot_cap, self.part, self.feat,
+                            self.cache, self.cache_stride, self.cache_rows, cur.slot_of,
+                            clear_ids, clear_cnt, prev.slot_of if k >= 1 else None,
+                            prev.occ if k >= 1 else None, cur.occ, cur.stage_stats, self.status,
+                            self.stage_ws, stream=ss.cuda_stream)
         _rec(ev[4], ss)
         if gs is not ss:
             staged = ev[4] if ev[4] is not None else self.staged[X]
@@ -421,8 +489,8 @@ class LookaheadPipeline:
         o = cur.win_out if out is None else out
         bounds = cur.frontier_off.data_ptr() + 8 * (self.L * Wk)
         gg.gg_gather_batch(cur.frontier_ids, bounds, Wk, o.shape[0], self.part, self.feat,
-                           cur.cache, self.cache_stride, g.hot_cap, cur.slot_of, o, self.stride,
-                           cur.gather_stats.data_ptr(), self.status, self.gather_ws,
+                           self.cache, self.cache_stride, self.cache_rows, cur.slot_of, o,
+                           self.stride, cur.gather_stats.data_ptr(), self.status, self.gather_ws,
                            stream=gs.cuda_stream, flags=gg.GG_GATHER_SHARED)
         _rec(end, gs)
         if sim is not None:           # simulator totals, in window order on the gather stream
@@ -446,11 +514,12 @@ class LookaheadPipeline:
         """Launches the gather of a finished window again (same inputs, same
         output, same flags) on `stream` (default: the caller's current
         stream), e.g. to time it with the chip to itself.  The window must be
-        complete."""
+        complete, and no window after the next one staged (that staging may
+        reuse the window's slots)."""
         o = bufs.win_out if out is None else out
         bounds = bufs.frontier_off.data_ptr() + 8 * (self.L * Wk)
         gg.gg_gather_batch(bufs.frontier_ids, bounds, Wk, o.shape[0], self.part, self.feat,
-                           bufs.cache, self.cache_stride, self.geo.hot_cap, bufs.slot_of, o,
+                           self.cache, self.cache_stride, self.cache_rows, bufs.slot_of, o,
                            self.stride, bufs.gather_stats.data_ptr(), self.status,
                            self.gather_ws, stream=stream, flags=gg.GG_GATHER_SHARED)
         return o

@@ -20,7 +20,7 @@ class World:
 
     def __init__(self, inst, W=None, n_hot=-1, local_owner=None, fanout=None, batch=None,
                  device="cuda:0", shards=None, row_bytes=None, stride=None, cache_stride=None,
-                 tensors=None, delta=False, hot_frac=None):
+                 tensors=None, delta=False, hot_frac=None, inplace=False):
         wl = inst.wl
         self.inst = inst
         self.wl = wl
@@ -45,16 +45,26 @@ class World:
         self.pipe = FetchPipeline(self.row_ptr_d, self.col_idx_d, self.P, wl.part_kind, self.local,
                                   self.rs, self.shards_d, rows, self.row_bytes, self.stride,
                                   self.W, self.fanout, self.batch, n_hot=n_hot, device=self.dev,
-                                  cache_stride=cache_stride, delta=delta, hot_frac=hot_frac)
+                                  cache_stride=cache_stride, delta=delta, hot_frac=hot_frac,
+                                  inplace=inplace)
         self.part_ref = ggref.make_part(self.P, wl.part_kind, self.local, wl.num_nodes, self.rs)
         self.feat_ref = ggref.make_feat(self.row_bytes, self.shards, [self.stride] * self.P)
         self.cstride = self.pipe.cache_stride
-        self.delta = delta
+        self.delta = delta or inplace
+        self.inplace = inplace
         self.hot_frac = hot_frac
-        self.cache_refs = [np.zeros((self.pipe.hot_cap, self.cstride), dtype=np.uint8)
-                           for _ in range(2 if delta else 1)]
-        self.slot_ref = np.full(wl.num_nodes, -1, dtype=np.int32)
+        self.cache_refs = [np.zeros((self.pipe.cache_rows, self.cstride), dtype=np.uint8)
+                           for _ in range(2 if delta and not inplace else 1)]
+        # the in-place driver alternates two remaps, each cleared of the
+        # window it held two windows back
+        self.slot_refs = [np.full(wl.num_nodes, -1, dtype=np.int32)
+                          for _ in range(2 if inplace else 1)]
+        self.held = [None, None]
         self.prev_ref = None
+
+    @property
+    def slot_ref(self):
+        return self.slot_refs[self.pipe.k % len(self.slot_refs)]
 
     def window_inputs(self, k, W=None):
         W = W or self.W
@@ -72,7 +82,7 @@ class World:
         pipe, rb, st = self.pipe, self.row_bytes, self.stride
         L = len(self.fanout)
         seeds_d = torch.from_numpy(np.ascontiguousarray(seeds, dtype=np.int32)).to(self.dev)
-        cur = pipe.k & 1
+        cur = pipe.slot_index()
         Wk = pipe.sample(seeds_d, so, b0, epoch, rng_seed)
         pipe.hotset(Wk, cur)
         pipe.bucket(cur)
@@ -104,19 +114,32 @@ class World:
         assert np.array_equal(g_freq, freq)
         assert np.array_equal(g_bucket, bucket)
         assert np.array_equal(g_owner_off, owner_off)
-        # stage (delta mode: retained rows come from the previous cache)
+        # stage (delta mode: retained rows come from the previous cache;
+        # in place: they stay in their slots)
         kk, nc = pipe.k, len(self.cache_refs)
         cache_ref = self.cache_refs[kk % nc]
-        src = self.cache_refs[(kk - 1) % nc] if (self.delta and kk > 0) else None
-        sst = ggref.stage_bulk(bucket, owner_off, self.part_ref, self.feat_ref, cache_ref,
-                               self.cstride, self.slot_ref, self.prev_ref, src_cache=src,
-                               src_slot_of=self.slot_ref if src is not None else None)
+        H = len(hot)
+        if self.inplace:
+            X = kk % 2
+            sst = ggref.stage_inplace(bucket, owner_off, self.part_ref, self.feat_ref, cache_ref,
+                                      self.cstride, self.slot_refs[X],
+                                      self.slot_refs[1 - X] if kk > 0 else None,
+                                      clear_ids=self.held[X])
+            self.held[X] = bucket.copy()
+            slots = self.slot_ref[bucket]
+            assert np.all(slots >= 0)
+            g_rows = pipe.staged_cache()[torch.from_numpy(slots.astype(np.int64)).to(self.dev)]
+            assert np.array_equal(g_rows.cpu().numpy()[:, :rb], cache_ref[slots, :rb])
+        else:
+            src = self.cache_refs[(kk - 1) % nc] if (self.delta and kk > 0) else None
+            sst = ggref.stage_bulk(bucket, owner_off, self.part_ref, self.feat_ref, cache_ref,
+                                   self.cstride, self.slot_ref, self.prev_ref, src_cache=src,
+                                   src_slot_of=self.slot_ref if src is not None else None)
+            g_cache = pipe.staged_cache()[:H].cpu().numpy()
+            assert np.array_equal(g_cache[:, :rb], cache_ref[:H, :rb])
         self.prev_ref = bucket.copy()
         assert pipe.stage_stats_dict() == sst
         assert np.array_equal(pipe.slot_of.cpu().numpy(), self.slot_ref)
-        H = len(hot)
-        g_cache = pipe.staged_cache()[:H].cpu().numpy()
-        assert np.array_equal(g_cache[:, :rb], cache_ref[:H, :rb])
         # gathers, one batch at a time, then the whole window in one launch
         refs, gstats = [], []
         for b in range(Wk):

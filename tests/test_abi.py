@@ -154,6 +154,20 @@ def test_bad_arguments_are_rejected_on_the_host(gg):
     with pytest.raises(gg.GGError):
         gg.gg_stage_bulk(t, t, 10, part, feat, t, 256, 10, t, None, None, None, None, t, t, t, stream=0)
     part = gg.make_part(4, gg.PART_MOD, 0, 100)
+    feat = gg.make_feat(256, [t] * 4, [256] * 4, [25] * 4)
+    u = _FakeTensor(1 << 22, 1 << 20)
+    big = _FakeTensor(1 << 23, 1 << 30)
+    for prev, occ_prev, occ, what in [(t, t, u, "remap"),          # previous remap = this one
+                                      (u, None, t, "both"),        # occupancy without remap
+                                      (u, t, t, "occupancy")]:     # occupancy buffers shared
+        with pytest.raises(gg.GGError):
+            gg.gg_stage_inplace(t, t, 10, part, feat, t, 256, 10, t, None, None, prev, occ_prev,
+                                occ, t, t, big, stream=0)
+        assert what in gg.gg_last_error()
+    with pytest.raises(gg.GGError):                                      # workspace too small
+        gg.gg_stage_inplace(t, t, 10, part, feat, t, 256, 10, t, None, None, None, None, u, t, t,
+                            _FakeTensor(1 << 24, 16), stream=0)
+    assert "workspace" in gg.gg_last_error()
     feat = gg.make_feat(250, [t] * 4, [256] * 4, [25] * 4)              # row_bytes % 4 != 0
     with pytest.raises(gg.GGError):
         gg.gg_gather_batch(t, t.data_ptr(), 1, 10, part, feat, t, 256, 10, t, t, 256,

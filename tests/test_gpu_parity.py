@@ -483,6 +483,80 @@ def test_delta_staging_matches_oracle(name, n_hot, W):
             assert st["retained"] + sum(st["rows"]) == st["rows_total"]
 
 
+@pytest.mark.parametrize("name,n_hot,W,rows", [("small", -1, None, None), ("small", 3000, None, None),
+                                               ("tiny", -1, 1, None), ("tiny", 700, 2, (2408, 2416)),
+                                               ("tiny", -1, 4, (1036, 1040)), ("tiny", 0, 2, None)])
+def test_inplace_staging_matches_oracle(name, n_hot, W, rows):
+    """Delta staging into one persistent cache over consecutive windows:
+    the remap, every staged row at its slot (retained rows keep theirs, the
+    delta takes the lowest free slots in bucket order), the statistics and
+    every gathered row equal the oracle's; with 2,408-byte rows (tail
+    words), an unaligned 1,036-byte row (the 4-byte path) and budgets that
+    leave misses."""
+    log(f"{name}: in-place staging over consecutive windows, n_hot={n_hot}, W={W}, rows={rows}")
+    inst = synth.instance(name)
+    kw = {}
+    if rows:
+        rng = np.random.default_rng(11)
+        kw = dict(shards=[rng.integers(0, 256, size=(sh.shape[0], rows[1]), dtype=np.uint8)
+                          for sh in inst.shards], row_bytes=rows[0], stride=rows[1])
+    w = world(inst, n_hot=n_hot, W=W, inplace=True, **kw)
+    nwin = synth.n_windows(w.inst.batch_off, w.W)
+    for k in range(min(nwin, 5)):
+        r = w.run_and_compare(k)
+        st = r["stage"]
+        if k > 0 and n_hot != 0:
+            assert st["retained"] > 0
+        assert st["retained"] + sum(st["rows"]) == st["rows_total"]
+
+
+def test_inplace_staging_out_of_slots_leaves_misses():
+    """A persistent cache one slot short of two windows' hot sets: the
+    second staging raises GG_DEV_CAPACITY and leaves the last delta row out
+    of the remap, and the gathers still return every row, that one through
+    the miss path."""
+    log("small: in-place staging with a cache one slot short of two windows")
+    import torch as T
+    from oracle import ggref
+    from paper_2606_02916_amd import gg
+    inst = synth.instance("small")
+    wl = inst.wl
+    L = len(wl.fanout)
+    w = world(inst, inplace=True)
+    p = w.pipe
+    hot = []
+    for k in range(2):
+        seeds, so, b0 = w.window_inputs(k)
+        fids, foff, _, _ = ggref.sample_window(inst.row_ptr, inst.col_idx, seeds, so, wl.fanout,
+                                               0, 0, b0)
+        hot.append(ggref.build_hotset(fids, foff, len(so) - 1, L, w.part_ref, -1)[0])
+    union = len(set(hot[0].tolist()) | set(hot[1].tolist()))
+    assert union - 1 >= len(hot[0]) and union - 1 <= p.cache_rows
+    p.cache_rows = union - 1
+    for k in range(2):
+        seeds, so, b0 = w.window_inputs(k)
+        Wk = p.window(T.from_numpy(seeds).to(w.dev), so, b0)
+        T.cuda.synchronize()
+        st = p.read_status()
+        assert st == (0 if k == 0 else gg.DEV_CAPACITY), (k, st)
+    fids, foff, _, _ = p.sample_outputs(Wk)
+    remap = p.slot_ofs[1].cpu().numpy()
+    placed = remap[hot[1]] >= 0
+    assert placed.sum() == len(hot[1]) - 1
+    left_out = int(hot[1][~placed][0])
+    base = int(foff[L * Wk])
+    ids = fids[base:int(foff[(L + 1) * Wk])]
+    got = p.win_out[:len(ids), :wl.row_bytes].cpu().numpy()
+    rs = inst.range_start
+    for r_, u in enumerate(ids.tolist()):
+        m = helpers.owner_of(wl.part_kind, wl.num_parts, rs, u)
+        want = inst.shards[m][helpers.row_of(wl.part_kind, wl.num_parts, rs, u), :wl.row_bytes]
+        assert np.array_equal(got[r_], want), (r_, u)
+    misses = sum(p.gather_stats_dict(b)["misses"] for b in range(Wk))
+    assert misses == sum(int(left_out in fids[foff[L * Wk + b]:foff[L * Wk + b + 1]])
+                         for b in range(Wk)) > 0
+
+
 @pytest.mark.parametrize("name,n_hot,W,nsets,host,gev", [
     ("small", -1, None, 2, False, None), ("small", 3000, None, 2, False, "both"),
     ("tiny", -1, 1, 2, False, None), ("small", -1, None, None, False, "end"),
