@@ -430,6 +430,7 @@ def main():
             g_bytes += gbytes_w[k][b]
             n_launch += 1
     win_bytes = (g_bytes + (st_bytes if pcie is None else 0)) / K
+    stage_call = "gg_stage_inplace" if inplace_cache else "gg_stage_bulk"
     avg_ms = g_ms / n_launch
     avg_bytes = g_bytes / n_launch
     achieved = avg_bytes / (avg_ms * 1e-3) / 1e9
@@ -497,11 +498,11 @@ def main():
                                "shards over the whole window time (sampling, hot set and "
                                "bucketing not counted): the share of HBM the overlapped kernels "
                                "use together"},
-        "stage_roofline": ({"kernel": "gg_stage_bulk", "bound": "hbm",
+        "stage_roofline": ({"kernel": stage_call, "bound": "hbm",
                             "achieved": round(stage_gbs, 1),
                             "frac": round(stage_gbs / HBM_PEAK_GBS, 4), "unit": "GB/s"}
                            if pcie is None else
-                           {"kernel": "gg_stage_bulk", "bound": "pcie",
+                           {"kernel": stage_call, "bound": "pcie",
                             "achieved": round(st_host_bytes / (st_ms * 1e-3) / 1e9, 2),
                             "peak": PCIE5_X16_GBS, "unit": "GB/s",
                             "frac": round(st_host_bytes / (st_ms * 1e-3) / 1e9 / PCIE5_X16_GBS, 4),

@@ -261,11 +261,14 @@ int gg_stage_bulk(const int32_t* bucket_ids_d, const int64_t* owner_off_d, int64
  * touched.  Every other node is the delta Delta_{k,m}: it is requested from
  * its owner m (one request per owner with a non-empty delta, the indicator
  * of Eq. (1)) and takes, in bucket order, the lowest slot below cache_rows
- * that the previous window does not occupy.  occ_prev_d is that occupancy,
- * one byte per slot (non-zero = in use; cache_rows rounded up to a multiple
- * of 32 bytes, 16-byte aligned) that the previous call wrote as occ_d;
- * occ_d (another buffer of the same size) receives this window's.  With
- * prev_slot_of_d and occ_prev_d
+ * that the previous window does not occupy.  occ_prev_d is that occupancy
+ * as the previous call wrote it to its occ_d; occ_d (another buffer of the
+ * same size) receives this window's.  An occupancy buffer is 16-byte
+ * aligned and holds 16 + cache_rows rounded up to a multiple of 32 bytes:
+ * an int64 extent (one past the highest slot any window has used; slots
+ * from there on are free), 8 bytes of padding and one byte per slot
+ * (non-zero = in use), valid below the extent.  With prev_slot_of_d and
+ * occ_prev_d
  * both NULL (a first window) every row is requested and takes slot = its
  * bucket position.  Only free slots are written, so the previous window's
  * gathers may run concurrently; the window before it must be finished.

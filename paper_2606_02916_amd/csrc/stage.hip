@@ -221,7 +221,10 @@ int stage_delta_blocks(int64_t cap) {
 // In-place staging into one persistent cache.  The delta rows of window k
 // take, in bucket order, the lowest slots that window k-1 does not occupy;
 // rows window k-1 cached keep their slot and are not copied.  Occupancy is
-// one byte per slot (plain byte stores, no atomics).
+// one byte per slot (plain byte stores, no atomics) after a 16-byte header
+// holding the extent: one past the highest slot any window has used.  Free
+// slots are taken lowest first, so every slot from the extent on is free and
+// only the map below it is scanned.
 //   k_inplace_prep  old slot of every bucket entry (-1: delta, -2: bad id),
 //                   the delta count of every range of 64 entries and of
 //                   every block (block b takes ranges b*R .. b*R+R-1),
@@ -309,11 +312,17 @@ __device__ __forceinline__ int64_t ranges_per_block(int64_t n, int gp) {
   return cdiv_dev(cdiv_dev(n, kRange), gp);
 }
 
+constexpr int kOccHeader = 16;          // bytes before an occupancy map: int64 extent
+
 __global__ void __launch_bounds__(kBlock) k_inplace_prep(
     const int32_t* bucket, const int64_t* owner_off, KPart part, StageArgs a, const int32_t* prev,
     int32_t* old_slot, int32_t* dcnt, int32_t* dr, int32_t* btot, const int32_t* clear,
     const int64_t* clear_count, int32_t* slot_of, const uint8_t* occ_prev, int32_t* fcnt,
     uint8_t* occ, int32_t* status) {
+  // extent of the previous window's map (0 without one)
+  const int64_t ext = occ_prev ? *(const int64_t*)occ_prev : 0;
+  const uint8_t* map_prev = occ_prev ? occ_prev + kOccHeader : nullptr;
+  uint8_t* map = occ + kOccHeader;
   __shared__ int32_t hist[GG_MAX_PARTS];
   __shared__ int64_t s_start[GG_MAX_PARTS + 1];
   __shared__ int64_t lds[kBlock / kWave];
@@ -364,20 +373,22 @@ __global__ void __launch_bounds__(kBlock) k_inplace_prep(
       if (u >= 0 && (int64_t)u < part.N) slot_of[u] = -1;
     }
   }
-  const int64_t groups = cdiv_dev(a.cache_rows, 32);     // 32-slot groups
-  if (occ_prev) {
-    const int64_t nch = cdiv_dev(a.cache_rows, kOccChunk);
-    for (int64_t c = blockIdx.x; c < nch; c += gridDim.x) {
-      const int64_t g = c * kBlock + threadIdx.x;
-      const int64_t f = block_sum(g < groups ? __popc(free_mask(occ_prev, g, a.cache_rows)) : 0,
-                                  lds);
-      if (threadIdx.x == 0) fcnt[c] = (int32_t)f;
-    }
+  // free slots per chunk below the extent
+  const int64_t lim = ext < a.cache_rows ? ext : a.cache_rows;
+  const int64_t nch = cdiv_dev(lim, kOccChunk);
+  for (int64_t c = blockIdx.x; c < nch; c += gridDim.x) {
+    const int64_t g = c * kBlock + threadIdx.x;
+    const int64_t f = block_sum(__popc(free_mask(map_prev, g, lim)), lds);
+    if (threadIdx.x == 0) fcnt[c] = (int32_t)f;
   }
+  // the new map below the extent this window can reach
+  int64_t zl = lim + n;
+  zl = zl < a.cache_rows ? zl : a.cache_rows;
   const u32x4 z = {0u, 0u, 0u, 0u};
-  for (int64_t q = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; q < groups * 2;
+  for (int64_t q = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; q < cdiv_dev(zl, 32) * 2;
        q += (int64_t)gridDim.x * blockDim.x)
-    ((u32x4*)occ)[q] = z;
+    ((u32x4*)map)[q] = z;
+  if (blockIdx.x == 0 && threadIdx.x == 0) *(int64_t*)occ = lim;   // raised by the rows kernel
   if (st) set_status(status, st);
   __syncthreads();
   for (int m = threadIdx.x; m < part.P; m += blockDim.x) dcnt[(int64_t)blockIdx.x * part.P + m] = hist[m];
@@ -385,12 +396,12 @@ __global__ void __launch_bounds__(kBlock) k_inplace_prep(
 }
 
 // Block 0 writes the exclusive prefix of the prep blocks' delta counts
-// (bpre) and the number of free slots.  With a previous occupancy, block b
-// also writes the free slots of occupancy chunk b at their place in the
-// ascending free list, as far as the delta needs: staged in LDS, then
-// stored contiguously; chunks past the delta's last slot return at once.
+// (bpre) and the number of free slots below the previous extent.  Block b
+// writes the free slots of occupancy chunk b (below the extent) at their
+// place in the ascending free list, as far as the delta needs: staged in
+// LDS, then stored contiguously; other blocks return at once.
 __global__ void __launch_bounds__(kBlock) k_inplace_emit(const uint8_t* occ_prev,
-                                                         const int32_t* fcnt, int32_t nch,
+                                                         const int32_t* fcnt,
                                                          const int32_t* btot, int32_t gp,
                                                          int64_t* bpre, int32_t* freel,
                                                          int64_t* nfree, StageArgs a) {
@@ -398,6 +409,10 @@ __global__ void __launch_bounds__(kBlock) k_inplace_emit(const uint8_t* occ_prev
   __shared__ int32_t buf[kOccChunk];
   constexpr int PT = kPrepBlocks / kBlock;     // block counts per thread
   const int b = blockIdx.x;
+  const int64_t ext = occ_prev ? *(const int64_t*)occ_prev : 0;
+  const int64_t lim = ext < a.cache_rows ? ext : a.cache_rows;
+  const int64_t nch = cdiv_dev(lim, kOccChunk);
+  if (b > 0 && b >= nch) return;
   int32_t bt[PT];
   int64_t v = 0;
 #pragma unroll
@@ -416,12 +431,8 @@ __global__ void __launch_bounds__(kBlock) k_inplace_emit(const uint8_t* occ_prev
       run += bt[q];
     }
   }
-  if (!occ_prev) {
-    if (b == 0 && threadIdx.x == 0) *nfree = a.cache_rows;
-    return;
-  }
   int64_t w = 0, all = 0;
-  for (int c = threadIdx.x; c < nch; c += blockDim.x) {
+  for (int64_t c = threadIdx.x; c < nch; c += blockDim.x) {
     const int64_t x = fcnt[c];
     all += x;
     if (c < b) w += x;
@@ -431,30 +442,37 @@ __global__ void __launch_bounds__(kBlock) k_inplace_emit(const uint8_t* occ_prev
     all = block_sum(all, lds);
     if (threadIdx.x == 0) *nfree = all;
   }
-  if (before >= need) return;                      // the delta's slots lie before this chunk
+  if (b >= nch || before >= need) return;          // the delta's slots lie before this chunk
   const int64_t g = (int64_t)b * kBlock + threadIdx.x;
-  uint32_t f = free_mask(occ_prev, g, a.cache_rows);
+  uint32_t f = free_mask(occ_prev + kOccHeader, g, lim);
   int64_t tot;
   int64_t pos = block_excl_scan<kBlock>((int64_t)__popc(f), lds, &tot);
   for (; f; f &= f - 1u) buf[pos++] = (int32_t)(g * 32 + (__ffs(f) - 1));
   __syncthreads();
-  const int64_t lim = need - before < tot ? need - before : tot;
-  for (int64_t i = threadIdx.x; i < lim; i += blockDim.x) freel[before + i] = buf[i];
+  const int64_t cnt = need - before < tot ? need - before : tot;
+  for (int64_t i = threadIdx.x; i < cnt; i += blockDim.x) freel[before + i] = buf[i];
 }
 
 template <int VB, bool NT>
 __global__ void __launch_bounds__(kBlock) k_inplace_rows(
     const int32_t* bucket, const int64_t* owner_off, KPart part, KFeat feat, StageArgs a,
     char* cache, int32_t* slot_of, const int32_t* old_slot, const int32_t* dr,
-    const int64_t* bpre, int32_t gp, const int32_t* freel, const int64_t* nfree_p,
-    bool have_free_list, uint8_t* occ, StageStatsArgs sa, int32_t* status) {
+    const int32_t* btot, const int64_t* bpre, int32_t gp, const int32_t* freel,
+    const int64_t* nfree_p, const uint8_t* occ_prev, uint8_t* occ, StageStatsArgs sa,
+    int32_t* status) {
   if (blockIdx.x == 0) stage_stats(owner_off, part, a, feat.row_bytes, sa, status);
   __shared__ int64_t s_start[GG_MAX_PARTS + 1];
   for (int t = threadIdx.x; t <= GG_MAX_PARTS; t += blockDim.x) s_start[t] = part.start[t];
   __syncthreads();
   const int64_t n = stage_n(owner_off, part.P, a);
   const int64_t R = ranges_per_block(n, gp);
+  // delta rank j takes free-list entry j below the previous extent, and
+  // slot ext + (j - nfree) above it
+  const int64_t ext0 = occ_prev ? *(const int64_t*)occ_prev : 0;
+  const int64_t ext = ext0 < a.cache_rows ? ext0 : a.cache_rows;
   const int64_t nfree = *nfree_p;
+  const int64_t need = bpre[gp - 1] + btot[gp - 1];
+  uint8_t* map = occ + kOccHeader;
   const int64_t ntiles = (n + a.tile - 1) / a.tile;
   const int lane = lane_id();
   int32_t st = 0;
@@ -485,11 +503,12 @@ __global__ void __launch_bounds__(kBlock) k_inplace_rows(
         st |= GG_DEV_BAD_ID;
       } else if (old >= 0) {
         slot_of[u] = old;                                    // retained in place
-        occ[old] = 1;
+        map[old] = 1;
       } else {
         const int64_t jj = j + lanes_below(fm);
-        int64_t slot = -1;
-        if (jj < nfree) slot = have_free_list ? (int64_t)freel[jj] : jj;
+        const int64_t slot = jj < nfree ? (int64_t)freel[jj] : ext + (jj - nfree);
+        if (jj == need - 1 && slot < a.cache_rows && slot + 1 > ext)
+          *(int64_t*)occ = slot + 1;                         // the last delta row: new extent
         if (slot < 0 || slot >= a.cache_rows) {
           st |= GG_DEV_CAPACITY;
         } else {
@@ -501,7 +520,7 @@ __global__ void __launch_bounds__(kBlock) k_inplace_rows(
             src = (long long)(feat.shard[m] + r * feat.stride[m]);   // requested from owner m
             dst = (long long)(cache + slot * a.cache_stride);
             slot_of[u] = (int32_t)slot;
-            occ[slot] = 1;
+            map[slot] = 1;
           }
         }
       }
@@ -664,9 +683,10 @@ extern "C" int gg_stage_inplace(const int32_t* bucket_ids_d, const int64_t* owne
                      owner_off_d, kp, a, prev_slot_of_d, w.old_slot, w.dcnt, w.dr, w.btot,
                      clear_ids_d, clear_count_d, slot_of_d, occ_prev_d, w.fcnt, occ_d, status_d);
   GG_LAUNCH_CHECK("k_inplace_prep");
+  // blocks past the previous extent's chunks return at once
   const int32_t nch = occ_prev_d ? (int32_t)cdiv(cache_rows, kOccChunk) : 0;
   hipLaunchKernelGGL(k_inplace_emit, dim3(std::max(nch, 1)), dim3(kBlock), 0, stream, occ_prev_d,
-                     w.fcnt, nch, w.btot, gridp, w.bpre, w.freel, w.nfree, a);
+                     w.fcnt, w.btot, gridp, w.bpre, w.freel, w.nfree, a);
   GG_LAUNCH_CHECK("k_inplace_emit");
   const int64_t ntiles = cdiv(std::min(cap, cache_rows), a.tile);
   static const int host_cap = env_int("GG_STAGE_HOST_BLOCKS", 128);
@@ -680,25 +700,24 @@ extern "C" int gg_stage_inplace(const int32_t* bucket_ids_d, const int64_t* owne
   sa.stats = stats_d;
   sa.nblk_delta = gridp;
   sa.has_src = prev_slot_of_d ? 1 : 0;
-  const bool fl = occ_prev_d != nullptr;
   if (v16) {
     if (nt)
       hipLaunchKernelGGL((k_inplace_rows<16, true>), dim3(grid), dim3(kBlock), 0, stream,
                          bucket_ids_d, owner_off_d, kp, kf, a, (char*)cache_d, slot_of_d,
-                         w.old_slot, w.dr, w.bpre, gridp, w.freel, w.nfree, fl, occ_d, sa, status_d);
+                         w.old_slot, w.dr, w.btot, w.bpre, gridp, w.freel, w.nfree, occ_prev_d, occ_d, sa, status_d);
     else
       hipLaunchKernelGGL((k_inplace_rows<16, false>), dim3(grid), dim3(kBlock), 0, stream,
                          bucket_ids_d, owner_off_d, kp, kf, a, (char*)cache_d, slot_of_d,
-                         w.old_slot, w.dr, w.bpre, gridp, w.freel, w.nfree, fl, occ_d, sa, status_d);
+                         w.old_slot, w.dr, w.btot, w.bpre, gridp, w.freel, w.nfree, occ_prev_d, occ_d, sa, status_d);
   } else {
     if (nt)
       hipLaunchKernelGGL((k_inplace_rows<4, true>), dim3(grid), dim3(kBlock), 0, stream,
                          bucket_ids_d, owner_off_d, kp, kf, a, (char*)cache_d, slot_of_d,
-                         w.old_slot, w.dr, w.bpre, gridp, w.freel, w.nfree, fl, occ_d, sa, status_d);
+                         w.old_slot, w.dr, w.btot, w.bpre, gridp, w.freel, w.nfree, occ_prev_d, occ_d, sa, status_d);
     else
       hipLaunchKernelGGL((k_inplace_rows<4, false>), dim3(grid), dim3(kBlock), 0, stream,
                          bucket_ids_d, owner_off_d, kp, kf, a, (char*)cache_d, slot_of_d,
-                         w.old_slot, w.dr, w.bpre, gridp, w.freel, w.nfree, fl, occ_d, sa, status_d);
+                         w.old_slot, w.dr, w.btot, w.bpre, gridp, w.freel, w.nfree, occ_prev_d, occ_d, sa, status_d);
   }
   GG_LAUNCH_CHECK("k_inplace_rows");
   return GG_OK;

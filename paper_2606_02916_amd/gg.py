@@ -302,9 +302,9 @@ def gg_stage_inplace(bucket_ids, owner_off, cap, part, feat, cache, cache_stride
 
 
 def occ_bytes(cache_rows):
-    """Bytes of a cache occupancy map (gg_stage_inplace): one per slot,
-    rounded up to a multiple of 32."""
-    return (int(cache_rows) + 31) // 32 * 32
+    """Bytes of a cache occupancy buffer (gg_stage_inplace): a 16-byte
+    header and one byte per slot, rounded up to a multiple of 32."""
+    return 16 + (int(cache_rows) + 31) // 32 * 32
 
 
 def gg_gather_batch(in_ids, bounds_ptr, nseg, n_cap, part, feat, cache, cache_stride, cache_rows,
