@@ -431,6 +431,9 @@ def main():
             n_launch += 1
     win_bytes = (g_bytes + (st_bytes if pcie is None else 0)) / K
     stage_call = "gg_stage_inplace" if inplace_cache else "gg_stage_bulk"
+    # per-window times: between consecutive windows' last gather ends (the
+    # first timed window has no predecessor event and is left out)
+    win_ms = [gevs[i - 1][-1][1].elapsed_time(gevs[i][-1][1]) for i in range(1, K)]
     avg_ms = g_ms / n_launch
     avg_bytes = g_bytes / n_launch
     achieved = avg_bytes / (avg_ms * 1e-3) / 1e9
@@ -510,6 +513,11 @@ def main():
                             "note": "host bytes the staging kernel reads over PCIe; peak is the "
                                     "PCIe 5.0 x16 link rate, dma_copy_gbps a measured "
                                     "pinned-to-device copy of 1 GiB"}),
+        "window_ms": ({"median": round(float(np.median(win_ms)), 4),
+                       "min": round(float(np.min(win_ms)), 4),
+                       "max": round(float(np.max(win_ms)), 4), "windows": len(win_ms),
+                       "note": "between consecutive windows' last gather ends"}
+                      if win_ms else None),
         "stage_ms_median": {k: round(float(np.median(v)), 4) for k, v in stage_ms.items() if v},
         "rows_per_window": int(np.mean(rows_w)),
         "hot_set_rows_per_window": int(np.mean(hot_w)),
