@@ -208,6 +208,9 @@ def main():
                     help="with --simulate: budgets relative to each window, e.g. 1/10,1/4: the "
                          "top fraction of the window's distinct remote nodes; the hit ratio is "
                          "then the share of remote requests that fraction covers")
+    ap.add_argument("--graph", action="store_true",
+                    help="time the sequential driver launched call by call against the same "
+                         "windows replayed from HIP graphs; prints one JSON line")
     ap.add_argument("--ablation", action="store_true",
                     help="measure per-row requests against bulk requests, rows per wavefront "
                          "copy step, and (host-resident shards) zero-copy staging against "
@@ -254,6 +257,8 @@ def main():
         return simulate(args, wl)
     if args.ablation:
         return ablation(args, wl)
+    if args.graph:
+        return graph_mode(args, wl)
     W = args.W or wl.W
     t = time.time()
     inst, row_ptr_d, col_idx_d, shards_d = synth.torch_instance(args.config, dev)
@@ -795,6 +800,82 @@ def ablation(args, wl):
         del pack, dma
     print(json.dumps({"ablation": args.config, "W": W, "window_rows": g_rows, "hot_set": H,
                       **res}), flush=True)
+
+
+def graph_mode(args, wl):
+    """The sequential driver (full restage, whole-window gather) launched call
+    by call against the same windows replayed from HIP graphs captured once
+    per window; one JSON line.  Every window's gathered rows from a replay
+    are compared byte for byte with the eager run's."""
+    import numpy as np
+    import torch
+
+    import synth
+    from paper_2606_02916_amd import FetchPipeline
+
+    dev = torch.device("cuda:0")
+    inst, row_ptr_d, col_idx_d, shards_d = synth.torch_instance(args.config, dev)
+    W = args.W or wl.W
+    L, rb = len(wl.fanout), wl.row_bytes
+    pipe = FetchPipeline(row_ptr_d, col_idx_d, wl.num_parts, wl.part_kind, wl.local_owner,
+                         inst.range_start, shards_d, [s.shape[0] for s in inst.shards], rb,
+                         wl.row_stride, W, wl.fanout, wl.batch_size, device=dev)
+    boff = inst.batch_off
+    nwin = synth.n_windows(boff, W)
+    wins = []
+    for k in range(nwin):
+        b0, b1 = synth.window_batches(boff, W, k)
+        s = torch.from_numpy(inst.seeds[boff[b0]:boff[b1]].copy()).to(dev)
+        wins.append((s, boff[b0:b1 + 1] - boff[b0], b0))
+    graphs = [pipe.capture_window(s, so, b0) for s, so, b0 in wins]
+    torch.cuda.synchronize()
+
+    def rows_now(Wk):
+        fo = pipe.frontier_off[:(L + 1) * Wk + 1].cpu().numpy()
+        return int(fo[-1] - fo[L * Wk])
+
+    nrows, same = [], True
+    for k, (s, so, b0) in enumerate(wins):
+        pipe.reset_cache()
+        Wk = pipe.window(s, so, b0)
+        torch.cuda.synchronize()
+        n = rows_now(Wk)
+        ref = pipe.win_out[:n, :rb].clone()
+        graphs[k][0].replay()
+        torch.cuda.synchronize()
+        same = same and rows_now(Wk) == n and bool(torch.equal(pipe.win_out[:n, :rb], ref))
+        nrows.append(n)
+        del ref
+    if pipe.read_status() != 0 or not same:
+        raise RuntimeError("graph replays differ from the eager windows")
+    K = args.steps
+    order = [i % nwin for i in range(K)]
+
+    def timed(fn):
+        for k in order[:nwin]:
+            fn(k)
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        for k in order:
+            fn(k)
+        torch.cuda.synchronize()
+        return (time.perf_counter() - t0) / K * 1e3
+
+    def eager(k):
+        s, so, b0 = wins[k]
+        pipe.reset_cache()
+        pipe.window(s, so, b0)
+
+    e_ms = timed(eager)
+    g_ms = timed(lambda k: graphs[k][0].replay())
+    rows = sum(nrows[k] for k in order) / K
+    print(json.dumps({"graph": args.config, "W": W, "windows": nwin, "steps": K,
+                      "rows_per_window": round(rows, 1),
+                      "eager_ms_per_window": round(e_ms, 4),
+                      "graph_ms_per_window": round(g_ms, 4),
+                      "speedup": round(e_ms / g_ms, 3),
+                      "graph_rows_per_s": round(rows / (g_ms * 1e-3), 1),
+                      "replays_equal_eager": same}), flush=True)
 
 
 def wsweep(args, wl):

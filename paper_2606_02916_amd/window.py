@@ -255,6 +255,31 @@ class FetchPipeline:
                            out, self.stride, self.gather_stats.data_ptr(), self.status, self.ws)
         return out
 
+    def capture_window(self, seeds, seed_off, batch0, epoch=0, rng_seed=0):
+        """Captures one whole window into a HIP graph on the current stream:
+        the remap reset (a fill kernel), then sampling, hot set, buckets,
+        staging and the whole-window gather into win_out.  Every replay
+        recomputes the window from `seeds` (refill it in place between
+        replays to change the seeds; its length and seed_off stay as
+        captured) into the same buffers, so a replay costs its kernels and
+        not their launches.  Full restage only: a replay starts from an empty
+        cache.  Returns (graph, number of batches)."""
+        if self.delta:
+            raise ValueError("graph capture replays full restages only")
+        self.win_out                       # allocated before the capture
+        cur = torch.cuda.current_stream(self.device)
+        side = torch.cuda.Stream(device=self.device)
+        side.wait_stream(cur)
+        with torch.cuda.stream(side):      # one eager pass first
+            self.reset_cache()
+            self.window(seeds, seed_off, batch0, epoch, rng_seed)
+        cur.wait_stream(side)
+        graph = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(graph):
+            self.reset_cache()
+            Wk = self.window(seeds, seed_off, batch0, epoch, rng_seed)
+        return graph, Wk
+
     def sim_accumulate(self, Wk, coeffs, acc):
         """Adds the window just gathered to the simulator totals `acc` (a
         device buffer of SIM_ACC_BYTES, zeroed before the first window)."""

@@ -483,6 +483,66 @@ def test_delta_staging_matches_oracle(name, n_hot, W):
             assert st["retained"] + sum(st["rows"]) == st["rows_total"]
 
 
+def test_window_graph_replays_match_eager():
+    """A whole sequential window captured into a HIP graph and replayed
+    three times, with eager GPU work, host synchronisation and a refill of
+    the seeds between replays: after every replay the sampled frontiers and
+    neighbour slots, hot set, buckets, remap, statistics and every gathered
+    row equal an eager run of the same seeds (at the captured batch index)."""
+    log("small: window graph replays against eager windows")
+    import torch as T
+    from paper_2606_02916_amd import FetchPipeline
+    inst = synth.instance("small")
+    wl = inst.wl
+    dev = T.device("cuda:0")
+    boff, W, L, rb = inst.batch_off, wl.W, len(wl.fanout), wl.row_bytes
+    wins = []
+    for k in range(2):
+        b0, b1 = synth.window_batches(boff, W, k)
+        wins.append((inst.seeds[boff[b0]:boff[b1]].copy(), boff[b0:b1 + 1] - boff[b0], b0))
+    assert np.array_equal(wins[0][1], wins[1][1])
+    so, b0 = wins[0][1], wins[0][2]
+    rp = T.from_numpy(inst.row_ptr).to(dev)
+    ci = T.from_numpy(inst.col_idx).to(dev)
+    sh = [T.from_numpy(x).to(dev) for x in inst.shards]
+
+    def make():
+        return FetchPipeline(rp, ci, wl.num_parts, wl.part_kind, wl.local_owner,
+                             inst.range_start, sh, [x.shape[0] for x in inst.shards], rb,
+                             wl.row_stride, W, wl.fanout, wl.batch_size, device=dev)
+
+    def snapshot(p, Wk):
+        fids, foff, nids, noff = p.sample_outputs(Wk)
+        hot, freq, cnt, bucket, owner_off = p.hot_outputs(0)
+        n = int(foff[(L + 1) * Wk] - foff[L * Wk])
+        return dict(fids=fids, foff=foff, nids=nids, noff=noff, hot=hot, freq=freq,
+                    bucket=bucket, owner_off=owner_off, remap=p.slot_of.cpu().numpy(),
+                    rows=p.win_out[:n, :rb].cpu().numpy(), stage=p.stage_stats_dict(),
+                    gather=[p.gather_stats_dict(b) for b in range(Wk)])
+
+    gpipe, epipe = make(), make()
+    seeds_buf = T.from_numpy(wins[0][0]).to(dev)
+    graph, Wk = gpipe.capture_window(seeds_buf, so, b0)
+    T.cuda.synchronize()
+    for rep, k in enumerate([0, 1, 0]):
+        seeds_buf.copy_(T.from_numpy(wins[k][0]).to(dev))
+        graph.replay()
+        T.cuda.synchronize()
+        got = snapshot(gpipe, Wk)
+        epipe.reset_cache()
+        epipe.window(T.from_numpy(wins[k][0]).to(dev), so, b0)
+        T.cuda.synchronize()
+        want = snapshot(epipe, Wk)
+        for key in want:
+            if isinstance(want[key], np.ndarray):
+                assert np.array_equal(got[key], want[key]), (rep, key)
+            else:
+                assert got[key] == want[key], (rep, key)
+        x = T.arange(1 << 20, device=dev, dtype=T.float32)     # eager work between replays
+        assert float((x * 2).max()) == 2.0 * ((1 << 20) - 1)
+    assert gpipe.read_status() == 0 and epipe.read_status() == 0
+
+
 @pytest.mark.parametrize("name,n_hot,W,rows", [("small", -1, None, None), ("small", 3000, None, None),
                                                ("tiny", -1, 1, None), ("tiny", 700, 2, (2408, 2416)),
                                                ("tiny", -1, 4, (1036, 1040)), ("tiny", 0, 2, None)])
