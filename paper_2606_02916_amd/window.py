@@ -418,7 +418,7 @@ class LookaheadPipeline:
         self.sets = [_Buffers(g, dev, own_cache=False) for _ in range(self.nsets)]
         # One persistent cache (gg_stage_inplace): rows a window shares with
         # the previous one stay in their slot; each set keeps its remap and
-        # occupancy bitmap.
+        # occupancy map.
         self.cache_rows = g.inplace_rows
         self.cache = torch.empty((g.inplace_rows, self.cache_stride), dtype=torch.uint8,
                                  device=dev)
