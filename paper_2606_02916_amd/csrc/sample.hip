@@ -115,6 +115,49 @@ __global__ void __launch_bounds__(kBlock) k_mark_seeds(const int32_t* seeds, See
   }
 }
 
+// Level 0 in one launch: block (c, b) assembles chunk c (kChunkWords
+// words) of batch b's bit set in LDS from the batch's seeds and stores it
+// whole, so the bit sets need no clearing pass and the seeds no global
+// atomics.  It also clears its part of the byte map (if any) and, spread
+// over the grid, the group totals.  Every block reads its batch's seeds, so
+// batches of at most kSeedBitsMaxBatch seeds take this path.
+constexpr int64_t kSeedBitsMaxBatch = 16384;
+
+__global__ void __launch_bounds__(kBlock) k_seed_bits(const int32_t* seeds, SeedOff so,
+                                                      uint32_t* bits, int64_t wpb, int64_t N,
+                                                      uint8_t* map, int32_t* btot, int32_t nbtot,
+                                                      int32_t* status) {
+  __shared__ uint32_t w[kChunkWords];
+  const int c = blockIdx.x, b = blockIdx.y;
+  const int64_t flat = ((int64_t)b * gridDim.x + c) * blockDim.x + threadIdx.x;
+  const int64_t nthreads = (int64_t)gridDim.x * gridDim.y * blockDim.x;
+  for (int64_t t = flat; t < nbtot; t += nthreads) btot[t] = 0;
+  for (int i = threadIdx.x; i < kChunkWords; i += blockDim.x) w[i] = 0u;
+  __syncthreads();
+  const int64_t lo = (int64_t)c * kChunkWords * 32, hi = lo + (int64_t)kChunkWords * 32;
+  int32_t st = 0;
+  for (int64_t i = so.off[b] + threadIdx.x; i < so.off[b + 1]; i += blockDim.x) {
+    const int32_t u = seeds[i];
+    if (u < 0 || (int64_t)u >= N) {
+      if (c == 0) st |= GG_DEV_BAD_ID;
+    } else if ((int64_t)u >= lo && (int64_t)u < hi) {
+      atomicOr(&w[(u - lo) >> 5], 1u << (u & 31));
+    }
+  }
+  __syncthreads();
+  u32x4* dst = (u32x4*)(bits + (int64_t)b * wpb + (int64_t)c * kChunkWords);
+  for (int i = threadIdx.x; i < kChunkWords / 4; i += blockDim.x) {
+    const u32x4 v = {w[4 * i], w[4 * i + 1], w[4 * i + 2], w[4 * i + 3]};
+    dst[i] = v;
+  }
+  if (map) {
+    u32x4* m = (u32x4*)(map + ((int64_t)b * wpb + (int64_t)c * kChunkWords) * 32);
+    const u32x4 z = {0u, 0u, 0u, 0u};
+    for (int i = threadIdx.x; i < kChunkWords * 2; i += blockDim.x) m[i] = z;
+  }
+  if (st) set_status(status, st);
+}
+
 // Popcount of one chunk (kChunkWords words) of one batch's bit set.  The
 // chunk's count goes to cnt and is added to its group's partial total (a
 // group is kGroupChunks consecutive chunks of one batch), spread over
@@ -393,7 +436,7 @@ __global__ void __launch_bounds__(kBlock) k_sample(const RowT* row_ptr, const in
 
 struct SampleWs {
   int32_t* cnt;       // per (batch, chunk) counts of the current level
-  int32_t* tot;       // per level: group totals; zeroed by k_zero_words
+  int32_t* tot;       // per level: group totals; zeroed by k_seed_bits (or k_zero_words)
   int32_t ngroups;    // groups of kGroupChunks chunks per batch
   int64_t tot_level;  // entries of tot per level
   LevelState* lvl;
@@ -480,14 +523,23 @@ extern "C" int gg_sample_window(const gg_csr_t* csr, const int32_t* seeds_d,
   const int64_t wpb = gg_bits_words(N);
   const int32_t nch = (int32_t)(wpb / kChunkWords);
 
-  const int64_t map4 = sw.map ? W * wpb * 2 : 0;   // 32 bytes per word, 16 per store
-  hipLaunchKernelGGL(k_zero_words, dim3((unsigned)std::min<int64_t>(cdiv(W * wpb / 4, kBlock), 4096)),
-                     dim3(kBlock), 0, stream, out->frontier_bits, W * wpb / 4, sw.map, map4, sw.tot,
-                     (int32_t)((L + 1) * sw.tot_level));
-  GG_LAUNCH_CHECK("k_zero_words");
   SeedOff so;
   for (int b = 0; b <= GG_MAX_W; ++b) so.off[b] = b <= W ? seed_off_h[b] : INT64_MAX;
-  if (seed_off_h[W] > 0) {
+  int64_t max_batch = 0;
+  for (int b = 0; b < W; ++b)
+    max_batch = std::max<int64_t>(max_batch, seed_off_h[b + 1] - seed_off_h[b]);
+  if (max_batch <= kSeedBitsMaxBatch) {
+    hipLaunchKernelGGL(k_seed_bits, dim3((unsigned)nch, (unsigned)W), dim3(kBlock), 0, stream,
+                       seeds_d, so, out->frontier_bits, wpb, N, sw.map, sw.tot,
+                       (int32_t)((L + 1) * sw.tot_level), status_d);
+    GG_LAUNCH_CHECK("k_seed_bits");
+  } else {
+    const int64_t map4 = sw.map ? W * wpb * 2 : 0;   // 32 bytes per word, 16 per store
+    hipLaunchKernelGGL(k_zero_words,
+                       dim3((unsigned)std::min<int64_t>(cdiv(W * wpb / 4, kBlock), 4096)),
+                       dim3(kBlock), 0, stream, out->frontier_bits, W * wpb / 4, sw.map, map4,
+                       sw.tot, (int32_t)((L + 1) * sw.tot_level));
+    GG_LAUNCH_CHECK("k_zero_words");
     hipLaunchKernelGGL(k_mark_seeds,
                        dim3((unsigned)std::min<int64_t>(cdiv(seed_off_h[W], kBlock), 4096)),
                        dim3(kBlock), 0, stream, seeds_d, so, W, out->frontier_bits, wpb, N,

@@ -114,6 +114,19 @@ def test_ragged_and_empty_batches():
     w.run_and_compare(0, seeds=seeds, so=so, b0=3)
 
 
+@pytest.mark.parametrize("sizes", [[16384, 3, 0], [16385, 700, 1]])
+def test_seed_batches_at_and_past_the_fused_level0_limit(sizes):
+    """Level 0 is built in one launch for batches of up to 16,384 seeds and
+    by a clearing pass plus atomic marks beyond; duplicated seeds either
+    way (batches larger than the graph's 10,000 nodes)."""
+    log(f"tiny: seed batches of {sizes}")
+    inst = synth.instance("tiny")
+    w = world(inst, W=len(sizes), batch=max(sizes))
+    seeds = np.random.default_rng(5).integers(0, inst.wl.num_nodes, sum(sizes)).astype(np.int32)
+    so = np.concatenate([[0], np.cumsum(sizes)]).astype(np.int64)
+    w.run_and_compare(0, seeds=seeds, so=so, b0=7)
+
+
 def test_fanout_above_every_degree_is_the_bfs_ball():
     log("hand graph: fanout above max degree")
     rng = np.random.default_rng(3)
