@@ -159,6 +159,24 @@ def summarize(args):
             f.write(f"# command (FETCH_SIZE, then WRITE_SIZE): {cmd}\n")
             f.write("# scale = known bytes of a 1 GiB device-to-device copy / counter reading\n")
             f.write(json.dumps(d, indent=1) + "\n")
+    if args.pmc_db:
+        # per-kernel averages of every counter in a rocprofv3 --pmc run
+        db = sqlite3.connect(args.pmc_db)
+        rows = db.execute("select kernel_name, counter_name, count(*), avg(value) from "
+                          "counters_collection group by kernel_name, counter_name").fetchall()
+        per = {}
+        for n, c, k, v in rows:
+            per.setdefault(_short(n), {})[c] = (k, v)
+        names = sorted({c for _, c, _, _ in rows})
+        out = [f"# rocprofv3 counters of bench.py, workload {wl}: per-dispatch averages",
+               f"# command: {cmd}",
+               f"{'kernel':40s} {'dispatches':>10s} " + " ".join(f"{c:>24s}" for c in names)]
+        for kn in sorted(per, key=lambda x: -max(v for _, v in per[x].values())):
+            k0 = max(k for k, _ in per[kn].values())
+            out.append(f"{kn:40s} {k0:10d} " + " ".join(
+                f"{per[kn][c][1]:24.1f}" if c in per[kn] else f"{'-':>24s}" for c in names))
+        with open(os.path.join(PROFILES, f"{args.pmc_out}_{wl}.txt"), "w") as f:
+            f.write("\n".join(out) + "\n")
     print("summaries written", file=sys.stderr)
 
 
@@ -223,6 +241,10 @@ def main():
     ap.add_argument("--fetch-db", default=None)
     ap.add_argument("--write-db", default=None)
     ap.add_argument("--summary-command", default="")
+    ap.add_argument("--pmc-db", default=None,
+                    help="with --summarize: a rocprofv3 --pmc database; writes per-kernel "
+                         "averages of its counters to profiles/<pmc-out>_<config>.txt")
+    ap.add_argument("--pmc-out", default="counters")
     ap.add_argument("--bench-json", default=None,
                     help="with --summarize: the JSON line bench.py printed in the traced run")
     ap.add_argument("--phases", default=None,
