@@ -49,6 +49,19 @@ __device__ __forceinline__ void seg_range(const int64_t* bounds, int s, const Ga
   *hi = h;
 }
 
+// Row ids and owners of one tile, loaded ahead of its copy.
+struct TileIds {
+  int32_t u;      // row id, or -1 for a lane past the tile or the segment
+  int32_t m;      // owner of u (-1 when u is absent or out of range)
+  int32_t s;      // slot of u for a remote owner, loaded one tile ahead
+  bool in;        // the lane holds a row of the segment
+};
+
+__device__ __forceinline__ bool tile_lane(int64_t t, int64_t ntiles, int64_t lo, int64_t hi,
+                                          int32_t tile, int lane) {
+  return t < ntiles && lane < tile && lo + t * tile + lane < hi;
+}
+
 template <int VB, bool NT, int U>
 __global__ void __launch_bounds__(kBlock) k_gather_rows(const int32_t* in_ids, const int64_t* bounds,
                                                         KPart part, KFeat feat, GatherArgs a,
@@ -66,39 +79,49 @@ __global__ void __launch_bounds__(kBlock) k_gather_rows(const int32_t* in_ids, c
   const int64_t begin = bounds[0];
   const int lane = lane_id();
   const int64_t ntiles = (hi - lo + a.tile - 1) / a.tile;
+  const int64_t step = (int64_t)gridDim.x * kTilesPerBlock;
   int32_t st = 0;
   int32_t c_local = 0, c_hit = 0;
-  for (int64_t t = (int64_t)blockIdx.x * kTilesPerBlock + threadIdx.x / kWave; t < ntiles;
-       t += (int64_t)gridDim.x * kTilesPerBlock) {
-    const int64_t r0 = lo + t * a.tile;
-    const int64_t i = r0 + lane;
+  // Software pipeline over the wave's tiles: while tile t is copied, the
+  // slots of tile t + step and the ids of tile t + 2 step are already in
+  // flight, so neither lookup waits in front of a copy.
+  auto load_ids = [&](int64_t t) -> TileIds {
+    TileIds x{-1, -1, -1, tile_lane(t, ntiles, lo, hi, a.tile, lane)};
+    if (x.in) x.u = in_ids[begin + lo + t * a.tile + lane];
+    return x;
+  };
+  auto load_slot = [&](TileIds& x) {
+    if (x.in && x.u >= 0 && (int64_t)x.u < part.N) {
+      x.m = owner_of(part, s_start, x.u);
+      if (x.m != part.local) x.s = slot_of[x.u];
+    }
+  };
+  int64_t t = (int64_t)blockIdx.x * kTilesPerBlock + threadIdx.x / kWave;
+  TileIds cur = load_ids(t);
+  load_slot(cur);
+  TileIds nxt = load_ids(t + step);
+  for (; t < ntiles; t += step) {
+    load_slot(nxt);
+    const TileIds after = load_ids(t + 2 * step);
     const char* src = nullptr;
     bool miss = false, is_local = false, is_hit = false;
-    int32_t u = -1, m = -1;
-    if (lane < a.tile && i < hi) {
-      u = in_ids[begin + i];
-      if (u < 0 || (int64_t)u >= part.N) {
+    if (cur.in) {
+      if (cur.m < 0) {
         st |= GG_DEV_BAD_ID;
-      } else {
-        m = owner_of(part, s_start, u);
-        if (m == part.local) {
-          const int64_t r = row_of(part, s_start, u, m);
-          if (r < feat.rows[m]) {
-            src = feat.shard[m] + r * feat.stride[m];
-            is_local = true;
-          } else {
-            st |= GG_DEV_BAD_ROW;
-          }
+      } else if (cur.m == part.local) {
+        const int64_t r = row_of(part, s_start, cur.u, cur.m);
+        if (r < feat.rows[cur.m]) {
+          src = feat.shard[cur.m] + r * feat.stride[cur.m];
+          is_local = true;
         } else {
-          const int32_t s = slot_of[u];
-          if (s >= 0 && (int64_t)s < a.cache_rows) {
-            src = cache + (int64_t)s * a.cache_stride;
-            is_hit = true;
-          } else {
-            if (s >= 0) st |= GG_DEV_BAD_ROW;
-            miss = true;
-          }
+          st |= GG_DEV_BAD_ROW;
         }
+      } else if (cur.s >= 0 && (int64_t)cur.s < a.cache_rows) {
+        src = cache + (int64_t)cur.s * a.cache_stride;
+        is_hit = true;
+      } else {
+        if (cur.s >= 0) st |= GG_DEV_BAD_ROW;
+        miss = true;
       }
     }
     const uint64_t ml = __ballot(is_local), mh = __ballot(is_hit), mm = __ballot(miss);
@@ -107,14 +130,17 @@ __global__ void __launch_bounds__(kBlock) k_gather_rows(const int32_t* in_ids, c
     // Per-owner miss counts: one ballot per owner present.
     for (uint64_t act = mm; act;) {
       const int leader = __ffsll((unsigned long long)act) - 1;
-      const int32_t ol = __shfl(m, leader, kWave);
-      const uint64_t sel = __ballot(miss && m == ol);
+      const int32_t ol = __shfl(cur.m, leader, kWave);
+      const uint64_t sel = __ballot(miss && cur.m == ol);
       if (lane == leader) atomicAdd(&s_cnt[2 + ol], (int32_t)__popcll(sel));
       act &= ~sel;
     }
+    const int64_t r0 = lo + t * a.tile;
     const int64_t left = hi - r0;
     const int nrows = left < a.tile ? (int)left : a.tile;
     wave_copy_rows<VB, NT, U>(src, out + r0 * a.out_stride, a.out_stride, nrows, a.geom);
+    cur = nxt;
+    nxt = after;
   }
   if (lane == 0) {
     if (c_local) atomicAdd(&s_cnt[0], c_local);

@@ -234,8 +234,9 @@ __device__ __forceinline__ void wave_copy_rows(const char* src, char* dst0, int6
   const long long srcl = (long long)src;
   for (uint32_t base = 0; base < total; base += kWave * U) {
     if (VB == 16) {
+      // Destinations are recomputed at the stores: holding U 64-bit
+      // pointers across the loads would cost 2U registers.
       u32x4 v[U];
-      char* dp[U];
       bool ok[U];
 #pragma unroll
       for (int j = 0; j < U; ++j) {
@@ -244,12 +245,15 @@ __device__ __forceinline__ void wave_copy_rows(const char* src, char* dst0, int6
         const uint32_t col = c - r * g.cpr;
         const char* sp = (const char*)__shfl(srcl, (int)(r & 63u), kWave);
         ok[j] = (c < total) && (sp != nullptr);
-        dp[j] = dst0 + (int64_t)r * dst_stride + (int64_t)col * 16;
         if (ok[j]) v[j] = *(const u32x4*)(sp + (int64_t)col * 16);
       }
 #pragma unroll
-      for (int j = 0; j < U; ++j)
-        if (ok[j]) st16<NT>(dp[j], v[j]);
+      for (int j = 0; j < U; ++j) {
+        const uint32_t c = base + (uint32_t)(j * kWave + lane);
+        const uint32_t r = __umulhi(c, g.magic);
+        const uint32_t col = c - r * g.cpr;
+        if (ok[j]) st16<NT>(dst0 + (int64_t)r * dst_stride + (int64_t)col * 16, v[j]);
+      }
     } else {
       uint32_t v[U];
       char* dp[U];
