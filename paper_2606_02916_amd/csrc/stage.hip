@@ -232,8 +232,9 @@ int stage_delta_blocks(int64_t cap) {
 //                   of the previous occupancy; clears the remap's stale
 //                   entries and the new occupancy.
 //   k_inplace_emit  the prefix of the block counts, and the ascending list
-//                   of the first |delta| free slots, one block per chunk
-//                   (chunks past them return at once).
+//                   of the first |delta| free slots; the blocks stride over
+//                   the chunks below the previous extent and stop at the
+//                   first chunk past those slots.
 //   k_inplace_rows  remap, occupancy and the delta rows' copies (the
 //                   requests); a tile's first delta rank is the prefix of
 //                   its range's block plus that block's range counts before
@@ -242,6 +243,12 @@ int stage_delta_blocks(int64_t cap) {
 constexpr int kRange = kWave;          // bucket entries per delta count (one wave)
 constexpr int kOccChunk = kBlock * 32; // slots per free-list block (one 32-slot group a thread)
 constexpr int kPrepBlocks = 1024;      // most prep blocks (block counts a rank sums)
+// Most free-list blocks.  Blocks past the previous extent return at once;
+// the cap keeps a large cache (4,224 chunks for the 34.6M slots of a
+// Papers100M share) from launching thousands of them.  GG_EMIT_BLOCKS (read
+// at every call) lowers it, so that small caches exercise blocks that take
+// several chunks.
+constexpr int kEmitBlocks = 512;
 
 struct InplaceWs {
   int32_t* old_slot;   // [cap]
@@ -268,7 +275,7 @@ size_t inplace_ws_layout(int64_t cap, int64_t cache_rows, int32_t P, char* base,
   w.old_slot = cv.take<int32_t>((size_t)std::max<int64_t>(cap, 1));
   w.dcnt = cv.take<int32_t>((size_t)gp * (size_t)P);
   w.dr = cv.take<int32_t>((size_t)nr);
-  w.btot = cv.take<int32_t>((size_t)gp);
+  w.btot = cv.take<int32_t>((size_t)align_up((size_t)gp, 4));   // read four at a time
   w.bpre = cv.take<int64_t>((size_t)gp);
   w.fcnt = cv.take<int32_t>((size_t)nch);
   w.freel = cv.take<int32_t>((size_t)std::max<int64_t>(cache_rows, 1));
@@ -279,11 +286,21 @@ size_t inplace_ws_layout(int64_t cap, int64_t cache_rows, int32_t P, char* base,
 
 // Free-slot mask of the 32 slots q*32 .. q*32+31 (bit i = slot q*32+i is
 // below cache_rows and its occupancy byte is 0).
-__device__ __forceinline__ uint32_t free_mask(const uint8_t* occ, int64_t q, int64_t cache_rows) {
-  const int64_t lim = cache_rows - q * 32;
-  if (lim <= 0) return 0u;
+// The 32 occupancy bytes of slots q*32 .. q*32+31, or zeros past cache_rows.
+__device__ __forceinline__ void occ_words(const uint8_t* occ, int64_t q, int64_t cache_rows,
+                                          u32x4* a, u32x4* b) {
+  const u32x4 z = {0u, 0u, 0u, 0u};
+  *a = z;
+  *b = z;
+  if (cache_rows - q * 32 <= 0) return;
   const u32x4* p = (const u32x4*)(occ + q * 32);
-  const u32x4 a = p[0], b = p[1];
+  *a = p[0];
+  *b = p[1];
+}
+
+// Bit i set where byte i of (a, b) is 0 and i < lim.
+__device__ __forceinline__ uint32_t zero_byte_bits(u32x4 a, u32x4 b, int64_t lim) {
+  if (lim <= 0) return 0u;
   const uint32_t w[8] = {a.x, a.y, a.z, a.w, b.x, b.y, b.z, b.w};
   uint32_t m = 0;
 #pragma unroll
@@ -293,6 +310,12 @@ __device__ __forceinline__ uint32_t free_mask(const uint8_t* occ, int64_t q, int
       m |= (((w[i] >> (8 * j)) & 0xFFu) == 0u ? 1u : 0u) << (4 * i + j);
   if (lim < 32) m &= (1u << lim) - 1u;
   return m;
+}
+
+__device__ __forceinline__ uint32_t free_mask(const uint8_t* occ, int64_t q, int64_t cache_rows) {
+  u32x4 a, b;
+  occ_words(occ, q, cache_rows, &a, &b);
+  return zero_byte_bits(a, b, cache_rows - q * 32);
 }
 
 // Sum of v over a block of kBlock threads (every thread gets it).
@@ -406,21 +429,32 @@ __global__ void __launch_bounds__(kBlock) k_inplace_emit(const uint8_t* occ_prev
                                                          int64_t* bpre, int32_t* freel,
                                                          int64_t* nfree, StageArgs a) {
   __shared__ int64_t lds[kBlock / kWave];
-  __shared__ int32_t buf[kOccChunk];
   constexpr int PT = kPrepBlocks / kBlock;     // block counts per thread
+  // Two dependent rounds of loads: the extent with the block counts, then
+  // the chunk counts with the occupancy bytes of the block's first chunk.
+  static_assert(PT == 4, "one 16-byte load of block counts per thread");
   const int b = blockIdx.x;
   const int64_t ext = occ_prev ? *(const int64_t*)occ_prev : 0;
+  const int i0 = threadIdx.x * PT;
+  u32x4 bv = {0u, 0u, 0u, 0u};
+  if (i0 < gp) bv = *(const u32x4*)(btot + i0);   // the workspace pads btot to a multiple of 4
+  const int32_t bt[PT] = {(int32_t)bv.x, i0 + 1 < gp ? (int32_t)bv.y : 0,
+                          i0 + 2 < gp ? (int32_t)bv.z : 0, i0 + 3 < gp ? (int32_t)bv.w : 0};
+  const int64_t v = (int64_t)bt[0] + bt[1] + bt[2] + bt[3];
   const int64_t lim = ext < a.cache_rows ? ext : a.cache_rows;
   const int64_t nch = cdiv_dev(lim, kOccChunk);
   if (b > 0 && b >= nch) return;
-  int32_t bt[PT];
-  int64_t v = 0;
-#pragma unroll
-  for (int q = 0; q < PT; ++q) {
-    const int i = threadIdx.x * PT + q;
-    bt[q] = i < gp ? btot[i] : 0;
-    v += bt[q];
+  const uint8_t* map_prev = occ_prev + kOccHeader;
+  const int64_t q0 = (int64_t)b * kBlock + threadIdx.x;
+  u32x4 o0, o1;
+  occ_words(map_prev, q0, b < nch ? lim : 0, &o0, &o1);
+  int64_t w = 0, all = 0;
+  for (int64_t c = threadIdx.x; c < nch; c += blockDim.x) {
+    const int64_t x = fcnt[c];
+    all += x;
+    if (c < b) w += x;
   }
+  uint32_t f = zero_byte_bits(o0, o1, lim - q0 * 32);
   int64_t need;
   int64_t run = block_excl_scan<kBlock>(v, lds, &need);
   if (b == 0) {
@@ -430,27 +464,27 @@ __global__ void __launch_bounds__(kBlock) k_inplace_emit(const uint8_t* occ_prev
       if (i < gp) bpre[i] = run;
       run += bt[q];
     }
-  }
-  int64_t w = 0, all = 0;
-  for (int64_t c = threadIdx.x; c < nch; c += blockDim.x) {
-    const int64_t x = fcnt[c];
-    all += x;
-    if (c < b) w += x;
-  }
-  const int64_t before = block_sum(w, lds);
-  if (b == 0) {
     all = block_sum(all, lds);
     if (threadIdx.x == 0) *nfree = all;
   }
-  if (b >= nch || before >= need) return;          // the delta's slots lie before this chunk
-  const int64_t g = (int64_t)b * kBlock + threadIdx.x;
-  uint32_t f = free_mask(occ_prev + kOccHeader, g, lim);
-  int64_t tot;
-  int64_t pos = block_excl_scan<kBlock>((int64_t)__popc(f), lds, &tot);
-  for (; f; f &= f - 1u) buf[pos++] = (int32_t)(g * 32 + (__ffs(f) - 1));
-  __syncthreads();
-  const int64_t cnt = need - before < tot ? need - before : tot;
-  for (int64_t i = threadIdx.x; i < cnt; i += blockDim.x) freel[before + i] = buf[i];
+  for (int64_t ch = b; ch < nch; ch += gridDim.x) {
+    if (ch != b) {
+      w = 0;
+      for (int64_t c = threadIdx.x; c < ch; c += blockDim.x) w += fcnt[c];
+      f = free_mask(map_prev, ch * kBlock + threadIdx.x, lim);
+    }
+    const int64_t before = block_sum(w, lds);
+    if (before >= need) return;    // the delta's slots lie before this chunk and the later ones
+    // Every thread writes its own free slots at its place in the list.  A
+    // version that staged the chunk's list in 32 KB of LDS took ~200 us
+    // beside the gather of a Papers100M share against 5-14 us alone (a
+    // kernel with little LDS, the prep, ran equally fast in both); without
+    // the LDS it takes 15-20 us there.
+    const int64_t g = ch * kBlock + threadIdx.x;
+    int64_t tot;
+    int64_t pos = before + block_excl_scan<kBlock>((int64_t)__popc(f), lds, &tot);
+    for (; f && pos < need; f &= f - 1u) freel[pos++] = (int32_t)(g * 32 + (__ffs(f) - 1));
+  }
 }
 
 template <int VB, bool NT>
@@ -683,9 +717,11 @@ extern "C" int gg_stage_inplace(const int32_t* bucket_ids_d, const int64_t* owne
                      owner_off_d, kp, a, prev_slot_of_d, w.old_slot, w.dcnt, w.dr, w.btot,
                      clear_ids_d, clear_count_d, slot_of_d, occ_prev_d, w.fcnt, occ_d, status_d);
   GG_LAUNCH_CHECK("k_inplace_prep");
-  // blocks past the previous extent's chunks return at once
-  const int32_t nch = occ_prev_d ? (int32_t)cdiv(cache_rows, kOccChunk) : 0;
-  hipLaunchKernelGGL(k_inplace_emit, dim3(std::max(nch, 1)), dim3(kBlock), 0, stream, occ_prev_d,
+  // the extent is known on the device only: blocks past its chunks return
+  // at once, and the grid is capped so that they stay few
+  const int emit_cap = std::min(std::max(env_int("GG_EMIT_BLOCKS", kEmitBlocks), 1), kEmitBlocks);
+  const int64_t nch = occ_prev_d ? std::min<int64_t>(cdiv(cache_rows, kOccChunk), emit_cap) : 0;
+  hipLaunchKernelGGL(k_inplace_emit, dim3((unsigned)std::max<int64_t>(nch, 1)), dim3(kBlock), 0, stream, occ_prev_d,
                      w.fcnt, w.btot, gridp, w.bpre, w.freel, w.nfree, a);
   GG_LAUNCH_CHECK("k_inplace_emit");
   const int64_t ntiles = cdiv(std::min(cap, cache_rows), a.tile);

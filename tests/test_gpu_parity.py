@@ -583,6 +583,24 @@ def test_inplace_staging_matches_oracle(name, n_hot, W, rows):
         assert st["retained"] + sum(st["rows"]) == st["rows_total"]
 
 
+@pytest.mark.parametrize("emit_blocks", [1, 2])
+def test_inplace_free_list_blocks_take_several_chunks(emit_blocks, monkeypatch):
+    """The free list of the persistent cache is emitted by at most a fixed
+    number of blocks that stride over the 8,192-slot chunks below the
+    previous extent; GG_EMIT_BLOCKS=1 or 2 makes every block take several
+    chunks on the small graph, whose extent passes two chunks."""
+    log(f"small: in-place staging, free list emitted by {emit_blocks} block(s)")
+    monkeypatch.setenv("GG_EMIT_BLOCKS", str(emit_blocks))
+    w = world(synth.instance("small"), inplace=True)
+    nwin = synth.n_windows(w.inst.batch_off, w.W)
+    ext = []
+    for k in range(min(nwin, 5)):
+        w.run_and_compare(k)
+        # window k's occupancy map starts with its extent (int64)
+        ext.append(int(w.pipe.occs[k % 2][:8].cpu().numpy().view(np.int64)[0]))
+    assert max(ext[:-1]) > 2 * 8192, ext
+
+
 def test_inplace_staging_out_of_slots_leaves_misses():
     """A persistent cache one slot short of two windows' hot sets: the
     second staging raises GG_DEV_CAPACITY and leaves the last delta row out
