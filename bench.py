@@ -742,16 +742,21 @@ def ablation(args, wl):
     del dst, sub_cache, sub_slot
 
     # -- rows per wavefront copy step ---------------------------------------
-    def tile_rows(max_bytes):
+    def tile_rows(max_bytes):          # staging: a power of two
         t = 64
         while t > 1 and t * rb > max_bytes:
             t //= 2
         return t
 
+    def fill_rows(max_bytes):          # gather: as many rows as fit
+        return max(1, min(64, max_bytes // rb))
+
+    # the sequential driver's gather (eight loads, power-of-two tiles); the
+    # look-ahead's shared gather fills its tiles (fill_rows), swept as well
     defaults = {"gather": tile_rows(8192), "stage": tile_rows(32768)}
     ref_out, ref_cache, tiles = None, None, []
     try:
-        for t in sorted({64, 16, 4, 1, *defaults.values()}, reverse=True):
+        for t in sorted({64, 16, 4, 1, fill_rows(8192), *defaults.values()}, reverse=True):
             os.environ["GG_TILE_ROWS"] = str(t)
             gm = timed(lambda: pipe.gather_window(Wk), 10)
             sm = timed(stage_full, 10)

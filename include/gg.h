@@ -304,8 +304,9 @@ int gg_stage_inplace(const int32_t* bucket_ids_d, const int64_t* owner_off_d, in
  * latency-bound work (sampling) on the device at the same time: each lane
  * then keeps half as many row loads in flight, which costs the gather a few
  * percent alone and leaves the memory system's queues short enough for the
- * concurrent work.  Results are identical either way; any other flag bit is
- * GG_ERR_ARG. */
+ * concurrent work, and a wavefront's tile of rows holds as many rows as fit
+ * in 8 KB rather than a power of two.  Results are identical either way;
+ * any other flag bit is GG_ERR_ARG. */
 #define GG_GATHER_SHARED 1
 int gg_gather_batch(const int32_t* in_ids_d, const int64_t* bounds_d, int32_t nseg,
                     int64_t n_cap, const gg_part_t* part, const gg_feat_t* feat,

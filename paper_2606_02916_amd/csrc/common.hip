@@ -77,12 +77,10 @@ int env_int(const char* name, int dflt) {
   return (v && *v) ? atoi(v) : dflt;
 }
 
-int32_t copy_tile(int32_t row_bytes, int32_t max_bytes) {
+int32_t copy_tile(int32_t row_bytes, int32_t max_bytes, bool pow2) {
   const int v = env_int("GG_TILE_ROWS", 0);
-  if (v <= 0) return tile_rows(row_bytes, max_bytes);
-  int32_t p = 1;
-  while (p * 2 <= v && p * 2 <= kWave) p *= 2;
-  return p;
+  if (v > 0) return v < kWave ? v : kWave;
+  return pow2 ? tile_rows(row_bytes, max_bytes) : fill_rows(row_bytes, max_bytes);
 }
 
 int host_shards(const KFeat& f) {

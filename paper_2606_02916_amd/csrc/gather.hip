@@ -329,12 +329,17 @@ extern "C" int gg_gather_batch(const int32_t* in_ids_d, const int64_t* bounds_d,
   a.out_stride = out_stride;
   a.nseg = nseg;
   a.nstat = 2 + kp.P;
-  // Tiles of up to 8 KB: 16 rows of 400 bytes, 2 of 2,408.  Against 32 KB
-  // tiles the isolated gather took 228 instead of 237 us on a 1.5M-row
-  // window of 400-byte rows and 246 instead of 261 us on 275K rows of
-  // 2,408 bytes: more, smaller tiles leave a shorter tail of waves still
-  // copying their last tile.
-  a.tile = copy_tile(kf.row_bytes, 8192);
+  // Tiles of up to 8 KB.  Against 32 KB tiles the isolated gather took 228
+  // instead of 237 us on a 1.5M-row window of 400-byte rows and 246 instead
+  // of 261 us on 275K rows of 2,408 bytes: more, smaller tiles leave a
+  // shorter tail of waves still copying their last tile.  With four loads
+  // in flight (shared) a tile holds as many rows as fit, 20 of 400 bytes
+  // (500 chunks: two steps of 256 loads, 98% full), which took the isolated
+  // gather from 0.58 to 0.60 of HBM peak on that window and from 0.55 to
+  // 0.57 on the wide rows; with eight (alone) it stays a power of two, 16
+  // rows and 2, which measured 1-3% faster there than 20 and 3.
+  const bool shared = (flags & GG_GATHER_SHARED) != 0;
+  a.tile = copy_tile(kf.row_bytes, 8192, !shared);
   a.pad_ = 0;
   a.geom = copy_geom(kf.row_bytes, v16 ? 16 : 4);
   const int32_t bx = blocks_per_seg(n_cap, nseg);
@@ -344,7 +349,7 @@ extern "C" int gg_gather_batch(const int32_t* in_ids_d, const int64_t* bounds_d,
   // window took 6% longer, for 4% more gather speed).
   static const int unroll_alone = env_int("GG_GATHER_UNROLL", 8);
   static const int unroll_shared = env_int("GG_GATHER_UNROLL_SHARED", 4);
-  const int unroll = (flags & GG_GATHER_SHARED) ? unroll_shared : unroll_alone;
+  const int unroll = shared ? unroll_shared : unroll_alone;
   const char* cache = (const char*)cache_d;
   char* out = (char*)out_d;
   if (v16) {

@@ -54,10 +54,20 @@ inline int32_t tile_rows(int32_t row_bytes, int32_t max_bytes) {
   return t;
 }
 
-// tile_rows(row_bytes, max_bytes), or, when GG_TILE_ROWS is set (read at
-// every call), the largest power of two at most that and 64 (1 makes a
-// wavefront copy one row per step).
-int32_t copy_tile(int32_t row_bytes, int32_t max_bytes);
+// Rows a wavefront takes per step of a row copy: as many as fit in
+// max_bytes, up to 64.  Any count works, since the copy engine spreads a
+// tile's 16-byte chunks over all lanes; 20 rows of 400 bytes (500 chunks)
+// fill two steps of 256 loads to 98%, where 16 rows (400 chunks) fill
+// them to 78%.
+inline int32_t fill_rows(int32_t row_bytes, int32_t max_bytes) {
+  const int64_t t = row_bytes > 0 ? max_bytes / row_bytes : 64;
+  return (int32_t)(t < 1 ? 1 : (t > 64 ? 64 : t));
+}
+
+// pow2 ? tile_rows(row_bytes, max_bytes) : fill_rows(row_bytes, max_bytes),
+// or, when GG_TILE_ROWS is set (read at every call), that count, at most 64
+// (1 makes a wavefront copy one row per step).
+int32_t copy_tile(int32_t row_bytes, int32_t max_bytes, bool pow2 = true);
 
 inline bool aligned16(const void* p) { return ((uintptr_t)p & 15u) == 0; }
 
