@@ -648,26 +648,37 @@ def test_inplace_staging_out_of_slots_leaves_misses():
                          for b in range(Wk)) > 0
 
 
-@pytest.mark.parametrize("name,n_hot,W,nsets,host,gev", [
-    ("small", -1, None, 2, False, None), ("small", 3000, None, 2, False, "both"),
-    ("tiny", -1, 1, 2, False, None), ("small", -1, None, None, False, "end"),
-    ("tiny", 2000, 1, 3, False, "end"), ("small", 3000, None, 4, False, "both"),
-    ("small", -1, None, None, True, "both"), ("small", 3000, None, 3, True, "end")])
-def test_lookahead_pipeline_equals_sequential(name, n_hot, W, nsets, host, gev):
+@pytest.mark.parametrize("name,n_hot,W,nsets,host,gev,rows", [
+    ("small", -1, None, 2, False, None, None), ("small", 3000, None, 2, False, "both", None),
+    ("tiny", -1, 1, 2, False, None, None), ("small", -1, None, None, False, "end", None),
+    ("tiny", 2000, 1, 3, False, "end", None), ("small", 3000, None, 4, False, "both", None),
+    ("small", -1, None, None, True, "both", None), ("small", 3000, None, 3, True, "end", None),
+    ("tiny", 700, 2, None, False, "end", (1036, 1040)),
+    ("small", 3000, None, None, False, "end", (2408, 2416))])
+def test_lookahead_pipeline_equals_sequential(name, n_hot, W, nsets, host, gev, rows):
     """The look-ahead driver against the sequential delta-staging driver,
     window by window: with shards in device memory (staging on the build
     stream) and with the remote shards in pinned host memory (staging on
     the fetch stream, gathers on a third stream); without gather events,
     with both, and with only the end event, which then also releases the
-    buffer set (the benchmark's configuration)."""
+    buffer set (the benchmark's configuration).  Rows of 1,036 and 2,408
+    bytes give the look-ahead's gather (four loads, tiles of as many rows
+    as fit in 8 KB) tiles of 7 and 3 rows, where the sequential driver's
+    gather takes 4 and 2."""
     log(f"{name}: look-ahead pipeline vs sequential delta windows, n_hot={n_hot}, W={W}, "
-        f"nsets={nsets}, host shards={host}, gather events={gev}")
+        f"nsets={nsets}, host shards={host}, gather events={gev}, rows={rows}")
     import torch as T
     from paper_2606_02916_amd import LookaheadPipeline
     inst = synth.instance(name)
     wl = inst.wl
-    seq = world(inst, n_hot=n_hot, W=W, delta=True)
+    kw = {}
+    if rows:
+        rng = np.random.default_rng(13)
+        kw = dict(shards=[rng.integers(0, 256, size=(sh.shape[0], rows[1]), dtype=np.uint8)
+                          for sh in inst.shards], row_bytes=rows[0], stride=rows[1])
+    seq = world(inst, n_hot=n_hot, W=W, delta=True, **kw)
     W = seq.W
+    rb = seq.row_bytes
     dev = seq.dev
     shards = seq.shards_d
     if host:
@@ -675,7 +686,7 @@ def test_lookahead_pipeline_equals_sequential(name, n_hot, W, nsets, host, gev):
                   for m, s in enumerate(seq.shards_d)]
     look = LookaheadPipeline(seq.row_ptr_d, seq.col_idx_d, wl.num_parts, wl.part_kind,
                              wl.local_owner, inst.range_start, shards,
-                             [s.shape[0] for s in inst.shards], wl.row_bytes, wl.row_stride, W,
+                             [s.shape[0] for s in inst.shards], rb, seq.stride, W,
                              wl.fanout, wl.batch_size, n_hot=n_hot, device=dev, nsets=nsets)
     assert (look.stage_stream is look.fetch_stream) == host
     assert (look.gather_stream is look.fetch_stream) != host
@@ -688,13 +699,13 @@ def test_lookahead_pipeline_equals_sequential(name, n_hot, W, nsets, host, gev):
     expected = []
     for k in range(nwin):
         r = seq.run_and_compare(k)
-        expected.append((np.concatenate(r["outs"])[:, :wl.row_bytes], r["stage"]))
+        expected.append((np.concatenate(r["outs"])[:, :rb], r["stage"]))
 
     def read(k, Wk, bufs):
         look.gathered_event(k).synchronize()
         foff = bufs.frontier_off[:(L + 1) * Wk + 1].cpu().numpy()
         n = int(foff[-1] - foff[L * Wk])
-        return bufs.win_out[:n, :wl.row_bytes].cpu().numpy(), bufs.stage_stats_dict()
+        return bufs.win_out[:n, :rb].cpu().numpy(), bufs.stage_stats_dict()
 
     got, pending = [], None
     for k in range(nwin):
