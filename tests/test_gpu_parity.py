@@ -240,20 +240,25 @@ def test_large_sparse_full_window_matches_oracle():
 
 
 @pytest.mark.timeout(900)
-def test_large_sparse_lookahead_as_benchmarked():
+@pytest.mark.parametrize("name", ["large_sparse", "dense_mid"])
+def test_lookahead_as_benchmarked(name):
     """The benchmark's launch configuration: the look-ahead driver with
     its default three buffer sets and only a gather end event per window,
-    over four consecutive windows of large_sparse.  Every
+    over four consecutive windows of large_sparse (400-byte rows, 20-row
+    gather tiles) and of dense_mid (2,408-byte rows, 3-row tiles).  Every
     gathered row equals the row of the unsharded feature matrix (the
     ground truth independent of the cache), N_b of the first and last batch
     of every window equals the oracle's, and the hot set is the union of the
     window's remote N_b."""
-    log("large_sparse: look-ahead driver (default buffer sets), windows 0-3, every gathered row")
+    log(f"{name}: look-ahead driver (default buffer sets), windows 0-3, every gathered row")
     import torch as T
     from oracle import ggref
     from paper_2606_02916_amd import LookaheadPipeline
-    inst, rp_d, ci_d, sh_d = synth.torch_instance("large_sparse", "cuda:0")
+    inst, rp_d, ci_d, sh_d = synth.torch_instance(name, "cuda:0")
     wl = inst.wl
+    # owner 0 holds [rs[0], rs[1]) and is local; the shards in owner order
+    # are the feature matrix in node order
+    assert wl.part_kind == synth.PART_RANGE and wl.local_owner == 0
     P, L, W = wl.num_parts, len(wl.fanout), wl.W
     dev = T.device("cuda:0")
     look = LookaheadPipeline(rp_d, ci_d, P, wl.part_kind, wl.local_owner, inst.range_start, sh_d,
