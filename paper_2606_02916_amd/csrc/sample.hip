@@ -23,7 +23,7 @@ struct SeedOff {
 struct LevelArgs {
   int32_t lv, L, W, k;
   int32_t nch;
-  int32_t pad_;
+  int32_t cnt_only;   // offsets from the chunk counts alone (no group totals)
   int64_t fcap, ncap;
 };
 
@@ -122,12 +122,17 @@ __global__ void __launch_bounds__(kBlock) k_mark_seeds(const int32_t* seeds, See
 // over the grid, the group totals.  Every block reads its batch's seeds, so
 // batches of at most kSeedBitsMaxBatch seeds take this path.
 constexpr int64_t kSeedBitsMaxBatch = 16384;
+// Most chunks (W times the chunks of one bit set) for which a level-0 emit
+// block sums every chunk count before its own: 608 for 16 batches over
+// 2.45M nodes; 27K for the 111M-node graph keeps the counting pass.
+constexpr int64_t kCntOnlyMaxChunks = 4096;
 
 __global__ void __launch_bounds__(kBlock) k_seed_bits(const int32_t* seeds, SeedOff so,
                                                       uint32_t* bits, int64_t wpb, int64_t N,
                                                       uint8_t* map, int32_t* btot, int32_t nbtot,
-                                                      int32_t* status) {
+                                                      int32_t* cnt, int32_t* status) {
   __shared__ uint32_t w[kChunkWords];
+  __shared__ int32_t s_pop[kBlock / kWave];
   const int c = blockIdx.x, b = blockIdx.y;
   const int64_t flat = ((int64_t)b * gridDim.x + c) * blockDim.x + threadIdx.x;
   const int64_t nthreads = (int64_t)gridDim.x * gridDim.y * blockDim.x;
@@ -146,9 +151,21 @@ __global__ void __launch_bounds__(kBlock) k_seed_bits(const int32_t* seeds, Seed
   }
   __syncthreads();
   u32x4* dst = (u32x4*)(bits + (int64_t)b * wpb + (int64_t)c * kChunkWords);
+  int32_t pop = 0;
   for (int i = threadIdx.x; i < kChunkWords / 4; i += blockDim.x) {
     const u32x4 v = {w[4 * i], w[4 * i + 1], w[4 * i + 2], w[4 * i + 3]};
     dst[i] = v;
+    pop += __popc(v.x) + __popc(v.y) + __popc(v.z) + __popc(v.w);
+  }
+  if (cnt) {   // the chunk's count, so that level 0 needs no counting pass
+    pop = wave_sum(pop);
+    if (lane_id() == 0) s_pop[threadIdx.x / kWave] = pop;
+    __syncthreads();
+    if (threadIdx.x == 0) {
+      int32_t n = 0;
+      for (int q = 0; q < kBlock / kWave; ++q) n += s_pop[q];
+      cnt[(int64_t)b * gridDim.x + c] = n;
+    }
   }
   if (map) {
     u32x4* m = (u32x4*)(map + ((int64_t)b * wpb + (int64_t)c * kChunkWords) * 32);
@@ -255,17 +272,30 @@ __global__ void __launch_bounds__(kBlock) k_bits_emit(const uint32_t* bits, int6
   const int64_t raw_base = a.lv == 0 ? 0 : ls->fend[a.lv - 1];
   const int64_t raw_nbase = a.lv == 0 ? 0 : ls->nend[a.lv - 1];
   int64_t v[3] = {0, 0, 0};  // batches before b, all batches (block (0, 0)), chunks of b before c
-  const int64_t per_batch = (int64_t)tt.ngroups * kTotLanes;
-  const int64_t upto = (b == 0 && c == 0) ? a.W * per_batch : b * per_batch;
-  for (int64_t t = threadIdx.x; t < upto; t += kBlock) {
-    const int64_t x = tt.gtot[t];
-    v[1] += x;
-    if (t < b * per_batch) v[0] += x;
+  if (a.cnt_only) {
+    // a window of few chunks: every block sums the chunk counts before it
+    const int64_t mine = (int64_t)b * nch;
+    const int64_t upto = (b == 0 && c == 0) ? (int64_t)a.W * nch : mine + c;
+    for (int64_t t = threadIdx.x; t < upto; t += kBlock) {
+      const int64_t x = cnt[t];
+      v[1] += x;
+      if (t < mine) v[0] += x;
+      else if (t < mine + c) v[2] += x;
+    }
+  } else {
+    const int64_t per_batch = (int64_t)tt.ngroups * kTotLanes;
+    const int64_t upto = (b == 0 && c == 0) ? a.W * per_batch : b * per_batch;
+    for (int64_t t = threadIdx.x; t < upto; t += kBlock) {
+      const int64_t x = tt.gtot[t];
+      v[1] += x;
+      if (t < b * per_batch) v[0] += x;
+    }
+    const int g = c / kGroupChunks;
+    const int32_t* gb = tt.gtot + b * per_batch;
+    for (int t = threadIdx.x; t < g * kTotLanes; t += kBlock) v[2] += gb[t];
+    for (int t = g * kGroupChunks + threadIdx.x; t < c; t += kBlock)
+      v[2] += cnt[(int64_t)b * nch + t];
   }
-  const int g = c / kGroupChunks;
-  const int32_t* gb = tt.gtot + b * per_batch;
-  for (int t = threadIdx.x; t < g * kTotLanes; t += kBlock) v[2] += gb[t];
-  for (int t = g * kGroupChunks + threadIdx.x; t < c; t += kBlock) v[2] += cnt[(int64_t)b * nch + t];
   block_sum3(v, lds3);
   const int64_t cb = raw_base < a.fcap ? raw_base : a.fcap;
   if (threadIdx.x == 0) {
@@ -528,10 +558,15 @@ extern "C" int gg_sample_window(const gg_csr_t* csr, const int32_t* seeds_d,
   int64_t max_batch = 0;
   for (int b = 0; b < W; ++b)
     max_batch = std::max<int64_t>(max_batch, seed_off_h[b + 1] - seed_off_h[b]);
+  // With few chunks in the window, level 0's counts come from k_seed_bits
+  // and its emit sums them directly: one launch fewer.  Beside a running
+  // gather even a small launch costs 7-12 us.
+  const bool seed_counts = max_batch <= kSeedBitsMaxBatch && (int64_t)W * nch <= kCntOnlyMaxChunks;
   if (max_batch <= kSeedBitsMaxBatch) {
     hipLaunchKernelGGL(k_seed_bits, dim3((unsigned)nch, (unsigned)W), dim3(kBlock), 0, stream,
                        seeds_d, so, out->frontier_bits, wpb, N, sw.map, sw.tot,
-                       (int32_t)((L + 1) * sw.tot_level), status_d);
+                       (int32_t)((L + 1) * sw.tot_level), seed_counts ? sw.cnt : nullptr,
+                       status_d);
     GG_LAUNCH_CHECK("k_seed_bits");
   } else {
     const int64_t map4 = sw.map ? W * wpb * 2 : 0;   // 32 bytes per word, 16 per store
@@ -579,16 +614,19 @@ extern "C" int gg_sample_window(const gg_csr_t* csr, const int32_t* seeds_d,
     Totals tt;
     tt.gtot = sw.tot + (int64_t)lv * sw.tot_level;
     tt.ngroups = sw.ngroups;
-    hipLaunchKernelGGL(k_bits_count, dim3(nch, W), dim3(kBlock), 0, stream, out->frontier_bits, wpb,
-                       lv == L ? sw.map : nullptr, sw.cnt, tt);
-    GG_LAUNCH_CHECK("k_bits_count");
+    const bool cnt_only = lv == 0 && seed_counts;
+    if (!cnt_only) {
+      hipLaunchKernelGGL(k_bits_count, dim3(nch, W), dim3(kBlock), 0, stream, out->frontier_bits,
+                         wpb, lv == L ? sw.map : nullptr, sw.cnt, tt);
+      GG_LAUNCH_CHECK("k_bits_count");
+    }
     LevelArgs la;
     la.lv = lv;
     la.L = L;
     la.W = W;
     la.k = lv < L ? fanout_h[lv] : 0;
     la.nch = nch;
-    la.pad_ = 0;
+    la.cnt_only = cnt_only ? 1 : 0;
     la.fcap = out->frontier_cap;
     la.ncap = out->nbr_cap;
     hipLaunchKernelGGL(k_bits_emit, dim3(nch, W), dim3(kBlock), 0, stream, out->frontier_bits, wpb,
