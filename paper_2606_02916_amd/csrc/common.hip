@@ -97,16 +97,6 @@ int host_shards(const KFeat& f) {
   return n;
 }
 
-CopyGeom copy_geom(int32_t row_bytes, int vb) {
-  CopyGeom g;
-  g.row_bytes = row_bytes;
-  g.cpr = (uint32_t)(row_bytes / vb);
-  g.tail = vb == 16 ? (uint32_t)((row_bytes % 16) / 4) : 0u;
-  g.magic = g.cpr ? (uint32_t)(((1ULL << 32) + g.cpr - 1) / g.cpr) : 0u;
-  g.tmagic = g.tail ? (uint32_t)(((1ULL << 32) + g.tail - 1) / g.tail) : 0u;
-  return g;
-}
-
 }  // namespace gg
 
 extern "C" {

@@ -4,6 +4,7 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include "copy_geom.hpp"
 #include "gg.h"
 
 namespace gg {
@@ -197,18 +198,9 @@ __device__ __forceinline__ void wave_hist_add(int32_t* hist, bool valid, int32_t
 // spread over the wave, so consecutive lanes move consecutive chunks of one
 // row and then of the next: every load and store instruction covers a
 // contiguous run of up to 1 KB, and short rows do not leave lanes idle.
-// Chunk c belongs to row c / cpr, computed as umulhi(c, magic) with
-// magic = ceil(2^32 / cpr) (exact for cpr <= 8192).
+// Chunk c belongs to row c / cpr, computed by chunk_row (copy_geom.hpp).
 // ---------------------------------------------------------------------------
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
-
-struct CopyGeom {
-  int32_t row_bytes;
-  uint32_t cpr;       // full VB-byte chunks per row
-  uint32_t magic;     // ceil(2^32 / cpr)
-  uint32_t tail;      // 4-byte words after the full chunks (VB = 16 only)
-  uint32_t tmagic;    // ceil(2^32 / tail)
-};
 
 template <bool NT>
 __device__ __forceinline__ void st16(char* p, u32x4 v) {
@@ -241,7 +233,7 @@ __device__ __forceinline__ void wave_copy_rows(const char* src, char* dst0, int6
 #pragma unroll
       for (int j = 0; j < U; ++j) {
         const uint32_t c = base + (uint32_t)(j * kWave + lane);
-        const uint32_t r = __umulhi(c, g.magic);
+        const uint32_t r = chunk_row(c, g.magic);
         const uint32_t col = c - r * g.cpr;
         const char* sp = (const char*)__shfl(srcl, (int)(r & 63u), kWave);
         ok[j] = (c < total) && (sp != nullptr);
@@ -250,7 +242,7 @@ __device__ __forceinline__ void wave_copy_rows(const char* src, char* dst0, int6
 #pragma unroll
       for (int j = 0; j < U; ++j) {
         const uint32_t c = base + (uint32_t)(j * kWave + lane);
-        const uint32_t r = __umulhi(c, g.magic);
+        const uint32_t r = chunk_row(c, g.magic);
         const uint32_t col = c - r * g.cpr;
         if (ok[j]) st16<NT>(dst0 + (int64_t)r * dst_stride + (int64_t)col * 16, v[j]);
       }
@@ -261,7 +253,7 @@ __device__ __forceinline__ void wave_copy_rows(const char* src, char* dst0, int6
 #pragma unroll
       for (int j = 0; j < U; ++j) {
         const uint32_t c = base + (uint32_t)(j * kWave + lane);
-        const uint32_t r = __umulhi(c, g.magic);
+        const uint32_t r = chunk_row(c, g.magic);
         const uint32_t col = c - r * g.cpr;
         const char* sp = (const char*)__shfl(srcl, (int)(r & 63u), kWave);
         ok[j] = (c < total) && (sp != nullptr);
@@ -278,7 +270,7 @@ __device__ __forceinline__ void wave_copy_rows(const char* src, char* dst0, int6
     const int64_t off0 = (int64_t)g.cpr * 16;
     for (uint32_t base = 0; base < ttotal; base += kWave) {
       const uint32_t c = base + (uint32_t)lane;
-      const uint32_t r = __umulhi(c, g.tmagic);
+      const uint32_t r = chunk_row(c, g.tmagic);
       const uint32_t w = c - r * g.tail;
       const char* sp = (const char*)__shfl(srcl, (int)(r & 63u), kWave);
       if (c < ttotal && sp != nullptr) {
@@ -305,7 +297,7 @@ __device__ __forceinline__ void wave_copy_rows_to(const char* src, char* dst, in
 #pragma unroll
       for (int j = 0; j < U; ++j) {
         const uint32_t c = base + (uint32_t)(j * kWave + lane);
-        const uint32_t r = __umulhi(c, g.magic);
+        const uint32_t r = chunk_row(c, g.magic);
         const uint32_t col = c - r * g.cpr;
         const char* sp = (const char*)__shfl(srcl, (int)(r & 63u), kWave);
         dp[j] = (char*)__shfl(dstl, (int)(r & 63u), kWave) + (int64_t)col * 16;
@@ -322,7 +314,7 @@ __device__ __forceinline__ void wave_copy_rows_to(const char* src, char* dst, in
 #pragma unroll
       for (int j = 0; j < U; ++j) {
         const uint32_t c = base + (uint32_t)(j * kWave + lane);
-        const uint32_t r = __umulhi(c, g.magic);
+        const uint32_t r = chunk_row(c, g.magic);
         const uint32_t col = c - r * g.cpr;
         const char* sp = (const char*)__shfl(srcl, (int)(r & 63u), kWave);
         dp[j] = (char*)__shfl(dstl, (int)(r & 63u), kWave) + (int64_t)col * 4;
@@ -339,7 +331,7 @@ __device__ __forceinline__ void wave_copy_rows_to(const char* src, char* dst, in
     const int64_t off0 = (int64_t)g.cpr * 16;
     for (uint32_t base = 0; base < ttotal; base += kWave) {
       const uint32_t c = base + (uint32_t)lane;
-      const uint32_t r = __umulhi(c, g.tmagic);
+      const uint32_t r = chunk_row(c, g.tmagic);
       const uint32_t w = c - r * g.tail;
       const char* sp = (const char*)__shfl(srcl, (int)(r & 63u), kWave);
       char* dp = (char*)__shfl(dstl, (int)(r & 63u), kWave);

@@ -42,9 +42,6 @@ int pack_part(const gg_part_t* part, KPart* out);
 // Checks feature shards against a partition book and packs them.
 int pack_feat(const gg_feat_t* feat, const gg_part_t* part, KFeat* out);
 
-// Geometry of the row copy for row_bytes and the vector width vb (16 or 4).
-CopyGeom copy_geom(int32_t row_bytes, int vb);
-
 // Rows a wavefront takes per step of a row copy: the largest power of two
 // up to 64 whose rows fit in max_bytes, so that wide rows still spread over
 // every wave of the grid.

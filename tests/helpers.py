@@ -93,12 +93,13 @@ def floyd_sequences(d, k):
 _built = {}
 
 
-def build_helper(src_name, extra=(), compiler="gcc"):
-    """Compiles a helper under tests/pins into a temp dir (cached per session)."""
+def build_helper(src_name, extra=(), compiler="gcc", subdir="pins"):
+    """Compiles a helper under tests/<subdir> into a temp dir (cached per
+    session)."""
     if src_name in _built:
         return _built[src_name]
     out = os.path.join(tempfile.mkdtemp(prefix="ggpin_"), os.path.splitext(src_name)[0])
-    cmd = [compiler, "-O2", os.path.join(ROOT, "tests", "pins", src_name), "-o", out, *extra]
+    cmd = [compiler, "-O2", os.path.join(ROOT, "tests", subdir, src_name), "-o", out, *extra]
     subprocess.run(cmd, check=True)
     _built[src_name] = out
     return out
