@@ -384,6 +384,7 @@ int ggref_stage_inplace(const int32_t* bucket_ids, const int64_t* owner_off,
   for (int64_t i = 0; i < clear_count; ++i) slot_of[clear_ids[i]] = -1;
   stats->invalidated = clear_count;
   size_t next_free = 0;
+  bool short_of_slots = false;
   for (int32_t m = 0; m < P; ++m) {
     for (int64_t s = owner_off[m]; s < owner_off[m + 1]; ++s) {
       const int32_t u = bucket_ids[s];
@@ -396,19 +397,25 @@ int ggref_stage_inplace(const int32_t* bucket_ids, const int64_t* owner_off,
         ++stats->retained;
         continue;
       }
-      if (next_free == free_slots.size()) return GGREF_ERR_CAPACITY;
+      ++stats->delta_rows[m];
+      if (next_free == free_slots.size()) {
+        // No free slot is left: the row is not cached this window, so a
+        // gather serves it as a miss.
+        slot_of[u] = -1;
+        short_of_slots = true;
+        continue;
+      }
       const int64_t slot = free_slots[next_free++];
       std::memcpy((char*)cache + slot * cache_stride, src_row(feat, m, r), (size_t)feat->row_bytes);
       slot_of[u] = (int32_t)slot;
       ++stats->rows[m];
-      ++stats->delta_rows[m];
     }
     stats->bytes[m] = stats->rows[m] * feat->row_bytes;
     stats->requests[m] = (stats->rows[m] > 0) ? 1 : 0;
     stats->requests_total += stats->requests[m];
   }
   stats->rows_total = owner_off[P];
-  return GGREF_OK;
+  return short_of_slots ? GGREF_ERR_CAPACITY : GGREF_OK;
 }
 
 // Per-batch feature assembly (Algorithm 1, inner loop): a local node is

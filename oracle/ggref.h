@@ -159,8 +159,10 @@ int ggref_stage_bulk(const int32_t* bucket_ids, const int64_t* owner_off,
  * and its row stays where it is.  Every other node is the rebuild delta: it
  * is requested from its owner (one request per owner whose delta is
  * non-empty) and takes, in bucket order, the lowest cache slot that
- * prev_slot_of does not hold.  Returns GGREF_ERR_CAPACITY when the free
- * slots run out. */
+ * prev_slot_of does not hold.  When the free slots run out, the delta rows
+ * left over are not cached (slot_of = -1, nothing copied, not counted in
+ * rows/bytes/requests, still counted in delta_rows), the call completes
+ * and returns GGREF_ERR_CAPACITY. */
 int ggref_stage_inplace(const int32_t* bucket_ids, const int64_t* owner_off,
                         const ggref_part_t* part, const ggref_feat_t* feat, void* cache,
                         int64_t cache_stride, int64_t cache_rows, int32_t* slot_of,

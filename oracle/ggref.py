@@ -14,6 +14,7 @@ import numpy as np
 MAX_PARTS = 64
 PART_MOD = 0
 PART_RANGE = 1
+ERR_CAPACITY = -2   # GGREF_ERR_CAPACITY
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
 # GGREF_LIB lets the oracle's own mutation tests load a deliberately broken
@@ -259,21 +260,26 @@ def stage_bulk(bucket_ids, owner_off, part, feat, cache, cache_stride, slot_of, 
 
 
 def stage_inplace(bucket_ids, owner_off, part, feat, cache, cache_stride, slot_of, prev_slot_of,
-                  clear_ids=None):
+                  clear_ids=None, allow_short=False):
     """Delta staging into one persistent cache: cache (rows x cache_stride,
     uint8) and slot_of (int32[N], this window's remap) are updated in place;
     prev_slot_of is the previous window's remap (None for a first window);
-    clear_ids: entries of slot_of to clear first."""
+    clear_ids: entries of slot_of to clear first.  When the free slots run
+    out the call raises, unless allow_short: it then returns (stats, True)
+    with the delta rows left over uncached, and (stats, False) otherwise."""
     st = StageStats()
     bucket_ids = np.ascontiguousarray(bucket_ids, dtype=np.int32)
     owner_off = np.ascontiguousarray(owner_off, dtype=np.int64)
     clr = None if clear_ids is None else np.ascontiguousarray(clear_ids, dtype=np.int32)
     ncl = 0 if clr is None else clr.shape[0]
-    _check(lib().ggref_stage_inplace(_p(bucket_ids), _p(owner_off), C.byref(part), C.byref(feat),
-                                     _p(cache), cache_stride, cache.shape[0], _p(slot_of),
-                                     _p(clr), ncl, _p(prev_slot_of), C.byref(st)),
-           "ggref_stage_inplace")
-    return stats_dict(st, part.num_parts)
+    rc = lib().ggref_stage_inplace(_p(bucket_ids), _p(owner_off), C.byref(part), C.byref(feat),
+                                   _p(cache), cache_stride, cache.shape[0], _p(slot_of),
+                                   _p(clr), ncl, _p(prev_slot_of), C.byref(st))
+    short = rc == ERR_CAPACITY
+    if not (allow_short and short):
+        _check(rc, "ggref_stage_inplace")
+    d = stats_dict(st, part.num_parts)
+    return (d, short) if allow_short else d
 
 
 def gather_batch(in_ids, part, feat, cache, cache_stride, slot_of, out, out_stride):

@@ -58,6 +58,11 @@ MUTANTS = [
      "        ++stats->retained;\n        ++stats->rows[m];\n        continue;"),
     ("in-place staging ignores the previous slots", "if (s >= 0) used[(size_t)s] = 1;",
      "(void)s;"),
+    ("in-place rows left uncached counted as fetched",
+     "        slot_of[u] = -1;\n        short_of_slots = true;\n        continue;",
+     "        slot_of[u] = -1;\n        short_of_slots = true;\n        ++stats->rows[m];\n        continue;"),
+    ("in-place staging stops at the first row without a slot",
+     "        short_of_slots = true;\n        continue;", "        short_of_slots = true;\n        break;"),
     ("miss request counts rows", "stats->miss_requests[m] = miss[m].empty() ? 0 : 1;",
      "stats->miss_requests[m] = (int64_t)miss[m].size();"),
     ("slot 0 treated as a miss", "} else if (slot_of[u] >= 0) {", "} else if (slot_of[u] > 0) {"),

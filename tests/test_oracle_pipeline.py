@@ -522,6 +522,84 @@ def test_inplace_staging_capacity_is_the_union_of_two_windows():
                 ggref.stage_inplace(hs[1][0], hs[1][1], part, feat, cache, 8, r1, r0)
 
 
+def _expected_inplace(H, old_map, cache_rows):
+    """Slots of the hot set H (bucket order) under in-place staging, from
+    the definition: a node the previous remap holds keeps its slot; the
+    delta takes, in bucket order, the ascending slots the previous remap
+    does not hold; delta rows past the last free slot stay uncached (-1)."""
+    taken = set() if old_map is None else {int(x) for x in old_map if x >= 0}
+    free = [x for x in range(cache_rows) if x not in taken]
+    want, j = {}, 0
+    for u in H:
+        if old_map is not None and old_map[u] >= 0:
+            want[u] = int(old_map[u])
+        elif j < len(free):
+            want[u] = free[j]
+            j += 1
+        else:
+            want[u] = -1
+    return want
+
+
+@pytest.mark.parametrize("short_by", [1, 7])
+def test_inplace_staging_after_running_out_of_slots(short_by):
+    """Reading R22: a cache smaller than the union of two windows' hot sets
+    leaves the delta rows past the last free slot uncached (their remap
+    entries -1, served as misses) and the call reports the shortfall; the
+    next window then treats every slot the short window did fill as taken,
+    so none of its delta rows lands on a row it keeps, and the nodes left
+    out are part of its delta.  Three consecutive windows against the
+    definition (Python sets and sorted lists) and the unsharded matrix."""
+    rng = np.random.default_rng(59)
+    N = 300
+    row_ptr, col_idx = helpers.random_graph(N, 2000, rng)
+    part, feat, full, shards, rs = make_world(row_ptr, col_idx, ggref.PART_MOD, 4, 0, 8, 16, rng)
+    hs = []
+    for k in range(3):
+        seeds, soff = random_seeds(N, 2, 4, rng)
+        fids, foff, _, _ = ggref.sample_window(row_ptr, col_idx, seeds, soff, (2, 2), 1, 0, 2 * k)
+        hot, _ = ggref.build_hotset(fids, foff, 2, 2, part, -1)
+        hs.append(ggref.bucket_by_owner(hot, part))
+    union01 = len(set(hs[0][0].tolist()) | set(hs[1][0].tolist()))
+    rows = union01 - short_by
+    assert rows >= len(hs[0][0]) and rows >= len(hs[2][0])
+    cache = np.zeros((rows, 16), dtype=np.uint8)
+    remaps = [np.full(N, -1, np.int32), np.full(N, -1, np.int32)]
+    held = [None, None]
+    shorts = []
+    for k in range(3):
+        bucket, owner_off = hs[k]
+        cur, old = remaps[k % 2], (remaps[(k - 1) % 2].copy() if k else None)
+        before = cache.copy()
+        H = bucket.tolist()
+        want = _expected_inplace(H, old, rows)
+        st, short = ggref.stage_inplace(bucket, owner_off, part, feat, cache, 16, cur, old,
+                                        clear_ids=held[k % 2], allow_short=True)
+        held[k % 2] = bucket.copy()
+        shorts.append(short)
+        assert short == (min(want.values()) < 0)
+        for u in H:
+            assert cur[u] == want[u], (k, u)
+            if want[u] >= 0:
+                assert np.array_equal(cache[want[u], :8], full[u, :8])
+            if old is not None and old[u] >= 0:
+                assert np.array_equal(cache[old[u]], before[old[u]])      # kept, not rewritten
+        mask = np.ones(N, bool)
+        mask[H] = False
+        assert np.all(cur[mask] == -1)
+        for m in range(4):
+            seg = H[owner_off[m]:owner_off[m + 1]]
+            delta = [u for u in seg if old is None or old[u] < 0]
+            placed = [u for u in delta if want[u] >= 0]
+            assert st["delta_rows"][m] == len(delta)
+            assert st["rows"][m] == len(placed)
+            assert st["bytes"][m] == 8 * len(placed)
+            assert st["requests"][m] == (1 if placed else 0)
+        assert st["retained"] == sum(1 for u in H if old is not None and old[u] >= 0)
+        assert st["rows_total"] == len(H)
+    assert shorts[0] is False and shorts[1] is True
+
+
 def test_paper_consolidation_example():
     """Sec. IV-C: W = 16 batches over three remote owners turn up to
     16 x 3 = 48 per-batch requests into 3 bulk transfers."""
