@@ -273,10 +273,12 @@ int gg_stage_bulk(const int32_t* bucket_ids_d, const int64_t* owner_off_d, int64
  * bucket position.  Only free slots are written, so the previous window's
  * gathers may run concurrently; the window before it must be finished.
  * The cache must hold both windows: when the free slots run out,
- * GG_DEV_CAPACITY is raised and the rows left over are not staged (their
- * remap entries stay -1, so a gather serves them as misses).  Statistics
- * as gg_stage_bulk's with a source cache: rows, bytes and requests count
- * the delta, retained the rows kept in place. */
+ * GG_DEV_CAPACITY is raised and the delta rows past the last free slot
+ * are not staged (their remap entries stay -1, so a gather serves them as
+ * misses); the extent then covers the whole cache, so the next call treats
+ * every slot this one filled as taken.  Statistics as gg_stage_bulk's with
+ * a source cache: rows, bytes and requests count the delta rows copied,
+ * delta_rows the whole delta, retained the rows kept in place. */
 int gg_stage_inplace(const int32_t* bucket_ids_d, const int64_t* owner_off_d, int64_t cap,
                      const gg_part_t* part, const gg_feat_t* feat, void* cache_d,
                      int64_t cache_stride, int64_t cache_rows, int32_t* slot_of_d,

@@ -31,6 +31,15 @@ __device__ __forceinline__ int64_t stage_n(const int64_t* owner_off, int32_t P, 
   return n < a.cache_rows ? n : a.cache_rows;
 }
 
+// Bucket entries an in-place call handles: every entry, since a retained
+// row keeps its slot wherever it sits in the list, and a delta row past the
+// free slots is left uncached rather than dropped from the count.
+__device__ __forceinline__ int64_t inplace_n(const int64_t* owner_off, int32_t P,
+                                             const StageArgs& a) {
+  const int64_t n = owner_off[P];
+  return n < a.cap ? n : a.cap;
+}
+
 // Old slots and the rebuild delta: old_slot[s] = the slot the source remap
 // (or, without a source cache, the current remap before clearing) gives
 // the node of bucket entry s; rows with none are the delta.  Every block
@@ -99,6 +108,12 @@ struct StageStatsArgs {
   const int64_t* prev_count;
   const int32_t* dcnt;
   gg_stage_stats_t* stats;
+  // In place only (else NULL): the free slots below the previous extent and
+  // the previous occupancy (NULL for a first window).  The delta takes free
+  // slots in bucket order, i.e. owner by owner, so owner m's delta rows
+  // copied are those of its ranks below the slots available.
+  const int64_t* nfree;
+  const uint8_t* occ_prev;
   int32_t nblk_delta;
   int32_t has_src;
 };
@@ -119,7 +134,15 @@ __device__ void stage_stats(const int64_t* owner_off, const KPart& part, const S
     if (lane_id() == 0 && v) atomicAdd(&s_delta[m], v);
   }
   __syncthreads();
-  const int64_t n = stage_n(owner_off, part.P, a);
+  const int64_t n = sa.nfree ? inplace_n(owner_off, part.P, a) : stage_n(owner_off, part.P, a);
+  // slots the delta can take (in place): free ones below the previous
+  // extent, and every slot from the extent to the end of the cache
+  int64_t avail = INT64_MAX;
+  if (sa.nfree) {
+    int64_t ext = sa.occ_prev ? *(const int64_t*)sa.occ_prev : 0;
+    ext = ext < a.cache_rows ? ext : a.cache_rows;
+    avail = *sa.nfree + (a.cache_rows - ext);
+  }
   __shared__ int64_t s_req[GG_MAX_PARTS], s_rows[GG_MAX_PARTS];
   if (threadIdx.x < GG_MAX_PARTS) {
     const int m = threadIdx.x;
@@ -129,7 +152,12 @@ __device__ void stage_stats(const int64_t* owner_off, const KPart& part, const S
       lo = lo < n ? lo : n;
       hi = hi < n ? hi : n;
       rows = hi > lo ? hi - lo : 0;
-      if (has_src) rows = s_delta[m];    // only the delta is requested
+      if (has_src) {                     // only the delta is requested
+        int64_t before = 0;              // delta ranks of the owners before m
+        for (int q = 0; q < m; ++q) before += s_delta[q];
+        const int64_t fit = avail - before;
+        rows = fit <= 0 ? 0 : (fit < s_delta[m] ? fit : (int64_t)s_delta[m]);
+      }
     }
     stats->rows[m] = rows;
     stats->bytes[m] = rows * row_bytes;
@@ -140,15 +168,15 @@ __device__ void stage_stats(const int64_t* owner_off, const KPart& part, const S
   }
   __syncthreads();
   if (threadIdx.x == 0) {
-    int64_t req = 0, fetched = 0;
+    int64_t req = 0, delta = 0;
     for (int m = 0; m < part.P; ++m) {
       req += s_req[m];
-      fetched += s_rows[m];
+      delta += s_delta[m];
     }
     stats->rows_total = n;
     stats->requests_total = req;
     stats->invalidated = prev_count ? prev_count[0] : 0;
-    stats->retained = has_src ? n - fetched : 0;
+    stats->retained = has_src ? n - delta : 0;
     if (owner_off[part.P] > n) set_status(status, GG_DEV_CAPACITY);
   }
 }
@@ -354,7 +382,7 @@ __global__ void __launch_bounds__(kBlock) k_inplace_prep(
   for (int t = threadIdx.x; t <= GG_MAX_PARTS; t += blockDim.x) s_start[t] = part.start[t];
   if (threadIdx.x == 0) s_fresh = 0;
   __syncthreads();
-  const int64_t n = stage_n(owner_off, part.P, a);
+  const int64_t n = inplace_n(owner_off, part.P, a);
   const int64_t nr = cdiv_dev(n, kRange);
   const int64_t R = ranges_per_block(n, gridDim.x);
   const int64_t rend = (int64_t)(blockIdx.x + 1) * R < nr ? (int64_t)(blockIdx.x + 1) * R : nr;
@@ -498,7 +526,7 @@ __global__ void __launch_bounds__(kBlock) k_inplace_rows(
   __shared__ int64_t s_start[GG_MAX_PARTS + 1];
   for (int t = threadIdx.x; t <= GG_MAX_PARTS; t += blockDim.x) s_start[t] = part.start[t];
   __syncthreads();
-  const int64_t n = stage_n(owner_off, part.P, a);
+  const int64_t n = inplace_n(owner_off, part.P, a);
   const int64_t R = ranges_per_block(n, gp);
   // delta rank j takes free-list entry j below the previous extent, and
   // slot ext + (j - nfree) above it
@@ -541,8 +569,13 @@ __global__ void __launch_bounds__(kBlock) k_inplace_rows(
       } else {
         const int64_t jj = j + lanes_below(fm);
         const int64_t slot = jj < nfree ? (int64_t)freel[jj] : ext + (jj - nfree);
-        if (jj == need - 1 && slot < a.cache_rows && slot + 1 > ext)
-          *(int64_t*)occ = slot + 1;                         // the last delta row: new extent
+        if (jj == need - 1) {
+          // The last delta rank raises the extent past every slot the delta
+          // took from the extent on; when the cache runs out, those are all
+          // the slots up to its end (the ranks beyond stay uncached).
+          const int64_t e = slot + 1 < a.cache_rows ? slot + 1 : a.cache_rows;
+          if (e > ext) *(int64_t*)occ = e;
+        }
         if (slot < 0 || slot >= a.cache_rows) {
           st |= GG_DEV_CAPACITY;
         } else {
@@ -652,6 +685,8 @@ extern "C" int gg_stage_bulk(const int32_t* bucket_ids_d, const int64_t* owner_o
   sa.prev_count = clear_count_d;
   sa.dcnt = dcnt;
   sa.stats = stats_d;
+  sa.nfree = nullptr;
+  sa.occ_prev = nullptr;
   sa.nblk_delta = gridd;
   sa.has_src = src_cache_d ? 1 : 0;
   if (v16)
@@ -734,8 +769,10 @@ extern "C" int gg_stage_inplace(const int32_t* bucket_ids_d, const int64_t* owne
   sa.prev_count = clear_count_d;
   sa.dcnt = w.dcnt;
   sa.stats = stats_d;
+  sa.nfree = w.nfree;
+  sa.occ_prev = occ_prev_d;
   sa.nblk_delta = gridp;
-  sa.has_src = prev_slot_of_d ? 1 : 0;
+  sa.has_src = 1;
   if (v16) {
     if (nt)
       hipLaunchKernelGGL((k_inplace_rows<16, true>), dim3(grid), dim3(kBlock), 0, stream,

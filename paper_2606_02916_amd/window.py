@@ -103,12 +103,15 @@ class _Buffers:
 class FetchPipeline:
     def __init__(self, row_ptr, col_idx, num_parts, part_kind, local_owner, range_start, shards,
                  shard_rows, row_bytes, stride, W, fanout, max_batch, n_hot=-1, device=None,
-                 out_buffers=2, cache_stride=None, delta=False, hot_frac=None, inplace=False):
+                 out_buffers=2, cache_stride=None, delta=False, hot_frac=None, inplace=False,
+                 cache_rows=None):
         """delta: rebuild the cache from the previous window's, requesting only
         the rebuild delta; the cache then alternates between two buffers and
         the rows still wanted are copied across.  inplace (implies delta):
         one persistent cache in which those rows stay put (gg_stage_inplace);
-        the remap then alternates between two buffers."""
+        the remap then alternates between two buffers.  cache_rows (in place
+        only): slots of the persistent cache, by default enough for two
+        windows' hot sets; fewer leave rows to the miss path."""
         self.device = torch.device(device if device is not None else "cuda")
         self.N = int(row_ptr.numel() - 1)
         self.W = int(W)
@@ -149,13 +152,14 @@ class FetchPipeline:
         self.bucket_ids = [torch.empty(g.hot_cap, dtype=torch.int32, device=dev)
                            for _ in range(self.nslot)]
         if self.inplace:
-            self.cache_rows = g.inplace_rows
-            self.caches = [torch.empty((g.inplace_rows, self.cache_stride), dtype=torch.uint8,
+            rows = g.inplace_rows if cache_rows is None else int(cache_rows)
+            self.cache_rows = rows
+            self.caches = [torch.empty((max(rows, 1), self.cache_stride), dtype=torch.uint8,
                                        device=dev)]
             self.slot_ofs = [b.slot_of, torch.full_like(b.slot_of, -1)]
-            self.occs = [torch.zeros(gg.occ_bytes(g.inplace_rows), dtype=torch.uint8,
-                                     device=dev) for _ in range(2)]
-            self.stage_ws = torch.empty(gg.gg_ws_stage_inplace(g.hot_cap, g.inplace_rows, self.P),
+            self.occs = [torch.zeros(gg.occ_bytes(rows), dtype=torch.uint8, device=dev)
+                         for _ in range(2)]
+            self.stage_ws = torch.empty(gg.gg_ws_stage_inplace(g.hot_cap, rows, self.P),
                                         dtype=torch.uint8, device=dev)
         else:
             # With delta staging the cache alternates between two buffers.
@@ -245,14 +249,17 @@ class FetchPipeline:
                            self.staged_cache(), self.cache_stride, self.cache_rows, self.slot_of,
                            out, self.stride, stats, self.status, self.ws)
 
-    def gather_window(self, Wk, out=None):
+    def gather_window(self, Wk, out=None, flags=0):
         """All Wk batches of the window in one launch; batch b's rows start at
-        row frontier_off[L*Wk + b] - frontier_off[L*Wk] of out."""
+        row frontier_off[L*Wk + b] - frontier_off[L*Wk] of out.  flags:
+        gg_gather_batch's (GG_GATHER_SHARED: the look-ahead's tiles and
+        loads in flight)."""
         out = self.win_out if out is None else out
         bounds = self.frontier_off.data_ptr() + 8 * (self.L * Wk)
         gg.gg_gather_batch(self.frontier_ids, bounds, Wk, out.shape[0], self.part, self.feat,
                            self.staged_cache(), self.cache_stride, self.cache_rows, self.slot_of,
-                           out, self.stride, self.gather_stats.data_ptr(), self.status, self.ws)
+                           out, self.stride, self.gather_stats.data_ptr(), self.status, self.ws,
+                           flags=flags)
         return out
 
     def capture_window(self, seeds, seed_off, batch0, epoch=0, rng_seed=0):
