@@ -8,7 +8,7 @@ import torch
 
 import synth
 from oracle import ggref
-from paper_2606_02916_amd import FetchPipeline
+from paper_2606_02916_amd import FetchPipeline, gg
 
 
 def log(msg):
@@ -20,7 +20,7 @@ class World:
 
     def __init__(self, inst, W=None, n_hot=-1, local_owner=None, fanout=None, batch=None,
                  device="cuda:0", shards=None, row_bytes=None, stride=None, cache_stride=None,
-                 tensors=None, delta=False, hot_frac=None, inplace=False):
+                 tensors=None, delta=False, hot_frac=None, inplace=False, cache_rows=None):
         wl = inst.wl
         self.inst = inst
         self.wl = wl
@@ -46,7 +46,7 @@ class World:
                                   self.rs, self.shards_d, rows, self.row_bytes, self.stride,
                                   self.W, self.fanout, self.batch, n_hot=n_hot, device=self.dev,
                                   cache_stride=cache_stride, delta=delta, hot_frac=hot_frac,
-                                  inplace=inplace)
+                                  inplace=inplace, cache_rows=cache_rows)
         self.part_ref = ggref.make_part(self.P, wl.part_kind, self.local, wl.num_nodes, self.rs)
         self.feat_ref = ggref.make_feat(self.row_bytes, self.shards, [self.stride] * self.P)
         self.cstride = self.pipe.cache_stride
@@ -88,7 +88,7 @@ class World:
         pipe.bucket(cur)
         pipe.stage(cur)
         torch.cuda.synchronize()
-        assert pipe.read_status() == 0, pipe.read_status()
+        stage_status = pipe.read_status()
         # sampling
         fids, foff, nids, noff = ggref.sample_window(self.inst.row_ptr, self.inst.col_idx, seeds,
                                                      so, self.fanout, rng_seed, epoch, b0)
@@ -99,11 +99,7 @@ class World:
         assert np.array_equal(g_nids, nids)
         # the bit sets hold exactly N_b
         bits = pipe.frontier_bits.view(torch.int32)[:Wk * pipe.wpb].cpu().numpy().view(np.uint32)
-        for b in range(Wk):
-            ids = fids[foff[L * Wk + b]:foff[L * Wk + b + 1]]
-            row = bits[b * pipe.wpb:(b + 1) * pipe.wpb]
-            got = np.nonzero(np.unpackbits(row.view(np.uint8), bitorder="little"))[0]
-            assert np.array_equal(got, ids)
+        check_bits(bits, pipe.wpb, Wk, lambda b: fids[foff[L * Wk + b]:foff[L * Wk + b + 1]])
         # hot set and buckets
         hot, freq = ggref.build_hotset(fids, foff, Wk, L, self.part_ref, self.n_hot,
                                        hot_frac=self.hot_frac)
@@ -119,15 +115,17 @@ class World:
         kk, nc = pipe.k, len(self.cache_refs)
         cache_ref = self.cache_refs[kk % nc]
         H = len(hot)
+        short = False
         if self.inplace:
             X = kk % 2
-            sst = ggref.stage_inplace(bucket, owner_off, self.part_ref, self.feat_ref, cache_ref,
-                                      self.cstride, self.slot_refs[X],
-                                      self.slot_refs[1 - X] if kk > 0 else None,
-                                      clear_ids=self.held[X])
+            sst, short = ggref.stage_inplace(bucket, owner_off, self.part_ref, self.feat_ref,
+                                             cache_ref, self.cstride, self.slot_refs[X],
+                                             self.slot_refs[1 - X] if kk > 0 else None,
+                                             clear_ids=self.held[X], allow_short=True)
             self.held[X] = bucket.copy()
             slots = self.slot_ref[bucket]
-            assert np.all(slots >= 0)
+            slots = slots[slots >= 0]
+            assert short or len(slots) == len(bucket)
             g_rows = pipe.staged_cache()[torch.from_numpy(slots.astype(np.int64)).to(self.dev)]
             assert np.array_equal(g_rows.cpu().numpy()[:, :rb], cache_ref[slots, :rb])
         else:
@@ -137,6 +135,10 @@ class World:
                                    src_slot_of=self.slot_ref if src is not None else None)
             g_cache = pipe.staged_cache()[:H].cpu().numpy()
             assert np.array_equal(g_cache[:, :rb], cache_ref[:H, :rb])
+        # a persistent cache too small for two windows flags the shortfall
+        assert stage_status == (gg.DEV_CAPACITY if short else 0), (stage_status, short)
+        if short:
+            pipe.status.zero_()
         self.prev_ref = bucket.copy()
         assert pipe.stage_stats_dict() == sst
         assert np.array_equal(pipe.slot_of.cpu().numpy(), self.slot_ref)
@@ -160,17 +162,116 @@ class World:
                 assert np.array_equal(got[:, :rb], ref[:, :rb]), f"batch {b}"
                 refs.append(ref)
             del out
-        pipe.gather_stats.zero_()
-        win = pipe.gather_window(Wk)
-        torch.cuda.synchronize()
-        assert pipe.read_status() == 0
+        # the whole window in one launch, as the sequential driver gathers it
+        # and with the look-ahead's flag (other tiles, fewer loads in flight);
+        # the output is overwritten with a pattern first
         base = foff[L * Wk]
-        for b in range(Wk):
-            assert pipe.gather_stats_dict(b) == gstats[b]
-            if check_outputs:
-                lo, hi = foff[L * Wk + b] - base, foff[L * Wk + b + 1] - base
-                got = win[lo:hi].cpu().numpy()
-                assert np.array_equal(got[:, :rb], refs[b][:, :rb]), f"window batch {b}"
+        for flags in (0, gg.GG_GATHER_SHARED):
+            pipe.gather_stats.zero_()
+            pipe.win_out.fill_(0xA5)
+            win = pipe.gather_window(Wk, flags=flags)
+            torch.cuda.synchronize()
+            assert pipe.read_status() == 0
+            for b in range(Wk):
+                assert pipe.gather_stats_dict(b) == gstats[b]
+                if check_outputs:
+                    lo, hi = foff[L * Wk + b] - base, foff[L * Wk + b + 1] - base
+                    got = win[lo:hi].cpu().numpy()
+                    assert np.array_equal(got[:, :rb], refs[b][:, :rb]), \
+                        f"window batch {b}, flags {flags}"
         pipe.k += 1
         return dict(Wk=Wk, fids=fids, foff=foff, nids=nids, noff=noff, hot=hot, stage=sst,
-                    outs=refs if check_outputs else None)
+                    outs=refs if check_outputs else None, short=short)
+
+
+def check_bits(words, wpb, Wk, ids_of_batch):
+    """The W bit sets hold exactly N_b: every id's bit is set and each set
+    has as many bits as N_b has ids."""
+    for b in range(Wk):
+        row = words[b * wpb:(b + 1) * wpb]
+        ids = ids_of_batch(b)
+        assert int(np.bitwise_count(row).sum()) == len(ids), f"bit set of batch {b}"
+        if len(ids):
+            assert np.all((row[ids >> 5] >> (ids & 31).astype(np.uint32)) & 1), \
+                f"bit set of batch {b}"
+
+
+class LookaheadOracle:
+    """The oracle's run of consecutive windows as the look-ahead driver
+    computes them (delta staging into one persistent cache), checked against
+    a finished window's buffer set element by element: every batch's
+    frontiers and neighbour slots, the bit sets, hot set, frequencies,
+    counts, buckets and owner offsets, the staging statistics, the whole
+    remap, every staged row at its slot, the gather statistics and every
+    gathered row."""
+
+    def __init__(self, inst, look, n_hot=-1, shards=None, hot_frac=None):
+        wl = inst.wl
+        self.inst, self.look, self.n_hot, self.hot_frac = inst, look, n_hot, hot_frac
+        self.shards = inst.shards if shards is None else shards
+        self.P, self.L = wl.num_parts, len(look.fanout)
+        self.part = ggref.make_part(self.P, wl.part_kind, wl.local_owner, wl.num_nodes,
+                                    inst.range_start)
+        self.feat = ggref.make_feat(look.row_bytes, self.shards, [look.stride] * self.P)
+        self.cache = np.zeros((look.cache_rows, look.cache_stride), dtype=np.uint8)
+        # one remap per buffer set of the driver, each cleared of the window
+        # that last used the set
+        self.remaps = [np.full(wl.num_nodes, -1, dtype=np.int32) for _ in range(look.nsets)]
+        self.held = [None] * look.nsets
+        self.k = 0
+
+    def check(self, k, Wk, bufs, seeds, so, b0, rng_seed=0, epoch=0):
+        """Window k (the next one in order) after its gather finished."""
+        assert k == self.k
+        look, L, rb = self.look, self.L, self.look.row_bytes
+        torch.cuda.synchronize()
+        fids, foff, nids, noff = ggref.sample_window(self.inst.row_ptr, self.inst.col_idx, seeds,
+                                                     so, look.fanout, rng_seed, epoch, b0)
+        g_foff = bufs.frontier_off[:(L + 1) * Wk + 1].cpu().numpy()
+        g_noff = bufs.nbr_off[:L * Wk + 1].cpu().numpy()
+        assert np.array_equal(g_foff, foff), f"window {k} frontier offsets"
+        assert np.array_equal(g_noff, noff), f"window {k} neighbour offsets"
+        assert np.array_equal(bufs.frontier_ids[:int(foff[-1])].cpu().numpy(), fids), \
+            f"window {k} frontiers"
+        assert np.array_equal(bufs.nbr_ids[:int(noff[-1])].cpu().numpy(), nids), \
+            f"window {k} neighbour slots"
+        wpb = look.geo.wpb
+        words = bufs.frontier_bits.view(torch.int32)[:Wk * wpb].cpu().numpy().view(np.uint32)
+        check_bits(words, wpb, Wk, lambda b: fids[foff[L * Wk + b]:foff[L * Wk + b + 1]])
+        hot, freq = ggref.build_hotset(fids, foff, Wk, L, self.part, self.n_hot,
+                                       hot_frac=self.hot_frac)
+        bucket, owner_off = ggref.bucket_by_owner(hot, self.part)
+        T = k % look.NSLOT
+        cnt = look.hot_count[T].cpu().numpy()
+        assert int(cnt[0]) == len(hot) == int(cnt[1]), f"window {k} hot count"
+        assert np.array_equal(bufs.hot_ids[:len(hot)].cpu().numpy(), hot), f"window {k} hot set"
+        assert np.array_equal(bufs.hot_freq[:len(hot)].cpu().numpy(), freq), f"window {k} freq"
+        assert np.array_equal(look.bucket_ids[T][:len(hot)].cpu().numpy(), bucket), \
+            f"window {k} buckets"
+        assert np.array_equal(bufs.owner_off.cpu().numpy(), owner_off), f"window {k} owner_off"
+        X, ns = k % look.nsets, look.nsets
+        sst, short = ggref.stage_inplace(bucket, owner_off, self.part, self.feat, self.cache,
+                                         look.cache_stride, self.remaps[X],
+                                         self.remaps[(k - 1) % ns] if k > 0 else None,
+                                         clear_ids=self.held[X], allow_short=True)
+        assert not short
+        self.held[X] = bucket.copy()
+        assert bufs.stage_stats_dict() == sst, f"window {k} staging statistics"
+        remap = self.remaps[X]
+        assert np.array_equal(bufs.slot_of.cpu().numpy(), remap), f"window {k} remap"
+        slots = remap[bucket].astype(np.int64)
+        got = look.cache[torch.from_numpy(slots).to(look.device)][:, :rb].cpu().numpy()
+        assert np.array_equal(got, self.cache[slots, :rb]), f"window {k} staged rows"
+        base = int(foff[L * Wk])
+        win = bufs.win_out[:int(foff[-1]) - base, :rb].cpu().numpy()
+        for b in range(Wk):
+            s = L * Wk + b
+            ids = fids[foff[s]:foff[s + 1]]
+            ref = np.zeros((len(ids), look.stride), dtype=np.uint8)
+            gs = ggref.gather_batch(ids, self.part, self.feat, self.cache, look.cache_stride,
+                                    remap, ref, look.stride)
+            assert bufs.gather_stats_dict(b) == gs, f"window {k} batch {b} gather statistics"
+            lo, hi = foff[s] - base, foff[s + 1] - base
+            assert np.array_equal(win[lo:hi], ref[:, :rb]), f"window {k} batch {b} rows"
+        self.k += 1
+        return dict(Wk=Wk, hot=hot, stage=sst, fids=fids, foff=foff)

@@ -165,6 +165,31 @@ def test_row_with_tail_words():
     w.run_and_compare(0)
 
 
+@pytest.mark.parametrize("rows", [(4, 4), (4, 16), (16, 16), (20, 20), (20, 32), (100, 100),
+                                  (100, 112), (1204, 1204), (1204, 1216)])
+def test_row_widths_with_one_chunk_or_one_tail_word(rows):
+    """Row widths whose copy geometry has a divisor of 1: one 16-byte chunk
+    per row (16 and 20 bytes), one 4-byte tail word (4, 20, 100 and 1,204
+    bytes on the vector path) or one word per row (4 bytes on the word
+    path), with strides that are and are not multiples of 16.  Through
+    k_stage_rows and both gathers with a budget that leaves misses
+    (k_gather_finish), then through in-place staging (k_inplace_rows) over
+    two windows with the union."""
+    rb, stride = rows
+    log(f"tiny: {rb}-byte rows at stride {stride}")
+    inst = synth.instance("tiny")
+    rng = np.random.default_rng(rb * 7 + stride)
+    shards = [rng.integers(0, 256, size=(s.shape[0], stride), dtype=np.uint8)
+              for s in inst.shards]
+    w = world(inst, shards=shards, row_bytes=rb, stride=stride, n_hot=700)
+    r = w.run_and_compare(0)
+    assert sum(sum(g["miss_rows"]) for g in [w.pipe.gather_stats_dict(b)
+                                            for b in range(r["Wk"])]) > 0
+    w = world(inst, shards=shards, row_bytes=rb, stride=stride, W=2, inplace=True)
+    for k in range(2):
+        w.run_and_compare(k)
+
+
 @pytest.mark.parametrize("tile", [None, 64])
 @pytest.mark.parametrize("n_hot", [0, 700, -1])
 def test_wide_rows_with_misses(n_hot, tile, monkeypatch):
@@ -239,64 +264,62 @@ def test_large_sparse_full_window_matches_oracle():
     w.run_and_compare(0)
 
 
-@pytest.mark.timeout(900)
-@pytest.mark.parametrize("name", ["large_sparse", "dense_mid"])
+def rows_from_shards(inst, ids, rb):
+    """Feature rows of `ids` read straight from the owners' shards (range
+    book): ground truth independent of any cache."""
+    rs = inst.range_start
+    out = np.empty((len(ids), rb), dtype=np.uint8)
+    owner = np.searchsorted(np.asarray(rs), ids, side="right") - 1
+    for m in range(len(rs) - 1):
+        sel = owner == m
+        out[sel] = inst.shards[m][ids[sel] - rs[m], :rb]
+    return out
+
+
+@pytest.mark.timeout(1500)
+@pytest.mark.parametrize("name", ["large_sparse", "dense_mid", "papers_share"])
 def test_lookahead_as_benchmarked(name):
-    """The benchmark's launch configuration: the look-ahead driver with
-    its default three buffer sets and only a gather end event per window,
-    over four consecutive windows of large_sparse (400-byte rows, 20-row
-    gather tiles) and of dense_mid (2,408-byte rows, 3-row tiles).  Every
-    gathered row equals the row of the unsharded feature matrix (the
-    ground truth independent of the cache), N_b of the first and last batch
-    of every window equals the oracle's, and the hot set is the union of the
-    window's remote N_b."""
-    log(f"{name}: look-ahead driver (default buffer sets), windows 0-3, every gathered row")
+    """The benchmark's launch configuration: the look-ahead driver with its
+    default buffer sets (three with every shard in HBM; two on the
+    Papers100M share, whose remote shards sit in pinned host memory, with
+    staging on the fetch stream and the gather on a third stream) and only
+    a gather end event per window, over four consecutive windows (window
+    k+1 is enqueued before window k is read).  Every window against the
+    oracle element by element: every batch's frontiers, neighbour slots and
+    bit set, the hot set, buckets, staging statistics, the whole remap,
+    every staged row, gather statistics and every gathered row; the gathered
+    rows also against the owners' shards directly."""
+    log(f"{name}: look-ahead driver as benchmarked, windows 0-3 against the oracle")
     import torch as T
-    from oracle import ggref
     from paper_2606_02916_amd import LookaheadPipeline
+    from tests.gpu_util import LookaheadOracle
     inst, rp_d, ci_d, sh_d = synth.torch_instance(name, "cuda:0")
     wl = inst.wl
-    # owner 0 holds [rs[0], rs[1]) and is local; the shards in owner order
-    # are the feature matrix in node order
     assert wl.part_kind == synth.PART_RANGE and wl.local_owner == 0
     P, L, W = wl.num_parts, len(wl.fanout), wl.W
     dev = T.device("cuda:0")
     look = LookaheadPipeline(rp_d, ci_d, P, wl.part_kind, wl.local_owner, inst.range_start, sh_d,
                              [s.shape[0] for s in inst.shards], wl.row_bytes, wl.row_stride, W,
                              wl.fanout, wl.batch_size, device=dev)
-    assert look.nsets == 3 and look.stage_stream is look.build_stream
+    host = wl.remote_on_host
+    assert look.nsets == (2 if host else 3)
+    assert (look.stage_stream is look.build_stream) != host
+    orc = LookaheadOracle(inst, look)
     seeds_d = T.from_numpy(inst.seeds).to(dev)
-    boff, rs, rb = inst.batch_off, inst.range_start, wl.row_bytes
-    feats = np.concatenate([s[:, :rb] for s in inst.shards])      # row u = node u
+    boff, rb = inst.batch_off, wl.row_bytes
 
-    def check(k, Wk, bufs, b0, hot_slot):
+    def check(k, Wk, bufs, b0, b1):
         look.gathered_event(k).synchronize()
-        foff = bufs.frontier_off[:(L + 1) * Wk + 1].cpu().numpy()
-        fids = bufs.frontier_ids[:int(foff[-1])].cpu().numpy()
-        base = int(foff[L * Wk])
-        n = int(foff[-1]) - base
-        allN = fids[base:]
-        got = bufs.win_out[:n, :rb].cpu().numpy()
-        assert np.array_equal(got, feats[allN]), f"window {k} rows"
-        for b in (0, Wk - 1):
-            s = inst.seeds[boff[b0 + b]:boff[b0 + b + 1]]
-            f1, o1, _, _ = ggref.sample_window(inst.row_ptr, inst.col_idx, s,
-                                               np.array([0, len(s)], np.int64), wl.fanout, 0, 0,
-                                               b0 + b)
-            for l in range(L + 1):
-                assert np.array_equal(fids[foff[l * Wk + b]:foff[l * Wk + b + 1]],
-                                      f1[o1[l]:o1[l + 1]]), (k, b, l)
-        remote = allN[(allN < rs[0]) | (allN >= rs[1])]
-        uniq = np.unique(remote)
-        cnt = look.hot_count[hot_slot].cpu().numpy()
-        assert int(cnt[0]) == len(uniq)
-        assert np.array_equal(bufs.hot_ids[:len(uniq)].cpu().numpy(), uniq)
+        log(f"{name}: checking window {k} ({Wk} batches)")
+        seeds = inst.seeds[boff[b0]:boff[b1]]
+        r = orc.check(k, Wk, bufs, seeds, boff[b0:b1 + 1] - boff[b0], b0)
+        fids, foff = r["fids"], r["foff"]
+        allN = fids[int(foff[L * Wk]):]
+        got = bufs.win_out[:len(allN), :rb].cpu().numpy()
+        assert np.array_equal(got, rows_from_shards(inst, allN, rb)), f"window {k} rows"
         for b in range(Wk):
             gs = bufs.gather_stats_dict(b)
             assert gs["misses"] == 0 and gs["local"] + gs["hits"] == gs["rows"]
-        st = bufs.stage_stats_dict()
-        assert st["rows_total"] == len(uniq)
-        assert st["retained"] + sum(st["rows"]) == st["rows_total"]
 
     pending = None
     for k in range(4):
@@ -305,7 +328,7 @@ def test_lookahead_as_benchmarked(name):
                                gather_events=(None, T.cuda.Event(enable_timing=True)))
         if pending is not None:
             check(*pending)
-        pending = (k, Wk, bufs, b0, k % look.NSLOT)
+        pending = (k, Wk, bufs, b0, b1)
     check(*pending)
     assert look.read_status() == 0
 
@@ -358,132 +381,38 @@ def test_bucket_by_owner_direct(kind, order, flags):
     assert np.all(out[ids.shape[0]:].cpu().numpy() == -7)
 
 
-@pytest.mark.timeout(900)
-def test_wsweep_batch4096_w2_matches_oracle():
-    log("wsweep graph: batch 4096, W=2, window 0, full compare")
-    w = world(synth.instance("wsweep"), W=2)
-    w.run_and_compare(0)
-
-
-@pytest.mark.timeout(900)
-def test_wsweep_batch4096_w32_sampled_batches_and_invariants():
-    log("wsweep graph: batch 4096, W=32, window 0: sampled batches vs oracle, invariants")
-    import torch as T
-    from oracle import ggref
-    inst = synth.instance("wsweep")
-    wl = inst.wl
-    w = world(inst, W=32)
-    p = w.pipe
-    seeds, so, b0 = w.window_inputs(0)
-    Wk = p.window(T.from_numpy(seeds).to(w.dev), so, b0)
-    T.cuda.synchronize()
-    assert p.read_status() == 0
-    L = len(wl.fanout)
-    fids, foff, nids, noff = p.sample_outputs(Wk)
-    base = int(foff[L * Wk])
-    rs = inst.range_start
-    full_rows = {}
-    # batches 0, 17 and 31 against the oracle run on that batch alone (N_b
-    # does not depend on the window it falls in)
-    for b in (0, 17, 31):
-        s = seeds[so[b]:so[b + 1]]
-        f1, o1, n1, no1 = ggref.sample_window(inst.row_ptr, inst.col_idx, s,
-                                              np.array([0, len(s)], np.int64), wl.fanout, 0, 0,
-                                              b0 + b)
-        for l in range(L + 1):
-            got = fids[foff[l * Wk + b]:foff[l * Wk + b + 1]]
-            assert np.array_equal(got, f1[o1[l]:o1[l + 1]]), (b, l)
-        for l in range(L):
-            got = nids[noff[l * Wk + b]:noff[l * Wk + b + 1]]
-            assert np.array_equal(got, n1[no1[l]:no1[l + 1]]), (b, l)
-    # hot set = union of the remote N_b, with per-batch frequencies
-    lo, hi = rs[0], rs[1]
-    allN = fids[foff[L * Wk]:foff[(L + 1) * Wk]]
-    remote = allN[(allN < lo) | (allN >= hi)]
-    uniq, cnt = np.unique(remote, return_counts=True)
-    hot, freq, hc, bucket, owner_off = p.hot_outputs()
-    assert np.array_equal(hot, uniq) and np.array_equal(freq, cnt)
-    assert np.array_equal(bucket, hot)                     # ranges: identity bucketing
-    for m in range(4):
-        assert owner_off[m] == np.searchsorted(hot, rs[m])
-    # staged rows and gathered rows equal the source rows, on a sample
-    rng = np.random.default_rng(1)
-    cache = p.cache
-    slots = rng.choice(len(hot), 2000, replace=False)
-    for s_ in slots.tolist():
-        u = int(bucket[s_])
-        m = int(np.searchsorted(rs, u, side="right") - 1)
-        want = inst.shards[m][u - rs[m], :wl.row_bytes]
-        assert np.array_equal(cache[s_, :wl.row_bytes].cpu().numpy(), want)
-    out = p.win_out
-    rows = rng.choice(foff[(L + 1) * Wk] - base, 5000, replace=False)
-    got = out[T.from_numpy(rows).to(w.dev)].cpu().numpy()
-    for r_, g in zip(rows.tolist(), got):
-        u = int(fids[base + r_])
-        m = int(np.searchsorted(rs, u, side="right") - 1)
-        assert np.array_equal(g[:wl.row_bytes], inst.shards[m][u - rs[m], :wl.row_bytes])
-    total = 0
-    for b in range(Wk):
-        gs = p.gather_stats_dict(b)
-        n = int(foff[L * Wk + b + 1] - foff[L * Wk + b])
-        assert gs["rows"] == n and gs["misses"] == 0 and gs["local"] + gs["hits"] == n
-        total += n
-    assert total == len(allN)
+@pytest.mark.timeout(1200)
+@pytest.mark.parametrize("W,nwin", [(1, 2), (2, 2), (4, 2), (8, 2), (16, 1), (32, 1)])
+def test_wsweep_batch4096_matches_oracle(W, nwin):
+    """The W sweep at batch 4096 on the large sparse graph: window 0 (and
+    window 1 where W <= 8) of every W against the oracle, every
+    intermediate element by element (sampling, bit sets, hot set, buckets,
+    staged cache, remap, statistics, per-batch and whole-window gathers)."""
+    log(f"wsweep graph: batch 4096, W={W}, windows 0..{nwin - 1}, full compare")
+    w = world(synth.instance("wsweep"), W=W)
+    for k in range(nwin):
+        r = w.run_and_compare(k)
+        assert r["Wk"] == W
 
 
 @pytest.mark.timeout(1800)
-def test_papers_share_sampled_batches_and_invariants():
+def test_papers_share_windows_match_oracle():
+    """The Papers100M-shaped share (111M nodes, 1.6B edges, fp16 x 128; the
+    three remote shards in pinned host memory, read over PCIe) through the
+    sequential driver, windows 0 and 1: every intermediate against the
+    oracle element by element (all 16 batches' frontiers and neighbour
+    slots, bit sets, hot set, frequencies, buckets, owner offsets, staging
+    statistics, the whole remap, every cache row, every gathered row of the
+    per-batch and whole-window gathers)."""
     log("papers_share: 111M nodes, 1.6B edges, fp16x128, remote shards in pinned host memory, "
-        "W=16 window 0: sampled batches vs oracle, hot set, staged and gathered rows")
-    import torch as T
-    from oracle import ggref
+        "W=16, windows 0 and 1 against the oracle")
     inst, rp_d, ci_d, sh_d = synth.torch_instance("papers_share", "cuda:0")
-    wl = inst.wl
     assert all(not sh_d[m].is_cuda for m in (1, 2, 3)) and sh_d[0].is_cuda
     w = world(inst, tensors=(rp_d, ci_d, sh_d))
-    p = w.pipe
-    seeds, so, b0 = w.window_inputs(0)
-    log(f"papers_share: running window 0 ({len(seeds)} seeds)")
-    Wk = p.window(T.from_numpy(seeds).to(w.dev), so, b0)
-    T.cuda.synchronize()
-    assert p.read_status() == 0
-    L = len(wl.fanout)
-    fids, foff, nids, noff = p.sample_outputs(Wk)
-    rs = inst.range_start
-    for b in (0, 9, 15):
-        log(f"papers_share: oracle on batch {b}")
-        s = seeds[so[b]:so[b + 1]]
-        f1, o1, n1, no1 = ggref.sample_window(inst.row_ptr, inst.col_idx, s,
-                                              np.array([0, len(s)], np.int64), wl.fanout, 0, 0,
-                                              b0 + b)
-        for l in range(L + 1):
-            assert np.array_equal(fids[foff[l * Wk + b]:foff[l * Wk + b + 1]], f1[o1[l]:o1[l + 1]])
-        for l in range(L):
-            assert np.array_equal(nids[noff[l * Wk + b]:noff[l * Wk + b + 1]], n1[no1[l]:no1[l + 1]])
-    allN = fids[foff[L * Wk]:foff[(L + 1) * Wk]]
-    remote = allN[(allN < rs[0]) | (allN >= rs[1])]
-    uniq, cnt = np.unique(remote, return_counts=True)
-    hot, freq, hc, bucket, owner_off = p.hot_outputs()
-    assert np.array_equal(hot, uniq) and np.array_equal(freq, cnt)
-    assert np.array_equal(bucket, hot)
-    st = p.stage_stats_dict()
-    assert st["requests"] == [0, 1, 1, 1] and st["rows_total"] == len(hot)
-    rng = np.random.default_rng(3)
-    rb = wl.row_bytes
-    for s_ in rng.choice(len(hot), 3000, replace=False).tolist():
-        u = int(bucket[s_])
-        m = int(np.searchsorted(rs, u, side="right") - 1)
-        assert np.array_equal(p.cache[s_, :rb].cpu().numpy(), inst.shards[m][u - rs[m], :rb])
-    base = int(foff[L * Wk])
-    rows = rng.choice(len(allN), 5000, replace=False)
-    got = p.win_out[T.from_numpy(rows).to(w.dev)].cpu().numpy()
-    for r_, g in zip(rows.tolist(), got):
-        u = int(fids[base + r_])
-        m = int(np.searchsorted(rs, u, side="right") - 1)
-        assert np.array_equal(g[:rb], inst.shards[m][u - rs[m], :rb])
-    for b in range(Wk):
-        gs = p.gather_stats_dict(b)
-        assert gs["misses"] == 0 and gs["local"] + gs["hits"] == gs["rows"]
+    for k in range(2):
+        log(f"papers_share: window {k}")
+        r = w.run_and_compare(k)
+        assert r["stage"]["requests"] == [0, 1, 1, 1]
 
 
 @pytest.mark.parametrize("name,n_hot,W", [("small", -1, None), ("small", 3000, None),
@@ -606,51 +535,39 @@ def test_inplace_free_list_blocks_take_several_chunks(emit_blocks, monkeypatch):
     assert max(ext[:-1]) > 2 * 8192, ext
 
 
-def test_inplace_staging_out_of_slots_leaves_misses():
-    """A persistent cache one slot short of two windows' hot sets: the
-    second staging raises GG_DEV_CAPACITY and leaves the last delta row out
-    of the remap, and the gathers still return every row, that one through
-    the miss path."""
-    log("small: in-place staging with a cache one slot short of two windows")
-    import torch as T
+@pytest.mark.parametrize("short_by", [1, 40])
+def test_inplace_staging_out_of_slots_leaves_misses(short_by):
+    """A persistent cache short of two windows' hot sets: the second staging
+    raises GG_DEV_CAPACITY and leaves the delta rows past the last free slot
+    out of the remap, and the gathers still return every row, those through
+    the miss path.  The third window must treat every slot the short window
+    filled as taken (the occupancy extent covers the whole cache), so none of
+    its delta rows lands on a row it keeps.  All three windows against the
+    oracle: remaps, every staged row, statistics, every gathered row."""
+    log(f"small: in-place staging with a cache {short_by} slot(s) short of two windows, "
+        "three windows")
     from oracle import ggref
-    from paper_2606_02916_amd import gg
     inst = synth.instance("small")
     wl = inst.wl
     L = len(wl.fanout)
-    w = world(inst, inplace=True)
-    p = w.pipe
+    part = ggref.make_part(wl.num_parts, wl.part_kind, wl.local_owner, wl.num_nodes,
+                           inst.range_start)
     hot = []
     for k in range(2):
-        seeds, so, b0 = w.window_inputs(k)
+        b0, b1 = synth.window_batches(inst.batch_off, wl.W, k)
+        boff = inst.batch_off
+        seeds, so = inst.seeds[boff[b0]:boff[b1]], boff[b0:b1 + 1] - boff[b0]
         fids, foff, _, _ = ggref.sample_window(inst.row_ptr, inst.col_idx, seeds, so, wl.fanout,
                                                0, 0, b0)
-        hot.append(ggref.build_hotset(fids, foff, len(so) - 1, L, w.part_ref, -1)[0])
+        hot.append(ggref.build_hotset(fids, foff, len(so) - 1, L, part, -1)[0])
     union = len(set(hot[0].tolist()) | set(hot[1].tolist()))
-    assert union - 1 >= len(hot[0]) and union - 1 <= p.cache_rows
-    p.cache_rows = union - 1
-    for k in range(2):
-        seeds, so, b0 = w.window_inputs(k)
-        Wk = p.window(T.from_numpy(seeds).to(w.dev), so, b0)
-        T.cuda.synchronize()
-        st = p.read_status()
-        assert st == (0 if k == 0 else gg.DEV_CAPACITY), (k, st)
-    fids, foff, _, _ = p.sample_outputs(Wk)
-    remap = p.slot_ofs[1].cpu().numpy()
-    placed = remap[hot[1]] >= 0
-    assert placed.sum() == len(hot[1]) - 1
-    left_out = int(hot[1][~placed][0])
-    base = int(foff[L * Wk])
-    ids = fids[base:int(foff[(L + 1) * Wk])]
-    got = p.win_out[:len(ids), :wl.row_bytes].cpu().numpy()
-    rs = inst.range_start
-    for r_, u in enumerate(ids.tolist()):
-        m = helpers.owner_of(wl.part_kind, wl.num_parts, rs, u)
-        want = inst.shards[m][helpers.row_of(wl.part_kind, wl.num_parts, rs, u), :wl.row_bytes]
-        assert np.array_equal(got[r_], want), (r_, u)
-    misses = sum(p.gather_stats_dict(b)["misses"] for b in range(Wk))
-    assert misses == sum(int(left_out in fids[foff[L * Wk + b]:foff[L * Wk + b + 1]])
-                         for b in range(Wk)) > 0
+    rows = union - short_by
+    assert rows >= len(hot[0])
+    w = world(inst, inplace=True, cache_rows=rows)
+    shorts = [w.run_and_compare(k)["short"] for k in range(3)]
+    assert shorts[:2] == [False, True], shorts
+    # the short window's occupancy extent covers the whole cache
+    assert int(w.pipe.occs[1][:8].cpu().numpy().view(np.int64)[0]) == rows
 
 
 @pytest.mark.parametrize("name,n_hot,W,nsets,host,gev,rows", [
