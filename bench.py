@@ -211,6 +211,9 @@ def main():
     ap.add_argument("--breakdown", action="store_true",
                     help="record events between sampling, hot set and bucketing as well (each "
                          "event on the build stream costs a few us per window)")
+    ap.add_argument("--tune", default=None, metavar="FIELD=VALUE,...",
+                    help="launch tuning passed to every call (gg_tuning_t fields, e.g. "
+                         "gather_blocks=768,gather_loads=8); results do not change")
     ap.add_argument("--sets", type=int, default=None,
                     help="buffer sets of the look-ahead pipeline (how far building may run ahead)")
     ap.add_argument("--wsweep", default=None,
@@ -293,11 +296,12 @@ def main():
              wl.batch_size)
     look = args.pipeline == "lookahead"
     inplace_cache = args.pipeline in ("lookahead", "inplace")
+    tuning = parse_tuning(args.tune)
     if look:
-        pipe = LookaheadPipeline(*pargs, device=dev, nsets=args.sets)
+        pipe = LookaheadPipeline(*pargs, device=dev, nsets=args.sets, tuning=tuning)
     else:
         pipe = FetchPipeline(*pargs, device=dev, delta=args.pipeline == "delta",
-                             inplace=args.pipeline == "inplace")
+                             inplace=args.pipeline == "inplace", tuning=tuning)
     boff = inst.batch_off
     nwin = synth.n_windows(boff, W)
     wins = []
@@ -502,6 +506,7 @@ def main():
                    "fanout": list(wl.fanout), "batch": wl.batch_size, "W": W,
                    "partitions": P, "local_owner": wl.local_owner, "windows_per_epoch": nwin,
                    "gather_launch": "per batch" if pb else "per window",
+                   "tuning": args.tune or "defaults",
                    "driver": args.pipeline + (f" ({pipe.nsets} buffer sets, staging on the "
                                               f"{'build' if stage_on_build else 'fetch'} stream)"
                                               if look else "")},
@@ -554,6 +559,18 @@ def main():
         "cpu_baseline": cpu,
     }
     print(json.dumps(line), flush=True)
+
+
+def parse_tuning(spec):
+    """--tune FIELD=VALUE,... as a gg_tuning_t (None when empty)."""
+    from paper_2606_02916_amd import gg
+    if not spec:
+        return None
+    fields = {}
+    for item in spec.split(","):
+        k, _, v = item.partition("=")
+        fields[k.strip()] = int(v)
+    return gg.make_tuning(**fields)
 
 
 def consumer_report(dims, lev_w, order, cevs, wl):
@@ -674,7 +691,7 @@ def ablation(args, wl):
 
     def stage(ids, off, n, out, slot, stats):
         gg.gg_stage_bulk(ids, off, n, pipe.part, pipe.feat, out, stride, n, slot, None, None,
-                         None, None, stats, pipe.status, pipe.ws)
+                         None, None, stats, pipe.status, pipe.ws, tuning=pipe.tuning)
 
     def stage_full():
         stage(bucket, owner_off, pipe.hot_cap, cache, pipe.slot_of, pipe.stage_stats)
@@ -757,7 +774,7 @@ def ablation(args, wl):
     ref_out, ref_cache, tiles = None, None, []
     try:
         for t in sorted({64, 16, 4, 1, fill_rows(8192), *defaults.values()}, reverse=True):
-            os.environ["GG_TILE_ROWS"] = str(t)
+            pipe.tuning = gg.make_tuning(tile_rows=t)
             gm = timed(lambda: pipe.gather_window(Wk), 10)
             sm = timed(stage_full, 10)
             out = pipe.win_out[:g_rows, :rb]
@@ -773,7 +790,7 @@ def ablation(args, wl):
                           "stage_GBps": round(s_bytes / (sm * 1e-3) / 1e9, 1)})
             log(json.dumps(tiles[-1]))
     finally:
-        os.environ.pop("GG_TILE_ROWS", None)
+        pipe.tuning = None
     res["tile"] = tiles
     del ref_out, ref_cache
 

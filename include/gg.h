@@ -23,9 +23,11 @@
  *    The caller owns every buffer and keeps it alive until the work queued
  *    on `stream` has finished.
  *  - Calls only enqueue work on `stream`; they never allocate, never
- *    synchronise and keep no state between calls.  Scratch memory is the
- *    caller's workspace `ws` of at least the size returned by the matching
- *    gg_ws_* function; its contents need no initialisation.
+ *    synchronise and keep no state between calls (the library reads no
+ *    environment and holds no global settings: launch tuning is an
+ *    argument, gg_tuning_t).  Scratch memory is the caller's workspace `ws`
+ *    of at least the size returned by the matching gg_ws_* function; its
+ *    contents need no initialisation.
  *  - Return value: GG_OK, or a GG_ERR_* code when a host-visible argument
  *    is invalid (nothing is enqueued then) or a launch failed;
  *    gg_last_error() gives a message (per thread).
@@ -153,6 +155,33 @@ typedef struct gg_gather_stats {
   int64_t miss_rows[GG_MAX_PARTS];
 } gg_gather_stats_t;
 
+/* Launch tuning.  Results never depend on it: it only changes how the work
+ * is spread over the chip (for sweeps of the launch shape, and for tests
+ * that reach code paths small inputs would not).  Every call that takes a
+ * `tuning` pointer accepts NULL (all defaults), and a field left 0 keeps
+ * its default; values outside the stated ranges are GG_ERR_ARG.  A call
+ * and the gg_ws_* function that sized its workspace must be given the same
+ * values (the hot-set chunk limit, the byte-map limit and the gather's
+ * block count change workspace layouts). */
+typedef struct gg_tuning {
+  int32_t tile_rows;         /* rows a wavefront copies per step, 1..64 (staging and gathers);
+                                default: as many as fit in 32 KB (staging) or 8 KB (gathers),
+                                a power of two except for a GG_GATHER_SHARED gather */
+  int32_t gather_blocks;     /* blocks of one gather launch, shared by its segments,
+                                8..65536 (default 1024) */
+  int32_t gather_loads;      /* 16-byte row loads in flight per lane in a gather: 2, 4 or 8
+                                (default 8, or 4 with GG_GATHER_SHARED) */
+  int32_t stage_blocks;      /* most blocks of a staging copy, 1..65536 (default 16384) */
+  int32_t stage_host_blocks; /* most blocks of a staging copy when a shard lives in host
+                                memory, 1..65536, or -1 for stage_blocks (default 128) */
+  int32_t emit_blocks;       /* most blocks of gg_stage_inplace's free-list emit, 1..512
+                                (default 512) */
+  int32_t hot_max_chunks;    /* most chunks of gg_build_hotset's passes, 1..4096 (default
+                                4096; fewer make every chunk span several passes) */
+  int32_t bytemap_max_mb;    /* largest byte map (MB) into which the sampler's last hop marks
+                                its draws, 1..65536, or -1 for none (default 512) */
+} gg_tuning_t;
+
 /* Words per batch of frontier_bits (a multiple of 2048). */
 int64_t gg_bits_words(int64_t num_nodes);
 
@@ -164,12 +193,12 @@ int gg_sample_caps(int64_t num_nodes, int32_t W, int64_t max_batch, const int32_
                    int32_t L, int64_t* frontier_cap, int64_t* nbr_cap);
 
 /* Workspace sizes in bytes. */
-size_t gg_ws_sample(int64_t num_nodes, int32_t W);
-size_t gg_ws_hotset(int64_t num_nodes, int32_t W);
+size_t gg_ws_sample(int64_t num_nodes, int32_t W, const gg_tuning_t* tuning);
+size_t gg_ws_hotset(int64_t num_nodes, int32_t W, const gg_tuning_t* tuning);
 size_t gg_ws_bucket(int64_t cap, int32_t num_parts);
 size_t gg_ws_stage(int64_t cap, int32_t num_parts);
 size_t gg_ws_stage_inplace(int64_t cap, int64_t cache_rows, int32_t num_parts);
-size_t gg_ws_gather(int64_t n_cap, int32_t nseg, int32_t num_parts);
+size_t gg_ws_gather(int64_t n_cap, int32_t nseg, int32_t num_parts, const gg_tuning_t* tuning);
 
 /* Neighbour sampling of one window (Sec. IV-A step 2: one epoch of
  * deterministic sampling under fixed seeds fixes every later access).
@@ -183,13 +212,15 @@ size_t gg_ws_gather(int64_t n_cap, int32_t nseg, int32_t num_parts);
  * floor(r * (d-k+i+1) / 2^32)), ascending.  F_{l+1} is F_l together with
  * the neighbours drawn at hop l.  batch0 is the epoch-global index of the
  * window's first batch, so N_b does not depend on W.  When W * 32 *
- * gg_bits_words(num_nodes) is at most 512 MB the workspace also holds a
- * byte map (one byte per node and batch) into which the last hop marks its
- * draws; gg_ws_sample includes it. */
+ * gg_bits_words(num_nodes) is at most tuning->bytemap_max_mb (512 MB by
+ * default) the workspace also holds a byte map (one byte per node and
+ * batch) into which the last hop marks its draws; gg_ws_sample includes
+ * it. */
 int gg_sample_window(const gg_csr_t* csr, const int32_t* seeds_d, const int64_t* seed_off_h,
                      int32_t W, const int32_t* fanout_h, int32_t L, uint64_t rng_seed,
-                     int32_t epoch, int64_t batch0, const gg_wsample_t* out, int32_t* status_d,
-                     void* ws, size_t ws_bytes, hipStream_t stream);
+                     int32_t epoch, int64_t batch0, const gg_wsample_t* out,
+                     const gg_tuning_t* tuning, int32_t* status_d, void* ws, size_t ws_bytes,
+                     hipStream_t stream);
 
 /* Hot set of the window (Sec. IV-A: the most frequently accessed remote
  * nodes of the window).  Input: the W bit sets N_b written by
@@ -206,8 +237,9 @@ int gg_sample_window(const gg_csr_t* csr, const int32_t* seeds_d, const int64_t*
  * required. */
 int gg_build_hotset(const uint32_t* frontier_bits_d, int32_t W, const gg_part_t* part,
                     int64_t n_hot, int64_t hot_num, int64_t hot_den, int32_t* hot_ids_d,
-                    int32_t* hot_freq_d, int64_t cap, int64_t* hot_count_d, int32_t* status_d,
-                    void* ws, size_t ws_bytes, hipStream_t stream);
+                    int32_t* hot_freq_d, int64_t cap, int64_t* hot_count_d,
+                    const gg_tuning_t* tuning, int32_t* status_d, void* ws, size_t ws_bytes,
+                    hipStream_t stream);
 
 /* Groups the hot set by owner, one bucket per owner (Sec. IV-A: one bulk
  * request per partition owner): bucket_ids_d receives the hot_count_d[0]
@@ -247,8 +279,8 @@ int gg_stage_bulk(const int32_t* bucket_ids_d, const int64_t* owner_off_d, int64
                   int64_t cache_stride, int64_t cache_rows, int32_t* slot_of_d,
                   const int32_t* clear_ids_d, const int64_t* clear_count_d,
                   const void* src_cache_d, const int32_t* src_slot_of_d,
-                  gg_stage_stats_t* stats_d, int32_t* status_d, void* ws, size_t ws_bytes,
-                  hipStream_t stream);
+                  gg_stage_stats_t* stats_d, const gg_tuning_t* tuning, int32_t* status_d,
+                  void* ws, size_t ws_bytes, hipStream_t stream);
 
 /* Delta staging into one persistent cache (Sec. IV-A rebuild events,
  * Eq. (1); Algorithm 1 WarmCache(H_{k+1} \ C)): rows the previous window
@@ -284,8 +316,8 @@ int gg_stage_inplace(const int32_t* bucket_ids_d, const int64_t* owner_off_d, in
                      int64_t cache_stride, int64_t cache_rows, int32_t* slot_of_d,
                      const int32_t* clear_ids_d, const int64_t* clear_count_d,
                      const int32_t* prev_slot_of_d, const uint8_t* occ_prev_d, uint8_t* occ_d,
-                     gg_stage_stats_t* stats_d, int32_t* status_d, void* ws, size_t ws_bytes,
-                     hipStream_t stream);
+                     gg_stage_stats_t* stats_d, const gg_tuning_t* tuning, int32_t* status_d,
+                     void* ws, size_t ws_bytes, hipStream_t stream);
 
 /* Assembles the input features of nseg consecutive batches (Algorithm 1
  * inner loop) in one launch.  Segment s (s < nseg) is batch s: its ids are
@@ -314,8 +346,8 @@ int gg_gather_batch(const int32_t* in_ids_d, const int64_t* bounds_d, int32_t ns
                     int64_t n_cap, const gg_part_t* part, const gg_feat_t* feat,
                     const void* cache_d, int64_t cache_stride, int64_t cache_rows,
                     const int32_t* slot_of_d, void* out_d, int64_t out_stride, int32_t flags,
-                    gg_gather_stats_t* stats_d, int32_t* status_d, void* ws, size_t ws_bytes,
-                    hipStream_t stream);
+                    gg_gather_stats_t* stats_d, const gg_tuning_t* tuning, int32_t* status_d,
+                    void* ws, size_t ws_bytes, hipStream_t stream);
 
 /* ---------------------------------------------------------------------------
  * Window-size simulator counts.  The paper scores a candidate window size W

@@ -66,20 +66,43 @@ int pack_feat(const gg_feat_t* feat, const gg_part_t* part, KFeat* out) {
   return GG_OK;
 }
 
-bool env_flag(const char* name, bool dflt) {
-  const char* v = getenv(name);
-  if (!v || !*v) return dflt;
-  return strcmp(v, "0") != 0;
+int resolve_tuning(const gg_tuning_t* t, Tune* out) {
+  const gg_tuning_t z = {};
+  if (!t) t = &z;
+  GG_REQUIRE(t->tile_rows >= 0 && t->tile_rows <= kWave, "tuning: tile_rows %d outside 1..%d",
+             t->tile_rows, kWave);
+  GG_REQUIRE(t->gather_blocks == 0 || (t->gather_blocks >= 8 && t->gather_blocks <= 65536),
+             "tuning: gather_blocks %d outside 8..65536", t->gather_blocks);
+  GG_REQUIRE(t->gather_loads == 0 || t->gather_loads == 2 || t->gather_loads == 4 ||
+                 t->gather_loads == 8,
+             "tuning: gather_loads %d is not 2, 4 or 8", t->gather_loads);
+  GG_REQUIRE(t->stage_blocks >= 0 && t->stage_blocks <= 65536,
+             "tuning: stage_blocks %d outside 1..65536", t->stage_blocks);
+  GG_REQUIRE(t->stage_host_blocks >= -1 && t->stage_host_blocks <= 65536,
+             "tuning: stage_host_blocks %d outside 1..65536 (or -1)", t->stage_host_blocks);
+  GG_REQUIRE(t->emit_blocks >= 0 && t->emit_blocks <= kEmitBlocksMax,
+             "tuning: emit_blocks %d outside 1..%d", t->emit_blocks, kEmitBlocksMax);
+  GG_REQUIRE(t->hot_max_chunks >= 0 && t->hot_max_chunks <= kHotMaxChunks,
+             "tuning: hot_max_chunks %d outside 1..%d", t->hot_max_chunks, kHotMaxChunks);
+  GG_REQUIRE(t->bytemap_max_mb >= -1 && t->bytemap_max_mb <= 65536,
+             "tuning: bytemap_max_mb %d outside 1..65536 (or -1)", t->bytemap_max_mb);
+  out->tile_rows = t->tile_rows;
+  out->gather_blocks = t->gather_blocks ? t->gather_blocks : kGatherBlocksDefault;
+  out->gather_loads = t->gather_loads;
+  out->stage_blocks = t->stage_blocks ? t->stage_blocks : kStageBlocksDefault;
+  out->stage_host_blocks = t->stage_host_blocks == 0 ? kStageHostBlocksDefault
+                           : t->stage_host_blocks < 0 ? out->stage_blocks
+                                                      : t->stage_host_blocks;
+  out->emit_blocks = t->emit_blocks ? t->emit_blocks : kEmitBlocksMax;
+  out->hot_max_chunks = t->hot_max_chunks ? t->hot_max_chunks : kHotMaxChunks;
+  out->bytemap_max_bytes = t->bytemap_max_mb == 0 ? kByteMapMaxBytes
+                           : t->bytemap_max_mb < 0 ? -1
+                                                   : (int64_t)t->bytemap_max_mb << 20;
+  return GG_OK;
 }
 
-int env_int(const char* name, int dflt) {
-  const char* v = getenv(name);
-  return (v && *v) ? atoi(v) : dflt;
-}
-
-int32_t copy_tile(int32_t row_bytes, int32_t max_bytes, bool pow2) {
-  const int v = env_int("GG_TILE_ROWS", 0);
-  if (v > 0) return v < kWave ? v : kWave;
+int32_t copy_tile(const Tune& tune, int32_t row_bytes, int32_t max_bytes, bool pow2) {
+  if (tune.tile_rows > 0) return tune.tile_rows;
   return pow2 ? tile_rows(row_bytes, max_bytes) : fill_rows(row_bytes, max_bytes);
 }
 

@@ -21,10 +21,10 @@ namespace gg {
 namespace {
 
 constexpr int kTilesPerBlock = kBlock / kWave;  // 4 waves
-// Blocks per launch, shared by the segments: 1024 (four per CU) beat 512,
-// 768, 1536 and 2048 on a 1.5M-row window, alone (236 us warm, 267 us
-// cold) and beside the next window's sampling.
-constexpr int kMaxBlocks = 1024;
+// Blocks per launch, shared by the segments (tuning gather_blocks): the
+// default 1024 (four per CU) beat 512, 768, 1536 and 2048 on a 1.5M-row
+// window, alone (236 us warm, 267 us cold) and beside the next window's
+// sampling.
 
 struct GatherArgs {
   int64_t n_cap;        // output rows available
@@ -244,15 +244,15 @@ struct GatherWs {
   int32_t* blk_stat;   // per row block: local, hits, misses per owner
 };
 
-int32_t blocks_per_seg(int64_t n_cap, int32_t nseg) {
-  static const int max_blocks = env_int("GG_GATHER_BLOCKS", kMaxBlocks);
-  int64_t bx = std::max<int64_t>(max_blocks / nseg, 8);
+int32_t blocks_per_seg(int64_t n_cap, int32_t nseg, const Tune& tune) {
+  int64_t bx = std::max<int64_t>(tune.gather_blocks / nseg, 8);
   bx = std::min<int64_t>(bx, std::max<int64_t>(1, cdiv(n_cap, kBlock)));
   return (int32_t)bx;
 }
 
-size_t gather_ws_layout(int64_t n_cap, int32_t nseg, int32_t P, char* base, GatherWs* out) {
-  const int64_t bx = blocks_per_seg(n_cap, nseg);
+size_t gather_ws_layout(int64_t n_cap, int32_t nseg, int32_t P, const Tune& tune, char* base,
+                        GatherWs* out) {
+  const int64_t bx = blocks_per_seg(n_cap, nseg, tune);
   Carve cv{base, 0, ~(size_t)0};
   GatherWs g;
   g.blk_stat = cv.take<int32_t>((size_t)(nseg * bx * (2 + P)));
@@ -286,18 +286,24 @@ void launch_gather(hipStream_t stream, int unroll, int32_t bx, const int32_t* in
 
 using namespace gg;
 
-extern "C" size_t gg_ws_gather(int64_t n_cap, int32_t nseg, int32_t num_parts) {
+extern "C" size_t gg_ws_gather(int64_t n_cap, int32_t nseg, int32_t num_parts,
+                               const gg_tuning_t* tuning) {
+  Tune tune;
+  if (resolve_tuning(tuning, &tune) != GG_OK) return 0;
   if (nseg < 1) nseg = 1;
-  return gather_ws_layout(n_cap, nseg, num_parts, nullptr, nullptr);
+  return gather_ws_layout(n_cap, nseg, num_parts, tune, nullptr, nullptr);
 }
 
 extern "C" int gg_gather_batch(const int32_t* in_ids_d, const int64_t* bounds_d, int32_t nseg,
                                int64_t n_cap, const gg_part_t* part, const gg_feat_t* feat,
                                const void* cache_d, int64_t cache_stride, int64_t cache_rows,
                                const int32_t* slot_of_d, void* out_d, int64_t out_stride,
-                               int32_t flags, gg_gather_stats_t* stats_d, int32_t* status_d,
-                               void* ws, size_t ws_bytes, hipStream_t stream) {
+                               int32_t flags, gg_gather_stats_t* stats_d,
+                               const gg_tuning_t* tuning, int32_t* status_d, void* ws,
+                               size_t ws_bytes, hipStream_t stream) {
   GG_REQUIRE(bounds_d && slot_of_d && stats_d && status_d, "NULL argument");
+  Tune tune;
+  if (resolve_tuning(tuning, &tune) != GG_OK) return GG_ERR_ARG;
   GG_REQUIRE((flags & ~GG_GATHER_SHARED) == 0, "unknown flags 0x%x", (unsigned)flags);
   GG_REQUIRE(nseg >= 1 && nseg <= GG_MAX_W, "nseg = %d outside 1..%d", nseg, GG_MAX_W);
   GG_REQUIRE(n_cap >= 0 && n_cap < (1LL << 31), "n_cap %lld unsupported", (long long)n_cap);
@@ -316,7 +322,7 @@ extern "C" int gg_gather_batch(const int32_t* in_ids_d, const int64_t* bounds_d,
   GG_REQUIRE(((uintptr_t)out_d & 3u) == 0 && ((uintptr_t)cache_d & 3u) == 0,
              "output and cache must be 4-byte aligned");
   GatherWs gw;
-  const size_t need_ws = gather_ws_layout(n_cap, nseg, kp.P, (char*)ws, &gw);
+  const size_t need_ws = gather_ws_layout(n_cap, nseg, kp.P, tune, (char*)ws, &gw);
   GG_REQUIRE(ws && ws_bytes >= need_ws, "workspace of %zu bytes < %zu", ws_bytes, need_ws);
   bool v16 = aligned16(out_d) && out_stride % 16 == 0 &&
              (cache_rows == 0 || (aligned16(cache_d) && cache_stride % 16 == 0));
@@ -339,34 +345,24 @@ extern "C" int gg_gather_batch(const int32_t* in_ids_d, const int64_t* bounds_d,
   // 0.57 on the wide rows; with eight (alone) it stays a power of two, 16
   // rows and 2, which measured 1-3% faster there than 20 and 3.
   const bool shared = (flags & GG_GATHER_SHARED) != 0;
-  a.tile = copy_tile(kf.row_bytes, 8192, !shared);
+  a.tile = copy_tile(tune, kf.row_bytes, 8192, !shared);
   a.pad_ = 0;
   a.geom = copy_geom(kf.row_bytes, v16 ? 16 : 4);
-  const int32_t bx = blocks_per_seg(n_cap, nseg);
-  static const bool nt = env_flag("GG_NT_GATHER", true);
+  const int32_t bx = blocks_per_seg(n_cap, nseg, tune);
   // Row loads in flight per lane: eight alone; four when sharing the chip
   // (with eight, a concurrent sampler ran ~15% slower and the look-ahead
   // window took 6% longer, for 4% more gather speed).
-  static const int unroll_alone = env_int("GG_GATHER_UNROLL", 8);
-  static const int unroll_shared = env_int("GG_GATHER_UNROLL_SHARED", 4);
-  const int unroll = shared ? unroll_shared : unroll_alone;
+  const int unroll = tune.gather_loads ? tune.gather_loads
+                                       : (shared ? kGatherLoadsShared : kGatherLoadsAlone);
   const char* cache = (const char*)cache_d;
   char* out = (char*)out_d;
-  if (v16) {
-    if (nt)
-      launch_gather<16, true>(stream, unroll, bx, in_ids_d, bounds_d, kp, kf, a, cache, slot_of_d, out, gw,
-                              stats_d, status_d);
-    else
-      launch_gather<16, false>(stream, unroll, bx, in_ids_d, bounds_d, kp, kf, a, cache, slot_of_d, out, gw,
-                               stats_d, status_d);
-  } else {
-    if (nt)
-      launch_gather<4, true>(stream, unroll, bx, in_ids_d, bounds_d, kp, kf, a, cache, slot_of_d, out, gw,
-                             stats_d, status_d);
-    else
-      launch_gather<4, false>(stream, unroll, bx, in_ids_d, bounds_d, kp, kf, a, cache, slot_of_d, out, gw,
-                              stats_d, status_d);
-  }
+  // Output rows are stored non-temporally: the gather never reads them back.
+  if (v16)
+    launch_gather<16, true>(stream, unroll, bx, in_ids_d, bounds_d, kp, kf, a, cache, slot_of_d,
+                            out, gw, stats_d, status_d);
+  else
+    launch_gather<4, true>(stream, unroll, bx, in_ids_d, bounds_d, kp, kf, a, cache, slot_of_d,
+                           out, gw, stats_d, status_d);
   GG_LAUNCH_CHECK("k_gather_rows/k_gather_finish");
   return GG_OK;
 }

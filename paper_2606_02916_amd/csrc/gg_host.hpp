@@ -61,16 +61,38 @@ inline int32_t fill_rows(int32_t row_bytes, int32_t max_bytes) {
   return (int32_t)(t < 1 ? 1 : (t > 64 ? 64 : t));
 }
 
+// Launch-shape defaults (gg_tuning_t fields left 0).
+constexpr int kGatherBlocksDefault = 1024;   // gather blocks per launch
+constexpr int kGatherLoadsAlone = 8;         // row loads in flight per lane
+constexpr int kGatherLoadsShared = 4;        // ... under GG_GATHER_SHARED
+constexpr int kStageBlocksDefault = 16384;   // most staging blocks (device shards)
+constexpr int kStageHostBlocksDefault = 128; // ... when a shard is in host memory
+constexpr int kEmitBlocksMax = 512;          // most in-place free-list blocks
+constexpr int kHotMaxChunks = 4096;          // most hot-set chunks
+constexpr int64_t kByteMapMaxBytes = 512LL << 20;  // largest sampler byte map
+
+// gg_tuning_t checked and resolved against the defaults.
+struct Tune {
+  int32_t tile_rows;          // 0: by row width
+  int32_t gather_blocks;
+  int32_t gather_loads;       // 0: by GG_GATHER_SHARED
+  int32_t stage_blocks;
+  int32_t stage_host_blocks;
+  int32_t emit_blocks;
+  int32_t hot_max_chunks;
+  int64_t bytemap_max_bytes;  // -1: no byte map
+};
+
+// Resolves `t` (NULL: every default) into *out; GG_ERR_ARG (with a message)
+// for a value outside its range.
+int resolve_tuning(const gg_tuning_t* t, Tune* out);
+
 // pow2 ? tile_rows(row_bytes, max_bytes) : fill_rows(row_bytes, max_bytes),
-// or, when GG_TILE_ROWS is set (read at every call), that count, at most 64
-// (1 makes a wavefront copy one row per step).
-int32_t copy_tile(int32_t row_bytes, int32_t max_bytes, bool pow2 = true);
+// or the tuning's tile_rows when set (1 makes a wavefront copy one row per
+// step).
+int32_t copy_tile(const Tune& tune, int32_t row_bytes, int32_t max_bytes, bool pow2 = true);
 
 inline bool aligned16(const void* p) { return ((uintptr_t)p & 15u) == 0; }
-
-// Tuning switches read once from the environment: a flag is on unless "0".
-bool env_flag(const char* name, bool dflt);
-int env_int(const char* name, int dflt);
 
 // Number of shards with rows whose memory is pinned host memory (read by
 // the kernels over PCIe rather than from HBM).

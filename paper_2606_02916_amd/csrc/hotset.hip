@@ -90,7 +90,7 @@ __device__ __forceinline__ uint32_t remote_mask(const KPart& p, int64_t w) {
 // chunks of one pass, a 111M-node one 3,388 chunks of four.
 constexpr int kHotWords = kBlock;
 constexpr int kHotMaxIds = kHotWords * 32;  // ids one pass can emit
-constexpr int kHotMaxChunks = 4096;
+static_assert(kHotMaxChunks == 4096, "emit blocks sum at most 16 counts per thread");
 
 // Sums word w of every batch's set into the planes, eight loads in flight.
 __device__ __forceinline__ void load_planes(const uint32_t* bits, const HotArgs& a, int64_t w,
@@ -345,22 +345,20 @@ struct HotWs {
 };
 
 // Passes per chunk and chunks for a window of num_nodes nodes.  The chunk
-// limit can be lowered through GG_HOT_MAX_CHUNKS (read at every call), which
-// lets small graphs exercise multi-pass chunks; it must not change between a
-// gg_ws_hotset call and the calls that use that workspace.
-void hot_chunks(int64_t num_nodes, int32_t* passes, int32_t* nch) {
+// limit is the tuning's hot_max_chunks (at most kHotMaxChunks); a lower one
+// lets small graphs exercise multi-pass chunks, and the workspace layout
+// depends on it.
+void hot_chunks(int64_t num_nodes, const Tune& tune, int32_t* passes, int32_t* nch) {
   const int64_t runs = gg_bits_words(num_nodes) / kHotWords;
-  const char* e = getenv("GG_HOT_MAX_CHUNKS");
-  int64_t maxc = (e && *e) ? atoll(e) : kHotMaxChunks;
-  maxc = std::min<int64_t>(std::max<int64_t>(maxc, 1), kHotMaxChunks);
+  const int64_t maxc = tune.hot_max_chunks;
   const int64_t p = std::max<int64_t>(1, cdiv(runs, maxc));
   *passes = (int32_t)p;
   *nch = (int32_t)cdiv(runs, p);
 }
 
-size_t hot_ws_layout(int64_t num_nodes, int32_t W, char* base, HotWs* out) {
+size_t hot_ws_layout(int64_t num_nodes, int32_t W, const Tune& tune, char* base, HotWs* out) {
   int32_t passes, nch;
-  hot_chunks(num_nodes, &passes, &nch);
+  hot_chunks(num_nodes, tune, &passes, &nch);
   Carve cv{base, 0, ~(size_t)0};
   HotWs h;
   h.chunk_hist = cv.take<int32_t>((size_t)nch * (W + 1));
@@ -376,17 +374,22 @@ size_t hot_ws_layout(int64_t num_nodes, int32_t W, char* base, HotWs* out) {
 
 using namespace gg;
 
-extern "C" size_t gg_ws_hotset(int64_t num_nodes, int32_t W) {
-  return hot_ws_layout(num_nodes, W, nullptr, nullptr);
+extern "C" size_t gg_ws_hotset(int64_t num_nodes, int32_t W, const gg_tuning_t* tuning) {
+  Tune tune;
+  if (resolve_tuning(tuning, &tune) != GG_OK) return 0;
+  return hot_ws_layout(num_nodes, W, tune, nullptr, nullptr);
 }
 
 extern "C" int gg_build_hotset(const uint32_t* frontier_bits_d, int32_t W, const gg_part_t* part,
                                int64_t n_hot, int64_t hot_num, int64_t hot_den,
                                int32_t* hot_ids_d, int32_t* hot_freq_d, int64_t cap,
-                               int64_t* hot_count_d, int32_t* status_d, void* ws,
-                               size_t ws_bytes, hipStream_t stream) {
+                               int64_t* hot_count_d, const gg_tuning_t* tuning,
+                               int32_t* status_d, void* ws, size_t ws_bytes,
+                               hipStream_t stream) {
   GG_REQUIRE(frontier_bits_d && hot_count_d && status_d && (cap == 0 || hot_ids_d),
              "NULL argument");
+  Tune tune;
+  if (resolve_tuning(tuning, &tune) != GG_OK) return GG_ERR_ARG;
   GG_REQUIRE(W >= 1 && W <= GG_MAX_W, "W = %d outside 1..%d", W, GG_MAX_W);
   GG_REQUIRE(cap >= 0, "negative capacity");
   GG_REQUIRE(hot_den >= 0 && hot_den <= (1LL << 31), "hot_den %lld outside 0..2^31",
@@ -399,11 +402,11 @@ extern "C" int gg_build_hotset(const uint32_t* frontier_bits_d, int32_t W, const
   if (rc != GG_OK) return rc;
   GG_REQUIRE(kp.N >= 1, "empty graph");
   HotWs hw;
-  const size_t need_ws = hot_ws_layout(kp.N, W, (char*)ws, &hw);
+  const size_t need_ws = hot_ws_layout(kp.N, W, tune, (char*)ws, &hw);
   GG_REQUIRE(ws && ws_bytes >= need_ws, "workspace of %zu bytes < %zu", ws_bytes, need_ws);
   const int64_t wpb = gg_bits_words(kp.N);
   int32_t passes, nch;
-  hot_chunks(kp.N, &passes, &nch);
+  hot_chunks(kp.N, tune, &passes, &nch);
   HotArgs a;
   a.wpb = wpb;
   a.cap = cap;

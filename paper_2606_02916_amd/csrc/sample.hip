@@ -51,16 +51,11 @@ struct SampleArgs {
 // is at most this large: a random byte store costs about a third of a
 // random atomic, and folding the map into the bit sets is one streaming
 // pass.  Above it (the 111M-node graph) the pass would cost more than the
-// atomics it saves.
-// GG_BYTEMAP_MAX_MB overrides the limit (0 turns the map off); it is read
-// at every call and must not change between gg_ws_sample and the calls
-// that use that workspace.
-constexpr int64_t kByteMapMaxBytes = 512LL << 20;
-
-inline bool use_bytemap(int64_t num_nodes, int32_t W) {
-  const char* e = getenv("GG_BYTEMAP_MAX_MB");
-  const int64_t lim = (e && *e) ? (int64_t)atoll(e) << 20 : kByteMapMaxBytes;
-  return (int64_t)W * gg_bits_words(num_nodes) * 32 <= lim;
+// atomics it saves.  The limit is the tuning's bytemap_max_mb (default
+// kByteMapMaxBytes); the workspace layout depends on it.
+inline bool use_bytemap(int64_t num_nodes, int32_t W, const Tune& tune) {
+  return tune.bytemap_max_bytes >= 0 &&
+         (int64_t)W * gg_bits_words(num_nodes) * 32 <= tune.bytemap_max_bytes;
 }
 
 // Largest b in [0, 64) with off[b] <= x, for a table padded with INT64_MAX.
@@ -473,7 +468,8 @@ struct SampleWs {
   uint8_t* map;       // the last hop's byte map (32 * wpb bytes per batch), or null
 };
 
-size_t sample_ws_layout(int64_t num_nodes, int32_t W, char* base, SampleWs* out) {
+size_t sample_ws_layout(int64_t num_nodes, int32_t W, const Tune& tune, char* base,
+                        SampleWs* out) {
   const int64_t nch = gg_bits_words(num_nodes) / kChunkWords;
   Carve cv{base, 0, ~(size_t)0};
   SampleWs s;
@@ -482,7 +478,7 @@ size_t sample_ws_layout(int64_t num_nodes, int32_t W, char* base, SampleWs* out)
   s.tot_level = (int64_t)W * kTotLanes * s.ngroups;
   s.tot = cv.take<int32_t>((size_t)(GG_MAX_LAYERS + 1) * s.tot_level);
   s.lvl = cv.take<LevelState>(1);
-  s.map = use_bytemap(num_nodes, W)
+  s.map = use_bytemap(num_nodes, W, tune)
               ? cv.take<uint8_t>((size_t)W * (size_t)gg_bits_words(num_nodes) * 32)
               : nullptr;
   if (out) *out = s;
@@ -515,16 +511,21 @@ int launch_sample(const gg_csr_t* csr, const gg_wsample_t* out, const SampleWs& 
 
 using namespace gg;
 
-extern "C" size_t gg_ws_sample(int64_t num_nodes, int32_t W) {
-  return sample_ws_layout(num_nodes, W, nullptr, nullptr);
+extern "C" size_t gg_ws_sample(int64_t num_nodes, int32_t W, const gg_tuning_t* tuning) {
+  Tune tune;
+  if (resolve_tuning(tuning, &tune) != GG_OK) return 0;
+  return sample_ws_layout(num_nodes, W, tune, nullptr, nullptr);
 }
 
 extern "C" int gg_sample_window(const gg_csr_t* csr, const int32_t* seeds_d,
                                 const int64_t* seed_off_h, int32_t W, const int32_t* fanout_h,
                                 int32_t L, uint64_t rng_seed, int32_t epoch, int64_t batch0,
-                                const gg_wsample_t* out, int32_t* status_d, void* ws,
-                                size_t ws_bytes, hipStream_t stream) {
+                                const gg_wsample_t* out, const gg_tuning_t* tuning,
+                                int32_t* status_d, void* ws, size_t ws_bytes,
+                                hipStream_t stream) {
   GG_REQUIRE(csr && out && seed_off_h && fanout_h && status_d, "NULL argument");
+  Tune tune;
+  if (resolve_tuning(tuning, &tune) != GG_OK) return GG_ERR_ARG;
   GG_REQUIRE(W >= 1 && W <= GG_MAX_W, "W = %d outside 1..%d", W, GG_MAX_W);
   GG_REQUIRE(L >= 1 && L <= GG_MAX_LAYERS, "L = %d outside 1..%d", L, GG_MAX_LAYERS);
   GG_REQUIRE(csr->num_nodes >= 1 && csr->num_nodes < (1LL << 31), "num_nodes %lld unsupported",
@@ -547,7 +548,7 @@ extern "C" int gg_sample_window(const gg_csr_t* csr, const int32_t* seeds_d,
   GG_REQUIRE(aligned16(out->frontier_bits), "frontier_bits must be 16-byte aligned");
   const int64_t N = csr->num_nodes;
   SampleWs sw;
-  const size_t need_ws = sample_ws_layout(N, W, (char*)ws, &sw);
+  const size_t need_ws = sample_ws_layout(N, W, tune, (char*)ws, &sw);
   GG_REQUIRE(ws && ws_bytes >= need_ws, "workspace of %zu bytes < %zu", ws_bytes, need_ws);
 
   const int64_t wpb = gg_bits_words(N);

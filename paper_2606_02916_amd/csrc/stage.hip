@@ -228,17 +228,14 @@ __global__ void __launch_bounds__(kBlock) k_stage_rows(const int32_t* bucket, co
   if (st) set_status(status, st);
 }
 
+// Cache rows are stored with ordinary stores: the gathers read them next.
 template <int VB>
-void launch_stage_rows(bool nt, int grid, hipStream_t stream, const int32_t* bucket,
+void launch_stage_rows(int grid, hipStream_t stream, const int32_t* bucket,
                        const int64_t* owner_off, const KPart& kp, const KFeat& kf,
                        const StageArgs& a, char* cache, int32_t* slot_of, const char* src_cache,
                        const int32_t* old_slot, const StageStatsArgs& sa, int32_t* status) {
-  if (nt)
-    hipLaunchKernelGGL((k_stage_rows<VB, true>), dim3(grid), dim3(kBlock), 0, stream, bucket,
-                       owner_off, kp, kf, a, cache, slot_of, src_cache, old_slot, sa, status);
-  else
-    hipLaunchKernelGGL((k_stage_rows<VB, false>), dim3(grid), dim3(kBlock), 0, stream, bucket,
-                       owner_off, kp, kf, a, cache, slot_of, src_cache, old_slot, sa, status);
+  hipLaunchKernelGGL((k_stage_rows<VB, false>), dim3(grid), dim3(kBlock), 0, stream, bucket,
+                     owner_off, kp, kf, a, cache, slot_of, src_cache, old_slot, sa, status);
 }
 
 int stage_delta_blocks(int64_t cap) {
@@ -271,12 +268,11 @@ int stage_delta_blocks(int64_t cap) {
 constexpr int kRange = kWave;          // bucket entries per delta count (one wave)
 constexpr int kOccChunk = kBlock * 32; // slots per free-list block (one 32-slot group a thread)
 constexpr int kPrepBlocks = 1024;      // most prep blocks (block counts a rank sums)
-// Most free-list blocks.  Blocks past the previous extent return at once;
-// the cap keeps a large cache (4,224 chunks for the 34.6M slots of a
-// Papers100M share) from launching thousands of them.  GG_EMIT_BLOCKS (read
-// at every call) lowers it, so that small caches exercise blocks that take
-// several chunks.
-constexpr int kEmitBlocks = 512;
+// Most free-list blocks (kEmitBlocksMax, or the tuning's emit_blocks).
+// Blocks past the previous extent return at once; the cap keeps a large
+// cache (4,224 chunks for the 34.6M slots of a Papers100M share) from
+// launching thousands of them, and a lower one makes small caches exercise
+// blocks that take several chunks.
 
 struct InplaceWs {
   int32_t* old_slot;   // [cap]
@@ -620,9 +616,11 @@ extern "C" int gg_stage_bulk(const int32_t* bucket_ids_d, const int64_t* owner_o
                              int64_t cache_stride, int64_t cache_rows, int32_t* slot_of_d,
                              const int32_t* clear_ids_d, const int64_t* clear_count_d,
                              const void* src_cache_d, const int32_t* src_slot_of_d,
-                             gg_stage_stats_t* stats_d, int32_t* status_d, void* ws,
-                             size_t ws_bytes, hipStream_t stream) {
+                             gg_stage_stats_t* stats_d, const gg_tuning_t* tuning,
+                             int32_t* status_d, void* ws, size_t ws_bytes, hipStream_t stream) {
   GG_REQUIRE(owner_off_d && slot_of_d && stats_d && status_d, "NULL argument");
+  Tune tune;
+  if (resolve_tuning(tuning, &tune) != GG_OK) return GG_ERR_ARG;
   GG_REQUIRE(cap >= 0 && cap < (1LL << 31) && cache_rows >= 0, "bad capacity");
   GG_REQUIRE(cap == 0 || bucket_ids_d, "bucket ids are NULL");
   GG_REQUIRE(cache_rows == 0 || cache_d, "cache is NULL");
@@ -648,10 +646,9 @@ extern "C" int gg_stage_bulk(const int32_t* bucket_ids_d, const int64_t* owner_o
   a.cap = cap;
   a.cache_rows = cache_rows;
   a.cache_stride = cache_stride;
-  a.tile = copy_tile(kf.row_bytes, 32768);
+  a.tile = copy_tile(tune, kf.row_bytes, 32768);
   a.pad_ = 0;
   a.geom = copy_geom(kf.row_bytes, v16 ? 16 : 4);
-  static const bool nt = env_flag("GG_NT_STAGE", false);
 
   const int gridd = stage_delta_blocks(cap);
   GG_REQUIRE(ws && ws_bytes >= gg_ws_stage(cap, kp.P), "workspace of %zu bytes < %zu", ws_bytes,
@@ -676,10 +673,7 @@ extern "C" int gg_stage_bulk(const int32_t* bucket_ids_d, const int64_t* owner_o
   // Rows read over PCIe need few waves in flight to keep the link busy; a
   // full grid would hold every CU while it waits and starve kernels on
   // other streams (the next window's sampling), so cap it then.
-  static const int host_cap = env_int("GG_STAGE_HOST_BLOCKS", 128);
-  static const int hbm_cap = env_int("GG_STAGE_BLOCKS", 16384);
-  int64_t gmax = hbm_cap;
-  if (host_cap > 0 && host_shards(kf) > 0) gmax = host_cap;
+  const int64_t gmax = host_shards(kf) > 0 ? tune.stage_host_blocks : tune.stage_blocks;
   const int grid = (int)std::min<int64_t>(std::max<int64_t>(cdiv(ntiles, kBlock / kWave), 1), gmax);
   StageStatsArgs sa;
   sa.prev_count = clear_count_d;
@@ -690,10 +684,10 @@ extern "C" int gg_stage_bulk(const int32_t* bucket_ids_d, const int64_t* owner_o
   sa.nblk_delta = gridd;
   sa.has_src = src_cache_d ? 1 : 0;
   if (v16)
-    launch_stage_rows<16>(nt, grid, stream, bucket_ids_d, owner_off_d, kp, kf, a, (char*)cache_d,
+    launch_stage_rows<16>(grid, stream, bucket_ids_d, owner_off_d, kp, kf, a, (char*)cache_d,
                           slot_of_d, (const char*)src_cache_d, old_slot, sa, status_d);
   else
-    launch_stage_rows<4>(nt, grid, stream, bucket_ids_d, owner_off_d, kp, kf, a, (char*)cache_d,
+    launch_stage_rows<4>(grid, stream, bucket_ids_d, owner_off_d, kp, kf, a, (char*)cache_d,
                          slot_of_d, (const char*)src_cache_d, old_slot, sa, status_d);
   GG_LAUNCH_CHECK("k_stage_rows");
   return GG_OK;
@@ -710,9 +704,12 @@ extern "C" int gg_stage_inplace(const int32_t* bucket_ids_d, const int64_t* owne
                                 int32_t* slot_of_d, const int32_t* clear_ids_d,
                                 const int64_t* clear_count_d, const int32_t* prev_slot_of_d,
                                 const uint8_t* occ_prev_d, uint8_t* occ_d,
-                                gg_stage_stats_t* stats_d, int32_t* status_d, void* ws,
-                                size_t ws_bytes, hipStream_t stream) {
+                                gg_stage_stats_t* stats_d, const gg_tuning_t* tuning,
+                                int32_t* status_d, void* ws, size_t ws_bytes,
+                                hipStream_t stream) {
   GG_REQUIRE(owner_off_d && slot_of_d && occ_d && stats_d && status_d, "NULL argument");
+  Tune tune;
+  if (resolve_tuning(tuning, &tune) != GG_OK) return GG_ERR_ARG;
   GG_REQUIRE(cap >= 0 && cap < (1LL << 31), "bad capacity");
   GG_REQUIRE(cache_rows >= 0 && cache_rows < (1LL << 31), "bad cache_rows");
   GG_REQUIRE(cap == 0 || bucket_ids_d, "bucket ids are NULL");
@@ -741,10 +738,9 @@ extern "C" int gg_stage_inplace(const int32_t* bucket_ids_d, const int64_t* owne
   a.cap = cap;
   a.cache_rows = cache_rows;
   a.cache_stride = cache_stride;
-  a.tile = copy_tile(kf.row_bytes, 32768);
+  a.tile = copy_tile(tune, kf.row_bytes, 32768);
   a.pad_ = 0;
   a.geom = copy_geom(kf.row_bytes, v16 ? 16 : 4);
-  static const bool nt = env_flag("GG_NT_STAGE", false);
   GG_REQUIRE(((uintptr_t)occ_d & 15u) == 0 && ((uintptr_t)occ_prev_d & 15u) == 0,
              "occupancy maps must be 16-byte aligned");
   const int gridp = inplace_prep_blocks(cap, cache_rows);
@@ -754,16 +750,13 @@ extern "C" int gg_stage_inplace(const int32_t* bucket_ids_d, const int64_t* owne
   GG_LAUNCH_CHECK("k_inplace_prep");
   // the extent is known on the device only: blocks past its chunks return
   // at once, and the grid is capped so that they stay few
-  const int emit_cap = std::min(std::max(env_int("GG_EMIT_BLOCKS", kEmitBlocks), 1), kEmitBlocks);
-  const int64_t nch = occ_prev_d ? std::min<int64_t>(cdiv(cache_rows, kOccChunk), emit_cap) : 0;
+  const int64_t nch =
+      occ_prev_d ? std::min<int64_t>(cdiv(cache_rows, kOccChunk), tune.emit_blocks) : 0;
   hipLaunchKernelGGL(k_inplace_emit, dim3((unsigned)std::max<int64_t>(nch, 1)), dim3(kBlock), 0, stream, occ_prev_d,
                      w.fcnt, w.btot, gridp, w.bpre, w.freel, w.nfree, a);
   GG_LAUNCH_CHECK("k_inplace_emit");
   const int64_t ntiles = cdiv(std::min(cap, cache_rows), a.tile);
-  static const int host_cap = env_int("GG_STAGE_HOST_BLOCKS", 128);
-  static const int hbm_cap = env_int("GG_STAGE_BLOCKS", 16384);
-  int64_t gmax = hbm_cap;
-  if (host_cap > 0 && host_shards(kf) > 0) gmax = host_cap;
+  const int64_t gmax = host_shards(kf) > 0 ? tune.stage_host_blocks : tune.stage_blocks;
   const int grid = (int)std::min<int64_t>(std::max<int64_t>(cdiv(ntiles, kBlock / kWave), 1), gmax);
   StageStatsArgs sa;
   sa.prev_count = clear_count_d;
@@ -773,25 +766,17 @@ extern "C" int gg_stage_inplace(const int32_t* bucket_ids_d, const int64_t* owne
   sa.occ_prev = occ_prev_d;
   sa.nblk_delta = gridp;
   sa.has_src = 1;
-  if (v16) {
-    if (nt)
-      hipLaunchKernelGGL((k_inplace_rows<16, true>), dim3(grid), dim3(kBlock), 0, stream,
-                         bucket_ids_d, owner_off_d, kp, kf, a, (char*)cache_d, slot_of_d,
-                         w.old_slot, w.dr, w.btot, w.bpre, gridp, w.freel, w.nfree, occ_prev_d, occ_d, sa, status_d);
-    else
-      hipLaunchKernelGGL((k_inplace_rows<16, false>), dim3(grid), dim3(kBlock), 0, stream,
-                         bucket_ids_d, owner_off_d, kp, kf, a, (char*)cache_d, slot_of_d,
-                         w.old_slot, w.dr, w.btot, w.bpre, gridp, w.freel, w.nfree, occ_prev_d, occ_d, sa, status_d);
-  } else {
-    if (nt)
-      hipLaunchKernelGGL((k_inplace_rows<4, true>), dim3(grid), dim3(kBlock), 0, stream,
-                         bucket_ids_d, owner_off_d, kp, kf, a, (char*)cache_d, slot_of_d,
-                         w.old_slot, w.dr, w.btot, w.bpre, gridp, w.freel, w.nfree, occ_prev_d, occ_d, sa, status_d);
-    else
-      hipLaunchKernelGGL((k_inplace_rows<4, false>), dim3(grid), dim3(kBlock), 0, stream,
-                         bucket_ids_d, owner_off_d, kp, kf, a, (char*)cache_d, slot_of_d,
-                         w.old_slot, w.dr, w.btot, w.bpre, gridp, w.freel, w.nfree, occ_prev_d, occ_d, sa, status_d);
-  }
+  // Cache rows are stored with ordinary stores: the gathers read them next.
+  if (v16)
+    hipLaunchKernelGGL((k_inplace_rows<16, false>), dim3(grid), dim3(kBlock), 0, stream,
+                       bucket_ids_d, owner_off_d, kp, kf, a, (char*)cache_d, slot_of_d,
+                       w.old_slot, w.dr, w.btot, w.bpre, gridp, w.freel, w.nfree, occ_prev_d,
+                       occ_d, sa, status_d);
+  else
+    hipLaunchKernelGGL((k_inplace_rows<4, false>), dim3(grid), dim3(kBlock), 0, stream,
+                       bucket_ids_d, owner_off_d, kp, kf, a, (char*)cache_d, slot_of_d,
+                       w.old_slot, w.dr, w.btot, w.bpre, gridp, w.freel, w.nfree, occ_prev_d,
+                       occ_d, sa, status_d);
   GG_LAUNCH_CHECK("k_inplace_rows");
   return GG_OK;
 }

@@ -91,6 +91,16 @@ class gg_sim_acc_t(C.Structure):
                 ("e_stall", C.c_double), ("e_phy", C.c_double)]
 
 
+class gg_tuning_t(C.Structure):
+    _fields_ = [("tile_rows", C.c_int32), ("gather_blocks", C.c_int32),
+                ("gather_loads", C.c_int32), ("stage_blocks", C.c_int32),
+                ("stage_host_blocks", C.c_int32), ("emit_blocks", C.c_int32),
+                ("hot_max_chunks", C.c_int32), ("bytemap_max_mb", C.c_int32)]
+
+
+TUNING_FIELDS = tuple(name for name, _ in gg_tuning_t._fields_)
+
+
 class gg_sage_layer_t(C.Structure):
     _fields_ = [("d_in", C.c_int32), ("d_out", C.c_int32), ("relu", C.c_int32),
                 ("w_self", C.c_void_p), ("w_neigh", C.c_void_p), ("bias", C.c_void_p)]
@@ -106,23 +116,23 @@ _P, _I32, _I64, _U64, _SZ = C.c_void_p, C.c_int32, C.c_int64, C.c_uint64, C.c_si
 SIGNATURES = {
     "gg_bits_words": (_I64, [_I64]),
     "gg_sample_caps": (C.c_int, [_I64, _I32, _I64, _P, _I32, _P, _P]),
-    "gg_ws_sample": (_SZ, [_I64, _I32]),
-    "gg_ws_hotset": (_SZ, [_I64, _I32]),
+    "gg_ws_sample": (_SZ, [_I64, _I32, _P]),
+    "gg_ws_hotset": (_SZ, [_I64, _I32, _P]),
     "gg_ws_bucket": (_SZ, [_I64, _I32]),
     "gg_ws_stage": (_SZ, [_I64, _I32]),
     "gg_ws_stage_inplace": (_SZ, [_I64, _I64, _I32]),
-    "gg_ws_gather": (_SZ, [_I64, _I32, _I32]),
-    "gg_sample_window": (C.c_int, [_P, _P, _P, _I32, _P, _I32, _U64, _I32, _I64, _P, _P, _P, _SZ,
-                                   _P]),
-    "gg_build_hotset": (C.c_int, [_P, _I32, _P, _I64, _I64, _I64, _P, _P, _I64, _P, _P, _P, _SZ,
-                                  _P]),
+    "gg_ws_gather": (_SZ, [_I64, _I32, _I32, _P]),
+    "gg_sample_window": (C.c_int, [_P, _P, _P, _I32, _P, _I32, _U64, _I32, _I64, _P, _P, _P, _P,
+                                   _SZ, _P]),
+    "gg_build_hotset": (C.c_int, [_P, _I32, _P, _I64, _I64, _I64, _P, _P, _I64, _P, _P, _P, _P,
+                                  _SZ, _P]),
     "gg_bucket_by_owner": (C.c_int, [_P, _P, _I64, _P, _I32, _P, _P, _P, _P, _SZ, _P]),
     "gg_stage_bulk": (C.c_int, [_P, _P, _I64, _P, _P, _P, _I64, _I64, _P, _P, _P, _P, _P, _P, _P,
-                                _P, _SZ, _P]),
+                                _P, _P, _SZ, _P]),
     "gg_stage_inplace": (C.c_int, [_P, _P, _I64, _P, _P, _P, _I64, _I64, _P, _P, _P, _P, _P,
-                                   _P, _P, _P, _P, _SZ, _P]),
+                                   _P, _P, _P, _P, _P, _SZ, _P]),
     "gg_gather_batch": (C.c_int, [_P, _P, _I32, _I64, _P, _P, _P, _I64, _I64, _P, _P, _I64, _I32,
-                                  _P, _P, _P, _SZ, _P]),
+                                  _P, _P, _P, _P, _SZ, _P]),
     "gg_sim_accumulate": (C.c_int, [_P, _P, _I32, _P, _P, _P, _P]),
     "gg_ws_sage": (_SZ, [_I64, _I32, _I64, _I32, _P]),
     "gg_sage_forward": (C.c_int, [_P, _I64, _I32, _I32, _P, _P, _I32, _I64, _I64, _P, _P, _I64, _P,
@@ -162,6 +172,23 @@ def _stream(stream):
         import torch
         return torch.cuda.current_stream().cuda_stream
     return stream.cuda_stream if hasattr(stream, "cuda_stream") else stream
+
+
+def make_tuning(**fields):
+    """A gg_tuning_t with the given fields set (the rest 0: library
+    defaults), or None when no field is given."""
+    if not fields:
+        return None
+    t = gg_tuning_t()
+    for k, v in fields.items():
+        if k not in TUNING_FIELDS:
+            raise GGError(f"unknown tuning field {k!r}")
+        setattr(t, k, int(v))
+    return t
+
+
+def _tune(tuning):
+    return None if tuning is None else C.byref(tuning)
 
 
 def make_csr(row_ptr, col_idx, num_nodes=None):
@@ -223,12 +250,12 @@ def gg_sample_caps(num_nodes, W, max_batch, fanout):
     return fc.value, nc.value
 
 
-def gg_ws_sample(num_nodes, W):
-    return int(lib.gg_ws_sample(num_nodes, W))
+def gg_ws_sample(num_nodes, W, tuning=None):
+    return int(lib.gg_ws_sample(num_nodes, W, _tune(tuning)))
 
 
-def gg_ws_hotset(num_nodes, W):
-    return int(lib.gg_ws_hotset(num_nodes, W))
+def gg_ws_hotset(num_nodes, W, tuning=None):
+    return int(lib.gg_ws_hotset(num_nodes, W, _tune(tuning)))
 
 
 def gg_ws_bucket(cap, num_parts):
@@ -239,12 +266,12 @@ def gg_ws_stage(cap, num_parts):
     return int(lib.gg_ws_stage(cap, num_parts))
 
 
-def gg_ws_gather(n_cap, nseg, num_parts):
-    return int(lib.gg_ws_gather(n_cap, nseg, num_parts))
+def gg_ws_gather(n_cap, nseg, num_parts, tuning=None):
+    return int(lib.gg_ws_gather(n_cap, nseg, num_parts, _tune(tuning)))
 
 
 def gg_sample_window(csr, seeds, seed_off, W, fanout, L, rng_seed, epoch, batch0, out, status, ws,
-                     stream=None):
+                     stream=None, tuning=None):
     so = np.ascontiguousarray(seed_off, dtype=np.int64)
     fan = np.ascontiguousarray(fanout, dtype=np.int32)
     if seeds is not None and hasattr(seeds, "numel") and seeds.numel() < int(so[-1]):
@@ -252,19 +279,19 @@ def gg_sample_window(csr, seeds, seed_off, W, fanout, L, rng_seed, epoch, batch0
                       f"{seeds.numel()} seeds were given")
     return check(lib.gg_sample_window(C.byref(csr), _ptr(seeds), so.ctypes.data, W,
                                       fan.ctypes.data, L, C.c_uint64(rng_seed), epoch, batch0,
-                                      C.byref(out), _ptr(status), _ptr(ws), ws.numel(),
-                                      _stream(stream)), "gg_sample_window")
+                                      C.byref(out), _tune(tuning), _ptr(status), _ptr(ws),
+                                      ws.numel(), _stream(stream)), "gg_sample_window")
 
 
 def gg_build_hotset(frontier_bits, W, part, n_hot, hot_ids, hot_freq, cap, hot_count, status, ws,
-                    stream=None, hot_frac=None):
+                    stream=None, hot_frac=None, tuning=None):
     """hot_frac = (num, den): budget ceil(U * num / den) of the window's U
     distinct remote nodes (n_hot must then be -1)."""
     num, den = hot_frac if hot_frac is not None else (0, 0)
     return check(lib.gg_build_hotset(_ptr(frontier_bits), W, C.byref(part), n_hot, num, den,
                                      _ptr(hot_ids), _ptr(hot_freq), cap, _ptr(hot_count),
-                                     _ptr(status), _ptr(ws), ws.numel(), _stream(stream)),
-                 "gg_build_hotset")
+                                     _tune(tuning), _ptr(status), _ptr(ws), ws.numel(),
+                                     _stream(stream)), "gg_build_hotset")
 
 
 def gg_bucket_by_owner(hot_ids, hot_count, cap, part, bucket_ids, owner_off, status, ws,
@@ -277,13 +304,14 @@ def gg_bucket_by_owner(hot_ids, hot_count, cap, part, bucket_ids, owner_off, sta
 
 
 def gg_stage_bulk(bucket_ids, owner_off, cap, part, feat, cache, cache_stride, cache_rows, slot_of,
-                  clear_ids, clear_count, src_cache, src_slot_of, stats, status, ws, stream=None):
+                  clear_ids, clear_count, src_cache, src_slot_of, stats, status, ws, stream=None,
+                  tuning=None):
     return check(lib.gg_stage_bulk(_ptr(bucket_ids), _ptr(owner_off), cap, C.byref(part),
                                    C.byref(feat), _ptr(cache), cache_stride, cache_rows,
                                    _ptr(slot_of), _ptr(clear_ids), _ptr(clear_count),
                                    _ptr(src_cache), _ptr(src_slot_of), _ptr(stats),
-                                   _ptr(status), _ptr(ws), ws.numel(), _stream(stream)),
-                 "gg_stage_bulk")
+                                   _tune(tuning), _ptr(status), _ptr(ws), ws.numel(),
+                                   _stream(stream)), "gg_stage_bulk")
 
 
 def gg_ws_stage_inplace(cap, cache_rows, num_parts):
@@ -292,13 +320,13 @@ def gg_ws_stage_inplace(cap, cache_rows, num_parts):
 
 def gg_stage_inplace(bucket_ids, owner_off, cap, part, feat, cache, cache_stride, cache_rows,
                      slot_of, clear_ids, clear_count, prev_slot_of, occ_prev, occ, stats, status,
-                     ws, stream=None):
+                     ws, stream=None, tuning=None):
     return check(lib.gg_stage_inplace(_ptr(bucket_ids), _ptr(owner_off), cap, C.byref(part),
                                       C.byref(feat), _ptr(cache), cache_stride, cache_rows,
                                       _ptr(slot_of), _ptr(clear_ids), _ptr(clear_count),
                                       _ptr(prev_slot_of), _ptr(occ_prev), _ptr(occ), _ptr(stats),
-                                      _ptr(status), _ptr(ws), ws.numel(), _stream(stream)),
-                 "gg_stage_inplace")
+                                      _tune(tuning), _ptr(status), _ptr(ws), ws.numel(),
+                                      _stream(stream)), "gg_stage_inplace")
 
 
 def occ_bytes(cache_rows):
@@ -308,15 +336,16 @@ def occ_bytes(cache_rows):
 
 
 def gg_gather_batch(in_ids, bounds_ptr, nseg, n_cap, part, feat, cache, cache_stride, cache_rows,
-                    slot_of, out, out_stride, stats_ptr, status, ws, stream=None, flags=0):
+                    slot_of, out, out_stride, stats_ptr, status, ws, stream=None, flags=0,
+                    tuning=None):
     """bounds_ptr and stats_ptr are raw device addresses (e.g. an offset into
     frontier_off, or into an array of nseg statistics structures).  flags =
     GG_GATHER_SHARED when other streams sample on the device meanwhile."""
     return check(lib.gg_gather_batch(_ptr(in_ids), bounds_ptr, nseg, n_cap, C.byref(part),
                                      C.byref(feat), _ptr(cache), cache_stride, cache_rows,
                                      _ptr(slot_of), _ptr(out), out_stride, flags, stats_ptr,
-                                     _ptr(status), _ptr(ws), ws.numel(), _stream(stream)),
-                 "gg_gather_batch")
+                                     _tune(tuning), _ptr(status), _ptr(ws), ws.numel(),
+                                     _stream(stream)), "gg_gather_batch")
 
 
 def make_sim_coeffs(P, eps_init, eps_row, lam_init, lam_row, bw_bytes_per_s, row_bytes, p_idle):

@@ -32,7 +32,8 @@ def _bucket_flags(part):
 class _Geometry:
     """Sizes shared by all buffer sets of a pipeline."""
 
-    def __init__(self, N, W, fanout, max_batch, P, local_owner, shard_rows, stride, cache_stride):
+    def __init__(self, N, W, fanout, max_batch, P, local_owner, shard_rows, stride, cache_stride,
+                 tuning=None):
         self.N, self.W, self.P = N, W, P
         self.fanout = [int(k) for k in fanout]
         self.L = len(self.fanout)
@@ -50,10 +51,10 @@ class _Geometry:
         self.inplace_rows = max(1, min(remote, 2 * W * self.out_cap))
         self.win_cap = W * self.out_cap                 # rows of a whole window
         self.seed_cap = W * max(min(max_batch, N), 1)   # F_0 rows of a whole window
-        self.ws_bytes = max(gg.gg_ws_sample(N, W), gg.gg_ws_hotset(N, W),
+        self.ws_bytes = max(gg.gg_ws_sample(N, W, tuning), gg.gg_ws_hotset(N, W, tuning),
                             gg.gg_ws_bucket(self.hot_cap, P), gg.gg_ws_stage(self.hot_cap, P),
-                            gg.gg_ws_gather(self.out_cap, 1, P),
-                            gg.gg_ws_gather(self.win_cap, W, P))
+                            gg.gg_ws_gather(self.out_cap, 1, P, tuning),
+                            gg.gg_ws_gather(self.win_cap, W, P, tuning))
 
 
 class _Buffers:
@@ -104,14 +105,15 @@ class FetchPipeline:
     def __init__(self, row_ptr, col_idx, num_parts, part_kind, local_owner, range_start, shards,
                  shard_rows, row_bytes, stride, W, fanout, max_batch, n_hot=-1, device=None,
                  out_buffers=2, cache_stride=None, delta=False, hot_frac=None, inplace=False,
-                 cache_rows=None):
+                 cache_rows=None, tuning=None):
         """delta: rebuild the cache from the previous window's, requesting only
         the rebuild delta; the cache then alternates between two buffers and
         the rows still wanted are copied across.  inplace (implies delta):
         one persistent cache in which those rows stay put (gg_stage_inplace);
         the remap then alternates between two buffers.  cache_rows (in place
         only): slots of the persistent cache, by default enough for two
-        windows' hot sets; fewer leave rows to the miss path."""
+        windows' hot sets; fewer leave rows to the miss path.  tuning: a
+        gg_tuning_t (gg.make_tuning) passed to every call, or None."""
         self.device = torch.device(device if device is not None else "cuda")
         self.N = int(row_ptr.numel() - 1)
         self.W = int(W)
@@ -132,8 +134,9 @@ class FetchPipeline:
         self.csr = gg.make_csr(row_ptr, col_idx)
         self.part = gg.make_part(self.P, part_kind, local_owner, self.N, range_start)
         self.feat = gg.make_feat(self.row_bytes, shards, [self.stride] * self.P, shard_rows)
+        self.tuning = tuning
         self.geo = _Geometry(self.N, self.W, self.fanout, max_batch, self.P, local_owner,
-                             shard_rows, self.stride, self.cache_stride)
+                             shard_rows, self.stride, self.cache_stride, tuning)
         g, dev = self.geo, self.device
         self.out_cap, self.hot_cap, self.win_cap, self.wpb = g.out_cap, g.hot_cap, g.win_cap, g.wpb
         self.buf = _Buffers(g, dev, own_cache=not self.inplace)
@@ -194,13 +197,13 @@ class FetchPipeline:
     def sample(self, seeds, seed_off, batch0, epoch=0, rng_seed=0):
         Wk = len(seed_off) - 1
         gg.gg_sample_window(self.csr, seeds, seed_off, Wk, self.fanout, self.L, rng_seed, epoch,
-                            batch0, self.wsample, self.status, self.ws)
+                            batch0, self.wsample, self.status, self.ws, tuning=self.tuning)
         return Wk
 
     def hotset(self, Wk, cur):
         gg.gg_build_hotset(self.frontier_bits, Wk, self.part, self.n_hot, self.hot_ids,
                            self.hot_freq, self.hot_cap, self.hot_count[cur], self.status, self.ws,
-                           hot_frac=self.hot_frac)
+                           hot_frac=self.hot_frac, tuning=self.tuning)
 
     def bucket(self, cur):
         gg.gg_bucket_by_owner(self.hot_ids, self.hot_count[cur], self.hot_cap, self.part,
@@ -223,7 +226,7 @@ class FetchPipeline:
                                 self.hot_count[old] if k >= 2 else None,
                                 self.slot_ofs[1 - X] if k >= 1 else None,
                                 self.occs[1 - X] if k >= 1 else None, self.occs[X],
-                                self.stage_stats, self.status, self.stage_ws)
+                                self.stage_stats, self.status, self.stage_ws, tuning=self.tuning)
             return
         prev = (cur - 1) % self.nslot
         have_prev = self.k > 0
@@ -235,7 +238,7 @@ class FetchPipeline:
                          self.bucket_ids[prev] if have_prev else None,
                          self.hot_count[prev] if have_prev else None,
                          src, self.slot_of if src is not None else None, self.stage_stats,
-                         self.status, self.ws)
+                         self.status, self.ws, tuning=self.tuning)
 
     def staged_cache(self):
         """The cache stage() just filled (valid until the window advances)."""
@@ -247,7 +250,7 @@ class FetchPipeline:
         stats = self.gather_stats.data_ptr() + b * gg.GATHER_STATS_BYTES
         gg.gg_gather_batch(self.frontier_ids, bounds, 1, out.shape[0], self.part, self.feat,
                            self.staged_cache(), self.cache_stride, self.cache_rows, self.slot_of,
-                           out, self.stride, stats, self.status, self.ws)
+                           out, self.stride, stats, self.status, self.ws, tuning=self.tuning)
 
     def gather_window(self, Wk, out=None, flags=0):
         """All Wk batches of the window in one launch; batch b's rows start at
@@ -259,7 +262,7 @@ class FetchPipeline:
         gg.gg_gather_batch(self.frontier_ids, bounds, Wk, out.shape[0], self.part, self.feat,
                            self.staged_cache(), self.cache_stride, self.cache_rows, self.slot_of,
                            out, self.stride, self.gather_stats.data_ptr(), self.status, self.ws,
-                           flags=flags)
+                           flags=flags, tuning=self.tuning)
         return out
 
     def capture_window(self, seeds, seed_off, batch0, epoch=0, rng_seed=0):
@@ -397,7 +400,7 @@ class LookaheadPipeline:
 
     def __init__(self, row_ptr, col_idx, num_parts, part_kind, local_owner, range_start, shards,
                  shard_rows, row_bytes, stride, W, fanout, max_batch, n_hot=-1, device=None,
-                 cache_stride=None, nsets=None, hot_frac=None):
+                 cache_stride=None, nsets=None, hot_frac=None, tuning=None):
         self.device = torch.device(device if device is not None else "cuda")
         self.N = int(row_ptr.numel() - 1)
         self.W = int(W)
@@ -412,8 +415,9 @@ class LookaheadPipeline:
         self.part = gg.make_part(self.P, part_kind, local_owner, self.N, range_start)
         self.feat = gg.make_feat(self.row_bytes, shards, [self.stride] * self.P, shard_rows)
         self.shards = shards
+        self.tuning = tuning
         self.geo = g = _Geometry(self.N, self.W, self.fanout, max_batch, self.P, local_owner,
-                                 shard_rows, self.stride, self.cache_stride)
+                                 shard_rows, self.stride, self.cache_stride, tuning)
         dev = self.device
         on_host = any(t is not None and not t.is_cuda for t in shards)
         if nsets is None:
@@ -481,11 +485,12 @@ class LookaheadPipeline:
         s = bs.cuda_stream
         _rec(ev[0], bs)
         gg.gg_sample_window(self.csr, seeds, seed_off, Wk, self.fanout, self.L, rng_seed, epoch,
-                            batch0, cur.wsample, self.status, cur.ws, stream=s)
+                            batch0, cur.wsample, self.status, cur.ws, stream=s,
+                            tuning=self.tuning)
         _rec(ev[1], bs)
         gg.gg_build_hotset(cur.frontier_bits, Wk, self.part, self.n_hot, cur.hot_ids,
                            cur.hot_freq, g.hot_cap, self.hot_count[T], self.status, cur.ws,
-                           stream=s, hot_frac=self.hot_frac)
+                           stream=s, hot_frac=self.hot_frac, tuning=self.tuning)
         _rec(ev[2], bs)
         gg.gg_bucket_by_owner(cur.hot_ids, self.hot_count[T], g.hot_cap, self.part,
                               self.bucket_ids[T], cur.owner_off, self.status, cur.ws, stream=s,
@@ -509,7 +514,7 @@ class LookaheadPipeline:
                             self.cache, self.cache_stride, self.cache_rows, cur.slot_of,
                             clear_ids, clear_cnt, prev.slot_of if k >= 1 else None,
                             prev.occ if k >= 1 else None, cur.occ, cur.stage_stats, self.status,
-                            self.stage_ws, stream=ss.cuda_stream)
+                            self.stage_ws, stream=ss.cuda_stream, tuning=self.tuning)
         _rec(ev[4], ss)
         if gs is not ss:
             staged = ev[4] if ev[4] is not None else self.staged[X]
@@ -523,7 +528,7 @@ class LookaheadPipeline:
         gg.gg_gather_batch(cur.frontier_ids, bounds, Wk, o.shape[0], self.part, self.feat,
                            self.cache, self.cache_stride, self.cache_rows, cur.slot_of, o,
                            self.stride, cur.gather_stats.data_ptr(), self.status, self.gather_ws,
-                           stream=gs.cuda_stream, flags=gg.GG_GATHER_SHARED)
+                           stream=gs.cuda_stream, flags=gg.GG_GATHER_SHARED, tuning=self.tuning)
         _rec(end, gs)
         if sim is not None:           # simulator totals, in window order on the gather stream
             gg.gg_sim_accumulate(cur.stage_stats, cur.gather_stats.data_ptr(), Wk, self.part,
@@ -553,7 +558,8 @@ class LookaheadPipeline:
         gg.gg_gather_batch(bufs.frontier_ids, bounds, Wk, o.shape[0], self.part, self.feat,
                            self.cache, self.cache_stride, self.cache_rows, bufs.slot_of, o,
                            self.stride, bufs.gather_stats.data_ptr(), self.status,
-                           self.gather_ws, stream=stream, flags=gg.GG_GATHER_SHARED)
+                           self.gather_ws, stream=stream, flags=gg.GG_GATHER_SHARED,
+                           tuning=self.tuning)
         return o
 
     def gathered_event(self, k):

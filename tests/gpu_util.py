@@ -20,7 +20,8 @@ class World:
 
     def __init__(self, inst, W=None, n_hot=-1, local_owner=None, fanout=None, batch=None,
                  device="cuda:0", shards=None, row_bytes=None, stride=None, cache_stride=None,
-                 tensors=None, delta=False, hot_frac=None, inplace=False, cache_rows=None):
+                 tensors=None, delta=False, hot_frac=None, inplace=False, cache_rows=None,
+                 tuning=None):
         wl = inst.wl
         self.inst = inst
         self.wl = wl
@@ -46,7 +47,7 @@ class World:
                                   self.rs, self.shards_d, rows, self.row_bytes, self.stride,
                                   self.W, self.fanout, self.batch, n_hot=n_hot, device=self.dev,
                                   cache_stride=cache_stride, delta=delta, hot_frac=hot_frac,
-                                  inplace=inplace, cache_rows=cache_rows)
+                                  inplace=inplace, cache_rows=cache_rows, tuning=tuning)
         self.part_ref = ggref.make_part(self.P, wl.part_kind, self.local, wl.num_nodes, self.rs)
         self.feat_ref = ggref.make_feat(self.row_bytes, self.shards, [self.stride] * self.P)
         self.cstride = self.pipe.cache_stride

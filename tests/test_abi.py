@@ -65,6 +65,9 @@ int main() {
   F(gg_sim_acc_t, hits) F(gg_sim_acc_t, e_rebuild) F(gg_sim_acc_t, t_stall) F(gg_sim_acc_t, e_phy)
   S(gg_sage_layer_t) F(gg_sage_layer_t, relu) F(gg_sage_layer_t, w_self)
   F(gg_sage_layer_t, w_neigh) F(gg_sage_layer_t, bias)
+  S(gg_tuning_t) F(gg_tuning_t, gather_blocks) F(gg_tuning_t, gather_loads)
+  F(gg_tuning_t, stage_blocks) F(gg_tuning_t, stage_host_blocks) F(gg_tuning_t, emit_blocks)
+  F(gg_tuning_t, hot_max_chunks) F(gg_tuning_t, bytemap_max_mb)
   return 0;
 }
 """
@@ -104,6 +107,18 @@ def test_host_helpers(gg):
     for f in (gg.gg_ws_sample, gg.gg_ws_hotset):
         assert f(10_000, 4) > 0 and f(10_000, 4) % 256 == 0
     assert gg.gg_ws_bucket(0, 4) > 0 and gg.gg_ws_gather(0, 1, 4) > 0 and gg.gg_ws_stage(0, 4) > 0
+    # tuning that changes workspace layouts changes the sizes; bad tuning sizes nothing
+    N, W = 2_450_000, 16
+    assert gg.gg_ws_sample(N, W) > gg.gg_ws_sample(N, W, gg.make_tuning(bytemap_max_mb=-1))
+    assert gg.gg_ws_sample(N, W, gg.make_tuning(bytemap_max_mb=1)) == \
+        gg.gg_ws_sample(N, W, gg.make_tuning(bytemap_max_mb=-1))
+    assert gg.gg_ws_hotset(N, W, gg.make_tuning(hot_max_chunks=4)) < gg.gg_ws_hotset(N, W)
+    assert gg.gg_ws_gather(10**6, 1, 4, gg.make_tuning(gather_blocks=64)) < \
+        gg.gg_ws_gather(10**6, 1, 4)
+    assert gg.gg_ws_gather(10**6, 1, 4, gg.make_tuning(gather_loads=3)) == 0
+    assert gg.make_tuning() is None
+    with pytest.raises(gg.GGError):
+        gg.make_tuning(tile=3)
     # the status read checks its pointers before any HIP call
     with pytest.raises(gg.GGError, match="null"):
         gg.gg_read_status(None, stream=0)
@@ -181,6 +196,18 @@ def test_bad_arguments_are_rejected_on_the_host(gg):
         gg.gg_gather_batch(t, t.data_ptr(), 1, 10, part, feat, t, 256, 10, t, t, 256,
                            t.data_ptr(), t, t, stream=0, flags=2)
     assert "flags" in gg.gg_last_error()
+    for field, bad in [("tile_rows", 65), ("tile_rows", -1), ("gather_blocks", 4),
+                       ("gather_loads", 3), ("stage_blocks", -2), ("stage_host_blocks", -2),
+                       ("emit_blocks", 513), ("hot_max_chunks", 4097), ("bytemap_max_mb", -2)]:
+        tune = gg.make_tuning(**{field: bad})
+        with pytest.raises(gg.GGError):                                  # tuning out of range
+            gg.gg_gather_batch(t, t.data_ptr(), 1, 10, part, feat, t, 256, 10, t, t, 256,
+                               t.data_ptr(), t, t, stream=0, tuning=tune)
+        assert field in gg.gg_last_error()
+        with pytest.raises(gg.GGError):
+            gg.gg_stage_inplace(t, t, 10, part, feat, t, 256, 10, t, None, None, None, None, u,
+                                t, t, big, stream=0, tuning=tune)
+        assert field in gg.gg_last_error()
     c = gg.make_sim_coeffs(4, 1.0, 0.01, 1e-3, 1e-5, 0.0, 256, 30.0)    # no bandwidth ceiling
     with pytest.raises(gg.GGError):
         gg.gg_sim_accumulate(t, t.data_ptr(), 4, part, c, t, stream=0)

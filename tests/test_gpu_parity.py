@@ -65,26 +65,26 @@ def test_small_window_sizes(W):
 
 
 @pytest.mark.parametrize("n_hot", [-1, 0, 1, 2000])
-def test_hot_set_in_multi_pass_chunks(n_hot, monkeypatch):
+def test_hot_set_in_multi_pass_chunks(n_hot):
     """The hot set's chunks span several 256-word passes once a graph has
-    more than 1024 of them (the 111M-node graph); GG_HOT_MAX_CHUNKS=2
-    forces that layout on the small graph, with and without a budget."""
+    more than 4096 of them; tuning hot_max_chunks = 2 forces that layout on
+    the small graph, with and without a budget."""
     log(f"small: hot set in two chunks of several passes, n_hot={n_hot}")
-    monkeypatch.setenv("GG_HOT_MAX_CHUNKS", "2")
-    w = world(synth.instance("small"), n_hot=n_hot)
+    from paper_2606_02916_amd import gg
+    w = world(synth.instance("small"), n_hot=n_hot, tuning=gg.make_tuning(hot_max_chunks=2))
     w.run_and_compare(0)
     w.run_and_compare(1)
 
 
 @pytest.mark.parametrize("tile", [1, 4, 16])
 @pytest.mark.parametrize("n_hot", [-1, 300])
-def test_fewer_rows_per_wave_step(tile, n_hot, monkeypatch):
-    """GG_TILE_ROWS shrinks the rows a wavefront copies per step in the
+def test_fewer_rows_per_wave_step(tile, n_hot):
+    """Tuning tile_rows shrinks the rows a wavefront copies per step in the
     stage and the gather (1 = one row per wavefront step), the variants the
     benchmark's ablation times: same bytes, with and without misses."""
     log(f"small: {tile} rows per wave step, n_hot={n_hot}")
-    monkeypatch.setenv("GG_TILE_ROWS", str(tile))
-    w = world(synth.instance("small"), n_hot=n_hot)
+    from paper_2606_02916_amd import gg
+    w = world(synth.instance("small"), n_hot=n_hot, tuning=gg.make_tuning(tile_rows=tile))
     w.run_and_compare(0)
     w.run_and_compare(1)
 
@@ -192,19 +192,41 @@ def test_row_widths_with_one_chunk_or_one_tail_word(rows):
 
 @pytest.mark.parametrize("tile", [None, 64])
 @pytest.mark.parametrize("n_hot", [0, 700, -1])
-def test_wide_rows_with_misses(n_hot, tile, monkeypatch):
+def test_wide_rows_with_misses(n_hot, tile):
     """2,408-byte rows at a 2,416-byte stride (by default eight rows per
-    staging step and two per gather step; GG_TILE_ROWS=64 makes both 64)
-    through both gathers and the miss path: with n_hot = 0 every remote row
-    is a miss, with 700 some are."""
+    staging step and two per gather step; tuning tile_rows = 64 makes both
+    64) through both gathers and the miss path: with n_hot = 0 every remote
+    row is a miss, with 700 some are."""
     log(f"tiny: 2408-byte rows, tile {tile or 'default'}, n_hot={n_hot}, consecutive windows")
-    if tile:
-        monkeypatch.setenv("GG_TILE_ROWS", str(tile))
+    from paper_2606_02916_amd import gg
     inst = synth.instance("tiny")
     rng = np.random.default_rng(8)
     shards = [rng.integers(0, 256, size=(s.shape[0], 2416), dtype=np.uint8) for s in inst.shards]
-    w = world(inst, shards=shards, row_bytes=2408, stride=2416, n_hot=n_hot, W=2)
+    w = world(inst, shards=shards, row_bytes=2408, stride=2416, n_hot=n_hot, W=2,
+              tuning=gg.make_tuning(tile_rows=tile) if tile else None)
     for k in range(2):
+        w.run_and_compare(k)
+
+
+@pytest.mark.parametrize("fields", [
+    dict(bytemap_max_mb=-1), dict(bytemap_max_mb=1),
+    dict(gather_loads=2, gather_blocks=8), dict(gather_loads=4), dict(gather_loads=8, tile_rows=3),
+    dict(stage_blocks=1, tile_rows=7), dict(stage_blocks=3, emit_blocks=1, hot_max_chunks=1)])
+def test_launch_tuning_leaves_results_unchanged(fields):
+    """Launch tuning changes only how the work is spread: the sampler's last
+    hop with atomic marks instead of the byte map (as on the 111M-node
+    graph), gathers with 2, 4 or 8 loads in flight and few blocks (many
+    tiles per wave), staging by one or three blocks, one hot-set chunk and
+    one free-list block.  Full restage, then in-place staging over three
+    windows, each against the oracle with a budget that leaves misses."""
+    log(f"small: tuning {fields}")
+    from paper_2606_02916_amd import gg
+    tune = gg.make_tuning(**fields)
+    inst = synth.instance("small")
+    w = world(inst, n_hot=3000, tuning=tune)
+    w.run_and_compare(0)
+    w = world(inst, n_hot=3000, inplace=True, tuning=tune)
+    for k in range(3):
         w.run_and_compare(k)
 
 
@@ -518,14 +540,15 @@ def test_inplace_staging_matches_oracle(name, n_hot, W, rows):
 
 
 @pytest.mark.parametrize("emit_blocks", [1, 2])
-def test_inplace_free_list_blocks_take_several_chunks(emit_blocks, monkeypatch):
+def test_inplace_free_list_blocks_take_several_chunks(emit_blocks):
     """The free list of the persistent cache is emitted by at most a fixed
     number of blocks that stride over the 8,192-slot chunks below the
-    previous extent; GG_EMIT_BLOCKS=1 or 2 makes every block take several
-    chunks on the small graph, whose extent passes two chunks."""
+    previous extent; tuning emit_blocks = 1 or 2 makes every block take
+    several chunks on the small graph, whose extent passes two chunks."""
     log(f"small: in-place staging, free list emitted by {emit_blocks} block(s)")
-    monkeypatch.setenv("GG_EMIT_BLOCKS", str(emit_blocks))
-    w = world(synth.instance("small"), inplace=True)
+    from paper_2606_02916_amd import gg
+    w = world(synth.instance("small"), inplace=True,
+              tuning=gg.make_tuning(emit_blocks=emit_blocks))
     nwin = synth.n_windows(w.inst.batch_off, w.W)
     ext = []
     for k in range(min(nwin, 5)):
