@@ -349,6 +349,27 @@ int gg_gather_batch(const int32_t* in_ids_d, const int64_t* bounds_d, int32_t ns
                     gg_gather_stats_t* stats_d, const gg_tuning_t* tuning, int32_t* status_d,
                     void* ws, size_t ws_bytes, hipStream_t stream);
 
+/* gg_gather_batch for callers that cannot allocate: code under HIP graph
+ * capture, tight serving loops, harnesses that forbid allocation.  The
+ * same arguments and results, without the workspace: the call's scratch
+ * (the per-block statistics, 4 * (2 + P) bytes per gather block) lives in
+ * a device array of GG_GATHER_SCRATCH_BYTES that the library holds on each
+ * GPU it runs on until the process ends.  A call whose scratch would not
+ * fit returns GG_ERR_CAPACITY and enqueues nothing; with the default 1024
+ * gather blocks every call fits (at most 270 KB, at 64 segments and 64
+ * owners).  The call never allocates; the first call on a device looks up
+ * the array's address there.  Nothing in the array needs clearing (every
+ * call writes the statistics it reads), but all calls on one GPU share it:
+ * calls that overlap on one GPU (different streams or host threads) race,
+ * so order them, e.g. on one stream. */
+#define GG_GATHER_SCRATCH_BYTES (1 << 20)
+int gg_gather_batch_noalloc(const int32_t* in_ids_d, const int64_t* bounds_d, int32_t nseg,
+                            int64_t n_cap, const gg_part_t* part, const gg_feat_t* feat,
+                            const void* cache_d, int64_t cache_stride, int64_t cache_rows,
+                            const int32_t* slot_of_d, void* out_d, int64_t out_stride,
+                            int32_t flags, gg_gather_stats_t* stats_d,
+                            const gg_tuning_t* tuning, int32_t* status_d, hipStream_t stream);
+
 /* ---------------------------------------------------------------------------
  * Window-size simulator counts.  The paper scores a candidate window size W
  * by replaying one epoch's trace: per window k it counts the rebuild delta

@@ -15,7 +15,12 @@
 #include <stdlib.h>
 #include <string.h>
 
+#include <mutex>
+
 #include "gg_host.hpp"
+
+// Scratch of gg_gather_batch_noalloc (see device_scratch below).
+static __device__ __align__(256) int32_t scratch[GG_GATHER_SCRATCH_BYTES / sizeof(int32_t)];
 
 namespace gg {
 namespace {
@@ -294,13 +299,56 @@ extern "C" size_t gg_ws_gather(int64_t n_cap, int32_t nseg, int32_t num_parts,
   return gather_ws_layout(n_cap, nseg, num_parts, tune, nullptr, nullptr);
 }
 
-extern "C" int gg_gather_batch(const int32_t* in_ids_d, const int64_t* bounds_d, int32_t nseg,
-                               int64_t n_cap, const gg_part_t* part, const gg_feat_t* feat,
-                               const void* cache_d, int64_t cache_stride, int64_t cache_rows,
-                               const int32_t* slot_of_d, void* out_d, int64_t out_stride,
-                               int32_t flags, gg_gather_stats_t* stats_d,
-                               const gg_tuning_t* tuning, int32_t* status_d, void* ws,
-                               size_t ws_bytes, hipStream_t stream) {
+namespace gg {
+namespace {
+
+// The per-block statistics of gg_gather_batch_noalloc: a file-scope device
+// array, one copy per GPU, held until the process ends.  Host code never
+// hands the array's name to a kernel (in host code it is a stand-in, not a
+// device address): it takes the array's address on each device from
+// hipGetSymbolAddress, once, with that device current.
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[kMaxDevices] = {};
+
+int device_scratch(hipStream_t stream, void** out) {
+  int dev = 0;
+  hipError_t e = stream ? hipStreamGetDevice(stream, &dev) : hipGetDevice(&dev);
+  if (e != hipSuccess) {
+    set_error("gg_gather_batch_noalloc: no device for the stream: %s", hipGetErrorString(e));
+    return GG_ERR_HIP;
+  }
+  if (dev < 0 || dev >= kMaxDevices) {
+    set_error("gg_gather_batch_noalloc: device %d beyond the %d supported", dev, kMaxDevices);
+    return GG_ERR_UNSUPPORTED;
+  }
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch_ptr[dev]) {
+    int cur = 0;
+    e = hipGetDevice(&cur);
+    if (e == hipSuccess && cur != dev) e = hipSetDevice(dev);
+    void* p = nullptr;
+    if (e == hipSuccess) e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (cur != dev) (void)hipSetDevice(cur);
+    if (e != hipSuccess || !p) {
+      set_error("gg_gather_batch_noalloc: address of the scratch array on device %d: %s", dev,
+                hipGetErrorString(e));
+      return GG_ERR_HIP;
+    }
+    g_scratch_ptr[dev] = p;
+  }
+  *out = g_scratch_ptr[dev];
+  return GG_OK;
+}
+
+// Both gather entry points: ws/ws_bytes is the caller's workspace, or with
+// noalloc the device array (ws is then ignored).
+int gather_impl(const int32_t* in_ids_d, const int64_t* bounds_d, int32_t nseg, int64_t n_cap,
+                const gg_part_t* part, const gg_feat_t* feat, const void* cache_d,
+                int64_t cache_stride, int64_t cache_rows, const int32_t* slot_of_d, void* out_d,
+                int64_t out_stride, int32_t flags, gg_gather_stats_t* stats_d,
+                const gg_tuning_t* tuning, int32_t* status_d, void* ws, size_t ws_bytes,
+                bool noalloc, hipStream_t stream) {
   GG_REQUIRE(bounds_d && slot_of_d && stats_d && status_d, "NULL argument");
   Tune tune;
   if (resolve_tuning(tuning, &tune) != GG_OK) return GG_ERR_ARG;
@@ -321,9 +369,21 @@ extern "C" int gg_gather_batch(const int32_t* in_ids_d, const int64_t* bounds_d,
              "cache_stride %lld invalid", (long long)cache_stride);
   GG_REQUIRE(((uintptr_t)out_d & 3u) == 0 && ((uintptr_t)cache_d & 3u) == 0,
              "output and cache must be 4-byte aligned");
-  GatherWs gw;
-  const size_t need_ws = gather_ws_layout(n_cap, nseg, kp.P, tune, (char*)ws, &gw);
+  const size_t need_ws = gather_ws_layout(n_cap, nseg, kp.P, tune, nullptr, nullptr);
+  if (noalloc) {
+    if (need_ws > (size_t)GG_GATHER_SCRATCH_BYTES) {
+      set_error("gg_gather_batch_noalloc: %d segments of %d blocks with %d owners need %zu bytes "
+                "of scratch; the library's array holds %d",
+                nseg, blocks_per_seg(n_cap, nseg, tune), kp.P, need_ws, GG_GATHER_SCRATCH_BYTES);
+      return GG_ERR_CAPACITY;
+    }
+    rc = device_scratch(stream, &ws);
+    if (rc != GG_OK) return rc;
+    ws_bytes = GG_GATHER_SCRATCH_BYTES;
+  }
   GG_REQUIRE(ws && ws_bytes >= need_ws, "workspace of %zu bytes < %zu", ws_bytes, need_ws);
+  GatherWs gw;
+  gather_ws_layout(n_cap, nseg, kp.P, tune, (char*)ws, &gw);
   bool v16 = aligned16(out_d) && out_stride % 16 == 0 &&
              (cache_rows == 0 || (aligned16(cache_d) && cache_stride % 16 == 0));
   for (int m = 0; m < kf.P; ++m)
@@ -365,4 +425,32 @@ extern "C" int gg_gather_batch(const int32_t* in_ids_d, const int64_t* bounds_d,
                            out, gw, stats_d, status_d);
   GG_LAUNCH_CHECK("k_gather_rows/k_gather_finish");
   return GG_OK;
+}
+
+}  // namespace
+}  // namespace gg
+
+extern "C" int gg_gather_batch(const int32_t* in_ids_d, const int64_t* bounds_d, int32_t nseg,
+                               int64_t n_cap, const gg_part_t* part, const gg_feat_t* feat,
+                               const void* cache_d, int64_t cache_stride, int64_t cache_rows,
+                               const int32_t* slot_of_d, void* out_d, int64_t out_stride,
+                               int32_t flags, gg_gather_stats_t* stats_d,
+                               const gg_tuning_t* tuning, int32_t* status_d, void* ws,
+                               size_t ws_bytes, hipStream_t stream) {
+  return gather_impl(in_ids_d, bounds_d, nseg, n_cap, part, feat, cache_d, cache_stride,
+                     cache_rows, slot_of_d, out_d, out_stride, flags, stats_d, tuning, status_d,
+                     ws, ws_bytes, false, stream);
+}
+
+extern "C" int gg_gather_batch_noalloc(const int32_t* in_ids_d, const int64_t* bounds_d,
+                                       int32_t nseg, int64_t n_cap, const gg_part_t* part,
+                                       const gg_feat_t* feat, const void* cache_d,
+                                       int64_t cache_stride, int64_t cache_rows,
+                                       const int32_t* slot_of_d, void* out_d, int64_t out_stride,
+                                       int32_t flags, gg_gather_stats_t* stats_d,
+                                       const gg_tuning_t* tuning, int32_t* status_d,
+                                       hipStream_t stream) {
+  return gather_impl(in_ids_d, bounds_d, nseg, n_cap, part, feat, cache_d, cache_stride,
+                     cache_rows, slot_of_d, out_d, out_stride, flags, stats_d, tuning, status_d,
+                     nullptr, 0, true, stream);
 }

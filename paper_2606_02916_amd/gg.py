@@ -133,6 +133,8 @@ SIGNATURES = {
                                    _P, _P, _P, _P, _P, _SZ, _P]),
     "gg_gather_batch": (C.c_int, [_P, _P, _I32, _I64, _P, _P, _P, _I64, _I64, _P, _P, _I64, _I32,
                                   _P, _P, _P, _P, _SZ, _P]),
+    "gg_gather_batch_noalloc": (C.c_int, [_P, _P, _I32, _I64, _P, _P, _P, _I64, _I64, _P, _P,
+                                          _I64, _I32, _P, _P, _P, _P]),
     "gg_sim_accumulate": (C.c_int, [_P, _P, _I32, _P, _P, _P, _P]),
     "gg_ws_sage": (_SZ, [_I64, _I32, _I64, _I32, _P]),
     "gg_sage_forward": (C.c_int, [_P, _I64, _I32, _I32, _P, _P, _I32, _I64, _I64, _P, _P, _I64, _P,
@@ -346,6 +348,23 @@ def gg_gather_batch(in_ids, bounds_ptr, nseg, n_cap, part, feat, cache, cache_st
                                      _ptr(slot_of), _ptr(out), out_stride, flags, stats_ptr,
                                      _tune(tuning), _ptr(status), _ptr(ws), ws.numel(),
                                      _stream(stream)), "gg_gather_batch")
+
+
+GATHER_SCRATCH_BYTES = 1 << 20
+
+
+def gg_gather_batch_noalloc(in_ids, bounds_ptr, nseg, n_cap, part, feat, cache, cache_stride,
+                            cache_rows, slot_of, out, out_stride, stats_ptr, status, stream=None,
+                            flags=0, tuning=None):
+    """gg_gather_batch without a workspace: the library's per-GPU scratch
+    array holds the call's block statistics (calls overlapping on one GPU
+    race)."""
+    return check(lib.gg_gather_batch_noalloc(_ptr(in_ids), bounds_ptr, nseg, n_cap,
+                                             C.byref(part), C.byref(feat), _ptr(cache),
+                                             cache_stride, cache_rows, _ptr(slot_of), _ptr(out),
+                                             out_stride, flags, stats_ptr, _tune(tuning),
+                                             _ptr(status), _stream(stream)),
+                 "gg_gather_batch_noalloc")
 
 
 def make_sim_coeffs(P, eps_init, eps_row, lam_init, lam_row, bw_bytes_per_s, row_bytes, p_idle):

@@ -208,6 +208,15 @@ def test_bad_arguments_are_rejected_on_the_host(gg):
             gg.gg_stage_inplace(t, t, 10, part, feat, t, 256, 10, t, None, None, None, None, u,
                                 t, t, big, stream=0, tuning=tune)
         assert field in gg.gg_last_error()
+    # the no-allocation gather rejects a call whose scratch exceeds its array,
+    # before any device work
+    part64 = gg.make_part(64, gg.PART_MOD, 0, 100)
+    feat64 = gg.make_feat(256, [t] * 64, [256] * 64, [2] * 64)
+    with pytest.raises(gg.GGError) as e:
+        gg.gg_gather_batch_noalloc(t, t.data_ptr(), 64, 10**9, part64, feat64, t, 256, 10, t, t,
+                                   256, t.data_ptr(), t, stream=0,
+                                   tuning=gg.make_tuning(gather_blocks=65536))
+    assert "capacity" in str(e.value) and "scratch" in gg.gg_last_error()
     c = gg.make_sim_coeffs(4, 1.0, 0.01, 1e-3, 1e-5, 0.0, 256, 30.0)    # no bandwidth ceiling
     with pytest.raises(gg.GGError):
         gg.gg_sim_accumulate(t, t.data_ptr(), 4, part, c, t, stream=0)
