@@ -189,6 +189,9 @@ def main():
                     help="tiny | dense_mid | large_sparse | wsweep | small")
     ap.add_argument("--W", type=int, default=None, help="window size (default: the workload's)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--line-wsweep", default="1,2,4,8,16,32",
+                    help="window sizes of the W sweep added to the default line (batch 4096 "
+                         "on the large sparse graph, look-ahead driver); empty to skip")
     ap.add_argument("--cpu-seconds", type=float, default=10.0,
                     help="minimum oracle time for the CPU baseline sample")
     ap.add_argument("--per-batch", action="store_true",
@@ -345,6 +348,7 @@ def main():
     rows_w, gbytes_w, hot_w, sbytes_w, req_w, hbytes_w, lev_w = [], [], [], [], [], [], []
     pb = args.per_batch
     iso_ms = []      # gather launches with the chip to themselves
+    iso_st_ms = []   # staging calls with the chip to themselves
     flush = torch.empty(512 << 20, dtype=torch.uint8, device=dev) if look else None
     for k, (s, so, b0) in enumerate(wins):
         ge = [(mk(), mk()) for _ in range(W if pb else 1)]
@@ -361,6 +365,14 @@ def main():
             pipe.regather(sb, Wk)
             ge[0][1].record()
             torch.cuda.synchronize()
+            # and its staging call, the same way (it rewrites the same slots)
+            se = (mk(), mk())
+            flush.fill_((k + 1) & 0xFF)
+            se[0].record()
+            pipe.restage()
+            se[1].record()
+            torch.cuda.synchronize()
+            iso_st_ms.append(se[0].elapsed_time(se[1]))
         iso_ms += [a.elapsed_time(b) for a, b in ge[:Wk if pb else 1]]
         st = pipe.read_status()
         if st != 0:
@@ -472,6 +484,20 @@ def main():
     iso_avg_ms = float(np.mean(iso_ms))
     iso_achieved = float(np.mean(all_gb)) / (iso_avg_ms * 1e-3) / 1e9
     stage_gbs = st_bytes / (st_ms * 1e-3) / 1e9
+    iso_stage = None
+    if iso_st_ms:
+        # window 0 stages every row (no previous cache); the steady state is
+        # the windows after it
+        steady = list(range(1, nwin)) if nwin > 1 else [0]
+        ib = float(np.mean([sbytes_w[k] for k in steady]))
+        it = float(np.mean([iso_st_ms[k] for k in steady]))
+        iso_stage = {"achieved": round(ib / (it * 1e-3) / 1e9, 1),
+                     "frac": round(ib / (it * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
+                     "avg_call_us": round(it * 1e3, 2), "bytes_per_call": int(ib),
+                     "calls": len(steady),
+                     "note": "the look-ahead driver's staging call (all its kernels) launched "
+                             "again on one stream after each pre-pass window, behind a 512 MiB "
+                             "fill; windows after the first"}
 
     if args.copy_calibration_mib:
         nb = args.copy_calibration_mib << 20
@@ -506,7 +532,7 @@ def main():
                    "fanout": list(wl.fanout), "batch": wl.batch_size, "W": W,
                    "partitions": P, "local_owner": wl.local_owner, "windows_per_epoch": nwin,
                    "gather_launch": "per batch" if pb else "per window",
-                   "tuning": args.tune or "defaults",
+                   "tuning": args.tune or "the driver's defaults",
                    "driver": args.pipeline + (f" ({pipe.nsets} buffer sets, staging on the "
                                               f"{'build' if stage_on_build else 'fetch'} stream)"
                                               if look else "")},
@@ -535,7 +561,10 @@ def main():
                                "use together"},
         "stage_roofline": ({"kernel": stage_call, "bound": "hbm",
                             "achieved": round(stage_gbs, 1),
-                            "frac": round(stage_gbs / HBM_PEAK_GBS, 4), "unit": "GB/s"}
+                            "frac": round(stage_gbs / HBM_PEAK_GBS, 4), "unit": "GB/s",
+                            "bytes_per_call": int(np.mean(sbytes_w)),
+                            "overlapped": look,
+                            "isolated": iso_stage}
                            if pcie is None else
                            {"kernel": stage_call, "bound": "pcie",
                             "achieved": round(st_host_bytes / (st_ms * 1e-3) / 1e9, 2),
@@ -557,7 +586,21 @@ def main():
         "gather_rows_per_s": round(rows / (g_ms * 1e-3) if g_ms else 0.0, 1),
         "consumer": consumer_report(cons_dims, lev_w, order, cevs, wl) if cons else None,
         "cpu_baseline": cpu,
+        "wsweep": None,
     }
+    if args.line_wsweep and args.config == "large_sparse" and not args.consumer:
+        del pipe
+        torch.cuda.empty_cache()
+        Ws = [int(x) for x in args.line_wsweep.split(",")]
+        t_sw = time.perf_counter()
+        sweep = {"workload": "wsweep", "batch": synth.WORKLOADS["wsweep"].batch_size,
+                 "driver": "lookahead", "per_W": wsweep_lookahead(dev, "wsweep", Ws, tuning),
+                 "note": "one untimed epoch per W, then at least 8 timed windows cycling the "
+                         "epoch; gather rate from HIP events as in roofline; counts from the "
+                         "untimed epoch (bulk bytes per owner: the rows each owner's one request "
+                         "moves, i.e. the rebuild delta)"}
+        sweep["wall_s"] = round(time.perf_counter() - t_sw, 1)
+        line["wsweep"] = sweep
     print(json.dumps(line), flush=True)
 
 
@@ -1021,6 +1064,96 @@ def wsweep(args, wl):
     print(json.dumps(line), flush=True)
 
 
+def wsweep_lookahead(dev, name, Ws, tuning=None, reps=2):
+    """The W sweep as the default bench reports it: for each W, one epoch of
+    the workload `name` through the look-ahead driver (the benchmarked
+    configuration), after one untimed epoch, cycled `reps` times (at least
+    8 windows).  Per W: rows gathered/s over the timed windows, the
+    gather's rate from HIP events (the same method as the main line: a
+    gather ends at its end event and started at the later of its window's
+    staging end and the previous gather's end), and the epoch's counts from
+    the untimed pass: hot-set rows, bulk bytes per owner and rebuild-delta
+    rows per window, bulk requests per epoch and the reuse factor."""
+    import numpy as np
+    import torch
+
+    import synth
+    from paper_2606_02916_amd import LookaheadPipeline
+    wl = synth.WORKLOADS[name]
+    inst, row_ptr_d, col_idx_d, shards_d = synth.torch_instance(name, dev)
+    P, rb = wl.num_parts, wl.row_bytes
+    seeds_d = torch.from_numpy(inst.seeds).to(dev)
+    boff = inst.batch_off
+    mk = lambda: torch.cuda.Event(enable_timing=True)  # noqa: E731
+    out = []
+    for W in Ws:
+        t_w = time.perf_counter()
+        look = LookaheadPipeline(row_ptr_d, col_idx_d, P, wl.part_kind, wl.local_owner,
+                                 inst.range_start, shards_d, [s.shape[0] for s in inst.shards],
+                                 rb, wl.row_stride, W, wl.fanout, wl.batch_size, device=dev,
+                                 tuning=tuning)
+        nwin = synth.n_windows(boff, W)
+        wins = []
+        for k in range(nwin):
+            b0, b1 = synth.window_batches(boff, W, k)
+            wins.append((seeds_d[boff[b0]:boff[b1]], boff[b0:b1 + 1] - boff[b0], b0))
+        hot, delta, owner_bytes, requests, rows, remote, gbytes = [], [], [], [], [], [], []
+        for s_, so, b0 in wins:          # untimed epoch: counts
+            Wk, bufs = look.window(s_, so, b0)
+            look.synchronize()
+            st = bufs.stage_stats_dict()
+            g = [bufs.gather_stats_dict(b) for b in range(Wk)]
+            hot.append(st["rows_total"])
+            delta.append(sum(st["delta_rows"]))
+            owner_bytes.append(st["bytes"])
+            requests.append(st["requests_total"])
+            rows.append(sum(x["rows"] for x in g))
+            remote.append(sum(x["hits"] + x["misses"] for x in g))
+            gbytes.append(sum(x["rows"] * (2 * rb + 4) + (x["hits"] + x["misses"]) * 4
+                              for x in g))
+        if look.read_status() != 0:
+            raise RuntimeError(f"device status {look.read_status()} at W={W}")
+        K = max(reps * nwin, 8)
+        order = [i % nwin for i in range(K)]
+        sev = [mk() for _ in range(K)]
+        gev = [mk() for _ in range(K)]
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        for i, k in enumerate(order):
+            s_, so, b0 = wins[k]
+            look.window(s_, so, b0, events=[None, None, None, None, sev[i]],
+                        gather_events=(None, gev[i]))
+        look.synchronize()
+        el = time.perf_counter() - t0
+        if look.read_status() != 0:
+            raise RuntimeError(f"device status {look.read_status()} at W={W}")
+        g_ms = 0.0
+        for i in range(K):
+            t = sev[i].elapsed_time(gev[i])
+            if i > 0:
+                t = min(t, gev[i - 1].elapsed_time(gev[i]))
+            g_ms += t
+        g_bytes = sum(gbytes[k] for k in order)
+        g_gbs = g_bytes / (g_ms * 1e-3) / 1e9
+        r = {"W": W, "windows_per_epoch": nwin,
+             "rows_per_s": round(sum(rows[k] for k in order) / el, 1),
+             "ms_per_window": round(el / K * 1e3, 4),
+             "gather_GBps": round(g_gbs, 1), "gather_frac": round(g_gbs / HBM_PEAK_GBS, 4),
+             "hot_set_rows_per_window": round(float(np.mean(hot)), 1),
+             "bulk_bytes_per_owner_per_window": [round(float(x), 1)
+                                                 for x in np.mean(owner_bytes, axis=0)],
+             "delta_rows_per_window": round(float(np.mean(delta)), 1),
+             "bulk_requests_per_epoch": int(sum(requests)),
+             "reuse_factor": round(sum(remote) / max(1, sum(hot)), 3),
+             "wall_s": None}
+        del look
+        torch.cuda.empty_cache()
+        r["wall_s"] = round(time.perf_counter() - t_w, 2)
+        log(f"wsweep W={W}: " + json.dumps(r))
+        out.append(r)
+    return out
+
+
 def sim_coefficients(wl):
     """Synthetic coefficients of the analytical energy model, the same for
     every owner: a 500 us request initiation at 50 W, rows at 1.25 GB/s
@@ -1111,7 +1244,9 @@ def simulate(args, wl):
 def cpu_baseline(inst, wl, W, so, b0, min_seconds):
     """The CPU oracle, untuned and single-threaded, on window 0 of the same
     workload; repeated until at least min_seconds of work when one window is
-    shorter than that."""
+    shorter than that.  The calling thread (the oracle runs no threads of its
+    own) is pinned to one core for the duration, and each step of the path
+    is timed on its own."""
     import numpy as np
 
     from oracle import ggref
@@ -1122,36 +1257,53 @@ def cpu_baseline(inst, wl, W, so, b0, min_seconds):
     seeds = inst.seeds[boff[b0]:boff[b0 + len(so) - 1]]
     slot_of = np.full(wl.num_nodes, -1, dtype=np.int32)
     cache = None
-    reps, rows, t_total = 0, 0, 0.0
-    while True:
-        t = time.perf_counter()
-        fids, foff, nids, noff = ggref.sample_window(inst.row_ptr, inst.col_idx, seeds, so,
-                                                     wl.fanout, 0, 0, b0)
-        Wk = len(so) - 1
-        L = len(wl.fanout)
-        hot, freq = ggref.build_hotset(fids, foff, Wk, L, part, -1)
-        bucket, owner_off = ggref.bucket_by_owner(hot, part)
-        if cache is None or cache.shape[0] < len(hot):
-            t_alloc = time.perf_counter()
-            cache = np.zeros((len(hot), wl.row_stride), dtype=np.uint8)
-            t += time.perf_counter() - t_alloc
-        slot_of.fill(-1)
-        ggref.stage_bulk(bucket, owner_off, part, feat, cache, wl.row_stride, slot_of, None)
-        for b in range(Wk):
-            s = L * Wk + b
-            ids = fids[foff[s]:foff[s + 1]]
-            out = np.empty((len(ids), wl.row_stride), dtype=np.uint8)
-            ggref.gather_batch(ids, part, feat, cache, wl.row_stride, slot_of, out, wl.row_stride)
-            rows += len(ids)
-        t_total += time.perf_counter() - t
-        reps += 1
-        if t_total >= min_seconds or reps >= 1000:
-            break
-    log(f"cpu oracle: {reps} window(s), {rows} rows in {t_total:.1f}s")
-    return {"value": round(rows / t_total, 1), "unit": "rows/s", "cores": 1, "kind": "oracle",
+    reps, rows = 0, 0
+    steps = {"sample": 0.0, "hotset": 0.0, "bucket": 0.0, "stage": 0.0, "gather": 0.0}
+    affinity = os.sched_getaffinity(0)
+    core = max(affinity)
+    os.sched_setaffinity(0, {core})
+    try:
+        while True:
+            Wk, L = len(so) - 1, len(wl.fanout)
+            t0 = time.perf_counter()
+            fids, foff, nids, noff = ggref.sample_window(inst.row_ptr, inst.col_idx, seeds, so,
+                                                         wl.fanout, 0, 0, b0)
+            t1 = time.perf_counter()
+            hot, freq = ggref.build_hotset(fids, foff, Wk, L, part, -1)
+            t2 = time.perf_counter()
+            bucket, owner_off = ggref.bucket_by_owner(hot, part)
+            t3 = time.perf_counter()
+            steps["sample"] += t1 - t0
+            steps["hotset"] += t2 - t1
+            steps["bucket"] += t3 - t2
+            if cache is None or cache.shape[0] < len(hot):              # not timed
+                cache = np.zeros((len(hot), wl.row_stride), dtype=np.uint8)
+            slot_of.fill(-1)
+            t0 = time.perf_counter()
+            ggref.stage_bulk(bucket, owner_off, part, feat, cache, wl.row_stride, slot_of, None)
+            steps["stage"] += time.perf_counter() - t0
+            for b in range(Wk):
+                s = L * Wk + b
+                ids = fids[foff[s]:foff[s + 1]]
+                out = np.empty((len(ids), wl.row_stride), dtype=np.uint8)  # not timed
+                t0 = time.perf_counter()
+                ggref.gather_batch(ids, part, feat, cache, wl.row_stride, slot_of, out,
+                                   wl.row_stride)
+                steps["gather"] += time.perf_counter() - t0
+                rows += len(ids)
+            reps += 1
+            if sum(steps.values()) >= min_seconds or reps >= 1000:
+                break
+    finally:
+        os.sched_setaffinity(0, affinity)
+    total = sum(steps.values())
+    log(f"cpu oracle: {reps} window(s), {rows} rows in {total:.1f}s on core {core}")
+    return {"value": round(rows / total, 1), "unit": "rows/s", "cores": 1, "kind": "oracle",
             "sample": f"{reps} x window 0 of {wl.name} (W={len(so) - 1}, {rows // reps} rows per "
-                      f"window), single-threaded C++ oracle, excluding input generation",
-            "host_cpu": cpu_model(), "host_nproc": os.cpu_count()}
+                      f"window), single-threaded C++ oracle pinned to one core, excluding input "
+                      f"generation and buffer allocation",
+            "seconds_per_window": {k: round(v / reps, 4) for k, v in steps.items()},
+            "host_cpu": cpu_model(), "host_nproc": os.cpu_count(), "pinned_core": core}
 
 
 if __name__ == "__main__":

@@ -180,7 +180,20 @@ typedef struct gg_tuning {
                                 4096; fewer make every chunk span several passes) */
   int32_t bytemap_max_mb;    /* largest byte map (MB) into which the sampler's last hop marks
                                 its draws, 1..65536, or -1 for none (default 512) */
+  int32_t sample_order;      /* GG_SAMPLE_BATCH_ORDER (default): one lane per frontier entry,
+                                batch by batch.  GG_SAMPLE_TILES_LAST: the last hop in node
+                                tiles (a wavefront samples one tile of consecutive node ids in
+                                every batch of the window, so the batches share the CSR lines
+                                they fetch: less HBM traffic, which pays when other kernels
+                                share the memory system).  GG_SAMPLE_TILES_ALL: every hop in
+                                node tiles.  The workspace holds the tiles' table unless
+                                batch order. */
+  int32_t sample_tile_runs;  /* node tiles of this many runs of 256 ids, a power of two up to
+                                64; 0: sized per hop from its entry count */
 } gg_tuning_t;
+#define GG_SAMPLE_BATCH_ORDER 0
+#define GG_SAMPLE_TILES_LAST 1
+#define GG_SAMPLE_TILES_ALL 2
 
 /* Words per batch of frontier_bits (a multiple of 2048). */
 int64_t gg_bits_words(int64_t num_nodes);

@@ -86,6 +86,11 @@ int resolve_tuning(const gg_tuning_t* t, Tune* out) {
              "tuning: hot_max_chunks %d outside 1..%d", t->hot_max_chunks, kHotMaxChunks);
   GG_REQUIRE(t->bytemap_max_mb >= -1 && t->bytemap_max_mb <= 65536,
              "tuning: bytemap_max_mb %d outside 1..65536 (or -1)", t->bytemap_max_mb);
+  GG_REQUIRE(t->sample_order >= GG_SAMPLE_BATCH_ORDER && t->sample_order <= GG_SAMPLE_TILES_ALL,
+             "tuning: sample_order %d unknown", t->sample_order);
+  GG_REQUIRE(t->sample_tile_runs >= 0 && t->sample_tile_runs <= 64 &&
+                 (t->sample_tile_runs & (t->sample_tile_runs - 1)) == 0,
+             "tuning: sample_tile_runs %d is not a power of two up to 64", t->sample_tile_runs);
   out->tile_rows = t->tile_rows;
   out->gather_blocks = t->gather_blocks ? t->gather_blocks : kGatherBlocksDefault;
   out->gather_loads = t->gather_loads;
@@ -98,6 +103,8 @@ int resolve_tuning(const gg_tuning_t* t, Tune* out) {
   out->bytemap_max_bytes = t->bytemap_max_mb == 0 ? kByteMapMaxBytes
                            : t->bytemap_max_mb < 0 ? -1
                                                    : (int64_t)t->bytemap_max_mb << 20;
+  out->sample_order = t->sample_order;
+  out->sample_tile_runs = t->sample_tile_runs;
   return GG_OK;
 }
 

@@ -81,6 +81,8 @@ struct Tune {
   int32_t emit_blocks;
   int32_t hot_max_chunks;
   int64_t bytemap_max_bytes;  // -1: no byte map
+  int32_t sample_order;       // GG_SAMPLE_*
+  int32_t sample_tile_runs;   // 0: per hop
 };
 
 // Resolves `t` (NULL: every default) into *out; GG_ERR_ARG (with a message)

@@ -25,6 +25,13 @@ struct LevelArgs {
   int32_t nch;
   int32_t cnt_only;   // offsets from the chunk counts alone (no group totals)
   int64_t fcap, ncap;
+  // Node-tile table of the level for the next hop's sampler (tile_runs = 0:
+  // none): tstart[b * ntiles + t] = list position of batch b's first entry
+  // in tile t, a tile being tile_runs runs of 256 nodes.
+  int64_t* tstart;
+  int64_t ntiles;
+  int32_t tile_runs;
+  int32_t pad_;
 };
 
 // Raw (unclamped) running ends of the window's frontier and neighbour
@@ -329,6 +336,11 @@ __global__ void __launch_bounds__(kBlock) k_bits_emit(const uint32_t* bits, int6
   for (int j = 0; j < 8; ++j) n += __popc(w[j]);
   int32_t tot;
   int64_t pos = s_off + block_excl_scan<kBlock>(n, lds, &tot);
+  if (a.tile_runs) {
+    // this thread's run of 8 words starts a tile every tile_runs runs
+    const int64_t run = (int64_t)c * kBlock + threadIdx.x;
+    if (run % a.tile_runs == 0) a.tstart[(int64_t)b * a.ntiles + run / a.tile_runs] = pos;
+  }
 #pragma unroll
   for (int j = 0; j < 8; ++j) {
     for (uint32_t m = w[j]; m; m &= m - 1u) {
@@ -459,6 +471,83 @@ __global__ void __launch_bounds__(kBlock) k_sample(const RowT* row_ptr, const in
   if (st) set_status(status, st);
 }
 
+// Node-tile order: a wavefront takes one tile of consecutive node ids
+// (tile_runs runs of 256) and samples the entries of that tile in every
+// batch of the window, batch by batch.  A node that several batches reach
+// is then sampled by the same wavefront, whose CSR lines (row_ptr and the
+// node's neighbour row) the caches serve after the first batch fetches
+// them; in batch order the batches' copies of a node land on different
+// CUs and XCDs, and every batch fetches the lines again.  Each entry is
+// sampled exactly once, by the same code, so results do not depend on the
+// order.  Lane b (b < W) finds batch b's entries of the tile from the
+// level's tile table; pair j of the tile belongs to the first batch whose
+// running count exceeds j, found by a binary search over the lanes.  A
+// wavefront's tile is g consecutive tiles of the table (ntab of them), g a
+// power of two chosen from the level's entry count so that a tile holds
+// about a wavefront of entries (at most gmax); with fixed = 1, g = 1.
+// Too few entries per wavefront would launch many thinly filled waves,
+// which beside another kernel's resident blocks wait for CU slots in
+// several rounds.
+template <typename RowT, int KMAX>
+__global__ void __launch_bounds__(kBlock) k_sample_tiles(const RowT* row_ptr,
+                                                         const int32_t* col_idx,
+                                                         const int32_t* fids,
+                                                         const int64_t* frontier_off,
+                                                         const LevelState* ls,
+                                                         const int64_t* tstart, int64_t ntab,
+                                                         int32_t gmax, int32_t* nbr,
+                                                         uint32_t* bits, int32_t* status,
+                                                         SampleArgs a) {
+  __shared__ int64_t so[GG_MAX_W + 1];
+  __shared__ int64_t s_nbase;
+  for (int t = threadIdx.x; t <= GG_MAX_W; t += blockDim.x)
+    so[t] = t <= a.W ? frontier_off[(int64_t)a.l * a.W + t] : INT64_MAX;
+  if (threadIdx.x == 0) s_nbase = ls->nbase[a.l];
+  __syncthreads();
+  const int64_t begin = so[0];
+  const int64_t nbase = s_nbase;
+  const int lane = lane_id();
+  // table tiles per wavefront tile: about kWave entries each on average
+  const int64_t entries = so[a.W] - begin;
+  int64_t g = 1;
+  while (g < gmax && (g * 2) * entries <= ntab * kWave) g *= 2;
+  const int64_t ntiles = (ntab + g - 1) / g;
+  int32_t st = 0;
+  for (int64_t t = (int64_t)blockIdx.x * (kBlock / kWave) + threadIdx.x / kWave; t < ntiles;
+       t += (int64_t)gridDim.x * (kBlock / kWave)) {
+    // batch `lane`'s entries of tile t, clamped to its (clamped) segment
+    int64_t lo = 0, n = 0;
+    if (lane < a.W) {
+      const int64_t* tb = tstart + (int64_t)lane * ntab;
+      const int64_t s0 = so[lane], s1 = so[lane + 1];
+      lo = tb[t * g];
+      int64_t hi = (t + 1) * g < ntab ? tb[(t + 1) * g] : s1;
+      lo = lo < s0 ? s0 : (lo > s1 ? s1 : lo);
+      hi = hi > s1 ? s1 : (hi < lo ? lo : hi);
+      n = hi - lo;
+    }
+    const int64_t inc = wave_incl_scan(n);
+    const int64_t total = __shfl(inc, a.W - 1, kWave);
+    for (int64_t j0 = 0; j0 < total; j0 += kWave) {
+      const int64_t j = j0 + lane;
+      // b = number of batches whose running count is at most j
+      int b = 0;
+#pragma unroll
+      for (int step = kWave / 2; step >= 1; step >>= 1) {
+        const int probe = b + step - 1;
+        const int64_t v = __shfl(inc, probe < a.W ? probe : a.W - 1, kWave);
+        if (probe < a.W && v <= j) b += step;
+      }
+      const int bb = b < a.W ? b : a.W - 1;
+      const int64_t before = __shfl(inc - n, bb, kWave);
+      const int64_t gi = __shfl(lo, bb, kWave) + (j - before);
+      if (j < total)
+        sample_one<RowT, KMAX>(row_ptr, col_idx, fids, gi, bb, begin, nbase, nbr, bits, a, st);
+    }
+  }
+  if (st) set_status(status, st);
+}
+
 struct SampleWs {
   int32_t* cnt;       // per (batch, chunk) counts of the current level
   int32_t* tot;       // per level: group totals; zeroed by k_seed_bits (or k_zero_words)
@@ -466,6 +555,7 @@ struct SampleWs {
   int64_t tot_level;  // entries of tot per level
   LevelState* lvl;
   uint8_t* map;       // the last hop's byte map (32 * wpb bytes per batch), or null
+  int64_t* tstart;    // node-tile table of one level: W * (wpb / 8) entries at most
 };
 
 size_t sample_ws_layout(int64_t num_nodes, int32_t W, const Tune& tune, char* base,
@@ -481,15 +571,58 @@ size_t sample_ws_layout(int64_t num_nodes, int32_t W, const Tune& tune, char* ba
   s.map = use_bytemap(num_nodes, W, tune)
               ? cv.take<uint8_t>((size_t)W * (size_t)gg_bits_words(num_nodes) * 32)
               : nullptr;
+  s.tstart = tune.sample_order != GG_SAMPLE_BATCH_ORDER
+                 ? cv.take<int64_t>((size_t)W * (size_t)(gg_bits_words(num_nodes) / kWordsPerThread))
+                 : nullptr;
   if (out) *out = s;
   return align_up(cv.used, 256);
 }
 
+// Runs of 256 nodes per tile of the table a level's emit writes for the
+// next hop's sampler (level lv of at most `bound` entries over nruns runs),
+// or 0 for batch order.  Node tiles cover the last hop only, or every hop
+// (the tuning's sample_order).  Sized per hop, a table tile is a power of
+// two (at most 64) that holds at most a wavefront of entries by the bound,
+// and the sampler joins table tiles by the level's actual count (deeper
+// levels reach far fewer entries than their bound, as batches overlap);
+// the tuning's sample_tile_runs fixes the size instead.  Measured beside
+// the look-ahead's gather on the 2.45M-node graph, last-hop tiles cut that
+// hop's fetched bytes by a third; tiles at the first two hops, whose
+// frontiers the batches share little, made the window slower.
+int32_t tile_runs_for(const Tune& tune, int lv, int L, int64_t nruns, int64_t bound) {
+  if (tune.sample_order == GG_SAMPLE_BATCH_ORDER) return 0;
+  if (tune.sample_order == GG_SAMPLE_TILES_LAST && lv != L - 1) return 0;
+  if (tune.sample_tile_runs > 0) return tune.sample_tile_runs;
+  int64_t g = 1;
+  while (g < 64 && (g * 2) * std::max<int64_t>(bound, 1) <= nruns * kWave) g *= 2;
+  return (int32_t)g;
+}
+
 template <typename RowT>
 int launch_sample(const gg_csr_t* csr, const gg_wsample_t* out, const SampleWs& ws, int32_t* status,
-                  const SampleArgs& a, int64_t bound, hipStream_t stream) {
-  const int grid = (int)std::min<int64_t>(std::max<int64_t>(cdiv(bound, kBlock), 1), 8192);
+                  const SampleArgs& a, int64_t bound, int64_t ntab, int32_t gmax,
+                  hipStream_t stream) {
   const RowT* rp = (const RowT*)csr->row_ptr;
+  if (ntab > 0) {
+    // one wavefront per node tile, four per block; the tiles are joined
+    // table tiles, so there are at most ntab
+    const int grid = (int)std::min<int64_t>(cdiv(ntab, kBlock / kWave), 8192);
+    if (a.k <= 8)
+      hipLaunchKernelGGL((k_sample_tiles<RowT, 8>), dim3(grid), dim3(kBlock), 0, stream, rp,
+                         csr->col_idx, out->frontier_ids, out->frontier_off, ws.lvl, ws.tstart,
+                         ntab, gmax, out->nbr_ids, out->frontier_bits, status, a);
+    else if (a.k <= 16)
+      hipLaunchKernelGGL((k_sample_tiles<RowT, 16>), dim3(grid), dim3(kBlock), 0, stream, rp,
+                         csr->col_idx, out->frontier_ids, out->frontier_off, ws.lvl, ws.tstart,
+                         ntab, gmax, out->nbr_ids, out->frontier_bits, status, a);
+    else
+      hipLaunchKernelGGL((k_sample_tiles<RowT, 32>), dim3(grid), dim3(kBlock), 0, stream, rp,
+                         csr->col_idx, out->frontier_ids, out->frontier_off, ws.lvl, ws.tstart,
+                         ntab, gmax, out->nbr_ids, out->frontier_bits, status, a);
+    GG_LAUNCH_CHECK("k_sample_tiles");
+    return GG_OK;
+  }
+  const int grid = (int)std::min<int64_t>(std::max<int64_t>(cdiv(bound, kBlock), 1), 8192);
   if (a.k <= 8)
     hipLaunchKernelGGL((k_sample<RowT, 8>), dim3(grid), dim3(kBlock), 0, stream, rp, csr->col_idx,
                        out->frontier_ids, out->frontier_off, ws.lvl, out->nbr_ids,
@@ -591,6 +724,9 @@ extern "C" int gg_sample_window(const gg_csr_t* csr, const int32_t* seeds_d,
       if (l < L) lev = std::min<int64_t>(lev * (fanout_h[l] + 1), N);
     }
   }
+  const int64_t nruns = wpb / kWordsPerThread;
+  int64_t ntab_prev = 0;     // tiles of the previous level's table (0: none)
+  int32_t gmax_prev = 1;     // table tiles a sampler tile may join
   for (int lv = 0; lv <= L; ++lv) {
     if (lv > 0) {
       SampleArgs a;
@@ -608,8 +744,10 @@ extern "C" int gg_sample_window(const gg_csr_t* csr, const int32_t* seeds_d,
       a.bytemap = lv == L ? sw.map : nullptr;
       const int64_t bnd = std::min<int64_t>(bound[lv - 1], out->frontier_cap);
       int rc = csr->row_ptr_bits == 64
-                   ? launch_sample<int64_t>(csr, out, sw, status_d, a, bnd, stream)
-                   : launch_sample<int32_t>(csr, out, sw, status_d, a, bnd, stream);
+                   ? launch_sample<int64_t>(csr, out, sw, status_d, a, bnd, ntab_prev, gmax_prev,
+                                            stream)
+                   : launch_sample<int32_t>(csr, out, sw, status_d, a, bnd, ntab_prev, gmax_prev,
+                                            stream);
       if (rc != GG_OK) return rc;
     }
     Totals tt;
@@ -630,6 +768,14 @@ extern "C" int gg_sample_window(const gg_csr_t* csr, const int32_t* seeds_d,
     la.cnt_only = cnt_only ? 1 : 0;
     la.fcap = out->frontier_cap;
     la.ncap = out->nbr_cap;
+    // the tile table for the next hop's sampler
+    la.tile_runs = (lv < L && sw.tstart) ? tile_runs_for(tune, lv, L, nruns, bound[lv]) : 0;
+    la.ntiles = la.tile_runs ? nruns / la.tile_runs : 0;
+    la.tstart = la.tile_runs ? sw.tstart : nullptr;
+    la.pad_ = 0;
+    ntab_prev = la.ntiles;
+    // a fixed tile size is kept as is; otherwise tiles of up to 64 runs
+    gmax_prev = tune.sample_tile_runs > 0 ? 1 : (la.tile_runs ? 64 / la.tile_runs : 1);
     hipLaunchKernelGGL(k_bits_emit, dim3(nch, W), dim3(kBlock), 0, stream, out->frontier_bits, wpb,
                        sw.cnt, tt, out->frontier_ids, out->frontier_off, out->nbr_off, sw.lvl,
                        out->need, status_d, la);

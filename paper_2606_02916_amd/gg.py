@@ -95,10 +95,12 @@ class gg_tuning_t(C.Structure):
     _fields_ = [("tile_rows", C.c_int32), ("gather_blocks", C.c_int32),
                 ("gather_loads", C.c_int32), ("stage_blocks", C.c_int32),
                 ("stage_host_blocks", C.c_int32), ("emit_blocks", C.c_int32),
-                ("hot_max_chunks", C.c_int32), ("bytemap_max_mb", C.c_int32)]
+                ("hot_max_chunks", C.c_int32), ("bytemap_max_mb", C.c_int32),
+                ("sample_order", C.c_int32), ("sample_tile_runs", C.c_int32)]
 
 
 TUNING_FIELDS = tuple(name for name, _ in gg_tuning_t._fields_)
+GG_SAMPLE_BATCH_ORDER, GG_SAMPLE_TILES_LAST, GG_SAMPLE_TILES_ALL = 0, 1, 2
 
 
 class gg_sage_layer_t(C.Structure):

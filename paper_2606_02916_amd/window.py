@@ -23,6 +23,12 @@ import torch
 from . import gg
 
 
+# Largest sampler byte map (MB) the look-ahead driver lets the last hop use:
+# above it the map's scattered writes, clearing and folding cost more HBM
+# traffic than atomic marks into the bit sets.
+LOOKAHEAD_BYTEMAP_MAX_MB = 8
+
+
 def _bucket_flags(part):
     """The hot set comes out ascending, which under a range book is owner
     order: bucketing is then one copy pass."""
@@ -415,6 +421,16 @@ class LookaheadPipeline:
         self.part = gg.make_part(self.P, part_kind, local_owner, self.N, range_start)
         self.feat = gg.make_feat(self.row_bytes, shards, [self.stride] * self.P, shard_rows)
         self.shards = shards
+        # Beside the gather, traffic decides: the last hop samples in node
+        # tiles (the batches share the CSR lines they fetch) and marks with
+        # atomics unless its byte map stays small enough to live in the
+        # caches (on the 2.45M-node graph, 0.444 -> 0.431 ms per window;
+        # the sequential driver, alone on the chip, keeps the library's
+        # defaults, which are faster there).  A caller's tuning replaces
+        # this one as a whole.
+        if tuning is None:
+            tuning = gg.make_tuning(sample_order=gg.GG_SAMPLE_TILES_LAST,
+                                    bytemap_max_mb=LOOKAHEAD_BYTEMAP_MAX_MB)
         self.tuning = tuning
         self.geo = g = _Geometry(self.N, self.W, self.fanout, max_batch, self.P, local_owner,
                                  shard_rows, self.stride, self.cache_stride, tuning)
@@ -510,11 +526,12 @@ class LookaheadPipeline:
         C = (k - self.nsets) % self.NSLOT
         clear_ids = self.bucket_ids[C] if k >= self.nsets else None
         clear_cnt = self.hot_count[C] if k >= self.nsets else None
-        gg.gg_stage_inplace(self.bucket_ids[T], cur.owner_off, g.hot_cap, self.part, self.feat,
-                            self.cache, self.cache_stride, self.cache_rows, cur.slot_of,
-                            clear_ids, clear_cnt, prev.slot_of if k >= 1 else None,
-                            prev.occ if k >= 1 else None, cur.occ, cur.stage_stats, self.status,
-                            self.stage_ws, stream=ss.cuda_stream, tuning=self.tuning)
+        stage_args = (self.bucket_ids[T], cur.owner_off, g.hot_cap, self.part, self.feat,
+                      self.cache, self.cache_stride, self.cache_rows, cur.slot_of, clear_ids,
+                      clear_cnt, prev.slot_of if k >= 1 else None, prev.occ if k >= 1 else None,
+                      cur.occ, cur.stage_stats, self.status, self.stage_ws)
+        self._last_stage = stage_args
+        gg.gg_stage_inplace(*stage_args, stream=ss.cuda_stream, tuning=self.tuning)
         _rec(ev[4], ss)
         if gs is not ss:
             staged = ev[4] if ev[4] is not None else self.staged[X]
@@ -561,6 +578,15 @@ class LookaheadPipeline:
                            self.gather_ws, stream=stream, flags=gg.GG_GATHER_SHARED,
                            tuning=self.tuning)
         return o
+
+    def restage(self, stream=None):
+        """Launches the staging call of the last window again, with the same
+        arguments, on `stream` (default: the caller's current stream), e.g.
+        to time it with the chip to itself.  The window must be complete and
+        no later window enqueued; the call then writes the same slots, remap
+        and statistics again (its inputs, the previous window's remap and
+        occupancy, are unchanged)."""
+        gg.gg_stage_inplace(*self._last_stage, stream=stream, tuning=self.tuning)
 
     def gathered_event(self, k):
         return self.gathered[k % self.nsets]

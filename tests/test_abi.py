@@ -67,7 +67,7 @@ int main() {
   F(gg_sage_layer_t, w_neigh) F(gg_sage_layer_t, bias)
   S(gg_tuning_t) F(gg_tuning_t, gather_blocks) F(gg_tuning_t, gather_loads)
   F(gg_tuning_t, stage_blocks) F(gg_tuning_t, stage_host_blocks) F(gg_tuning_t, emit_blocks)
-  F(gg_tuning_t, hot_max_chunks) F(gg_tuning_t, bytemap_max_mb)
+  F(gg_tuning_t, hot_max_chunks) F(gg_tuning_t, bytemap_max_mb) F(gg_tuning_t, sample_order) F(gg_tuning_t, sample_tile_runs)
   return 0;
 }
 """
@@ -112,6 +112,7 @@ def test_host_helpers(gg):
     assert gg.gg_ws_sample(N, W) > gg.gg_ws_sample(N, W, gg.make_tuning(bytemap_max_mb=-1))
     assert gg.gg_ws_sample(N, W, gg.make_tuning(bytemap_max_mb=1)) == \
         gg.gg_ws_sample(N, W, gg.make_tuning(bytemap_max_mb=-1))
+    assert gg.gg_ws_sample(N, W) < gg.gg_ws_sample(N, W, gg.make_tuning(sample_order=1))
     assert gg.gg_ws_hotset(N, W, gg.make_tuning(hot_max_chunks=4)) < gg.gg_ws_hotset(N, W)
     assert gg.gg_ws_gather(10**6, 1, 4, gg.make_tuning(gather_blocks=64)) < \
         gg.gg_ws_gather(10**6, 1, 4)
@@ -198,7 +199,9 @@ def test_bad_arguments_are_rejected_on_the_host(gg):
     assert "flags" in gg.gg_last_error()
     for field, bad in [("tile_rows", 65), ("tile_rows", -1), ("gather_blocks", 4),
                        ("gather_loads", 3), ("stage_blocks", -2), ("stage_host_blocks", -2),
-                       ("emit_blocks", 513), ("hot_max_chunks", 4097), ("bytemap_max_mb", -2)]:
+                       ("emit_blocks", 513), ("hot_max_chunks", 4097), ("bytemap_max_mb", -2),
+                       ("sample_tile_runs", 3), ("sample_tile_runs", 128),
+                       ("sample_tile_runs", -1), ("sample_order", 3), ("sample_order", -1)]:
         tune = gg.make_tuning(**{field: bad})
         with pytest.raises(gg.GGError):                                  # tuning out of range
             gg.gg_gather_batch(t, t.data_ptr(), 1, 10, part, feat, t, 256, 10, t, t, 256,

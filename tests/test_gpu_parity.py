@@ -211,13 +211,16 @@ def test_wide_rows_with_misses(n_hot, tile):
 @pytest.mark.parametrize("fields", [
     dict(bytemap_max_mb=-1), dict(bytemap_max_mb=1),
     dict(gather_loads=2, gather_blocks=8), dict(gather_loads=4), dict(gather_loads=8, tile_rows=3),
-    dict(stage_blocks=1, tile_rows=7), dict(stage_blocks=3, emit_blocks=1, hot_max_chunks=1)])
+    dict(stage_blocks=1, tile_rows=7), dict(stage_blocks=3, emit_blocks=1, hot_max_chunks=1),
+    dict(sample_order=1), dict(sample_order=2), dict(sample_order=2, sample_tile_runs=1),
+    dict(sample_order=2, sample_tile_runs=64), dict(sample_order=1, bytemap_max_mb=-1)])
 def test_launch_tuning_leaves_results_unchanged(fields):
     """Launch tuning changes only how the work is spread: the sampler's last
     hop with atomic marks instead of the byte map (as on the 111M-node
-    graph), gathers with 2, 4 or 8 loads in flight and few blocks (many
-    tiles per wave), staging by one or three blocks, one hot-set chunk and
-    one free-list block.  Full restage, then in-place staging over three
+    graph), the sampler in node tiles at the last hop or at every hop
+    (sized per hop, or fixed at 256 or 16,384 ids), gathers with 2, 4 or 8 loads in flight and few blocks (many tiles
+    per wave), staging by one or three blocks, one hot-set chunk and one
+    free-list block.  Full restage, then in-place staging over three
     windows, each against the oracle with a budget that leaves misses."""
     log(f"small: tuning {fields}")
     from paper_2606_02916_amd import gg
