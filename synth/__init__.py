@@ -18,7 +18,8 @@ import os
 import numpy as np
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
-LIB_PATH = os.path.join(_HERE, "libsynth.so")
+# SYNTH_LIB lets the sanitizer test tier load an instrumented build.
+LIB_PATH = os.environ.get("SYNTH_LIB") or os.path.join(_HERE, "libsynth.so")
 
 PART_MOD = 0
 PART_RANGE = 1
