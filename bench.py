@@ -159,6 +159,50 @@ def summarize(args):
             f.write(f"# command (FETCH_SIZE, then WRITE_SIZE): {cmd}\n")
             f.write("# scale = known bytes of a 1 GiB device-to-device copy / counter reading\n")
             f.write(json.dumps(d, indent=1) + "\n")
+    if args.fetch_db and args.write_db and args.trace_db and args.traffic_out:
+        # every kernel's HBM-side traffic: FETCH_SIZE and WRITE_SIZE per
+        # dispatch, scaled by what they read for the run's 1 GiB copies,
+        # beside its average duration from the kernel trace
+        def per_name(path, counter):
+            db = sqlite3.connect(path)
+            r = db.execute("select kernel_name, value from counters_collection where "
+                           "counter_name = ?", (counter,)).fetchall()
+            agg, copies = {}, sorted((v for n, v in r if "copyBuffer" in n), reverse=True)[:3]
+            for n, v in r:
+                a = agg.setdefault(_short(n), [0, 0.0])
+                a[0] += 1
+                a[1] += v
+            return agg, sum(copies) / len(copies)
+        fa, f_c = per_name(args.fetch_db, "FETCH_SIZE")
+        wa, w_c = per_name(args.write_db, "WRITE_SIZE")
+        known_kib = args.copy_calibration_mib * 1024
+        fs, wsc = known_kib / f_c, known_kib / w_c
+        db = sqlite3.connect(args.trace_db)
+        dur = {}
+        for n, c, a in db.execute("select name, count(*), avg(end-start) from kernels group by "
+                                  "name").fetchall():
+            d = dur.setdefault(_short(n), [0, 0.0])
+            d[1] = (d[1] * d[0] + a * c) / (d[0] + c)
+            d[0] += c
+        out = [f"# HBM-side traffic of every kernel of bench.py, workload {wl}: FETCH_SIZE and "
+               f"WRITE_SIZE per dispatch",
+               f"# command (trace, FETCH_SIZE, WRITE_SIZE: three runs): {cmd}",
+               f"# scale: known bytes of a {args.copy_calibration_mib} MiB device-to-device copy / "
+               f"counter reading (fetch x{fs:.3f}, write x{wsc:.3f}); MB = 1e6 bytes; the "
+               f"counters see L2 misses, some of which the last-level (Infinity) cache serves",
+               f"{'kernel':40s} {'dispatches':>10s} {'avg_us':>8s} {'fetch_MB':>9s} "
+               f"{'write_MB':>9s} {'GB/s':>8s}"]
+        names = sorted(fa, key=lambda k: -(fa[k][1] / fa[k][0] * fs +
+                                           wa.get(k, (1, 0.0))[1] / wa.get(k, (1, 0.0))[0] * wsc))
+        for k in names:
+            f_mb = fa[k][1] / fa[k][0] * fs * 1024 / 1e6
+            w = wa.get(k)
+            w_mb = (w[1] / w[0] * wsc * 1024 / 1e6) if w else 0.0
+            us = dur.get(k, [0, 0.0])[1] / 1e3
+            gbs = (f_mb + w_mb) * 1e6 / (us * 1e-6) / 1e9 if us else 0.0
+            out.append(f"{k:40s} {fa[k][0]:10d} {us:8.2f} {f_mb:9.2f} {w_mb:9.2f} {gbs:8.1f}")
+        with open(os.path.join(PROFILES, f"{args.traffic_out}_{wl}.txt"), "w") as f:
+            f.write("\n".join(out) + "\n")
     if args.pmc_db:
         # per-kernel averages of every counter in a rocprofv3 --pmc run
         db = sqlite3.connect(args.pmc_db)
@@ -251,6 +295,9 @@ def main():
                     help="with --summarize: a rocprofv3 --pmc database; writes per-kernel "
                          "averages of its counters to profiles/<pmc-out>_<config>.txt")
     ap.add_argument("--pmc-out", default="counters")
+    ap.add_argument("--traffic-out", default=None,
+                    help="with --summarize and trace, fetch and write databases: write every "
+                         "kernel's calibrated traffic and duration to profiles/<name>_<config>.txt")
     ap.add_argument("--bench-json", default=None,
                     help="with --summarize: the JSON line bench.py printed in the traced run")
     ap.add_argument("--phases", default=None,

@@ -235,6 +235,27 @@ int gg_sample_window(const gg_csr_t* csr, const int32_t* seeds_d, const int64_t*
                      const gg_tuning_t* tuning, int32_t* status_d, void* ws, size_t ws_bytes,
                      hipStream_t stream);
 
+/* gg_sample_window in two calls, so that a caller can write the window's
+ * N_b lists on another stream while the hot set is built from the bit sets
+ * (the hot set, buckets and staging read only frontier_bits; the lists are
+ * first read by the gathers).  part GG_SAMPLE_PART_BITS enqueues everything
+ * but the compaction of the last level: once it completes, frontier_bits
+ * holds every batch's N_b, and the lists, offsets and neighbour slots of
+ * levels 0..L-1 are written.  part GG_SAMPLE_PART_LAST enqueues that
+ * compaction: F_L into frontier_ids, its offsets, and need.  The second
+ * call must start after the first completes (stream order, or an event
+ * across streams) and be given the same arguments, ws included, whose
+ * contents carry the level counts from one call to the other; nothing may
+ * reuse ws or frontier_bits before it completes.  Any other part is
+ * GG_ERR_ARG. */
+#define GG_SAMPLE_PART_BITS 1
+#define GG_SAMPLE_PART_LAST 2
+int gg_sample_window_part(const gg_csr_t* csr, const int32_t* seeds_d, const int64_t* seed_off_h,
+                          int32_t W, const int32_t* fanout_h, int32_t L, uint64_t rng_seed,
+                          int32_t epoch, int64_t batch0, const gg_wsample_t* out, int32_t part,
+                          const gg_tuning_t* tuning, int32_t* status_d, void* ws,
+                          size_t ws_bytes, hipStream_t stream);
+
 /* Hot set of the window (Sec. IV-A: the most frequently accessed remote
  * nodes of the window).  Input: the W bit sets N_b written by
  * gg_sample_window (frontier_bits_d).  freq(u) = number of batches whose N_b

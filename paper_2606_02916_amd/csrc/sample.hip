@@ -650,13 +650,20 @@ extern "C" size_t gg_ws_sample(int64_t num_nodes, int32_t W, const gg_tuning_t* 
   return sample_ws_layout(num_nodes, W, tune, nullptr, nullptr);
 }
 
-extern "C" int gg_sample_window(const gg_csr_t* csr, const int32_t* seeds_d,
-                                const int64_t* seed_off_h, int32_t W, const int32_t* fanout_h,
-                                int32_t L, uint64_t rng_seed, int32_t epoch, int64_t batch0,
-                                const gg_wsample_t* out, const gg_tuning_t* tuning,
-                                int32_t* status_d, void* ws, size_t ws_bytes,
-                                hipStream_t stream) {
+namespace gg {
+namespace {
+
+// The sampling of one window, or a part of it: GG_SAMPLE_PART_BITS is everything
+// up to the last level's compaction (with a byte map, its fold into the bit
+// sets included), GG_SAMPLE_PART_LAST that compaction (the count, unless the
+// fold already made it, and the emit of F_L).
+int sample_window_impl(const gg_csr_t* csr, const int32_t* seeds_d, const int64_t* seed_off_h,
+                       int32_t W, const int32_t* fanout_h, int32_t L, uint64_t rng_seed,
+                       int32_t epoch, int64_t batch0, const gg_wsample_t* out,
+                       const gg_tuning_t* tuning, int32_t* status_d, void* ws, size_t ws_bytes,
+                       int32_t part, hipStream_t stream) {
   GG_REQUIRE(csr && out && seed_off_h && fanout_h && status_d, "NULL argument");
+  const bool do_bits = (part & GG_SAMPLE_PART_BITS) != 0, do_last = (part & GG_SAMPLE_PART_LAST) != 0;
   Tune tune;
   if (resolve_tuning(tuning, &tune) != GG_OK) return GG_ERR_ARG;
   GG_REQUIRE(W >= 1 && W <= GG_MAX_W, "W = %d outside 1..%d", W, GG_MAX_W);
@@ -696,7 +703,10 @@ extern "C" int gg_sample_window(const gg_csr_t* csr, const int32_t* seeds_d,
   // and its emit sums them directly: one launch fewer.  Beside a running
   // gather even a small launch costs 7-12 us.
   const bool seed_counts = max_batch <= kSeedBitsMaxBatch && (int64_t)W * nch <= kCntOnlyMaxChunks;
-  if (max_batch <= kSeedBitsMaxBatch) {
+  if (!do_bits) {
+    // the last level only: its count unless the fold already made it, and
+    // its emit
+  } else if (max_batch <= kSeedBitsMaxBatch) {
     hipLaunchKernelGGL(k_seed_bits, dim3((unsigned)nch, (unsigned)W), dim3(kBlock), 0, stream,
                        seeds_d, so, out->frontier_bits, wpb, N, sw.map, sw.tot,
                        (int32_t)((L + 1) * sw.tot_level), seed_counts ? sw.cnt : nullptr,
@@ -728,7 +738,9 @@ extern "C" int gg_sample_window(const gg_csr_t* csr, const int32_t* seeds_d,
   int64_t ntab_prev = 0;     // tiles of the previous level's table (0: none)
   int32_t gmax_prev = 1;     // table tiles a sampler tile may join
   for (int lv = 0; lv <= L; ++lv) {
-    if (lv > 0) {
+    const bool last = lv == L;
+    if (!last && !do_bits) continue;
+    if (lv > 0 && do_bits) {
       SampleArgs a;
       a.N = N;
       a.wpb = wpb;
@@ -754,7 +766,11 @@ extern "C" int gg_sample_window(const gg_csr_t* csr, const int32_t* seeds_d,
     tt.gtot = sw.tot + (int64_t)lv * sw.tot_level;
     tt.ngroups = sw.ngroups;
     const bool cnt_only = lv == 0 && seed_counts;
-    if (!cnt_only) {
+    // the last level's count folds the byte map, which the hot set needs,
+    // so it belongs to the bits part then; without a map it belongs to the
+    // compaction
+    const bool count_here = last ? (sw.map ? do_bits : do_last) : do_bits;
+    if (!cnt_only && count_here) {
       hipLaunchKernelGGL(k_bits_count, dim3(nch, W), dim3(kBlock), 0, stream, out->frontier_bits,
                          wpb, lv == L ? sw.map : nullptr, sw.cnt, tt);
       GG_LAUNCH_CHECK("k_bits_count");
@@ -776,10 +792,37 @@ extern "C" int gg_sample_window(const gg_csr_t* csr, const int32_t* seeds_d,
     ntab_prev = la.ntiles;
     // a fixed tile size is kept as is; otherwise tiles of up to 64 runs
     gmax_prev = tune.sample_tile_runs > 0 ? 1 : (la.tile_runs ? 64 / la.tile_runs : 1);
+    if (last && !do_last) break;
     hipLaunchKernelGGL(k_bits_emit, dim3(nch, W), dim3(kBlock), 0, stream, out->frontier_bits, wpb,
                        sw.cnt, tt, out->frontier_ids, out->frontier_off, out->nbr_off, sw.lvl,
                        out->need, status_d, la);
     GG_LAUNCH_CHECK("k_bits_emit");
   }
   return GG_OK;
+}
+
+}  // namespace
+}  // namespace gg
+
+extern "C" int gg_sample_window(const gg_csr_t* csr, const int32_t* seeds_d,
+                                const int64_t* seed_off_h, int32_t W, const int32_t* fanout_h,
+                                int32_t L, uint64_t rng_seed, int32_t epoch, int64_t batch0,
+                                const gg_wsample_t* out, const gg_tuning_t* tuning,
+                                int32_t* status_d, void* ws, size_t ws_bytes,
+                                hipStream_t stream) {
+  return sample_window_impl(csr, seeds_d, seed_off_h, W, fanout_h, L, rng_seed, epoch, batch0,
+                            out, tuning, status_d, ws, ws_bytes,
+                            GG_SAMPLE_PART_BITS | GG_SAMPLE_PART_LAST, stream);
+}
+
+extern "C" int gg_sample_window_part(const gg_csr_t* csr, const int32_t* seeds_d,
+                                     const int64_t* seed_off_h, int32_t W,
+                                     const int32_t* fanout_h, int32_t L, uint64_t rng_seed,
+                                     int32_t epoch, int64_t batch0, const gg_wsample_t* out,
+                                     int32_t part, const gg_tuning_t* tuning, int32_t* status_d,
+                                     void* ws, size_t ws_bytes, hipStream_t stream) {
+  GG_REQUIRE(part == GG_SAMPLE_PART_BITS || part == GG_SAMPLE_PART_LAST, "part %d is not GG_SAMPLE_PART_BITS "
+             "or GG_SAMPLE_PART_LAST", part);
+  return sample_window_impl(csr, seeds_d, seed_off_h, W, fanout_h, L, rng_seed, epoch, batch0,
+                            out, tuning, status_d, ws, ws_bytes, part, stream);
 }

@@ -126,6 +126,8 @@ SIGNATURES = {
     "gg_ws_gather": (_SZ, [_I64, _I32, _I32, _P]),
     "gg_sample_window": (C.c_int, [_P, _P, _P, _I32, _P, _I32, _U64, _I32, _I64, _P, _P, _P, _P,
                                    _SZ, _P]),
+    "gg_sample_window_part": (C.c_int, [_P, _P, _P, _I32, _P, _I32, _U64, _I32, _I64, _P, _I32,
+                                        _P, _P, _P, _SZ, _P]),
     "gg_build_hotset": (C.c_int, [_P, _I32, _P, _I64, _I64, _I64, _P, _P, _I64, _P, _P, _P, _P,
                                   _SZ, _P]),
     "gg_bucket_by_owner": (C.c_int, [_P, _P, _I64, _P, _I32, _P, _P, _P, _P, _SZ, _P]),
@@ -285,6 +287,22 @@ def gg_sample_window(csr, seeds, seed_off, W, fanout, L, rng_seed, epoch, batch0
                                       fan.ctypes.data, L, C.c_uint64(rng_seed), epoch, batch0,
                                       C.byref(out), _tune(tuning), _ptr(status), _ptr(ws),
                                       ws.numel(), _stream(stream)), "gg_sample_window")
+
+
+GG_SAMPLE_PART_BITS, GG_SAMPLE_PART_LAST = 1, 2
+
+
+def gg_sample_window_part(csr, seeds, seed_off, W, fanout, L, rng_seed, epoch, batch0, out, part,
+                          status, ws, stream=None, tuning=None):
+    """One part of gg_sample_window (GG_SAMPLE_PART_BITS, then
+    GG_SAMPLE_PART_LAST with the same arguments and workspace)."""
+    so = np.ascontiguousarray(seed_off, dtype=np.int64)
+    fan = np.ascontiguousarray(fanout, dtype=np.int32)
+    return check(lib.gg_sample_window_part(C.byref(csr), _ptr(seeds), so.ctypes.data, W,
+                                           fan.ctypes.data, L, C.c_uint64(rng_seed), epoch,
+                                           batch0, C.byref(out), part, _tune(tuning),
+                                           _ptr(status), _ptr(ws), ws.numel(), _stream(stream)),
+                 "gg_sample_window_part")
 
 
 def gg_build_hotset(frontier_bits, W, part, n_hot, hot_ids, hot_freq, cap, hot_count, status, ws,

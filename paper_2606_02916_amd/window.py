@@ -61,6 +61,9 @@ class _Geometry:
                             gg.gg_ws_bucket(self.hot_cap, P), gg.gg_ws_stage(self.hot_cap, P),
                             gg.gg_ws_gather(self.out_cap, 1, P, tuning),
                             gg.gg_ws_gather(self.win_cap, W, P, tuning))
+        # hot set and bucketing, while the sampler's workspace still serves
+        # the last level's compaction on another stream
+        self.ws2_bytes = max(gg.gg_ws_hotset(N, W, tuning), gg.gg_ws_bucket(self.hot_cap, P))
 
 
 class _Buffers:
@@ -69,7 +72,7 @@ class _Buffers:
     With own_cache=False the cache is the pipeline's persistent one and the
     set holds an occupancy bitmap of it instead."""
 
-    def __init__(self, g: _Geometry, dev, own_cache=True):
+    def __init__(self, g: _Geometry, dev, own_cache=True, split=False):
         self.g, self.dev = g, dev
         self.frontier_ids = torch.empty(max(g.fcap, 1), dtype=torch.int32, device=dev)
         self.frontier_off = torch.zeros((g.L + 1) * g.W + 1, dtype=torch.int64, device=dev)
@@ -88,6 +91,7 @@ class _Buffers:
                     torch.zeros(gg.occ_bytes(g.inplace_rows), dtype=torch.uint8, device=dev))
         self.slot_of = torch.full((g.N,), -1, dtype=torch.int32, device=dev)
         self.ws = torch.empty(g.ws_bytes, dtype=torch.uint8, device=dev)
+        self.ws2 = torch.empty(g.ws2_bytes, dtype=torch.uint8, device=dev) if split else self.ws
         self.stage_stats = torch.zeros(gg.STAGE_STATS_BYTES, dtype=torch.uint8, device=dev)
         self.gather_stats = torch.zeros((g.W, gg.GATHER_STATS_BYTES), dtype=torch.uint8,
                                         device=dev)
@@ -406,7 +410,7 @@ class LookaheadPipeline:
 
     def __init__(self, row_ptr, col_idx, num_parts, part_kind, local_owner, range_start, shards,
                  shard_rows, row_bytes, stride, W, fanout, max_batch, n_hot=-1, device=None,
-                 cache_stride=None, nsets=None, hot_frac=None, tuning=None):
+                 cache_stride=None, nsets=None, hot_frac=None, tuning=None, split_last=None):
         self.device = torch.device(device if device is not None else "cuda")
         self.N = int(row_ptr.numel() - 1)
         self.W = int(W)
@@ -442,7 +446,20 @@ class LookaheadPipeline:
             raise ValueError("the look-ahead pipeline needs at least two buffer sets")
         self.nsets = int(nsets)
         self.NSLOT = 2 * self.nsets
-        self.sets = [_Buffers(g, dev, own_cache=False) for _ in range(self.nsets)]
+        # The hot set, buckets and staging read only the bit sets; the last
+        # level's lists are first read by the gather.  With split_last that
+        # compaction moves from the build stream to the gather stream, ahead
+        # of the gather: it shortens the build chain and lengthens the
+        # gather chain, which pays where the build is the longer chain.
+        # The build grows with the sampling depth (a hop and a compaction
+        # per level) and the gather does not, so by default the split is
+        # taken from three hops on: on the 2.45M-node graph (three hops) the
+        # window went from 0.430 to 0.419 ms; on the 233K-node graph (two
+        # hops, gather-bound) it went from 0.335 to 0.350 ms, and to
+        # 0.337-0.343 with the compaction on a fourth stream.
+        self.split_last = (self.L >= 3) if split_last is None else bool(split_last)
+        self.sets = [_Buffers(g, dev, own_cache=False, split=self.split_last)
+                     for _ in range(self.nsets)]
         # One persistent cache (gg_stage_inplace): rows a window shares with
         # the previous one stay in their slot; each set keeps its remap and
         # occupancy map.
@@ -466,6 +483,7 @@ class LookaheadPipeline:
             self.stage_stream = self.build_stream
             self.gather_stream = self.fetch_stream
         self.built = [torch.cuda.Event() for _ in range(self.nsets)]
+        self.sampled = [torch.cuda.Event() for _ in range(self.nsets)]
         self.staged = [torch.cuda.Event() for _ in range(self.nsets)]
         self._released = [torch.cuda.Event() for _ in range(self.nsets)]
         self.gathered = list(self._released)
@@ -500,16 +518,25 @@ class LookaheadPipeline:
             bs.wait_event(self.gathered[X])      # window k - nsets read this set
         s = bs.cuda_stream
         _rec(ev[0], bs)
-        gg.gg_sample_window(self.csr, seeds, seed_off, Wk, self.fanout, self.L, rng_seed, epoch,
-                            batch0, cur.wsample, self.status, cur.ws, stream=s,
-                            tuning=self.tuning)
+        sargs = (self.csr, seeds, seed_off, Wk, self.fanout, self.L, rng_seed, epoch, batch0,
+                 cur.wsample)
+        if self.split_last:
+            gg.gg_sample_window_part(*sargs, gg.GG_SAMPLE_PART_BITS, self.status, cur.ws,
+                                     stream=s, tuning=self.tuning)
+            self.sampled[X].record(bs)
+            # the last level's lists on the gather stream, before the gather
+            gs.wait_event(self.sampled[X])
+            gg.gg_sample_window_part(*sargs, gg.GG_SAMPLE_PART_LAST, self.status, cur.ws,
+                                     stream=gs.cuda_stream, tuning=self.tuning)
+        else:
+            gg.gg_sample_window(*sargs, self.status, cur.ws, stream=s, tuning=self.tuning)
         _rec(ev[1], bs)
         gg.gg_build_hotset(cur.frontier_bits, Wk, self.part, self.n_hot, cur.hot_ids,
-                           cur.hot_freq, g.hot_cap, self.hot_count[T], self.status, cur.ws,
+                           cur.hot_freq, g.hot_cap, self.hot_count[T], self.status, cur.ws2,
                            stream=s, hot_frac=self.hot_frac, tuning=self.tuning)
         _rec(ev[2], bs)
         gg.gg_bucket_by_owner(cur.hot_ids, self.hot_count[T], g.hot_cap, self.part,
-                              self.bucket_ids[T], cur.owner_off, self.status, cur.ws, stream=s,
+                              self.bucket_ids[T], cur.owner_off, self.status, cur.ws2, stream=s,
                               flags=_bucket_flags(self.part))
         _rec(ev[3], bs)
         if ss is not bs:

@@ -233,6 +233,49 @@ def test_launch_tuning_leaves_results_unchanged(fields):
         w.run_and_compare(k)
 
 
+@pytest.mark.parametrize("fields", [dict(), dict(bytemap_max_mb=-1), dict(sample_order=1)])
+def test_sample_window_in_two_parts_across_streams(fields):
+    """gg_sample_window_part: the bits part on one stream, then (after an
+    event) the last level's compaction on another; the bit sets are final
+    after the first part (the byte map folded in, when one is used), and
+    after the second every output equals the oracle's."""
+    log(f"small: sampling in two parts on two streams, tuning {fields}")
+    import torch as T
+    from oracle import ggref
+    from paper_2606_02916_amd import gg
+    tune = gg.make_tuning(**fields)
+    w = world(synth.instance("small"), tuning=tune)
+    p = w.pipe
+    L = len(w.fanout)
+    s1, s2 = T.cuda.Stream(), T.cuda.Stream()
+    for k in range(2):
+        seeds, so, b0 = w.window_inputs(k)
+        sd = T.from_numpy(seeds).to(w.dev)
+        p.frontier_ids.fill_(-7)
+        T.cuda.synchronize()
+        args = (p.csr, sd, so, len(so) - 1, list(w.fanout), L, 0, 0, b0, p.wsample)
+        gg.gg_sample_window_part(*args, gg.GG_SAMPLE_PART_BITS, p.status, p.ws, stream=s1,
+                                 tuning=tune)
+        ev = T.cuda.Event()
+        ev.record(s1)
+        s2.wait_event(ev)
+        gg.gg_sample_window_part(*args, gg.GG_SAMPLE_PART_LAST, p.status, p.ws, stream=s2,
+                                 tuning=tune)
+        T.cuda.synchronize()
+        assert p.read_status() == 0
+        Wk = len(so) - 1
+        fids, foff, nids, noff = ggref.sample_window(w.inst.row_ptr, w.inst.col_idx, seeds, so,
+                                                     w.fanout, 0, 0, b0)
+        g_fids, g_foff, g_nids, g_noff = p.sample_outputs(Wk)
+        assert np.array_equal(g_foff, foff) and np.array_equal(g_fids, fids)
+        assert np.array_equal(g_noff, noff) and np.array_equal(g_nids, nids)
+        from tests.gpu_util import check_bits
+        bits = p.frontier_bits[:Wk * p.wpb].cpu().numpy().view(np.uint32)
+        check_bits(bits, p.wpb, Wk, lambda b: fids[foff[L * Wk + b]:foff[L * Wk + b + 1]])
+    with pytest.raises(gg.GGError):
+        gg.gg_sample_window_part(*args, 3, p.status, p.ws, tuning=tune)
+
+
 @pytest.mark.parametrize("n_hot", [-1, 200])
 def test_every_limit_at_once(n_hot):
     """The ABI's limits together: W = 64 batches (of 16 seeds), L = 4 hops
@@ -355,6 +398,47 @@ def test_lookahead_as_benchmarked(name):
             check(*pending)
         pending = (k, Wk, bufs, b0, b1)
     check(*pending)
+    assert look.read_status() == 0
+
+
+@pytest.mark.parametrize("split,host", [(True, False), (False, False), (True, True)])
+def test_lookahead_split_sampling_matches_oracle(split, host):
+    """The look-ahead driver with the last level's compaction on the gather
+    stream (split) or on the build stream, with shards in device memory and
+    with the remote shards in pinned host memory: five consecutive windows
+    of the small graph against the oracle, element by element."""
+    log(f"small: look-ahead, split_last={split}, host shards={host}, windows 0-4")
+    import torch as T
+    from paper_2606_02916_amd import LookaheadPipeline
+    from tests.gpu_util import LookaheadOracle
+    inst = synth.instance("small")
+    wl = inst.wl
+    dev = T.device("cuda:0")
+    rp_d, ci_d = T.from_numpy(inst.row_ptr).to(dev), T.from_numpy(inst.col_idx).to(dev)
+    sh_d = [T.from_numpy(sh).to(dev) if (m == wl.local_owner or not host)
+            else T.from_numpy(sh).pin_memory() for m, sh in enumerate(inst.shards)]
+    look = LookaheadPipeline(rp_d, ci_d, wl.num_parts, wl.part_kind, wl.local_owner,
+                             inst.range_start, sh_d, [x.shape[0] for x in inst.shards],
+                             wl.row_bytes, wl.row_stride, wl.W, wl.fanout, wl.batch_size,
+                             device=dev, split_last=split)
+    assert look.split_last == split
+    orc = LookaheadOracle(inst, look)
+    boff = inst.batch_off
+    seeds_d = T.from_numpy(inst.seeds).to(dev)
+    pending = None
+    for k in range(min(5, synth.n_windows(boff, wl.W))):
+        b0, b1 = synth.window_batches(boff, wl.W, k)
+        Wk, bufs = look.window(seeds_d[boff[b0]:boff[b1]], boff[b0:b1 + 1] - boff[b0], b0,
+                               gather_events=(None, T.cuda.Event()))
+        if pending is not None:
+            pk, pW, pb, pb0, pb1 = pending
+            look.gathered_event(pk).synchronize()
+            orc.check(pk, pW, pb, inst.seeds[boff[pb0]:boff[pb1]], boff[pb0:pb1 + 1] - boff[pb0],
+                      pb0)
+        pending = (k, Wk, bufs, b0, b1)
+    pk, pW, pb, pb0, pb1 = pending
+    look.gathered_event(pk).synchronize()
+    orc.check(pk, pW, pb, inst.seeds[boff[pb0]:boff[pb1]], boff[pb0:pb1 + 1] - boff[pb0], pb0)
     assert look.read_status() == 0
 
 
