@@ -82,6 +82,7 @@ def summarize(args):
     """Writes profiles/ summaries from rocprofv3 databases of bench runs."""
     import sqlite3
     wl = args.config
+    name = args.profile_name or wl   # file names; gather counters only for the default run
     os.makedirs(PROFILES, exist_ok=True)
     cmd = args.summary_command
     if args.trace_db:
@@ -90,7 +91,7 @@ def summarize(args):
                           "sum(end-start) from kernels group by name order by sum(end-start) "
                           "desc").fetchall()
         tot = sum(r[5] for r in rows)
-        out = [f"# rocprofv3 kernel trace of bench.py, workload {wl}",
+        out = [f"# rocprofv3 kernel trace of bench.py, workload {wl} ({name})",
                f"# command: {cmd}",
                f"# gather source sha: {gather_source_sha()}",
                f"{'kernel':40s} {'calls':>6s} {'avg_us':>9s} {'min_us':>9s} {'max_us':>9s} "
@@ -132,9 +133,21 @@ def summarize(args):
                        f"gg_gather_batch {r['avg_launch_us']} us per launch over the timed steps "
                        f"(HIP events, frac {r['frac']}), {r['isolated']['avg_launch_us']} us "
                        f"isolated (frac {r['isolated']['frac']})")
-        with open(os.path.join(PROFILES, f"kernels_{wl}.txt"), "w") as f:
+        copies = [r[0] for r in db.execute("select end-start from kernels where name like "
+                                           "'%copyBuffer%' order by end-start desc limit 3")]
+        if args.copy_calibration_mib and copies:
+            # the run's plain 1 GiB device-to-device copies: the practical
+            # ceiling of a streaming copy on this part
+            us = sorted(copies)[len(copies) // 2] / 1e3
+            nb = 2 * args.copy_calibration_mib * (1 << 20)
+            out.append("")
+            out.append(f"# practical ceiling: {args.copy_calibration_mib} MiB device-to-device "
+                       f"copy (runtime copy kernel), median of the 3 longest: {us:.1f} us, "
+                       f"{nb / (us * 1e-6) / 1e12:.2f} TB/s read+write "
+                       f"({nb / (us * 1e-6) / 1e9 / HBM_PEAK_GBS:.2f} of {HBM_PEAK_GBS / 1e3:.0f} TB/s)")
+        with open(os.path.join(PROFILES, f"kernels_{name}.txt"), "w") as f:
             f.write("\n".join(out) + "\n")
-    if args.fetch_db and args.write_db:
+    if args.fetch_db and args.write_db and name == wl:
         def per_kernel(path, counter):
             db = sqlite3.connect(path)
             r = db.execute("select kernel_name, value from counters_collection where "
@@ -184,8 +197,8 @@ def summarize(args):
             d = dur.setdefault(_short(n), [0, 0.0])
             d[1] = (d[1] * d[0] + a * c) / (d[0] + c)
             d[0] += c
-        out = [f"# HBM-side traffic of every kernel of bench.py, workload {wl}: FETCH_SIZE and "
-               f"WRITE_SIZE per dispatch",
+        out = [f"# HBM-side traffic of every kernel of bench.py, workload {wl} ({name}): "
+               f"FETCH_SIZE and WRITE_SIZE per dispatch",
                f"# command (trace, FETCH_SIZE, WRITE_SIZE: three runs): {cmd}",
                f"# scale: known bytes of a {args.copy_calibration_mib} MiB device-to-device copy / "
                f"counter reading (fetch x{fs:.3f}, write x{wsc:.3f}); MB = 1e6 bytes; the "
@@ -201,7 +214,7 @@ def summarize(args):
             us = dur.get(k, [0, 0.0])[1] / 1e3
             gbs = (f_mb + w_mb) * 1e6 / (us * 1e-6) / 1e9 if us else 0.0
             out.append(f"{k:40s} {fa[k][0]:10d} {us:8.2f} {f_mb:9.2f} {w_mb:9.2f} {gbs:8.1f}")
-        with open(os.path.join(PROFILES, f"{args.traffic_out}_{wl}.txt"), "w") as f:
+        with open(os.path.join(PROFILES, f"{args.traffic_out}_{name}.txt"), "w") as f:
             f.write("\n".join(out) + "\n")
     if args.pmc_db:
         # per-kernel averages of every counter in a rocprofv3 --pmc run
@@ -295,6 +308,10 @@ def main():
                     help="with --summarize: a rocprofv3 --pmc database; writes per-kernel "
                          "averages of its counters to profiles/<pmc-out>_<config>.txt")
     ap.add_argument("--pmc-out", default="counters")
+    ap.add_argument("--profile-name", default=None,
+                    help="with --summarize: name of the summaries (default: the workload); the "
+                         "gather's counter summary, which the bench line reads, is written only "
+                         "for the default name")
     ap.add_argument("--traffic-out", default=None,
                     help="with --summarize and trace, fetch and write databases: write every "
                          "kernel's calibrated traffic and duration to profiles/<name>_<config>.txt")
