@@ -659,7 +659,7 @@ def main():
         t_sw = time.perf_counter()
         sweep = {"workload": "wsweep", "batch": synth.WORKLOADS["wsweep"].batch_size,
                  "driver": "lookahead", "per_W": wsweep_lookahead(dev, "wsweep", Ws, tuning),
-                 "note": "one untimed epoch per W, then at least 8 timed windows cycling the "
+                 "note": "one untimed epoch per W (every buffer set used), then the epoch cycled 4 times (at least 8 windows) timed, cycling the "
                          "epoch; gather rate from HIP events as in roofline; counts from the "
                          "untimed epoch (bulk bytes per owner: the rows each owner's one request "
                          "moves, i.e. the rebuild delta)"}
@@ -1128,7 +1128,7 @@ def wsweep(args, wl):
     print(json.dumps(line), flush=True)
 
 
-def wsweep_lookahead(dev, name, Ws, tuning=None, reps=2):
+def wsweep_lookahead(dev, name, Ws, tuning=None, reps=4):
     """The W sweep as the default bench reports it: for each W, one epoch of
     the workload `name` through the look-ahead driver (the benchmarked
     configuration), after one untimed epoch, cycled `reps` times (at least
@@ -1150,8 +1150,14 @@ def wsweep_lookahead(dev, name, Ws, tuning=None, reps=2):
     boff = inst.batch_off
     mk = lambda: torch.cuda.Event(enable_timing=True)  # noqa: E731
     out = []
+    look = None
     for W in Ws:
         t_w = time.perf_counter()
+        # the previous W's buffers go back to the device before this W's
+        # are allocated (at W = 32 one set's output alone is about 31 GB)
+        look = None
+        torch.cuda.synchronize()
+        torch.cuda.empty_cache()
         look = LookaheadPipeline(row_ptr_d, col_idx_d, P, wl.part_kind, wl.local_owner,
                                  inst.range_start, shards_d, [s.shape[0] for s in inst.shards],
                                  rb, wl.row_stride, W, wl.fanout, wl.batch_size, device=dev,
@@ -1175,6 +1181,10 @@ def wsweep_lookahead(dev, name, Ws, tuning=None, reps=2):
             remote.append(sum(x["hits"] + x["misses"] for x in g))
             gbytes.append(sum(x["rows"] * (2 * rb + 4) + (x["hits"] + x["misses"]) * 4
                               for x in g))
+        for i in range(nwin, look.nsets):
+            # every buffer set runs once before the timed windows (its
+            # output is allocated on first use)
+            look.window(*wins[i % nwin])
         if look.read_status() != 0:
             raise RuntimeError(f"device status {look.read_status()} at W={W}")
         K = max(reps * nwin, 8)

@@ -205,7 +205,10 @@ int64_t gg_bits_words(int64_t num_nodes);
 int gg_sample_caps(int64_t num_nodes, int32_t W, int64_t max_batch, const int32_t* fanout_h,
                    int32_t L, int64_t* frontier_cap, int64_t* nbr_cap);
 
-/* Workspace sizes in bytes. */
+/* Workspace sizes in bytes.  Each serves every call of its entry point with
+ * at most the given batches (W), segments (nseg), rows (cap, n_cap) and
+ * cache rows, so one workspace sized for a window serves a shorter last
+ * window too. */
 size_t gg_ws_sample(int64_t num_nodes, int32_t W, const gg_tuning_t* tuning);
 size_t gg_ws_hotset(int64_t num_nodes, int32_t W, const gg_tuning_t* tuning);
 size_t gg_ws_bucket(int64_t cap, int32_t num_parts);

@@ -295,8 +295,13 @@ extern "C" size_t gg_ws_gather(int64_t n_cap, int32_t nseg, int32_t num_parts,
                                const gg_tuning_t* tuning) {
   Tune tune;
   if (resolve_tuning(tuning, &tune) != GG_OK) return 0;
-  if (nseg < 1) nseg = 1;
-  return gather_ws_layout(n_cap, nseg, num_parts, tune, nullptr, nullptr);
+  // Every call with at most nseg segments and n_cap rows fits: the blocks
+  // per segment divide the gather's block count, so fewer segments can
+  // launch more blocks in all (1024 blocks: 3 x 341, but 1 x 1024).
+  size_t need = 0;
+  for (int32_t s = 1; s <= std::min(std::max(nseg, 1), GG_MAX_W); ++s)
+    need = std::max(need, gather_ws_layout(n_cap, s, num_parts, tune, nullptr, nullptr));
+  return need;
 }
 
 namespace gg {

@@ -647,7 +647,17 @@ using namespace gg;
 extern "C" size_t gg_ws_sample(int64_t num_nodes, int32_t W, const gg_tuning_t* tuning) {
   Tune tune;
   if (resolve_tuning(tuning, &tune) != GG_OK) return 0;
-  return sample_ws_layout(num_nodes, W, tune, nullptr, nullptr);
+  size_t need = sample_ws_layout(num_nodes, W, tune, nullptr, nullptr);
+  // A call with fewer batches may take the byte map where W batches do not
+  // (the map grows with the batch count); the layout grows with the batch
+  // count otherwise, so the largest such call bounds the rest.
+  if (W > 1 && !use_bytemap(num_nodes, W, tune) && tune.bytemap_max_bytes >= 0) {
+    const int64_t per_batch = gg_bits_words(num_nodes) * 32;
+    const int64_t wmap = std::min<int64_t>(W - 1, tune.bytemap_max_bytes / per_batch);
+    if (wmap >= 1)
+      need = std::max(need, sample_ws_layout(num_nodes, (int32_t)wmap, tune, nullptr, nullptr));
+  }
+  return need;
 }
 
 namespace gg {

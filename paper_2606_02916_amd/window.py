@@ -23,10 +23,19 @@ import torch
 from . import gg
 
 
-# Largest sampler byte map (MB) the look-ahead driver lets the last hop use:
-# above it the map's scattered writes, clearing and folding cost more HBM
-# traffic than atomic marks into the bit sets.
+# Largest sampler byte map (MB) the look-ahead driver lets a sparse last hop
+# use: above it the map's scattered writes, clearing and folding cost more
+# HBM traffic than atomic marks into the bit sets.
 LOOKAHEAD_BYTEMAP_MAX_MB = 8
+
+
+def last_hop_density(num_nodes, fanout, max_batch):
+    """Bound on the last hop's draws per batch over the node count:
+    min(N, B * prod_{i<L-1}(k_i + 1)) * k_{L-1} / N."""
+    f = min(num_nodes, max_batch)
+    for k in fanout[:-1]:
+        f = min(num_nodes, f * (k + 1))
+    return f * fanout[-1] / max(num_nodes, 1)
 
 
 def _bucket_flags(part):
@@ -426,15 +435,21 @@ class LookaheadPipeline:
         self.feat = gg.make_feat(self.row_bytes, shards, [self.stride] * self.P, shard_rows)
         self.shards = shards
         # Beside the gather, traffic decides: the last hop samples in node
-        # tiles (the batches share the CSR lines they fetch) and marks with
+        # tiles (the batches share the CSR lines they fetch).  A sparse last
+        # hop (fewer draws per batch than nodes, by the bound) marks with
         # atomics unless its byte map stays small enough to live in the
-        # caches (on the 2.45M-node graph, 0.444 -> 0.431 ms per window;
-        # the sequential driver, alone on the chip, keeps the library's
-        # defaults, which are faster there).  A caller's tuning replaces
+        # caches: the map's fold pass costs more than the atomics it saves
+        # (2.45M nodes, batch 1024, density 0.37: 0.444 -> 0.431 ms per
+        # window).  A dense one keeps the map: at batch 4096 (density 1.47)
+        # the map took W = 16 from 0.86 to 0.77 ms per window.  The
+        # sequential driver, alone on the chip, keeps the library's
+        # defaults, which are faster there.  A caller's tuning replaces
         # this one as a whole.
         if tuning is None:
-            tuning = gg.make_tuning(sample_order=gg.GG_SAMPLE_TILES_LAST,
-                                    bytemap_max_mb=LOOKAHEAD_BYTEMAP_MAX_MB)
+            dense = last_hop_density(self.N, self.fanout, max_batch) >= 1.0
+            tuning = gg.make_tuning(
+                sample_order=gg.GG_SAMPLE_TILES_LAST,
+                **({} if dense else {"bytemap_max_mb": LOOKAHEAD_BYTEMAP_MAX_MB}))
         self.tuning = tuning
         self.geo = g = _Geometry(self.N, self.W, self.fanout, max_batch, self.P, local_owner,
                                  shard_rows, self.stride, self.cache_stride, tuning)

@@ -120,6 +120,33 @@ def test_host_helpers(gg):
     assert gg.make_tuning() is None
     with pytest.raises(gg.GGError):
         gg.make_tuning(tile=3)
+    # a workspace sized for W batches (nseg segments) serves every shorter
+    # call: a short last window may take the byte map that W batches do not
+    # (2.45M nodes: 2.49 MB of map per batch; 64 MB holds 25 batches, so
+    # W = 32 runs without it and a 16-batch window with it), and fewer
+    # segments may launch more gather blocks in all (1024 = 1 x 1024, but
+    # 3 x 341)
+    for t in (None, gg.make_tuning(bytemap_max_mb=64), gg.make_tuning(bytemap_max_mb=8),
+              gg.make_tuning(bytemap_max_mb=64, sample_order=1)):
+        for N in (60_001, 2_450_000):
+            for W in (1, 3, 16, 32, 64):
+                big = gg.gg_ws_sample(N, W, t)
+                assert all(gg.gg_ws_sample(N, w, t) <= big for w in range(1, W + 1)), (N, W)
+                big = gg.gg_ws_hotset(N, W, t)
+                assert all(gg.gg_ws_hotset(N, w, t) <= big for w in range(1, W + 1)), (N, W)
+    assert gg.gg_ws_sample(2_450_000, 32, gg.make_tuning(bytemap_max_mb=64)) >= \
+        2_450_000 * 16
+    for t in (None, gg.make_tuning(gather_blocks=1000), gg.make_tuning(gather_blocks=96)):
+        for n_cap in (1, 5000, 10**6, 4 * 10**7):
+            for nseg in (1, 3, 7, 16, 64):
+                big = gg.gg_ws_gather(n_cap, nseg, 4, t)
+                assert all(gg.gg_ws_gather(n, s, 4, t) <= big
+                           for s in range(1, nseg + 1) for n in (1, n_cap // 3, n_cap)), \
+                    (n_cap, nseg)
+    for cap in (0, 1, 1000, 10**6):
+        for f in (lambda c: gg.gg_ws_bucket(c, 4), lambda c: gg.gg_ws_stage(c, 4),
+                  lambda c: gg.gg_ws_stage_inplace(c, 2 * c, 4)):
+            assert all(f(c) <= f(cap) for c in (0, cap // 2, cap))
     # the status read checks its pointers before any HIP call
     with pytest.raises(gg.GGError, match="null"):
         gg.gg_read_status(None, stream=0)
@@ -240,3 +267,21 @@ def test_bad_arguments_are_rejected_on_the_host(gg):
         with pytest.raises(gg.GGError):
             gg.gg_sage_forward(smp, 1000, 4, [3, 2], t, dtype, stride, 100, arr, t, 100, t, t,
                                stream=0)
+
+
+def test_lookahead_byte_map_choice_follows_last_hop_density(gg):
+    """The look-ahead driver keeps the sampler's byte map for a dense last
+    hop (at least as many draws per batch as nodes, by the frontier bound)
+    and caps it otherwise: the bound is min(N, B * prod_{i<L-1}(k_i + 1))
+    draws of k_{L-1} each."""
+    from paper_2606_02916_amd.window import last_hop_density
+    assert last_hop_density(2_450_000, [15, 10, 5], 1024) == 1024 * 16 * 11 * 5 / 2_450_000
+    assert last_hop_density(2_450_000, [15, 10, 5], 4096) == 4096 * 16 * 11 * 5 / 2_450_000
+    assert last_hop_density(1000, [15, 10, 5], 512) == 1000 * 5 / 1000    # capped at N
+    assert last_hop_density(233_000, [25, 10], 1024) == 1024 * 26 * 10 / 233_000
+    assert last_hop_density(100, [7], 3) == 3 * 7 / 100                     # one hop: seeds
+    # frontier bound per level as gg_sample_caps sums it (one batch)
+    fc, nc = gg.gg_sample_caps(2_450_000, 1, 4096, [15, 10, 5])
+    lev2 = min(2_450_000, 4096 * 16 * 11)
+    assert nc == 4096 * 15 + 4096 * 16 * 10 + lev2 * 5
+    assert last_hop_density(2_450_000, [15, 10, 5], 4096) == lev2 * 5 / 2_450_000

@@ -442,6 +442,44 @@ def test_lookahead_split_sampling_matches_oracle(split, host):
     assert look.read_status() == 0
 
 
+def test_short_last_window_takes_the_byte_map():
+    """Workspaces sized for W = 20 batches of the small graph (1.3 MB of
+    byte map, over a 1 MB limit: the last hop marks with atomics) serve the
+    epoch's 4-batch last window, whose 256 KB map fits and is taken: the
+    sequential driver and the look-ahead driver (split sampling) over both
+    windows, against the oracle."""
+    log("small: W=20 (windows of 20 and 4 batches), byte map limit 1 MB")
+    import torch as T
+    from paper_2606_02916_amd import LookaheadPipeline, gg
+    from tests.gpu_util import LookaheadOracle
+    tune = gg.make_tuning(bytemap_max_mb=1)
+    inst = synth.instance("small")
+    wl, W = inst.wl, 20
+    boff = inst.batch_off
+    assert synth.n_windows(boff, W) == 2 and len(boff) - 1 == 24
+    per_batch = gg.gg_bits_words(wl.num_nodes) * 32
+    assert 4 * per_batch <= 1 << 20 < W * per_batch
+    w = world(inst, W=W, n_hot=3000, tuning=tune)
+    for k in range(2):
+        w.run_and_compare(k)
+    dev = T.device("cuda:0")
+    rp_d, ci_d = T.from_numpy(inst.row_ptr).to(dev), T.from_numpy(inst.col_idx).to(dev)
+    sh_d = [T.from_numpy(sh).to(dev) for sh in inst.shards]
+    look = LookaheadPipeline(rp_d, ci_d, wl.num_parts, wl.part_kind, wl.local_owner,
+                             inst.range_start, sh_d, [x.shape[0] for x in inst.shards],
+                             wl.row_bytes, wl.row_stride, W, wl.fanout, wl.batch_size,
+                             device=dev, tuning=tune)
+    assert look.split_last
+    orc = LookaheadOracle(inst, look)
+    seeds_d = T.from_numpy(inst.seeds).to(dev)
+    for k in range(2):
+        b0, b1 = synth.window_batches(boff, W, k)
+        Wk, bufs = look.window(seeds_d[boff[b0]:boff[b1]], boff[b0:b1 + 1] - boff[b0], b0)
+        look.gathered_event(k).synchronize()
+        orc.check(k, Wk, bufs, inst.seeds[boff[b0]:boff[b1]], boff[b0:b1 + 1] - boff[b0], b0)
+    assert look.read_status() == 0
+
+
 @pytest.mark.timeout(900)
 def test_dense_mid_full_window_matches_oracle():
     log("dense_mid: 233K nodes, 114M edges, fp32x602 (stride 2416), fanout [25,10], W=8, window 0")
