@@ -659,8 +659,9 @@ def main():
         t_sw = time.perf_counter()
         sweep = {"workload": "wsweep", "batch": synth.WORKLOADS["wsweep"].batch_size,
                  "driver": "lookahead", "per_W": wsweep_lookahead(dev, "wsweep", Ws, tuning),
-                 "note": "one untimed epoch per W (every buffer set used), then the epoch cycled 4 times (at least 8 windows) timed, cycling the "
-                         "epoch; gather rate from HIP events as in roofline; counts from the "
+                 "note": "one untimed epoch per W (every buffer set used once), then the "
+                         "epoch cycled 4 times (at least 8 windows) timed; gather rate from "
+                         "HIP events as in roofline; counts from the "
                          "untimed epoch (bulk bytes per owner: the rows each owner's one request "
                          "moves, i.e. the rebuild delta)"}
         sweep["wall_s"] = round(time.perf_counter() - t_sw, 1)
