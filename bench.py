@@ -1038,7 +1038,7 @@ def wsweep(args, wl):
     import torch
 
     import synth
-    from paper_2606_02916_amd import FetchPipeline, LookaheadPipeline
+    from paper_2606_02916_amd import FetchPipeline
     dev = torch.device("cuda:0")
     inst, row_ptr_d, col_idx_d, shards_d = synth.torch_instance(args.config, dev)
     P, rb = wl.num_parts, wl.row_bytes
@@ -1082,27 +1082,6 @@ def wsweep(args, wl):
         g_ms = sum(a.elapsed_time(b) for a, b in gev)
         del pipe
         torch.cuda.empty_cache()
-        # the same windows through the look-ahead driver (persistent cache),
-        # cycling the epoch for at least 8 windows after one untimed epoch
-        look = LookaheadPipeline(row_ptr_d, col_idx_d, P, wl.part_kind, wl.local_owner,
-                                 inst.range_start, shards_d, [s.shape[0] for s in inst.shards],
-                                 rb, wl.row_stride, W, wl.fanout, wl.batch_size, device=dev)
-        for s, so, b0 in wins:
-            look.window(s, so, b0)
-        look.synchronize()
-        K = max(2 * nwin, 8)
-        torch.cuda.synchronize()
-        t0 = time.perf_counter()
-        for i in range(K):
-            s, so, b0 = wins[i % nwin]
-            look.window(s, so, b0, gather_events=(None, mk()))
-        look.synchronize()
-        el_look = time.perf_counter() - t0
-        if look.read_status() != 0:
-            raise RuntimeError(f"device status {look.read_status()} at W={W}")
-        rows_look = sum(rows[i % nwin] for i in range(K))
-        del look
-        torch.cuda.empty_cache()
         r = {"W": W, "windows": nwin, "hot_set_rows_per_window": float(np.mean(hot)),
              "bulk_bytes_per_owner_per_window": [float(x) for x in np.mean(owner_bytes, axis=0)],
              "bulk_requests_per_epoch": int(sum(requests)),
@@ -1110,11 +1089,19 @@ def wsweep(args, wl):
              "rows_gathered_per_epoch": int(sum(rows)),
              "reuse_factor": round(sum(remote) / max(1, sum(hot)), 3),
              "epoch_ms": round(el * 1e3, 3), "rows_per_s": round(sum(rows) / el, 1),
-             "gather_GBps": round(sum(gbytes) / (g_ms * 1e-3) / 1e9, 1),
-             "lookahead_ms_per_window": round(el_look / K * 1e3, 4),
-             "lookahead_rows_per_s": round(rows_look / el_look, 1)}
+             "gather_GBps": round(sum(gbytes) / (g_ms * 1e-3) / 1e9, 1)}
         log(json.dumps(r))
         results.append(r)
+    # the same windows through the look-ahead driver (persistent cache), as
+    # the default line's sweep measures them (it uploads its own copy)
+    del row_ptr_d, col_idx_d, shards_d, seeds_d
+    torch.cuda.empty_cache()
+    for r, la in zip(results, wsweep_lookahead(dev, args.config, [r["W"] for r in results],
+                                               parse_tuning(args.tune))):
+        assert la["W"] == r["W"]
+        r["lookahead_ms_per_window"] = la["ms_per_window"]
+        r["lookahead_rows_per_s"] = la["rows_per_s"]
+        r["lookahead_gather_GBps"] = la["gather_GBps"]
     pick = next((r for r in results if r["W"] == wl.W), results[-1])
     line = {"metric": "feature rows gathered/s vs W (per-window fetch path)",
             "value": pick["rows_per_s"], "unit": "rows/s", "n_gpus": 1,
