@@ -161,8 +161,8 @@ typedef struct gg_gather_stats {
  * `tuning` pointer accepts NULL (all defaults), and a field left 0 keeps
  * its default; values outside the stated ranges are GG_ERR_ARG.  A call
  * and the gg_ws_* function that sized its workspace must be given the same
- * values (the hot-set chunk limit, the byte-map limit and the gather's
- * block count change workspace layouts). */
+ * values (the hot-set chunk limit, the byte-map and mark-slice limits and
+ * the gather's block count change workspace layouts). */
 typedef struct gg_tuning {
   int32_t tile_rows;         /* rows a wavefront copies per step, 1..64 (staging and gathers);
                                 default: as many as fit in 32 KB (staging) or 8 KB (gathers),
@@ -190,6 +190,15 @@ typedef struct gg_tuning {
                                 batch order. */
   int32_t sample_tile_runs;  /* node tiles of this many runs of 256 ids, a power of two up to
                                 64; 0: sized per hop from its entry count */
+  int32_t mark_slices_max;   /* the sampler marks each hop's draws into the bit sets in a pass of
+                                its own, one block per slice of a batch's set held in LDS (up to
+                                64 KB: 524,288 node ids), when a batch's set has at most this many
+                                slices, 1..4096; -1: never (the hop marks with atomic ORs, or
+                                the last hop into the byte map).  Default 8 */
+  int32_t mark_slice_chunks; /* chunks of 65,536 node ids (8 KB of a set) per mark slice, 1..8
+                                (default 8) */
+  int32_t mark_block;        /* lanes of a mark block: 256 (default) or 1024; a block keeps
+                                64 KB of slot loads in flight */
 } gg_tuning_t;
 #define GG_SAMPLE_BATCH_ORDER 0
 #define GG_SAMPLE_TILES_LAST 1

@@ -91,6 +91,12 @@ int resolve_tuning(const gg_tuning_t* t, Tune* out) {
   GG_REQUIRE(t->sample_tile_runs >= 0 && t->sample_tile_runs <= 64 &&
                  (t->sample_tile_runs & (t->sample_tile_runs - 1)) == 0,
              "tuning: sample_tile_runs %d is not a power of two up to 64", t->sample_tile_runs);
+  GG_REQUIRE(t->mark_slices_max >= -1 && t->mark_slices_max <= 4096,
+             "tuning: mark_slices_max %d outside 1..4096 (or -1)", t->mark_slices_max);
+  GG_REQUIRE(t->mark_slice_chunks >= 0 && t->mark_slice_chunks <= 8,
+             "tuning: mark_slice_chunks %d outside 1..8", t->mark_slice_chunks);
+  GG_REQUIRE(t->mark_block == 0 || t->mark_block == 256 || t->mark_block == 1024,
+             "tuning: mark_block %d is not 256 or 1024", t->mark_block);
   out->tile_rows = t->tile_rows;
   out->gather_blocks = t->gather_blocks ? t->gather_blocks : kGatherBlocksDefault;
   out->gather_loads = t->gather_loads;
@@ -105,6 +111,9 @@ int resolve_tuning(const gg_tuning_t* t, Tune* out) {
                                                    : (int64_t)t->bytemap_max_mb << 20;
   out->sample_order = t->sample_order;
   out->sample_tile_runs = t->sample_tile_runs;
+  out->mark_slices_max = t->mark_slices_max ? t->mark_slices_max : kMarkSlicesDefault;
+  out->mark_slice_chunks = t->mark_slice_chunks ? t->mark_slice_chunks : kMarkSliceChunksDefault;
+  out->mark_block = t->mark_block ? t->mark_block : kMarkBlockLanes;
   return GG_OK;
 }
 

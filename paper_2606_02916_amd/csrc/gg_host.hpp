@@ -70,6 +70,9 @@ constexpr int kStageHostBlocksDefault = 128; // ... when a shard is in host memo
 constexpr int kEmitBlocksMax = 512;          // most in-place free-list blocks
 constexpr int kHotMaxChunks = 4096;          // most hot-set chunks
 constexpr int64_t kByteMapMaxBytes = 512LL << 20;  // largest sampler byte map
+constexpr int kMarkSlicesDefault = 8;        // most LDS mark slices per batch
+constexpr int kMarkSliceChunksDefault = 8;   // 8 KB chunks per mark slice
+constexpr int kMarkBlockLanes = 256;         // lanes per mark block
 
 // gg_tuning_t checked and resolved against the defaults.
 struct Tune {
@@ -83,6 +86,9 @@ struct Tune {
   int64_t bytemap_max_bytes;  // -1: no byte map
   int32_t sample_order;       // GG_SAMPLE_*
   int32_t sample_tile_runs;   // 0: per hop
+  int32_t mark_slices_max;    // -1: marks by atomics (or the byte map)
+  int32_t mark_slice_chunks;  // 8 KB chunks of a batch's set per mark slice
+  int32_t mark_block;         // lanes per mark block: 256 or 1024
 };
 
 // Resolves `t` (NULL: every default) into *out; GG_ERR_ARG (with a message)

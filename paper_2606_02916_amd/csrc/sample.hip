@@ -8,6 +8,9 @@
 // per-batch totals), then an emit pass in which every block finds its own
 // place from those counts.  Deduplication therefore costs streaming passes
 // over N/8 bytes per batch and hop instead of a sort of the sampled ids.
+// Where a batch's set splits into few LDS-sized slices, a hop's draws are
+// ORed in by a pass of their own through LDS (k_mark_slices), which also
+// makes the counts; elsewhere the sampler ORs them in with atomics.
 #include <limits.h>
 #include <stdlib.h>
 
@@ -51,6 +54,7 @@ struct SampleArgs {
   int32_t W, l, k;
   uint32_t key0, key1, epoch;
   uint8_t* bytemap;   // non-null: marks go to one byte per node (bytes per batch: 32 * wpb)
+  int32_t nomark;     // marks are left to k_mark_slices
 };
 
 // The last hop marks its draws with byte stores into a byte map instead of
@@ -63,6 +67,28 @@ struct SampleArgs {
 inline bool use_bytemap(int64_t num_nodes, int32_t W, const Tune& tune) {
   return tune.bytemap_max_bytes >= 0 &&
          (int64_t)W * gg_bits_words(num_nodes) * 32 <= tune.bytemap_max_bytes;
+}
+
+// Marks through LDS: block (s, b) of k_mark_slices holds slice s of batch
+// b's set (the tuning's mark_slice_chunks chunks of 8 KB) and reads every slot the hop
+// wrote for batch b, so each slot is read once per slice: worth it while a
+// batch's set has few slices (at most the tuning's mark_slices_max).  A
+// random OR then costs an LDS atomic instead of one performed at memory
+// (about 32 bytes of memory-side traffic each, and the rate that bounds the
+// sampler's last hop).
+// A block is one wave per SIMD, so that it finds room beside a running
+// gather (four waves per SIMD of 74 VGPRs leave no SIMD room for a block
+// of four waves each: a 1,024-lane block waited 170 us for the gather to
+// drain); its lanes keep 16 loads of 16 bytes in flight instead.
+constexpr int kMarkBlockDefault = 256;
+constexpr int kMarkRoundBytes = 65536;   // slot bytes a block has in flight per round
+
+inline int64_t mark_slices(int64_t num_nodes, const Tune& tune) {
+  return cdiv(gg_bits_words(num_nodes) / kChunkWords, (int64_t)tune.mark_slice_chunks);
+}
+
+inline bool use_slices(int64_t num_nodes, const Tune& tune) {
+  return tune.mark_slices_max > 0 && mark_slices(num_nodes, tune) <= tune.mark_slices_max;
 }
 
 // Largest b in [0, 64) with off[b] <= x, for a table padded with INT64_MAX.
@@ -234,6 +260,146 @@ __global__ void __launch_bounds__(kBlock) k_bits_count(uint32_t* bits, int64_t w
   }
 }
 
+struct MarkArgs {
+  int64_t N, wpb, ncap;
+  int32_t W, l, k, nch;
+  int32_t vec;      // the slots are 16-byte aligned
+  int32_t schunks;  // chunks per slice (the block's dynamic LDS: schunks * 8 KB)
+};
+
+// The marks of hop l, with level l+1's counts (as k_bits_count makes them):
+// block (s, b) loads slice s of batch b's set (F_l's bits) into LDS, ORs in
+// every id in batch b's slots of hop l that falls in the slice, writes the
+// slice back and counts its chunks.  Only the slots of complete entries are
+// read: an entry that would pass the slot capacity wrote none of its slots,
+// and the end of the last complete one bounds what was written.
+// One round of a mark block's slot loads: lane t reads the 16-byte groups
+// at p + u * 4 * kMarkBlock (p at the lane's first group), all in flight at
+// once, then marks their slots.  The lane's groups end at `mine` slots past
+// p (a round's last lane may have fewer); a load past that end reads the
+// lane's last group again (in bounds, no branch) and its slots are not
+// marked, nor are the first `head` slots, which precede the batch's list.
+template <int kMarkBlock, typename F>
+__device__ __forceinline__ void mark_round(const int32_t* p, int32_t mine, int32_t head,
+                                           F& mark) {
+  constexpr int kMarkLoads = kMarkRoundBytes / 16 / kMarkBlock;
+  constexpr int kStep = 4 * kMarkBlock;
+  u32x4 t[kMarkLoads];
+#pragma unroll
+  for (int u = 0; u < kMarkLoads; ++u)
+    t[u] = *(const u32x4*)(p + (u * kStep < mine ? u * kStep : mine - 4));
+#pragma unroll
+  for (int u = 0; u < kMarkLoads; ++u) {
+    const bool ok = u * kStep < mine;
+    mark((int32_t)t[u].x, ok && u * kStep + 0 >= head);
+    mark((int32_t)t[u].y, ok && u * kStep + 1 >= head);
+    mark((int32_t)t[u].z, ok && u * kStep + 2 >= head);
+    mark((int32_t)t[u].w, ok && u * kStep + 3 >= head);
+  }
+}
+
+template <int kMarkBlock>
+__device__ __forceinline__ void mark_slices_body(uint32_t* bits, const int32_t* nbr,
+                                                            const int64_t* nbr_off,
+                                                            const LevelState* ls, int32_t* cnt,
+                                                            Totals tt, MarkArgs a) {
+  extern __shared__ uint32_t sl[];
+  const int s = blockIdx.x, b = blockIdx.y;
+  const int c0 = s * a.schunks;
+  const int nc = min(a.schunks, a.nch - c0);
+  const int nw = nc * kChunkWords;
+  uint32_t* brow = bits + (int64_t)b * a.wpb + (int64_t)c0 * kChunkWords;
+  int64_t lo = nbr_off[(int64_t)a.l * a.W + b], hi = nbr_off[(int64_t)a.l * a.W + b + 1];
+  const int64_t nbase = ls->nbase[a.l];
+  {
+    // the slice in one round of loads (at most 16 per lane): beside a
+    // gather that saturates HBM a round trip takes several microseconds
+    constexpr int kSliceLoads = 8 * kChunkWords / 4 / kMarkBlock;
+    u32x4 t[kSliceLoads];
+#pragma unroll
+    for (int u = 0; u < kSliceLoads; ++u) {
+      const int i = u * kMarkBlock + threadIdx.x;
+      if (i < nw / 4) t[u] = ((const u32x4*)brow)[i];
+    }
+#pragma unroll
+    for (int u = 0; u < kSliceLoads; ++u) {
+      const int i = u * kMarkBlock + threadIdx.x;
+      if (i < nw / 4) ((u32x4*)sl)[i] = t[u];
+    }
+  }
+  if (nbase < a.ncap) {
+    const int64_t lim = nbase + (a.ncap - nbase) / a.k * a.k;
+    hi = hi < lim ? hi : lim;
+  }
+  __syncthreads();
+  const uint32_t node_lo = (uint32_t)c0 * (uint32_t)(kChunkWords * 32);
+  const uint32_t span = (uint32_t)nw * 32u;
+  // Branch-free: every lane ORs, a value outside the slice (or not a slot
+  // of the batch) ORs 0 into a word of its own past the slice.  A branch per
+  // value would cost more than the extra LDS operations: a wave has few
+  // neighbours on its SIMD to hide the branch latency behind.
+  const uint32_t dummy = (uint32_t)nw + (uint32_t)lane_id();
+  auto mark = [&](int32_t v, bool ok) {
+    const uint32_t x = (uint32_t)v - node_lo;   // wraps above span for v < node_lo
+    const bool in = ok && x < span && (uint32_t)v < (uint32_t)a.N;
+    atomicOr(&sl[in ? x >> 5 : dummy], in ? 1u << (x & 31) : 0u);
+  };
+
+  // Rounds of up to kMarkLoads * 1,024 slots in whole 16-byte groups, from
+  // the boundary at or below lo to the one at or below hi, all of a round's
+  // loads in flight at once (a loop of one load per lane and step would pay
+  // a memory round trip per step); then the at most three slots after the
+  // last group.
+  constexpr int kRound = kMarkRoundBytes / 4;   // slots
+  if (a.vec) {
+    const int64_t a0 = lo & ~(int64_t)3, hv = hi & ~(int64_t)3;
+    // slots of this lane's first group before lo (lo - a0 < 4): 0..3
+    const int64_t h = lo - a0 - 4 * (int64_t)threadIdx.x;
+    int32_t head = h > 0 ? (int32_t)h : 0;
+    for (int64_t base = a0; base < hv; base += kRound, head = 0) {
+      const int64_t rem = hv - base;
+      const int32_t r = rem < kRound ? (int32_t)rem : kRound;   // a multiple of 4
+      const int32_t mine = r - 4 * (int32_t)threadIdx.x;       // <= 0: no group this round
+      if (mine > 0) mark_round<kMarkBlock>(nbr + base + 4 * threadIdx.x, mine, head, mark);
+    }
+    const int64_t q = (hv > lo ? hv : lo) + threadIdx.x;
+    if (q < hi) mark(nbr[q], true);
+  } else {
+    for (int64_t q = lo + threadIdx.x; q < hi; q += kMarkBlock) mark(nbr[q], true);
+  }
+  __syncthreads();
+  for (int i = threadIdx.x; i < nw / 4; i += kMarkBlock) ((u32x4*)brow)[i] = ((const u32x4*)sl)[i];
+  const int lane = lane_id();
+  for (int cc = threadIdx.x / kWave; cc < nc; cc += kMarkBlock / kWave) {
+    const u32x4* cw = (const u32x4*)(sl + cc * kChunkWords);
+    int n = 0;
+    for (int j = lane; j < kChunkWords / 4; j += kWave) {
+      const u32x4 w = cw[j];
+      n += __popc(w.x) + __popc(w.y) + __popc(w.z) + __popc(w.w);
+    }
+    n = wave_sum(n);
+    if (lane == 0) {
+      const int c = c0 + cc;
+      cnt[(int64_t)b * a.nch + c] = n;
+      if (n)
+        atomicAdd(tt.gtot + ((int64_t)b * tt.ngroups + c / kGroupChunks) * kTotLanes +
+                      (c & (kTotLanes - 1)),
+                  n);
+    }
+  }
+}
+
+#define GG_MARK_ARGS                                                                        \
+  uint32_t *bits, const int32_t *nbr, const int64_t *nbr_off, const LevelState *ls, int32_t *cnt, \
+      Totals tt, MarkArgs a
+__global__ void __launch_bounds__(256) k_mark_slices_256(GG_MARK_ARGS) {
+  mark_slices_body<256>(bits, nbr, nbr_off, ls, cnt, tt, a);
+}
+__global__ void __launch_bounds__(1024) k_mark_slices_1024(GG_MARK_ARGS) {
+  mark_slices_body<1024>(bits, nbr, nbr_off, ls, cnt, tt, a);
+}
+#undef GG_MARK_ARGS
+
 // Sums of three values over the block.
 __device__ __forceinline__ void block_sum3(int64_t (&v)[3], int64_t (*lds)[3]) {
   const int w = threadIdx.x / kWave;
@@ -393,8 +559,10 @@ __device__ __forceinline__ void floyd_positions(uint32_t u, uint32_t bglob, cons
 }
 
 // Samples frontier entry gi of level l (batch b): writes its k neighbour
-// slots and sets the sampled neighbours' bits in batch b's set.  All
-// neighbour loads are issued before any store or atomic.
+// slots and, unless a.nomark, sets the sampled neighbours' bits in batch
+// b's set.  All neighbour loads are issued before any store or atomic.  An
+// entry whose slots would pass the capacity writes neither slots nor bits,
+// so the ids in the written slots are exactly the marks.
 template <typename RowT, int KMAX>
 __device__ __forceinline__ void sample_one(const RowT* row_ptr, const int32_t* col_idx,
                                            const int32_t* fids, int64_t gi, int b, int64_t begin,
@@ -438,7 +606,7 @@ __device__ __forceinline__ void sample_one(const RowT* row_ptr, const int32_t* c
   for (int i = 0; i < KMAX; ++i) {
     if (i < k) {
       const int32_t x = v[i];
-      if (x >= 0) {
+      if (x >= 0 && !a.nomark) {
         if (a.bytemap)
           a.bytemap[(int64_t)b * a.wpb * 32 + x] = 1;
         else
@@ -568,7 +736,7 @@ size_t sample_ws_layout(int64_t num_nodes, int32_t W, const Tune& tune, char* ba
   s.tot_level = (int64_t)W * kTotLanes * s.ngroups;
   s.tot = cv.take<int32_t>((size_t)(GG_MAX_LAYERS + 1) * s.tot_level);
   s.lvl = cv.take<LevelState>(1);
-  s.map = use_bytemap(num_nodes, W, tune)
+  s.map = use_bytemap(num_nodes, W, tune) && !use_slices(num_nodes, tune)
               ? cv.take<uint8_t>((size_t)W * (size_t)gg_bits_words(num_nodes) * 32)
               : nullptr;
   s.tstart = tune.sample_order != GG_SAMPLE_BATCH_ORDER
@@ -651,7 +819,8 @@ extern "C" size_t gg_ws_sample(int64_t num_nodes, int32_t W, const gg_tuning_t* 
   // A call with fewer batches may take the byte map where W batches do not
   // (the map grows with the batch count); the layout grows with the batch
   // count otherwise, so the largest such call bounds the rest.
-  if (W > 1 && !use_bytemap(num_nodes, W, tune) && tune.bytemap_max_bytes >= 0) {
+  if (W > 1 && !use_bytemap(num_nodes, W, tune) && tune.bytemap_max_bytes >= 0 &&
+      !use_slices(num_nodes, tune)) {
     const int64_t per_batch = gg_bits_words(num_nodes) * 32;
     const int64_t wmap = std::min<int64_t>(W - 1, tune.bytemap_max_bytes / per_batch);
     if (wmap >= 1)
@@ -703,6 +872,7 @@ int sample_window_impl(const gg_csr_t* csr, const int32_t* seeds_d, const int64_
 
   const int64_t wpb = gg_bits_words(N);
   const int32_t nch = (int32_t)(wpb / kChunkWords);
+  const bool slices = use_slices(N, tune);
 
   SeedOff so;
   for (int b = 0; b <= GG_MAX_W; ++b) so.off[b] = b <= W ? seed_off_h[b] : INT64_MAX;
@@ -764,6 +934,7 @@ int sample_window_impl(const gg_csr_t* csr, const int32_t* seeds_d, const int64_
       a.key1 = (uint32_t)(rng_seed >> 32);
       a.epoch = (uint32_t)epoch;
       a.bytemap = lv == L ? sw.map : nullptr;
+      a.nomark = slices ? 1 : 0;
       const int64_t bnd = std::min<int64_t>(bound[lv - 1], out->frontier_cap);
       int rc = csr->row_ptr_bits == 64
                    ? launch_sample<int64_t>(csr, out, sw, status_d, a, bnd, ntab_prev, gmax_prev,
@@ -776,11 +947,32 @@ int sample_window_impl(const gg_csr_t* csr, const int32_t* seeds_d, const int64_
     tt.gtot = sw.tot + (int64_t)lv * sw.tot_level;
     tt.ngroups = sw.ngroups;
     const bool cnt_only = lv == 0 && seed_counts;
-    // the last level's count folds the byte map, which the hot set needs,
-    // so it belongs to the bits part then; without a map it belongs to the
-    // compaction
-    const bool count_here = last ? (sw.map ? do_bits : do_last) : do_bits;
-    if (!cnt_only && count_here) {
+    // the last level's count folds the byte map, or makes the marks, which
+    // the hot set needs, so it belongs to the bits part then; after atomic
+    // marks it belongs to the compaction
+    const bool count_here = last ? ((sw.map || slices) ? do_bits : do_last) : do_bits;
+    if (!cnt_only && count_here && slices && lv > 0) {
+      MarkArgs ma;
+      ma.N = N;
+      ma.wpb = wpb;
+      ma.ncap = out->nbr_cap;
+      ma.W = W;
+      ma.l = lv - 1;
+      ma.k = fanout_h[lv - 1];
+      ma.nch = nch;
+      ma.vec = aligned16(out->nbr_ids) ? 1 : 0;
+      ma.schunks = tune.mark_slice_chunks;
+      const dim3 mg((unsigned)mark_slices(N, tune), W);
+      // the slice, and a word per lane of a wavefront for the marks that miss it
+      const size_t lds = ((size_t)tune.mark_slice_chunks * kChunkWords + kWave) * 4;
+      if (tune.mark_block == 1024)
+        hipLaunchKernelGGL(k_mark_slices_1024, mg, dim3(1024), lds, stream, out->frontier_bits,
+                           out->nbr_ids, out->nbr_off, sw.lvl, sw.cnt, tt, ma);
+      else
+        hipLaunchKernelGGL(k_mark_slices_256, mg, dim3(256), lds, stream, out->frontier_bits,
+                           out->nbr_ids, out->nbr_off, sw.lvl, sw.cnt, tt, ma);
+      GG_LAUNCH_CHECK("k_mark_slices");
+    } else if (!cnt_only && count_here) {
       hipLaunchKernelGGL(k_bits_count, dim3(nch, W), dim3(kBlock), 0, stream, out->frontier_bits,
                          wpb, lv == L ? sw.map : nullptr, sw.cnt, tt);
       GG_LAUNCH_CHECK("k_bits_count");

@@ -96,7 +96,9 @@ class gg_tuning_t(C.Structure):
                 ("gather_loads", C.c_int32), ("stage_blocks", C.c_int32),
                 ("stage_host_blocks", C.c_int32), ("emit_blocks", C.c_int32),
                 ("hot_max_chunks", C.c_int32), ("bytemap_max_mb", C.c_int32),
-                ("sample_order", C.c_int32), ("sample_tile_runs", C.c_int32)]
+                ("sample_order", C.c_int32), ("sample_tile_runs", C.c_int32),
+                ("mark_slices_max", C.c_int32), ("mark_slice_chunks", C.c_int32),
+                ("mark_block", C.c_int32)]
 
 
 TUNING_FIELDS = tuple(name for name, _ in gg_tuning_t._fields_)

@@ -68,6 +68,8 @@ int main() {
   S(gg_tuning_t) F(gg_tuning_t, gather_blocks) F(gg_tuning_t, gather_loads)
   F(gg_tuning_t, stage_blocks) F(gg_tuning_t, stage_host_blocks) F(gg_tuning_t, emit_blocks)
   F(gg_tuning_t, hot_max_chunks) F(gg_tuning_t, bytemap_max_mb) F(gg_tuning_t, sample_order) F(gg_tuning_t, sample_tile_runs)
+  F(gg_tuning_t, mark_slices_max) F(gg_tuning_t, mark_slice_chunks)
+  F(gg_tuning_t, mark_block)
   return 0;
 }
 """
@@ -109,10 +111,18 @@ def test_host_helpers(gg):
     assert gg.gg_ws_bucket(0, 4) > 0 and gg.gg_ws_gather(0, 1, 4) > 0 and gg.gg_ws_stage(0, 4) > 0
     # tuning that changes workspace layouts changes the sizes; bad tuning sizes nothing
     N, W = 2_450_000, 16
-    assert gg.gg_ws_sample(N, W) > gg.gg_ws_sample(N, W, gg.make_tuning(bytemap_max_mb=-1))
+    assert gg.gg_ws_sample(N, W, gg.make_tuning(mark_slices_max=-1)) > \
+        gg.gg_ws_sample(N, W, gg.make_tuning(bytemap_max_mb=-1)) == gg.gg_ws_sample(N, W)
     assert gg.gg_ws_sample(N, W, gg.make_tuning(bytemap_max_mb=1)) == \
         gg.gg_ws_sample(N, W, gg.make_tuning(bytemap_max_mb=-1))
     assert gg.gg_ws_sample(N, W) < gg.gg_ws_sample(N, W, gg.make_tuning(sample_order=1))
+    # 2.45M nodes: 38 chunks of 65,536 ids, 5 slices of 8 chunks per batch;
+    # marks through LDS leave the byte map out
+    assert gg.gg_ws_sample(N, W, gg.make_tuning(mark_slices_max=5)) == \
+        gg.gg_ws_sample(N, W, gg.make_tuning(bytemap_max_mb=-1))
+    assert gg.gg_ws_sample(N, W, gg.make_tuning(mark_slices_max=4)) == \
+        gg.gg_ws_sample(N, W, gg.make_tuning(mark_slices_max=-1)) > \
+        gg.gg_ws_sample(N, W, gg.make_tuning(bytemap_max_mb=-1))
     assert gg.gg_ws_hotset(N, W, gg.make_tuning(hot_max_chunks=4)) < gg.gg_ws_hotset(N, W)
     assert gg.gg_ws_gather(10**6, 1, 4, gg.make_tuning(gather_blocks=64)) < \
         gg.gg_ws_gather(10**6, 1, 4)
@@ -126,16 +136,18 @@ def test_host_helpers(gg):
     # W = 32 runs without it and a 16-batch window with it), and fewer
     # segments may launch more gather blocks in all (1024 = 1 x 1024, but
     # 3 x 341)
-    for t in (None, gg.make_tuning(bytemap_max_mb=64), gg.make_tuning(bytemap_max_mb=8),
-              gg.make_tuning(bytemap_max_mb=64, sample_order=1)):
+    for t in (None, gg.make_tuning(bytemap_max_mb=64, mark_slices_max=-1),
+              gg.make_tuning(bytemap_max_mb=8, mark_slices_max=-1),
+              gg.make_tuning(bytemap_max_mb=64, sample_order=1, mark_slices_max=-1),
+              gg.make_tuning(bytemap_max_mb=64, mark_slices_max=4)):
         for N in (60_001, 2_450_000):
             for W in (1, 3, 16, 32, 64):
                 big = gg.gg_ws_sample(N, W, t)
                 assert all(gg.gg_ws_sample(N, w, t) <= big for w in range(1, W + 1)), (N, W)
                 big = gg.gg_ws_hotset(N, W, t)
                 assert all(gg.gg_ws_hotset(N, w, t) <= big for w in range(1, W + 1)), (N, W)
-    assert gg.gg_ws_sample(2_450_000, 32, gg.make_tuning(bytemap_max_mb=64)) >= \
-        2_450_000 * 16
+    assert gg.gg_ws_sample(2_450_000, 32, gg.make_tuning(bytemap_max_mb=64,
+                                                         mark_slices_max=-1)) >= 2_450_000 * 16
     for t in (None, gg.make_tuning(gather_blocks=1000), gg.make_tuning(gather_blocks=96)):
         for n_cap in (1, 5000, 10**6, 4 * 10**7):
             for nseg in (1, 3, 7, 16, 64):
@@ -228,7 +240,10 @@ def test_bad_arguments_are_rejected_on_the_host(gg):
                        ("gather_loads", 3), ("stage_blocks", -2), ("stage_host_blocks", -2),
                        ("emit_blocks", 513), ("hot_max_chunks", 4097), ("bytemap_max_mb", -2),
                        ("sample_tile_runs", 3), ("sample_tile_runs", 128),
-                       ("sample_tile_runs", -1), ("sample_order", 3), ("sample_order", -1)]:
+                       ("sample_tile_runs", -1), ("sample_order", 3), ("sample_order", -1),
+                       ("mark_slices_max", -2), ("mark_slices_max", 4097),
+                       ("mark_slice_chunks", -1), ("mark_slice_chunks", 9),
+                       ("mark_block", 128), ("mark_block", 512)]:
         tune = gg.make_tuning(**{field: bad})
         with pytest.raises(gg.GGError):                                  # tuning out of range
             gg.gg_gather_batch(t, t.data_ptr(), 1, 10, part, feat, t, 256, 10, t, t, 256,

@@ -209,18 +209,22 @@ def test_wide_rows_with_misses(n_hot, tile):
 
 
 @pytest.mark.parametrize("fields", [
-    dict(bytemap_max_mb=-1), dict(bytemap_max_mb=1),
+    dict(mark_slices_max=-1, bytemap_max_mb=-1), dict(mark_slices_max=-1, bytemap_max_mb=1),
+    dict(mark_slices_max=-1),
     dict(gather_loads=2, gather_blocks=8), dict(gather_loads=4), dict(gather_loads=8, tile_rows=3),
     dict(stage_blocks=1, tile_rows=7), dict(stage_blocks=3, emit_blocks=1, hot_max_chunks=1),
     dict(sample_order=1), dict(sample_order=2), dict(sample_order=2, sample_tile_runs=1),
-    dict(sample_order=2, sample_tile_runs=64), dict(sample_order=1, bytemap_max_mb=-1)])
+    dict(sample_order=2, sample_tile_runs=64),
+    dict(sample_order=1, bytemap_max_mb=-1, mark_slices_max=-1),
+    dict(sample_order=2, mark_slices_max=-1)])
 def test_launch_tuning_leaves_results_unchanged(fields):
-    """Launch tuning changes only how the work is spread: the sampler's last
-    hop with atomic marks instead of the byte map (as on the 111M-node
-    graph), the sampler in node tiles at the last hop or at every hop
-    (sized per hop, or fixed at 256 or 16,384 ids), gathers with 2, 4 or 8 loads in flight and few blocks (many tiles
-    per wave), staging by one or three blocks, one hot-set chunk and one
-    free-list block.  Full restage, then in-place staging over three
+    """Launch tuning changes only how the work is spread: the sampler's
+    marks through LDS (the default here), by atomic ORs (as on the
+    111M-node graph) or, at the last hop, into the byte map; the sampler in
+    node tiles at the last hop or at every hop (sized per hop, or fixed at
+    256 or 16,384 ids); gathers with 2, 4 or 8 loads in flight and few
+    blocks (many tiles per wave), staging by one or three blocks, one
+    hot-set chunk and one free-list block.  Full restage, then in-place staging over three
     windows, each against the oracle with a budget that leaves misses."""
     log(f"small: tuning {fields}")
     from paper_2606_02916_amd import gg
@@ -233,12 +237,15 @@ def test_launch_tuning_leaves_results_unchanged(fields):
         w.run_and_compare(k)
 
 
-@pytest.mark.parametrize("fields", [dict(), dict(bytemap_max_mb=-1), dict(sample_order=1)])
+@pytest.mark.parametrize("fields", [
+    dict(), dict(mark_slices_max=-1), dict(mark_slices_max=-1, bytemap_max_mb=-1),
+    dict(sample_order=1), dict(sample_order=1, mark_slices_max=-1)])
 def test_sample_window_in_two_parts_across_streams(fields):
     """gg_sample_window_part: the bits part on one stream, then (after an
     event) the last level's compaction on another; the bit sets are final
-    after the first part (the byte map folded in, when one is used), and
-    after the second every output equals the oracle's."""
+    after the first part (marked through LDS, or the byte map folded in,
+    when either is used), and after the second every output equals the
+    oracle's."""
     log(f"small: sampling in two parts on two streams, tuning {fields}")
     import torch as T
     from oracle import ggref
@@ -323,6 +330,54 @@ def test_capacity_overflow_is_flagged_and_clamped():
     assert int(p.need[0].item()) > 1000
     assert bool((small[1000:] == 0x7EADBEEF).all())
     assert int(p.frontier_off.max().item()) <= 1000
+
+
+@pytest.mark.parametrize("frac", [0.3, 0.8])
+def test_slot_overflow_leaves_the_same_sets_under_every_marking(frac):
+    """Neighbour slots too few for the window (a capacity of 30m + 1, a
+    multiple of no fan-out, so an entry straddles it): the status bit is
+    raised, nothing is written past the capacity, and marks through LDS
+    (which read the written slots of complete entries only), atomic ORs and
+    the last hop's byte map leave the same bit sets, lists and offsets."""
+    log(f"small: neighbour-slot capacity {frac} of the need, three ways of marking")
+    import torch as T
+    from paper_2606_02916_amd import gg
+    w = world(synth.instance("small"))
+    p = w.pipe
+    N, L = w.inst.wl.num_nodes, len(w.fanout)
+    seeds, so, b0 = w.window_inputs(0)
+    sd = T.from_numpy(seeds).to(w.dev)
+    Wk = len(so) - 1
+    gg.gg_sample_window(p.csr, sd, so, Wk, list(w.fanout), L, 0, 0, b0, p.wsample, p.status,
+                        p.ws)
+    T.cuda.synchronize()
+    assert p.read_status() == 0
+    need = int(p.need[1].item())
+    ncap = int(need * frac) // 30 * 30 + 1
+    assert 0 < ncap < need and all(ncap % k for k in w.fanout)
+    guard = 4096
+    outs = []
+    for fields in (dict(), dict(mark_slices_max=-1), dict(mark_slices_max=-1, bytemap_max_mb=-1)):
+        tune = gg.make_tuning(**fields)
+        ws = T.empty(gg.gg_ws_sample(N, Wk, tune), dtype=T.uint8, device=w.dev)
+        nb = T.full((ncap + guard,), 0x7EADBEEF, dtype=T.int32, device=w.dev)
+        wsm = gg.make_wsample(p.frontier_ids, p.frontier_off, nb[:ncap], p.nbr_off,
+                              p.frontier_bits, p.need)
+        p.frontier_ids.fill_(-7)
+        p.status.zero_()
+        gg.gg_sample_window(p.csr, sd, so, Wk, list(w.fanout), L, 0, 0, b0, wsm, p.status, ws,
+                            tuning=tune)
+        T.cuda.synchronize()
+        assert p.read_status() & gg.DEV_CAPACITY, fields
+        assert bool((nb[ncap:] == 0x7EADBEEF).all()), fields
+        foff = p.frontier_off[:(L + 1) * Wk + 1].cpu().numpy()
+        outs.append((p.frontier_bits[:Wk * p.wpb].cpu().numpy(), foff,
+                     p.frontier_ids[:int(foff[-1])].cpu().numpy(),
+                     p.nbr_off[:L * Wk + 1].cpu().numpy(), nb[:ncap].cpu().numpy(),
+                     p.need.cpu().numpy()))
+    for o in outs[1:]:
+        for x, y in zip(outs[0], o):
+            assert np.array_equal(x, y)
 
 
 @pytest.mark.timeout(900)
@@ -452,7 +507,7 @@ def test_short_last_window_takes_the_byte_map():
     import torch as T
     from paper_2606_02916_amd import LookaheadPipeline, gg
     from tests.gpu_util import LookaheadOracle
-    tune = gg.make_tuning(bytemap_max_mb=1)
+    tune = gg.make_tuning(bytemap_max_mb=1, mark_slices_max=-1)
     inst = synth.instance("small")
     wl, W = inst.wl, 20
     boff = inst.batch_off
