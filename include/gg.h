@@ -199,6 +199,12 @@ typedef struct gg_tuning {
                                 (default 8) */
   int32_t mark_block;        /* lanes of a mark block: 256 (default) or 1024; a block keeps
                                 64 KB of slot loads in flight */
+  int32_t mark_min_slots;    /* a hop before the last marks through LDS slices only when its
+                                bound on neighbour slots per batch, min(N, B * prod_{i<l}
+                                (k_i + 1)) * k_l with B the largest batch, is at least this
+                                (a smaller hop marks with atomics, which cost less than a
+                                pass over the slices); 0: the words of a slice (16,384 by
+                                default); -1: every hop */
 } gg_tuning_t;
 #define GG_SAMPLE_BATCH_ORDER 0
 #define GG_SAMPLE_TILES_LAST 1

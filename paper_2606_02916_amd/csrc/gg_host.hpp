@@ -89,6 +89,7 @@ struct Tune {
   int32_t mark_slices_max;    // -1: marks by atomics (or the byte map)
   int32_t mark_slice_chunks;  // 8 KB chunks of a batch's set per mark slice
   int32_t mark_block;         // lanes per mark block: 256 or 1024
+  int64_t mark_min_slots;     // a hop before the last: LDS marks from this slot bound per batch
 };
 
 // Resolves `t` (NULL: every default) into *out; GG_ERR_ARG (with a message)

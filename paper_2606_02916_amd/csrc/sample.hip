@@ -914,6 +914,22 @@ int sample_window_impl(const gg_csr_t* csr, const int32_t* seeds_d, const int64_
       if (l < L) lev = std::min<int64_t>(lev * (fanout_h[l] + 1), N);
     }
   }
+  // Hop lv - 1 (making level lv) marks through LDS slices when the graph's
+  // sets split into few slices and, before the last hop, when its bound on
+  // slots per batch reaches the tuning's minimum.
+  int64_t bbound[GG_MAX_LAYERS + 1];   // entries of the largest batch, by level
+  {
+    int64_t lev = std::min<int64_t>(max_batch, N);
+    for (int l = 0; l <= L; ++l) {
+      bbound[l] = lev;
+      if (l < L) lev = std::min<int64_t>(lev * (fanout_h[l] + 1), N);
+    }
+  }
+  auto lds_marks = [&](int lv) {
+    if (!slices) return false;
+    if (lv == L) return true;
+    return bbound[lv - 1] * fanout_h[lv - 1] >= tune.mark_min_slots;
+  };
   const int64_t nruns = wpb / kWordsPerThread;
   int64_t ntab_prev = 0;     // tiles of the previous level's table (0: none)
   int32_t gmax_prev = 1;     // table tiles a sampler tile may join
@@ -934,7 +950,7 @@ int sample_window_impl(const gg_csr_t* csr, const int32_t* seeds_d, const int64_
       a.key1 = (uint32_t)(rng_seed >> 32);
       a.epoch = (uint32_t)epoch;
       a.bytemap = lv == L ? sw.map : nullptr;
-      a.nomark = slices ? 1 : 0;
+      a.nomark = lds_marks(lv) ? 1 : 0;
       const int64_t bnd = std::min<int64_t>(bound[lv - 1], out->frontier_cap);
       int rc = csr->row_ptr_bits == 64
                    ? launch_sample<int64_t>(csr, out, sw, status_d, a, bnd, ntab_prev, gmax_prev,
@@ -951,7 +967,7 @@ int sample_window_impl(const gg_csr_t* csr, const int32_t* seeds_d, const int64_
     // the hot set needs, so it belongs to the bits part then; after atomic
     // marks it belongs to the compaction
     const bool count_here = last ? ((sw.map || slices) ? do_bits : do_last) : do_bits;
-    if (!cnt_only && count_here && slices && lv > 0) {
+    if (!cnt_only && count_here && lv > 0 && lds_marks(lv)) {
       MarkArgs ma;
       ma.N = N;
       ma.wpb = wpb;

@@ -29,13 +29,25 @@ from . import gg
 LOOKAHEAD_BYTEMAP_MAX_MB = 8
 
 
-def last_hop_density(num_nodes, fanout, max_batch):
-    """Bound on the last hop's draws per batch over the node count:
-    min(N, B * prod_{i<L-1}(k_i + 1)) * k_{L-1} / N."""
+def _last_frontier_bound(num_nodes, fanout, max_batch):
+    """min(N, B * prod_{i<L-1}(k_i + 1)): the bound on a batch's entries at
+    the last hop."""
     f = min(num_nodes, max_batch)
     for k in fanout[:-1]:
         f = min(num_nodes, f * (k + 1))
-    return f * fanout[-1] / max(num_nodes, 1)
+    return f
+
+
+def last_hop_density(num_nodes, fanout, max_batch):
+    """Bound on the last hop's draws per batch over the node count:
+    min(N, B * prod_{i<L-1}(k_i + 1)) * k_{L-1} / N."""
+    return _last_frontier_bound(num_nodes, fanout, max_batch) * fanout[-1] / max(num_nodes, 1)
+
+
+def last_hop_sharing(num_nodes, fanout, max_batch, W):
+    """Bound on the number of a window's batches whose last-hop frontier
+    holds a given node: W * min(N, B * prod_{i<L-1}(k_i + 1)) / N."""
+    return W * _last_frontier_bound(num_nodes, fanout, max_batch) / max(num_nodes, 1)
 
 
 def _bucket_flags(part):
@@ -153,6 +165,12 @@ class FetchPipeline:
         self.csr = gg.make_csr(row_ptr, col_idx)
         self.part = gg.make_part(self.P, part_kind, local_owner, self.N, range_start)
         self.feat = gg.make_feat(self.row_bytes, shards, [self.stride] * self.P, shard_rows)
+        # Alone on the chip the sampler's mark blocks may take whole CUs:
+        # 1,024 lanes (the library's 256 leave room beside a running gather)
+        # took the 2.45M-node window from 0.509 to 0.492 ms.  A caller's
+        # tuning replaces this one as a whole.
+        if tuning is None:
+            tuning = gg.make_tuning(mark_block=1024)
         self.tuning = tuning
         self.geo = _Geometry(self.N, self.W, self.fanout, max_batch, self.P, local_owner,
                              shard_rows, self.stride, self.cache_stride, tuning)
@@ -434,21 +452,26 @@ class LookaheadPipeline:
         self.part = gg.make_part(self.P, part_kind, local_owner, self.N, range_start)
         self.feat = gg.make_feat(self.row_bytes, shards, [self.stride] * self.P, shard_rows)
         self.shards = shards
-        # Beside the gather, traffic decides: the last hop samples in node
-        # tiles (the batches share the CSR lines they fetch).  A sparse last
-        # hop (fewer draws per batch than nodes, by the bound) marks with
-        # atomics unless its byte map stays small enough to live in the
-        # caches: the map's fold pass costs more than the atomics it saves
-        # (2.45M nodes, batch 1024, density 0.37: 0.444 -> 0.431 ms per
-        # window).  A dense one keeps the map: at batch 4096 (density 1.47)
-        # the map took W = 16 from 0.86 to 0.77 ms per window.  The
-        # sequential driver, alone on the chip, keeps the library's
-        # defaults, which are faster there.  A caller's tuning replaces
-        # this one as a whole.
+        # Beside the gather, traffic decides.  The last hop samples in node
+        # tiles when the window's batches share its frontier (a node in at
+        # least two of them, by the bound), so that they share the CSR lines
+        # they fetch: at batch 4096 on the 2.45M-node graph (4.7 batches)
+        # 0.703 -> 0.674 ms per window; at batch 1024 (1.2) batch order is
+        # faster, 0.401 -> 0.394, and on the 233K-node graph (0.9), 0.335 ->
+        # 0.330.  Where the sampler marks with atomics (sets too large for
+        # LDS slices), a sparse last hop (fewer draws per batch than nodes,
+        # by the bound) marks with atomics unless its byte map stays small
+        # enough to live in the caches: the map's fold pass costs more than
+        # the atomics it saves (batch 1024, density 0.37: 0.444 -> 0.431
+        # ms); a dense one keeps the map (batch 4096, density 1.47: W = 16
+        # from 0.86 to 0.77 ms).  The sequential driver, alone on the chip,
+        # keeps the library's defaults.  A caller's tuning replaces this one
+        # as a whole.
         if tuning is None:
             dense = last_hop_density(self.N, self.fanout, max_batch) >= 1.0
+            shared = last_hop_sharing(self.N, self.fanout, max_batch, self.W) >= 2.0
             tuning = gg.make_tuning(
-                sample_order=gg.GG_SAMPLE_TILES_LAST,
+                sample_order=gg.GG_SAMPLE_TILES_LAST if shared else gg.GG_SAMPLE_BATCH_ORDER,
                 **({} if dense else {"bytemap_max_mb": LOOKAHEAD_BYTEMAP_MAX_MB}))
         self.tuning = tuning
         self.geo = g = _Geometry(self.N, self.W, self.fanout, max_batch, self.P, local_owner,

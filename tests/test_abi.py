@@ -69,7 +69,7 @@ int main() {
   F(gg_tuning_t, stage_blocks) F(gg_tuning_t, stage_host_blocks) F(gg_tuning_t, emit_blocks)
   F(gg_tuning_t, hot_max_chunks) F(gg_tuning_t, bytemap_max_mb) F(gg_tuning_t, sample_order) F(gg_tuning_t, sample_tile_runs)
   F(gg_tuning_t, mark_slices_max) F(gg_tuning_t, mark_slice_chunks)
-  F(gg_tuning_t, mark_block)
+  F(gg_tuning_t, mark_block) F(gg_tuning_t, mark_min_slots)
   return 0;
 }
 """
@@ -243,7 +243,8 @@ def test_bad_arguments_are_rejected_on_the_host(gg):
                        ("sample_tile_runs", -1), ("sample_order", 3), ("sample_order", -1),
                        ("mark_slices_max", -2), ("mark_slices_max", 4097),
                        ("mark_slice_chunks", -1), ("mark_slice_chunks", 9),
-                       ("mark_block", 128), ("mark_block", 512)]:
+                       ("mark_block", 128), ("mark_block", 512),
+                       ("mark_min_slots", -2)]:
         tune = gg.make_tuning(**{field: bad})
         with pytest.raises(gg.GGError):                                  # tuning out of range
             gg.gg_gather_batch(t, t.data_ptr(), 1, 10, part, feat, t, 256, 10, t, t, 256,
@@ -288,8 +289,9 @@ def test_lookahead_byte_map_choice_follows_last_hop_density(gg):
     """The look-ahead driver keeps the sampler's byte map for a dense last
     hop (at least as many draws per batch as nodes, by the frontier bound)
     and caps it otherwise: the bound is min(N, B * prod_{i<L-1}(k_i + 1))
-    draws of k_{L-1} each."""
-    from paper_2606_02916_amd.window import last_hop_density
+    draws of k_{L-1} each.  It samples the last hop in node tiles when at
+    least two batches share a frontier node, by the same bound."""
+    from paper_2606_02916_amd.window import last_hop_density, last_hop_sharing
     assert last_hop_density(2_450_000, [15, 10, 5], 1024) == 1024 * 16 * 11 * 5 / 2_450_000
     assert last_hop_density(2_450_000, [15, 10, 5], 4096) == 4096 * 16 * 11 * 5 / 2_450_000
     assert last_hop_density(1000, [15, 10, 5], 512) == 1000 * 5 / 1000    # capped at N
@@ -300,3 +302,9 @@ def test_lookahead_byte_map_choice_follows_last_hop_density(gg):
     lev2 = min(2_450_000, 4096 * 16 * 11)
     assert nc == 4096 * 15 + 4096 * 16 * 10 + lev2 * 5
     assert last_hop_density(2_450_000, [15, 10, 5], 4096) == lev2 * 5 / 2_450_000
+    # batches sharing a last-hop node, by the bound: W * min(N, ...) / N
+    assert last_hop_sharing(2_450_000, [15, 10, 5], 4096, 16) == 16 * lev2 / 2_450_000 > 2
+    assert last_hop_sharing(2_450_000, [15, 10, 5], 1024, 16) == \
+        16 * 1024 * 16 * 11 / 2_450_000 < 2
+    assert last_hop_sharing(233_000, [25, 10], 1024, 8) == 8 * 1024 * 26 / 233_000 < 2
+    assert last_hop_sharing(1000, [15, 10, 5], 512, 4) == 4.0                # capped at N

@@ -216,11 +216,14 @@ def test_wide_rows_with_misses(n_hot, tile):
     dict(sample_order=1), dict(sample_order=2), dict(sample_order=2, sample_tile_runs=1),
     dict(sample_order=2, sample_tile_runs=64),
     dict(sample_order=1, bytemap_max_mb=-1, mark_slices_max=-1),
-    dict(sample_order=2, mark_slices_max=-1)])
+    dict(sample_order=2, mark_slices_max=-1),
+    dict(mark_min_slots=-1), dict(mark_min_slots=10**9), dict(mark_block=256),
+    dict(mark_block=1024, mark_min_slots=-1, sample_order=2)])
 def test_launch_tuning_leaves_results_unchanged(fields):
     """Launch tuning changes only how the work is spread: the sampler's
-    marks through LDS (the default here), by atomic ORs (as on the
-    111M-node graph) or, at the last hop, into the byte map; the sampler in
+    marks through LDS (in blocks of 256 or 1,024 lanes, at every hop or at
+    the last only), by atomic ORs (as on the 111M-node graph) or, at the
+    last hop, into the byte map; the sampler in
     node tiles at the last hop or at every hop (sized per hop, or fixed at
     256 or 16,384 ids); gathers with 2, 4 or 8 loads in flight and few
     blocks (many tiles per wave), staging by one or three blocks, one
