@@ -274,6 +274,10 @@ def main():
     ap.add_argument("--tune", default=None, metavar="FIELD=VALUE,...",
                     help="launch tuning passed to every call (gg_tuning_t fields, e.g. "
                          "gather_blocks=768,gather_loads=8); results do not change")
+    ap.add_argument("--stage-apart", type=int, default=None, choices=(0, 1),
+                    help="look-ahead driver: staging on a stream of its own (1) or after the "
+                         "build on the build stream (0); default: its own only with shards in "
+                         "host memory")
     ap.add_argument("--sets", type=int, default=None,
                     help="buffer sets of the look-ahead pipeline (how far building may run ahead)")
     ap.add_argument("--wsweep", default=None,
@@ -365,7 +369,9 @@ def main():
     inplace_cache = args.pipeline in ("lookahead", "inplace")
     tuning = parse_tuning(args.tune)
     if look:
-        pipe = LookaheadPipeline(*pargs, device=dev, nsets=args.sets, tuning=tuning)
+        pipe = LookaheadPipeline(*pargs, device=dev, nsets=args.sets, tuning=tuning,
+                                 stage_apart=None if args.stage_apart is None
+                                 else bool(args.stage_apart))
     else:
         pipe = FetchPipeline(*pargs, device=dev, delta=args.pipeline == "delta",
                              inplace=args.pipeline == "inplace", tuning=tuning)
@@ -470,14 +476,16 @@ def main():
     # later of its window's staging end (events[4]) and the previous
     # gather's end, and every marker left out of that queue saves a few us.
     stage_on_build = look and pipe.stage_stream is pipe.build_stream
-    # The build stream then carries the critical chain (build, staging) and
-    # each event on it costs a few us too: by default only the build's end
-    # and the staging's end are recorded there, and a build is taken to run
-    # from the previous window's staging end (--breakdown: every call).
-    lean = stage_on_build and not args.breakdown
+    # The build stream carries the critical chain and each event on it costs
+    # a few us too: by default only the build's end and the staging's end
+    # are recorded, and a build is taken to run from the previous window's
+    # staging end (staging on the build stream) or build end (staging on a
+    # stream of its own); a gather, from the later of its staging's end and
+    # the previous gather's end (--breakdown: every call).
+    lean = look and not args.breakdown
     evs = [[None if lean and j < 3 else mk() for j in range(5 if look else 6)]
            for _ in range(K)]
-    gevs = [[(None if stage_on_build else mk(), mk()) for _ in range(W if pb else 1)]
+    gevs = [[(None if lean or stage_on_build else mk(), mk()) for _ in range(W if pb else 1)]
             for _ in range(K)]
     cevs = [(mk(), mk()) for _ in range(K)] if cons else [None] * K
     order = [(args.warmup + i) % nwin for i in range(K)]
@@ -517,7 +525,7 @@ def main():
         e = evs[i]
         if lean:
             if i > 0:
-                stage_ms["build"].append(evs[i - 1][4].elapsed_time(e[3]))
+                stage_ms["build"].append(evs[i - 1][4 if stage_on_build else 3].elapsed_time(e[3]))
         else:
             for name, (a, b) in zip(stage_ms, [(0, 1), (1, 2), (2, 3)]):
                 stage_ms[name].append(e[a].elapsed_time(e[b]))
@@ -607,7 +615,8 @@ def main():
                      "bytes_per_launch": int(avg_bytes), "avg_launch_us": round(avg_ms * 1e3, 2),
                      "overlapped": look,
                      "start": ("later of the window's staging end and the previous gather's end "
-                               "(HIP events)" if stage_on_build else "HIP event before the launch"),
+                               "(HIP events)" if gevs[0][0][0] is None
+                               else "HIP event before the launch"),
                      "isolated": {"achieved": round(iso_achieved, 1),
                                   "frac": round(iso_achieved / HBM_PEAK_GBS, 4),
                                   "avg_launch_us": round(iso_avg_ms * 1e3, 2),

@@ -413,13 +413,13 @@ class LookaheadPipeline:
     so a window costs about the longer of the two chains instead of their
     sum.
 
-    With every shard in device memory, staging follows the build on the
-    build stream and the fetch stream only gathers: staging window k+1
-    (which writes its own buffer set and reads window k's cache) runs beside
-    window k's gather.  When shards live in pinned host memory, staging is
-    bound by PCIe rather than HBM and would hold up the next build, so it
-    runs on the fetch stream and the gather gets a stream of its own,
-    running beside the next window's staging.
+    Staging follows the build on the build stream and the fetch stream only
+    gathers: staging window k+1 (which writes its own buffer set and reads
+    window k's cache) runs beside window k's gather.  Where staging would
+    hold up the next build (stage_apart: by default when shards live in
+    pinned host memory, where staging is bound by PCIe, and when the build
+    is the longer chain), it runs on the fetch stream instead and the gather
+    gets a stream of its own, running beside the next window's staging.
 
     The cache is one persistent buffer (gg_stage_inplace): a row window k
     shares with window k-1 stays in its slot, and only the delta is
@@ -437,7 +437,8 @@ class LookaheadPipeline:
 
     def __init__(self, row_ptr, col_idx, num_parts, part_kind, local_owner, range_start, shards,
                  shard_rows, row_bytes, stride, W, fanout, max_batch, n_hot=-1, device=None,
-                 cache_stride=None, nsets=None, hot_frac=None, tuning=None, split_last=None):
+                 cache_stride=None, nsets=None, hot_frac=None, tuning=None, split_last=None,
+                 stage_apart=None):
         self.device = torch.device(device if device is not None else "cuda")
         self.N = int(row_ptr.numel() - 1)
         self.W = int(W)
@@ -467,9 +468,9 @@ class LookaheadPipeline:
         # from 0.86 to 0.77 ms).  The sequential driver, alone on the chip,
         # keeps the library's defaults.  A caller's tuning replaces this one
         # as a whole.
+        shared = last_hop_sharing(self.N, self.fanout, max_batch, self.W) >= 2.0
         if tuning is None:
             dense = last_hop_density(self.N, self.fanout, max_batch) >= 1.0
-            shared = last_hop_sharing(self.N, self.fanout, max_batch, self.W) >= 2.0
             tuning = gg.make_tuning(
                 sample_order=gg.GG_SAMPLE_TILES_LAST if shared else gg.GG_SAMPLE_BATCH_ORDER,
                 **({} if dense else {"bytemap_max_mb": LOOKAHEAD_BYTEMAP_MAX_MB}))
@@ -514,7 +515,17 @@ class LookaheadPipeline:
         self.status = torch.zeros(1, dtype=torch.int32, device=dev)
         self.build_stream = torch.cuda.Stream(device=dev)
         self.fetch_stream = torch.cuda.Stream(device=dev)
-        if on_host:
+        # Staging gets a stream of its own when it would otherwise hold up the
+        # next build: with shards in host memory (PCIe-bound), and where the
+        # build is the longer chain, i.e. three or more hops whose last
+        # frontier the batches barely share (2.45M-node graph, batch 1024:
+        # 0.394 -> 0.374 ms per window).  Where the gather is the longer
+        # chain, staging beside it only slows it (233K-node graph, two hops:
+        # 0.330 -> 0.342; batch 4096: 0.677 -> 0.715).
+        if stage_apart is None:
+            stage_apart = on_host or (self.L >= 3 and not shared)
+        self.stage_apart = bool(stage_apart)
+        if self.stage_apart:
             self.stage_stream = self.fetch_stream
             self.gather_stream = torch.cuda.Stream(device=dev)
         else:

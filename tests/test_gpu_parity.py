@@ -407,8 +407,10 @@ def rows_from_shards(inst, ids, rb):
 def test_lookahead_as_benchmarked(name):
     """The benchmark's launch configuration: the look-ahead driver with its
     default buffer sets (three with every shard in HBM; two on the
-    Papers100M share, whose remote shards sit in pinned host memory, with
-    staging on the fetch stream and the gather on a third stream) and only
+    Papers100M share, whose remote shards sit in pinned host memory) and
+    streams (staging on the fetch stream and the gather on a third stream on
+    that share and on the 2.45M-node graph, whose build is the longer
+    chain; staging after the build on the 233K-node graph) and only
     a gather end event per window, over four consecutive windows (window
     k+1 is enqueued before window k is read).  Every window against the
     oracle element by element: every batch's frontiers, neighbour slots and
@@ -429,7 +431,8 @@ def test_lookahead_as_benchmarked(name):
                              wl.fanout, wl.batch_size, device=dev)
     host = wl.remote_on_host
     assert look.nsets == (2 if host else 3)
-    assert (look.stage_stream is look.build_stream) != host
+    assert look.stage_apart == (host or name == "large_sparse")
+    assert (look.stage_stream is look.build_stream) != look.stage_apart
     orc = LookaheadOracle(inst, look)
     seeds_d = T.from_numpy(inst.seeds).to(dev)
     boff, rb = inst.batch_off, wl.row_bytes
@@ -781,13 +784,15 @@ def test_inplace_staging_out_of_slots_leaves_misses(short_by):
     ("tiny", -1, 1, 2, False, None, None), ("small", -1, None, None, False, "end", None),
     ("tiny", 2000, 1, 3, False, "end", None), ("small", 3000, None, 4, False, "both", None),
     ("small", -1, None, None, True, "both", None), ("small", 3000, None, 3, True, "end", None),
+    ("small", 3000, None, None, "apart", "end", None), ("tiny", -1, 1, 2, "apart", "both", None),
     ("tiny", 700, 2, None, False, "end", (1036, 1040)),
     ("small", 3000, None, None, False, "end", (2408, 2416))])
 def test_lookahead_pipeline_equals_sequential(name, n_hot, W, nsets, host, gev, rows):
     """The look-ahead driver against the sequential delta-staging driver,
     window by window: with shards in device memory (staging on the build
-    stream) and with the remote shards in pinned host memory (staging on
-    the fetch stream, gathers on a third stream); without gather events,
+    stream, or on a stream of its own: "apart") and with the remote shards
+    in pinned host memory (staging on the fetch stream, gathers on a third
+    stream); without gather events,
     with both, and with only the end event, which then also releases the
     buffer set (the benchmark's configuration).  Rows of 1,036 and 2,408
     bytes give the look-ahead's gather (four loads, tiles of as many rows
@@ -799,6 +804,8 @@ def test_lookahead_pipeline_equals_sequential(name, n_hot, W, nsets, host, gev, 
     from paper_2606_02916_amd import LookaheadPipeline
     inst = synth.instance(name)
     wl = inst.wl
+    apart = host == "apart"
+    host = host is True
     kw = {}
     if rows:
         rng = np.random.default_rng(13)
@@ -815,9 +822,11 @@ def test_lookahead_pipeline_equals_sequential(name, n_hot, W, nsets, host, gev, 
     look = LookaheadPipeline(seq.row_ptr_d, seq.col_idx_d, wl.num_parts, wl.part_kind,
                              wl.local_owner, inst.range_start, shards,
                              [s.shape[0] for s in inst.shards], rb, seq.stride, W,
-                             wl.fanout, wl.batch_size, n_hot=n_hot, device=dev, nsets=nsets)
-    assert (look.stage_stream is look.fetch_stream) == host
-    assert (look.gather_stream is look.fetch_stream) != host
+                             wl.fanout, wl.batch_size, n_hot=n_hot, device=dev, nsets=nsets,
+                             stage_apart=True if apart else None)
+    assert look.stage_apart == (host or apart)
+    assert (look.stage_stream is look.fetch_stream) == look.stage_apart
+    assert (look.gather_stream is look.fetch_stream) != look.stage_apart
     nsets = look.nsets
     mk = lambda: T.cuda.Event(enable_timing=True)  # noqa: E731
     seeds_d = T.from_numpy(inst.seeds).to(dev)
