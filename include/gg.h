@@ -205,6 +205,11 @@ typedef struct gg_tuning {
                                 (a smaller hop marks with atomics, which cost less than a
                                 pass over the slices); 0: the words of a slice (16,384 by
                                 default); -1: every hop */
+  int32_t mark_min_batches;  /* a hop marks through LDS slices only in a call of at least this
+                                many batches (a pass takes about as long for one batch as for
+                                many, where atomics and the byte map scale with the batches);
+                                0: 8 where the last hop could use the byte map, else 4;
+                                -1: any */
 } gg_tuning_t;
 #define GG_SAMPLE_BATCH_ORDER 0
 #define GG_SAMPLE_TILES_LAST 1

@@ -98,6 +98,8 @@ int resolve_tuning(const gg_tuning_t* t, Tune* out) {
   GG_REQUIRE(t->mark_block == 0 || t->mark_block == 256 || t->mark_block == 1024,
              "tuning: mark_block %d is not 256 or 1024", t->mark_block);
   GG_REQUIRE(t->mark_min_slots >= -1, "tuning: mark_min_slots %d below -1", t->mark_min_slots);
+  GG_REQUIRE(t->mark_min_batches >= -1 && t->mark_min_batches <= GG_MAX_W,
+             "tuning: mark_min_batches %d outside 1..%d (or -1)", t->mark_min_batches, GG_MAX_W);
   out->tile_rows = t->tile_rows;
   out->gather_blocks = t->gather_blocks ? t->gather_blocks : kGatherBlocksDefault;
   out->gather_loads = t->gather_loads;
@@ -116,6 +118,7 @@ int resolve_tuning(const gg_tuning_t* t, Tune* out) {
   out->mark_slice_chunks = t->mark_slice_chunks ? t->mark_slice_chunks : kMarkSliceChunksDefault;
   out->mark_block = t->mark_block ? t->mark_block : kMarkBlockLanes;
   // default: a slice's words (a smaller hop does not pay for a pass over the slices)
+  out->mark_min_batches = t->mark_min_batches;
   out->mark_min_slots = t->mark_min_slots == 0 ? (int64_t)out->mark_slice_chunks * 2048
                         : t->mark_min_slots < 0 ? 0
                                                 : t->mark_min_slots;

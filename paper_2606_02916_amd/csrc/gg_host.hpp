@@ -90,6 +90,7 @@ struct Tune {
   int32_t mark_slice_chunks;  // 8 KB chunks of a batch's set per mark slice
   int32_t mark_block;         // lanes per mark block: 256 or 1024
   int64_t mark_min_slots;     // a hop before the last: LDS marks from this slot bound per batch
+  int32_t mark_min_batches;   // LDS marks from this many batches; 0: by the alternative
 };
 
 // Resolves `t` (NULL: every default) into *out; GG_ERR_ARG (with a message)

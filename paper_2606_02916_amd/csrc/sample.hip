@@ -91,6 +91,29 @@ inline bool use_slices(int64_t num_nodes, const Tune& tune) {
   return tune.mark_slices_max > 0 && mark_slices(num_nodes, tune) <= tune.mark_slices_max;
 }
 
+// A mark pass runs slices x W blocks, each reading its batch's whole slot
+// list, so its time hardly falls with fewer batches, where atomic marks and
+// the byte map, spread over the chip, take time in proportion to the
+// batches.  At about 8 G slots/s per block against 26 G atomics/s and 80 G
+// byte stores/s for the chip, the pass pays from about 4 batches against
+// atomics and 8 against the byte map (batch 4096 on the 2.45M-node graph:
+// W = 1 0.247 ms per window through LDS, 0.190 with the map; W = 4 0.332
+// against 0.300; W = 16 0.679 against 0.816).  The tuning's
+// mark_min_batches fixes the minimum instead.
+constexpr int kMarkMinBatchesAtomic = 4;
+constexpr int kMarkMinBatchesMap = 8;
+
+inline int32_t min_batches(bool map_instead, const Tune& tune) {
+  if (tune.mark_min_batches != 0) return tune.mark_min_batches < 0 ? 1 : tune.mark_min_batches;
+  return map_instead ? kMarkMinBatchesMap : kMarkMinBatchesAtomic;
+}
+
+// The last hop of a W-batch call marks through LDS slices (else into the
+// byte map, if it fits, or with atomics).
+inline bool last_hop_slices(int64_t num_nodes, int32_t W, const Tune& tune) {
+  return use_slices(num_nodes, tune) && W >= min_batches(use_bytemap(num_nodes, W, tune), tune);
+}
+
 // Largest b in [0, 64) with off[b] <= x, for a table padded with INT64_MAX.
 __device__ __forceinline__ int find_batch(const int64_t* off, int64_t x) {
   int idx = 0;
@@ -265,7 +288,17 @@ struct MarkArgs {
   int32_t W, l, k, nch;
   int32_t vec;      // the slots are 16-byte aligned
   int32_t schunks;  // chunks per slice (the block's dynamic LDS: schunks * 8 KB)
+  int32_t nslices;  // slices per batch
+  int32_t pad_;
 };
+
+// Workgroups go to the chip's 8 XCDs (each with its own L2) round robin by
+// block index.  The grid is numbered so that every slice of a batch lands
+// on one XCD: the batch's slot list then comes from memory once and the
+// other slices' blocks read it from that L2.  Block i: XCD i mod 8, batch
+// (i / 8 / nslices) * 8 + i mod 8, slice (i / 8) mod nslices; a block past
+// the last batch has no work.
+constexpr int kXcds = 8;
 
 // The marks of hop l, with level l+1's counts (as k_bits_count makes them):
 // block (s, b) loads slice s of batch b's set (F_l's bits) into LDS, ORs in
@@ -304,7 +337,9 @@ __device__ __forceinline__ void mark_slices_body(uint32_t* bits, const int32_t* 
                                                             const LevelState* ls, int32_t* cnt,
                                                             Totals tt, MarkArgs a) {
   extern __shared__ uint32_t sl[];
-  const int s = blockIdx.x, b = blockIdx.y;
+  const int xcd = blockIdx.x % kXcds, j = blockIdx.x / kXcds;
+  const int s = j % a.nslices, b = j / a.nslices * kXcds + xcd;
+  if (b >= a.W) return;
   const int c0 = s * a.schunks;
   const int nc = min(a.schunks, a.nch - c0);
   const int nw = nc * kChunkWords;
@@ -736,7 +771,7 @@ size_t sample_ws_layout(int64_t num_nodes, int32_t W, const Tune& tune, char* ba
   s.tot_level = (int64_t)W * kTotLanes * s.ngroups;
   s.tot = cv.take<int32_t>((size_t)(GG_MAX_LAYERS + 1) * s.tot_level);
   s.lvl = cv.take<LevelState>(1);
-  s.map = use_bytemap(num_nodes, W, tune) && !use_slices(num_nodes, tune)
+  s.map = use_bytemap(num_nodes, W, tune) && !last_hop_slices(num_nodes, W, tune)
               ? cv.take<uint8_t>((size_t)W * (size_t)gg_bits_words(num_nodes) * 32)
               : nullptr;
   s.tstart = tune.sample_order != GG_SAMPLE_BATCH_ORDER
@@ -815,17 +850,12 @@ using namespace gg;
 extern "C" size_t gg_ws_sample(int64_t num_nodes, int32_t W, const gg_tuning_t* tuning) {
   Tune tune;
   if (resolve_tuning(tuning, &tune) != GG_OK) return 0;
-  size_t need = sample_ws_layout(num_nodes, W, tune, nullptr, nullptr);
   // A call with fewer batches may take the byte map where W batches do not
-  // (the map grows with the batch count); the layout grows with the batch
-  // count otherwise, so the largest such call bounds the rest.
-  if (W > 1 && !use_bytemap(num_nodes, W, tune) && tune.bytemap_max_bytes >= 0 &&
-      !use_slices(num_nodes, tune)) {
-    const int64_t per_batch = gg_bits_words(num_nodes) * 32;
-    const int64_t wmap = std::min<int64_t>(W - 1, tune.bytemap_max_bytes / per_batch);
-    if (wmap >= 1)
-      need = std::max(need, sample_ws_layout(num_nodes, (int32_t)wmap, tune, nullptr, nullptr));
-  }
+  // (the map grows with the batches, and LDS marks need enough of them),
+  // so the size is the largest over every call of at most W batches.
+  size_t need = sample_ws_layout(num_nodes, W, tune, nullptr, nullptr);
+  for (int32_t w = 1; w < std::min<int32_t>(W, GG_MAX_W); ++w)
+    need = std::max(need, sample_ws_layout(num_nodes, w, tune, nullptr, nullptr));
   return need;
 }
 
@@ -873,6 +903,7 @@ int sample_window_impl(const gg_csr_t* csr, const int32_t* seeds_d, const int64_
   const int64_t wpb = gg_bits_words(N);
   const int32_t nch = (int32_t)(wpb / kChunkWords);
   const bool slices = use_slices(N, tune);
+  const bool last_slices = last_hop_slices(N, W, tune);
 
   SeedOff so;
   for (int b = 0; b <= GG_MAX_W; ++b) so.off[b] = b <= W ? seed_off_h[b] : INT64_MAX;
@@ -926,9 +957,9 @@ int sample_window_impl(const gg_csr_t* csr, const int32_t* seeds_d, const int64_
     }
   }
   auto lds_marks = [&](int lv) {
-    if (!slices) return false;
-    if (lv == L) return true;
-    return bbound[lv - 1] * fanout_h[lv - 1] >= tune.mark_min_slots;
+    if (lv == L) return last_slices;
+    return slices && W >= min_batches(false, tune) &&
+           bbound[lv - 1] * fanout_h[lv - 1] >= tune.mark_min_slots;
   };
   const int64_t nruns = wpb / kWordsPerThread;
   int64_t ntab_prev = 0;     // tiles of the previous level's table (0: none)
@@ -966,7 +997,7 @@ int sample_window_impl(const gg_csr_t* csr, const int32_t* seeds_d, const int64_
     // the last level's count folds the byte map, or makes the marks, which
     // the hot set needs, so it belongs to the bits part then; after atomic
     // marks it belongs to the compaction
-    const bool count_here = last ? ((sw.map || slices) ? do_bits : do_last) : do_bits;
+    const bool count_here = last ? ((sw.map || last_slices) ? do_bits : do_last) : do_bits;
     if (!cnt_only && count_here && lv > 0 && lds_marks(lv)) {
       MarkArgs ma;
       ma.N = N;
@@ -978,7 +1009,9 @@ int sample_window_impl(const gg_csr_t* csr, const int32_t* seeds_d, const int64_
       ma.nch = nch;
       ma.vec = aligned16(out->nbr_ids) ? 1 : 0;
       ma.schunks = tune.mark_slice_chunks;
-      const dim3 mg((unsigned)mark_slices(N, tune), W);
+      ma.nslices = (int32_t)mark_slices(N, tune);
+      ma.pad_ = 0;
+      const dim3 mg((unsigned)(ma.nslices * cdiv(W, kXcds) * kXcds));
       // the slice, and a word per lane of a wavefront for the marks that miss it
       const size_t lds = ((size_t)tune.mark_slice_chunks * kChunkWords + kWave) * 4;
       if (tune.mark_block == 1024)

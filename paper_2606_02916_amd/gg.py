@@ -98,7 +98,8 @@ class gg_tuning_t(C.Structure):
                 ("hot_max_chunks", C.c_int32), ("bytemap_max_mb", C.c_int32),
                 ("sample_order", C.c_int32), ("sample_tile_runs", C.c_int32),
                 ("mark_slices_max", C.c_int32), ("mark_slice_chunks", C.c_int32),
-                ("mark_block", C.c_int32), ("mark_min_slots", C.c_int32)]
+                ("mark_block", C.c_int32), ("mark_min_slots", C.c_int32),
+                ("mark_min_batches", C.c_int32)]
 
 
 TUNING_FIELDS = tuple(name for name, _ in gg_tuning_t._fields_)

@@ -454,12 +454,15 @@ class LookaheadPipeline:
         self.feat = gg.make_feat(self.row_bytes, shards, [self.stride] * self.P, shard_rows)
         self.shards = shards
         # Beside the gather, traffic decides.  The last hop samples in node
-        # tiles when the window's batches share its frontier (a node in at
-        # least two of them, by the bound), so that they share the CSR lines
-        # they fetch: at batch 4096 on the 2.45M-node graph (4.7 batches)
-        # 0.703 -> 0.674 ms per window; at batch 1024 (1.2) batch order is
-        # faster, 0.401 -> 0.394, and on the 233K-node graph (0.9), 0.335 ->
-        # 0.330.  Where the sampler marks with atomics (sets too large for
+        # tiles, so that the batches share the CSR lines they fetch, when it
+        # is a third hop or later (its frontiers are large) or the window's
+        # batches share its frontier (a node in at least two of them, by the
+        # bound): on the 2.45M-node graph at batch 4096 (4.7 batches) 0.703
+        # -> 0.674 ms per window, at batch 1024 (1.2; staging on a stream of
+        # its own) 0.367 -> 0.351 (the last hop's CSR fetches fall from 264
+        # to about 170 MB); on the 233K-node graph (two hops, 0.9 batches)
+        # batch order is faster, 0.335 -> 0.330.  Where the sampler marks
+        # with atomics (sets too large for
         # LDS slices), a sparse last hop (fewer draws per batch than nodes,
         # by the bound) marks with atomics unless its byte map stays small
         # enough to live in the caches: the map's fold pass costs more than
@@ -471,8 +474,9 @@ class LookaheadPipeline:
         shared = last_hop_sharing(self.N, self.fanout, max_batch, self.W) >= 2.0
         if tuning is None:
             dense = last_hop_density(self.N, self.fanout, max_batch) >= 1.0
+            tiles = self.L >= 3 or shared
             tuning = gg.make_tuning(
-                sample_order=gg.GG_SAMPLE_TILES_LAST if shared else gg.GG_SAMPLE_BATCH_ORDER,
+                sample_order=gg.GG_SAMPLE_TILES_LAST if tiles else gg.GG_SAMPLE_BATCH_ORDER,
                 **({} if dense else {"bytemap_max_mb": LOOKAHEAD_BYTEMAP_MAX_MB}))
         self.tuning = tuning
         self.geo = g = _Geometry(self.N, self.W, self.fanout, max_batch, self.P, local_owner,

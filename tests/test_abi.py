@@ -70,6 +70,7 @@ int main() {
   F(gg_tuning_t, hot_max_chunks) F(gg_tuning_t, bytemap_max_mb) F(gg_tuning_t, sample_order) F(gg_tuning_t, sample_tile_runs)
   F(gg_tuning_t, mark_slices_max) F(gg_tuning_t, mark_slice_chunks)
   F(gg_tuning_t, mark_block) F(gg_tuning_t, mark_min_slots)
+  F(gg_tuning_t, mark_min_batches)
   return 0;
 }
 """
@@ -111,18 +112,22 @@ def test_host_helpers(gg):
     assert gg.gg_ws_bucket(0, 4) > 0 and gg.gg_ws_gather(0, 1, 4) > 0 and gg.gg_ws_stage(0, 4) > 0
     # tuning that changes workspace layouts changes the sizes; bad tuning sizes nothing
     N, W = 2_450_000, 16
-    assert gg.gg_ws_sample(N, W, gg.make_tuning(mark_slices_max=-1)) > \
-        gg.gg_ws_sample(N, W, gg.make_tuning(bytemap_max_mb=-1)) == gg.gg_ws_sample(N, W)
-    assert gg.gg_ws_sample(N, W, gg.make_tuning(bytemap_max_mb=1)) == \
-        gg.gg_ws_sample(N, W, gg.make_tuning(bytemap_max_mb=-1))
-    assert gg.gg_ws_sample(N, W) < gg.gg_ws_sample(N, W, gg.make_tuning(sample_order=1))
+    t = gg.make_tuning
+    nomap = gg.gg_ws_sample(N, W, t(bytemap_max_mb=-1))
+    assert gg.gg_ws_sample(N, W, t(bytemap_max_mb=1)) == nomap
+    assert gg.gg_ws_sample(N, W) < gg.gg_ws_sample(N, W, t(sample_order=1))
     # 2.45M nodes: 38 chunks of 65,536 ids, 5 slices of 8 chunks per batch;
-    # marks through LDS leave the byte map out
-    assert gg.gg_ws_sample(N, W, gg.make_tuning(mark_slices_max=5)) == \
-        gg.gg_ws_sample(N, W, gg.make_tuning(bytemap_max_mb=-1))
-    assert gg.gg_ws_sample(N, W, gg.make_tuning(mark_slices_max=4)) == \
-        gg.gg_ws_sample(N, W, gg.make_tuning(mark_slices_max=-1)) > \
-        gg.gg_ws_sample(N, W, gg.make_tuning(bytemap_max_mb=-1))
+    # marks through LDS leave the byte map out: at any batch count with
+    # mark_min_batches = -1; by default only from 8 batches on, so a
+    # 16-batch workspace holds the 7-batch map a shorter window may take
+    assert gg.gg_ws_sample(N, W, t(mark_slices_max=5, mark_min_batches=-1)) == nomap
+    per_batch_map = gg.gg_bits_words(N) * 32
+    assert gg.gg_ws_sample(N, W) >= 7 * per_batch_map
+    assert gg.gg_ws_sample(N, W) < nomap + 8 * per_batch_map
+    assert gg.gg_ws_sample(N, W, t(mark_slices_max=4)) == \
+        gg.gg_ws_sample(N, W, t(mark_slices_max=-1)) >= nomap + 16 * per_batch_map
+    assert gg.gg_ws_sample(N, W, t(mark_min_batches=17)) == \
+        gg.gg_ws_sample(N, W, t(mark_slices_max=-1))
     assert gg.gg_ws_hotset(N, W, gg.make_tuning(hot_max_chunks=4)) < gg.gg_ws_hotset(N, W)
     assert gg.gg_ws_gather(10**6, 1, 4, gg.make_tuning(gather_blocks=64)) < \
         gg.gg_ws_gather(10**6, 1, 4)
@@ -244,7 +249,8 @@ def test_bad_arguments_are_rejected_on_the_host(gg):
                        ("mark_slices_max", -2), ("mark_slices_max", 4097),
                        ("mark_slice_chunks", -1), ("mark_slice_chunks", 9),
                        ("mark_block", 128), ("mark_block", 512),
-                       ("mark_min_slots", -2)]:
+                       ("mark_min_slots", -2), ("mark_min_batches", -2),
+                       ("mark_min_batches", 65)]:
         tune = gg.make_tuning(**{field: bad})
         with pytest.raises(gg.GGError):                                  # tuning out of range
             gg.gg_gather_batch(t, t.data_ptr(), 1, 10, part, feat, t, 256, 10, t, t, 256,

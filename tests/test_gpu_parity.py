@@ -503,23 +503,28 @@ def test_lookahead_split_sampling_matches_oracle(split, host):
     assert look.read_status() == 0
 
 
-def test_short_last_window_takes_the_byte_map():
-    """Workspaces sized for W = 20 batches of the small graph (1.3 MB of
-    byte map, over a 1 MB limit: the last hop marks with atomics) serve the
-    epoch's 4-batch last window, whose 256 KB map fits and is taken: the
+@pytest.mark.parametrize("fields", [dict(bytemap_max_mb=1, mark_slices_max=-1), dict()])
+def test_short_last_window_takes_the_byte_map(fields):
+    """Workspaces sized for W = 20 batches of the small graph serve the
+    epoch's 4-batch last window, which takes the byte map where the 20-batch
+    window does not: with a 1 MB limit (1.3 MB of map for 20 batches: atomic
+    marks; 256 KB for 4), and by default (LDS marks from 8 batches on: the
+    20-batch window marks through LDS, the 4-batch one into the map).  The
     sequential driver and the look-ahead driver (split sampling) over both
     windows, against the oracle."""
-    log("small: W=20 (windows of 20 and 4 batches), byte map limit 1 MB")
+    log(f"small: W=20 (windows of 20 and 4 batches), tuning {fields}")
     import torch as T
     from paper_2606_02916_amd import LookaheadPipeline, gg
     from tests.gpu_util import LookaheadOracle
-    tune = gg.make_tuning(bytemap_max_mb=1, mark_slices_max=-1)
+    tune = gg.make_tuning(**fields)
     inst = synth.instance("small")
     wl, W = inst.wl, 20
     boff = inst.batch_off
     assert synth.n_windows(boff, W) == 2 and len(boff) - 1 == 24
     per_batch = gg.gg_bits_words(wl.num_nodes) * 32
     assert 4 * per_batch <= 1 << 20 < W * per_batch
+    # the 20-batch workspace holds the 4-batch window's map
+    assert gg.gg_ws_sample(wl.num_nodes, W, tune) >= 4 * per_batch
     w = world(inst, W=W, n_hot=3000, tuning=tune)
     for k in range(2):
         w.run_and_compare(k)
