@@ -383,6 +383,44 @@ def test_slot_overflow_leaves_the_same_sets_under_every_marking(frac):
             assert np.array_equal(x, y)
 
 
+@pytest.mark.parametrize("mark_block", [256, 1024])
+def test_marks_from_unaligned_slots_match_oracle(mark_block):
+    """Neighbour slots at an address that is not 16-byte aligned (a C
+    caller's buffer, one int32 past an aligned one): the mark pass reads
+    them one at a time instead of in 16-byte groups.  Every hop marks
+    through LDS; the window's frontiers, slots and bit sets against the
+    oracle."""
+    log(f"small: LDS marks from unaligned neighbour slots, {mark_block}-lane blocks")
+    import torch as T
+    from oracle import ggref
+    from paper_2606_02916_amd import gg
+    from tests.gpu_util import check_bits
+    tune = gg.make_tuning(mark_min_slots=-1, mark_min_batches=-1, mark_block=mark_block)
+    w = world(synth.instance("small"), tuning=tune)
+    p = w.pipe
+    L = len(w.fanout)
+    seeds, so, b0 = w.window_inputs(0)
+    sd = T.from_numpy(seeds).to(w.dev)
+    Wk = len(so) - 1
+    nb = T.full((p.nbr_ids.numel() + 1,), 0x7EADBEEF, dtype=T.int32, device=w.dev)
+    assert nb[1:].data_ptr() % 16 == 4
+    wsm = gg.make_wsample(p.frontier_ids, p.frontier_off, nb[1:], p.nbr_off, p.frontier_bits,
+                          p.need)
+    gg.gg_sample_window(p.csr, sd, so, Wk, list(w.fanout), L, 0, 0, b0, wsm, p.status, p.ws,
+                        tuning=tune)
+    T.cuda.synchronize()
+    assert p.read_status() == 0
+    fids, foff, nids, noff = ggref.sample_window(w.inst.row_ptr, w.inst.col_idx, seeds, so,
+                                                 w.fanout, 0, 0, b0)
+    g_foff = p.frontier_off[:(L + 1) * Wk + 1].cpu().numpy()
+    g_noff = p.nbr_off[:L * Wk + 1].cpu().numpy()
+    assert np.array_equal(g_foff, foff) and np.array_equal(g_noff, noff)
+    assert np.array_equal(p.frontier_ids[:int(foff[-1])].cpu().numpy(), fids)
+    assert np.array_equal(nb[1:1 + int(noff[-1])].cpu().numpy(), nids)
+    bits = p.frontier_bits.view(T.int32)[:Wk * p.wpb].cpu().numpy().view(np.uint32)
+    check_bits(bits, p.wpb, Wk, lambda b: fids[foff[L * Wk + b]:foff[L * Wk + b + 1]])
+
+
 @pytest.mark.timeout(900)
 def test_large_sparse_full_window_matches_oracle():
     log("large_sparse: 2.45M nodes, 62M edges, fanout [15,10,5], batch 1024, W=16, window 0")
