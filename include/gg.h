@@ -247,11 +247,15 @@ size_t gg_ws_gather(int64_t n_cap, int32_t nseg, int32_t num_parts, const gg_tun
  * (l << 16) | i/4), word i mod 4 for draw i, mapped onto [0, d-k+i] by
  * floor(r * (d-k+i+1) / 2^32)), ascending.  F_{l+1} is F_l together with
  * the neighbours drawn at hop l.  batch0 is the epoch-global index of the
- * window's first batch, so N_b does not depend on W.  When W * 32 *
- * gg_bits_words(num_nodes) is at most tuning->bytemap_max_mb (512 MB by
- * default) the workspace also holds a byte map (one byte per node and
- * batch) into which the last hop marks its draws; gg_ws_sample includes
- * it. */
+ * window's first batch, so N_b does not depend on W.  The marks that make
+ * F_{l+1} from a hop's draws are the same bits whichever way they are made:
+ * through LDS slices of each batch's set in a pass of their own (where a
+ * set has at most tuning->mark_slices_max slices of 64 KB, the hop is large
+ * enough and the call has enough batches: see gg_tuning_t), else with
+ * atomic ORs, or at the last hop into a byte map (one byte per node and
+ * batch) when W * 32 * gg_bits_words(num_nodes) is at most
+ * tuning->bytemap_max_mb (512 MB by default).  gg_ws_sample includes the
+ * byte map of any call of at most W batches that takes it. */
 int gg_sample_window(const gg_csr_t* csr, const int32_t* seeds_d, const int64_t* seed_off_h,
                      int32_t W, const int32_t* fanout_h, int32_t L, uint64_t rng_seed,
                      int32_t epoch, int64_t batch0, const gg_wsample_t* out,
