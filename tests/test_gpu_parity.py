@@ -422,9 +422,16 @@ def test_marks_from_unaligned_slots_match_oracle(mark_block):
 
 
 @pytest.mark.timeout(900)
-def test_large_sparse_full_window_matches_oracle():
-    log("large_sparse: 2.45M nodes, 62M edges, fanout [15,10,5], batch 1024, W=16, window 0")
-    w = world(synth.instance("large_sparse"))
+@pytest.mark.parametrize("fields", [dict(), dict(mark_slice_chunks=3, mark_slices_max=16,
+                                                mark_block=256, mark_min_slots=-1)])
+def test_large_sparse_full_window_matches_oracle(fields):
+    """Window 0 of the 2.45M-node graph against the oracle; with the second
+    tuning every hop marks through LDS slices of 3 chunks (13 slices per
+    batch, the last one of 2 chunks)."""
+    log(f"large_sparse: 2.45M nodes, 62M edges, fanout [15,10,5], batch 1024, W=16, window 0, "
+        f"tuning {fields}")
+    from paper_2606_02916_amd import gg
+    w = world(synth.instance("large_sparse"), tuning=gg.make_tuning(**fields))
     w.run_and_compare(0)
 
 
