@@ -70,17 +70,16 @@ inline bool use_bytemap(int64_t num_nodes, int32_t W, const Tune& tune) {
 }
 
 // Marks through LDS: block (s, b) of k_mark_slices holds slice s of batch
-// b's set (the tuning's mark_slice_chunks chunks of 8 KB) and reads every slot the hop
-// wrote for batch b, so each slot is read once per slice: worth it while a
-// batch's set has few slices (at most the tuning's mark_slices_max).  A
-// random OR then costs an LDS atomic instead of one performed at memory
-// (about 32 bytes of memory-side traffic each, and the rate that bounds the
-// sampler's last hop).
-// A block is one wave per SIMD, so that it finds room beside a running
-// gather (four waves per SIMD of 74 VGPRs leave no SIMD room for a block
-// of four waves each: a 1,024-lane block waited 170 us for the gather to
-// drain); its lanes keep 16 loads of 16 bytes in flight instead.
-constexpr int kMarkBlockDefault = 256;
+// b's set (the tuning's mark_slice_chunks chunks of 8 KB) and reads every
+// slot the hop wrote for batch b, so each slot is read once per slice:
+// worth it while a batch's set has few slices (at most the tuning's
+// mark_slices_max).  A random OR then costs an LDS atomic instead of one
+// performed at memory (about 32 bytes of memory-side traffic each, and the
+// rate that bounded the sampler's last hop).  By default a block is one
+// wave per SIMD (256 lanes), so that it finds room beside a running gather
+// (four waves per SIMD of 74 VGPRs leave no SIMD room for a block of four
+// waves each: a 1,024-lane block waited 170 us for the gather to drain);
+// its lanes keep 16 loads of 16 bytes in flight instead.
 constexpr int kMarkRoundBytes = 65536;   // slot bytes a block has in flight per round
 
 inline int64_t mark_slices(int64_t num_nodes, const Tune& tune) {
@@ -300,12 +299,6 @@ struct MarkArgs {
 // the last batch has no work.
 constexpr int kXcds = 8;
 
-// The marks of hop l, with level l+1's counts (as k_bits_count makes them):
-// block (s, b) loads slice s of batch b's set (F_l's bits) into LDS, ORs in
-// every id in batch b's slots of hop l that falls in the slice, writes the
-// slice back and counts its chunks.  Only the slots of complete entries are
-// read: an entry that would pass the slot capacity wrote none of its slots,
-// and the end of the last complete one bounds what was written.
 // One round of a mark block's slot loads: lane t reads the 16-byte groups
 // at p + u * 4 * kMarkBlock (p at the lane's first group), all in flight at
 // once, then marks their slots.  The lane's groups end at `mine` slots past
@@ -331,11 +324,16 @@ __device__ __forceinline__ void mark_round(const int32_t* p, int32_t mine, int32
   }
 }
 
+// The marks of hop l, with level l+1's counts (as k_bits_count makes them):
+// block (s, b) loads slice s of batch b's set (F_l's bits) into LDS, ORs in
+// every id in batch b's slots of hop l that falls in the slice, writes the
+// slice back and counts its chunks.  Only the slots of complete entries are
+// read: an entry that would pass the slot capacity wrote none of its slots,
+// and the end of the last complete one bounds what was written.
 template <int kMarkBlock>
 __device__ __forceinline__ void mark_slices_body(uint32_t* bits, const int32_t* nbr,
-                                                            const int64_t* nbr_off,
-                                                            const LevelState* ls, int32_t* cnt,
-                                                            Totals tt, MarkArgs a) {
+                                                 const int64_t* nbr_off, const LevelState* ls,
+                                                 int32_t* cnt, Totals tt, MarkArgs a) {
   extern __shared__ uint32_t sl[];
   const int xcd = blockIdx.x % kXcds, j = blockIdx.x / kXcds;
   const int s = j % a.nslices, b = j / a.nslices * kXcds + xcd;
@@ -347,8 +345,8 @@ __device__ __forceinline__ void mark_slices_body(uint32_t* bits, const int32_t* 
   int64_t lo = nbr_off[(int64_t)a.l * a.W + b], hi = nbr_off[(int64_t)a.l * a.W + b + 1];
   const int64_t nbase = ls->nbase[a.l];
   {
-    // the slice in one round of loads (at most 16 per lane): beside a
-    // gather that saturates HBM a round trip takes several microseconds
+    // the slice (at most 8 chunks) in one round of loads: beside a gather
+    // that saturates HBM a round trip takes several microseconds
     constexpr int kSliceLoads = 8 * kChunkWords / 4 / kMarkBlock;
     u32x4 t[kSliceLoads];
 #pragma unroll
@@ -380,7 +378,7 @@ __device__ __forceinline__ void mark_slices_body(uint32_t* bits, const int32_t* 
     atomicOr(&sl[in ? x >> 5 : dummy], in ? 1u << (x & 31) : 0u);
   };
 
-  // Rounds of up to kMarkLoads * 1,024 slots in whole 16-byte groups, from
+  // Rounds of up to kMarkRoundBytes of slots in whole 16-byte groups, from
   // the boundary at or below lo to the one at or below hi, all of a round's
   // loads in flight at once (a loop of one load per lane and step would pay
   // a memory round trip per step); then the at most three slots after the
