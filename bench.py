@@ -476,14 +476,18 @@ def main():
     # later of its window's staging end (events[4]) and the previous
     # gather's end, and every marker left out of that queue saves a few us.
     stage_on_build = look and pipe.stage_stream is pipe.build_stream
+    hs_on_stage = look and pipe.hotset_on_stage
     # The build stream carries the critical chain and each event on it costs
     # a few us too: by default only the build's end and the staging's end
     # are recorded, and a build is taken to run from the previous window's
     # staging end (staging on the build stream) or build end (staging on a
-    # stream of its own); a gather, from the later of its staging's end and
-    # the previous gather's end (--breakdown: every call).
+    # stream of its own; the build then ends with the sampling when the hot
+    # set and buckets follow it on the staging stream); a gather, from the
+    # later of its staging's end and the previous gather's end (--breakdown:
+    # every call).
     lean = look and not args.breakdown
-    evs = [[None if lean and j < 3 else mk() for j in range(5 if look else 6)]
+    b_end = 1 if hs_on_stage else 3      # the event that ends a build
+    evs = [[None if lean and j < 3 and j != b_end else mk() for j in range(5 if look else 6)]
            for _ in range(K)]
     gevs = [[(None if lean or stage_on_build else mk(), mk()) for _ in range(W if pb else 1)]
             for _ in range(K)]
@@ -525,14 +529,16 @@ def main():
         e = evs[i]
         if lean:
             if i > 0:
-                stage_ms["build"].append(evs[i - 1][4 if stage_on_build else 3].elapsed_time(e[3]))
+                stage_ms["build"].append(
+                    evs[i - 1][4 if stage_on_build else b_end].elapsed_time(e[b_end]))
         else:
             for name, (a, b) in zip(stage_ms, [(0, 1), (1, 2), (2, 3)]):
                 stage_ms[name].append(e[a].elapsed_time(e[b]))
         # staging follows the build on the build stream; on the fetch stream
         # (shards in host memory) it starts at the later of the build's end
         # and the previous window's staging end
-        t_st = e[3].elapsed_time(e[4])
+        # (with the hot set and buckets on the staging stream, they count here)
+        t_st = e[b_end if lean else 3].elapsed_time(e[4])
         if look and not stage_on_build and i > 0:
             t_st = min(t_st, evs[i - 1][4].elapsed_time(e[4]))
         stage_ms["stage"].append(t_st)

@@ -549,6 +549,12 @@ class LookaheadPipeline:
         if stage_apart is None:
             stage_apart = on_host or (self.L >= 3 and not shared)
         self.stage_apart = bool(stage_apart)
+        # With staging on a stream of its own and shards in device memory,
+        # the hot set and the buckets (which read only the bit sets and write
+        # the window's own buffers) follow the sampling on that stream too,
+        # so that the next window's sampling starts at once; with shards in
+        # host memory that stream is bound by PCIe and keeps only staging.
+        self.hotset_on_stage = self.stage_apart and not on_host
         if self.stage_apart:
             self.stage_stream = self.fetch_stream
             self.gather_stream = third
@@ -568,8 +574,10 @@ class LookaheadPipeline:
         window's rows land in the set's win_out (or `out`) on the gather
         stream; wait on gathered_event(k) before reading them.  Inputs
         uploaded on the caller's stream are visible to the build stream.
-        events: optional 5 torch events, four recorded on the build stream
-        around its three calls and one after staging on the staging stream.
+        events: optional 5 torch events recorded around the window's calls:
+        before and after sampling (build stream), after the hot set and after
+        the buckets (build stream, or the staging stream when
+        hotset_on_stage) and after staging (staging stream).
         gather_events: optional (start, end) pair recorded around the gather
         on the gather stream; start may be None, which keeps one marker out
         of that stream's queue (the gather then starts at the later of
@@ -604,15 +612,25 @@ class LookaheadPipeline:
         else:
             gg.gg_sample_window(*sargs, self.status, cur.ws, stream=s, tuning=self.tuning)
         _rec(ev[1], bs)
+        hs = bs
+        if self.hotset_on_stage:
+            # the sampling's end: the split's marker, a caller's event at
+            # that point, or the set's own
+            sampled = (self.sampled[X] if self.split_last
+                       else ev[1] if ev[1] is not None else self.built[X])
+            if sampled is self.built[X]:
+                sampled.record(bs)
+            ss.wait_event(sampled)
+            hs = ss
         gg.gg_build_hotset(cur.frontier_bits, Wk, self.part, self.n_hot, cur.hot_ids,
                            cur.hot_freq, g.hot_cap, self.hot_count[T], self.status, cur.ws2,
-                           stream=s, hot_frac=self.hot_frac, tuning=self.tuning)
-        _rec(ev[2], bs)
+                           stream=hs.cuda_stream, hot_frac=self.hot_frac, tuning=self.tuning)
+        _rec(ev[2], hs)
         gg.gg_bucket_by_owner(cur.hot_ids, self.hot_count[T], g.hot_cap, self.part,
-                              self.bucket_ids[T], cur.owner_off, self.status, cur.ws2, stream=s,
-                              flags=_bucket_flags(self.part))
-        _rec(ev[3], bs)
-        if ss is not bs:
+                              self.bucket_ids[T], cur.owner_off, self.status, cur.ws2,
+                              stream=hs.cuda_stream, flags=_bucket_flags(self.part))
+        _rec(ev[3], hs)
+        if ss is not hs:
             # a caller's event recorded at the same point serves as the
             # marker to wait on (one marker fewer in the queue)
             built = ev[3] if ev[3] is not None else self.built[X]
