@@ -513,8 +513,9 @@ class LookaheadPipeline:
         # The hot set, buckets and staging read only the bit sets; the last
         # level's lists are first read by the gather.  With split_last that
         # compaction moves from the build stream to the gather stream, ahead
-        # of the gather: it shortens the build chain and lengthens the
-        # gather chain, which pays where the build is the longer chain.
+        # of the gather (or to the staging stream, when the hot set follows
+        # the sampling there): it shortens the build chain, which pays where
+        # the build is the longer chain.
         # The build grows with the sampling depth (a hop and a compaction
         # per level) and the gather does not, so by default the split is
         # taken from three hops on: on the 2.45M-node graph (three hops) the
@@ -605,22 +606,25 @@ class LookaheadPipeline:
             gg.gg_sample_window_part(*sargs, gg.GG_SAMPLE_PART_BITS, self.status, cur.ws,
                                      stream=s, tuning=self.tuning)
             self.sampled[X].record(bs)
-            # the last level's lists on the gather stream, before the gather
-            gs.wait_event(self.sampled[X])
+            # the last level's lists before the gather: on the staging stream
+            # when the hot set follows the sampling there (the gather waits
+            # for its staging anyway), else on the gather stream
+            ls = ss if self.hotset_on_stage else gs
+            ls.wait_event(self.sampled[X])
             gg.gg_sample_window_part(*sargs, gg.GG_SAMPLE_PART_LAST, self.status, cur.ws,
-                                     stream=gs.cuda_stream, tuning=self.tuning)
+                                     stream=ls.cuda_stream, tuning=self.tuning)
         else:
             gg.gg_sample_window(*sargs, self.status, cur.ws, stream=s, tuning=self.tuning)
         _rec(ev[1], bs)
         hs = bs
         if self.hotset_on_stage:
-            # the sampling's end: the split's marker, a caller's event at
-            # that point, or the set's own
-            sampled = (self.sampled[X] if self.split_last
-                       else ev[1] if ev[1] is not None else self.built[X])
-            if sampled is self.built[X]:
-                sampled.record(bs)
-            ss.wait_event(sampled)
+            # the sampling's end: the split's marker (already waited for),
+            # a caller's event at that point, or the set's own
+            if not self.split_last:
+                sampled = ev[1] if ev[1] is not None else self.built[X]
+                if sampled is self.built[X]:
+                    sampled.record(bs)
+                ss.wait_event(sampled)
             hs = ss
         gg.gg_build_hotset(cur.frontier_bits, Wk, self.part, self.n_hot, cur.hot_ids,
                            cur.hot_freq, g.hot_cap, self.hot_count[T], self.status, cur.ws2,
