@@ -537,8 +537,9 @@ def main():
         # staging follows the build on the build stream; on the fetch stream
         # (shards in host memory) it starts at the later of the build's end
         # and the previous window's staging end
-        # (with the hot set and buckets on the staging stream, they count here)
-        t_st = e[b_end if lean else 3].elapsed_time(e[4])
+        # from the buckets' end (on the staging stream too when the hot set
+        # and buckets follow the sampling there)
+        t_st = e[3].elapsed_time(e[4])
         if look and not stage_on_build and i > 0:
             t_st = min(t_st, evs[i - 1][4].elapsed_time(e[4]))
         stage_ms["stage"].append(t_st)
@@ -643,6 +644,8 @@ def main():
                             "frac": round(stage_gbs / HBM_PEAK_GBS, 4), "unit": "GB/s",
                             "bytes_per_call": int(np.mean(sbytes_w)),
                             "overlapped": look,
+                            "start": ("the buckets' end, or the previous staging's end if later "
+                                      "(HIP events)" if look else "HIP event before the call"),
                             "isolated": iso_stage}
                            if pcie is None else
                            {"kernel": stage_call, "bound": "pcie",

@@ -198,7 +198,7 @@ typedef struct gg_tuning {
   int32_t mark_slice_chunks; /* chunks of 65,536 node ids (8 KB of a set) per mark slice, 1..8
                                 (default 8) */
   int32_t mark_block;        /* lanes of a mark block: 256 (default) or 1024; a block keeps
-                                64 KB of slot loads in flight */
+                                32 KB of slot loads in flight */
   int32_t mark_min_slots;    /* a hop before the last marks through LDS slices only when its
                                 bound on neighbour slots per batch, min(N, B * prod_{i<l}
                                 (k_i + 1)) * k_l with B the largest batch, is at least this

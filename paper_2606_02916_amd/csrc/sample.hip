@@ -79,8 +79,12 @@ inline bool use_bytemap(int64_t num_nodes, int32_t W, const Tune& tune) {
 // wave per SIMD (256 lanes), so that it finds room beside a running gather
 // (four waves per SIMD of 74 VGPRs leave no SIMD room for a block of four
 // waves each: a 1,024-lane block waited 170 us for the gather to drain);
-// its lanes keep 16 loads of 16 bytes in flight instead.
-constexpr int kMarkRoundBytes = 65536;   // slot bytes a block has in flight per round
+// its lanes keep 8 loads of 16 bytes in flight instead.  Registers decide
+// the size of a round: the 2.45M-node window took 0.341 ms per step with
+// 32 KB rounds (68 VGPRs, mostly the slice load's), 0.346 with 64 KB (100
+// VGPRs) and 0.423 with 96 KB (145 VGPRs): a block beside the gather and
+// the staging stream's kernels must find its registers free.
+constexpr int kMarkRoundBytes = 32768;   // slot bytes a block has in flight per round
 
 inline int64_t mark_slices(int64_t num_nodes, const Tune& tune) {
   return cdiv(gg_bits_words(num_nodes) / kChunkWords, (int64_t)tune.mark_slice_chunks);
