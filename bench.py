@@ -133,6 +133,20 @@ def summarize(args):
                        f"gg_gather_batch {r['avg_launch_us']} us per launch over the timed steps "
                        f"(HIP events, frac {r['frac']}), {r['isolated']['avg_launch_us']} us "
                        f"isolated (frac {r['isolated']['frac']})")
+        if args.plain_json:
+            # the same command without the profiler: rocprofv3 costs the host
+            # 10-40 us per launch, so a traced look-ahead run is bound by the
+            # host's enqueue, its chains overlap less and its gathers run
+            # with more of the chip than in the unprofiled run
+            with open(args.plain_json) as f:
+                b = json.loads(f.read().strip().splitlines()[-1])
+            r = b["roofline"]
+            out.append(f"# the same command without the profiler: ms_per_step "
+                       f"{b['ms_per_step']}, gg_gather_batch {r['avg_launch_us']} us per launch "
+                       f"over the timed steps (HIP events, frac {r['frac']}), "
+                       f"{r['isolated']['avg_launch_us']} us isolated (frac "
+                       f"{r['isolated']['frac']}); under the profiler the host's enqueue "
+                       f"(10-40 us per launch) bounds the pipeline, which then overlaps less")
         copies = [r[0] for r in db.execute("select end-start from kernels where name like "
                                            "'%copyBuffer%' order by end-start desc limit 3")]
         if args.copy_calibration_mib and copies:
@@ -321,6 +335,9 @@ def main():
                          "kernel's calibrated traffic and duration to profiles/<name>_<config>.txt")
     ap.add_argument("--bench-json", default=None,
                     help="with --summarize: the JSON line bench.py printed in the traced run")
+    ap.add_argument("--plain-json", default=None,
+                    help="with --summarize: the JSON line of the same command run without the "
+                         "profiler")
     ap.add_argument("--phases", default=None,
                     help="with --trace-db: gather launches of the pre-pass (two per window "
                          "with the look-ahead driver), warm-up and timed steps, e.g. 24,1,12, "
