@@ -898,8 +898,10 @@ def test_lookahead_pipeline_equals_sequential(name, n_hot, W, nsets, host, gev, 
     for k in range(nwin):
         b0, b1 = synth.window_batches(boff, W, k)
         ge = None if gev is None else (None if gev == "end" else mk(), mk())
+        # the seeds were uploaded on the caller's stream, which only the
+        # first window has to wait for
         Wk, bufs = look.window(seeds_d[boff[b0]:boff[b1]], boff[b0:b1 + 1] - boff[b0], b0,
-                               gather_events=ge)
+                               gather_events=ge, after_caller=k == 0)
         if ge is not None:
             assert (look.gathered_event(k) is ge[1])
         if pending is not None:                 # read window k-1 while k is in flight
