@@ -297,6 +297,8 @@ def main():
     ap.add_argument("--wsweep", default=None,
                     help="comma-separated window sizes: run one epoch per W and report, per W, "
                          "hot-set size, bulk bytes per owner, rebuild delta and gather rate")
+    ap.add_argument("--wsweep-table", default=None,
+                    help="with --wsweep: also write the sweep as a text table to this file")
     ap.add_argument("--simulate", default=None,
                     help="comma-separated window sizes: replay one epoch per W and per hot-set "
                          "budget through the fetch path and report the simulator's event counts "
@@ -698,7 +700,12 @@ def main():
                          "epoch cycled 4 times (at least 8 windows) timed; gather rate from "
                          "HIP events as in roofline; counts from the "
                          "untimed epoch (bulk bytes per owner: the rows each owner's one request "
-                         "moves, i.e. the rebuild delta)"}
+                         "moves, i.e. the rebuild delta); gpu_ms_per_window: mean period of the "
+                         "gather ends over whole epochs of windows enqueued behind a blocker on "
+                         "the caller's stream (the GPU runs them back to back, whatever the "
+                         "host's enqueue rate; queued says the host finished enqueuing before "
+                         "the GPU had gathered the third), host_enqueue_ms_per_window: the "
+                         "host's time per window in that run"}
         sweep["wall_s"] = round(time.perf_counter() - t_sw, 1)
         line["wsweep"] = sweep
     print(json.dumps(line), flush=True)
@@ -1137,6 +1144,9 @@ def wsweep(args, wl):
         r["lookahead_ms_per_window"] = la["ms_per_window"]
         r["lookahead_rows_per_s"] = la["rows_per_s"]
         r["lookahead_gather_GBps"] = la["gather_GBps"]
+        r["lookahead_gpu_ms_per_window"] = la["gpu_ms_per_window"]
+        r["lookahead_host_enqueue_ms_per_window"] = la["host_enqueue_ms_per_window"]
+        r["lookahead_queued"] = la["queued"]
     pick = next((r for r in results if r["W"] == wl.W), results[-1])
     line = {"metric": "feature rows gathered/s vs W (per-window fetch path)",
             "value": pick["rows_per_s"], "unit": "rows/s", "n_gpus": 1,
@@ -1148,7 +1158,48 @@ def wsweep(args, wl):
                        "features": f"{wl.feat_dtype}x{wl.feat_dim}", "fanout": list(wl.fanout),
                        "batch": wl.batch_size, "W_reported": pick["W"]},
             "w_sweep": results}
+    if args.wsweep_table:
+        write_wsweep_table(args, wl, results)
     print(json.dumps(line), flush=True)
+
+
+def write_wsweep_table(args, wl, results):
+    """The --wsweep results as a text table (the sweep's profile summary)."""
+    batches = results[0]["windows"] * results[0]["W"]
+    lines = [
+        f"# command: python3 bench.py --config {args.config} --wsweep {args.wsweep} "
+        f"--wsweep-table <file> (env SYNTH_CACHE_DIR=/tmp/synth_cache), one MI355X",
+        f"# {wl.num_nodes / 1e6:.2f}M-node / {wl.num_edges / 1e6:.0f}M-edge R-MAT, "
+        f"{wl.feat_dtype}x{wl.feat_dim} rows, fanout {list(wl.fanout)}, batch {wl.batch_size}, "
+        f"about {batches} batches per epoch",
+        "# columns 3-10: sequential driver (full restage of the hot set every window), one "
+        "timed epoch after an untimed one",
+        "# look: the look-ahead driver (persistent cache, delta staging) over the same windows, "
+        "epoch cycled 4 times after an untimed epoch",
+        "# look GPU ms/win: mean period over whole epochs of windows enqueued behind a blocker "
+        "(the GPU's own rate); host ms/win: the host's enqueue per window in that run",
+        "  W windows hot rows/win  delta/win bulk req/epoch  reuse  epoch ms       rows/s "
+        "gather GB/s | look ms/win  look rows/s look gather GB/s look GPU ms/win host ms/win",
+    ]
+    for r in results:
+        lines.append(
+            f"{r['W']:3d} {r['windows']:7d} {r['hot_set_rows_per_window']:12.0f} "
+            f"{r['delta_rows_per_window']:10.0f} {r['bulk_requests_per_epoch']:14d} "
+            f"{r['reuse_factor']:6.2f} {r['epoch_ms']:9.3f} {r['rows_per_s']:12.4g} "
+            f"{r['gather_GBps']:11.1f} | {r['lookahead_ms_per_window']:11.4f} "
+            f"{r['lookahead_rows_per_s']:12.4g} {r['lookahead_gather_GBps']:16.1f} "
+            f"{r['lookahead_gpu_ms_per_window']:15.4f}{'' if r['lookahead_queued'] else '*'} "
+            f"{r['lookahead_host_enqueue_ms_per_window']:11.4f}")
+    if not all(r["lookahead_queued"] for r in results):
+        lines.append("# *: the GPU reached the third queued window before the host had "
+                     "enqueued them all (not a clean GPU-only period)")
+    lines.append("# bulk bytes per owner per window, sequential driver (full restage; owners "
+                 f"0..{wl.num_parts - 1}, owner {wl.local_owner} local):")
+    for r in results:
+        lines.append(f"#  W={r['W']:2d}: " + ", ".join(
+            f"{x / 1e6:.1f} MB" for x in r["bulk_bytes_per_owner_per_window"]))
+    with open(args.wsweep_table, "w") as f:
+        f.write("\n".join(lines) + "\n")
 
 
 def wsweep_lookahead(dev, name, Ws, tuning=None, reps=4):
@@ -1232,6 +1283,27 @@ def wsweep_lookahead(dev, name, Ws, tuning=None, reps=4):
             g_ms += t
         g_bytes = sum(gbytes[k] for k in order)
         g_gbs = g_bytes / (g_ms * 1e-3) / 1e9
+        # The GPU's own period: the same windows enqueued behind a blocker on
+        # the caller's stream, which only the first window waits for, so the
+        # GPU runs them back to back whatever the host's enqueue rate (about
+        # 0.15-0.2 ms per window; the blocker lasts longer than the whole
+        # enqueue).  The period is the mean over whole epochs from the third
+        # window on (an epoch's windows may differ in size).
+        Kq = 3 + nwin * max(1, 37 // nwin)
+        qev = [mk() for _ in range(Kq)]
+        blocker = torch.empty(512 << 20, dtype=torch.uint8, device=dev)
+        torch.cuda.synchronize()
+        for i in range(Kq * 3):          # ~0.1 ms of GPU time per fill
+            blocker.fill_(i & 0xFF)
+        t1 = time.perf_counter()
+        for i in range(Kq):
+            s_, so, b0 = wins[i % nwin]
+            look.window(s_, so, b0, gather_events=(None, qev[i]), after_caller=(i == 0))
+        host_q = (time.perf_counter() - t1) / Kq
+        queued = not qev[2].query()
+        look.synchronize()
+        del blocker
+        q_ms = qev[2].elapsed_time(qev[Kq - 1]) / (Kq - 3)
         r = {"W": W, "windows_per_epoch": nwin,
              "rows_per_s": round(sum(rows[k] for k in order) / el, 1),
              "ms_per_window": round(el / K * 1e3, 4),
@@ -1242,6 +1314,8 @@ def wsweep_lookahead(dev, name, Ws, tuning=None, reps=4):
              "delta_rows_per_window": round(float(np.mean(delta)), 1),
              "bulk_requests_per_epoch": int(sum(requests)),
              "reuse_factor": round(sum(remote) / max(1, sum(hot)), 3),
+             "gpu_ms_per_window": round(q_ms, 4),
+             "host_enqueue_ms_per_window": round(host_q * 1e3, 4), "queued": queued,
              "wall_s": None}
         del look
         torch.cuda.empty_cache()
