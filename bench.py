@@ -553,14 +553,16 @@ def main():
         else:
             for name, (a, b) in zip(stage_ms, [(0, 1), (1, 2), (2, 3)]):
                 stage_ms[name].append(e[a].elapsed_time(e[b]))
-        # staging follows the build on the build stream; on the fetch stream
-        # (shards in host memory) it starts at the later of the build's end
-        # and the previous window's staging end
-        # from the buckets' end (on the staging stream too when the hot set
-        # and buckets follow the sampling there)
+        # staging starts at the buckets' end (on the staging stream too when
+        # the hot set and buckets follow the sampling there); on a stream of
+        # its own, at the later of that, the previous window's staging end
+        # and, with more than two buffer sets, the end of the gather of
+        # window k - 2, whose slots it may reuse and which it waits for
         t_st = e[3].elapsed_time(e[4])
         if look and not stage_on_build and i > 0:
             t_st = min(t_st, evs[i - 1][4].elapsed_time(e[4]))
+            if i > 1 and pipe.nsets > 2:
+                t_st = min(t_st, gevs[i - 2][-1][1].elapsed_time(e[4]))
         stage_ms["stage"].append(t_st)
         stage_ms["gathers"].append(gather_ms(gevs, i))
         st_ms += t_st
@@ -663,8 +665,10 @@ def main():
                             "frac": round(stage_gbs / HBM_PEAK_GBS, 4), "unit": "GB/s",
                             "bytes_per_call": int(np.mean(sbytes_w)),
                             "overlapped": look,
-                            "start": ("the buckets' end, or the previous staging's end if later "
-                                      "(HIP events)" if look else "HIP event before the call"),
+                            "start": ("the latest of the buckets' end, the previous staging's "
+                                      "end and (staging on a stream of its own) the end of the "
+                                      "gather whose slots it reuses (HIP events)" if look
+                                      else "HIP event before the call"),
                             "isolated": iso_stage}
                            if pcie is None else
                            {"kernel": stage_call, "bound": "pcie",
