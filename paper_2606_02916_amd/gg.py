@@ -154,6 +154,11 @@ SIGNATURES = {
 
 if not os.path.exists(LIB_PATH):
     raise ImportError(f"libgg is not built ({LIB_PATH}); run __graft_entry__.build()")
+# torch first: libgg must bind to the HIP runtime torch loads (its own copy),
+# since it is handed torch's streams; loaded first, libgg would bring in the
+# system runtime and torch a second one.
+import torch  # noqa: E402,F401
+
 lib = C.CDLL(LIB_PATH)
 for _name, (_res, _args) in SIGNATURES.items():
     _f = getattr(lib, _name)

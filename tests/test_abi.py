@@ -314,3 +314,19 @@ def test_lookahead_byte_map_choice_follows_last_hop_density(gg):
         16 * 1024 * 16 * 11 / 2_450_000 < 2
     assert last_hop_sharing(233_000, [25, 10], 1024, 8) == 8 * 1024 * 26 / 233_000 < 2
     assert last_hop_sharing(1000, [15, 10, 5], 512, 4) == 4.0                # capped at N
+
+
+@pytest.mark.parametrize("order", ["package first", "torch first"])
+def test_one_hip_runtime_whatever_the_import_order(gg, order):
+    """libgg is handed torch's streams, so it must bind to the HIP runtime
+    torch loads: imported before torch, it would bring in the system
+    runtime through its own search path, and torch a second one."""
+    first = ("from paper_2606_02916_amd import gg; import torch" if order == "package first"
+             else "import torch; from paper_2606_02916_amd import gg")
+    code = (f"{first}\n"
+            "maps = sorted({l.split()[-1] for l in open('/proc/self/maps') if 'libamdhip64' in l})\n"
+            "print(len(maps), maps)\n")
+    out = subprocess.run(["python3", "-c", code], cwd=ROOT, capture_output=True, text=True,
+                         timeout=300)
+    assert out.returncode == 0, out.stderr[-2000:]
+    assert out.stdout.split()[0] == "1", out.stdout
