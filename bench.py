@@ -1288,11 +1288,12 @@ def wsweep_lookahead(dev, name, Ws, tuning=None, reps=4):
         g_bytes = sum(gbytes[k] for k in order)
         g_gbs = g_bytes / (g_ms * 1e-3) / 1e9
         # The GPU's own period: the same windows enqueued behind a blocker on
-        # the caller's stream, which only the first window waits for, so the
-        # GPU runs them back to back whatever the host's enqueue rate (about
-        # 0.15-0.2 ms per window; the blocker lasts longer than the whole
-        # enqueue).  The period is the mean over whole epochs from the third
-        # window on (an epoch's windows may differ in size).
+        # the caller's stream (every window waits on that stream, as in the
+        # timed run), so the GPU runs them back to back whatever the host's
+        # enqueue rate (about 0.15-0.2 ms per window; the blocker lasts
+        # longer than the whole enqueue).  The period is the mean over whole
+        # epochs from the third window on (an epoch's windows may differ in
+        # size).
         Kq = 3 + nwin * max(1, 37 // nwin)
         qev = [mk() for _ in range(Kq)]
         blocker = torch.empty(512 << 20, dtype=torch.uint8, device=dev)
@@ -1302,7 +1303,7 @@ def wsweep_lookahead(dev, name, Ws, tuning=None, reps=4):
         t1 = time.perf_counter()
         for i in range(Kq):
             s_, so, b0 = wins[i % nwin]
-            look.window(s_, so, b0, gather_events=(None, qev[i]), after_caller=(i == 0))
+            look.window(s_, so, b0, gather_events=(None, qev[i]))
         host_q = (time.perf_counter() - t1) / Kq
         queued = not qev[2].query()
         look.synchronize()
